@@ -1,0 +1,178 @@
+"""CPU oracle for the Residual-DCN + QR-embedding path -- TEST INFRASTRUCTURE ONLY.
+
+Plain C loops (oracle.c) behind ctypes. Only the tests, the smoke check and the
+benchmark's CPU-baseline leg may import this package; the product library and
+its Python binding never do. See oracle.c for the paper passages each
+function follows.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+COMBINE = {"mul": 0, "sum": 1}
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c with gcc (no fused multiply-add, no fast-math)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math", "-fPIC",
+                               "-shared", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        L = ctypes.CDLL(_LIB)
+        i64, dbl, vp = ctypes.c_int64, ctypes.c_double, ctypes.c_void_p
+        L.orc_qr_quotient_rows.argtypes = [i64, i64]
+        L.orc_qr_quotient_rows.restype = i64
+        L.orc_qr_index.argtypes = [vp, i64, i64, i64, vp, vp]
+        L.orc_qr_index.restype = i64
+        L.orc_round_bf16_array.argtypes = [vp, vp, i64]
+        L.orc_round_bf16_array.restype = None
+        L.orc_gather.argtypes = [i64, i64, i64, i64, i64, i64, i64, ctypes.c_int, ctypes.c_int,
+                                 vp, vp, vp, vp, vp, vp]
+        L.orc_gather.restype = i64
+        L.orc_attention.argtypes = [i64, dbl, dbl, dbl, vp, vp, vp, vp, vp, vp]
+        L.orc_attention.restype = None
+        L.orc_forward.argtypes = [i64, i64, i64, i64, dbl, dbl, dbl, vp, vp, vp, vp, vp]
+        L.orc_forward.restype = ctypes.c_int
+        L.orc_backward.argtypes = [i64, i64, i64, i64, dbl, dbl, dbl, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.orc_backward.restype = ctypes.c_int
+        L.orc_embed_backward.argtypes = [i64, i64, i64, i64, i64, i64, i64, ctypes.c_int, vp, vp, vp, vp, vp,
+                                         vp, vp]
+        L.orc_embed_backward.restype = i64
+        _lib = L
+    return _lib
+
+
+def _c(a: np.ndarray, dtype) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _p(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data
+
+
+def _np(x, dtype):
+    if x is None:
+        return None
+    if hasattr(x, "numpy"):  # torch CPU tensor
+        x = x.float().numpy() if dtype in (np.float32, np.float64) else x.numpy()
+    return _c(x, dtype)
+
+
+def quotient_rows(vocab: int, m: int) -> int:
+    return int(lib().orc_qr_quotient_rows(vocab, m))
+
+
+def qr_index(ids, vocab: int, m: int):
+    ids = _np(ids, np.int64).reshape(-1)
+    qi = np.empty_like(ids)
+    ri = np.empty_like(ids)
+    bad = lib().orc_qr_index(_p(ids), ids.size, vocab, m, _p(qi), _p(ri))
+    return qi, ri, int(bad)
+
+
+def round_bf16(x) -> np.ndarray:
+    x = _np(x, np.float32)
+    y = np.empty_like(x)
+    lib().orc_round_bf16_array(_p(x), _p(y), x.size)
+    return y
+
+
+def gather(B: int, F: int, D: int, Nd: int, vocab: int, rows_q: int, m: int, combine: str, bf16: bool,
+           ids, offsets, q_tables, r_tables, dense):
+    """x0 [B, F*D+Nd] float32 (bf16-rounded values when bf16) and the out-of-range id count."""
+    ids = _np(ids, np.int64)
+    offsets = _np(offsets, np.int64)
+    qt = _np(q_tables, np.float32)
+    rt = _np(r_tables, np.float32)
+    dn = _np(dense, np.float32)
+    x0 = np.empty((B, F * D + Nd), np.float32)
+    bad = lib().orc_gather(B, F, D, Nd, vocab, rows_q, m, COMBINE[combine], int(bf16), _p(ids), _p(offsets),
+                           _p(qt), _p(rt), _p(dn), _p(x0))
+    if bad < 0:
+        raise ValueError("orc_gather: bad arguments")
+    return x0, int(bad)
+
+
+def attention(q, k, v, alpha: float, beta: float, tau: float):
+    """One sample: returns (A [r, r], o [r], h [r]) in float64."""
+    q, k, v = (_c(np.asarray(a), np.float64) for a in (q, k, v))
+    r = q.size
+    A = np.empty((r, r))
+    o = np.empty(r)
+    h = np.empty(r)
+    lib().orc_attention(r, alpha, beta, tau, _p(q), _p(k), _p(v), _p(A), _p(o), _p(h))
+    return A, o, h
+
+
+def _stack(ws: Sequence, dtype=np.float64) -> np.ndarray:
+    return _c(np.stack([_np(w, np.float64) for w in ws]), dtype)
+
+
+def forward(x0, w_down: Sequence, u: Sequence, bias: Sequence, alpha: float, beta: float, tau: float = 1.0):
+    """x_L [B, d] in float64 from storage values (x0, weights as float arrays / torch tensors)."""
+    x0 = _np(x0, np.float64)
+    B, d = x0.shape
+    L = len(w_down)
+    W, U, b = _stack(w_down), _stack(u), _stack(bias)
+    r = U.shape[2]
+    out = np.empty((B, d))
+    rc = lib().orc_forward(B, d, r, L, alpha, beta, tau, _p(x0), _p(W), _p(U), _p(b), _p(out))
+    if rc != 0:
+        raise ValueError("orc_forward: bad arguments")
+    return out
+
+
+def backward(x0, w_down: Sequence, u: Sequence, bias: Sequence, grad_out, alpha: float, beta: float,
+             tau: float = 1.0):
+    """(grad_x0 [B, d], g_w_down [L, n*r, d], g_u [L, d, r], g_bias [L, d]) in float64."""
+    x0 = _np(x0, np.float64)
+    G = _np(grad_out, np.float64)
+    B, d = x0.shape
+    L = len(w_down)
+    W, U, b = _stack(w_down), _stack(u), _stack(bias)
+    r = U.shape[2]
+    gx0 = np.empty((B, d))
+    gW = np.empty_like(W)
+    gU = np.empty_like(U)
+    gb = np.empty_like(b)
+    rc = lib().orc_backward(B, d, r, L, alpha, beta, tau, _p(x0), _p(W), _p(U), _p(b), _p(G), _p(gx0), _p(gW),
+                            _p(gU), _p(gb))
+    if rc != 0:
+        raise ValueError("orc_backward: bad arguments")
+    return gx0, gW, gU, gb
+
+
+def embed_backward(B: int, F: int, D: int, Nd: int, vocab: int, rows_q: int, m: int, combine: str, ids, offsets,
+                   q_tables, r_tables, grad_x0, grad_q=None, grad_r=None):
+    """Table gradients (float64, accumulated into grad_q / grad_r when given) and the bad-id count."""
+    ids = _np(ids, np.int64)
+    offsets = _np(offsets, np.int64)
+    qt = _np(q_tables, np.float32)
+    rt = _np(r_tables, np.float32)
+    g = _np(grad_x0, np.float64)
+    gq = np.zeros((F, rows_q, D)) if grad_q is None else _c(grad_q, np.float64)
+    gr = np.zeros((F, m, D)) if grad_r is None else _c(grad_r, np.float64)
+    bad = lib().orc_embed_backward(B, F, D, Nd, vocab, rows_q, m, COMBINE[combine], _p(ids), _p(offsets), _p(qt),
+                                   _p(rt), _p(g), _p(gq), _p(gr))
+    if bad < 0:
+        raise ValueError("orc_embed_backward: bad arguments")
+    return gq, gr, int(bad)

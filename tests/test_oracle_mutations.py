@@ -1,0 +1,57 @@
+"""The oracle's pins must catch plausible mistakes.
+
+Each case plants one mistake in a copy of oracle.c (a dropped term, a wrong
+sign, a swapped index, a transposed operand, a wrong rounding), builds it into
+a temporary directory and runs the pin file that should notice; the pins must
+fail. Runs on the CPU only; the real oracle is never modified.
+"""
+import os
+import shutil
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+MUTATIONS = {
+    "combine_sum_for_mul": ("gather", "? qrow[c] * rrow[c] : qrow[c] + rrow[c]",
+                            "? qrow[c] + rrow[c] : qrow[c] + rrow[c]"),
+    "pool_seeded_with_zero": ("gather", "acc[c] = started ? acc[c] + e : e;",
+                              "acc[c] = (started ? acc[c] : 0.0f) + e;"),
+    "rounding_ties_away": ("gather", "u = (u + 0x7fffu + keep_lsb) & 0xffff0000u;",
+                           "u = (u + 0x8000u) & 0xffff0000u;"),
+    "quotient_remainder_swapped": ("gather", "int64_t q = id / m;\n                int64_t r = id - q * m;\n"
+                                   "                if (q >= rows_q) {\n                    ++bad;",
+                                   "int64_t r = id / m;\n                int64_t q = id - r * m;\n"
+                                   "                if (q >= rows_q) {\n                    ++bad;"),
+    "temperature_inverted": ("dcn", "row[j] = q[i] * k[j] / tau;", "row[j] = q[i] * k[j] * tau;"),
+    "softmax_over_queries": ("dcn", "row[j] = q[i] * k[j] / tau;", "row[j] = q[j] * k[i] / tau;"),
+    "skip_dropped": ("dcn", "h[i] = beta * v[i] + alpha * oi;", "h[i] = alpha * oi;"),
+    "up_projection_transposed": ("dcn", "for (int64_t i = 0; i < r; ++i) s += U[c * r + i] * h[i];",
+                                 "for (int64_t i = 0; i < r; ++i) s += U[(i * d + c) % (d * r)] * h[i];"),
+    "bias_dropped": ("dcn", "double s = bl[c];", "double s = 0.0;"),
+    "residual_dropped": ("dcn", "xn[c] = x0[c] * s + xl[c];", "xn[c] = x0[c] * s;"),
+    "multiplier_x_l_not_x0": ("dcn", "xn[c] = x0[c] * s + xl[c];", "xn[c] = xl[c] * s + xl[c];"),
+    "bwd_x0_term_dropped": ("grad", "gx0[c] += g[c] * t[c];", "gx0[c] += 0.0;"),
+    "bwd_score_sign": ("grad", "* (v[j] - o[i]);", "* (o[i] - v[j]);"),
+    "bwd_key_temperature": ("grad", "dk[j] = s / tau;", "dk[j] = s;"),
+    "bwd_value_skip_dropped": ("grad", "dv[j] = beta * dh[j] + s;", "dv[j] = s;"),
+    "bwd_final_input_term_dropped": ("grad", "grad_x0[b * d + c] = gx0[c] + g[c];", "grad_x0[b * d + c] = gx0[c];"),
+    "emb_product_rule_wrong_row": ("grad", "gq[c] += g[c] * (double)rrow[c];", "gq[c] += g[c] * (double)qrow[c];"),
+}
+PIN_FILE = {"gather": "test_oracle_gather.py", "dcn": "test_oracle_dcn.py", "grad": "test_oracle_grad.py"}
+
+
+@pytest.mark.parametrize("name", list(MUTATIONS))
+def test_pins_catch_planted_mistake(name, tmp_path):
+    which, old, new = MUTATIONS[name]
+    src = open(os.path.join(ROOT, "oracle", "oracle.c")).read()
+    assert src.count(old) >= 1, "mutation anchor not found: " + name
+    for sub in ("oracle", "tests", "paper_2402_06859_amd"):
+        shutil.copytree(os.path.join(ROOT, sub), tmp_path / sub,
+                        ignore=shutil.ignore_patterns("*.so", "__pycache__", "_build*"))
+    (tmp_path / "oracle" / "oracle.c").write_text(src.replace(old, new, 1))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
+                        os.path.join("tests", PIN_FILE[which])], cwd=tmp_path, capture_output=True, text=True)
+    assert r.returncode == 1, "planted mistake %r was not caught:\n%s" % (name, r.stdout[-2000:])
