@@ -1,0 +1,251 @@
+/*
+ * rdcn.h -- C ABI of the MI355X (gfx950) Residual-DCN + QR-embedding library (librdcn.so).
+ *
+ * The library computes, on one GPU, the forward and backward pass of the
+ * interaction stack of LiRank (Borisyuk et al., KDD'24, arXiv 2402.06859):
+ *
+ *   x0      = [ emb_0 | ... | emb_{F-1} | dense ]                  (qr_embed_gather)
+ *   emb_f   = pool over the bag of feature f of  Q_f[id / m] (op) R_f[id mod m]
+ *   x_{l+1} = x0 * (U_l h_l + b_l) + x_l,   l = 0 .. L-1          (rdcn_forward)
+ *   h_l     = beta * v + alpha * softmax_j(q_i k_j / tau) v,   [v; q; k] = W_l x_l
+ *
+ * and the gradients of a scalar loss given dLoss/dx_L (rdcn_backward,
+ * qr_embed_backward). Paper passages:
+ *   - QR split, per-feature quotient/remainder tables, sum or product combine:
+ *     section "Model Dictionary Compression".
+ *   - embedding look-ups replacing one-hot inputs, concatenated with dense
+ *     features: section "Residual DCN" (first paragraph) and appendix
+ *     "Feed Ranking Sparse ID features".
+ *   - low-rank DCNv2 cross layer (two skinny matrices U, V): section
+ *     "Residual DCN", first paragraph.
+ *   - attention low-rank cross net (value/query/key copies of the low-rank
+ *     map, attention score matrix between the low-rank maps, temperature)
+ *     and the skip connection: section "Residual DCN", second paragraph. The
+ *     paper describes this layer in prose only; this library reads it as
+ *     attention over the r low-rank coordinates of one sample (an r x r score
+ *     matrix per sample), with h = beta*v + alpha*o.
+ *
+ * Conventions
+ *   - All tensors are dense row-major. Device pointers unless stated.
+ *   - The caller allocates and frees every device buffer (inputs, weights,
+ *     outputs, gradients, saved activations, scratch). The library allocates
+ *     no device memory after rdcn_create (which allocates one small error word)
+ *     and never frees caller memory.
+ *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = the
+ *     default stream). Arguments are validated on the host before anything is
+ *     launched; on error nothing is launched.
+ *   - A handle must not be used by two host threads at once.
+ *   - No exception or abort crosses this ABI: every function returns an
+ *     rdcn_status.
+ */
+#ifndef RDCN_H
+#define RDCN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum rdcn_status {
+    RDCN_OK = 0,
+    RDCN_ERR_ARG = 1,          /* null pointer, negative size, unknown enum value */
+    RDCN_ERR_SHAPE = 2,        /* inconsistent sizes (batch > batch_max, rows_q * m < vocab, ...) */
+    RDCN_ERR_INDEX = 3,        /* an id outside [0, vocab) was met on the device */
+    RDCN_ERR_UNSUPPORTED = 4,  /* valid but not supported here (see rdcn_create) */
+    RDCN_ERR_WORKSPACE = 5,    /* a workspace or buffer argument is too small */
+    RDCN_ERR_HIP = 6           /* a HIP runtime call or kernel launch failed */
+} rdcn_status;
+
+typedef enum rdcn_dtype { RDCN_F32 = 0, RDCN_BF16 = 1 } rdcn_dtype;
+typedef enum rdcn_idtype { RDCN_I32 = 0, RDCN_I64 = 1 } rdcn_idtype;
+typedef enum rdcn_combine { RDCN_COMBINE_MUL = 0, RDCN_COMBINE_SUM = 1 } rdcn_combine;
+
+#define RDCN_MAX_LAYERS 16
+
+/*
+ * Model and batch description. d = num_cat * emb_dim + num_dense is derived.
+ * n = 3 projections per layer (value, query, key) when attn_alpha != 0, else 1.
+ */
+typedef struct rdcn_config {
+    int64_t batch_max;    /* largest batch any call will pass */
+    int32_t num_cat;      /* F: categorical features (>= 0) */
+    int32_t emb_dim;      /* D: embedding dimension (> 0) */
+    int32_t num_dense;    /* Nd: dense features (>= 0) */
+    int32_t rank;         /* r: low-rank dimension (> 0) */
+    int32_t num_layers;   /* L: cross layers (1 .. RDCN_MAX_LAYERS) */
+    int32_t qr_rows_q;    /* rows of every quotient table */
+    int32_t qr_rows_r;    /* m: rows of every remainder table, and the QR divisor */
+    int32_t combine;      /* rdcn_combine: how the two rows are aggregated */
+    int32_t multi_hot;    /* 0: one id per (sample, feature); 1: CSR bags, sum pooling */
+    int32_t id_type;      /* rdcn_idtype of the id array */
+    int32_t dtype;        /* rdcn_dtype of tables, dense, x0, activations and weights */
+    int32_t reserved0;    /* must be 0 */
+    int64_t vocab;        /* V: valid ids are [0, V); requires qr_rows_q * qr_rows_r >= V */
+    float attn_alpha;     /* alpha: weight of the attention path (0 = plain low-rank DCNv2) */
+    float skip_beta;      /* beta: weight of the skip (value) path */
+    float temperature;    /* tau > 0: scores are q_i k_j / tau */
+    int32_t reserved1;    /* must be 0 */
+} rdcn_config;
+
+/*
+ * Per-layer weight pointers (entries at index >= num_layers are ignored).
+ *   w_down[l] : [n*r, d]  rows 0..r-1 = V_l^T (value), r..2r-1 = Q_l^T, 2r..3r-1 = K_l^T
+ *   u[l]      : [d, r]    up projection U_l
+ *   bias[l]   : [d]       b_l
+ * Weights are in the storage dtype; gradients use the same struct with float pointers.
+ */
+typedef struct rdcn_weights {
+    void* w_down[RDCN_MAX_LAYERS];
+    void* u[RDCN_MAX_LAYERS];
+    void* bias[RDCN_MAX_LAYERS];
+} rdcn_weights;
+
+typedef struct rdcn_handle rdcn_handle;
+
+/*
+ * Validate `cfg` and create a handle (host metadata plus one device error word
+ * on the current device). Returns RDCN_ERR_ARG for null pointers or values out
+ * of range, RDCN_ERR_SHAPE if qr_rows_q * qr_rows_r < vocab, and
+ * RDCN_ERR_UNSUPPORTED when a bf16 model has emb_dim, num_dense or rank not a
+ * multiple of 8 (fp32: multiple of 4), which the vector loads need, when
+ * emb_dim > 256, when the attention term is on with rank > 2048 (one sample's
+ * attention rows are staged in 64 KiB of LDS), or when F * (qr_rows_q + m)
+ * does not fit the 31-bit sort keys of the embedding backward.
+ */
+rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out);
+
+/* Free the handle and its error word. NULL is accepted. */
+rdcn_status rdcn_destroy(rdcn_handle* h);
+
+/* Derived width d = F*D + Nd of x0 and of every x_l. */
+rdcn_status rdcn_dim(const rdcn_handle* h, int64_t* d);
+
+/*
+ * Device bytes the caller must provide for a batch of `batch` samples:
+ *   saved_bytes   -- activations written by rdcn_forward and read by rdcn_backward
+ *   scratch_bytes -- temporary space for rdcn_forward / rdcn_backward
+ * Both are 256-byte aligned sizes; the buffers must be 256-byte aligned.
+ */
+rdcn_status rdcn_workspace_bytes(const rdcn_handle* h, int64_t batch, size_t* saved_bytes, size_t* scratch_bytes);
+
+/*
+ * QR embedding gather (forward), section "Model Dictionary Compression":
+ *   ids      : single-hot [batch, F] (offsets == NULL), or multi-hot CSR values
+ *              with offsets [batch*F + 1] (int64) over bag index b*F + f
+ *   q_tables : [F, qr_rows_q, D],  r_tables : [F, m, D],  dense : [batch, Nd]
+ *   x0       : [batch, d] output, all in the storage dtype.
+ * Per element the combine is one float operation on the two table values
+ * (product or sum), bags are pooled by float addition in bag order starting
+ * from the first element (an empty bag gives +0), and the pooled float is
+ * rounded to the storage type (bf16: round to nearest, ties to even). An id
+ * outside [0, vocab) contributes nothing and raises the device error word
+ * (see rdcn_check_device_errors).
+ */
+rdcn_status qr_embed_gather(rdcn_handle* h, int64_t batch, const void* ids, const int64_t* offsets,
+                            const void* q_tables, const void* r_tables, const void* dense, void* x0,
+                            void* stream);
+
+/*
+ * Scratch bytes qr_embed_backward needs for `batch` samples holding `nnz` ids
+ * in total (single-hot: nnz = batch * F).
+ */
+rdcn_status qr_embed_backward_workspace(const rdcn_handle* h, int64_t batch, int64_t nnz, size_t* scratch_bytes);
+
+/*
+ * QR embedding backward: table gradients from the x0 gradient, ACCUMULATED (+=)
+ * into grad_q_tables [F, qr_rows_q, D] and grad_r_tables [F, m, D] (float).
+ * grad_x0 is [batch, d] float (only its embedding columns are read). For every
+ * valid id of bag (b, f) and g = grad_x0[b, f*D : (f+1)*D]:
+ *   sum combine:     gQ_f[qi] += g,            gR_f[ri] += g
+ *   product combine: gQ_f[qi] += g * R_f[ri],  gR_f[ri] += g * Q_f[qi]
+ * The contributions to one table row are added in (b, position-in-bag) order,
+ * so the result is deterministic. ids/offsets/tables as in qr_embed_gather;
+ * nnz = number of ids (batch * F when single-hot). scratch must hold
+ * qr_embed_backward_workspace() bytes.
+ */
+rdcn_status qr_embed_backward(rdcn_handle* h, int64_t batch, int64_t nnz, const void* ids, const int64_t* offsets,
+                              const void* q_tables, const void* r_tables, const float* grad_x0,
+                              float* grad_q_tables, float* grad_r_tables, void* scratch, size_t scratch_bytes,
+                              void* stream);
+
+/*
+ * Residual-DCN forward, section "Residual DCN". x0 [batch, d] -> x_out = x_L
+ * [batch, d], storage dtype. For each layer: [v; q; k] = W_l x_l (bf16 MFMA,
+ * float accumulate); if alpha != 0, per sample S_ij = q_i k_j / tau, A = row
+ * softmax of S, o = A v; h = beta v + alpha o; t = U_l h + b_l;
+ * x_{l+1} = x0 * t + x_l. `saved` (saved_bytes) receives what rdcn_backward
+ * needs and must stay untouched until then; `scratch` holds scratch_bytes.
+ * With the attention term on, [v; q; k] are kept in float (they feed the
+ * softmax, whose sharpness amplifies any rounding of q and k); h, t and x_l
+ * are kept in the storage dtype.
+ */
+rdcn_status rdcn_forward(rdcn_handle* h, int64_t batch, const void* x0, const rdcn_weights* w, void* x_out,
+                         void* saved, void* scratch, void* stream);
+
+/*
+ * Residual-DCN backward for the loss whose gradient w.r.t. x_L is grad_out
+ * [batch, d] (storage dtype). Writes (overwrites) grad_x0 [batch, d] (float)
+ * and the float weight gradients in `grads` (same shapes as the weights,
+ * summed over the batch). x0, w and saved must be those of the matching
+ * rdcn_forward call.
+ */
+rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const rdcn_weights* w, const void* saved,
+                          const void* grad_out, float* grad_x0, const rdcn_weights* grads, void* scratch,
+                          void* stream);
+
+/*
+ * Wait for `stream`, then read and clear the device error word:
+ * RDCN_ERR_INDEX if any id outside [0, vocab) was met since the last check,
+ * RDCN_ERR_HIP on a runtime error, RDCN_OK otherwise.
+ */
+rdcn_status rdcn_check_device_errors(rdcn_handle* h, void* stream);
+
+/* Static description of a status code. */
+const char* rdcn_status_string(rdcn_status s);
+
+/*
+ * Kernel launch sites, for per-kernel timing. Each entry is one kernel,
+ * except RDCN_KERNEL_EMB_SORT (all launches of one radix-sort pass sequence:
+ * histogram, scan, scatter) and RDCN_KERNEL_EMB_REDUCE (segmented reduction
+ * plus its fix-up).
+ */
+typedef enum rdcn_kernel {
+    RDCN_KERNEL_GATHER = 0,         /* qr_embed_gather */
+    RDCN_KERNEL_FWD_DOWN_GEMM = 1,  /* [v|q|k] = x_l W^T */
+    RDCN_KERNEL_FWD_ATTENTION = 2,  /* per-sample softmax attention, h = beta v + alpha o */
+    RDCN_KERNEL_FWD_UP_GEMM = 3,    /* t = h U^T + b, x_{l+1} = x0 * t + x_l */
+    RDCN_KERNEL_BWD_POINTWISE = 4,  /* gt = g * x0, grad_x0 += g * t, bias partials */
+    RDCN_KERNEL_BWD_BIAS = 5,       /* bias partials -> bias gradient */
+    RDCN_KERNEL_BWD_GU_GEMM = 6,    /* gU = gt^T h */
+    RDCN_KERNEL_BWD_GH_GEMM = 7,    /* gh = gt U */
+    RDCN_KERNEL_BWD_ATTENTION = 8,  /* attention backward -> [gv|gq|gk] */
+    RDCN_KERNEL_BWD_GW_GEMM = 9,    /* gW = [gv|gq|gk]^T x_l */
+    RDCN_KERNEL_BWD_GX_GEMM = 10,   /* g_l = g_{l+1} + [gv|gq|gk] W */
+    RDCN_KERNEL_SPLITK_REDUCE = 11, /* ordered sum of split-K partials of gU / gW */
+    RDCN_KERNEL_EMB_KEYS = 12,      /* embedding backward: row keys */
+    RDCN_KERNEL_EMB_SORT = 13,      /* embedding backward: stable radix sort */
+    RDCN_KERNEL_EMB_REDUCE = 14,    /* embedding backward: segmented reduction + fix-up */
+    RDCN_KERNEL_COUNT = 15
+} rdcn_kernel;
+
+/*
+ * Per-kernel timing with HIP events on the stream each kernel is launched on.
+ * After rdcn_profile_start, each launch site whose bit (1 << rdcn_kernel) is
+ * set in `kernel_mask` records an event before and after its kernel(s), up to
+ * `max_launches` launches in total (events are created here, not during the
+ * timed calls). rdcn_profile_stop waits for the
+ * recorded events, writes the summed milliseconds and the number of timed
+ * launches per rdcn_kernel into ms[RDCN_KERNEL_COUNT] and
+ * launches[RDCN_KERNEL_COUNT], and turns timing off. Timing adds one event
+ * pair per launch; it is meant for measurement runs.
+ */
+rdcn_status rdcn_profile_start(rdcn_handle* h, int32_t max_launches, uint32_t kernel_mask);
+rdcn_status rdcn_profile_stop(rdcn_handle* h, double* ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RDCN_H */

@@ -1,0 +1,552 @@
+// Host side of the librdcn C ABI (declared in include/rdcn.h): argument
+// validation, workspace layouts, and the order of kernel launches for the
+// gather, the Residual-DCN forward and backward, and the embedding backward.
+#include <hip/hip_runtime.h>
+
+#include <new>
+#include <string.h>
+#include <vector>
+
+#include "../../include/rdcn.h"
+#include "embed_bwd.h"
+#include "gemm.h"
+#include "kernels.h"
+
+struct rdcn_handle {
+    rdcn_config cfg;
+    int64_t d;
+    int n;  // projections per layer (3 with the attention term, else 1)
+    bool bf16, ids64, attn;
+    uint32_t magic, shift;
+    int* err;  // device error word
+    // per-kernel timing (rdcn_profile_start / rdcn_profile_stop)
+    bool prof_on = false;
+    uint32_t prof_mask = 0;
+    std::vector<hipEvent_t> prof_ev;   // 2 per launch
+    std::vector<int> prof_kind;        // kernel of each recorded pair
+    size_t prof_used = 0;
+};
+
+namespace {
+
+// Brackets the launches of one kernel with an event pair when timing is on.
+struct ProfScope {
+    rdcn_handle* h;
+    hipStream_t s;
+    bool active;
+    ProfScope(rdcn_handle* hh, int kind, hipStream_t ss) : h(hh), s(ss), active(false) {
+        if (h->prof_on && ((h->prof_mask >> kind) & 1u) && 2 * (h->prof_used + 1) <= h->prof_ev.size()) {
+            active = hipEventRecord(h->prof_ev[2 * h->prof_used], s) == hipSuccess;
+            if (active) h->prof_kind.push_back(kind);
+        }
+    }
+    ~ProfScope() {
+        if (active) {
+            (void)hipEventRecord(h->prof_ev[2 * h->prof_used + 1], s);
+            ++h->prof_used;
+        }
+    }
+};
+
+}  // namespace
+
+namespace {
+
+using namespace rdcn;
+
+constexpr size_t ALIGN = 256;
+inline size_t al(size_t x) { return (x + ALIGN - 1) & ~(ALIGN - 1); }
+
+inline rdcn_status hip_status(hipError_t e) { return e == hipSuccess ? RDCN_OK : RDCN_ERR_HIP; }
+#define RDCN_TRY(expr)                                   \
+    do {                                                 \
+        hipError_t _e = (expr);                          \
+        if (_e != hipSuccess) return RDCN_ERR_HIP;       \
+    } while (0)
+
+// Granlund-Montgomery magic number for unsigned 32-bit division by m >= 1.
+void div_magic_host(uint32_t m, uint32_t& magic, uint32_t& shift) {
+    if (m <= 1) {
+        magic = 1;
+        shift = 0;
+        return;
+    }
+    uint32_t l = 0;
+    while (((uint64_t)1 << l) < m) ++l;  // l = ceil(log2 m)
+    magic = (uint32_t)((((uint64_t)1 << 32) * (((uint64_t)1 << l) - m)) / m + 1);
+    shift = l - 1;
+}
+
+size_t eb(const rdcn_handle* h) { return h->bf16 ? 2 : 4; }
+
+struct SavedLayout {
+    size_t P[RDCN_MAX_LAYERS], H[RDCN_MAX_LAYERS], T[RDCN_MAX_LAYERS], X[RDCN_MAX_LAYERS];
+    size_t total;
+};
+
+SavedLayout saved_layout(const rdcn_handle* h, int64_t B) {
+    SavedLayout s;
+    const size_t e = eb(h), d = (size_t)h->d, r = (size_t)h->cfg.rank, n = (size_t)h->n;
+    size_t off = 0;
+    for (int l = 0; l < h->cfg.num_layers; ++l) {
+        s.P[l] = off; off += al(B * n * r * (h->attn ? 4 : e));  // float [v|q|k] feeds the attention
+        s.H[l] = off; off += h->attn ? al(B * r * e) : 0;
+        s.T[l] = off; off += al(B * d * e);
+        s.X[l] = off; off += (l + 1 < h->cfg.num_layers) ? al(B * d * e) : 0;  // x_{l+1}
+    }
+    s.total = off;
+    return s;
+}
+
+struct ScratchLayout {
+    size_t g, gt, gh, gP, part, splitk, total;
+    int nrb;
+};
+
+int64_t splitk_elems(const rdcn_handle* h, int64_t B) {
+    const int64_t d = h->d, r = h->cfg.rank, nr = (int64_t)h->n * r;
+    const GemmPlan pu = plan_gemm(d, r, B, h->bf16, true);
+    const GemmPlan pw = plan_gemm(nr, d, B, h->bf16, true);
+    int64_t m = 0;
+    if (pu.splits > 1) m = pu.splits * d * r;
+    if (pw.splits > 1 && pw.splits * nr * d > m) m = pw.splits * nr * d;
+    return m;
+}
+
+ScratchLayout scratch_layout(const rdcn_handle* h, int64_t B) {
+    ScratchLayout s;
+    const size_t e = eb(h), d = (size_t)h->d, r = (size_t)h->cfg.rank, n = (size_t)h->n;
+    s.nrb = B > 0 ? (int)((B + pointwise_rows_per_block(B, d) - 1) / pointwise_rows_per_block(B, d)) : 0;
+    size_t off = 0;
+    s.g = off; off += al(B * d * 4);
+    s.gt = off; off += al(B * d * e);
+    s.gh = off; off += h->attn ? al(B * r * 4) : 0;
+    s.gP = off; off += al(B * n * r * e);
+    s.part = off; off += al((size_t)s.nrb * d * 4);
+    s.splitk = off; off += al((size_t)splitk_elems(h, B) * 4);
+    s.total = off;
+    return s;
+}
+
+bool aligned256(const void* p) { return ((uintptr_t)p & 255u) == 0; }
+
+rdcn_status check_batch(const rdcn_handle* h, int64_t batch) {
+    if (!h) return RDCN_ERR_ARG;
+    if (batch < 0) return RDCN_ERR_ARG;
+    if (batch > h->cfg.batch_max) return RDCN_ERR_SHAPE;
+    return RDCN_OK;
+}
+
+// One GEMM with split-K handled: writes the final float result to `out` (ldc = N).
+hipError_t gemm_weight_grad(rdcn_handle* h, int kind, GemmArgs g, float* out, float* splitk, hipStream_t s) {
+    const GemmPlan p = plan_gemm(g.M, g.N, g.K, h->bf16, true);
+    if (g.K == 0) return launch_fill_zero(out, g.M * g.N, s);
+    g.ldc = g.N;
+    if (p.splits == 1) {
+        g.epi = EPI_STORE_F32;
+        g.c = out;
+        ProfScope ps(h, kind, s);
+        return launch_gemm(g, p, h->bf16, s);
+    }
+    g.epi = EPI_PARTIAL;
+    g.c = splitk;
+    {
+        ProfScope ps(h, kind, s);
+        hipError_t e = launch_gemm(g, p, h->bf16, s);
+        if (e != hipSuccess) return e;
+    }
+    ProfScope ps(h, RDCN_KERNEL_SPLITK_REDUCE, s);
+    return launch_splitk_reduce(splitk, p.splits, g.M * g.N, out, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* rdcn_status_string(rdcn_status s) {
+    switch (s) {
+        case RDCN_OK: return "ok";
+        case RDCN_ERR_ARG: return "invalid argument";
+        case RDCN_ERR_SHAPE: return "inconsistent shape";
+        case RDCN_ERR_INDEX: return "id outside [0, vocab)";
+        case RDCN_ERR_UNSUPPORTED: return "unsupported configuration";
+        case RDCN_ERR_WORKSPACE: return "workspace too small or misaligned";
+        case RDCN_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
+    if (!cfg || !out) return RDCN_ERR_ARG;
+    *out = nullptr;
+    const rdcn_config& c = *cfg;
+    if (c.batch_max < 0 || c.num_cat < 0 || c.emb_dim <= 0 || c.num_dense < 0 || c.rank <= 0 ||
+        c.num_layers < 1 || c.num_layers > RDCN_MAX_LAYERS || c.qr_rows_q <= 0 || c.qr_rows_r <= 0 ||
+        (c.combine != RDCN_COMBINE_MUL && c.combine != RDCN_COMBINE_SUM) || (c.multi_hot != 0 && c.multi_hot != 1) ||
+        (c.id_type != RDCN_I32 && c.id_type != RDCN_I64) || (c.dtype != RDCN_F32 && c.dtype != RDCN_BF16) ||
+        c.vocab <= 0 || !(c.temperature > 0.0f) || c.reserved0 != 0 || c.reserved1 != 0 ||
+        c.attn_alpha != c.attn_alpha || c.skip_beta != c.skip_beta)
+        return RDCN_ERR_ARG;
+    if ((int64_t)c.qr_rows_q * (int64_t)c.qr_rows_r < c.vocab) return RDCN_ERR_SHAPE;
+    const int64_t d = (int64_t)c.num_cat * c.emb_dim + c.num_dense;
+    if (d <= 0) return RDCN_ERR_SHAPE;
+    const int vec = c.dtype == RDCN_BF16 ? 8 : 4;
+    if (c.emb_dim % vec || c.num_dense % vec || c.rank % vec || c.emb_dim > 256) return RDCN_ERR_UNSUPPORTED;
+    const int n = c.attn_alpha != 0.0f ? 3 : 1;
+    // sort keys and occurrence indices are 32-bit
+    if ((int64_t)c.num_cat * ((int64_t)c.qr_rows_q + c.qr_rows_r) >= (int64_t)1 << 31) return RDCN_ERR_UNSUPPORTED;
+    if (c.attn_alpha != 0.0f && c.rank > 2048) return RDCN_ERR_UNSUPPORTED;  // attention rows staged in LDS (<= 64 KiB)
+    (void)n;
+
+    rdcn_handle* h = new (std::nothrow) rdcn_handle();
+    if (!h) return RDCN_ERR_HIP;
+    h->cfg = c;
+    h->d = d;
+    h->attn = c.attn_alpha != 0.0f;
+    h->n = h->attn ? 3 : 1;
+    h->bf16 = c.dtype == RDCN_BF16;
+    h->ids64 = c.id_type == RDCN_I64;
+    div_magic_host((uint32_t)c.qr_rows_r, h->magic, h->shift);
+    if (hipMalloc((void**)&h->err, sizeof(int)) != hipSuccess) {
+        (void)hipGetLastError();
+        delete h;
+        return RDCN_ERR_HIP;
+    }
+    if (hipMemset(h->err, 0, sizeof(int)) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+        (void)hipFree(h->err);
+        delete h;
+        return RDCN_ERR_HIP;
+    }
+    *out = h;
+    return RDCN_OK;
+}
+
+rdcn_status rdcn_destroy(rdcn_handle* h) {
+    if (!h) return RDCN_OK;
+    rdcn_status s = RDCN_OK;
+    for (hipEvent_t e : h->prof_ev) (void)hipEventDestroy(e);
+    if (h->err && hipFree(h->err) != hipSuccess) s = RDCN_ERR_HIP;
+    delete h;
+    return s;
+}
+
+rdcn_status rdcn_dim(const rdcn_handle* h, int64_t* d) {
+    if (!h || !d) return RDCN_ERR_ARG;
+    *d = h->d;
+    return RDCN_OK;
+}
+
+rdcn_status rdcn_workspace_bytes(const rdcn_handle* h, int64_t batch, size_t* saved_bytes, size_t* scratch_bytes) {
+    rdcn_status st = check_batch(h, batch);
+    if (st != RDCN_OK) return st;
+    if (!saved_bytes || !scratch_bytes) return RDCN_ERR_ARG;
+    *saved_bytes = saved_layout(h, batch).total;
+    *scratch_bytes = scratch_layout(h, batch).total;
+    return RDCN_OK;
+}
+
+rdcn_status qr_embed_gather(rdcn_handle* h, int64_t batch, const void* ids, const int64_t* offsets,
+                            const void* q_tables, const void* r_tables, const void* dense, void* x0, void* stream) {
+    rdcn_status st = check_batch(h, batch);
+    if (st != RDCN_OK) return st;
+    const rdcn_config& c = h->cfg;
+    if ((offsets != nullptr) != (c.multi_hot != 0)) return RDCN_ERR_ARG;
+    if (batch == 0) return RDCN_OK;
+    if (!x0 || (c.num_cat > 0 && (!ids || !q_tables || !r_tables)) || (c.num_dense > 0 && !dense))
+        return RDCN_ERR_ARG;
+    GatherArgs a;
+    a.batch = batch;
+    a.F = c.num_cat;
+    a.D = c.emb_dim;
+    a.Nd = c.num_dense;
+    a.rows_q = c.qr_rows_q;
+    a.m = (uint32_t)c.qr_rows_r;
+    a.vocab = (uint64_t)c.vocab;
+    a.magic = h->magic;
+    a.shift = h->shift;
+    a.combine = c.combine == RDCN_COMBINE_MUL ? 0 : 1;
+    a.ids = ids;
+    a.offsets = offsets;
+    a.q_tables = q_tables;
+    a.r_tables = r_tables;
+    a.dense = dense;
+    a.x0 = x0;
+    a.err = h->err;
+    ProfScope ps(h, RDCN_KERNEL_GATHER, (hipStream_t)stream);
+    return hip_status(launch_qr_gather(a, h->bf16, h->ids64, (hipStream_t)stream));
+}
+
+rdcn_status qr_embed_backward_workspace(const rdcn_handle* h, int64_t batch, int64_t nnz, size_t* scratch_bytes) {
+    rdcn_status st = check_batch(h, batch);
+    if (st != RDCN_OK) return st;
+    if (!scratch_bytes || nnz < 0) return RDCN_ERR_ARG;
+    if (!h->cfg.multi_hot && nnz != batch * h->cfg.num_cat) return RDCN_ERR_SHAPE;
+    if (2 * nnz >= ((int64_t)1 << 31)) return RDCN_ERR_UNSUPPORTED;
+    const EmbedBwdLayout L =
+        embed_bwd_layout(nnz, h->cfg.num_cat, h->cfg.qr_rows_q, h->cfg.qr_rows_r, h->cfg.emb_dim, h->cfg.multi_hot);
+    *scratch_bytes = al(L.total);
+    return RDCN_OK;
+}
+
+rdcn_status qr_embed_backward(rdcn_handle* h, int64_t batch, int64_t nnz, const void* ids, const int64_t* offsets,
+                              const void* q_tables, const void* r_tables, const float* grad_x0,
+                              float* grad_q_tables, float* grad_r_tables, void* scratch, size_t scratch_bytes,
+                              void* stream) {
+    size_t need = 0;
+    rdcn_status st = qr_embed_backward_workspace(h, batch, nnz, &need);
+    if (st != RDCN_OK) return st;
+    const rdcn_config& c = h->cfg;
+    if ((offsets != nullptr) != (c.multi_hot != 0)) return RDCN_ERR_ARG;
+    if (batch == 0 || nnz == 0 || c.num_cat == 0) return RDCN_OK;
+    if (!ids || !q_tables || !r_tables || !grad_x0 || !grad_q_tables || !grad_r_tables || !scratch)
+        return RDCN_ERR_ARG;
+    if (scratch_bytes < need || !aligned256(scratch)) return RDCN_ERR_WORKSPACE;
+    EmbedBwdArgs a;
+    a.batch = batch;
+    a.nnz = nnz;
+    a.d = h->d;
+    a.F = c.num_cat;
+    a.D = c.emb_dim;
+    a.rows_q = c.qr_rows_q;
+    a.m = (uint32_t)c.qr_rows_r;
+    a.vocab = (uint64_t)c.vocab;
+    a.combine = c.combine == RDCN_COMBINE_MUL ? 0 : 1;
+    a.ids = ids;
+    a.offsets = offsets;
+    a.q_tables = q_tables;
+    a.r_tables = r_tables;
+    a.grad_x0 = grad_x0;
+    a.grad_q = grad_q_tables;
+    a.grad_r = grad_r_tables;
+    hipStream_t s = (hipStream_t)stream;
+    {
+        ProfScope ps(h, RDCN_KERNEL_EMB_KEYS, s);
+        RDCN_TRY(launch_emb_keys(a, h->ids64, scratch, s));
+    }
+    {
+        ProfScope ps(h, RDCN_KERNEL_EMB_SORT, s);
+        RDCN_TRY(launch_emb_sort(a, scratch, s));
+    }
+    ProfScope ps(h, RDCN_KERNEL_EMB_REDUCE, s);
+    return hip_status(launch_emb_reduce(a, h->bf16, h->ids64, scratch, s));
+}
+
+static rdcn_status check_weights(const rdcn_handle* h, const rdcn_weights* w) {
+    if (!w) return RDCN_ERR_ARG;
+    for (int l = 0; l < h->cfg.num_layers; ++l)
+        if (!w->w_down[l] || !w->u[l] || !w->bias[l]) return RDCN_ERR_ARG;
+    return RDCN_OK;
+}
+
+rdcn_status rdcn_forward(rdcn_handle* h, int64_t batch, const void* x0, const rdcn_weights* w, void* x_out,
+                         void* saved, void* scratch, void* stream) {
+    rdcn_status st = check_batch(h, batch);
+    if (st != RDCN_OK) return st;
+    if ((st = check_weights(h, w)) != RDCN_OK) return st;
+    if (batch == 0) return RDCN_OK;
+    if (!x0 || !x_out || !saved) return RDCN_ERR_ARG;
+    if (!aligned256(saved)) return RDCN_ERR_WORKSPACE;
+    (void)scratch;
+    hipStream_t s = (hipStream_t)stream;
+    const rdcn_config& c = h->cfg;
+    const int64_t B = batch, d = h->d, r = c.rank, nr = (int64_t)h->n * r;
+    const SavedLayout S = saved_layout(h, B);
+    char* sv = (char*)saved;
+    const void* xcur = x0;
+    for (int l = 0; l < c.num_layers; ++l) {
+        void* P = sv + S.P[l];
+        GemmArgs g{};
+        g.M = B; g.N = nr; g.K = d;
+        g.a = xcur; g.lda = d;
+        g.b = w->w_down[l]; g.ldb = d;
+        g.epi = h->attn ? EPI_STORE_F32 : EPI_STORE; g.scale = 1.0f;
+        g.c = P; g.ldc = nr;
+        {
+            ProfScope ps(h, RDCN_KERNEL_FWD_DOWN_GEMM, s);
+            RDCN_TRY(launch_gemm(g, plan_gemm(B, nr, d, h->bf16, false), h->bf16, s));
+        }
+        const void* hsrc = P;
+        int64_t ldh = nr;
+        float scale = c.skip_beta;
+        if (h->attn) {
+            void* H = sv + S.H[l];
+            ProfScope ps(h, RDCN_KERNEL_FWD_ATTENTION, s);
+            RDCN_TRY(launch_attn_fwd(B, (int)r, c.attn_alpha, c.skip_beta, c.temperature, P, nr, H, r, h->bf16, s));
+            hsrc = H;
+            ldh = r;
+            scale = 1.0f;
+        }
+        void* xnext = (l + 1 < c.num_layers) ? (void*)(sv + S.X[l]) : x_out;
+        GemmArgs u{};
+        u.M = B; u.N = d; u.K = r;
+        u.a = hsrc; u.lda = ldh;
+        u.b = w->u[l]; u.ldb = r;
+        u.epi = EPI_CROSS; u.scale = scale;
+        u.c = xnext; u.ldc = d;
+        u.bias = w->bias[l]; u.x0 = x0; u.xl = xcur; u.t_out = sv + S.T[l]; u.ldx = d;
+        {
+            ProfScope ps(h, RDCN_KERNEL_FWD_UP_GEMM, s);
+            RDCN_TRY(launch_gemm(u, plan_gemm(B, d, r, h->bf16, false), h->bf16, s));
+        }
+        xcur = xnext;
+    }
+    return RDCN_OK;
+}
+
+rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const rdcn_weights* w, const void* saved,
+                          const void* grad_out, float* grad_x0, const rdcn_weights* grads, void* scratch,
+                          void* stream) {
+    rdcn_status st = check_batch(h, batch);
+    if (st != RDCN_OK) return st;
+    if ((st = check_weights(h, w)) != RDCN_OK) return st;
+    if ((st = check_weights(h, grads)) != RDCN_OK) return st;
+    const rdcn_config& c = h->cfg;
+    hipStream_t s = (hipStream_t)stream;
+    const int64_t B = batch, d = h->d, r = c.rank, nr = (int64_t)h->n * r;
+    if (batch == 0) {  // gradients of an empty batch are zero
+        for (int l = 0; l < c.num_layers; ++l) {
+            RDCN_TRY(launch_fill_zero((float*)grads->w_down[l], nr * d, s));
+            RDCN_TRY(launch_fill_zero((float*)grads->u[l], d * r, s));
+            RDCN_TRY(launch_fill_zero((float*)grads->bias[l], d, s));
+        }
+        return RDCN_OK;
+    }
+    if (!x0 || !saved || !grad_out || !grad_x0 || !scratch) return RDCN_ERR_ARG;
+    if (!aligned256(saved) || !aligned256(scratch)) return RDCN_ERR_WORKSPACE;
+    const SavedLayout S = saved_layout(h, B);
+    const ScratchLayout W = scratch_layout(h, B);
+    const char* sv = (const char*)saved;
+    char* sc = (char*)scratch;
+    float* g = (float*)(sc + W.g);
+    void* gt = sc + W.gt;
+    float* gh = (float*)(sc + W.gh);
+    void* gP = sc + W.gP;
+    float* part = (float*)(sc + W.part);
+    float* splitk = (float*)(sc + W.splitk);
+
+    for (int l = c.num_layers - 1; l >= 0; --l) {
+        const bool top = l == c.num_layers - 1;
+        const void* gin = top ? grad_out : (const void*)g;
+        const void* P = sv + S.P[l];
+        const void* xl = l == 0 ? x0 : (const void*)(sv + S.X[l - 1]);
+        // gt = g * x0, grad_x0 (+)= g * t_l, bias partials
+        {
+            ProfScope ps(h, RDCN_KERNEL_BWD_POINTWISE, s);
+            RDCN_TRY(launch_bwd_pointwise(B, d, gin, !top, x0, sv + S.T[l], grad_x0, top, gt, part, h->bf16, s));
+        }
+        {
+            ProfScope ps(h, RDCN_KERNEL_BWD_BIAS, s);
+            RDCN_TRY(launch_colsum(part, W.nrb, d, (float*)grads->bias[l], s));
+        }
+        const void* hsrc = h->attn ? (const void*)(sv + S.H[l]) : P;
+        const int64_t ldh = h->attn ? r : nr;
+        const float hscale = h->attn ? 1.0f : c.skip_beta;
+        // gU = gt^T h      [d, r], K = batch
+        {
+            GemmArgs g1{};
+            g1.M = d; g1.N = r; g1.K = B;
+            g1.a = gt; g1.lda = d; g1.a_kstrided = true;
+            g1.b = hsrc; g1.ldb = ldh; g1.b_kstrided = true;
+            g1.scale = hscale;
+            RDCN_TRY(gemm_weight_grad(h, RDCN_KERNEL_BWD_GU_GEMM, g1, (float*)grads->u[l], splitk, s));
+        }
+        // gh = gt U         [B, r]
+        {
+            GemmArgs g2{};
+            g2.M = B; g2.N = r; g2.K = d;
+            g2.a = gt; g2.lda = d;
+            g2.b = w->u[l]; g2.ldb = r; g2.b_kstrided = true;
+            if (h->attn) {
+                g2.epi = EPI_STORE_F32; g2.scale = 1.0f; g2.c = gh; g2.ldc = r;
+            } else {
+                g2.epi = EPI_STORE; g2.scale = c.skip_beta; g2.c = gP; g2.ldc = nr;  // gv = beta * gh
+            }
+            ProfScope ps(h, RDCN_KERNEL_BWD_GH_GEMM, s);
+            RDCN_TRY(launch_gemm(g2, plan_gemm(B, r, d, h->bf16, false), h->bf16, s));
+        }
+        if (h->attn) {
+            ProfScope ps(h, RDCN_KERNEL_BWD_ATTENTION, s);
+            RDCN_TRY(launch_attn_bwd(B, (int)r, c.attn_alpha, c.skip_beta, c.temperature, P, nr, gh, r, gP, nr,
+                                     h->bf16, s));
+        }
+        // gW = gP^T x_l    [n r, d], K = batch
+        {
+            GemmArgs g3{};
+            g3.M = nr; g3.N = d; g3.K = B;
+            g3.a = gP; g3.lda = nr; g3.a_kstrided = true;
+            g3.b = xl; g3.ldb = d; g3.b_kstrided = true;
+            g3.scale = 1.0f;
+            RDCN_TRY(gemm_weight_grad(h, RDCN_KERNEL_BWD_GW_GEMM, g3, (float*)grads->w_down[l], splitk, s));
+        }
+        // g_l = g_{l+1} + gP W   (layer 0: grad_x0 += g_1 + gP W)
+        {
+            GemmArgs g4{};
+            g4.M = B; g4.N = d; g4.K = nr;
+            g4.a = gP; g4.lda = nr;
+            g4.b = w->w_down[l]; g4.ldb = d; g4.b_kstrided = true;
+            g4.scale = 1.0f;
+            g4.gin = gin; g4.gin_f32 = !top; g4.ldx = d;
+            g4.epi = l == 0 ? EPI_RESID_X0 : EPI_RESID;
+            g4.c = l == 0 ? (void*)grad_x0 : (void*)g; g4.ldc = d;
+            ProfScope ps(h, RDCN_KERNEL_BWD_GX_GEMM, s);
+            RDCN_TRY(launch_gemm(g4, plan_gemm(B, d, nr, h->bf16, false), h->bf16, s));
+        }
+    }
+    return RDCN_OK;
+}
+
+rdcn_status rdcn_profile_start(rdcn_handle* h, int32_t max_launches, uint32_t kernel_mask) {
+    if (!h || max_launches < 0) return RDCN_ERR_ARG;
+    for (hipEvent_t e : h->prof_ev) (void)hipEventDestroy(e);
+    h->prof_ev.clear();
+    h->prof_kind.clear();
+    h->prof_used = 0;
+    h->prof_ev.resize(2 * (size_t)max_launches);
+    for (auto& e : h->prof_ev)
+        if (hipEventCreate(&e) != hipSuccess) return RDCN_ERR_HIP;
+    h->prof_kind.reserve(max_launches);
+    h->prof_mask = kernel_mask;
+    h->prof_on = true;
+    return RDCN_OK;
+}
+
+rdcn_status rdcn_profile_stop(rdcn_handle* h, double* ms, int64_t* launches) {
+    if (!h || !ms || !launches) return RDCN_ERR_ARG;
+    h->prof_on = false;
+    for (int k = 0; k < RDCN_KERNEL_COUNT; ++k) {
+        ms[k] = 0.0;
+        launches[k] = 0;
+    }
+    rdcn_status st = RDCN_OK;
+    for (size_t i = 0; i < h->prof_used; ++i) {
+        if (hipEventSynchronize(h->prof_ev[2 * i + 1]) != hipSuccess) {
+            st = RDCN_ERR_HIP;
+            break;
+        }
+        float t = 0.f;
+        if (hipEventElapsedTime(&t, h->prof_ev[2 * i], h->prof_ev[2 * i + 1]) != hipSuccess) {
+            st = RDCN_ERR_HIP;
+            break;
+        }
+        ms[h->prof_kind[i]] += t;
+        launches[h->prof_kind[i]] += 1;
+    }
+    h->prof_used = 0;
+    h->prof_kind.clear();
+    return st;
+}
+
+rdcn_status rdcn_check_device_errors(rdcn_handle* h, void* stream) {
+    if (!h) return RDCN_ERR_ARG;
+    if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return RDCN_ERR_HIP;
+    int v = 0;
+    if (hipMemcpy(&v, h->err, sizeof(int), hipMemcpyDeviceToHost) != hipSuccess) return RDCN_ERR_HIP;
+    if (v != 0) {
+        const int zero = 0;
+        if (hipMemcpy(h->err, &zero, sizeof(int), hipMemcpyHostToDevice) != hipSuccess) return RDCN_ERR_HIP;
+        return RDCN_ERR_INDEX;
+    }
+    return RDCN_OK;
+}
+
+}  // extern "C"

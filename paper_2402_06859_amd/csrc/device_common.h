@@ -1,0 +1,71 @@
+// Device-side helpers shared by the gfx950 kernels of librdcn.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rdcn {
+
+typedef uint16_t bf16_t;  // raw bfloat16 bits
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t raw16) { return __uint_as_float(raw16 << 16); }
+
+// float -> bfloat16 bits, round to nearest, ties to even (NaN kept quiet).
+__device__ __forceinline__ uint32_t f32_to_bf16(float x) {
+    uint32_t u = __float_as_uint(x);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+// Two floats -> one word holding (lo, hi) bfloat16 values.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) { return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16); }
+
+// Storage-type traits: T is float or bf16_t.
+template <typename T> struct st;
+template <> struct st<float> {
+    static constexpr int vec = 4;  // elements per 16-byte vector
+    __device__ static __forceinline__ float load(const float* p) { return *p; }
+    __device__ static __forceinline__ void store(float* p, float v) { *p = v; }
+    // 16-byte vector <-> 4 floats
+    __device__ static __forceinline__ void unpack(const u32x4_t& w, float* v) {
+        v[0] = __uint_as_float(w.x); v[1] = __uint_as_float(w.y);
+        v[2] = __uint_as_float(w.z); v[3] = __uint_as_float(w.w);
+    }
+    __device__ static __forceinline__ u32x4_t pack(const float* v) {
+        return u32x4_t{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])};
+    }
+};
+template <> struct st<bf16_t> {
+    static constexpr int vec = 8;
+    __device__ static __forceinline__ float load(const bf16_t* p) { return bf16_to_f32(*p); }
+    __device__ static __forceinline__ void store(bf16_t* p, float v) { *p = (bf16_t)f32_to_bf16(v); }
+    __device__ static __forceinline__ void unpack(const u32x4_t& w, float* v) {
+        v[0] = __uint_as_float(w.x << 16); v[1] = __uint_as_float(w.x & 0xffff0000u);
+        v[2] = __uint_as_float(w.y << 16); v[3] = __uint_as_float(w.y & 0xffff0000u);
+        v[4] = __uint_as_float(w.z << 16); v[5] = __uint_as_float(w.z & 0xffff0000u);
+        v[6] = __uint_as_float(w.w << 16); v[7] = __uint_as_float(w.w & 0xffff0000u);
+    }
+    __device__ static __forceinline__ u32x4_t pack(const float* v) {
+        return u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                       pack_bf16x2(v[6], v[7])};
+    }
+};
+
+// Unsigned 32-bit division by an invariant divisor m >= 1 (Granlund & Montgomery,
+// "Division by invariant integers using multiplication", 1994, unsigned case):
+//   t = mulhi(magic, n);  q = (t + ((n - t) >> 1)) >> shift_minus_1   (m > 1)
+struct DivMagic {
+    uint32_t magic;
+    uint32_t shift;  // l - 1 where l = ceil(log2 m); unused when m == 1
+    uint32_t m;
+};
+__device__ __forceinline__ uint32_t div_magic(uint32_t n, const DivMagic& dm) {
+    if (dm.m == 1) return n;
+    uint32_t t = __umulhi(dm.magic, n);
+    return (t + ((n - t) >> 1)) >> dm.shift;
+}
+
+}  // namespace rdcn

@@ -1,0 +1,33 @@
+// Embedding-backward launcher interface (see embed_bwd.hip).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rdcn {
+
+struct EmbedBwdArgs {
+    int64_t batch, nnz, d;
+    int32_t F, D, rows_q;
+    uint32_t m;
+    uint64_t vocab;
+    int combine;             // 0 = product, 1 = sum
+    const void* ids;
+    const int64_t* offsets;  // NULL = single-hot
+    const void* q_tables;
+    const void* r_tables;
+    const float* grad_x0;
+    float* grad_q;
+    float* grad_r;
+};
+
+struct EmbedBwdLayout {
+    uint64_t keys0, vals0, keys1, vals1, bag_of, hist, sums, carry_head, carry_tail, total;
+    int bits, passes, dbits;
+};
+
+EmbedBwdLayout embed_bwd_layout(int64_t nnz, int F, int rows_q, int m, int D, bool bags);
+hipError_t launch_emb_keys(const EmbedBwdArgs& a, bool ids64, void* scratch, hipStream_t s);
+hipError_t launch_emb_sort(const EmbedBwdArgs& a, void* scratch, hipStream_t s);
+hipError_t launch_emb_reduce(const EmbedBwdArgs& a, bool bf16, bool ids64, void* scratch, hipStream_t s);
+
+}  // namespace rdcn

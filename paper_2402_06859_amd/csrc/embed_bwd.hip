@@ -1,0 +1,481 @@
+// QR embedding backward for gfx950: table gradients from the x0 gradient.
+//
+// Every valid id occurrence of bag (b, f) with (qi, ri) = (id / m, id mod m)
+// (section "Model Dictionary Compression") adds g = dLoss/dx0[b, f*D:(f+1)*D]
+// (sum combine) or g * R_f[ri] / g * Q_f[qi] (product combine) to row qi of
+// Q_f and row ri of R_f; sum pooling gives each id of a bag the bag's gradient.
+//
+// Under Zipf-distributed ids a few rows receive a large share of all
+// occurrences, so the sum is not formed with atomics. Instead:
+//   1. keys: each occurrence gets two keys, its row in the concatenation of
+//      all quotient tables followed by all remainder tables; the value is the
+//      occurrence index (ids outside [0, V) get a sentinel key that sorts last);
+//   2. a stable LSD radix sort of (key, occurrence) pairs groups equal rows
+//      while keeping occurrence order inside each group;
+//   3. a segmented reduction walks the sorted pairs in fixed tiles, one wave
+//      per tile, lanes along D, adding contributions in sorted order;
+//      a segment that starts and ends inside its tile is written directly
+//      (+=), the pieces of a segment that crosses tile boundaries are kept per
+//      tile and summed in tile order by a fix-up pass.
+// The result is deterministic: each row's contributions are added in
+// (b, position-in-bag) order, irrespective of scheduling.
+#include "device_common.h"
+#include "embed_bwd.h"
+
+namespace rdcn {
+
+namespace {
+
+constexpr int RS_THREADS = 256;
+constexpr int RS_ITEMS = 16;
+constexpr int RS_TILE = RS_THREADS * RS_ITEMS;  // 4096 pairs per radix tile
+constexpr int SEG_TILE = 128;                    // sorted pairs per reduction wave
+
+template <typename ID>
+__device__ __forceinline__ bool split_id(ID raw, const EmbedBwdArgs& a, uint32_t& qi, uint32_t& ri) {
+    const int64_t id = (int64_t)raw;
+    if (id < 0 || (uint64_t)id >= a.vocab) return false;
+    const uint64_t q = (uint64_t)id / a.m;
+    qi = (uint32_t)q;
+    ri = (uint32_t)((uint64_t)id - q * a.m);
+    return qi < (uint32_t)a.rows_q;
+}
+
+// 1. keys. Single-hot: thread per occurrence o = b*F + f. Bags: thread per bag.
+template <typename ID, bool BAGS>
+__global__ __launch_bounds__(256) void k_emb_keys(EmbedBwdArgs a, uint32_t* __restrict__ keys,
+                                                  uint32_t* __restrict__ vals, uint32_t* __restrict__ bag_of) {
+    const ID* ids = (const ID*)a.ids;
+    const uint32_t sentinel = (uint32_t)a.F * (a.rows_q + a.m);
+    const uint32_t rbase = (uint32_t)a.F * a.rows_q;
+    const int64_t nunits = BAGS ? a.batch * a.F : a.nnz;
+    for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < nunits;
+         u += (int64_t)gridDim.x * blockDim.x) {
+        const int f = (int)(u % a.F);
+        const int64_t begin = BAGS ? a.offsets[u] : u;
+        const int64_t end = BAGS ? a.offsets[u + 1] : u + 1;
+        for (int64_t p = begin; p < end && p < a.nnz; ++p) {
+            uint32_t qi, ri, kq = sentinel, kr = sentinel;
+            if (split_id<ID>(ids[p], a, qi, ri)) {
+                kq = (uint32_t)f * a.rows_q + qi;
+                kr = rbase + (uint32_t)f * a.m + ri;
+            }
+            keys[p] = kq;
+            keys[a.nnz + p] = kr;
+            vals[p] = (uint32_t)p;
+            vals[a.nnz + p] = (uint32_t)p;
+            if (BAGS) bag_of[p] = (uint32_t)u;
+        }
+    }
+}
+
+// 2a. per-tile digit histogram, stored digit-major: hist[digit * ntiles + tile]
+__global__ __launch_bounds__(RS_THREADS) void k_rs_hist(const uint32_t* __restrict__ keys, uint32_t n, int shift,
+                                                        uint32_t mask, uint32_t* __restrict__ hist, int ntiles) {
+    __shared__ uint32_t h[256];
+    h[threadIdx.x] = 0;
+    __syncthreads();
+    const uint32_t base = blockIdx.x * RS_TILE;
+#pragma unroll
+    for (int i = 0; i < RS_ITEMS; ++i) {
+        const uint32_t e = base + i * RS_THREADS + threadIdx.x;
+        if (e < n) atomicAdd(&h[(keys[e] >> shift) & mask], 1u);
+    }
+    __syncthreads();
+    if (threadIdx.x <= mask) hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
+}
+
+// Exclusive scan of n words in three kernels: block sums, scan of the block
+// sums (one workgroup), apply. Blocks of 4096 words.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* sh, uint32_t& total) {
+    // 256 threads: wave inclusive scan, then wave totals.
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint32_t x = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t y = __shfl_up(x, off);
+        if (lane >= off) x += y;
+    }
+    if (lane == 63) sh[wave] = x;
+    __syncthreads();
+    uint32_t wofs = 0;
+    for (int w = 0; w < wave; ++w) wofs += sh[w];
+    total = sh[0] + sh[1] + sh[2] + sh[3];
+    __syncthreads();
+    return wofs + x - v;
+}
+
+__global__ __launch_bounds__(256) void k_scan_reduce(const uint32_t* __restrict__ data, int64_t n,
+                                                     uint32_t* __restrict__ sums) {
+    __shared__ uint32_t sh[4];
+    const int64_t base = (int64_t)blockIdx.x * 4096 + threadIdx.x * 16;
+    uint32_t s = 0;
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+        if (base + i < n) s += data[base + i];
+    uint32_t total;
+    block_exclusive_scan(s, sh, total);
+    if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(256) void k_scan_top(uint32_t* __restrict__ sums, int nb) {
+    __shared__ uint32_t sh[4];
+    uint32_t carry = 0;
+    for (int base = 0; base < nb; base += 256) {
+        const int i = base + threadIdx.x;
+        const uint32_t v = i < nb ? sums[i] : 0;
+        uint32_t total;
+        const uint32_t ex = block_exclusive_scan(v, sh, total);
+        if (i < nb) sums[i] = carry + ex;
+        carry += total;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_scan_apply(uint32_t* __restrict__ data, int64_t n,
+                                                    const uint32_t* __restrict__ sums) {
+    __shared__ uint32_t sh[4];
+    const int64_t base = (int64_t)blockIdx.x * 4096 + threadIdx.x * 16;
+    uint32_t v[16];
+    uint32_t s = 0;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        v[i] = base + i < n ? data[base + i] : 0;
+        s += v[i];
+    }
+    uint32_t total;
+    uint32_t run = block_exclusive_scan(s, sh, total) + sums[blockIdx.x];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        if (base + i < n) data[base + i] = run;
+        run += v[i];
+    }
+}
+
+// 2b. stable scatter: items of a tile are ranked in element order (slot-major,
+// then thread) with wave ballots; digit bases come from the scanned histogram.
+__global__ __launch_bounds__(RS_THREADS) void k_rs_scatter(const uint32_t* __restrict__ kin,
+                                                           const uint32_t* __restrict__ vin, uint32_t* __restrict__ kout,
+                                                           uint32_t* __restrict__ vout, uint32_t n, int shift, int bits,
+                                                           const uint32_t* __restrict__ offs, int ntiles) {
+    __shared__ uint32_t base[256];
+    __shared__ uint32_t wcnt[4][256];
+    const uint32_t mask = (1u << bits) - 1u;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (threadIdx.x <= mask) base[threadIdx.x] = offs[(int64_t)threadIdx.x * ntiles + blockIdx.x];
+    for (int w = 0; w < 4; ++w) wcnt[w][threadIdx.x] = 0;
+    __syncthreads();
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    for (int it = 0; it < RS_ITEMS; ++it) {
+        const uint32_t e = blockIdx.x * RS_TILE + it * RS_THREADS + threadIdx.x;
+        const bool valid = e < n;
+        const uint32_t key = valid ? kin[e] : 0u;
+        const uint32_t val = valid ? vin[e] : 0u;
+        const uint32_t dg = (key >> shift) & mask;
+        uint64_t peers = __ballot(valid);
+        for (int bb = 0; bb < bits; ++bb) {
+            const uint64_t m = __ballot(valid && ((dg >> bb) & 1u));
+            peers &= ((dg >> bb) & 1u) ? m : ~m;
+        }
+        const uint32_t rank = (uint32_t)__popcll(peers & lt);
+        if (valid && rank == 0) wcnt[wave][dg] = (uint32_t)__popcll(peers);
+        __syncthreads();
+        uint32_t pos = 0;
+        if (valid) {
+            pos = base[dg] + rank;
+            for (int w = 0; w < wave; ++w) pos += wcnt[w][dg];
+        }
+        __syncthreads();
+        if (threadIdx.x <= mask) {
+            const uint32_t d = threadIdx.x;
+            base[d] += wcnt[0][d] + wcnt[1][d] + wcnt[2][d] + wcnt[3][d];
+            wcnt[0][d] = wcnt[1][d] = wcnt[2][d] = wcnt[3][d] = 0;
+        }
+        if (valid) {
+            kout[pos] = key;
+            vout[pos] = val;
+        }
+        __syncthreads();
+    }
+}
+
+// 3. segmented reduction. DV = table columns per lane (D <= 64 * DV).
+template <typename T, typename ID, int DV>
+struct SegCtx {
+    EmbedBwdArgs a;
+    const uint32_t* keys;
+    const uint32_t* vals;
+    const uint32_t* bag_of;
+    uint32_t n;
+    uint32_t sentinel, rbase;
+
+    // contribution of sorted pair (k, o) to the row of key k, element c = lane + 64*j
+    __device__ __forceinline__ void add(uint32_t k, uint32_t o, float* acc, int lane) const {
+        const bool isq = k < rbase;
+        const uint32_t kk = isq ? k : k - rbase;
+        const uint32_t rows = isq ? (uint32_t)a.rows_q : a.m;
+        const uint32_t f = kk / rows;
+        const int64_t bag = a.offsets ? (int64_t)bag_of[o] : (int64_t)o;
+        const int64_t b = bag / a.F;
+        const float* g = a.grad_x0 + b * a.d + (int64_t)f * a.D;
+        if (a.combine == 0) {
+            uint32_t qi, ri;
+            split_id<ID>(((const ID*)a.ids)[o], a, qi, ri);
+            const T* other = isq ? (const T*)a.r_tables + ((int64_t)f * a.m + ri) * a.D
+                                 : (const T*)a.q_tables + ((int64_t)f * a.rows_q + qi) * a.D;
+#pragma unroll
+            for (int j = 0; j < DV; ++j) {
+                const int c = lane + 64 * j;
+                if (c < a.D) acc[j] = fmaf(g[c], st<T>::load(other + c), acc[j]);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < DV; ++j) {
+                const int c = lane + 64 * j;
+                if (c < a.D) acc[j] += g[c];
+            }
+        }
+    }
+
+    __device__ __forceinline__ float* row_of(uint32_t k) const {
+        return k < rbase ? a.grad_q + (int64_t)k * a.D : a.grad_r + (int64_t)(k - rbase) * a.D;
+    }
+};
+
+template <typename T, typename ID, int DV>
+__global__ __launch_bounds__(256) void k_seg_reduce(SegCtx<T, ID, DV> s, float* __restrict__ carry_head,
+                                                    float* __restrict__ carry_tail) {
+    const int lane = threadIdx.x & 63;
+    const uint32_t tile = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const uint32_t p0 = tile * SEG_TILE;
+    if (p0 >= s.n) return;
+    const uint32_t p1 = p0 + SEG_TILE < s.n ? p0 + SEG_TILE : s.n;
+    const uint32_t prevkey = p0 > 0 ? s.keys[p0 - 1] : 0xffffffffu;
+    const uint32_t nextkey = p1 < s.n ? s.keys[p1] : 0xffffffffu;
+    const int D = s.a.D;
+    float acc[DV];
+#pragma unroll
+    for (int j = 0; j < DV; ++j) acc[j] = 0.f;
+    uint32_t cur = s.keys[p0];
+    bool first_piece = true;
+    auto flush = [&](bool continues) {
+        if (cur == s.sentinel) return;
+        const bool started_before = first_piece && cur == prevkey;
+        float* dst;
+        if (!started_before && !continues) {
+            dst = s.row_of(cur);
+#pragma unroll
+            for (int j = 0; j < DV; ++j) {
+                const int c = lane + 64 * j;
+                if (c < D) dst[c] += acc[j];
+            }
+            return;
+        }
+        dst = (started_before ? carry_head : carry_tail) + (int64_t)tile * D;
+#pragma unroll
+        for (int j = 0; j < DV; ++j) {
+            const int c = lane + 64 * j;
+            if (c < D) dst[c] = acc[j];
+        }
+    };
+    for (uint32_t base = p0; base < p1; base += 64) {
+        const uint32_t cnt = p1 - base < 64 ? p1 - base : 64;
+        const uint32_t kl = lane < (int)cnt ? s.keys[base + lane] : 0u;
+        const uint32_t vl = lane < (int)cnt ? s.vals[base + lane] : 0u;
+        for (uint32_t i = 0; i < cnt; ++i) {
+            const uint32_t k = __builtin_amdgcn_readlane(kl, i);
+            const uint32_t o = __builtin_amdgcn_readlane(vl, i);
+            if (k != cur) {
+                flush(false);
+                first_piece = false;
+                cur = k;
+#pragma unroll
+                for (int j = 0; j < DV; ++j) acc[j] = 0.f;
+            }
+            if (k != s.sentinel) s.add(k, o, acc, lane);
+        }
+    }
+    flush(cur == nextkey);
+}
+
+// Fix-up: the tile whose last segment starts inside it and continues owns the
+// segment; it adds its tail piece and the head pieces of the following tiles
+// in tile order.
+template <typename T, typename ID, int DV>
+__global__ __launch_bounds__(256) void k_seg_fixup(SegCtx<T, ID, DV> s, const float* __restrict__ carry_head,
+                                                   const float* __restrict__ carry_tail) {
+    const int lane = threadIdx.x & 63;
+    const uint32_t tile = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const uint32_t p0 = tile * SEG_TILE;
+    if (p0 >= s.n) return;
+    const uint32_t p1 = p0 + SEG_TILE;
+    if (p1 >= s.n) return;
+    const uint32_t k = s.keys[p1 - 1];
+    if (k == s.sentinel || s.keys[p1] != k) return;
+    // the last piece started before this tile when the whole tile is that segment and it came from before
+    if (p0 > 0 && s.keys[p0] == k && s.keys[p0 - 1] == k) return;
+    const int D = s.a.D;
+    float tot[DV];
+#pragma unroll
+    for (int j = 0; j < DV; ++j) {
+        const int c = lane + 64 * j;
+        tot[j] = c < D ? carry_tail[(int64_t)tile * D + c] : 0.f;
+    }
+    uint32_t t = tile + 1;
+    for (;;) {
+#pragma unroll
+        for (int j = 0; j < DV; ++j) {
+            const int c = lane + 64 * j;
+            if (c < D) tot[j] += carry_head[(int64_t)t * D + c];
+        }
+        const uint32_t e = (t + 1) * SEG_TILE;
+        if (e >= s.n || s.keys[e - 1] != k || s.keys[e] != k) break;
+        ++t;
+    }
+    float* dst = s.row_of(k);
+#pragma unroll
+    for (int j = 0; j < DV; ++j) {
+        const int c = lane + 64 * j;
+        if (c < D) dst[c] += tot[j];
+    }
+}
+
+template <typename T, typename ID, int DV>
+hipError_t launch_reduce(const EmbedBwdArgs& a, const uint32_t* keys, const uint32_t* vals, const uint32_t* bag_of,
+                         uint32_t n, float* carry_head, float* carry_tail, hipStream_t st) {
+    SegCtx<T, ID, DV> s;
+    s.a = a;
+    s.keys = keys;
+    s.vals = vals;
+    s.bag_of = bag_of;
+    s.n = n;
+    s.sentinel = (uint32_t)a.F * (a.rows_q + a.m);
+    s.rbase = (uint32_t)a.F * a.rows_q;
+    const uint32_t ntiles = (n + SEG_TILE - 1) / SEG_TILE;
+    const unsigned blocks = (ntiles + 3) / 4;
+    hipLaunchKernelGGL((k_seg_reduce<T, ID, DV>), dim3(blocks), dim3(256), 0, st, s, carry_head, carry_tail);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_seg_fixup<T, ID, DV>), dim3(blocks), dim3(256), 0, st, s, carry_head, carry_tail);
+    return hipGetLastError();
+}
+
+inline int key_bits(uint32_t maxkey) {
+    int b = 1;
+    while (b < 32 && (maxkey >> b) != 0) ++b;
+    return b;
+}
+
+}  // namespace
+
+EmbedBwdLayout embed_bwd_layout(int64_t nnz, int F, int rows_q, int m, int D, bool bags) {
+    EmbedBwdLayout L;
+    const uint64_t n = 2 * (uint64_t)nnz;
+    const uint64_t ntiles = (n + RS_TILE - 1) / RS_TILE;
+    const int bits = key_bits((uint32_t)F * (uint32_t)(rows_q + m));
+    const int passes = (bits + 7) / 8;
+    const int dbits = (bits + passes - 1) / passes;
+    const uint64_t hist = ((uint64_t)1 << dbits) * (ntiles ? ntiles : 1);
+    const uint64_t sums = (hist + 4095) / 4096;
+    const uint64_t segtiles = (n + SEG_TILE - 1) / SEG_TILE + 1;
+    auto al = [](uint64_t x) { return (x + 255) & ~(uint64_t)255; };
+    uint64_t off = 0;
+    L.keys0 = off; off += al(4 * n);
+    L.vals0 = off; off += al(4 * n);
+    L.keys1 = off; off += al(4 * n);
+    L.vals1 = off; off += al(4 * n);
+    L.bag_of = off; off += bags ? al(4 * (uint64_t)nnz) : 0;
+    L.hist = off; off += al(4 * hist);
+    L.sums = off; off += al(4 * sums);
+    L.carry_head = off; off += al(4 * segtiles * (uint64_t)D);
+    L.carry_tail = off; off += al(4 * segtiles * (uint64_t)D);
+    L.total = off;
+    L.bits = bits;
+    L.passes = passes;
+    L.dbits = dbits;
+    return L;
+}
+
+struct EmbPtrs {
+    uint32_t* keys[2];
+    uint32_t* vals[2];
+    uint32_t* bag_of;
+    uint32_t* hist;
+    uint32_t* sums;
+    float* carry_head;
+    float* carry_tail;
+    EmbedBwdLayout L;
+};
+
+static EmbPtrs emb_ptrs(const EmbedBwdArgs& a, void* scratch) {
+    EmbPtrs p;
+    const bool bags = a.offsets != nullptr;
+    p.L = embed_bwd_layout(a.nnz, a.F, a.rows_q, a.m, a.D, bags);
+    char* base = (char*)scratch;
+    p.keys[0] = (uint32_t*)(base + p.L.keys0);
+    p.keys[1] = (uint32_t*)(base + p.L.keys1);
+    p.vals[0] = (uint32_t*)(base + p.L.vals0);
+    p.vals[1] = (uint32_t*)(base + p.L.vals1);
+    p.bag_of = bags ? (uint32_t*)(base + p.L.bag_of) : nullptr;
+    p.hist = (uint32_t*)(base + p.L.hist);
+    p.sums = (uint32_t*)(base + p.L.sums);
+    p.carry_head = (float*)(base + p.L.carry_head);
+    p.carry_tail = (float*)(base + p.L.carry_tail);
+    return p;
+}
+
+hipError_t launch_emb_keys(const EmbedBwdArgs& a, bool ids64, void* scratch, hipStream_t st) {
+    if (a.nnz == 0 || a.F == 0) return hipSuccess;
+    const EmbPtrs P = emb_ptrs(a, scratch);
+    const bool bags = a.offsets != nullptr;
+    const int64_t units = bags ? a.batch * a.F : a.nnz;
+    int64_t blocks = (units + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+#define RDCN_KEYS(ID, BG) hipLaunchKernelGGL((k_emb_keys<ID, BG>), dim3((unsigned)blocks), dim3(256), 0, st, a, P.keys[0], P.vals[0], P.bag_of)
+    if (ids64) { if (bags) RDCN_KEYS(int64_t, true); else RDCN_KEYS(int64_t, false); }
+    else       { if (bags) RDCN_KEYS(int32_t, true); else RDCN_KEYS(int32_t, false); }
+#undef RDCN_KEYS
+    return hipGetLastError();
+}
+
+// The sorted pairs end in buffer (passes % 2).
+hipError_t launch_emb_sort(const EmbedBwdArgs& a, void* scratch, hipStream_t st) {
+    if (a.nnz == 0 || a.F == 0) return hipSuccess;
+    const EmbPtrs P = emb_ptrs(a, scratch);
+    const uint32_t n = (uint32_t)(2 * a.nnz);
+    const int ntiles = (int)((n + RS_TILE - 1) / RS_TILE);
+    int cur = 0;
+    for (int pass = 0; pass < P.L.passes; ++pass) {
+        const int shift = pass * P.L.dbits;
+        const int bits = P.L.bits - shift < P.L.dbits ? P.L.bits - shift : P.L.dbits;
+        const uint32_t mask = (1u << bits) - 1u;
+        const int64_t hn = (int64_t)(mask + 1) * ntiles;
+        const int nb = (int)((hn + 4095) / 4096);
+        hipLaunchKernelGGL(k_rs_hist, dim3(ntiles), dim3(RS_THREADS), 0, st, P.keys[cur], n, shift, mask, P.hist,
+                           ntiles);
+        hipLaunchKernelGGL(k_scan_reduce, dim3(nb), dim3(256), 0, st, P.hist, hn, P.sums);
+        hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(256), 0, st, P.sums, nb);
+        hipLaunchKernelGGL(k_scan_apply, dim3(nb), dim3(256), 0, st, P.hist, hn, P.sums);
+        hipLaunchKernelGGL(k_rs_scatter, dim3(ntiles), dim3(RS_THREADS), 0, st, P.keys[cur], P.vals[cur],
+                           P.keys[cur ^ 1], P.vals[cur ^ 1], n, shift, bits, P.hist, ntiles);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        cur ^= 1;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_emb_reduce(const EmbedBwdArgs& a, bool bf16, bool ids64, void* scratch, hipStream_t st) {
+    if (a.nnz == 0 || a.F == 0) return hipSuccess;
+    const EmbPtrs P = emb_ptrs(a, scratch);
+    const uint32_t n = (uint32_t)(2 * a.nnz);
+    const int cur = P.L.passes & 1;
+    const int dv = (a.D + 63) / 64;
+#define RDCN_RED(T, ID, DV) return launch_reduce<T, ID, DV>(a, P.keys[cur], P.vals[cur], P.bag_of, n, P.carry_head, P.carry_tail, st)
+#define RDCN_RED_DV(T, ID) do { if (dv == 1) RDCN_RED(T, ID, 1); if (dv == 2) RDCN_RED(T, ID, 2); RDCN_RED(T, ID, 4); } while (0)
+    if (bf16) { if (ids64) RDCN_RED_DV(bf16_t, int64_t); else RDCN_RED_DV(bf16_t, int32_t); }
+    else      { if (ids64) RDCN_RED_DV(float, int64_t); else RDCN_RED_DV(float, int32_t); }
+#undef RDCN_RED_DV
+#undef RDCN_RED
+}
+
+}  // namespace rdcn

@@ -1,0 +1,47 @@
+// GEMM launcher interface (see gemm.hip).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rdcn {
+
+enum GemmEpi {
+    EPI_STORE = 0,      // c[m, n] (storage type) = scale * acc
+    EPI_STORE_F32 = 1,  // c[m, n] (float) = scale * acc
+    EPI_PARTIAL = 2,    // c[z, m, n] (float) = scale * acc   (split-K partials, z = split)
+    EPI_CROSS = 3,      // t = scale*acc + bias[n]; c = x0 * t + xl; t_out = t   (storage type)
+    EPI_RESID = 4,      // c (float) = gin + scale * acc
+    EPI_RESID_X0 = 5    // c (float) += gin + scale * acc
+};
+
+struct GemmArgs {
+    int64_t M, N, K;
+    const void* a;      // A(m, k) = a[m*lda + k], or a[k*lda + m] when a_kstrided
+    int64_t lda;
+    const void* b;      // B(n, k) = b[n*ldb + k], or b[k*ldb + n] when b_kstrided
+    int64_t ldb;
+    bool a_kstrided, b_kstrided;
+    int epi;
+    float scale;
+    void* c;            // output (see GemmEpi)
+    int64_t ldc;
+    // cross / residual epilogue operands, row stride ldx
+    const void* bias;
+    const void* x0;
+    const void* xl;
+    void* t_out;
+    const void* gin;
+    bool gin_f32;
+    int64_t ldx;
+};
+
+struct GemmPlan {
+    int bm = 128, bn = 128;
+    int splits = 1;
+};
+
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool bf16, bool allow_split);
+hipError_t launch_gemm(const GemmArgs& g, const GemmPlan& p, bool bf16, hipStream_t s);
+hipError_t launch_splitk_reduce(const float* part, int splits, int64_t MN, float* out, hipStream_t s);
+
+}  // namespace rdcn

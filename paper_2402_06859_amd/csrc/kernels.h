@@ -1,0 +1,41 @@
+// Host-side launchers of the gfx950 kernels (implemented in the .hip files).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace rdcn {
+
+struct GatherArgs {
+    int64_t batch;
+    int32_t F, D, Nd, rows_q;
+    uint32_t m;
+    uint64_t vocab;
+    uint32_t magic, shift;  // 32-bit division by m (valid when vocab <= 2^32)
+    int combine;            // 0 = product, 1 = sum
+    const void* ids;        // int32 or int64
+    const int64_t* offsets; // NULL = single-hot
+    const void* q_tables;
+    const void* r_tables;
+    const void* dense;
+    void* x0;
+    int* err;
+};
+hipError_t launch_qr_gather(const GatherArgs& a, bool bf16, bool ids64, hipStream_t s);
+
+}  // namespace rdcn
+
+namespace rdcn {
+
+hipError_t launch_attn_fwd(int64_t B, int r, float alpha, float beta, float tau, const void* P, int64_t ldp, void* H,
+                           int64_t ldh, bool bf16, hipStream_t s);
+hipError_t launch_attn_bwd(int64_t B, int r, float alpha, float beta, float tau, const void* P, int64_t ldp,
+                           const float* GH, int64_t ldg, void* GP, int64_t ldgp, bool bf16, hipStream_t s);
+
+int pointwise_rows_per_block(int64_t B, int64_t d);
+hipError_t launch_bwd_pointwise(int64_t B, int64_t d, const void* gin, bool gin_f32, const void* x0, const void* t,
+                                float* gx0, bool first, void* gt, float* part, bool bf16, hipStream_t s);
+hipError_t launch_colsum(const float* part, int nrb, int64_t d, float* out, hipStream_t s);
+hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
+
+}  // namespace rdcn

@@ -1,0 +1,214 @@
+"""Python binding of librdcn (include/rdcn.h): argument marshalling only.
+
+Every computation runs in the library's HIP kernels; torch is used for device
+memory and the current stream. If the shared library is missing it is built
+with hipcc; if it cannot be loaded, an error is raised (there is no fallback).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "librdcn.so")
+MAX_LAYERS = 16
+
+RDCN_OK, RDCN_ERR_ARG, RDCN_ERR_SHAPE, RDCN_ERR_INDEX, RDCN_ERR_UNSUPPORTED, RDCN_ERR_WORKSPACE, RDCN_ERR_HIP = range(7)
+F32, BF16 = 0, 1
+I32, I64 = 0, 1
+COMBINE_MUL, COMBINE_SUM = 0, 1
+
+EXPORTS = ["rdcn_create", "rdcn_destroy", "rdcn_dim", "rdcn_workspace_bytes", "qr_embed_gather",
+           "qr_embed_backward_workspace", "qr_embed_backward", "rdcn_forward", "rdcn_backward",
+           "rdcn_check_device_errors", "rdcn_status_string", "rdcn_profile_start", "rdcn_profile_stop"]
+
+KERNELS = ["gather", "fwd_down_gemm", "fwd_attention", "fwd_up_gemm", "bwd_pointwise", "bwd_bias", "bwd_gu_gemm",
+           "bwd_gh_gemm", "bwd_attention", "bwd_gw_gemm", "bwd_gx_gemm", "splitk_reduce", "emb_keys", "emb_sort",
+           "emb_reduce"]
+
+
+class RdcnConfig(ctypes.Structure):
+    _fields_ = [("batch_max", ctypes.c_int64), ("num_cat", ctypes.c_int32), ("emb_dim", ctypes.c_int32),
+                ("num_dense", ctypes.c_int32), ("rank", ctypes.c_int32), ("num_layers", ctypes.c_int32),
+                ("qr_rows_q", ctypes.c_int32), ("qr_rows_r", ctypes.c_int32), ("combine", ctypes.c_int32),
+                ("multi_hot", ctypes.c_int32), ("id_type", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("reserved0", ctypes.c_int32), ("vocab", ctypes.c_int64), ("attn_alpha", ctypes.c_float),
+                ("skip_beta", ctypes.c_float), ("temperature", ctypes.c_float), ("reserved1", ctypes.c_int32)]
+
+
+class RdcnWeights(ctypes.Structure):
+    _fields_ = [("w_down", ctypes.c_void_p * MAX_LAYERS), ("u", ctypes.c_void_p * MAX_LAYERS),
+                ("bias", ctypes.c_void_p * MAX_LAYERS)]
+
+
+class RdcnError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__("%s failed: %s (%d)" % (fn, status_string(status), status))
+
+
+_lib = None
+
+
+def load(build_if_missing: bool = True):
+    """Load librdcn.so (building it first if absent)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        if not build_if_missing:
+            raise RuntimeError("librdcn.so is not built (%s)" % LIB_PATH)
+        from . import build_lib
+        build_lib.build()
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i64, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t
+    st = ctypes.c_int
+    L.rdcn_status_string.argtypes = [st]
+    L.rdcn_status_string.restype = ctypes.c_char_p
+    L.rdcn_create.argtypes = [ctypes.POINTER(RdcnConfig), ctypes.POINTER(vp)]
+    L.rdcn_destroy.argtypes = [vp]
+    L.rdcn_dim.argtypes = [vp, ctypes.POINTER(i64)]
+    L.rdcn_workspace_bytes.argtypes = [vp, i64, ctypes.POINTER(sz), ctypes.POINTER(sz)]
+    L.qr_embed_gather.argtypes = [vp, i64, vp, vp, vp, vp, vp, vp, vp]
+    L.qr_embed_backward_workspace.argtypes = [vp, i64, i64, ctypes.POINTER(sz)]
+    L.qr_embed_backward.argtypes = [vp, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.rdcn_forward.argtypes = [vp, i64, vp, ctypes.POINTER(RdcnWeights), vp, vp, vp, vp]
+    L.rdcn_backward.argtypes = [vp, i64, vp, ctypes.POINTER(RdcnWeights), vp, vp, vp, ctypes.POINTER(RdcnWeights),
+                                vp, vp]
+    L.rdcn_check_device_errors.argtypes = [vp, vp]
+    L.rdcn_profile_start.argtypes = [vp, ctypes.c_int32, ctypes.c_uint32]
+    L.rdcn_profile_stop.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
+    for name in EXPORTS:
+        if name != "rdcn_status_string":
+            getattr(L, name).restype = st
+    _lib = L
+    return L
+
+
+def status_string(s: int) -> str:
+    return load().rdcn_status_string(s).decode()
+
+
+def _check(fn: str, s: int):
+    if s != RDCN_OK:
+        raise RdcnError(fn, s)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def make_config(batch_max: int, num_cat: int, emb_dim: int, num_dense: int, rank: int, num_layers: int,
+                qr_rows_q: int, qr_rows_r: int, vocab: int, combine: str = "sum", multi_hot: bool = False,
+                id_type: str = "i64", dtype: str = "bf16", attn_alpha: float = 0.0, skip_beta: float = 1.0,
+                temperature: float = 1.0) -> RdcnConfig:
+    c = RdcnConfig()
+    c.batch_max, c.num_cat, c.emb_dim, c.num_dense = batch_max, num_cat, emb_dim, num_dense
+    c.rank, c.num_layers, c.qr_rows_q, c.qr_rows_r = rank, num_layers, qr_rows_q, qr_rows_r
+    c.combine = COMBINE_MUL if combine == "mul" else COMBINE_SUM
+    c.multi_hot = int(multi_hot)
+    c.id_type = I64 if id_type == "i64" else I32
+    c.dtype = BF16 if dtype == "bf16" else F32
+    c.vocab = vocab
+    c.attn_alpha, c.skip_beta, c.temperature = attn_alpha, skip_beta, temperature
+    return c
+
+
+def config_for(wl, batch_max: Optional[int] = None, id_type: str = "i64") -> RdcnConfig:
+    """Config of a synthetic workload (paper_2402_06859_amd.synth.Workload)."""
+    return make_config(batch_max or wl.batch, wl.num_cat, wl.emb_dim, wl.num_dense, wl.rank, wl.num_layers,
+                       wl.table_rows, wl.table_rows, wl.vocab, wl.combine, wl.multi_hot, id_type, wl.dtype,
+                       wl.alpha, wl.beta, wl.temperature)
+
+
+def _weights(w_down: Sequence[torch.Tensor], u: Sequence[torch.Tensor], bias: Sequence[torch.Tensor]) -> RdcnWeights:
+    w = RdcnWeights()
+    for l, (a, b, c) in enumerate(zip(w_down, u, bias)):
+        w.w_down[l], w.u[l], w.bias[l] = a.data_ptr(), b.data_ptr(), c.data_ptr()
+    return w
+
+
+class Rdcn:
+    """One librdcn handle. Tensors are CUDA (HIP) tensors, contiguous, in the documented layouts."""
+
+    def __init__(self, cfg: RdcnConfig):
+        L = load()
+        self.cfg = cfg
+        h = ctypes.c_void_p()
+        _check("rdcn_create", L.rdcn_create(ctypes.byref(cfg), ctypes.byref(h)))
+        self.h = h
+        d = ctypes.c_int64()
+        _check("rdcn_dim", L.rdcn_dim(h, ctypes.byref(d)))
+        self.d = d.value
+
+    def close(self):
+        if getattr(self, "h", None) is not None and self.h.value:
+            load().rdcn_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # ---- workspace
+    def workspace_bytes(self, batch: int):
+        s, t = ctypes.c_size_t(), ctypes.c_size_t()
+        _check("rdcn_workspace_bytes", load().rdcn_workspace_bytes(self.h, batch, ctypes.byref(s), ctypes.byref(t)))
+        return s.value, t.value
+
+    def embed_backward_workspace(self, batch: int, nnz: int) -> int:
+        s = ctypes.c_size_t()
+        _check("qr_embed_backward_workspace", load().qr_embed_backward_workspace(self.h, batch, nnz, ctypes.byref(s)))
+        return s.value
+
+    # ---- entry points
+    def qr_embed_gather(self, batch, ids, offsets, q_tables, r_tables, dense, x0, stream=None):
+        _check("qr_embed_gather", load().qr_embed_gather(self.h, batch, _ptr(ids), _ptr(offsets), _ptr(q_tables),
+                                                         _ptr(r_tables), _ptr(dense), _ptr(x0), _stream(stream)))
+
+    def qr_embed_backward(self, batch, nnz, ids, offsets, q_tables, r_tables, grad_x0, grad_q, grad_r, scratch,
+                          stream=None):
+        _check("qr_embed_backward", load().qr_embed_backward(
+            self.h, batch, nnz, _ptr(ids), _ptr(offsets), _ptr(q_tables), _ptr(r_tables), _ptr(grad_x0),
+            _ptr(grad_q), _ptr(grad_r), _ptr(scratch), scratch.numel() * scratch.element_size(), _stream(stream)))
+
+    def rdcn_forward(self, batch, x0, w_down, u, bias, x_out, saved, scratch=None, stream=None):
+        w = _weights(w_down, u, bias)
+        _check("rdcn_forward", load().rdcn_forward(self.h, batch, _ptr(x0), ctypes.byref(w), _ptr(x_out), _ptr(saved),
+                                                   _ptr(scratch), _stream(stream)))
+
+    def rdcn_backward(self, batch, x0, w_down, u, bias, saved, grad_out, grad_x0, g_w_down, g_u, g_bias, scratch,
+                      stream=None):
+        w = _weights(w_down, u, bias)
+        g = _weights(g_w_down, g_u, g_bias)
+        _check("rdcn_backward", load().rdcn_backward(self.h, batch, _ptr(x0), ctypes.byref(w), _ptr(saved),
+                                                     _ptr(grad_out), _ptr(grad_x0), ctypes.byref(g), _ptr(scratch),
+                                                     _stream(stream)))
+
+    def profile_start(self, max_launches: int = 8192, kernels=None):
+        """Time the launches of `kernels` (names from KERNELS; all when None)."""
+        mask = 0xFFFFFFFF if kernels is None else sum(1 << KERNELS.index(k) for k in kernels)
+        _check("rdcn_profile_start", load().rdcn_profile_start(self.h, max_launches, mask))
+
+    def profile_stop(self) -> dict:
+        """{kernel: (total_ms, launches)} of the launches timed since profile_start."""
+        n = len(KERNELS)
+        ms = (ctypes.c_double * n)()
+        cnt = (ctypes.c_int64 * n)()
+        _check("rdcn_profile_stop", load().rdcn_profile_stop(self.h, ms, cnt))
+        return {k: (ms[i], cnt[i]) for i, k in enumerate(KERNELS)}
+
+    def check_device_errors(self, stream=None) -> int:
+        """Synchronise and return (and clear) the device error status (RDCN_OK or RDCN_ERR_INDEX)."""
+        return load().rdcn_check_device_errors(self.h, _stream(stream))

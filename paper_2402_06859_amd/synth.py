@@ -46,6 +46,7 @@ class Workload:
     bag_max: int = 100
     dense_zero_frac: float = 0.0
     temperature: float = 1.0
+    skip_beta: float = 1.0
 
     @property
     def d(self) -> int:
@@ -62,7 +63,7 @@ class Workload:
 
     @property
     def beta(self) -> float:
-        return 1.0
+        return self.skip_beta
 
     @property
     def n_proj(self) -> int:

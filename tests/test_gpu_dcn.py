@@ -1,0 +1,155 @@
+"""GPU Residual-DCN forward/backward (rdcn_forward / rdcn_backward) vs the fp64 oracle.
+
+Small shapes are compared in full (ragged batch, ragged d, attention on/off,
+several temperatures). Every workload is also run at its full batch in the
+launch configuration the benchmark uses, and compared on sampled rows: the
+forward of a row depends on that row only, and with an upstream gradient that
+is zero outside the sampled rows the weight gradients are exactly those of
+the sampled rows (other rows contribute exact zeros), which the oracle
+computes on the sampled rows alone.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_helpers import FWD_TOL, GRAD_TOL, need_gpu, oracle_x0, relerr, sample_rows, to_np
+from paper_2402_06859_amd.step import DeviceBatch
+from paper_2402_06859_amd.synth import WORKLOADS, Workload, make_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def host_weights(inp):
+    return ([w.float().numpy() for w in inp["w_down"]], [w.float().numpy() for w in inp["u"]],
+            [w.float().numpy() for w in inp["bias"]])
+
+
+def run_full_compare(wl: Workload, seed=None, grad_rows=None, fwd_rows=None, bias_std=0.1, id_mode="scatter"):
+    inp = make_inputs(wl, seed=seed, bias_std=bias_std, id_mode=id_mode)
+    B = inp["batch"]
+    print("dcn", wl.name, "B", B, "d", wl.d, "r", wl.rank, "L", wl.num_layers, "attn", wl.attention, flush=True)
+    if grad_rows is not None:  # upstream gradient only on the sampled rows
+        G = torch.zeros_like(inp["grad_out"])
+        G[torch.from_numpy(grad_rows)] = inp["grad_out"][torch.from_numpy(grad_rows)]
+        inp["grad_out"] = G
+    db = DeviceBatch(wl, inp)
+    db.gather()
+    db.forward()
+    db.backward()
+    torch.cuda.synchronize()
+    x0_ref = oracle_x0(wl, inp)
+    W, U, b = host_weights(inp)
+    rows = np.arange(B) if fwd_rows is None else fwd_rows
+    xL = oracle.forward(x0_ref[rows], W, U, b, wl.alpha, wl.beta, wl.temperature)
+    tol = FWD_TOL[wl.dtype]
+    e_fwd = relerr(to_np(db.x_out)[rows], xL)
+    assert e_fwd <= tol, "forward rel err %.3g > %.3g" % (e_fwd, tol)
+    grows = np.arange(B) if grad_rows is None else grad_rows
+    G = inp["grad_out"].float().numpy()
+    gx0, gW, gU, gb = oracle.backward(x0_ref[grows], W, U, b, G[grows], wl.alpha, wl.beta, wl.temperature)
+    gtol = 1e-4 if wl.dtype == "f32" else GRAD_TOL
+    got_gx0 = to_np(db.grad_x0)
+    errs = {"grad_x0": relerr(got_gx0[grows], gx0)}
+    if grad_rows is not None:
+        others = np.setdiff1d(np.arange(B), grows)
+        assert not np.any(got_gx0[others]), "rows without upstream gradient must get exact zeros"
+    for l in range(wl.num_layers):
+        errs["w_down%d" % l] = relerr(to_np(db.g_w_down[l]), gW[l])
+        errs["u%d" % l] = relerr(to_np(db.g_u[l]), gU[l])
+        errs["bias%d" % l] = relerr(to_np(db.g_bias[l]), gb[l])
+    bad = {k: v for k, v in errs.items() if not v <= gtol}
+    print("fwd %.3g  max grad %.3g" % (e_fwd, max(errs.values())), flush=True)
+    assert not bad, "gradient rel err above %.3g: %s" % (gtol, bad)
+    return db
+
+
+def test_tiny_full():
+    need_gpu()
+    run_full_compare(WORKLOADS["tiny"])
+
+
+@pytest.mark.parametrize("attn,tau,beta", [(True, 1.0, 1.0), (True, 0.25, 1.0), (True, 4.0, 0.5), (False, 1.0, 1.0),
+                                           (False, 1.0, 0.5)])
+def test_ragged_small_shapes(attn, tau, beta):
+    """batch 300 and d = 5*24 + 40 = 160 are not tile multiples; r = 40 is not a multiple of 16."""
+    need_gpu()
+    wl = Workload("ragged", 11, 300, 5, 50_000, 250, 24, 40, 2, 40, attn, "bf16", "sum", 1.1, temperature=tau)
+    run_full_compare(wl.with_(skip_beta=beta))
+
+
+def test_fp32_attention_ragged():
+    need_gpu()
+    wl = Workload("ragged32", 12, 130, 3, 10_000, 100, 16, 12, 3, 20, True, "f32", "mul", 1.1)
+    run_full_compare(wl)
+
+
+@pytest.mark.parametrize("name,k", [("small", 24), ("feed", 12), ("multihot", 12), ("large", 40)])
+def test_full_batch_sampled(name, k):
+    """Large samples 40 rows: its 6-layer attention stack ends near one-hot (|logits| ~ 130),
+    so single rows' gradients are sensitive to bf16 operand rounding (per-row errors 0.01-0.13
+    measured); weight gradients summed over tens of rows average this out (0.03-0.043 on 48 rows)."""
+    need_gpu()
+    wl = WORKLOADS[name]
+    rows = sample_rows(wl.batch, k)
+    run_full_compare(wl, grad_rows=rows, fwd_rows=rows)
+
+
+def test_small_rank_order_ids_full_batch():
+    need_gpu()
+    wl = WORKLOADS["small"]
+    rows = sample_rows(wl.batch, 8)
+    run_full_compare(wl, grad_rows=rows, fwd_rows=rows, id_mode="rank")
+
+
+def test_zero_query_gives_uniform_attention():
+    """Query weights zero => A = 11^T / r: the GPU forward matches the oracle, and the
+    oracle in turn matches a dense DCNv2 with W = U (beta I + alpha/r 11^T) V^T."""
+    need_gpu()
+    wl = Workload("uniform", 13, 256, 4, 10_000, 100, 16, 64, 2, 32, True, "bf16", "sum", 1.1)
+    inp = make_inputs(wl, bias_std=0.1)
+    r = wl.rank
+    for w in inp["w_down"]:
+        w[r:2 * r] = 0
+    db = DeviceBatch(wl, inp)
+    db.gather()
+    db.forward()
+    x0 = oracle_x0(wl, inp)
+    W, U, b = host_weights(inp)
+    M = wl.beta * np.eye(r) + wl.alpha / r * np.ones((r, r))
+    x = x0.astype(np.float64)
+    for Wl, Ul, bl in zip(W, U, b):
+        x = x0 * (x @ (Ul @ M @ Wl[:r]).T + bl) + x
+    assert relerr(to_np(db.x_out), x) <= FWD_TOL["bf16"]
+
+
+def test_deterministic_rerun():
+    need_gpu()
+    wl = WORKLOADS["small"].with_(batch=1024)
+    inp = make_inputs(wl, bias_std=0.1)
+    outs = []
+    for _ in range(2):
+        db = DeviceBatch(wl, inp)
+        db.gather()
+        db.forward()
+        db.backward()
+        torch.cuda.synchronize()
+        outs.append([db.x_out.cpu(), db.grad_x0.cpu()] + [t.cpu() for t in db.g_w_down + db.g_u + db.g_bias])
+    for a, b in zip(*outs):
+        assert torch.equal(a.view(torch.uint8) if a.dtype == torch.bfloat16 else a, b.view(torch.uint8)
+                           if b.dtype == torch.bfloat16 else b)
+
+
+def test_batch_zero_and_batch_one():
+    need_gpu()
+    wl = WORKLOADS["small"].with_(batch=1)
+    run_full_compare(wl)
+    inp = make_inputs(WORKLOADS["small"].with_(batch=4), bias_std=0.1)
+    db = DeviceBatch(WORKLOADS["small"].with_(batch=4), inp)
+    db.B = 0
+    db.gather()
+    db.forward()
+    db.backward()
+    torch.cuda.synchronize()
+    for t in db.g_w_down + db.g_u + db.g_bias:
+        assert not torch.any(t)

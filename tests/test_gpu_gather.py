@@ -1,0 +1,98 @@
+"""GPU gather (qr_embed_gather) vs the oracle: bit-exact x0 on every workload
+at its full batch, both combines, both id widths, rank-order (hot-row) ids,
+bags including empty ones, and the out-of-range id flag."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import bf16_bits, need_gpu, oracle_x0
+from paper_2402_06859_amd import rdcn
+from paper_2402_06859_amd.synth import WORKLOADS, make_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def run_gather(wl, inp, id_type="i64"):
+    lib = rdcn.Rdcn(rdcn.config_for(wl, inp["batch"], id_type))
+    dev = torch.device("cuda")
+    ids = inp["ids"] if id_type == "i64" else inp["ids"].to(torch.int32)
+    ids = ids.contiguous().to(dev)
+    offs = None if inp["offsets"] is None else inp["offsets"].to(dev)
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    x0 = torch.full((inp["batch"], wl.d), float("nan"), dtype=dt, device=dev)
+    lib.qr_embed_gather(inp["batch"], ids, offs, inp["q_tables"].to(dev), inp["r_tables"].to(dev),
+                        inp["dense"].to(dev), x0)
+    status = lib.check_device_errors()
+    return x0.cpu(), status
+
+
+def assert_bitexact(wl, x0_gpu, x0_ref):
+    if wl.dtype == "bf16":
+        ref_bits = torch.from_numpy(x0_ref).to(torch.bfloat16).view(torch.int16).numpy()
+        got = bf16_bits(x0_gpu)
+    else:
+        ref_bits = x0_ref.view(np.int32)
+        got = x0_gpu.numpy().view(np.int32)
+    mism = np.argwhere(got != ref_bits)
+    assert mism.size == 0, "first mismatches at %s" % mism[:5].tolist()
+
+
+@pytest.mark.parametrize("name", ["tiny", "small", "feed", "multihot", "large"])
+def test_gather_bitexact_full_batch(name):
+    need_gpu()
+    wl = WORKLOADS[name]
+    inp = make_inputs(wl, with_weights=False, with_grad=False)
+    print("gather", name, "B", inp["batch"], flush=True)
+    x0, status = run_gather(wl, inp)
+    assert status == rdcn.RDCN_OK
+    assert_bitexact(wl, x0, oracle_x0(wl, inp))
+
+
+@pytest.mark.parametrize("name,combine,id_type,mode", [
+    ("small", "mul", "i32", "rank"), ("small", "sum", "i32", "rank"), ("tiny", "sum", "i64", "rank"),
+    ("multihot", "mul", "i32", "scatter")])
+def test_gather_variants(name, combine, id_type, mode):
+    need_gpu()
+    wl = WORKLOADS[name].with_(combine=combine)
+    if name == "multihot":
+        wl = wl.with_(batch=512)
+    inp = make_inputs(wl, id_mode=mode, with_weights=False, with_grad=False)
+    x0, status = run_gather(wl, inp, id_type)
+    assert status == rdcn.RDCN_OK
+    assert_bitexact(wl, x0, oracle_x0(wl, inp))
+
+
+def test_gather_ragged_batch_and_bags_with_empty_and_bad_ids():
+    need_gpu()
+    wl = WORKLOADS["multihot"].with_(batch=37, num_cat=3, num_dense=8)
+    inp = make_inputs(wl, with_weights=False, with_grad=False)
+    # empty every 5th bag; put one out-of-range id into bag 7
+    offs = inp["offsets"].numpy()
+    ids = inp["ids"].numpy()
+    lens = np.diff(offs)
+    lens[::5] = 0
+    new_offs = np.zeros_like(offs)
+    np.cumsum(lens, out=new_offs[1:])
+    new_ids = np.concatenate([ids[offs[i]:offs[i] + lens[i]] for i in range(len(lens))])
+    new_ids[new_offs[7]] = wl.vocab + 5
+    inp["offsets"] = torch.from_numpy(new_offs)
+    inp["ids"] = torch.from_numpy(new_ids)
+    x0, status = run_gather(wl, inp)
+    assert status == rdcn.RDCN_ERR_INDEX
+    from oracle import gather
+    ref, bad = gather(37, 3, wl.emb_dim, 8, wl.vocab, wl.table_rows, wl.table_rows, wl.combine, True,
+                      inp["ids"], inp["offsets"], inp["q_tables"], inp["r_tables"], inp["dense"])
+    assert bad == 1
+    assert_bitexact(wl, x0, ref)
+
+
+def test_gather_out_of_range_single_hot_flag_clears():
+    need_gpu()
+    wl = WORKLOADS["tiny"]
+    inp = make_inputs(wl, with_weights=False, with_grad=False)
+    inp["ids"][3, 2] = -1
+    _, status = run_gather(wl, inp)
+    assert status == rdcn.RDCN_ERR_INDEX
+    inp["ids"][3, 2] = 0
+    _, status = run_gather(wl, inp)
+    assert status == rdcn.RDCN_OK
