@@ -81,7 +81,9 @@ typedef struct rdcn_config {
     int32_t multi_hot;    /* 0: one id per (sample, feature); 1: CSR bags, sum pooling */
     int32_t id_type;      /* rdcn_idtype of the id array */
     int32_t dtype;        /* rdcn_dtype of tables, dense, x0, activations and weights */
-    int32_t reserved0;    /* must be 0 */
+    int32_t split_activations; /* 0 or 1, bf16 only: keep x_l (l >= 1) and h as hi + lo bf16
+                                  pairs (about 16 significant bits) and run the down and
+                                  up projections as two bf16 MFMA passes over them */
     int64_t vocab;        /* V: valid ids are [0, V); requires qr_rows_q * qr_rows_r >= V */
     float attn_alpha;     /* alpha: weight of the attention path (0 = plain low-rank DCNv2) */
     float skip_beta;      /* beta: weight of the skip (value) path */
@@ -179,7 +181,11 @@ rdcn_status qr_embed_backward(rdcn_handle* h, int64_t batch, int64_t nnz, const 
  * needs and must stay untouched until then; `scratch` holds scratch_bytes.
  * With the attention term on, [v; q; k] are kept in float (they feed the
  * softmax, whose sharpness amplifies any rounding of q and k); h, t and x_l
- * are kept in the storage dtype.
+ * are kept in the storage dtype, or, with split_activations, x_l (l >= 1) and
+ * h as hi + lo bf16 pairs whose sum carries about 16 significant bits: the
+ * projections then see the activations at that precision (two MFMA passes
+ * against the exact bf16 weights). Deep stacks whose attention is close to
+ * one-hot need this to keep gradients within a few percent of exact.
  */
 rdcn_status rdcn_forward(rdcn_handle* h, int64_t batch, const void* x0, const rdcn_weights* w, void* x_out,
                          void* saved, void* scratch, void* stream);

@@ -16,7 +16,7 @@ struct rdcn_handle {
     rdcn_config cfg;
     int64_t d;
     int n;  // projections per layer (3 with the attention term, else 1)
-    bool bf16, ids64, attn;
+    bool bf16, ids64, attn, split;
     uint32_t magic, shift;
     int* err;  // device error word
     // per-kernel timing (rdcn_profile_start / rdcn_profile_stop)
@@ -79,20 +79,29 @@ void div_magic_host(uint32_t m, uint32_t& magic, uint32_t& shift) {
 
 size_t eb(const rdcn_handle* h) { return h->bf16 ? 2 : 4; }
 
+// Per layer: [v|q|k] (float with the attention term, else storage; plus a lo plane
+// of v when split), h and its lo plane (attention only), t, x_{l+1} and its lo plane
+// (l < L-1). Lo planes exist only with split_activations.
 struct SavedLayout {
-    size_t P[RDCN_MAX_LAYERS], H[RDCN_MAX_LAYERS], T[RDCN_MAX_LAYERS], X[RDCN_MAX_LAYERS];
+    size_t P[RDCN_MAX_LAYERS], P2[RDCN_MAX_LAYERS], H[RDCN_MAX_LAYERS], H2[RDCN_MAX_LAYERS], T[RDCN_MAX_LAYERS],
+        X[RDCN_MAX_LAYERS], X2[RDCN_MAX_LAYERS];
     size_t total;
 };
 
 SavedLayout saved_layout(const rdcn_handle* h, int64_t B) {
     SavedLayout s;
     const size_t e = eb(h), d = (size_t)h->d, r = (size_t)h->cfg.rank, n = (size_t)h->n;
+    const bool sp = h->split;
     size_t off = 0;
     for (int l = 0; l < h->cfg.num_layers; ++l) {
+        const bool more = l + 1 < h->cfg.num_layers;
         s.P[l] = off; off += al(B * n * r * (h->attn ? 4 : e));  // float [v|q|k] feeds the attention
+        s.P2[l] = off; off += (sp && !h->attn) ? al(B * r * e) : 0;
         s.H[l] = off; off += h->attn ? al(B * r * e) : 0;
+        s.H2[l] = off; off += (sp && h->attn) ? al(B * r * e) : 0;
         s.T[l] = off; off += al(B * d * e);
-        s.X[l] = off; off += (l + 1 < h->cfg.num_layers) ? al(B * d * e) : 0;  // x_{l+1}
+        s.X[l] = off; off += more ? al(B * d * e) : 0;  // x_{l+1}
+        s.X2[l] = off; off += (sp && more) ? al(B * d * e) : 0;
     }
     s.total = off;
     return s;
@@ -184,7 +193,8 @@ rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
         c.num_layers < 1 || c.num_layers > RDCN_MAX_LAYERS || c.qr_rows_q <= 0 || c.qr_rows_r <= 0 ||
         (c.combine != RDCN_COMBINE_MUL && c.combine != RDCN_COMBINE_SUM) || (c.multi_hot != 0 && c.multi_hot != 1) ||
         (c.id_type != RDCN_I32 && c.id_type != RDCN_I64) || (c.dtype != RDCN_F32 && c.dtype != RDCN_BF16) ||
-        c.vocab <= 0 || !(c.temperature > 0.0f) || c.reserved0 != 0 || c.reserved1 != 0 ||
+        c.vocab <= 0 || !(c.temperature > 0.0f) || (c.split_activations != 0 && c.split_activations != 1) ||
+        c.reserved1 != 0 ||
         c.attn_alpha != c.attn_alpha || c.skip_beta != c.skip_beta)
         return RDCN_ERR_ARG;
     if ((int64_t)c.qr_rows_q * (int64_t)c.qr_rows_r < c.vocab) return RDCN_ERR_SHAPE;
@@ -196,6 +206,7 @@ rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
     // sort keys and occurrence indices are 32-bit
     if ((int64_t)c.num_cat * ((int64_t)c.qr_rows_q + c.qr_rows_r) >= (int64_t)1 << 31) return RDCN_ERR_UNSUPPORTED;
     if (c.attn_alpha != 0.0f && c.rank > 2048) return RDCN_ERR_UNSUPPORTED;  // attention rows staged in LDS (<= 64 KiB)
+    if (c.split_activations && c.dtype != RDCN_BF16) return RDCN_ERR_UNSUPPORTED;  // float storage has nothing to split
     (void)n;
 
     rdcn_handle* h = new (std::nothrow) rdcn_handle();
@@ -206,6 +217,7 @@ rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
     h->n = h->attn ? 3 : 1;
     h->bf16 = c.dtype == RDCN_BF16;
     h->ids64 = c.id_type == RDCN_I64;
+    h->split = c.split_activations != 0;
     div_magic_host((uint32_t)c.qr_rows_r, h->magic, h->shift);
     if (hipMalloc((void**)&h->err, sizeof(int)) != hipSuccess) {
         (void)hipGetLastError();
@@ -352,43 +364,50 @@ rdcn_status rdcn_forward(rdcn_handle* h, int64_t batch, const void* x0, const rd
     const int64_t B = batch, d = h->d, r = c.rank, nr = (int64_t)h->n * r;
     const SavedLayout S = saved_layout(h, B);
     char* sv = (char*)saved;
-    const void* xcur = x0;
+    const void* xcur = x0;     // x_l (hi plane when split)
+    const void* xcur2 = nullptr;  // lo plane of x_l (x0 is exact in bf16: none)
     for (int l = 0; l < c.num_layers; ++l) {
+        const bool more = l + 1 < c.num_layers;
         void* P = sv + S.P[l];
         GemmArgs g{};
         g.M = B; g.N = nr; g.K = d;
-        g.a = xcur; g.lda = d;
+        g.a = xcur; g.a2 = xcur2; g.lda = d;
         g.b = w->w_down[l]; g.ldb = d;
         g.epi = h->attn ? EPI_STORE_F32 : EPI_STORE; g.scale = 1.0f;
         g.c = P; g.ldc = nr;
+        if (h->split && !h->attn) g.c2 = sv + S.P2[l];  // v as hi + lo for the up projection
         {
             ProfScope ps(h, RDCN_KERNEL_FWD_DOWN_GEMM, s);
             RDCN_TRY(launch_gemm(g, plan_gemm(B, nr, d, h->bf16, false), h->bf16, s));
         }
         const void* hsrc = P;
+        const void* hsrc2 = g.c2;
         int64_t ldh = nr;
         float scale = c.skip_beta;
         if (h->attn) {
             void* H = sv + S.H[l];
+            void* H2 = h->split ? (void*)(sv + S.H2[l]) : nullptr;
             ProfScope ps(h, RDCN_KERNEL_FWD_ATTENTION, s);
-            RDCN_TRY(launch_attn_fwd(B, (int)r, c.attn_alpha, c.skip_beta, c.temperature, P, nr, H, r, h->bf16, s));
+            RDCN_TRY(launch_attn_fwd(B, (int)r, c.attn_alpha, c.skip_beta, c.temperature, P, nr, H, H2, r, h->bf16, s));
             hsrc = H;
+            hsrc2 = H2;
             ldh = r;
             scale = 1.0f;
         }
-        void* xnext = (l + 1 < c.num_layers) ? (void*)(sv + S.X[l]) : x_out;
+        void* xnext = more ? (void*)(sv + S.X[l]) : x_out;
         GemmArgs u{};
         u.M = B; u.N = d; u.K = r;
-        u.a = hsrc; u.lda = ldh;
+        u.a = hsrc; u.a2 = hsrc2; u.lda = ldh;
         u.b = w->u[l]; u.ldb = r;
         u.epi = EPI_CROSS; u.scale = scale;
-        u.c = xnext; u.ldc = d;
-        u.bias = w->bias[l]; u.x0 = x0; u.xl = xcur; u.t_out = sv + S.T[l]; u.ldx = d;
+        u.c = xnext; u.c2 = (h->split && more) ? (void*)(sv + S.X2[l]) : nullptr; u.ldc = d;
+        u.bias = w->bias[l]; u.x0 = x0; u.xl = xcur; u.xl2 = xcur2; u.t_out = sv + S.T[l]; u.ldx = d;
         {
             ProfScope ps(h, RDCN_KERNEL_FWD_UP_GEMM, s);
             RDCN_TRY(launch_gemm(u, plan_gemm(B, d, r, h->bf16, false), h->bf16, s));
         }
         xcur = xnext;
+        xcur2 = u.c2;
     }
     return RDCN_OK;
 }

@@ -48,7 +48,7 @@ __device__ __forceinline__ void block_minmax(float lo, float hi, float* red, flo
 template <typename T>
 __global__ __launch_bounds__(256) void k_attn_fwd(int64_t B, int r, float alpha, float beta, float inv_tau,
                                                  const float* __restrict__ P, int64_t ldp, T* __restrict__ H,
-                                                 int64_t ldh) {
+                                                 T* __restrict__ H2, int64_t ldh) {
     extern __shared__ float smem[];
     float* sk = smem;          // [r]
     float* sv = smem + r;      // [r]
@@ -86,7 +86,9 @@ __global__ __launch_bounds__(256) void k_attn_fwd(int64_t B, int r, float alpha,
             s0 = fmaf(e0, sv[j], s0);
         }
         const float o = (s0 + s1) / (z0 + z1);
-        st<T>::store(H + b * ldh + i, beta * sv[i] + alpha * o);
+        const float hv = beta * sv[i] + alpha * o;
+        st<T>::store(H + b * ldh + i, hv);
+        if (H2) st<T>::store(H2 + b * ldh + i, hv - st<T>::load(H + b * ldh + i));  // lo part of a hi + lo pair
     }
 }
 
@@ -175,16 +177,16 @@ int attn_threads(int r) {
 }  // namespace
 
 hipError_t launch_attn_fwd(int64_t B, int r, float alpha, float beta, float tau, const void* P, int64_t ldp, void* H,
-                           int64_t ldh, bool bf16, hipStream_t s) {
+                           void* H2, int64_t ldh, bool bf16, hipStream_t s) {
     if (B == 0) return hipSuccess;
     const size_t lds = sizeof(float) * (2 * (size_t)r + 32);
     const int th = attn_threads(r);
     if (bf16)
         hipLaunchKernelGGL(k_attn_fwd<bf16_t>, dim3((unsigned)B), dim3(th), lds, s, B, r, alpha, beta, 1.0f / tau,
-                           (const float*)P, ldp, (bf16_t*)H, ldh);
+                           (const float*)P, ldp, (bf16_t*)H, (bf16_t*)H2, ldh);
     else
         hipLaunchKernelGGL(k_attn_fwd<float>, dim3((unsigned)B), dim3(th), lds, s, B, r, alpha, beta, 1.0f / tau,
-                           (const float*)P, ldp, (float*)H, ldh);
+                           (const float*)P, ldp, (float*)H, (float*)H2, ldh);
     return hipGetLastError();
 }
 

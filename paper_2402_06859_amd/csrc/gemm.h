@@ -6,10 +6,11 @@
 namespace rdcn {
 
 enum GemmEpi {
-    EPI_STORE = 0,      // c[m, n] (storage type) = scale * acc
+    EPI_STORE = 0,      // c[m, n] (storage type) = scale * acc; with c2: bf16 hi in c, lo in c2
     EPI_STORE_F32 = 1,  // c[m, n] (float) = scale * acc
     EPI_PARTIAL = 2,    // c[z, m, n] (float) = scale * acc   (split-K partials, z = split)
-    EPI_CROSS = 3,      // t = scale*acc + bias[n]; c = x0 * t + xl; t_out = t   (storage type)
+    EPI_CROSS = 3,      // t = scale*acc + bias[n]; c = x0 * t + xl; t_out = t   (storage type;
+                        // xl2 / c2: lo planes of a hi + lo bf16 input / output)
     EPI_RESID = 4,      // c (float) = gin + scale * acc
     EPI_RESID_X0 = 5    // c (float) += gin + scale * acc
 };
@@ -17,6 +18,7 @@ enum GemmEpi {
 struct GemmArgs {
     int64_t M, N, K;
     const void* a;      // A(m, k) = a[m*lda + k], or a[k*lda + m] when a_kstrided
+    const void* a2;     // optional second A plane: C = (A + A2) B^T as two passes over K (no split-K)
     int64_t lda;
     const void* b;      // B(n, k) = b[n*ldb + k], or b[k*ldb + n] when b_kstrided
     int64_t ldb;
@@ -24,11 +26,13 @@ struct GemmArgs {
     int epi;
     float scale;
     void* c;            // output (see GemmEpi)
+    void* c2;           // optional lo plane of a hi + lo bf16 output
     int64_t ldc;
     // cross / residual epilogue operands, row stride ldx
     const void* bias;
     const void* x0;
     const void* xl;
+    const void* xl2;    // optional lo plane of x_l
     void* t_out;
     const void* gin;
     bool gin_f32;
@@ -38,6 +42,7 @@ struct GemmArgs {
 struct GemmPlan {
     int bm = 128, bn = 128;
     int splits = 1;
+    int stages = 3;  // LDS ring depth (2 lets two workgroups share a CU)
 };
 
 GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool bf16, bool allow_split);

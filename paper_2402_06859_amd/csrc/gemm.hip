@@ -12,15 +12,13 @@
 //            gW    = gP^T x_l       both K-strided (split-K over the batch)
 //
 // Tiling: 256 threads = 4 waves in a 2 x 2 grid; a wave owns a (BM/2) x (BN/2)
-// block of 16 x 16 MFMA tiles (v_mfma_f32_16x16x32_bf16). Tiles of A and B are
-// staged in LDS as [row][k] with a 16-byte row pad, double-buffered, with one
-// barrier per K step of 64; the next K step's global loads are in flight
-// while the current one is multiplied. A K-strided operand is read as 8 x 8
-// blocks (8 k-rows of 16 bytes), transposed in registers and written to LDS
-// in the same [row][k] layout, so the MFMA feed is identical for every case.
-// The MFMA is issued with B as its first operand, so each lane ends up with
-// four consecutive output columns of one row: epilogue loads and stores are
-// 8- or 16-byte vectors along the rows of x0, x_l, t and g.
+// block of 16 x 16 MFMA tiles (v_mfma_f32_16x16x32_bf16). Each K step of 64 is
+// one stage of a 3-stage ring in LDS, filled by direct global-to-LDS loads two
+// steps ahead of the multiply; K-strided operands stay [k][m] in LDS and are
+// transposed on the way out by ds_read_b64_tr_b16, so no operand is ever
+// transposed in memory. The MFMA is issued with B as its first operand, so each
+// lane ends up with four consecutive output columns of one row: epilogue loads
+// and stores are 8- or 16-byte vectors along the rows of x0, x_l, t and g.
 #include "device_common.h"
 #include "gemm.h"
 
@@ -29,7 +27,6 @@ namespace rdcn {
 namespace {
 
 constexpr int BK = 64;
-constexpr int LDS_LD = BK + 8;  // bf16 elements per LDS row (16-byte pad)
 
 template <typename T>
 __device__ __forceinline__ void load4(const T* p, float* v);
@@ -55,6 +52,23 @@ __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, const float* v) {
     *(uint2*)p = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
 }
 
+// hi = bf16(v), lo = bf16(v - hi): the pair carries about 16 significant bits.
+// (float storage has no split; the lo plane is not used there.)
+template <typename T>
+__device__ __forceinline__ void store_split4(T* hi, T* lo, const float* v);
+template <>
+__device__ __forceinline__ void store_split4<float>(float* hi, float*, const float* v) {
+    store4<float>(hi, v);
+}
+template <>
+__device__ __forceinline__ void store_split4<bf16_t>(bf16_t* hi, bf16_t* lo, const float* v) {
+    const uint32_t h0 = f32_to_bf16(v[0]), h1 = f32_to_bf16(v[1]), h2 = f32_to_bf16(v[2]), h3 = f32_to_bf16(v[3]);
+    float r[4] = {v[0] - __uint_as_float(h0 << 16), v[1] - __uint_as_float(h1 << 16), v[2] - __uint_as_float(h2 << 16),
+                  v[3] - __uint_as_float(h3 << 16)};
+    *(uint2*)hi = make_uint2(h0 | (h1 << 16), h2 | (h3 << 16));
+    store4<bf16_t>(lo, r);
+}
+
 // Epilogue on four consecutive columns n .. n+3 of row m (n + 3 < N guaranteed).
 template <typename T>
 __device__ __forceinline__ void epilogue4(const GemmArgs& g, int64_t m, int64_t n, int z, float* v) {
@@ -62,7 +76,8 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& g, int64_t m, int64_t 
     for (int e = 0; e < 4; ++e) v[e] *= g.scale;
     switch (g.epi) {
         case EPI_STORE:
-            store4<T>((T*)g.c + m * g.ldc + n, v);
+            if (g.c2) store_split4((T*)g.c + m * g.ldc + n, (T*)g.c2 + m * g.ldc + n, v);
+            else store4<T>((T*)g.c + m * g.ldc + n, v);
             break;
         case EPI_STORE_F32:
             store4<float>((float*)g.c + m * g.ldc + n, v);
@@ -75,13 +90,20 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& g, int64_t m, int64_t 
             load4<T>((const T*)g.bias + n, b);
             load4<T>((const T*)g.x0 + m * g.ldx + n, x0);
             load4<T>((const T*)g.xl + m * g.ldx + n, xl);
+            if (g.xl2) {
+                float lo[4];
+                load4<T>((const T*)g.xl2 + m * g.ldx + n, lo);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) xl[e] += lo[e];
+            }
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 v[e] += b[e];
                 xn[e] = x0[e] * v[e] + xl[e];
             }
             store4<T>((T*)g.t_out + m * g.ldx + n, v);
-            store4<T>((T*)g.c + m * g.ldc + n, xn);
+            if (g.c2) store_split4((T*)g.c + m * g.ldc + n, (T*)g.c2 + m * g.ldc + n, xn);
+            else store4<T>((T*)g.c + m * g.ldc + n, xn);
             break;
         }
         case EPI_RESID:      // g_out = g_in + acc
@@ -104,75 +126,6 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& g, int64_t m, int64_t 
     }
 }
 
-// 8 x 8 bf16 block transpose in registers: in[r] holds row r (8 values along the
-// contiguous dimension), out[c] receives column c (8 values along k).
-__device__ __forceinline__ void transpose8x8(const u32x4_t* in, u32x4_t* out) {
-#pragma unroll
-    for (int c2 = 0; c2 < 4; ++c2) {
-        uint32_t lo[4], hi[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const uint32_t a = in[2 * j][c2], b = in[2 * j + 1][c2];
-            lo[j] = (a & 0xffffu) | (b << 16);
-            hi[j] = (a >> 16) | (b & 0xffff0000u);
-        }
-        out[2 * c2] = u32x4_t{lo[0], lo[1], lo[2], lo[3]};
-        out[2 * c2 + 1] = u32x4_t{hi[0], hi[1], hi[2], hi[3]};
-    }
-}
-
-// Operand tile loader: ROWS x BK bf16 tile starting at (row0, k0).
-template <int ROWS, bool KSTRIDED>
-struct TileLoader {
-    // K-contiguous: ROWS*BK/8 vectors of 16 bytes, spread over 256 threads.
-    // K-strided:    (ROWS/8)*(BK/8) 8x8 blocks; one block per thread.
-    static constexpr int NVEC = KSTRIDED ? 8 : (ROWS * BK / 8) / 256;
-    u32x4_t r[NVEC > 0 ? NVEC : 1];
-    bool active;
-
-    __device__ __forceinline__ void load(const bf16_t* base, int64_t ld, int64_t rows, int64_t K, int64_t row0,
-                                         int64_t k0, int tid) {
-        if (!KSTRIDED) {
-#pragma unroll
-            for (int i = 0; i < NVEC; ++i) {
-                const int v = tid + 256 * i;
-                const int row = v / (BK / 8), kv = v % (BK / 8);
-                const int64_t gr = row0 + row, gk = k0 + kv * 8;
-                if (gr < rows && gk < K) r[i] = *(const u32x4_t*)(base + gr * ld + gk);
-                else r[i] = u32x4_t{0, 0, 0, 0};
-            }
-        } else {
-            constexpr int NB = (ROWS / 8) * (BK / 8);
-            active = tid < NB;
-            const int kb = tid % (BK / 8), rb = tid / (BK / 8);
-            const int64_t gr = row0 + rb * 8;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int64_t gk = k0 + kb * 8 + i;
-                if (active && gr < rows && gk < K) r[i] = *(const u32x4_t*)(base + gk * ld + gr);
-                else r[i] = u32x4_t{0, 0, 0, 0};
-            }
-        }
-    }
-
-    __device__ __forceinline__ void store(bf16_t* lds, int tid) {
-        if (!KSTRIDED) {
-#pragma unroll
-            for (int i = 0; i < NVEC; ++i) {
-                const int v = tid + 256 * i;
-                const int row = v / (BK / 8), kv = v % (BK / 8);
-                *(u32x4_t*)(lds + row * LDS_LD + kv * 8) = r[i];
-            }
-        } else if (active) {
-            const int kb = tid % (BK / 8), rb = tid / (BK / 8);
-            u32x4_t t[8];
-            transpose8x8(r, t);
-#pragma unroll
-            for (int c = 0; c < 8; ++c) *(u32x4_t*)(lds + (rb * 8 + c) * LDS_LD + kb * 8) = t[c];
-        }
-    }
-};
-
 __device__ __forceinline__ int xcd_remap(int id, int n) {
     // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
     // contiguous range of tiles so neighbouring tiles share its L2.
@@ -180,87 +133,257 @@ __device__ __forceinline__ int xcd_remap(int id, int n) {
     return (id % 8) * (n / 8) + id / 8;
 }
 
-template <int BM, int BN, bool AKS, bool BKS, typename T>
-__global__ __launch_bounds__(256, 2) void k_gemm_mfma(GemmArgs g) {
-    constexpr int TM = BM / 32, TN = BN / 32;  // 16x16 tiles per wave
-    __shared__ __attribute__((aligned(16))) bf16_t sA[2][BM * LDS_LD];
-    __shared__ __attribute__((aligned(16))) bf16_t sB[2][BN * LDS_LD];
+// ---------------------------------------------------------------------------
+// LDS layouts (one stage = one BK = 64 slice of A and of B):
+//  K-contiguous operand, ROWS x 64 bf16: row r holds 8 chunks of 16 bytes; the
+//    chunk of logical k-block kc sits in slot kc ^ ((r >> 1) & 7). Two rows share
+//    a 256-byte bank window, so 16 consecutive rows reading the same kc hit 16
+//    distinct 16-byte bank groups (ds_read_b128 without conflicts).
+//  K-strided operand, 64 k-rows x ROWS bf16 (rows contiguous along m): a k-row
+//    holds ROWS/16 chunks of 32 bytes (16 m values); chunk c sits in slot
+//    c ^ h(k). MFMA fragments are read with ds_read_b64_tr_b16, which transposes
+//    within each 16-lane group: lane (g, j) reads the 4 m values 4(j%4)..+3 of
+//    k-row 8g + j/4 (+4 for the second read) and receives the 8 k values of its
+//    own m. h(k) spreads the 16 k-rows of one read over all bank groups.
+// Loads go straight from global memory into LDS (global_load_lds, 16 bytes per
+// lane, lane l writes bytes 16 l .. 16 l + 15 of a 1 KiB block), so the global
+// address of each lane is chosen to land in the swizzled position.
+// ---------------------------------------------------------------------------
+#define LDS_AS __attribute__((address_space(3)))
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    const int tiles_n = (int)((g.N + BN - 1) / BN);
-    const int ntiles = (int)(((g.M + BM - 1) / BM) * tiles_n);
-    const int t = xcd_remap(blockIdx.x, ntiles);
-    const int64_t m0 = (int64_t)(t / tiles_n) * BM, n0 = (int64_t)(t % tiles_n) * BN;
+// 16-byte direct global-to-LDS load: lane l's 16 bytes land at LDS byte address
+// m0 + 16 l. Issued through asm so that the compiler adds no waits of its own:
+// every consumer below waits explicitly (wait_vmcnt + s_barrier) for the stage
+// it reads. M0 needs one wait state after it is written.
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(gptr), "s"(lds_base)
+                 : "memory");
+}
 
-    // split-K range
-    const int z = blockIdx.z;
-    const int64_t kchunk = ((g.K + (int64_t)gridDim.z * BK - 1) / ((int64_t)gridDim.z * BK)) * BK;
-    const int64_t kbeg = z * kchunk;
-    const int64_t kend = kbeg + kchunk < g.K ? kbeg + kchunk : g.K;
+__device__ __forceinline__ uint32_t lds_addr(const bf16_t* p) { return (uint32_t)(uintptr_t)((LDS_AS const char*)p); }
 
-    f32x4_t acc[TM][TN];
+template <int ROWS>
+__device__ __forceinline__ int kstr_swz(int k) {
+    // ROWS = 128: 8 slots of 32 B per k-row; ROWS = 64: 4 slots, two k-rows per 256 B window
+    return ROWS == 128 ? (((k & 3) << 1) | ((k >> 3) & 1)) : ((((k >> 1) & 1) << 1) | ((k >> 3) & 1));
+}
+
+// Issue this thread's direct-to-LDS loads of one stage for one operand.
+template <int ROWS, bool KS>
+__device__ __forceinline__ void stage_load(const bf16_t* __restrict__ base, int64_t ld, int64_t rows, int64_t row0,
+                                           int64_t k0, int64_t kend, bf16_t* lds, int wave, int lane) {
+    constexpr int NI = ROWS / 32;  // wave-instructions per thread (ROWS * 8 chunks / 64 lanes / 4 waves)
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-    const bf16_t* A = (const bf16_t*)g.a;
-    const bf16_t* B = (const bf16_t*)g.b;
-    TileLoader<BM, AKS> la;
-    TileLoader<BN, BKS> lb;
-
-    if (kbeg < kend) {
-        la.load(A, g.lda, g.M, kend, m0, kbeg, tid);
-        lb.load(B, g.ldb, g.N, kend, n0, kbeg, tid);
-        la.store(sA[0], tid);
-        lb.store(sB[0], tid);
-    }
-    __syncthreads();
-
-    int cur = 0;
-    for (int64_t k0 = kbeg; k0 < kend; k0 += BK) {
-        const bool more = k0 + BK < kend;
-        if (more) {
-            la.load(A, g.lda, g.M, kend, m0, k0 + BK, tid);
-            lb.load(B, g.ldb, g.N, kend, n0, k0 + BK, tid);
+    for (int j = 0; j < NI; ++j) {
+        const int blk = wave * NI + j;  // 1 KiB block index within the stage
+        int64_t gr, gk;
+        if (!KS) {
+            const int r = blk * 8 + (lane >> 3);
+            const int kc = (lane & 7) ^ ((r >> 1) & 7);
+            gr = row0 + r;
+            gk = k0 + kc * 8;
+            if (gr >= rows) gr = rows - 1;
+            if (gk >= kend) gk = kend - 8;
+            dma16(base + gr * ld + gk, lds_addr(lds) + (uint32_t)__builtin_amdgcn_readfirstlane(blk) * 1024u);
+        } else {
+            constexpr int RPB = ROWS == 128 ? 4 : 8;  // k-rows per 1 KiB block
+            constexpr int QPR = 64 / RPB;             // 16-byte pieces per k-row
+            const int kr = blk * RPB + lane / QPR;
+            const int q = lane % QPR;
+            const int c = (q >> 1) ^ kstr_swz<ROWS>(kr);
+            gk = k0 + kr;
+            gr = row0 + c * 16 + (q & 1) * 8;
+            if (gk >= kend) gk = kend - 1;
+            if (gr >= rows) gr = rows - 8;
+            dma16(base + gk * ld + gr, lds_addr(lds) + (uint32_t)__builtin_amdgcn_readfirstlane(blk) * 1024u);
         }
-        const bf16_t* a_s = sA[cur];
-        const bf16_t* b_s = sB[cur];
+    }
+}
+
+// Zero the k positions >= kvalid of one stage (tail tile of a K range).
+template <int ROWS, bool KS>
+__device__ __forceinline__ void stage_zero_tail(bf16_t* lds, int kvalid, int tid) {
+    if (!KS) {
+        const int nch = 8 - kvalid / 8;  // chunks per row to clear
+        for (int e = tid; e < ROWS * nch; e += 256) {
+            const int r = e / nch, kc = kvalid / 8 + e % nch;
+            *(u32x4_t*)(lds + r * 64 + ((kc ^ ((r >> 1) & 7)) * 8)) = u32x4_t{0, 0, 0, 0};
+        }
+    } else {
+        const int n = (64 - kvalid) * ROWS / 8;  // 16-byte pieces in the k-rows to clear
+        for (int e = tid; e < n; e += 256)
+            *(u32x4_t*)(lds + kvalid * ROWS + e * 8) = u32x4_t{0, 0, 0, 0};
+    }
+}
+
+// MFMA fragment (16 rows x 32 k) of an operand tile at row offset rt, k offset ks.
+template <int ROWS, bool KS>
+__device__ __forceinline__ bf16x8_t load_frag(const bf16_t* lds, int rt, int ks, int lane) {
+    const int i = lane & 15, g = lane >> 4;
+    if (!KS) {
+        const int r = rt + i;
+        const int kc = ks / 8 + g;
+        return __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(lds + r * 64 + ((kc ^ ((r >> 1) & 7)) * 8)));
+    } else {
+        const int c = rt / 16;
+        s16x4_t lo, hi;
+        {
+            const int kr = ks + 8 * g + (i >> 2);
+            const int off = kr * ROWS + ((c ^ kstr_swz<ROWS>(kr)) * 16) + (i & 3) * 4;
+            lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4_t*)(lds + off));
+        }
+        {
+            const int kr = ks + 8 * g + 4 + (i >> 2);
+            const int off = kr * ROWS + ((c ^ kstr_swz<ROWS>(kr)) * 16) + (i & 3) * 4;
+            hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4_t*)(lds + off));
+        }
+        typedef short s16x8_t __attribute__((ext_vector_type(8)));
+        const s16x8_t v = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        return __builtin_bit_cast(bf16x8_t, v);
+    }
+}
+
+__device__ __forceinline__ void wait_vmcnt(int n) {
+    // s_waitcnt with vmcnt = n (n <= 63), expcnt and lgkmcnt left at their maxima
+    switch (n) {
+        case 0: __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (15 << 8)); break;
+        case 2: __builtin_amdgcn_s_waitcnt(2 | (7 << 4) | (15 << 8)); break;
+        case 4: __builtin_amdgcn_s_waitcnt(4 | (7 << 4) | (15 << 8)); break;
+        case 6: __builtin_amdgcn_s_waitcnt(6 | (7 << 4) | (15 << 8)); break;
+        case 8: __builtin_amdgcn_s_waitcnt(8 | (7 << 4) | (15 << 8)); break;
+        case 12: __builtin_amdgcn_s_waitcnt(12 | (7 << 4) | (15 << 8)); break;
+        case 16: __builtin_amdgcn_s_waitcnt(0 | (1 << 14) | (7 << 4) | (15 << 8)); break;
+        default: __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (15 << 8)); break;
+    }
+}
+
+__device__ __forceinline__ void wait_lgkm0() {
+    // s_waitcnt lgkmcnt(0), vmcnt and expcnt left at their maxima
+    __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (0 << 8));
+}
+
+template <int BM, int BN, bool AKS, bool BKS, int ST>
+struct Pipe {
+    static constexpr int TM = BM / 32, TN = BN / 32;  // 16x16 MFMA tiles per wave
+    static constexpr int LOADS = BM / 32 + BN / 32;   // load instructions per thread per stage
+    static constexpr int STAGE_ELEMS = (BM + BN) * BK;
+
+    struct Ctx {
+        const GemmArgs* g;
+        int nk;          // K tiles per A plane
+        int ntot;        // nk * planes
+        int64_t kbeg, kend, m0, n0;
+        int tid;
+    };
+
+    // Loads of tile `t` (clamped to the last tile; planes follow each other) into `buf`.
+    __device__ __forceinline__ static void issue(const Ctx& c, int t, bf16_t* buf) {
+        const int lane = c.tid & 63, wave = c.tid >> 6;
+        if (t > c.ntot - 1) t = c.ntot - 1;
+        const int plane = t >= c.nk;
+        const int64_t k0 = c.kbeg + (int64_t)(t - plane * c.nk) * BK;
+        const bf16_t* a = (const bf16_t*)(plane ? c.g->a2 : c.g->a);
+        stage_load<BM, AKS>(a, c.g->lda, c.g->M, c.m0, k0, c.kend, buf, wave, lane);
+        stage_load<BN, BKS>((const bf16_t*)c.g->b, c.g->ldb, c.g->N, c.n0, k0, c.kend, buf + BM * BK, wave, lane);
+    }
+
+    // One step on tile kt held in `cur`; prefetch tile kt + ST - 1 into `nxt`.
+    // Every step issues the same number of loads (past the last tile they re-read
+    // it), so "all but the newest ST - 2 stages" is a fixed count on every path.
+    __device__ __forceinline__ static void step(const Ctx& c, bf16_t* cur, bf16_t* nxt, int kt,
+                                                f32x4_t (&acc)[TM][TN]) {
+        const int lane = c.tid & 63, wave = c.tid >> 6, wm = wave >> 1, wn = wave & 1;
+        wait_vmcnt(LOADS * (ST - 2));
+        __builtin_amdgcn_s_barrier();
+        issue(c, kt + ST - 1, nxt);
+        const int kk = kt >= c.nk ? kt - c.nk : kt;
+        const int64_t kv = c.kend - (c.kbeg + (int64_t)kk * BK);
+        if (kv < BK) {  // tail tile: clear k positions past the range
+            stage_zero_tail<BM, AKS>(cur, (int)kv, c.tid);
+            stage_zero_tail<BN, BKS>(cur + BM * BK, (int)kv, c.tid);
+            wait_lgkm0();
+            __builtin_amdgcn_s_barrier();
+        }
 #pragma unroll
         for (int ks = 0; ks < BK; ks += 32) {
             bf16x8_t af[TM], bfr[TN];
-            const int kk = ks + (lane >> 4) * 8;
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-                af[i] = __builtin_bit_cast(bf16x8_t,
-                                           *(const u32x4_t*)(a_s + (wm * (BM / 2) + i * 16 + (lane & 15)) * LDS_LD + kk));
+            for (int i = 0; i < TM; ++i) af[i] = load_frag<BM, AKS>(cur, wm * (BM / 2) + i * 16, ks, lane);
 #pragma unroll
-            for (int j = 0; j < TN; ++j)
-                bfr[j] = __builtin_bit_cast(bf16x8_t,
-                                            *(const u32x4_t*)(b_s + (wn * (BN / 2) + j * 16 + (lane & 15)) * LDS_LD + kk));
+            for (int j = 0; j < TN; ++j) bfr[j] = load_frag<BN, BKS>(cur + BM * BK, wn * (BN / 2) + j * 16, ks, lane);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
         }
-        if (more) {
-            la.store(sA[cur ^ 1], tid);
-            lb.store(sB[cur ^ 1], tid);
+    }
+};
+
+// C = A B^T with an ST-stage direct-to-LDS pipeline (see layouts above).
+template <int BM, int BN, bool AKS, bool BKS, int ST, typename T>
+__global__ __launch_bounds__(256, ST == 2 ? 2 : 1) void k_gemm_mfma(GemmArgs g) {
+    using P = Pipe<BM, BN, AKS, BKS, ST>;
+    __shared__ __attribute__((aligned(1024))) bf16_t lds0[P::STAGE_ELEMS];
+    __shared__ __attribute__((aligned(1024))) bf16_t lds1[P::STAGE_ELEMS];
+    __shared__ __attribute__((aligned(1024))) bf16_t lds2[ST == 3 ? P::STAGE_ELEMS : 8];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int tiles_n = (int)((g.N + BN - 1) / BN);
+    const int ntiles = (int)(((g.M + BM - 1) / BM) * tiles_n);
+    const int t = xcd_remap(blockIdx.x, ntiles);
+
+    typename P::Ctx c;
+    c.g = &g;
+    c.tid = tid;
+    c.m0 = (int64_t)(t / tiles_n) * BM;
+    c.n0 = (int64_t)(t % tiles_n) * BN;
+    const int z = blockIdx.z;
+    const int64_t kchunk = ((g.K + (int64_t)gridDim.z * BK - 1) / ((int64_t)gridDim.z * BK)) * BK;
+    c.kbeg = z * kchunk;
+    c.kend = c.kbeg + kchunk < g.K ? c.kbeg + kchunk : g.K;
+    c.nk = c.kbeg < c.kend ? (int)((c.kend - c.kbeg + BK - 1) / BK) : 0;
+    c.ntot = c.nk * (g.a2 ? 2 : 1);
+
+    f32x4_t acc[P::TM][P::TN];
+#pragma unroll
+    for (int i = 0; i < P::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < P::TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    if (c.ntot > 0) {
+        P::issue(c, 0, lds0);
+        if (ST == 3) {
+            P::issue(c, 1, lds1);
+            for (int kt = 0; kt < c.ntot; kt += 3) {
+                P::step(c, lds0, lds2, kt, acc);
+                if (kt + 1 >= c.ntot) break;
+                P::step(c, lds1, lds0, kt + 1, acc);
+                if (kt + 2 >= c.ntot) break;
+                P::step(c, lds2, lds1, kt + 2, acc);
+            }
+        } else {
+            for (int kt = 0; kt < c.ntot; kt += 2) {
+                P::step(c, lds0, lds1, kt, acc);
+                if (kt + 1 >= c.ntot) break;
+                P::step(c, lds1, lds0, kt + 1, acc);
+            }
         }
-        __syncthreads();
-        cur ^= 1;
+        wait_vmcnt(0);  // the trailing re-read loads land before the workgroup ends
     }
 
     // lane holds C[m = tile_m + (lane & 15)][n = tile_n + 4 * (lane >> 4) + e]
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
-        const int64_t m = m0 + wm * (BM / 2) + i * 16 + (lane & 15);
+    for (int i = 0; i < P::TM; ++i) {
+        const int64_t m = c.m0 + wm * (BM / 2) + i * 16 + (lane & 15);
         if (m >= g.M) continue;
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int64_t n = n0 + wn * (BN / 2) + j * 16 + 4 * (lane >> 4);
+        for (int j = 0; j < P::TN; ++j) {
+            const int64_t n = c.n0 + wn * (BN / 2) + j * 16 + 4 * (lane >> 4);
             if (n >= g.N) continue;
             float v[4] = {acc[i][j].x, acc[i][j].y, acc[i][j].z, acc[i][j].w};
             epilogue4<T>(g, m, n, z, v);
@@ -330,11 +453,11 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float* part, int sp
     }
 }
 
-template <int BM, int BN, typename T>
+template <int BM, int BN, int ST, typename T>
 hipError_t launch_tile(const GemmArgs& g, int splits, hipStream_t s) {
     const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
     dim3 grid((unsigned)tiles, 1, (unsigned)splits);
-#define RDCN_GEMM(AK, BKS) hipLaunchKernelGGL((k_gemm_mfma<BM, BN, AK, BKS, T>), grid, dim3(256), 0, s, g)
+#define RDCN_GEMM(AK, BKS) hipLaunchKernelGGL((k_gemm_mfma<BM, BN, AK, BKS, ST, T>), grid, dim3(256), 0, s, g)
     if (g.a_kstrided) {
         if (g.b_kstrided) RDCN_GEMM(true, true); else RDCN_GEMM(true, false);
     } else {
@@ -365,6 +488,10 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool bf16, bool allow_split)
         if (s < 1) s = 1;
         p.splits = (int)s;
     }
+    // 128 x 128 tiles: two LDS stages (64 KiB) let two workgroups share a CU, which
+    // overlaps one tile's epilogue with another's main loop; long K ranges keep
+    // the deeper three-stage ring.
+    p.stages = (p.bm == 128 && K / p.splits <= 1024) ? 2 : 3;
     return p;
 }
 
@@ -375,8 +502,12 @@ hipError_t launch_gemm(const GemmArgs& g, const GemmPlan& p, bool bf16, hipStrea
         hipLaunchKernelGGL(k_gemm_f32, dim3((unsigned)tiles, 1, (unsigned)p.splits), dim3(256), 0, s, g);
         return hipGetLastError();
     }
-    if (p.bm == 128) return launch_tile<128, 128, bf16_t>(g, p.splits, s);
-    return launch_tile<64, 64, bf16_t>(g, p.splits, s);
+    if (p.bm == 128) {
+        if (p.stages == 2) return launch_tile<128, 128, 2, bf16_t>(g, p.splits, s);
+        return launch_tile<128, 128, 3, bf16_t>(g, p.splits, s);
+    }
+    if (p.stages == 2) return launch_tile<64, 64, 2, bf16_t>(g, p.splits, s);
+    return launch_tile<64, 64, 3, bf16_t>(g, p.splits, s);
 }
 
 hipError_t launch_splitk_reduce(const float* part, int splits, int64_t MN, float* out, hipStream_t s) {

@@ -28,7 +28,7 @@ hipError_t launch_qr_gather(const GatherArgs& a, bool bf16, bool ids64, hipStrea
 namespace rdcn {
 
 hipError_t launch_attn_fwd(int64_t B, int r, float alpha, float beta, float tau, const void* P, int64_t ldp, void* H,
-                           int64_t ldh, bool bf16, hipStream_t s);
+                           void* H2, int64_t ldh, bool bf16, hipStream_t s);
 hipError_t launch_attn_bwd(int64_t B, int r, float alpha, float beta, float tau, const void* P, int64_t ldp,
                            const float* GH, int64_t ldg, void* GP, int64_t ldgp, bool bf16, hipStream_t s);
 

@@ -47,6 +47,7 @@ class Workload:
     dense_zero_frac: float = 0.0
     temperature: float = 1.0
     skip_beta: float = 1.0
+    split_activations: bool = False  # activations as hi + lo bf16 pairs (deep attention stacks)
 
     @property
     def d(self) -> int:
@@ -80,7 +81,8 @@ WORKLOADS: Dict[str, Workload] = {
                      dense_zero_frac=0.05),
     "multihot": Workload("multihot", 3, 8192, 64, 10_000_000, 3163, 64, 256, 3, 512, False, "bf16", "sum", 1.1,
                          multi_hot=True),
-    "large": Workload("large", 4, 32768, 200, 20_000_000, 4473, 48, 1024, 6, 1024, True, "bf16", "sum", 1.1),
+    "large": Workload("large", 4, 32768, 200, 20_000_000, 4473, 48, 1024, 6, 1024, True, "bf16", "sum", 1.1,
+                      split_activations=True),
 }
 
 

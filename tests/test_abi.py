@@ -60,7 +60,7 @@ def good():
     ("emb_dim", 0, rdcn.RDCN_ERR_ARG), ("num_cat", -1, rdcn.RDCN_ERR_ARG), ("batch_max", -1, rdcn.RDCN_ERR_ARG),
     ("combine", 7, rdcn.RDCN_ERR_ARG), ("dtype", 3, rdcn.RDCN_ERR_ARG), ("id_type", 2, rdcn.RDCN_ERR_ARG),
     ("temperature", 0.0, rdcn.RDCN_ERR_ARG), ("temperature", -1.0, rdcn.RDCN_ERR_ARG), ("vocab", 0, rdcn.RDCN_ERR_ARG),
-    ("reserved0", 1, rdcn.RDCN_ERR_ARG), ("multi_hot", 2, rdcn.RDCN_ERR_ARG),
+    ("split_activations", 2, rdcn.RDCN_ERR_ARG), ("multi_hot", 2, rdcn.RDCN_ERR_ARG),
     ("vocab", 626, rdcn.RDCN_ERR_SHAPE),                      # 25 * 25 < 626: ids would not fit the tables
     ("emb_dim", 12, rdcn.RDCN_ERR_UNSUPPORTED), ("num_dense", 4, rdcn.RDCN_ERR_UNSUPPORTED),
     ("rank", 12, rdcn.RDCN_ERR_UNSUPPORTED), ("emb_dim", 264, rdcn.RDCN_ERR_UNSUPPORTED),
@@ -71,6 +71,13 @@ def test_create_rejects_bad_config_before_hip(field, value, expect):
     h = ctypes.c_void_p()
     assert rdcn.load().rdcn_create(ctypes.byref(c), ctypes.byref(h)) == expect
     assert not h.value
+
+
+def test_split_needs_bf16():
+    c = good()
+    c.dtype, c.emb_dim, c.num_dense, c.rank, c.split_activations = rdcn.F32, 16, 32, 8, 1
+    h = ctypes.c_void_p()
+    assert rdcn.load().rdcn_create(ctypes.byref(c), ctypes.byref(h)) == rdcn.RDCN_ERR_UNSUPPORTED
 
 
 def test_create_null_arguments():
