@@ -112,8 +112,8 @@ typedef struct rdcn_handle rdcn_handle;
  * of range, RDCN_ERR_SHAPE if qr_rows_q * qr_rows_r < vocab, and
  * RDCN_ERR_UNSUPPORTED when a bf16 model has emb_dim, num_dense or rank not a
  * multiple of 8 (fp32: multiple of 4), which the vector loads need, when
- * emb_dim > 256, when the attention term is on with rank > 2048 (one sample's
- * attention rows are staged in 64 KiB of LDS), or when F * (qr_rows_q + m)
+ * emb_dim > 256, when the attention term is on with rank > 1024 (one sample's
+ * attention operands are staged in 64 KiB of LDS), or when F * (qr_rows_q + m)
  * does not fit the 31-bit sort keys of the embedding backward.
  */
 rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out);

@@ -205,7 +205,7 @@ rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
     const int n = c.attn_alpha != 0.0f ? 3 : 1;
     // sort keys and occurrence indices are 32-bit
     if ((int64_t)c.num_cat * ((int64_t)c.qr_rows_q + c.qr_rows_r) >= (int64_t)1 << 31) return RDCN_ERR_UNSUPPORTED;
-    if (c.attn_alpha != 0.0f && c.rank > 2048) return RDCN_ERR_UNSUPPORTED;  // attention rows staged in LDS (<= 64 KiB)
+    if (c.attn_alpha != 0.0f && c.rank > 1024) return RDCN_ERR_UNSUPPORTED;  // one sample's attention staged in LDS (<= 64 KiB)
     if (c.split_activations && c.dtype != RDCN_BF16) return RDCN_ERR_UNSUPPORTED;  // float storage has nothing to split
     (void)n;
 
@@ -330,6 +330,10 @@ rdcn_status qr_embed_backward(rdcn_handle* h, int64_t batch, int64_t nnz, const 
     a.grad_x0 = grad_x0;
     a.grad_q = grad_q_tables;
     a.grad_r = grad_r_tables;
+    div_magic_host((uint32_t)c.num_cat, a.magic_f, a.shift_f);
+    div_magic_host((uint32_t)c.qr_rows_q, a.magic_q, a.shift_q);
+    a.magic_m = h->magic;
+    a.shift_m = h->shift;
     hipStream_t s = (hipStream_t)stream;
     {
         ProfScope ps(h, RDCN_KERNEL_EMB_KEYS, s);

@@ -18,6 +18,8 @@ struct EmbedBwdArgs {
     const float* grad_x0;
     float* grad_q;
     float* grad_r;
+    // invariant-divisor multipliers (device_common.h DivMagic) for F, rows_q and m
+    uint32_t magic_f, shift_f, magic_q, shift_q, magic_m, shift_m;
 };
 
 struct EmbedBwdLayout {

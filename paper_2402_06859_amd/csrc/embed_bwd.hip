@@ -35,10 +35,15 @@ template <typename ID>
 __device__ __forceinline__ bool split_id(ID raw, const EmbedBwdArgs& a, uint32_t& qi, uint32_t& ri) {
     const int64_t id = (int64_t)raw;
     if (id < 0 || (uint64_t)id >= a.vocab) return false;
-    const uint64_t q = (uint64_t)id / a.m;
-    qi = (uint32_t)q;
-    ri = (uint32_t)((uint64_t)id - q * a.m);
-    return qi < (uint32_t)a.rows_q;
+    if (a.vocab <= 0x100000000ull) {
+        qi = div_magic((uint32_t)id, DivMagic{a.magic_m, a.shift_m, a.m});
+        ri = (uint32_t)id - qi * a.m;
+    } else {
+        const uint64_t q = (uint64_t)id / a.m;
+        qi = (uint32_t)q;
+        ri = (uint32_t)((uint64_t)id - q * a.m);
+    }
+    return qi < (uint32_t)a.rows_q && ri < a.m;
 }
 
 // 1. keys. Single-hot: thread per occurrence o = b*F + f. Bags: thread per bag.
@@ -70,10 +75,13 @@ __global__ __launch_bounds__(256) void k_emb_keys(EmbedBwdArgs a, uint32_t* __re
 }
 
 // 2a. per-tile digit histogram, stored digit-major: hist[digit * ntiles + tile]
+constexpr int RS_MAX_BITS = 10;  // digits of up to 10 bits (1024 buckets)
+constexpr int RS_BUCKETS = 1 << RS_MAX_BITS;
+
 __global__ __launch_bounds__(RS_THREADS) void k_rs_hist(const uint32_t* __restrict__ keys, uint32_t n, int shift,
                                                         uint32_t mask, uint32_t* __restrict__ hist, int ntiles) {
-    __shared__ uint32_t h[256];
-    h[threadIdx.x] = 0;
+    __shared__ uint32_t h[RS_BUCKETS];
+    for (int d = threadIdx.x; d < RS_BUCKETS; d += RS_THREADS) h[d] = 0;
     __syncthreads();
     const uint32_t base = blockIdx.x * RS_TILE;
 #pragma unroll
@@ -82,11 +90,10 @@ __global__ __launch_bounds__(RS_THREADS) void k_rs_hist(const uint32_t* __restri
         if (e < n) atomicAdd(&h[(keys[e] >> shift) & mask], 1u);
     }
     __syncthreads();
-    if (threadIdx.x <= mask) hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
+    for (uint32_t d = threadIdx.x; d <= mask; d += RS_THREADS) hist[(int64_t)d * ntiles + blockIdx.x] = h[d];
 }
 
-// Exclusive scan of n words in three kernels: block sums, scan of the block
-// sums (one workgroup), apply. Blocks of 4096 words.
+// Exclusive scan of one value per thread over a 256-thread workgroup.
 __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* sh, uint32_t& total) {
     // 256 threads: wave inclusive scan, then wave totals.
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -105,50 +112,29 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
     return wofs + x - v;
 }
 
-__global__ __launch_bounds__(256) void k_scan_reduce(const uint32_t* __restrict__ data, int64_t n,
-                                                     uint32_t* __restrict__ sums) {
-    __shared__ uint32_t sh[4];
-    const int64_t base = (int64_t)blockIdx.x * 4096 + threadIdx.x * 16;
-    uint32_t s = 0;
-#pragma unroll
-    for (int i = 0; i < 16; ++i)
-        if (base + i < n) s += data[base + i];
-    uint32_t total;
-    block_exclusive_scan(s, sh, total);
-    if (threadIdx.x == 0) sums[blockIdx.x] = total;
-}
-
-__global__ __launch_bounds__(256) void k_scan_top(uint32_t* __restrict__ sums, int nb) {
-    __shared__ uint32_t sh[4];
-    uint32_t carry = 0;
-    for (int base = 0; base < nb; base += 256) {
-        const int i = base + threadIdx.x;
-        const uint32_t v = i < nb ? sums[i] : 0;
-        uint32_t total;
-        const uint32_t ex = block_exclusive_scan(v, sh, total);
-        if (i < nb) sums[i] = carry + ex;
-        carry += total;
+// Per digit d (thread per digit): exclusive prefix over tiles of hist[d][*] in
+// place, digit total into tot[d].
+__global__ __launch_bounds__(256) void k_digit_prefix(uint32_t* __restrict__ hist, int ndig, int ntiles,
+                                                      uint32_t* __restrict__ tot) {
+    const int d = blockIdx.x * blockDim.x + threadIdx.x;
+    if (d >= ndig) return;
+    uint32_t* row = hist + (int64_t)d * ntiles;
+    uint32_t run = 0;
+    int t = 0;
+    for (; t + 4 <= ntiles; t += 4) {
+        const uint32_t v0 = row[t], v1 = row[t + 1], v2 = row[t + 2], v3 = row[t + 3];
+        row[t] = run;
+        row[t + 1] = run + v0;
+        row[t + 2] = run + v0 + v1;
+        row[t + 3] = run + v0 + v1 + v2;
+        run += v0 + v1 + v2 + v3;
     }
-}
-
-__global__ __launch_bounds__(256) void k_scan_apply(uint32_t* __restrict__ data, int64_t n,
-                                                    const uint32_t* __restrict__ sums) {
-    __shared__ uint32_t sh[4];
-    const int64_t base = (int64_t)blockIdx.x * 4096 + threadIdx.x * 16;
-    uint32_t v[16];
-    uint32_t s = 0;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-        v[i] = base + i < n ? data[base + i] : 0;
-        s += v[i];
+    for (; t < ntiles; ++t) {
+        const uint32_t v = row[t];
+        row[t] = run;
+        run += v;
     }
-    uint32_t total;
-    uint32_t run = block_exclusive_scan(s, sh, total) + sums[blockIdx.x];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-        if (base + i < n) data[base + i] = run;
-        run += v[i];
-    }
+    tot[d] = run;
 }
 
 // 2b. stable scatter: items of a tile are ranked in element order (slot-major,
@@ -156,13 +142,34 @@ __global__ __launch_bounds__(256) void k_scan_apply(uint32_t* __restrict__ data,
 __global__ __launch_bounds__(RS_THREADS) void k_rs_scatter(const uint32_t* __restrict__ kin,
                                                            const uint32_t* __restrict__ vin, uint32_t* __restrict__ kout,
                                                            uint32_t* __restrict__ vout, uint32_t n, int shift, int bits,
-                                                           const uint32_t* __restrict__ offs, int ntiles) {
-    __shared__ uint32_t base[256];
-    __shared__ uint32_t wcnt[4][256];
+                                                           const uint32_t* __restrict__ offs, int ntiles,
+                                                           const uint32_t* __restrict__ tot) {
+    __shared__ uint32_t base[RS_BUCKETS];
+    __shared__ uint32_t wcnt[4][RS_BUCKETS];
+    __shared__ uint32_t sh[4];
     const uint32_t mask = (1u << bits) - 1u;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    if (threadIdx.x <= mask) base[threadIdx.x] = offs[(int64_t)threadIdx.x * ntiles + blockIdx.x];
-    for (int w = 0; w < 4; ++w) wcnt[w][threadIdx.x] = 0;
+    // digit bases: exclusive scan of the digit totals (4 consecutive digits per thread)
+    {
+        uint32_t v[4], s4 = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t d = threadIdx.x * 4 + e;
+            v[e] = d <= mask ? tot[d] : 0u;
+            s4 += v[e];
+        }
+        uint32_t total;
+        uint32_t run = block_exclusive_scan(s4, sh, total);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t d = threadIdx.x * 4 + e;
+            if (d <= mask) {
+                base[d] = run + offs[(int64_t)d * ntiles + blockIdx.x];
+                wcnt[0][d] = wcnt[1][d] = wcnt[2][d] = wcnt[3][d] = 0;
+            }
+            run += v[e];
+        }
+    }
     __syncthreads();
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     for (int it = 0; it < RS_ITEMS; ++it) {
@@ -185,8 +192,7 @@ __global__ __launch_bounds__(RS_THREADS) void k_rs_scatter(const uint32_t* __res
             for (int w = 0; w < wave; ++w) pos += wcnt[w][dg];
         }
         __syncthreads();
-        if (threadIdx.x <= mask) {
-            const uint32_t d = threadIdx.x;
+        for (uint32_t d = threadIdx.x; d <= mask; d += RS_THREADS) {
             base[d] += wcnt[0][d] + wcnt[1][d] + wcnt[2][d] + wcnt[3][d];
             wcnt[0][d] = wcnt[1][d] = wcnt[2][d] = wcnt[3][d] = 0;
         }
@@ -208,14 +214,14 @@ struct SegCtx {
     uint32_t n;
     uint32_t sentinel, rbase;
 
-    // contribution of sorted pair (k, o) to the row of key k, element c = lane + 64*j
-    __device__ __forceinline__ void add(uint32_t k, uint32_t o, float* acc, int lane) const {
+    // contribution of sorted pair (k, o) to the row of key k, elements c = lane + 64*j
+    __device__ __forceinline__ void contrib(uint32_t k, uint32_t o, float* out, int lane) const {
         const bool isq = k < rbase;
         const uint32_t kk = isq ? k : k - rbase;
-        const uint32_t rows = isq ? (uint32_t)a.rows_q : a.m;
-        const uint32_t f = kk / rows;
-        const int64_t bag = a.offsets ? (int64_t)bag_of[o] : (int64_t)o;
-        const int64_t b = bag / a.F;
+        const uint32_t f = isq ? div_magic(kk, DivMagic{a.magic_q, a.shift_q, (uint32_t)a.rows_q})
+                               : div_magic(kk, DivMagic{a.magic_m, a.shift_m, a.m});
+        const uint32_t bag = a.offsets ? bag_of[o] : o;
+        const int64_t b = div_magic(bag, DivMagic{a.magic_f, a.shift_f, (uint32_t)a.F});
         const float* g = a.grad_x0 + b * a.d + (int64_t)f * a.D;
         if (a.combine == 0) {
             uint32_t qi, ri;
@@ -225,13 +231,13 @@ struct SegCtx {
 #pragma unroll
             for (int j = 0; j < DV; ++j) {
                 const int c = lane + 64 * j;
-                if (c < a.D) acc[j] = fmaf(g[c], st<T>::load(other + c), acc[j]);
+                out[j] = c < a.D ? g[c] * st<T>::load(other + c) : 0.f;
             }
         } else {
 #pragma unroll
             for (int j = 0; j < DV; ++j) {
                 const int c = lane + 64 * j;
-                if (c < a.D) acc[j] += g[c];
+                out[j] = c < a.D ? g[c] : 0.f;
             }
         }
     }
@@ -277,21 +283,34 @@ __global__ __launch_bounds__(256) void k_seg_reduce(SegCtx<T, ID, DV> s, float* 
             if (c < D) dst[c] = acc[j];
         }
     };
+    constexpr int U = 8;  // entries whose gradient slices are in flight together
     for (uint32_t base = p0; base < p1; base += 64) {
         const uint32_t cnt = p1 - base < 64 ? p1 - base : 64;
-        const uint32_t kl = lane < (int)cnt ? s.keys[base + lane] : 0u;
+        const uint32_t kl = lane < (int)cnt ? s.keys[base + lane] : s.sentinel;
         const uint32_t vl = lane < (int)cnt ? s.vals[base + lane] : 0u;
-        for (uint32_t i = 0; i < cnt; ++i) {
-            const uint32_t k = __builtin_amdgcn_readlane(kl, i);
-            const uint32_t o = __builtin_amdgcn_readlane(vl, i);
-            if (k != cur) {
-                flush(false);
-                first_piece = false;
-                cur = k;
+        for (uint32_t i = 0; i < cnt; i += U) {
+            float cv[U][DV];
 #pragma unroll
-                for (int j = 0; j < DV; ++j) acc[j] = 0.f;
+            for (int u = 0; u < U; ++u) {  // loads first ...
+                const uint32_t k = __builtin_amdgcn_readlane(kl, i + u);
+                const uint32_t o = __builtin_amdgcn_readlane(vl, i + u);
+                if (i + u < cnt && k != s.sentinel) s.contrib(k, o, cv[u], lane);
             }
-            if (k != s.sentinel) s.add(k, o, acc, lane);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {  // ... then the in-order sums
+                if (i + u >= cnt) break;
+                const uint32_t k = __builtin_amdgcn_readlane(kl, i + u);
+                if (k != cur) {
+                    flush(false);
+                    first_piece = false;
+                    cur = k;
+#pragma unroll
+                    for (int j = 0; j < DV; ++j) acc[j] = 0.f;
+                }
+                if (k != s.sentinel)
+#pragma unroll
+                    for (int j = 0; j < DV; ++j) acc[j] += cv[u][j];
+            }
         }
     }
     flush(cur == nextkey);
@@ -372,10 +391,10 @@ EmbedBwdLayout embed_bwd_layout(int64_t nnz, int F, int rows_q, int m, int D, bo
     const uint64_t n = 2 * (uint64_t)nnz;
     const uint64_t ntiles = (n + RS_TILE - 1) / RS_TILE;
     const int bits = key_bits((uint32_t)F * (uint32_t)(rows_q + m));
-    const int passes = (bits + 7) / 8;
+    const int passes = (bits + RS_MAX_BITS - 1) / RS_MAX_BITS;
     const int dbits = (bits + passes - 1) / passes;
     const uint64_t hist = ((uint64_t)1 << dbits) * (ntiles ? ntiles : 1);
-    const uint64_t sums = (hist + 4095) / 4096;
+    const uint64_t sums = RS_BUCKETS;  // digit totals of one pass
     const uint64_t segtiles = (n + SEG_TILE - 1) / SEG_TILE + 1;
     auto al = [](uint64_t x) { return (x + 255) & ~(uint64_t)255; };
     uint64_t off = 0;
@@ -448,15 +467,12 @@ hipError_t launch_emb_sort(const EmbedBwdArgs& a, void* scratch, hipStream_t st)
         const int shift = pass * P.L.dbits;
         const int bits = P.L.bits - shift < P.L.dbits ? P.L.bits - shift : P.L.dbits;
         const uint32_t mask = (1u << bits) - 1u;
-        const int64_t hn = (int64_t)(mask + 1) * ntiles;
-        const int nb = (int)((hn + 4095) / 4096);
         hipLaunchKernelGGL(k_rs_hist, dim3(ntiles), dim3(RS_THREADS), 0, st, P.keys[cur], n, shift, mask, P.hist,
                            ntiles);
-        hipLaunchKernelGGL(k_scan_reduce, dim3(nb), dim3(256), 0, st, P.hist, hn, P.sums);
-        hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(256), 0, st, P.sums, nb);
-        hipLaunchKernelGGL(k_scan_apply, dim3(nb), dim3(256), 0, st, P.hist, hn, P.sums);
+        const int ndig = (int)(mask + 1);
+        hipLaunchKernelGGL(k_digit_prefix, dim3((ndig + 255) / 256), dim3(256), 0, st, P.hist, ndig, ntiles, P.sums);
         hipLaunchKernelGGL(k_rs_scatter, dim3(ntiles), dim3(RS_THREADS), 0, st, P.keys[cur], P.vals[cur],
-                           P.keys[cur ^ 1], P.vals[cur ^ 1], n, shift, bits, P.hist, ntiles);
+                           P.keys[cur ^ 1], P.vals[cur ^ 1], n, shift, bits, P.hist, ntiles, P.sums);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         cur ^= 1;
