@@ -126,10 +126,95 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& g, int64_t m, int64_t 
     }
 }
 
+template <typename T>
+__device__ __forceinline__ void load8(const T* p, float* v) {
+    load4<T>(p, v);
+    load4<T>(p + 4, v + 4);
+}
+template <>
+__device__ __forceinline__ void load8<bf16_t>(const bf16_t* p, float* v) {
+    const u32x4_t w = *(const u32x4_t*)p;
+    st<bf16_t>::unpack(w, v);
+}
+template <typename T>
+__device__ __forceinline__ void store8(T* p, const float* v) {
+    store4<T>(p, v);
+    store4<T>(p + 4, v + 4);
+}
+template <>
+__device__ __forceinline__ void store8<bf16_t>(bf16_t* p, const float* v) {
+    *(u32x4_t*)p = st<bf16_t>::pack(v);
+}
+template <typename T>
+__device__ __forceinline__ void store_split8(T* hi, T* lo, const float* v) {
+    store_split4<T>(hi, lo, v);
+    store_split4<T>(hi + 4, lo + 4, v + 4);
+}
+
+// Epilogue on eight consecutive columns n .. n+7 of row m (n + 7 < N guaranteed):
+// 16-byte accesses along the rows of x0, x_l, t and g.
+template <typename T>
+__device__ __forceinline__ void epilogue8(const GemmArgs& g, int64_t m, int64_t n, int z, float* v) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] *= g.scale;
+    switch (g.epi) {
+        case EPI_STORE:
+            if (g.c2) store_split8((T*)g.c + m * g.ldc + n, (T*)g.c2 + m * g.ldc + n, v);
+            else store8<T>((T*)g.c + m * g.ldc + n, v);
+            break;
+        case EPI_STORE_F32:
+            store8<float>((float*)g.c + m * g.ldc + n, v);
+            break;
+        case EPI_PARTIAL:
+            store8<float>((float*)g.c + ((int64_t)z * g.M + m) * g.ldc + n, v);
+            break;
+        case EPI_CROSS: {
+            float b[8], x0[8], xl[8], xn[8];
+            load8<T>((const T*)g.bias + n, b);
+            load8<T>((const T*)g.x0 + m * g.ldx + n, x0);
+            load8<T>((const T*)g.xl + m * g.ldx + n, xl);
+            if (g.xl2) {
+                float lo[8];
+                load8<T>((const T*)g.xl2 + m * g.ldx + n, lo);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) xl[e] += lo[e];
+            }
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                v[e] += b[e];
+                xn[e] = x0[e] * v[e] + xl[e];
+            }
+            store8<T>((T*)g.t_out + m * g.ldx + n, v);
+            if (g.c2) store_split8((T*)g.c + m * g.ldc + n, (T*)g.c2 + m * g.ldc + n, xn);
+            else store8<T>((T*)g.c + m * g.ldc + n, xn);
+            break;
+        }
+        case EPI_RESID:
+        case EPI_RESID_X0: {
+            float gi[8];
+            if (g.gin_f32) load8<float>((const float*)g.gin + m * g.ldx + n, gi);
+            else load8<T>((const T*)g.gin + m * g.ldx + n, gi);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] += gi[e];
+            float* out = (float*)g.c + m * g.ldc + n;
+            if (g.epi == EPI_RESID_X0) {
+                float o[8];
+                load8<float>(out, o);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] += o[e];
+            }
+            store8<float>(out, v);
+            break;
+        }
+    }
+}
+
 __device__ __forceinline__ int xcd_remap(int id, int n) {
     // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
-    // contiguous range of tiles so neighbouring tiles share its L2.
-    if (n % 8 != 0) return id;
+    // contiguous range of tiles so neighbouring tiles share its L2. The last
+    // n % 8 workgroups keep their own index.
+    const int full = n / 8 * 8;
+    if (id >= full) return id;
     return (id % 8) * (n / 8) + id / 8;
 }
 
@@ -327,9 +412,11 @@ struct Pipe {
 template <int BM, int BN, bool AKS, bool BKS, int ST, typename T>
 __global__ __launch_bounds__(256, ST == 2 ? 2 : 1) void k_gemm_mfma(GemmArgs g) {
     using P = Pipe<BM, BN, AKS, BKS, ST>;
-    __shared__ __attribute__((aligned(1024))) bf16_t lds0[P::STAGE_ELEMS];
-    __shared__ __attribute__((aligned(1024))) bf16_t lds1[P::STAGE_ELEMS];
-    __shared__ __attribute__((aligned(1024))) bf16_t lds2[ST == 3 ? P::STAGE_ELEMS : 8];
+    // one buffer: the stage ring during the K loop, the C staging area afterwards
+    __shared__ __attribute__((aligned(1024))) bf16_t smem[ST * P::STAGE_ELEMS];
+    bf16_t* lds0 = smem;
+    bf16_t* lds1 = smem + P::STAGE_ELEMS;
+    bf16_t* lds2 = smem + (ST == 3 ? 2 : 0) * P::STAGE_ELEMS;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
@@ -376,17 +463,33 @@ __global__ __launch_bounds__(256, ST == 2 ? 2 : 1) void k_gemm_mfma(GemmArgs g) 
         wait_vmcnt(0);  // the trailing re-read loads land before the workgroup ends
     }
 
-    // lane holds C[m = tile_m + (lane & 15)][n = tile_n + 4 * (lane >> 4) + e]
+    // Epilogue through LDS: lane holds C[m = tile_m + (lane & 15)][n = tile_n + 4 (lane >> 4) + e];
+    // the tile is staged row-major (64 rows at a time), then each thread applies the
+    // epilogue to 8 consecutive columns of a row.
+    constexpr int CH = 64;                 // rows staged per pass
+    constexpr int CP = BN + 4;             // float pitch of a staged row
+    static_assert(CH * CP * 4 <= ST * P::STAGE_ELEMS * 2, "C staging must fit the stage ring");
+    float* cs = (float*)smem;
 #pragma unroll
-    for (int i = 0; i < P::TM; ++i) {
-        const int64_t m = c.m0 + wm * (BM / 2) + i * 16 + (lane & 15);
-        if (m >= g.M) continue;
+    for (int h = 0; h < BM / CH; ++h) {
+        __syncthreads();
 #pragma unroll
-        for (int j = 0; j < P::TN; ++j) {
-            const int64_t n = c.n0 + wn * (BN / 2) + j * 16 + 4 * (lane >> 4);
-            if (n >= g.N) continue;
-            float v[4] = {acc[i][j].x, acc[i][j].y, acc[i][j].z, acc[i][j].w};
-            epilogue4<T>(g, m, n, z, v);
+        for (int i = 0; i < P::TM; ++i) {
+            const int row = wm * (BM / 2) + i * 16 + (lane & 15) - h * CH;
+            if (row < 0 || row >= CH) continue;
+#pragma unroll
+            for (int j = 0; j < P::TN; ++j)
+                *(f32x4_t*)(cs + row * CP + wn * (BN / 2) + j * 16 + 4 * (lane >> 4)) = acc[i][j];
+        }
+        __syncthreads();
+        for (int q = tid; q < CH * (BN / 8); q += 256) {
+            const int row = q / (BN / 8), col = (q % (BN / 8)) * 8;
+            const int64_t m = c.m0 + h * CH + row, n = c.n0 + col;
+            if (m >= g.M || n >= g.N) continue;
+            float v[8];
+            *(f32x4_t*)v = *(const f32x4_t*)(cs + row * CP + col);
+            *(f32x4_t*)(v + 4) = *(const f32x4_t*)(cs + row * CP + col + 4);
+            epilogue8<T>(g, m, n, z, v);
         }
     }
 }
@@ -475,23 +578,25 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool bf16, bool allow_split)
         p.bm = p.bn = 64;
     } else {
         const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
-        if (t128 >= 240) p.bm = p.bn = 128;
+        // Weight gradients (split-K allowed) take big tiles, which halve the operand
+        // re-reads, and recover parallelism by splitting the batch dimension.
+        if (t128 >= 240 || (allow_split && M >= 128 && N >= 128)) p.bm = p.bn = 128;
         else p.bm = p.bn = 64;
     }
     const int64_t tiles = ((M + p.bm - 1) / p.bm) * ((N + p.bn - 1) / p.bn);
     p.splits = 1;
     if (allow_split && tiles < 256) {
-        int64_t s = (512 + tiles - 1) / tiles;
-        const int64_t kmax = K / 256;  // keep >= 4 K steps of 64 per split
+        int64_t s = (384 + tiles - 1) / tiles;
+        const int64_t kmax = K / 512;  // keep >= 8 K steps of 64 per split
         if (s > kmax) s = kmax;
-        if (s > 32) s = 32;
+        if (s > 16) s = 16;
         if (s < 1) s = 1;
         p.splits = (int)s;
     }
     // 128 x 128 tiles: two LDS stages (64 KiB) let two workgroups share a CU, which
-    // overlaps one tile's epilogue with another's main loop; long K ranges keep
-    // the deeper three-stage ring.
-    p.stages = (p.bm == 128 && K / p.splits <= 1024) ? 2 : 3;
+    // overlaps one tile's loads and epilogue with the other's multiplies; this beats
+    // a third stage (one workgroup per CU) at every K measured.
+    p.stages = p.bm == 128 ? 2 : 3;
     return p;
 }
 
