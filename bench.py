@@ -46,9 +46,10 @@ def kernel_work(wl, B: int) -> dict:
     ALU work of the per-sample attention kernels in FMA-equivalent flops per
     (query, key) pair: the exponent argument (one FMA = 2), the exponential
     (EXP_SLOTS FMA slots = 4) and, for bf16 models whose sums run on the matrix
-    cores, half a packed f16 conversion (1); the backward evaluates every pair
-    twice. Float-storage models accumulate on the vector ALU instead
-    (forward + 3 flops, backward + 11 flops per pair).
+    cores, half a packed f16 conversion (1); their backward evaluates every pair
+    once (the forward saved each row's normaliser). Float-storage models
+    accumulate on the vector ALU instead (forward + 3 flops per pair; backward
+    evaluates every pair twice, + 11 flops).
     """
     d, r, n = wl.d, wl.rank, wl.n_proj
     nr = n * r
@@ -63,8 +64,9 @@ def kernel_work(wl, B: int) -> dict:
     w["fwd_down_gemm"] = (2.0 * B * nr * d, B * d * eb + nr * d * eb + B * nr * pb, 0.0)
     exp_f = 2.0 * EXP_SLOTS
     pair_fwd = (2.0 + exp_f + 1.0) if wl.dtype == "bf16" else (2.0 + exp_f + 3.0)
-    pair_bwd = 2 * (2.0 + exp_f + 1.0) if wl.dtype == "bf16" else (2 * (2.0 + exp_f) + 11.0)
-    w["fwd_attention"] = (0.0, B * (3 * r * 4 + r * eb), pair_fwd * B * r * r)
+    pair_bwd = (2.0 + exp_f + 1.0) if wl.dtype == "bf16" else (2 * (2.0 + exp_f) + 11.0)
+    stats = 2 * r * 4 if wl.dtype == "bf16" else 0  # saved (o, Z) per row
+    w["fwd_attention"] = (0.0, B * (3 * r * 4 + r * eb + stats), pair_fwd * B * r * r)
     # up projection + cross epilogue: h, U, bias, x0, x_l in; t, x_{l+1} out
     w["fwd_up_gemm"] = (2.0 * B * d * r, B * r * eb + d * r * eb + d * eb + 4 * B * d * eb, 0.0)
     # average over layers of: g in (storage on the top layer, float below), x0, t, grad_x0 (rmw below top), gt out
@@ -74,7 +76,7 @@ def kernel_work(wl, B: int) -> dict:
     w["bwd_bias"] = (0.0, -(-B // 128) * d * 4 + d * 4, 0.0)
     w["bwd_gu_gemm"] = (2.0 * d * r * B, B * d * eb + B * r * eb + d * r * 4, 0.0)
     w["bwd_gh_gemm"] = (2.0 * B * r * d, B * d * eb + d * r * eb + B * r * (4 if wl.attention else eb), 0.0)
-    w["bwd_attention"] = (0.0, B * (3 * r * 4 + r * 4 + 3 * r * eb), pair_bwd * B * r * r)
+    w["bwd_attention"] = (0.0, B * (3 * r * 4 + r * 4 + stats + 3 * r * eb), pair_bwd * B * r * r)
     w["bwd_gw_gemm"] = (2.0 * nr * d * B, B * nr * eb + B * d * eb + nr * d * 4, 0.0)
     w["bwd_gx_gemm"] = (2.0 * B * d * nr, B * nr * eb + nr * d * eb + 2 * B * d * 4, 0.0)
     # embedding backward: nnz ids, 2 (key, occurrence) pairs of 4 + 4 bytes per id

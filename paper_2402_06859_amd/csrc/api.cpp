@@ -80,11 +80,12 @@ void div_magic_host(uint32_t m, uint32_t& magic, uint32_t& shift) {
 size_t eb(const rdcn_handle* h) { return h->bf16 ? 2 : 4; }
 
 // Per layer: [v|q|k] (float with the attention term, else storage; plus a lo plane
-// of v when split), h and its lo plane (attention only), t, x_{l+1} and its lo plane
-// (l < L-1). Lo planes exist only with split_activations.
+// of v when split), h and its lo plane (attention only), the attention row
+// statistics [o | Z] (float, bf16 storage with attention), t, x_{l+1} and its lo
+// plane (l < L-1). Lo planes exist only with split_activations.
 struct SavedLayout {
-    size_t P[RDCN_MAX_LAYERS], P2[RDCN_MAX_LAYERS], H[RDCN_MAX_LAYERS], H2[RDCN_MAX_LAYERS], T[RDCN_MAX_LAYERS],
-        X[RDCN_MAX_LAYERS], X2[RDCN_MAX_LAYERS];
+    size_t P[RDCN_MAX_LAYERS], P2[RDCN_MAX_LAYERS], H[RDCN_MAX_LAYERS], H2[RDCN_MAX_LAYERS], A[RDCN_MAX_LAYERS],
+        T[RDCN_MAX_LAYERS], X[RDCN_MAX_LAYERS], X2[RDCN_MAX_LAYERS];
     size_t total;
 };
 
@@ -99,6 +100,7 @@ SavedLayout saved_layout(const rdcn_handle* h, int64_t B) {
         s.P2[l] = off; off += (sp && !h->attn) ? al(B * r * e) : 0;
         s.H[l] = off; off += h->attn ? al(B * r * e) : 0;
         s.H2[l] = off; off += (sp && h->attn) ? al(B * r * e) : 0;
+        s.A[l] = off; off += (h->attn && h->bf16) ? al(B * 2 * r * 4) : 0;
         s.T[l] = off; off += al(B * d * e);
         s.X[l] = off; off += more ? al(B * d * e) : 0;  // x_{l+1}
         s.X2[l] = off; off += (sp && more) ? al(B * d * e) : 0;
@@ -392,7 +394,8 @@ rdcn_status rdcn_forward(rdcn_handle* h, int64_t batch, const void* x0, const rd
             void* H = sv + S.H[l];
             void* H2 = h->split ? (void*)(sv + S.H2[l]) : nullptr;
             ProfScope ps(h, RDCN_KERNEL_FWD_ATTENTION, s);
-            RDCN_TRY(launch_attn_fwd(B, (int)r, c.attn_alpha, c.skip_beta, c.temperature, P, nr, H, H2, r, h->bf16, s));
+            RDCN_TRY(launch_attn_fwd(B, (int)r, c.attn_alpha, c.skip_beta, c.temperature, P, nr, H, H2, r,
+                                     (float*)(sv + S.A[l]), h->bf16, s));
             hsrc = H;
             hsrc2 = H2;
             ldh = r;
@@ -489,8 +492,8 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
         }
         if (h->attn) {
             ProfScope ps(h, RDCN_KERNEL_BWD_ATTENTION, s);
-            RDCN_TRY(launch_attn_bwd(B, (int)r, c.attn_alpha, c.skip_beta, c.temperature, P, nr, gh, r, gP, nr,
-                                     h->bf16, s));
+            RDCN_TRY(launch_attn_bwd(B, (int)r, c.attn_alpha, c.skip_beta, c.temperature, P, nr,
+                                     (const float*)(sv + S.A[l]), gh, r, gP, nr, h->bf16, s));
         }
         // gW = gP^T x_l    [n r, d], K = batch
         {

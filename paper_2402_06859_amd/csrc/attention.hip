@@ -170,20 +170,36 @@ __global__ __launch_bounds__(256) void k_attn_bwd(int64_t B, int r, float alpha,
 }
 
 // ---------------------------------------------------------------------------
-// bf16 models: the exponentials are computed on the vector ALU, but every
-// weighted sum over them runs on the matrix cores. For a 16-row x 32-key block
-// of one sample, each lane computes the 8 values e_ij of its row i = lane % 16
-// for keys 8 (lane / 16) .. +7, which is exactly the B-operand layout of
-// v_mfma_f32_16x16x32_f16; the A operand is a small per-sample matrix X^T whose
-// rows are the quantities to be summed against e (v, 1, v k, k, or the column
-// coefficients of the backward), each stored as an f16 hi + lo pair scaled by a
-// power of two so the pair keeps about 21 significant bits. e itself is rounded
-// to f16 (relative 2^-11); all sums of one row use the same rounded e, so the
-// normalisation by Z is consistent. Output lane l holds quantities
-// 4 (l / 16) .. +3 of row l % 16.
+// bf16 models: the exponentials are computed on the vector ALU, every weighted
+// sum over them runs on the matrix cores. For a 16-row x 32-key block of one
+// sample, each lane computes the 8 values e_ij of its row i = lane % 16 for keys
+// 8 (lane / 16) .. +7, which is exactly the B-operand layout of
+// v_mfma_f32_16x16x32_f16 with K running over keys; the A operand is a small
+// per-sample matrix X^T whose rows are the quantities summed against e (v, 1,
+// v k, k), each stored as an f16 hi + lo pair scaled by a power of two so the
+// pair keeps about 21 significant bits. e itself is rounded to f16 (relative
+// 2^-11); all sums of one row use the same rounded e, so the normalisation by Z
+// is consistent. Output lane l holds quantities 4 (l / 16) .. +3 of row l % 16.
+//
+// One wave owns up to ATT_NT 16-row tiles of one sample and loops over all keys,
+// so row sums never leave its registers and the setup needs no workgroup
+// barrier; a sample with more rows is split over W = ceil(tiles / ATT_NT) waves
+// of one workgroup.
+//
+// The forward saves each row's o_i and Z_i. The backward then needs every e_ij
+// only once: the row sums (over keys) take e in the layout above, and the column
+// sums (over rows, weighted by per-row coefficients that depend on o_i and Z_i)
+// take the same values transposed: the wave writes its 32-row x 32-key block of
+// e to LDS and reads it back with ds_read_b64_tr_b16, which delivers the B
+// operand with K running over rows.
 // ---------------------------------------------------------------------------
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x8_t __attribute__((ext_vector_type(8)));
+#define LDS_AS __attribute__((address_space(3)))
+
+constexpr int ATT_NT = 16;  // 16-row tiles per wave
 
 __device__ __forceinline__ uint32_t pk_f16(float a, float b) {
     const f16x2_t v = {(_Float16)a, (_Float16)b};
@@ -199,255 +215,347 @@ __device__ __forceinline__ float pow2_ceil(float m) {
     return ldexpf(1.f, e);
 }
 
-__device__ __forceinline__ float block_max_abs(float x, float* red) {
+__device__ __forceinline__ float wave_max(float x) {
     for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    __syncthreads();
-    if (lane == 0) red[wave] = x;
-    __syncthreads();
-    return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    return x;
+}
+__device__ __forceinline__ float wave_min(float x) {
+    for (int off = 32; off > 0; off >>= 1) x = fminf(x, __shfl_xor(x, off));
+    return x;
 }
 
-// X^T row n, keys j0 .. j0+7 as an f16 A fragment (rows >= nx read as zero).
-__device__ __forceinline__ f16x8_t xfrag(const _Float16* sx, int rpad, int n, int nx, int j0) {
+// Row n (< nx, else zero) of an f16 matrix with row stride ld, entries j0 .. j0+7.
+__device__ __forceinline__ f16x8_t xfrag(const _Float16* sx, int ld, int n, int nx, int j0) {
     if (n >= nx) return f16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-    return __builtin_bit_cast(f16x8_t, *(const u32x4_t*)(sx + n * rpad + j0));
+    return __builtin_bit_cast(f16x8_t, *(const u32x4_t*)(sx + n * ld + j0));
 }
 
 // e for one row (c, m) and 8 keys kv[0..7], packed as the B fragment.
-__device__ __forceinline__ f16x8_t efrag(float c, float m, const float* kv) {
+__device__ __forceinline__ u32x4_t efrag(float c, float m, const float* kv) {
     float e[8];
 #pragma unroll
     for (int t = 0; t < 8; ++t) e[t] = __builtin_amdgcn_exp2f(fmaf(c, kv[t], m));
-    const u32x4_t w = {pk_f16(e[0], e[1]), pk_f16(e[2], e[3]), pk_f16(e[4], e[5]), pk_f16(e[6], e[7])};
-    return __builtin_bit_cast(f16x8_t, w);
+    return u32x4_t{pk_f16(e[0], e[1]), pk_f16(e[2], e[3]), pk_f16(e[4], e[5]), pk_f16(e[6], e[7])};
 }
 
-constexpr int ATT_RT = 4;  // 16-row tiles a wave keeps in flight (register blocking)
-
-// Row pass over all keys for the row tiles rt = first + 4 q (q < ATT_RT, rt < ntile):
-// acc[q] += X^T (rows nx) . E^T over keys.
-__device__ __forceinline__ void row_pass(const float* sk, const float* sc, const float* sm, const _Float16* sx, int nx,
-                                         int rpad, int first, int ntile, int lane, f32x4_t (&acc)[ATT_RT]) {
-    const int g = lane >> 4, n = lane & 15;
-    float c[ATT_RT], m[ATT_RT];
-#pragma unroll
-    for (int q = 0; q < ATT_RT; ++q) {
-        acc[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        const int rt = first + 4 * q;
-        const int i = (rt < ntile ? rt : 0) * 16 + n;
-        c[q] = sc[i];
-        m[q] = sm[i];
-    }
-    for (int j0 = 0; j0 < rpad; j0 += 32) {
-        const int jj = j0 + 8 * g;
-        float kv[8];
-        *(u32x4_t*)kv = *(const u32x4_t*)(sk + jj);
-        *(u32x4_t*)(kv + 4) = *(const u32x4_t*)(sk + jj + 4);
-        const f16x8_t a = xfrag(sx, rpad, n, nx, jj);
-#pragma unroll
-        for (int q = 0; q < ATT_RT; ++q) {
-            if (first + 4 * q < ntile)
-                acc[q] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, efrag(c[q], m[q], kv), acc[q], 0, 0, 0);
-        }
-    }
+// Write quantity x / s as an f16 hi + lo pair into rows (row, row + 1) of X^T.
+__device__ __forceinline__ void put_pair(_Float16* sx, int ld, int row, int j, float xs) {
+    const _Float16 h = (_Float16)xs;
+    sx[row * ld + j] = h;
+    sx[(row + 1) * ld + j] = (_Float16)(xs - (float)h);
 }
 
-// Shared per-sample setup: k, v, row constants; returns kmin/kmax via LDS.
-// Padded keys / rows (index >= r) get k = 0, c = 0, m = 0 and zero X^T entries.
-__device__ __forceinline__ void setup_rows(const float* pv, const float* pq, const float* pk, int r, int rpad,
-                                           float inv_tau, float* sk, float* sv, float* sc, float* sm, float* red) {
+// Which sample and which block of row tiles a wave owns.
+struct WaveRows {
+    int64_t b;   // sample
+    int w;       // part of the sample (0 .. W-1)
+    int t0, nt;  // first tile, tiles owned
+};
+__device__ __forceinline__ WaveRows wave_rows(int W, int ntile) {
+    WaveRows o;
+    const int64_t gw = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    o.b = gw / W;
+    o.w = (int)(gw - o.b * W);
+    const int per = (((ntile + W - 1) / W) + 1) & ~1;  // even, <= ATT_NT for the W chosen at launch
+    o.t0 = o.w * per;
+    o.nt = ntile - o.t0 < per ? ntile - o.t0 : per;
+    if (o.nt < 0) o.nt = 0;
+    // wave-uniform: keep them in scalar registers
+    o.b = ((int64_t)__builtin_amdgcn_readfirstlane((int)(o.b >> 32)) << 32) |
+          (uint32_t)__builtin_amdgcn_readfirstlane((int)(o.b & 0xffffffff));
+    o.w = __builtin_amdgcn_readfirstlane(o.w);
+    o.t0 = __builtin_amdgcn_readfirstlane(o.t0);
+    o.nt = __builtin_amdgcn_readfirstlane(o.nt);
+    return o;
+}
+
+// Keys of the sample into sk (padding keys 0), their range, and the row constants
+// c_i = q_i log2(e) / tau, m_i = -c_i k*_i of the wave's rows (lane's row in tile t).
+__device__ __forceinline__ void key_setup(const float* pk, int r, int rpad, float* sk, float& kmin, float& kmax,
+                                          int lane) {
     float lo = INFINITY, hi = -INFINITY;
-    for (int j = threadIdx.x; j < rpad; j += blockDim.x) {
+    for (int j = lane; j < rpad; j += 64) {
         const float kj = j < r ? pk[j] : 0.f;
         sk[j] = kj;
-        sv[j] = j < r ? pv[j] : 0.f;
         if (j < r) {
             lo = fminf(lo, kj);
             hi = fmaxf(hi, kj);
         }
     }
-    float kmin, kmax;
-    block_minmax(lo, hi, red, kmin, kmax);
-    for (int i = threadIdx.x; i < rpad; i += blockDim.x) {
-        const float c = i < r ? pq[i] * (LOG2E * inv_tau) : 0.f;
-        sc[i] = c;
-        sm[i] = i < r ? -(c * (c >= 0.f ? kmax : kmin)) : 0.f;
+    kmin = wave_min(lo);
+    kmax = wave_max(hi);
+}
+
+// (c_i, m_i) of rows t0 * 16 + il, il < 16 * NT, into scm[il] (rows past r: c = m = 0).
+template <int NT>
+__device__ __forceinline__ void row_consts(const float* pq, int r, int t0, int lane, float inv_tau, float kmin,
+                                           float kmax, float2* scm) {
+    for (int il = lane; il < 16 * NT; il += 64) {
+        const int i = t0 * 16 + il;
+        const float ci = i < r ? pq[i] * (LOG2E * inv_tau) : 0.f;
+        scm[il] = make_float2(ci, i < r ? -(ci * (ci >= 0.f ? kmax : kmin)) : 0.f);
     }
 }
 
-// Write quantity x_j / s as an f16 hi + lo pair into rows (hi_row, hi_row + 1) of X^T.
-__device__ __forceinline__ void put_pair(_Float16* sx, int rpad, int hi_row, int j, float xs) {
-    const _Float16 h = (_Float16)xs;
-    sx[hi_row * rpad + j] = h;
-    sx[(hi_row + 1) * rpad + j] = (_Float16)(xs - (float)h);
-}
+// LDS words per wave of the forward: keys, row constants, X^T (3 rows).
+__host__ __device__ constexpr int attn_fwd_wave_floats(int rpad) { return rpad + 2 * 16 * ATT_NT + 3 * rpad / 2; }
 
-template <typename T>
-__global__ __launch_bounds__(256) void k_attn_fwd_mfma(int r, int rpad, float alpha, float beta, float inv_tau,
-                                                      const float* __restrict__ P, int64_t ldp, T* __restrict__ H,
-                                                      T* __restrict__ H2, int64_t ldh) {
+// NT: tiles computed per wave (a power of two >= the tiles it owns; the extra ones
+// are computed on harmless row constants and discarded).
+template <typename T, int NT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_attn_fwd_mfma(int64_t B, int r, int rpad, int W, float alpha, float beta,
+                                                      float inv_tau, const float* __restrict__ P, int64_t ldp,
+                                                      T* __restrict__ H, T* __restrict__ H2, int64_t ldh,
+                                                      float* __restrict__ stats) {
     extern __shared__ __attribute__((aligned(16))) float smem[];
-    float* sk = smem;              // [rpad]
-    float* sv = sk + rpad;         // [rpad]
-    float* sc = sv + rpad;         // [rpad]
-    float* sm = sc + rpad;         // [rpad]
-    float* red = sm + rpad;        // [32]
-    _Float16* sx = (_Float16*)(red + 32);  // X^T: 3 rows x rpad (v hi, v lo, 1)
-    const int64_t b = blockIdx.x;
-    const float* pv = P + b * ldp;
-    setup_rows(pv, pv + r, pv + 2 * r, r, rpad, inv_tau, sk, sv, sc, sm, red);
-    float vmax = 0.f;
-    for (int j = threadIdx.x; j < r; j += blockDim.x) vmax = fmaxf(vmax, fabsf(sv[j]));
-    const float vs = pow2_ceil(block_max_abs(vmax, red));
-    for (int j = threadIdx.x; j < rpad; j += blockDim.x) {
-        put_pair(sx, rpad, 0, j, sv[j] / vs);
-        sx[2 * rpad + j] = (_Float16)(j < r ? 1.f : 0.f);
-    }
-    __syncthreads();
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int ntile = rpad / 16;
-    for (int first = wave; first < ntile; first += 4 * ATT_RT) {
-        f32x4_t acc[ATT_RT];
-        row_pass(sk, sc, sm, sx, 3, rpad, first, ntile, lane, acc);
-        if (lane < 16) {
+    const WaveRows wr = wave_rows(W, ntile);
+    if (wr.b >= B) return;
+    float* sk = smem + wave * attn_fwd_wave_floats(rpad);  // [rpad] keys
+    float2* scm = (float2*)(sk + rpad);                       // [16 ATT_NT] row constants
+    _Float16* sx = (_Float16*)(scm + 16 * ATT_NT);            // X^T: 3 rows x rpad (v hi, v lo, 1)
+    const float* pv = P + wr.b * ldp;
+    float kmin, kmax;
+    key_setup(pv + 2 * r, r, rpad, sk, kmin, kmax, lane);
+    float vmax = 0.f;
+    for (int j = lane; j < r; j += 64) vmax = fmaxf(vmax, fabsf(pv[j]));
+    const float vs = pow2_ceil(wave_max(vmax));
+    for (int j = lane; j < rpad; j += 64) {
+        put_pair(sx, rpad, 0, j, j < r ? pv[j] / vs : 0.f);
+        sx[2 * rpad + j] = (_Float16)(j < r ? 1.f : 0.f);
+    }
+    row_consts<NT>(pv + r, r, wr.t0, lane, inv_tau, kmin, kmax, scm);
+    __builtin_amdgcn_wave_barrier();
+    const int g = lane >> 4, n = lane & 15;
+    f32x4_t acc[NT];
 #pragma unroll
-            for (int q = 0; q < ATT_RT; ++q) {
-                const int i = (first + 4 * q) * 16 + lane;
-                if (first + 4 * q < ntile && i < r) {
-                    const float o = (acc[q].x + acc[q].y) * vs / acc[q].z;
-                    const float hv = beta * sv[i] + alpha * o;
-                    st<T>::store(H + b * ldh + i, hv);
-                    if (H2) st<T>::store(H2 + b * ldh + i, hv - st<T>::load(H + b * ldh + i));
-                }
+    for (int t = 0; t < NT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j0 = 0; j0 < rpad; j0 += 32) {
+        const int jj = j0 + 8 * g;
+        float kv[8];
+        *(u32x4_t*)kv = *(const u32x4_t*)(sk + jj);
+        *(u32x4_t*)(kv + 4) = *(const u32x4_t*)(sk + jj + 4);
+        const f16x8_t a = xfrag(sx, rpad, n, 3, jj);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const float2 cm = scm[16 * t + n];
+            acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, __builtin_bit_cast(f16x8_t, efrag(cm.x, cm.y, kv)),
+                                                            acc[t], 0, 0, 0);
+        }
+    }
+    if (lane < 16) {
+        float* so = stats + wr.b * 2 * (int64_t)r;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const int i = (wr.t0 + t) * 16 + lane;
+            if (t < wr.nt && i < r) {
+                const float z = acc[t].z;
+                const float o = (acc[t].x + acc[t].y) * vs / z;
+                const float hv = beta * pv[i] + alpha * o;
+                st<T>::store(H + wr.b * ldh + i, hv);
+                if (H2) st<T>::store(H2 + wr.b * ldh + i, hv - st<T>::load(H + wr.b * ldh + i));
+                so[i] = o;
+                so[r + i] = z;
             }
         }
     }
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void k_attn_bwd_mfma(int r, int rpad, float alpha, float beta, float inv_tau,
-                                                      const float* __restrict__ P, int64_t ldp,
-                                                      const float* __restrict__ GH, int64_t ldg, T* __restrict__ GP,
-                                                      int64_t ldgp) {
+// LDS of the backward. Per sample (shared by its W waves): keys and X^T (4 rows).
+// Per wave: row constants, Y^T (6 rows of the wave's rows), one 32 x 32 f16 block
+// of e, and (W > 1) two column-partial slots.
+__host__ __device__ constexpr int attn_bwd_sample_floats(int rpad) { return 3 * rpad; }
+__host__ __device__ constexpr int attn_bwd_slot_offset() { return 2 * 16 * ATT_NT + 3 * (16 * ATT_NT) + 512; }
+__host__ __device__ constexpr int attn_bwd_wave_floats(int W) { return attn_bwd_slot_offset() + (W > 1 ? 2 * 96 : 0); }
+__host__ __device__ constexpr int attn_bwd_block_floats(int rpad, int W) {
+    return (4 / W) * attn_bwd_sample_floats(rpad) + 4 * attn_bwd_wave_floats(W);
+}
+
+// ds_read_b64_tr_b16 of the e block: lane (g, i) receives e[8 g + t][16 h + i]
+// for t = 0..7 (rows t < 4 from the first read, t >= 4 from the second). Block
+// rows hold 32 keys as four 16-byte chunks, chunk index XOR ((row >> 2) & 3).
+__device__ __forceinline__ f16x8_t e_transposed(const _Float16* se, int h, int lane) {
+    const int g = lane >> 4, i = lane & 15;
+    const int chunk = 2 * h + ((i & 3) >> 1);
+    const int r0 = 8 * g + (i >> 2), r1 = r0 + 4;
+    const int o0 = r0 * 32 + ((chunk ^ ((r0 >> 2) & 3)) * 8) + 4 * (i & 1);
+    const int o1 = r1 * 32 + ((chunk ^ ((r1 >> 2) & 3)) * 8) + 4 * (i & 1);
+    const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4_t*)(se + o0));
+    const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4_t*)(se + o1));
+    const s16x8_t v = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    return __builtin_bit_cast(f16x8_t, v);
+}
+
+// Backward. Row sums W1_i = sum_j e v_j k_j, W2_i = sum_j e k_j give
+// dq_i = go_i / (Z_i tau) (W1_i - o_i W2_i); column sums C1_j = sum_i e a_i,
+// C2_j = sum_i e a_i o_i, C3_j = sum_i e go_i / Z_i with a_i = go_i q_i / (Z_i tau)
+// give dk_j = v_j C1_j - C2_j and dv_j = beta gh_j + C3_j (go = alpha gh).
+template <typename T, int W, int NT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_attn_bwd_mfma(int64_t B, int r, int rpad, float alpha, float beta,
+                                                      float inv_tau, const float* __restrict__ P, int64_t ldp,
+                                                      const float* __restrict__ stats,
+                                                      const float* __restrict__ GH, int64_t ldg,
+                                                      T* __restrict__ GP, int64_t ldgp) {
     extern __shared__ __attribute__((aligned(16))) float smem[];
-    float* sk = smem;
-    float* sv = sk + rpad;
-    float* sc = sv + rpad;
-    float* sm = sc + rpad;
-    float* sa = sm + rpad;   // a_i = go_i q_i / (Z_i tau)
-    float* sb = sa + rpad;   // b_i = a_i o_i
-    float* sg = sb + rpad;   // c_i = go_i / Z_i
-    float* red = sg + rpad;  // [32]
-    _Float16* sx = (_Float16*)(red + 32);  // X^T rows: v hi/lo, 1, 0, v k hi/lo, k hi/lo   (8 x rpad)
-    _Float16* sy = sx + 8 * rpad;          // Y^T rows: a hi/lo, b hi/lo, c hi/lo             (6 x rpad)
-    const int64_t b = blockIdx.x;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int ntile = rpad / 16;
+    const WaveRows wr = wave_rows(W, ntile);
+    const bool live = wr.b < B;
+    if (W == 1 && !live) return;  // with W > 1 every wave takes part in the barriers
+    constexpr int RW = 16 * ATT_NT;
+    float* sk = smem + (wave / W) * attn_bwd_sample_floats(rpad);  // [rpad] keys (shared by the sample's waves)
+    _Float16* sx = (_Float16*)(sk + rpad);                           // 4 x rpad: v k hi/lo, k hi/lo
+    float* pw = smem + (4 / W) * attn_bwd_sample_floats(rpad) + wave * attn_bwd_wave_floats(W);
+    float2* scm = (float2*)pw;                   // [RW] row constants
+    _Float16* sy = (_Float16*)(scm + RW);        // 6 x RW: a hi/lo, a o hi/lo, go/Z hi/lo
+    _Float16* se = sy + 6 * RW;                  // 32 x 32 e block
+    float* slot = pw + attn_bwd_slot_offset();   // 2 x 96 column partials (W > 1)
+    const int g = lane >> 4, n = lane & 15;
+    const int64_t b = live ? wr.b : 0;
     const float* pv = P + b * ldp;
     const float* pq = pv + r;
+    const float* pk = pv + 2 * r;
     const float* gh = GH + b * ldg;
-    setup_rows(pv, pq, pv + 2 * r, r, rpad, inv_tau, sk, sv, sc, sm, red);
-    float mv = 0.f, mvk = 0.f, mk = 0.f;
-    for (int j = threadIdx.x; j < r; j += blockDim.x) {
-        mv = fmaxf(mv, fabsf(sv[j]));
-        mvk = fmaxf(mvk, fabsf(sv[j] * sk[j]));
-        mk = fmaxf(mk, fabsf(sk[j]));
+    const float* so = stats + b * 2 * (int64_t)r;
+    // every wave reduces over all keys (from memory); each writes its share of the
+    // sample's key arrays
+    float lo = INFINITY, hi = -INFINITY, mvk = 0.f, mk = 0.f;
+    for (int j = lane; j < r; j += 64) {
+        const float kj = pk[j];
+        lo = fminf(lo, kj);
+        hi = fmaxf(hi, kj);
+        mvk = fmaxf(mvk, fabsf(pv[j] * kj));
+        mk = fmaxf(mk, fabsf(kj));
     }
-    const float vs = pow2_ceil(block_max_abs(mv, red));
-    const float vks = pow2_ceil(block_max_abs(mvk, red));
-    const float ks = pow2_ceil(block_max_abs(mk, red));
-    for (int j = threadIdx.x; j < rpad; j += blockDim.x) {
-        put_pair(sx, rpad, 0, j, sv[j] / vs);
-        sx[2 * rpad + j] = (_Float16)(j < r ? 1.f : 0.f);
-        sx[3 * rpad + j] = (_Float16)0.f;
-        put_pair(sx, rpad, 4, j, sv[j] * sk[j] / vks);
-        put_pair(sx, rpad, 6, j, sk[j] / ks);
+    const float kmin = wave_min(lo), kmax = wave_max(hi);
+    const float vks = pow2_ceil(wave_max(mvk)), ks = pow2_ceil(wave_max(mk));
+    for (int j = lane + 64 * wr.w; j < rpad; j += 64 * W) {
+        const float kj = j < r ? pk[j] : 0.f, vj = j < r ? pv[j] : 0.f;
+        sk[j] = kj;
+        put_pair(sx, rpad, 0, j, vj * kj / vks);
+        put_pair(sx, rpad, 2, j, kj / ks);
     }
-    __syncthreads();
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int ntile = rpad / 16;
-    // row pass: Z, S = sum e v, W1 = sum e v k, W2 = sum e k per query row
-    for (int first = wave; first < ntile; first += 4 * ATT_RT) {
-        f32x4_t acc[ATT_RT];
-        row_pass(sk, sc, sm, sx, 8, rpad, first, ntile, lane, acc);
-#pragma unroll
-        for (int q = 0; q < ATT_RT; ++q) {
-            // lanes 16..31 hold (W1 hi, W1 lo, W2 hi, W2 lo) of row lane - 16
-            const float w1 = __shfl((acc[q].x + acc[q].y) * vks, lane + 16);
-            const float w2 = __shfl((acc[q].z + acc[q].w) * ks, lane + 16);
-            const int i = (first + 4 * q) * 16 + lane;
-            if (lane < 16 && first + 4 * q < ntile) {
-                if (i < r) {
-                    const float z = acc[q].z;
-                    const float o = (acc[q].x + acc[q].y) * vs / z;
-                    const float go = alpha * gh[i];
-                    const float rz = 1.0f / z;
-                    const float a = go * pq[i] * rz * inv_tau;
-                    st<T>::store(GP + b * ldgp + r + i, go * rz * inv_tau * (w1 - o * w2));
-                    sa[i] = a;
-                    sb[i] = a * o;
-                    sg[i] = go * rz;
-                } else {
-                    sa[i] = sb[i] = sg[i] = 0.f;
-                }
-            }
-        }
-    }
-    __syncthreads();
+    // per-row coefficients of the wave's rows
     float ma = 0.f, mb = 0.f, mc = 0.f;
-    for (int i = threadIdx.x; i < r; i += blockDim.x) {
-        ma = fmaxf(ma, fabsf(sa[i]));
-        mb = fmaxf(mb, fabsf(sb[i]));
-        mc = fmaxf(mc, fabsf(sg[i]));
-    }
-    const float as = pow2_ceil(block_max_abs(ma, red));
-    const float bs = pow2_ceil(block_max_abs(mb, red));
-    const float cs = pow2_ceil(block_max_abs(mc, red));
-    for (int i = threadIdx.x; i < rpad; i += blockDim.x) {
-        put_pair(sy, rpad, 0, i, sa[i] / as);
-        put_pair(sy, rpad, 2, i, sb[i] / bs);
-        put_pair(sy, rpad, 4, i, sg[i] / cs);
-    }
-    __syncthreads();
-    // column pass: for keys j, sum over rows i of e_ij (a_i, b_i, c_i);
-    // lane (j = lane % 16, g) computes e for rows 8 g .. +7 of a 32-row chunk.
-    const int g = lane >> 4, n = lane & 15;
-    for (int first = wave; first < ntile; first += 4 * ATT_RT) {
-        f32x4_t acc[ATT_RT];
-        float kj[ATT_RT];
-#pragma unroll
-        for (int q = 0; q < ATT_RT; ++q) {
-            acc[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            const int ct = first + 4 * q;
-            kj[q] = sk[(ct < ntile ? ct : 0) * 16 + n];
+    for (int il = lane; il < RW; il += 64) {
+        const int i = wr.t0 * 16 + il;
+        if (il < wr.nt * 16 && i < r) {
+            const float go = alpha * gh[i], rz = 1.0f / so[r + i];
+            const float a = go * pq[i] * rz * inv_tau;
+            ma = fmaxf(ma, fabsf(a));
+            mb = fmaxf(mb, fabsf(a * so[i]));
+            mc = fmaxf(mc, fabsf(go * rz));
         }
-        for (int i0 = 0; i0 < rpad; i0 += 32) {
-            const int ii = i0 + 8 * g;
-            float cv[8], mv8[8];
-            *(u32x4_t*)cv = *(const u32x4_t*)(sc + ii);
-            *(u32x4_t*)(cv + 4) = *(const u32x4_t*)(sc + ii + 4);
-            *(u32x4_t*)mv8 = *(const u32x4_t*)(sm + ii);
-            *(u32x4_t*)(mv8 + 4) = *(const u32x4_t*)(sm + ii + 4);
-            const f16x8_t a = xfrag(sy, rpad, n, 6, ii);
+    }
+    const float as = pow2_ceil(wave_max(ma)), bs = pow2_ceil(wave_max(mb)), cs = pow2_ceil(wave_max(mc));
+    for (int il = lane; il < RW; il += 64) {
+        const int i = wr.t0 * 16 + il;
+        float a = 0.f, ao = 0.f, gz = 0.f;
+        if (il < wr.nt * 16 && i < r) {
+            const float go = alpha * gh[i], rz = 1.0f / so[r + i];
+            a = go * pq[i] * rz * inv_tau;
+            ao = a * so[i];
+            gz = go * rz;
+        }
+        put_pair(sy, RW, 0, il, a / as);
+        put_pair(sy, RW, 2, il, ao / bs);
+        put_pair(sy, RW, 4, il, gz / cs);
+    }
+    row_consts<NT>(pq, r, wr.t0, lane, inv_tau, kmin, kmax, scm);
+    if (W > 1) __syncthreads();
+    else __builtin_amdgcn_wave_barrier();
+
+    f32x4_t acc[NT];
 #pragma unroll
-            for (int q = 0; q < ATT_RT; ++q) {
-                if (first + 4 * q < ntile) {
-                    float e[8];
+    for (int t = 0; t < NT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int chunk = 0, j0 = 0; j0 < rpad; j0 += 32, ++chunk) {
+        const int jj = j0 + 8 * g;
+        float kv[8];
+        *(u32x4_t*)kv = *(const u32x4_t*)(sk + jj);
+        *(u32x4_t*)(kv + 4) = *(const u32x4_t*)(sk + jj + 4);
+        const f16x8_t ax = xfrag(sx, rpad, n, 4, jj);
+        f32x4_t col[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
-                    for (int t = 0; t < 8; ++t) e[t] = __builtin_amdgcn_exp2f(fmaf(cv[t], kj[q], mv8[t]));
-                    const u32x4_t w = {pk_f16(e[0], e[1]), pk_f16(e[2], e[3]), pk_f16(e[4], e[5]), pk_f16(e[6], e[7])};
-                    acc[q] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, __builtin_bit_cast(f16x8_t, w), acc[q], 0, 0, 0);
+        for (int p = 0; p < NT / 2; ++p) {
+            {
+                // the wave's LDS operations run in order, so this pair's writes
+                // follow the previous pair's transposed reads of the same block
+                __builtin_amdgcn_wave_barrier();
+                _Float16* eb = se;
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    const int t = 2 * p + q;
+                    const float2 cm = scm[16 * t + n];
+                    const u32x4_t e = efrag(cm.x, cm.y, kv);
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax, __builtin_bit_cast(f16x8_t, e), acc[t], 0,
+                                                                    0, 0);
+                    const int row = 16 * q + n;
+                    *(u32x4_t*)(eb + row * 32 + ((g ^ ((row >> 2) & 3)) * 8)) = e;
+                }
+                const f16x8_t ay = xfrag(sy, RW, n, 6, 32 * p + 8 * g);
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+                    col[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ay, e_transposed(eb, h, lane), col[h], 0, 0, 0);
+            }
+        }
+        // lanes 0..15: (a hi, a lo, a o hi, a o lo) of key n (+16 h); lanes 16..31: (go/Z hi, lo)
+        if (W == 1) {
+            if (lane < 32) {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int j = j0 + 16 * h + n;
+                    if (j < r) {
+                        if (lane < 16) {
+                            const float c1 = (col[h].x + col[h].y) * as, c2 = (col[h].z + col[h].w) * bs;
+                            st<T>::store(GP + b * ldgp + 2 * r + j, pv[j] * c1 - c2);
+                        } else {
+                            st<T>::store(GP + b * ldgp + j, beta * gh[j] + (col[h].x + col[h].y) * cs);
+                        }
+                    }
+                }
+            }
+        } else {
+            float* sl = slot + (chunk & 1) * 96;
+            if (lane < 32) {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    if (lane < 16) {
+                        sl[16 * h + n] = (col[h].x + col[h].y) * as;
+                        sl[32 + 16 * h + n] = (col[h].z + col[h].w) * bs;
+                    } else {
+                        sl[64 + 16 * h + n] = (col[h].x + col[h].y) * cs;
+                    }
+                }
+            }
+            __syncthreads();
+            // the sample's first wave adds the W partials in wave order
+            if (live && wr.w == 0 && lane < 32) {
+                const int j = j0 + lane;
+                float c1 = 0.f, c2 = 0.f, c3 = 0.f;
+#pragma unroll
+                for (int w = 0; w < W; ++w) {
+                    const float* so2 = smem + (4 / W) * attn_bwd_sample_floats(rpad) +
+                                       (wave + w) * attn_bwd_wave_floats(W) + attn_bwd_slot_offset() + (chunk & 1) * 96;
+                    c1 += so2[lane];
+                    c2 += so2[32 + lane];
+                    c3 += so2[64 + lane];
+                }
+                if (j < r) {
+                    st<T>::store(GP + b * ldgp + 2 * r + j, pv[j] * c1 - c2);
+                    st<T>::store(GP + b * ldgp + j, beta * gh[j] + c3);
                 }
             }
         }
+    }
+    if (live && lane < 16) {
 #pragma unroll
-        for (int q = 0; q < ATT_RT; ++q) {
-            const float c3 = __shfl((acc[q].x + acc[q].y) * cs, lane + 16);
-            const int j = (first + 4 * q) * 16 + lane;
-            if (lane < 16 && first + 4 * q < ntile && j < r) {
-                const float c1 = (acc[q].x + acc[q].y) * as;
-                const float c2 = (acc[q].z + acc[q].w) * bs;
-                st<T>::store(GP + b * ldgp + 2 * r + j, sv[j] * c1 - c2);
-                st<T>::store(GP + b * ldgp + j, beta * gh[j] + c3);
+        for (int t = 0; t < NT; ++t) {
+            const int i = (wr.t0 + t) * 16 + lane;
+            if (t < wr.nt && i < r) {
+                const float w1 = (acc[t].x + acc[t].y) * vks, w2 = (acc[t].z + acc[t].w) * ks;
+                const float go = alpha * gh[i], rz = 1.0f / so[r + i];
+                st<T>::store(GP + b * ldgp + r + i, go * rz * inv_tau * (w1 - so[i] * w2));
             }
         }
     }
@@ -460,37 +568,80 @@ int attn_threads(int r) {
 
 }  // namespace
 
+// waves per sample: 1, 2 or 4 (a workgroup of 4 waves holds whole samples)
+static int attn_waves(int rpad) {
+    const int ntile = rpad / 16;
+    return ntile <= ATT_NT ? 1 : ntile <= 2 * ATT_NT ? 2 : 4;
+}
+// tiles computed per wave: the power of two (>= 2) covering the tiles one wave owns
+static int attn_tiles(int rpad, int W) {
+    const int ntile = rpad / 16;
+    const int per = (((ntile + W - 1) / W) + 1) & ~1;
+    int nt = 2;
+    while (nt < per) nt *= 2;
+    return nt;
+}
+
 hipError_t launch_attn_fwd(int64_t B, int r, float alpha, float beta, float tau, const void* P, int64_t ldp, void* H,
-                           void* H2, int64_t ldh, bool bf16, hipStream_t s) {
+                           void* H2, int64_t ldh, float* stats, bool bf16, hipStream_t s) {
     if (B == 0) return hipSuccess;
     if (bf16) {
+        if (r > 4 * 16 * ATT_NT || !stats) return hipErrorInvalidValue;
         const int rpad = (r + 31) / 32 * 32;
-        const size_t lds = sizeof(float) * (4 * (size_t)rpad + 32) + sizeof(_Float16) * 3 * (size_t)rpad;
-        hipLaunchKernelGGL(k_attn_fwd_mfma<bf16_t>, dim3((unsigned)B), dim3(256), lds, s, r, rpad, alpha, beta,
-                           1.0f / tau, (const float*)P, ldp, (bf16_t*)H, (bf16_t*)H2, ldh);
+        const int W = attn_waves(rpad);
+        const int NT = attn_tiles(rpad, W);
+        const int64_t blocks = (B * W + 3) / 4;
+        const size_t lds = 4 * sizeof(float) * (size_t)attn_fwd_wave_floats(rpad);
+#define RDCN_AFWD(NTV)                                                                                          \
+    hipLaunchKernelGGL((k_attn_fwd_mfma<bf16_t, NTV>), dim3((unsigned)blocks), dim3(256), lds, s, B, r, rpad, W, \
+                       alpha, beta, 1.0f / tau, (const float*)P, ldp, (bf16_t*)H, (bf16_t*)H2, ldh, stats)
+        if (NT == 2) RDCN_AFWD(2);
+        else if (NT == 4) RDCN_AFWD(4);
+        else if (NT == 8) RDCN_AFWD(8);
+        else RDCN_AFWD(16);
+#undef RDCN_AFWD
         return hipGetLastError();
     }
     const size_t lds = sizeof(float) * (2 * (size_t)r + 32);
     const int th = attn_threads(r);
-        hipLaunchKernelGGL(k_attn_fwd<float>, dim3((unsigned)B), dim3(th), lds, s, B, r, alpha, beta, 1.0f / tau,
-                           (const float*)P, ldp, (float*)H, (float*)H2, ldh);
+    hipLaunchKernelGGL(k_attn_fwd<float>, dim3((unsigned)B), dim3(th), lds, s, B, r, alpha, beta, 1.0f / tau,
+                       (const float*)P, ldp, (float*)H, (float*)H2, ldh);
     return hipGetLastError();
 }
 
 hipError_t launch_attn_bwd(int64_t B, int r, float alpha, float beta, float tau, const void* P, int64_t ldp,
-                           const float* GH, int64_t ldg, void* GP, int64_t ldgp, bool bf16, hipStream_t s) {
+                           const float* stats, const float* GH, int64_t ldg, void* GP, int64_t ldgp, bool bf16,
+                           hipStream_t s) {
     if (B == 0) return hipSuccess;
     if (bf16) {
+        if (r > 4 * 16 * ATT_NT || !stats) return hipErrorInvalidValue;
         const int rpad = (r + 31) / 32 * 32;
-        const size_t lds = sizeof(float) * (7 * (size_t)rpad + 32) + sizeof(_Float16) * 14 * (size_t)rpad;
-        hipLaunchKernelGGL(k_attn_bwd_mfma<bf16_t>, dim3((unsigned)B), dim3(256), lds, s, r, rpad, alpha, beta,
-                           1.0f / tau, (const float*)P, ldp, GH, ldg, (bf16_t*)GP, ldgp);
+        const int W = attn_waves(rpad);
+        const int NT = attn_tiles(rpad, W);
+        const int64_t blocks = (B * W + 3) / 4;
+        const size_t lds = sizeof(float) * (size_t)attn_bwd_block_floats(rpad, W);
+#define RDCN_ABWD(WV, NTV)                                                                                          \
+    hipLaunchKernelGGL((k_attn_bwd_mfma<bf16_t, WV, NTV>), dim3((unsigned)blocks), dim3(256), lds, s, B, r, rpad,     \
+                       alpha, beta, 1.0f / tau, (const float*)P, ldp, stats, GH, ldg, (bf16_t*)GP, ldgp)
+        if (W == 1) {
+            if (NT == 2) RDCN_ABWD(1, 2);
+            else if (NT == 4) RDCN_ABWD(1, 4);
+            else if (NT == 8) RDCN_ABWD(1, 8);
+            else RDCN_ABWD(1, 16);
+        } else if (W == 2) {
+            if (NT == 8) RDCN_ABWD(2, 8);
+            else RDCN_ABWD(2, 16);
+        } else {
+            if (NT == 8) RDCN_ABWD(4, 8);
+            else RDCN_ABWD(4, 16);
+        }
+#undef RDCN_ABWD
         return hipGetLastError();
     }
     const size_t lds = sizeof(float) * (7 * (size_t)r + 32);
     const int th = attn_threads(r);
-        hipLaunchKernelGGL(k_attn_bwd<float>, dim3((unsigned)B), dim3(th), lds, s, B, r, alpha, beta, 1.0f / tau,
-                           (const float*)P, ldp, GH, ldg, (float*)GP, ldgp);
+    hipLaunchKernelGGL(k_attn_bwd<float>, dim3((unsigned)B), dim3(th), lds, s, B, r, alpha, beta, 1.0f / tau,
+                       (const float*)P, ldp, GH, ldg, (float*)GP, ldgp);
     return hipGetLastError();
 }
 

@@ -27,8 +27,8 @@ namespace rdcn {
 namespace {
 
 constexpr int RS_THREADS = 256;
-constexpr int RS_ITEMS = 16;
-constexpr int RS_TILE = RS_THREADS * RS_ITEMS;  // 4096 pairs per radix tile
+constexpr int RS_ITEMS = 4;
+constexpr int RS_TILE = RS_THREADS * RS_ITEMS;  // 1024 pairs per radix tile
 constexpr int SEG_TILE = 128;                    // sorted pairs per reduction wave
 
 template <typename ID>
@@ -112,29 +112,22 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
     return wofs + x - v;
 }
 
-// Per digit d (thread per digit): exclusive prefix over tiles of hist[d][*] in
-// place, digit total into tot[d].
-__global__ __launch_bounds__(256) void k_digit_prefix(uint32_t* __restrict__ hist, int ndig, int ntiles,
-                                                      uint32_t* __restrict__ tot) {
-    const int d = blockIdx.x * blockDim.x + threadIdx.x;
-    if (d >= ndig) return;
-    uint32_t* row = hist + (int64_t)d * ntiles;
+// Per digit d (one workgroup per digit): exclusive prefix over the tiles of
+// hist[d][*] in place, 256 tiles per round; digit total into tot[d].
+__global__ __launch_bounds__(256) void k_digit_scan(uint32_t* __restrict__ hist, int ntiles,
+                                                    uint32_t* __restrict__ tot) {
+    __shared__ uint32_t sh[4];
+    uint32_t* row = hist + (int64_t)blockIdx.x * ntiles;
     uint32_t run = 0;
-    int t = 0;
-    for (; t + 4 <= ntiles; t += 4) {
-        const uint32_t v0 = row[t], v1 = row[t + 1], v2 = row[t + 2], v3 = row[t + 3];
-        row[t] = run;
-        row[t + 1] = run + v0;
-        row[t + 2] = run + v0 + v1;
-        row[t + 3] = run + v0 + v1 + v2;
-        run += v0 + v1 + v2 + v3;
+    for (int t0 = 0; t0 < ntiles; t0 += 256) {
+        const int t = t0 + threadIdx.x;
+        const uint32_t v = t < ntiles ? row[t] : 0u;
+        uint32_t total;
+        const uint32_t ex = block_exclusive_scan(v, sh, total);
+        if (t < ntiles) row[t] = run + ex;
+        run += total;
     }
-    for (; t < ntiles; ++t) {
-        const uint32_t v = row[t];
-        row[t] = run;
-        run += v;
-    }
-    tot[d] = run;
+    if (threadIdx.x == 0) tot[blockIdx.x] = run;
 }
 
 // 2b. stable scatter: items of a tile are ranked in element order (slot-major,
@@ -204,8 +197,17 @@ __global__ __launch_bounds__(RS_THREADS) void k_rs_scatter(const uint32_t* __res
     }
 }
 
-// 3. segmented reduction. DV = table columns per lane (D <= 64 * DV).
-template <typename T, typename ID, int DV>
+// 3. segmented reduction. A wave takes SEG_TILE consecutive sorted pairs. L lanes
+// (a power of two, 4 L >= D) hold one pair's gradient slice, four columns per lane,
+// so one wave step covers E = 64 / L pairs; all slices of up to 16 steps are loaded
+// before any is summed. Sums run in a fixed order: inside a step a segmented
+// inclusive scan over the E pairs (Hillis-Steele, lane shuffles), across steps a
+// running carry in front of the step's partial sum.
+struct Cols4 {
+    float v[4];
+};
+
+template <typename T, typename ID>
 struct SegCtx {
     EmbedBwdArgs a;
     const uint32_t* keys;
@@ -214,32 +216,34 @@ struct SegCtx {
     uint32_t n;
     uint32_t sentinel, rbase;
 
-    // contribution of sorted pair (k, o) to the row of key k, elements c = lane + 64*j
-    __device__ __forceinline__ void contrib(uint32_t k, uint32_t o, float* out, int lane) const {
+    // contribution of sorted pair (k, o) to the row of key k, columns c .. c+3
+    template <bool VEC>
+    __device__ __forceinline__ Cols4 contrib(uint32_t k, uint32_t o, int c) const {
+        Cols4 out = {{0.f, 0.f, 0.f, 0.f}};
+        if (c >= a.D) return out;
         const bool isq = k < rbase;
         const uint32_t kk = isq ? k : k - rbase;
         const uint32_t f = isq ? div_magic(kk, DivMagic{a.magic_q, a.shift_q, (uint32_t)a.rows_q})
                                : div_magic(kk, DivMagic{a.magic_m, a.shift_m, a.m});
         const uint32_t bag = a.offsets ? bag_of[o] : o;
         const int64_t b = div_magic(bag, DivMagic{a.magic_f, a.shift_f, (uint32_t)a.F});
-        const float* g = a.grad_x0 + b * a.d + (int64_t)f * a.D;
+        const float* g = a.grad_x0 + b * a.d + (int64_t)f * a.D + c;
+        if (VEC) {
+            const f32x4_t w = *(const f32x4_t*)g;
+            out.v[0] = w.x; out.v[1] = w.y; out.v[2] = w.z; out.v[3] = w.w;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) out.v[e] = g[e];
+        }
         if (a.combine == 0) {
             uint32_t qi, ri;
             split_id<ID>(((const ID*)a.ids)[o], a, qi, ri);
-            const T* other = isq ? (const T*)a.r_tables + ((int64_t)f * a.m + ri) * a.D
-                                 : (const T*)a.q_tables + ((int64_t)f * a.rows_q + qi) * a.D;
+            const T* other = isq ? (const T*)a.r_tables + ((int64_t)f * a.m + ri) * a.D + c
+                                 : (const T*)a.q_tables + ((int64_t)f * a.rows_q + qi) * a.D + c;
 #pragma unroll
-            for (int j = 0; j < DV; ++j) {
-                const int c = lane + 64 * j;
-                out[j] = c < a.D ? g[c] * st<T>::load(other + c) : 0.f;
-            }
-        } else {
-#pragma unroll
-            for (int j = 0; j < DV; ++j) {
-                const int c = lane + 64 * j;
-                out[j] = c < a.D ? g[c] : 0.f;
-            }
+            for (int e = 0; e < 4; ++e) out.v[e] *= st<T>::load(other + e);
         }
+        return out;
     }
 
     __device__ __forceinline__ float* row_of(uint32_t k) const {
@@ -247,80 +251,135 @@ struct SegCtx {
     }
 };
 
-template <typename T, typename ID, int DV>
-__global__ __launch_bounds__(256) void k_seg_reduce(SegCtx<T, ID, DV> s, float* __restrict__ carry_head,
+template <bool VEC>
+__device__ __forceinline__ Cols4 load4(const float* p) {
+    Cols4 x;
+    if (VEC) {
+        const f32x4_t w = *(const f32x4_t*)p;
+        x.v[0] = w.x; x.v[1] = w.y; x.v[2] = w.z; x.v[3] = w.w;
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x.v[e] = p[e];
+    }
+    return x;
+}
+
+template <bool VEC>
+__device__ __forceinline__ void store4(float* p, const Cols4& x) {
+    if (VEC) {
+        *(f32x4_t*)p = f32x4_t{x.v[0], x.v[1], x.v[2], x.v[3]};
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) p[e] = x.v[e];
+    }
+}
+
+constexpr uint32_t SEG_PAD = 0xffffffffu;  // key of the slots past the last sorted pair
+
+// Where a finished piece goes: 0 nowhere (padding, ids out of range, or lanes past
+// D), 1 the table row (+=), 2 this tile's head carry, 3 its tail carry.
+enum { DST_NONE = 0, DST_ROW = 1, DST_HEAD = 2, DST_TAIL = 3 };
+
+template <typename T, typename ID, int L, bool VEC>
+__global__ __launch_bounds__(256) void k_seg_reduce(SegCtx<T, ID> s, float* __restrict__ carry_head,
                                                     float* __restrict__ carry_tail) {
-    const int lane = threadIdx.x & 63;
+    constexpr int E = 64 / L;
+    constexpr int STEPS = SEG_TILE / E;
+    constexpr int U = STEPS < 16 ? STEPS : 16;
+    const int lane = threadIdx.x & 63, grp = lane / L, sub = lane % L, c = 4 * sub;
     const uint32_t tile = blockIdx.x * 4 + (threadIdx.x >> 6);
     const uint32_t p0 = tile * SEG_TILE;
     if (p0 >= s.n) return;
-    const uint32_t p1 = p0 + SEG_TILE < s.n ? p0 + SEG_TILE : s.n;
-    const uint32_t prevkey = p0 > 0 ? s.keys[p0 - 1] : 0xffffffffu;
-    const uint32_t nextkey = p1 < s.n ? s.keys[p1] : 0xffffffffu;
+    const uint32_t cnt = s.n - p0 < (uint32_t)SEG_TILE ? s.n - p0 : (uint32_t)SEG_TILE;
     const int D = s.a.D;
-    float acc[DV];
+    const uint32_t first_key = s.keys[p0], last_key = s.keys[p0 + cnt - 1];
+    // the first segment started in an earlier tile / the last one goes on in a later tile
+    const bool head_cont = p0 > 0 && s.keys[p0 - 1] == first_key;
+    const bool tail_cont = p0 + cnt < s.n && s.keys[p0 + cnt] == last_key;
+    Cols4 carry = {{0.f, 0.f, 0.f, 0.f}};
+    uint32_t carry_key = SEG_PAD;
+    for (int s0 = 0; s0 < STEPS; s0 += U) {
+        uint32_t key[U], val[U];
 #pragma unroll
-    for (int j = 0; j < DV; ++j) acc[j] = 0.f;
-    uint32_t cur = s.keys[p0];
-    bool first_piece = true;
-    auto flush = [&](bool continues) {
-        if (cur == s.sentinel) return;
-        const bool started_before = first_piece && cur == prevkey;
-        float* dst;
-        if (!started_before && !continues) {
-            dst = s.row_of(cur);
-#pragma unroll
-            for (int j = 0; j < DV; ++j) {
-                const int c = lane + 64 * j;
-                if (c < D) dst[c] += acc[j];
-            }
-            return;
+        for (int u = 0; u < U; ++u) {
+            const uint32_t e = (uint32_t)((s0 + u) * E + grp);
+            key[u] = e < cnt ? s.keys[p0 + e] : SEG_PAD;
+            val[u] = e < cnt ? s.vals[p0 + e] : 0u;
         }
-        dst = (started_before ? carry_head : carry_tail) + (int64_t)tile * D;
+        // which pairs end a piece (the next pair has another key, or the tile ends)
+        // and where that piece goes; the old table rows of direct writes are loaded
+        // together with the gradient slices
+        int dst[U];
 #pragma unroll
-        for (int j = 0; j < DV; ++j) {
-            const int c = lane + 64 * j;
-            if (c < D) dst[c] = acc[j];
-        }
-    };
-    constexpr int U = 8;  // entries whose gradient slices are in flight together
-    for (uint32_t base = p0; base < p1; base += 64) {
-        const uint32_t cnt = p1 - base < 64 ? p1 - base : 64;
-        const uint32_t kl = lane < (int)cnt ? s.keys[base + lane] : s.sentinel;
-        const uint32_t vl = lane < (int)cnt ? s.vals[base + lane] : 0u;
-        for (uint32_t i = 0; i < cnt; i += U) {
-            float cv[U][DV];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {  // loads first ...
-                const uint32_t k = __builtin_amdgcn_readlane(kl, i + u);
-                const uint32_t o = __builtin_amdgcn_readlane(vl, i + u);
-                if (i + u < cnt && k != s.sentinel) s.contrib(k, o, cv[u], lane);
+        for (int u = 0; u < U; ++u) {
+            const uint32_t e = (uint32_t)((s0 + u) * E + grp);
+            uint32_t knext = __shfl_down(key[u], L);
+            if (u + 1 < U) {
+                const uint32_t k0 = __shfl(key[u + 1], sub);
+                if (grp == E - 1) knext = k0;
+            } else if (grp == E - 1) {
+                const uint32_t en = (uint32_t)((s0 + U) * E);
+                knext = en < cnt ? s.keys[p0 + en] : SEG_PAD;
             }
+            const uint32_t k = key[u];
+            int d = DST_NONE;
+            if (k != SEG_PAD && k != s.sentinel && c < D && (knext != k || e + 1 == cnt)) {
+                if (head_cont && k == first_key) d = DST_HEAD;
+                else if (tail_cont && k == last_key) d = DST_TAIL;
+                else d = DST_ROW;
+            }
+            dst[u] = d;
+        }
+        Cols4 x[U], old[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {  // ... then the in-order sums
-                if (i + u >= cnt) break;
-                const uint32_t k = __builtin_amdgcn_readlane(kl, i + u);
-                if (k != cur) {
-                    flush(false);
-                    first_piece = false;
-                    cur = k;
+        for (int u = 0; u < U; ++u) {
+            if (key[u] != SEG_PAD && key[u] != s.sentinel) x[u] = s.template contrib<VEC>(key[u], val[u], c);
+            else x[u] = Cols4{{0.f, 0.f, 0.f, 0.f}};
+            if (dst[u] == DST_ROW) old[u] = load4<VEC>(s.row_of(key[u]) + c);
+        }
 #pragma unroll
-                    for (int j = 0; j < DV; ++j) acc[j] = 0.f;
+        for (int u = 0; u < U; ++u) {
+            const uint32_t k = key[u];
+            const uint32_t kprev = __shfl_up(k, L);
+            bool head = grp == 0 ? k != carry_key : k != kprev;
+            Cols4 v = x[u];
+#pragma unroll
+            for (int off = 1; off < E; off <<= 1) {
+                Cols4 y;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) y.v[e] = __shfl_up(v.v[e], off * L);
+                const bool hy = __shfl_up((int)head, off * L) != 0;
+                if (grp >= off && !head) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v.v[e] = y.v[e] + v.v[e];
                 }
-                if (k != s.sentinel)
-#pragma unroll
-                    for (int j = 0; j < DV; ++j) acc[j] += cv[u][j];
+                if (grp >= off) head = head || hy;
             }
+            if (!head) {  // the segment reaches back into the carried one
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v.v[e] = carry.v[e] + v.v[e];
+            }
+            if (dst[u] == DST_ROW) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) old[u].v[e] += v.v[e];
+                store4<VEC>(s.row_of(k) + c, old[u]);
+            } else if (dst[u] == DST_HEAD) {
+                store4<VEC>(carry_head + (int64_t)tile * D + c, v);
+            } else if (dst[u] == DST_TAIL) {
+                store4<VEC>(carry_tail + (int64_t)tile * D + c, v);
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) carry.v[e] = __shfl(v.v[e], (E - 1) * L + sub);
+            carry_key = __shfl(k, (E - 1) * L + sub);
         }
     }
-    flush(cur == nextkey);
 }
 
 // Fix-up: the tile whose last segment starts inside it and continues owns the
 // segment; it adds its tail piece and the head pieces of the following tiles
 // in tile order.
 template <typename T, typename ID, int DV>
-__global__ __launch_bounds__(256) void k_seg_fixup(SegCtx<T, ID, DV> s, const float* __restrict__ carry_head,
+__global__ __launch_bounds__(256) void k_seg_fixup(SegCtx<T, ID> s, const float* __restrict__ carry_head,
                                                    const float* __restrict__ carry_tail) {
     const int lane = threadIdx.x & 63;
     const uint32_t tile = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -358,10 +417,10 @@ __global__ __launch_bounds__(256) void k_seg_fixup(SegCtx<T, ID, DV> s, const fl
     }
 }
 
-template <typename T, typename ID, int DV>
+template <typename T, typename ID, int L, bool VEC, int DV>
 hipError_t launch_reduce(const EmbedBwdArgs& a, const uint32_t* keys, const uint32_t* vals, const uint32_t* bag_of,
                          uint32_t n, float* carry_head, float* carry_tail, hipStream_t st) {
-    SegCtx<T, ID, DV> s;
+    SegCtx<T, ID> s;
     s.a = a;
     s.keys = keys;
     s.vals = vals;
@@ -371,11 +430,23 @@ hipError_t launch_reduce(const EmbedBwdArgs& a, const uint32_t* keys, const uint
     s.rbase = (uint32_t)a.F * a.rows_q;
     const uint32_t ntiles = (n + SEG_TILE - 1) / SEG_TILE;
     const unsigned blocks = (ntiles + 3) / 4;
-    hipLaunchKernelGGL((k_seg_reduce<T, ID, DV>), dim3(blocks), dim3(256), 0, st, s, carry_head, carry_tail);
+    hipLaunchKernelGGL((k_seg_reduce<T, ID, L, VEC>), dim3(blocks), dim3(256), 0, st, s, carry_head, carry_tail);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((k_seg_fixup<T, ID, DV>), dim3(blocks), dim3(256), 0, st, s, carry_head, carry_tail);
     return hipGetLastError();
+}
+
+// lanes per pair (4 columns each) and fix-up columns per lane for table width D <= 256
+template <typename T, typename ID, bool VEC>
+hipError_t launch_reduce_d(const EmbedBwdArgs& a, const uint32_t* keys, const uint32_t* vals, const uint32_t* bag_of,
+                           uint32_t n, float* ch, float* ct, hipStream_t st) {
+    const int q = (a.D + 3) / 4;
+    if (q <= 4) return launch_reduce<T, ID, 4, VEC, 1>(a, keys, vals, bag_of, n, ch, ct, st);
+    if (q <= 8) return launch_reduce<T, ID, 8, VEC, 1>(a, keys, vals, bag_of, n, ch, ct, st);
+    if (q <= 16) return launch_reduce<T, ID, 16, VEC, 1>(a, keys, vals, bag_of, n, ch, ct, st);
+    if (q <= 32) return launch_reduce<T, ID, 32, VEC, 2>(a, keys, vals, bag_of, n, ch, ct, st);
+    return launch_reduce<T, ID, 64, VEC, 4>(a, keys, vals, bag_of, n, ch, ct, st);
 }
 
 inline int key_bits(uint32_t maxkey) {
@@ -470,7 +541,7 @@ hipError_t launch_emb_sort(const EmbedBwdArgs& a, void* scratch, hipStream_t st)
         hipLaunchKernelGGL(k_rs_hist, dim3(ntiles), dim3(RS_THREADS), 0, st, P.keys[cur], n, shift, mask, P.hist,
                            ntiles);
         const int ndig = (int)(mask + 1);
-        hipLaunchKernelGGL(k_digit_prefix, dim3((ndig + 255) / 256), dim3(256), 0, st, P.hist, ndig, ntiles, P.sums);
+        hipLaunchKernelGGL(k_digit_scan, dim3(ndig), dim3(256), 0, st, P.hist, ntiles, P.sums);
         hipLaunchKernelGGL(k_rs_scatter, dim3(ntiles), dim3(RS_THREADS), 0, st, P.keys[cur], P.vals[cur],
                            P.keys[cur ^ 1], P.vals[cur ^ 1], n, shift, bits, P.hist, ntiles, P.sums);
         hipError_t e = hipGetLastError();
@@ -485,12 +556,15 @@ hipError_t launch_emb_reduce(const EmbedBwdArgs& a, bool bf16, bool ids64, void*
     const EmbPtrs P = emb_ptrs(a, scratch);
     const uint32_t n = (uint32_t)(2 * a.nnz);
     const int cur = P.L.passes & 1;
-    const int dv = (a.D + 63) / 64;
-#define RDCN_RED(T, ID, DV) return launch_reduce<T, ID, DV>(a, P.keys[cur], P.vals[cur], P.bag_of, n, P.carry_head, P.carry_tail, st)
-#define RDCN_RED_DV(T, ID) do { if (dv == 1) RDCN_RED(T, ID, 1); if (dv == 2) RDCN_RED(T, ID, 2); RDCN_RED(T, ID, 4); } while (0)
-    if (bf16) { if (ids64) RDCN_RED_DV(bf16_t, int64_t); else RDCN_RED_DV(bf16_t, int32_t); }
-    else      { if (ids64) RDCN_RED_DV(float, int64_t); else RDCN_RED_DV(float, int32_t); }
-#undef RDCN_RED_DV
+    // 16-byte column groups: D and d are multiples of 4 (checked at create), so only
+    // the base pointers decide
+    const bool vec = (((uintptr_t)a.grad_x0 | (uintptr_t)a.grad_q | (uintptr_t)a.grad_r) & 15) == 0 &&
+                     a.D % 4 == 0 && a.d % 4 == 0;
+#define RDCN_RED(T, ID) \
+    return vec ? launch_reduce_d<T, ID, true>(a, P.keys[cur], P.vals[cur], P.bag_of, n, P.carry_head, P.carry_tail, st) \
+               : launch_reduce_d<T, ID, false>(a, P.keys[cur], P.vals[cur], P.bag_of, n, P.carry_head, P.carry_tail, st)
+    if (bf16) { if (ids64) RDCN_RED(bf16_t, int64_t); else RDCN_RED(bf16_t, int32_t); }
+    else      { if (ids64) RDCN_RED(float, int64_t); else RDCN_RED(float, int32_t); }
 #undef RDCN_RED
 }
 

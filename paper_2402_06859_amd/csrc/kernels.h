@@ -27,10 +27,13 @@ hipError_t launch_qr_gather(const GatherArgs& a, bool bf16, bool ids64, hipStrea
 
 namespace rdcn {
 
+// bf16 storage: the forward writes o_i and Z_i of every row to stats ([o | Z] per
+// sample, row stride 2 r) and the backward reads them back.
 hipError_t launch_attn_fwd(int64_t B, int r, float alpha, float beta, float tau, const void* P, int64_t ldp, void* H,
-                           void* H2, int64_t ldh, bool bf16, hipStream_t s);
+                           void* H2, int64_t ldh, float* stats, bool bf16, hipStream_t s);
 hipError_t launch_attn_bwd(int64_t B, int r, float alpha, float beta, float tau, const void* P, int64_t ldp,
-                           const float* GH, int64_t ldg, void* GP, int64_t ldgp, bool bf16, hipStream_t s);
+                           const float* stats, const float* GH, int64_t ldg, void* GP, int64_t ldgp, bool bf16,
+                           hipStream_t s);
 
 int pointwise_rows_per_block(int64_t B, int64_t d);
 hipError_t launch_bwd_pointwise(int64_t B, int64_t d, const void* gin, bool gin_f32, const void* x0, const void* t,

@@ -89,6 +89,16 @@ def test_split_activations_ragged(attn):
     run_full_compare(wl, fwd_tol=2e-3)
 
 
+@pytest.mark.parametrize("rank,batch", [(296, 77), (600, 37)])
+def test_attention_multiwave_ragged(rank, batch):
+    """Ranks above 256 split one sample's rows over 2 or 4 waves of a workgroup (the
+    backward adds their column sums in wave order); odd batches leave idle waves in
+    the last workgroup, and ranks that are no multiple of 32 leave padded keys."""
+    need_gpu()
+    wl = Workload("multiwave", 15, batch, 4, 20_000, 150, 16, 64, 2, rank, True, "bf16", "sum", 1.1)
+    run_full_compare(wl)
+
+
 def test_fp32_attention_ragged():
     need_gpu()
     wl = Workload("ragged32", 12, 130, 3, 10_000, 100, 16, 12, 3, 20, True, "f32", "mul", 1.1)
