@@ -165,7 +165,8 @@ rdcn_status qr_embed_backward_workspace(const rdcn_handle* h, int64_t batch, int
  * The contributions to one table row are added in (b, position-in-bag) order,
  * so the result is deterministic. ids/offsets/tables as in qr_embed_gather;
  * nnz = number of ids (batch * F when single-hot). scratch must hold
- * qr_embed_backward_workspace() bytes.
+ * qr_embed_backward_workspace() bytes. grad_x0, grad_q_tables and
+ * grad_r_tables must be 16-byte aligned (RDCN_ERR_ARG otherwise).
  */
 rdcn_status qr_embed_backward(rdcn_handle* h, int64_t batch, int64_t nnz, const void* ids, const int64_t* offsets,
                               const void* q_tables, const void* r_tables, const float* grad_x0,

@@ -297,7 +297,8 @@ rdcn_status qr_embed_backward_workspace(const rdcn_handle* h, int64_t batch, int
     if (!h->cfg.multi_hot && nnz != batch * h->cfg.num_cat) return RDCN_ERR_SHAPE;
     if (2 * nnz >= ((int64_t)1 << 31)) return RDCN_ERR_UNSUPPORTED;
     const EmbedBwdLayout L =
-        embed_bwd_layout(nnz, h->cfg.num_cat, h->cfg.qr_rows_q, h->cfg.qr_rows_r, h->cfg.emb_dim, h->cfg.multi_hot);
+        embed_bwd_layout(nnz, h->cfg.num_cat, h->cfg.qr_rows_q, h->cfg.qr_rows_r, h->cfg.emb_dim, h->cfg.multi_hot,
+                         h->cfg.combine == RDCN_COMBINE_MUL);
     *scratch_bytes = al(L.total);
     return RDCN_OK;
 }
@@ -315,6 +316,7 @@ rdcn_status qr_embed_backward(rdcn_handle* h, int64_t batch, int64_t nnz, const 
     if (!ids || !q_tables || !r_tables || !grad_x0 || !grad_q_tables || !grad_r_tables || !scratch)
         return RDCN_ERR_ARG;
     if (scratch_bytes < need || !aligned256(scratch)) return RDCN_ERR_WORKSPACE;
+    if ((((uintptr_t)grad_x0) | ((uintptr_t)grad_q_tables) | ((uintptr_t)grad_r_tables)) & 15) return RDCN_ERR_ARG;
     EmbedBwdArgs a;
     a.batch = batch;
     a.nnz = nnz;
@@ -346,7 +348,7 @@ rdcn_status qr_embed_backward(rdcn_handle* h, int64_t batch, int64_t nnz, const 
         RDCN_TRY(launch_emb_sort(a, scratch, s));
     }
     ProfScope ps(h, RDCN_KERNEL_EMB_REDUCE, s);
-    return hip_status(launch_emb_reduce(a, h->bf16, h->ids64, scratch, s));
+    return hip_status(launch_emb_reduce(a, h->bf16, scratch, s));
 }
 
 static rdcn_status check_weights(const rdcn_handle* h, const rdcn_weights* w) {

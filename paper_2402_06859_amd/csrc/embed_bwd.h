@@ -23,13 +23,14 @@ struct EmbedBwdArgs {
 };
 
 struct EmbedBwdLayout {
-    uint64_t keys0, vals0, keys1, vals1, bag_of, hist, sums, carry_head, carry_tail, total;
+    uint64_t keys0, vals0, keys1, vals1, bag_of, qrow, rrow, hist, sums, carry_head, carry_tail, total;
     int bits, passes, dbits;
 };
 
-EmbedBwdLayout embed_bwd_layout(int64_t nnz, int F, int rows_q, int m, int D, bool bags);
+EmbedBwdLayout embed_bwd_layout(int64_t nnz, int F, int rows_q, int m, int D, bool bags, bool mul);
 hipError_t launch_emb_keys(const EmbedBwdArgs& a, bool ids64, void* scratch, hipStream_t s);
 hipError_t launch_emb_sort(const EmbedBwdArgs& a, void* scratch, hipStream_t s);
-hipError_t launch_emb_reduce(const EmbedBwdArgs& a, bool bf16, bool ids64, void* scratch, hipStream_t s);
+// grad_x0, grad_q and grad_r must be 16-byte aligned (checked by the caller).
+hipError_t launch_emb_reduce(const EmbedBwdArgs& a, bool bf16, void* scratch, hipStream_t s);
 
 }  // namespace rdcn

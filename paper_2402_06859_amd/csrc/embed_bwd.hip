@@ -47,9 +47,12 @@ __device__ __forceinline__ bool split_id(ID raw, const EmbedBwdArgs& a, uint32_t
 }
 
 // 1. keys. Single-hot: thread per occurrence o = b*F + f. Bags: thread per bag.
-template <typename ID, bool BAGS>
+// With the product combine each occurrence also records its quotient and
+// remainder rows (the reduction multiplies by the row of the other table).
+template <typename ID, bool BAGS, bool MUL>
 __global__ __launch_bounds__(256) void k_emb_keys(EmbedBwdArgs a, uint32_t* __restrict__ keys,
-                                                  uint32_t* __restrict__ vals, uint32_t* __restrict__ bag_of) {
+                                                  uint32_t* __restrict__ vals, uint32_t* __restrict__ bag_of,
+                                                  uint32_t* __restrict__ qrow, uint32_t* __restrict__ rrow) {
     const ID* ids = (const ID*)a.ids;
     const uint32_t sentinel = (uint32_t)a.F * (a.rows_q + a.m);
     const uint32_t rbase = (uint32_t)a.F * a.rows_q;
@@ -60,16 +63,22 @@ __global__ __launch_bounds__(256) void k_emb_keys(EmbedBwdArgs a, uint32_t* __re
         const int64_t begin = BAGS ? a.offsets[u] : u;
         const int64_t end = BAGS ? a.offsets[u + 1] : u + 1;
         for (int64_t p = begin; p < end && p < a.nnz; ++p) {
-            uint32_t qi, ri, kq = sentinel, kr = sentinel;
+            uint32_t qi = 0, ri = 0, kq = sentinel, kr = sentinel;
             if (split_id<ID>(ids[p], a, qi, ri)) {
                 kq = (uint32_t)f * a.rows_q + qi;
                 kr = rbase + (uint32_t)f * a.m + ri;
+            } else {
+                qi = ri = 0;
             }
             keys[p] = kq;
             keys[a.nnz + p] = kr;
             vals[p] = (uint32_t)p;
             vals[a.nnz + p] = (uint32_t)p;
             if (BAGS) bag_of[p] = (uint32_t)u;
+            if (MUL) {
+                qrow[p] = qi;
+                rrow[p] = ri;
+            }
         }
     }
 }
@@ -207,42 +216,40 @@ struct Cols4 {
     float v[4];
 };
 
-template <typename T, typename ID>
+template <typename T>
 struct SegCtx {
     EmbedBwdArgs a;
     const uint32_t* keys;
     const uint32_t* vals;
-    const uint32_t* bag_of;
+    const uint32_t* bag_of;  // bags
+    const uint32_t* qrow;    // product combine
+    const uint32_t* rrow;
     uint32_t n;
     uint32_t sentinel, rbase;
 
-    // contribution of sorted pair (k, o) to the row of key k, columns c .. c+3
-    template <bool VEC>
-    __device__ __forceinline__ Cols4 contrib(uint32_t k, uint32_t o, int c) const {
-        Cols4 out = {{0.f, 0.f, 0.f, 0.f}};
-        if (c >= a.D) return out;
-        const bool isq = k < rbase;
-        const uint32_t kk = isq ? k : k - rbase;
+    // contribution of sorted pair (k, o) to the row of key k, columns c .. c+3.
+    // Every load is issued unconditionally (ok = false reads row 0 / occurrence 0
+    // and returns zeros), so the loads of many pairs can be in flight together.
+    template <bool MUL, bool BAGS>
+    __device__ __forceinline__ Cols4 contrib(uint32_t k, uint32_t o, int c, bool ok) const {
+        const uint32_t kk0 = ok ? k : 0u;
+        const bool isq = kk0 < rbase;
+        const uint32_t kk = isq ? kk0 : kk0 - rbase;
         const uint32_t f = isq ? div_magic(kk, DivMagic{a.magic_q, a.shift_q, (uint32_t)a.rows_q})
                                : div_magic(kk, DivMagic{a.magic_m, a.shift_m, a.m});
-        const uint32_t bag = a.offsets ? bag_of[o] : o;
+        const uint32_t oo = ok ? o : 0u;
+        const int cc = ok ? c : 0;
+        const uint32_t bag = BAGS ? bag_of[oo] : oo;
         const int64_t b = div_magic(bag, DivMagic{a.magic_f, a.shift_f, (uint32_t)a.F});
-        const float* g = a.grad_x0 + b * a.d + (int64_t)f * a.D + c;
-        if (VEC) {
-            const f32x4_t w = *(const f32x4_t*)g;
-            out.v[0] = w.x; out.v[1] = w.y; out.v[2] = w.z; out.v[3] = w.w;
-        } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) out.v[e] = g[e];
-        }
-        if (a.combine == 0) {
-            uint32_t qi, ri;
-            split_id<ID>(((const ID*)a.ids)[o], a, qi, ri);
-            const T* other = isq ? (const T*)a.r_tables + ((int64_t)f * a.m + ri) * a.D + c
-                                 : (const T*)a.q_tables + ((int64_t)f * a.rows_q + qi) * a.D + c;
+        const f32x4_t w = *(const f32x4_t*)(a.grad_x0 + b * a.d + (int64_t)f * a.D + cc);
+        Cols4 out = {{w.x, w.y, w.z, w.w}};
+        if (MUL) {
+            const T* other = isq ? (const T*)a.r_tables + ((int64_t)f * a.m + rrow[oo]) * a.D + cc
+                                 : (const T*)a.q_tables + ((int64_t)f * a.rows_q + qrow[oo]) * a.D + cc;
 #pragma unroll
             for (int e = 0; e < 4; ++e) out.v[e] *= st<T>::load(other + e);
         }
+        if (!ok) out = Cols4{{0.f, 0.f, 0.f, 0.f}};
         return out;
     }
 
@@ -251,27 +258,14 @@ struct SegCtx {
     }
 };
 
-template <bool VEC>
+// 16-byte column groups (D and d are multiples of 4, the float buffers 16-byte aligned)
 __device__ __forceinline__ Cols4 load4(const float* p) {
-    Cols4 x;
-    if (VEC) {
-        const f32x4_t w = *(const f32x4_t*)p;
-        x.v[0] = w.x; x.v[1] = w.y; x.v[2] = w.z; x.v[3] = w.w;
-    } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) x.v[e] = p[e];
-    }
-    return x;
+    const f32x4_t w = *(const f32x4_t*)p;
+    return Cols4{{w.x, w.y, w.z, w.w}};
 }
 
-template <bool VEC>
 __device__ __forceinline__ void store4(float* p, const Cols4& x) {
-    if (VEC) {
-        *(f32x4_t*)p = f32x4_t{x.v[0], x.v[1], x.v[2], x.v[3]};
-    } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) p[e] = x.v[e];
-    }
+    *(f32x4_t*)p = f32x4_t{x.v[0], x.v[1], x.v[2], x.v[3]};
 }
 
 constexpr uint32_t SEG_PAD = 0xffffffffu;  // key of the slots past the last sorted pair
@@ -280,8 +274,8 @@ constexpr uint32_t SEG_PAD = 0xffffffffu;  // key of the slots past the last sor
 // D), 1 the table row (+=), 2 this tile's head carry, 3 its tail carry.
 enum { DST_NONE = 0, DST_ROW = 1, DST_HEAD = 2, DST_TAIL = 3 };
 
-template <typename T, typename ID, int L, bool VEC>
-__global__ __launch_bounds__(256) void k_seg_reduce(SegCtx<T, ID> s, float* __restrict__ carry_head,
+template <typename T, int L, bool MUL, bool BAGS>
+__global__ __launch_bounds__(256) void k_seg_reduce(SegCtx<T> s, float* __restrict__ carry_head,
                                                     float* __restrict__ carry_tail) {
     constexpr int E = 64 / L;
     constexpr int STEPS = SEG_TILE / E;
@@ -292,6 +286,7 @@ __global__ __launch_bounds__(256) void k_seg_reduce(SegCtx<T, ID> s, float* __re
     if (p0 >= s.n) return;
     const uint32_t cnt = s.n - p0 < (uint32_t)SEG_TILE ? s.n - p0 : (uint32_t)SEG_TILE;
     const int D = s.a.D;
+    const bool colok = c < D;
     const uint32_t first_key = s.keys[p0], last_key = s.keys[p0 + cnt - 1];
     // the first segment started in an earlier tile / the last one goes on in a later tile
     const bool head_cont = p0 > 0 && s.keys[p0 - 1] == first_key;
@@ -303,9 +298,13 @@ __global__ __launch_bounds__(256) void k_seg_reduce(SegCtx<T, ID> s, float* __re
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const uint32_t e = (uint32_t)((s0 + u) * E + grp);
-            key[u] = e < cnt ? s.keys[p0 + e] : SEG_PAD;
-            val[u] = e < cnt ? s.vals[p0 + e] : 0u;
+            const uint32_t ec = e < cnt ? e : cnt - 1;
+            key[u] = s.keys[p0 + ec];
+            val[u] = s.vals[p0 + ec];
+            if (e >= cnt) key[u] = SEG_PAD;
         }
+        const uint32_t en = (uint32_t)((s0 + U) * E);
+        const uint32_t key_after = en < cnt ? s.keys[p0 + en] : SEG_PAD;
         // which pairs end a piece (the next pair has another key, or the tile ends)
         // and where that piece goes; the old table rows of direct writes are loaded
         // together with the gradient slices
@@ -314,16 +313,11 @@ __global__ __launch_bounds__(256) void k_seg_reduce(SegCtx<T, ID> s, float* __re
         for (int u = 0; u < U; ++u) {
             const uint32_t e = (uint32_t)((s0 + u) * E + grp);
             uint32_t knext = __shfl_down(key[u], L);
-            if (u + 1 < U) {
-                const uint32_t k0 = __shfl(key[u + 1], sub);
-                if (grp == E - 1) knext = k0;
-            } else if (grp == E - 1) {
-                const uint32_t en = (uint32_t)((s0 + U) * E);
-                knext = en < cnt ? s.keys[p0 + en] : SEG_PAD;
-            }
+            const uint32_t k0 = u + 1 < U ? __shfl(key[u + 1 < U ? u + 1 : u], sub) : key_after;
+            if (grp == E - 1) knext = k0;
             const uint32_t k = key[u];
             int d = DST_NONE;
-            if (k != SEG_PAD && k != s.sentinel && c < D && (knext != k || e + 1 == cnt)) {
+            if (k != SEG_PAD && k != s.sentinel && colok && (knext != k || e + 1 == cnt)) {
                 if (head_cont && k == first_key) d = DST_HEAD;
                 else if (tail_cont && k == last_key) d = DST_TAIL;
                 else d = DST_ROW;
@@ -333,9 +327,9 @@ __global__ __launch_bounds__(256) void k_seg_reduce(SegCtx<T, ID> s, float* __re
         Cols4 x[U], old[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            if (key[u] != SEG_PAD && key[u] != s.sentinel) x[u] = s.template contrib<VEC>(key[u], val[u], c);
-            else x[u] = Cols4{{0.f, 0.f, 0.f, 0.f}};
-            if (dst[u] == DST_ROW) old[u] = load4<VEC>(s.row_of(key[u]) + c);
+            const bool ok = key[u] != SEG_PAD && key[u] != s.sentinel && colok;
+            x[u] = s.template contrib<MUL, BAGS>(key[u], val[u], c, ok);
+            old[u] = load4(s.row_of(dst[u] == DST_ROW ? key[u] : 0u) + (colok ? c : 0));
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -362,11 +356,11 @@ __global__ __launch_bounds__(256) void k_seg_reduce(SegCtx<T, ID> s, float* __re
             if (dst[u] == DST_ROW) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) old[u].v[e] += v.v[e];
-                store4<VEC>(s.row_of(k) + c, old[u]);
+                store4(s.row_of(k) + c, old[u]);
             } else if (dst[u] == DST_HEAD) {
-                store4<VEC>(carry_head + (int64_t)tile * D + c, v);
+                store4(carry_head + (int64_t)tile * D + c, v);
             } else if (dst[u] == DST_TAIL) {
-                store4<VEC>(carry_tail + (int64_t)tile * D + c, v);
+                store4(carry_tail + (int64_t)tile * D + c, v);
             }
 #pragma unroll
             for (int e = 0; e < 4; ++e) carry.v[e] = __shfl(v.v[e], (E - 1) * L + sub);
@@ -376,77 +370,100 @@ __global__ __launch_bounds__(256) void k_seg_reduce(SegCtx<T, ID> s, float* __re
 }
 
 // Fix-up: the tile whose last segment starts inside it and continues owns the
-// segment; it adds its tail piece and the head pieces of the following tiles
-// in tile order.
-template <typename T, typename ID, int DV>
-__global__ __launch_bounds__(256) void k_seg_fixup(SegCtx<T, ID> s, const float* __restrict__ carry_head,
+// segment. Its wave finds the following tiles that open with the same key 64 at a
+// time (one ballot over their first keys), loads their head pieces E tiles per
+// step (lanes as in the reduction), and adds them in a fixed order: each lane
+// group sums its tiles in tile order, then the groups are added pairwise, and the
+// owner's tail piece goes in front.
+template <int L>
+__global__ __launch_bounds__(256) void k_seg_fixup(const uint32_t* __restrict__ keys, uint32_t n, uint32_t sentinel,
+                                                   uint32_t rbase, int D, float* __restrict__ grad_q,
+                                                   float* __restrict__ grad_r, const float* __restrict__ carry_head,
                                                    const float* __restrict__ carry_tail) {
-    const int lane = threadIdx.x & 63;
+    constexpr int E = 64 / L;
+    const int lane = threadIdx.x & 63, grp = lane / L, sub = lane % L, c = 4 * sub;
     const uint32_t tile = blockIdx.x * 4 + (threadIdx.x >> 6);
     const uint32_t p0 = tile * SEG_TILE;
-    if (p0 >= s.n) return;
+    if (p0 >= n) return;
     const uint32_t p1 = p0 + SEG_TILE;
-    if (p1 >= s.n) return;
-    const uint32_t k = s.keys[p1 - 1];
-    if (k == s.sentinel || s.keys[p1] != k) return;
+    if (p1 >= n) return;
+    const uint32_t k = keys[p1 - 1];
+    if (k == sentinel || keys[p1] != k) return;
     // the last piece started before this tile when the whole tile is that segment and it came from before
-    if (p0 > 0 && s.keys[p0] == k && s.keys[p0 - 1] == k) return;
-    const int D = s.a.D;
-    float tot[DV];
+    if (p0 > 0 && keys[p0] == k && keys[p0 - 1] == k) return;
+    const uint32_t ntiles = (n + SEG_TILE - 1) / SEG_TILE;
+    Cols4 acc = {{0.f, 0.f, 0.f, 0.f}};
+    for (uint32_t base = tile + 1;; base += 64) {
+        const uint32_t t = base + lane;
+        const bool cont = t < ntiles && keys[t * SEG_TILE] == k;
+        const uint64_t mask = __ballot(cont);
+        const int run = mask == ~0ull ? 64 : __builtin_ctzll(~mask);  // tiles base .. base+run-1 continue it
+        for (int st = 0; st < run; st += E) {
+            if (st + grp < run && c < D) {
+                const Cols4 x = load4(carry_head + (int64_t)(base + st + grp) * D + c);
 #pragma unroll
-    for (int j = 0; j < DV; ++j) {
-        const int c = lane + 64 * j;
-        tot[j] = c < D ? carry_tail[(int64_t)tile * D + c] : 0.f;
-    }
-    uint32_t t = tile + 1;
-    for (;;) {
-#pragma unroll
-        for (int j = 0; j < DV; ++j) {
-            const int c = lane + 64 * j;
-            if (c < D) tot[j] += carry_head[(int64_t)t * D + c];
+                for (int e = 0; e < 4; ++e) acc.v[e] += x.v[e];
+            }
         }
-        const uint32_t e = (t + 1) * SEG_TILE;
-        if (e >= s.n || s.keys[e - 1] != k || s.keys[e] != k) break;
-        ++t;
+        if (run < 64) break;
     }
-    float* dst = s.row_of(k);
 #pragma unroll
-    for (int j = 0; j < DV; ++j) {
-        const int c = lane + 64 * j;
-        if (c < D) dst[c] += tot[j];
+    for (int off = 1; off < E; off <<= 1) {  // group g adds group g + off (pairwise tree)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float y = __shfl_down(acc.v[e], off * L);
+            if ((grp & (2 * off - 1)) == 0) acc.v[e] += y;
+        }
+    }
+    if (grp == 0 && c < D) {
+        Cols4 tot = load4(carry_tail + (int64_t)tile * D + c);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) tot.v[e] += acc.v[e];
+        float* dst = (k < rbase ? grad_q + (int64_t)k * D : grad_r + (int64_t)(k - rbase) * D) + c;
+        Cols4 old = load4(dst);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) old.v[e] += tot.v[e];
+        store4(dst, old);
     }
 }
 
-template <typename T, typename ID, int L, bool VEC, int DV>
-hipError_t launch_reduce(const EmbedBwdArgs& a, const uint32_t* keys, const uint32_t* vals, const uint32_t* bag_of,
-                         uint32_t n, float* carry_head, float* carry_tail, hipStream_t st) {
-    SegCtx<T, ID> s;
+struct RedPtrs {
+    const uint32_t *keys, *vals, *bag_of, *qrow, *rrow;
+    float *carry_head, *carry_tail;
+};
+
+template <typename T, int L, bool MUL, bool BAGS>
+hipError_t launch_reduce(const EmbedBwdArgs& a, const RedPtrs& p, uint32_t n, hipStream_t st) {
+    SegCtx<T> s;
     s.a = a;
-    s.keys = keys;
-    s.vals = vals;
-    s.bag_of = bag_of;
+    s.keys = p.keys;
+    s.vals = p.vals;
+    s.bag_of = p.bag_of;
+    s.qrow = p.qrow;
+    s.rrow = p.rrow;
     s.n = n;
     s.sentinel = (uint32_t)a.F * (a.rows_q + a.m);
     s.rbase = (uint32_t)a.F * a.rows_q;
     const uint32_t ntiles = (n + SEG_TILE - 1) / SEG_TILE;
     const unsigned blocks = (ntiles + 3) / 4;
-    hipLaunchKernelGGL((k_seg_reduce<T, ID, L, VEC>), dim3(blocks), dim3(256), 0, st, s, carry_head, carry_tail);
+    hipLaunchKernelGGL((k_seg_reduce<T, L, MUL, BAGS>), dim3(blocks), dim3(256), 0, st, s, p.carry_head,
+                       p.carry_tail);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_seg_fixup<T, ID, DV>), dim3(blocks), dim3(256), 0, st, s, carry_head, carry_tail);
+    hipLaunchKernelGGL((k_seg_fixup<L>), dim3(blocks), dim3(256), 0, st, p.keys, n, s.sentinel, s.rbase, a.D,
+                       a.grad_q, a.grad_r, p.carry_head, p.carry_tail);
     return hipGetLastError();
 }
 
-// lanes per pair (4 columns each) and fix-up columns per lane for table width D <= 256
-template <typename T, typename ID, bool VEC>
-hipError_t launch_reduce_d(const EmbedBwdArgs& a, const uint32_t* keys, const uint32_t* vals, const uint32_t* bag_of,
-                           uint32_t n, float* ch, float* ct, hipStream_t st) {
+// lanes per pair (4 columns each) for table width D <= 256
+template <typename T, bool MUL, bool BAGS>
+hipError_t launch_reduce_d(const EmbedBwdArgs& a, const RedPtrs& p, uint32_t n, hipStream_t st) {
     const int q = (a.D + 3) / 4;
-    if (q <= 4) return launch_reduce<T, ID, 4, VEC, 1>(a, keys, vals, bag_of, n, ch, ct, st);
-    if (q <= 8) return launch_reduce<T, ID, 8, VEC, 1>(a, keys, vals, bag_of, n, ch, ct, st);
-    if (q <= 16) return launch_reduce<T, ID, 16, VEC, 1>(a, keys, vals, bag_of, n, ch, ct, st);
-    if (q <= 32) return launch_reduce<T, ID, 32, VEC, 2>(a, keys, vals, bag_of, n, ch, ct, st);
-    return launch_reduce<T, ID, 64, VEC, 4>(a, keys, vals, bag_of, n, ch, ct, st);
+    if (q <= 4) return launch_reduce<T, 4, MUL, BAGS>(a, p, n, st);
+    if (q <= 8) return launch_reduce<T, 8, MUL, BAGS>(a, p, n, st);
+    if (q <= 16) return launch_reduce<T, 16, MUL, BAGS>(a, p, n, st);
+    if (q <= 32) return launch_reduce<T, 32, MUL, BAGS>(a, p, n, st);
+    return launch_reduce<T, 64, MUL, BAGS>(a, p, n, st);
 }
 
 inline int key_bits(uint32_t maxkey) {
@@ -457,7 +474,7 @@ inline int key_bits(uint32_t maxkey) {
 
 }  // namespace
 
-EmbedBwdLayout embed_bwd_layout(int64_t nnz, int F, int rows_q, int m, int D, bool bags) {
+EmbedBwdLayout embed_bwd_layout(int64_t nnz, int F, int rows_q, int m, int D, bool bags, bool mul) {
     EmbedBwdLayout L;
     const uint64_t n = 2 * (uint64_t)nnz;
     const uint64_t ntiles = (n + RS_TILE - 1) / RS_TILE;
@@ -474,6 +491,8 @@ EmbedBwdLayout embed_bwd_layout(int64_t nnz, int F, int rows_q, int m, int D, bo
     L.keys1 = off; off += al(4 * n);
     L.vals1 = off; off += al(4 * n);
     L.bag_of = off; off += bags ? al(4 * (uint64_t)nnz) : 0;
+    L.qrow = off; off += mul ? al(4 * (uint64_t)nnz) : 0;
+    L.rrow = off; off += mul ? al(4 * (uint64_t)nnz) : 0;
     L.hist = off; off += al(4 * hist);
     L.sums = off; off += al(4 * sums);
     L.carry_head = off; off += al(4 * segtiles * (uint64_t)D);
@@ -489,6 +508,7 @@ struct EmbPtrs {
     uint32_t* keys[2];
     uint32_t* vals[2];
     uint32_t* bag_of;
+    uint32_t *qrow, *rrow;
     uint32_t* hist;
     uint32_t* sums;
     float* carry_head;
@@ -499,13 +519,16 @@ struct EmbPtrs {
 static EmbPtrs emb_ptrs(const EmbedBwdArgs& a, void* scratch) {
     EmbPtrs p;
     const bool bags = a.offsets != nullptr;
-    p.L = embed_bwd_layout(a.nnz, a.F, a.rows_q, a.m, a.D, bags);
+    const bool mul = a.combine == 0;
+    p.L = embed_bwd_layout(a.nnz, a.F, a.rows_q, a.m, a.D, bags, mul);
     char* base = (char*)scratch;
     p.keys[0] = (uint32_t*)(base + p.L.keys0);
     p.keys[1] = (uint32_t*)(base + p.L.keys1);
     p.vals[0] = (uint32_t*)(base + p.L.vals0);
     p.vals[1] = (uint32_t*)(base + p.L.vals1);
     p.bag_of = bags ? (uint32_t*)(base + p.L.bag_of) : nullptr;
+    p.qrow = mul ? (uint32_t*)(base + p.L.qrow) : nullptr;
+    p.rrow = mul ? (uint32_t*)(base + p.L.rrow) : nullptr;
     p.hist = (uint32_t*)(base + p.L.hist);
     p.sums = (uint32_t*)(base + p.L.sums);
     p.carry_head = (float*)(base + p.L.carry_head);
@@ -520,9 +543,13 @@ hipError_t launch_emb_keys(const EmbedBwdArgs& a, bool ids64, void* scratch, hip
     const int64_t units = bags ? a.batch * a.F : a.nnz;
     int64_t blocks = (units + 255) / 256;
     if (blocks > 65536) blocks = 65536;
-#define RDCN_KEYS(ID, BG) hipLaunchKernelGGL((k_emb_keys<ID, BG>), dim3((unsigned)blocks), dim3(256), 0, st, a, P.keys[0], P.vals[0], P.bag_of)
-    if (ids64) { if (bags) RDCN_KEYS(int64_t, true); else RDCN_KEYS(int64_t, false); }
-    else       { if (bags) RDCN_KEYS(int32_t, true); else RDCN_KEYS(int32_t, false); }
+#define RDCN_KEYS(ID, BG, MU)                                                                                   \
+    hipLaunchKernelGGL((k_emb_keys<ID, BG, MU>), dim3((unsigned)blocks), dim3(256), 0, st, a, P.keys[0], P.vals[0], \
+                       P.bag_of, P.qrow, P.rrow)
+#define RDCN_KEYS_M(ID, BG) do { if (a.combine == 0) RDCN_KEYS(ID, BG, true); else RDCN_KEYS(ID, BG, false); } while (0)
+    if (ids64) { if (bags) RDCN_KEYS_M(int64_t, true); else RDCN_KEYS_M(int64_t, false); }
+    else       { if (bags) RDCN_KEYS_M(int32_t, true); else RDCN_KEYS_M(int32_t, false); }
+#undef RDCN_KEYS_M
 #undef RDCN_KEYS
     return hipGetLastError();
 }
@@ -551,20 +578,19 @@ hipError_t launch_emb_sort(const EmbedBwdArgs& a, void* scratch, hipStream_t st)
     return hipSuccess;
 }
 
-hipError_t launch_emb_reduce(const EmbedBwdArgs& a, bool bf16, bool ids64, void* scratch, hipStream_t st) {
+hipError_t launch_emb_reduce(const EmbedBwdArgs& a, bool bf16, void* scratch, hipStream_t st) {
     if (a.nnz == 0 || a.F == 0) return hipSuccess;
     const EmbPtrs P = emb_ptrs(a, scratch);
     const uint32_t n = (uint32_t)(2 * a.nnz);
     const int cur = P.L.passes & 1;
-    // 16-byte column groups: D and d are multiples of 4 (checked at create), so only
-    // the base pointers decide
-    const bool vec = (((uintptr_t)a.grad_x0 | (uintptr_t)a.grad_q | (uintptr_t)a.grad_r) & 15) == 0 &&
-                     a.D % 4 == 0 && a.d % 4 == 0;
-#define RDCN_RED(T, ID) \
-    return vec ? launch_reduce_d<T, ID, true>(a, P.keys[cur], P.vals[cur], P.bag_of, n, P.carry_head, P.carry_tail, st) \
-               : launch_reduce_d<T, ID, false>(a, P.keys[cur], P.vals[cur], P.bag_of, n, P.carry_head, P.carry_tail, st)
-    if (bf16) { if (ids64) RDCN_RED(bf16_t, int64_t); else RDCN_RED(bf16_t, int32_t); }
-    else      { if (ids64) RDCN_RED(float, int64_t); else RDCN_RED(float, int32_t); }
+    const RedPtrs rp = {P.keys[cur], P.vals[cur], P.bag_of, P.qrow, P.rrow, P.carry_head, P.carry_tail};
+    const bool mul = a.combine == 0, bags = a.offsets != nullptr;
+#define RDCN_RED(T) do {                                                  \
+        if (mul) return bags ? launch_reduce_d<T, true, true>(a, rp, n, st) : launch_reduce_d<T, true, false>(a, rp, n, st); \
+        return bags ? launch_reduce_d<T, false, true>(a, rp, n, st) : launch_reduce_d<T, false, false>(a, rp, n, st);      \
+    } while (0)
+    if (bf16) RDCN_RED(bf16_t);
+    RDCN_RED(float);
 #undef RDCN_RED
 }
 
