@@ -105,6 +105,49 @@ def roofline_for(name: str, work: tuple, avg_s: float, bf16: bool) -> dict:
     return {"bound": "hbm", "achieved": nbytes / avg_s / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
 
 
+# Source files whose text determines each kernel class (a counter reading is only
+# valid for the code it was taken on).
+KERNEL_SOURCES = {
+    "fwd_attention": ["attention.hip", "device_common.h"],
+    "bwd_attention": ["attention.hip", "device_common.h"],
+    "gather": ["gather.hip", "device_common.h"],
+    "bwd_pointwise": ["pointwise.hip", "device_common.h"],
+    "emb_keys": ["embed_bwd.hip", "device_common.h"],
+    "emb_sort": ["embed_bwd.hip", "device_common.h"],
+    "emb_reduce": ["embed_bwd.hip", "device_common.h"],
+}
+for _k in ("fwd_down_gemm", "fwd_up_gemm", "bwd_gu_gemm", "bwd_gh_gemm", "bwd_gw_gemm", "bwd_gx_gemm"):
+    KERNEL_SOURCES[_k] = ["gemm.hip", "gemm.h", "device_common.h"]
+
+
+def sources_sha256(kernel: str) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES.get(kernel, []):
+        with open(os.path.join(ROOT, "paper_2402_06859_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` on `workload` from the counter summaries
+    under profiles/ (lines 'traffic: {json}'), or None when there is none or the
+    kernel's sources changed since the counters were taken."""
+    import glob
+    if kernel not in KERNEL_SOURCES:
+        return None
+    sha = sources_sha256(kernel)
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        with open(path) as fh:
+            for line in fh:
+                if not line.startswith("traffic: "):
+                    continue
+                rec = json.loads(line[len("traffic: "):])
+                if rec.get("kernel") == kernel and rec.get("workload") == workload and rec.get("sha256") == sha:
+                    return float(rec["bytes_per_launch"])
+    return None
+
+
 def cpu_baseline(wl, target_s: float) -> dict:
     """The oracle (plain single-threaded C) timed on a sub-batch sized to about
     `target_s` seconds: one step = gather + forward + backward (which recomputes
@@ -208,7 +251,7 @@ def main():
     avg_s = dom[0] / dom[1] / 1e3
     roof = roofline_for(dominant, work[dominant], avg_s, wl.dtype == "bf16")
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic(dominant, wl.name)
     roof["kernel"] = dominant
     roof["avg_us"] = avg_s * 1e6
     roof["launches"] = dom[1]

@@ -13,6 +13,8 @@
 //
 // One workgroup per sample; k and v (and, in the backward column pass, the
 // per-row coefficients) are staged in LDS as floats and read as broadcasts.
+#include <type_traits>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -224,25 +226,92 @@ __device__ __forceinline__ float wave_min(float x) {
     return x;
 }
 
-// Row n (< nx, else zero) of an f16 matrix with row stride ld, entries j0 .. j0+7.
+// The X^T / Y^T operand matrices (a few rows of f16, row stride ld, ld a multiple
+// of 32) keep entry j of row n in 8-element chunk (j / 8) XOR (n & 3): the rows one
+// fragment read touches then fall in different LDS banks.
+__device__ __forceinline__ int xoff(int n, int j, int ld) { return n * ld + ((((j >> 3) ^ n) & 3) | ((j >> 3) & ~3)) * 8 + (j & 7); }
+
+// Row n (< nx, else zero) of an operand matrix, entries j0 .. j0+7 (j0 % 8 == 0).
 __device__ __forceinline__ f16x8_t xfrag(const _Float16* sx, int ld, int n, int nx, int j0) {
     if (n >= nx) return f16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-    return __builtin_bit_cast(f16x8_t, *(const u32x4_t*)(sx + n * ld + j0));
+    return __builtin_bit_cast(f16x8_t, *(const u32x4_t*)(sx + xoff(n, j0, ld)));
 }
 
-// e for one row (c, m) and 8 keys kv[0..7], packed as the B fragment.
+// Key order inside one 32-key chunk. Lane (g, n)'s 8 K slots of a fragment hold
+// keys j0 + 4 g + t (t < 4) and j0 + 16 + 4 g + (t - 4) (t >= 4): the layout in
+// which two 16x16x16 MFMA outputs (keys j0 .. +15 and j0 + 16 .. +31) leave the
+// exponent arguments. Everything indexed by key within a chunk (X^T fragments,
+// the LDS e block) follows it; sums over K do not depend on the order.
+typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ u32x4_t pack_e(const float (&e)[8]) {
+    return u32x4_t{pk_f16(e[0], e[1]), pk_f16(e[2], e[3]), pk_f16(e[4], e[5]), pk_f16(e[6], e[7])};
+}
+
+// e for one row (c, m) and the lane's 8 keys kv[0..7] (in the order above),
+// exponent arguments by FMA.
 __device__ __forceinline__ u32x4_t efrag(float c, float m, const float* kv) {
     float e[8];
 #pragma unroll
     for (int t = 0; t < 8; ++t) e[t] = __builtin_amdgcn_exp2f(fmaf(c, kv[t], m));
-    return u32x4_t{pk_f16(e[0], e[1]), pk_f16(e[2], e[3]), pk_f16(e[4], e[5]), pk_f16(e[6], e[7])};
+    return pack_e(e);
 }
+
+// Exponent arguments on the matrix cores: x = c k + m as a 16 (keys) x 16 (rows)
+// product with K = 5 of 16 slots used, from f16 hi + lo parts of c, k and m:
+//   keys (A, lane (g, n), key n):   g = 0: (k_hi, k_hi, 1, 1)   g = 1: (k_lo, 0, 0, 0)
+//   rows (B, lane (g, n), row n):   (c_hi, c_lo, m_hi, m_lo) for every g
+// giving c_hi k_hi + c_lo k_hi + m_hi + m_lo + c_hi k_lo: every product is exact in
+// the float accumulator and only c_lo k_lo (relative 2^-22 of c k) is left out.
+__device__ __forceinline__ f16x4_t key_frag(float k, int g) {
+    const _Float16 hi = (_Float16)k, lo = (_Float16)(k - (float)hi);
+    if (g == 0) return f16x4_t{hi, hi, (_Float16)1.f, (_Float16)1.f};
+    if (g == 1) return f16x4_t{lo, (_Float16)0.f, (_Float16)0.f, (_Float16)0.f};
+    return f16x4_t{(_Float16)0.f, (_Float16)0.f, (_Float16)0.f, (_Float16)0.f};
+}
+
+__device__ __forceinline__ f16x4_t row_rec(float c, float m) {
+    const _Float16 ch = (_Float16)c, mh = (_Float16)m;
+    return f16x4_t{ch, (_Float16)(c - (float)ch), mh, (_Float16)(m - (float)mh)};
+}
+
+__device__ __forceinline__ u32x4_t efrag_mfma(const f16x4_t& k0, const f16x4_t& k1, const f16x4_t& rec) {
+    const f32x4_t z = {0.f, 0.f, 0.f, 0.f};
+    const f32x4_t x0 = __builtin_amdgcn_mfma_f32_16x16x16f16(k0, rec, z, 0, 0, 0);
+    const f32x4_t x1 = __builtin_amdgcn_mfma_f32_16x16x16f16(k1, rec, z, 0, 0, 0);
+    float e[8];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        e[t] = __builtin_amdgcn_exp2f(x0[t]);
+        e[4 + t] = __builtin_amdgcn_exp2f(x1[t]);
+    }
+    return pack_e(e);
+}
+
+// X^T fragment of row n (< nx, else zero) for the chunk at j0, keys in the order above.
+__device__ __forceinline__ f16x8_t xfrag_perm(const _Float16* sx, int ld, int n, int nx, int j0, int g) {
+    if (n >= nx) return f16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    const f16x4_t lo = *(const f16x4_t*)(sx + xoff(n, j0 + 4 * g, ld));
+    const f16x4_t hi = *(const f16x4_t*)(sx + xoff(n, j0 + 16 + 4 * g, ld));
+    return f16x8_t{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+}
+
+// The lane's 8 keys (order above) from the float key array.
+__device__ __forceinline__ void keys_perm(const float* sk, int j0, int g, float (&kv)[8]) {
+    *(u32x4_t*)kv = *(const u32x4_t*)(sk + j0 + 4 * g);
+    *(u32x4_t*)(kv + 4) = *(const u32x4_t*)(sk + j0 + 16 + 4 * g);
+}
+
+// Exponent arguments go through the matrix cores when every c, m and k of the
+// wave fits f16 with margin; otherwise (extreme logits) through FMAs. The forward
+// and the backward take the same decision from the same values.
+constexpr float ATT_F16_SAFE = 16384.f;
 
 // Write quantity x / s as an f16 hi + lo pair into rows (row, row + 1) of X^T.
 __device__ __forceinline__ void put_pair(_Float16* sx, int ld, int row, int j, float xs) {
     const _Float16 h = (_Float16)xs;
-    sx[row * ld + j] = h;
-    sx[(row + 1) * ld + j] = (_Float16)(xs - (float)h);
+    sx[xoff(row, j, ld)] = h;
+    sx[xoff(row + 1, j, ld)] = (_Float16)(xs - (float)h);
 }
 
 // Which sample and which block of row tiles a wave owns.
@@ -269,32 +338,86 @@ __device__ __forceinline__ WaveRows wave_rows(int W, int ntile) {
     return o;
 }
 
-// Keys of the sample into sk (padding keys 0), their range, and the row constants
-// c_i = q_i log2(e) / tau, m_i = -c_i k*_i of the wave's rows (lane's row in tile t).
-__device__ __forceinline__ void key_setup(const float* pk, int r, int rpad, float* sk, float& kmin, float& kmax,
-                                          int lane) {
+// Setup reads every per-sample operand a lane needs with one batch of loads
+// (indices clamped to the valid range, so each load is issued; values past r are
+// replaced by zeros), then works from registers.
+//   keys / values: lane holds j = 64 u + lane, u < KPL (KPL * 64 >= rpad)
+//   the wave's rows: lane holds il = 64 u + lane, u < RPL (RPL * 64 >= 16 NT)
+template <int KPL>
+__device__ __forceinline__ void load_keys(const float* pv, const float* pk, int r, int lane, float (&k)[KPL],
+                                          float (&v)[KPL]) {
+#pragma unroll
+    for (int u = 0; u < KPL; ++u) {
+        const int j = 64 * u + lane;
+        const int jc = j < r ? j : r - 1;
+        k[u] = pk[jc];
+        v[u] = pv[jc];
+    }
+#pragma unroll
+    for (int u = 0; u < KPL; ++u) {
+        if (64 * u + lane >= r) k[u] = v[u] = 0.f;
+    }
+}
+
+template <int NT>
+struct RowsPerLane {
+    static constexpr int value = (16 * NT + 63) / 64;
+};
+
+// rows t0 * 16 + il of quantity x (zero past r or past the rows in range)
+template <int RPL>
+__device__ __forceinline__ void load_rows(const float* x, int r, int t0, int nrows, int lane, float (&out)[RPL]) {
+#pragma unroll
+    for (int u = 0; u < RPL; ++u) {
+        const int il = 64 * u + lane, i = t0 * 16 + il;
+        out[u] = x[i < r ? i : r - 1];
+    }
+#pragma unroll
+    for (int u = 0; u < RPL; ++u) {
+        const int il = 64 * u + lane, i = t0 * 16 + il;
+        if (!(il < nrows && i < r)) out[u] = 0.f;
+    }
+}
+
+// key range over the keys held (valid keys only)
+template <int KPL>
+__device__ __forceinline__ void key_range(const float (&k)[KPL], int r, int lane, float& kmin, float& kmax) {
     float lo = INFINITY, hi = -INFINITY;
-    for (int j = lane; j < rpad; j += 64) {
-        const float kj = j < r ? pk[j] : 0.f;
-        sk[j] = kj;
-        if (j < r) {
-            lo = fminf(lo, kj);
-            hi = fmaxf(hi, kj);
+#pragma unroll
+    for (int u = 0; u < KPL; ++u) {
+        if (64 * u + lane < r) {
+            lo = fminf(lo, k[u]);
+            hi = fmaxf(hi, k[u]);
         }
     }
     kmin = wave_min(lo);
     kmax = wave_max(hi);
 }
 
-// (c_i, m_i) of rows t0 * 16 + il, il < 16 * NT, into scm[il] (rows past r: c = m = 0).
-template <int NT>
-__device__ __forceinline__ void row_consts(const float* pq, int r, int t0, int lane, float inv_tau, float kmin,
-                                           float kmax, float2* scm) {
-    for (int il = lane; il < 16 * NT; il += 64) {
-        const int i = t0 * 16 + il;
-        const float ci = i < r ? pq[i] * (LOG2E * inv_tau) : 0.f;
-        scm[il] = make_float2(ci, i < r ? -(ci * (ci >= 0.f ? kmax : kmin)) : 0.f);
+// (c_i, m_i) = (q_i log2(e) / tau, -c_i k*_i) of rows il = 64 u + lane < 16 NT into
+// scm[il] (rows past r: c = m = 0; q holds zeros there): as floats, or, when every
+// c, m of rows il < nrows and every key fits f16 (returned, wave-uniform), as the
+// f16 record row_rec of the matrix-core path.
+template <int NT, int RPL>
+__device__ __forceinline__ bool put_row_consts(const float (&q)[RPL], int lane, int nrows, float inv_tau,
+                                               float kmin, float kmax, float2* scm) {
+    float c[RPL], m[RPL], big = fmaxf(fabsf(kmin), fabsf(kmax));
+#pragma unroll
+    for (int u = 0; u < RPL; ++u) {
+        c[u] = q[u] * (LOG2E * inv_tau);
+        m[u] = -(c[u] * (c[u] >= 0.f ? kmax : kmin));
+        if (64 * u + lane < nrows) big = fmaxf(big, fmaxf(fabsf(c[u]), fabsf(m[u])));
     }
+    const bool fast = wave_max(big) < ATT_F16_SAFE;  // false for NaN too
+#pragma unroll
+    for (int u = 0; u < RPL; ++u) {
+        const int il = 64 * u + lane;
+        if (il < 16 * NT) {
+            if (fast) *(f16x4_t*)(scm + il) = row_rec(c[u], m[u]);
+            else scm[il] = make_float2(c[u], m[u]);
+        }
+    }
+    return fast;
 }
 
 // LDS words per wave of the forward: keys, row constants, X^T (3 rows).
@@ -302,7 +425,8 @@ __host__ __device__ constexpr int attn_fwd_wave_floats(int rpad) { return rpad +
 
 // NT: tiles computed per wave (a power of two >= the tiles it owns; the extra ones
 // are computed on harmless row constants and discarded).
-template <typename T, int NT>
+// KB: 256-key batches a lane's registers cover (4 KB >= rpad / 64).
+template <typename T, int NT, int KB>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_attn_fwd_mfma(int64_t B, int r, int rpad, int W, float alpha, float beta,
                                                       float inv_tau, const float* __restrict__ P, int64_t ldp,
                                                       T* __restrict__ H, T* __restrict__ H2, int64_t ldh,
@@ -316,45 +440,77 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     float2* scm = (float2*)(sk + rpad);                       // [16 ATT_NT] row constants
     _Float16* sx = (_Float16*)(scm + 16 * ATT_NT);            // X^T: 3 rows x rpad (v hi, v lo, 1)
     const float* pv = P + wr.b * ldp;
+    constexpr int KPL = 4 * KB;
+    constexpr int RPL = RowsPerLane<NT>::value;
+    float kr[KPL], vr[KPL], qr[RPL];
+    load_keys<KPL>(pv, pv + 2 * r, r, lane, kr, vr);
+    load_rows<RPL>(pv + r, r, wr.t0, 16 * NT, lane, qr);
     float kmin, kmax;
-    key_setup(pv + 2 * r, r, rpad, sk, kmin, kmax, lane);
+    key_range<KPL>(kr, r, lane, kmin, kmax);
     float vmax = 0.f;
-    for (int j = lane; j < r; j += 64) vmax = fmaxf(vmax, fabsf(pv[j]));
+#pragma unroll
+    for (int u = 0; u < KPL; ++u) vmax = fmaxf(vmax, fabsf(vr[u]));
     const float vs = pow2_ceil(wave_max(vmax));
-    for (int j = lane; j < rpad; j += 64) {
-        put_pair(sx, rpad, 0, j, j < r ? pv[j] / vs : 0.f);
-        sx[2 * rpad + j] = (_Float16)(j < r ? 1.f : 0.f);
+    const int ldx = rpad;
+#pragma unroll
+    for (int u = 0; u < KPL; ++u) {
+        const int j = 64 * u + lane;
+        if (j < rpad) {
+            sk[j] = kr[u];
+            put_pair(sx, ldx, 0, j, vr[u] / vs);
+            sx[xoff(2, j, ldx)] = (_Float16)(j < r ? 1.f : 0.f);
+        }
     }
-    row_consts<NT>(pv + r, r, wr.t0, lane, inv_tau, kmin, kmax, scm);
+    const bool fast = put_row_consts<NT, RPL>(qr, lane, 16 * wr.nt, inv_tau, kmin, kmax, scm);
     __builtin_amdgcn_wave_barrier();
     const int g = lane >> 4, n = lane & 15;
     f32x4_t acc[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int j0 = 0; j0 < rpad; j0 += 32) {
-        const int jj = j0 + 8 * g;
-        float kv[8];
-        *(u32x4_t*)kv = *(const u32x4_t*)(sk + jj);
-        *(u32x4_t*)(kv + 4) = *(const u32x4_t*)(sk + jj + 4);
-        const f16x8_t a = xfrag(sx, rpad, n, 3, jj);
+    auto chunks = [&](auto fast_c) {
+        constexpr bool FAST = decltype(fast_c)::value;
+        for (int j0 = 0; j0 < rpad; j0 += 32) {
+            float kv[8];
+            f16x4_t k0, k1;
+            if (FAST) {
+                k0 = key_frag(sk[j0 + n], g);
+                k1 = key_frag(sk[j0 + 16 + n], g);
+            } else {
+                keys_perm(sk, j0, g, kv);
+            }
+            const f16x8_t a = xfrag_perm(sx, ldx, n, 3, j0, g);
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const float2 cm = scm[16 * t + n];
-            acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, __builtin_bit_cast(f16x8_t, efrag(cm.x, cm.y, kv)),
-                                                            acc[t], 0, 0, 0);
+            for (int t = 0; t < NT; ++t) {
+                u32x4_t e;
+                if (FAST) {
+                    e = efrag_mfma(k0, k1, *(const f16x4_t*)(scm + 16 * t + n));
+                } else {
+                    const float2 cm = scm[16 * t + n];
+                    e = efrag(cm.x, cm.y, kv);
+                }
+                acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, __builtin_bit_cast(f16x8_t, e), acc[t], 0, 0, 0);
+            }
         }
-    }
+    };
+    if (fast) chunks(std::true_type{});
+    else chunks(std::false_type{});
     if (lane < 16) {
         float* so = stats + wr.b * 2 * (int64_t)r;
+        float vi[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {  // all loads first
+            const int i = (wr.t0 + t) * 16 + lane;
+            vi[t] = pv[i < r ? i : r - 1];
+        }
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             const int i = (wr.t0 + t) * 16 + lane;
             if (t < wr.nt && i < r) {
                 const float z = acc[t].z;
                 const float o = (acc[t].x + acc[t].y) * vs / z;
-                const float hv = beta * pv[i] + alpha * o;
+                const float hv = beta * vi[t] + alpha * o;
                 st<T>::store(H + wr.b * ldh + i, hv);
-                if (H2) st<T>::store(H2 + wr.b * ldh + i, hv - st<T>::load(H + wr.b * ldh + i));
+                if (H2) st<T>::store(H2 + wr.b * ldh + i, hv - st<T>::round(hv));
                 so[i] = o;
                 so[r + i] = z;
             }
@@ -405,11 +561,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     if (W == 1 && !live) return;  // with W > 1 every wave takes part in the barriers
     constexpr int RW = 16 * ATT_NT;
     float* sk = smem + (wave / W) * attn_bwd_sample_floats(rpad);  // [rpad] keys (shared by the sample's waves)
-    _Float16* sx = (_Float16*)(sk + rpad);                           // 4 x rpad: v k hi/lo, k hi/lo
+    _Float16* sx = (_Float16*)(sk + rpad);                           // 4 rows: v k hi/lo, k hi/lo
     float* pw = smem + (4 / W) * attn_bwd_sample_floats(rpad) + wave * attn_bwd_wave_floats(W);
     float2* scm = (float2*)pw;                   // [RW] row constants
-    _Float16* sy = (_Float16*)(scm + RW);        // 6 x RW: a hi/lo, a o hi/lo, go/Z hi/lo
+    _Float16* sy = (_Float16*)(scm + RW);        // 6 rows: a hi/lo, a o hi/lo, go/Z hi/lo
     _Float16* se = sy + 6 * RW;                  // 32 x 32 e block
+    const int ldx = rpad, ldy = RW;
     float* slot = pw + attn_bwd_slot_offset();   // 2 x 96 column partials (W > 1)
     const int g = lane >> 4, n = lane & 15;
     const int64_t b = live ? wr.b : 0;
@@ -418,144 +575,182 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     const float* pk = pv + 2 * r;
     const float* gh = GH + b * ldg;
     const float* so = stats + b * 2 * (int64_t)r;
-    // every wave reduces over all keys (from memory); each writes its share of the
-    // sample's key arrays
-    float lo = INFINITY, hi = -INFINITY, mvk = 0.f, mk = 0.f;
-    for (int j = lane; j < r; j += 64) {
-        const float kj = pk[j];
-        lo = fminf(lo, kj);
-        hi = fmaxf(hi, kj);
-        mvk = fmaxf(mvk, fabsf(pv[j] * kj));
-        mk = fmaxf(mk, fabsf(kj));
+    constexpr int KPL = W == 1 ? 4 : 16;
+    constexpr int RPL = RowsPerLane<NT>::value;
+    float kr[KPL], vr[KPL], qr[RPL], ghr[RPL], orr[RPL], zr[RPL];
+    load_keys<KPL>(pv, pk, r, lane, kr, vr);
+    load_rows<RPL>(pq, r, wr.t0, 16 * wr.nt, lane, qr);
+    load_rows<RPL>(gh, r, wr.t0, 16 * wr.nt, lane, ghr);
+    load_rows<RPL>(so, r, wr.t0, 16 * wr.nt, lane, orr);
+    load_rows<RPL>(so + r, r, wr.t0, 16 * wr.nt, lane, zr);
+    // every wave reduces over all keys; each writes its share of the sample's key arrays
+    float kmin, kmax;
+    key_range<KPL>(kr, r, lane, kmin, kmax);
+    float mvk = 0.f, mk = 0.f;
+#pragma unroll
+    for (int u = 0; u < KPL; ++u) {
+        mvk = fmaxf(mvk, fabsf(vr[u] * kr[u]));
+        mk = fmaxf(mk, fabsf(kr[u]));
     }
-    const float kmin = wave_min(lo), kmax = wave_max(hi);
     const float vks = pow2_ceil(wave_max(mvk)), ks = pow2_ceil(wave_max(mk));
-    for (int j = lane + 64 * wr.w; j < rpad; j += 64 * W) {
-        const float kj = j < r ? pk[j] : 0.f, vj = j < r ? pv[j] : 0.f;
-        sk[j] = kj;
-        put_pair(sx, rpad, 0, j, vj * kj / vks);
-        put_pair(sx, rpad, 2, j, kj / ks);
-    }
-    // per-row coefficients of the wave's rows
-    float ma = 0.f, mb = 0.f, mc = 0.f;
-    for (int il = lane; il < RW; il += 64) {
-        const int i = wr.t0 * 16 + il;
-        if (il < wr.nt * 16 && i < r) {
-            const float go = alpha * gh[i], rz = 1.0f / so[r + i];
-            const float a = go * pq[i] * rz * inv_tau;
-            ma = fmaxf(ma, fabsf(a));
-            mb = fmaxf(mb, fabsf(a * so[i]));
-            mc = fmaxf(mc, fabsf(go * rz));
+#pragma unroll
+    for (int u = 0; u < KPL; ++u) {
+        const int j = 64 * u + lane;
+        if (j < rpad && u % W == wr.w) {
+            sk[j] = kr[u];
+            put_pair(sx, ldx, 0, j, vr[u] * kr[u] / vks);
+            put_pair(sx, ldx, 2, j, kr[u] / ks);
         }
+    }
+    // per-row coefficients of the wave's rows (zero past its rows)
+    float ca[RPL], cb[RPL], cg[RPL];
+    float ma = 0.f, mb = 0.f, mc = 0.f;
+#pragma unroll
+    for (int u = 0; u < RPL; ++u) {
+        const float go = alpha * ghr[u], rz = zr[u] != 0.f ? 1.0f / zr[u] : 0.f;
+        ca[u] = go * qr[u] * rz * inv_tau;
+        cb[u] = ca[u] * orr[u];
+        cg[u] = go * rz;
+        ma = fmaxf(ma, fabsf(ca[u]));
+        mb = fmaxf(mb, fabsf(cb[u]));
+        mc = fmaxf(mc, fabsf(cg[u]));
     }
     const float as = pow2_ceil(wave_max(ma)), bs = pow2_ceil(wave_max(mb)), cs = pow2_ceil(wave_max(mc));
-    for (int il = lane; il < RW; il += 64) {
-        const int i = wr.t0 * 16 + il;
-        float a = 0.f, ao = 0.f, gz = 0.f;
-        if (il < wr.nt * 16 && i < r) {
-            const float go = alpha * gh[i], rz = 1.0f / so[r + i];
-            a = go * pq[i] * rz * inv_tau;
-            ao = a * so[i];
-            gz = go * rz;
+#pragma unroll
+    for (int u = 0; u < RPL; ++u) {
+        const int il = 64 * u + lane;
+        if (il < 16 * NT) {
+            put_pair(sy, ldy, 0, il, ca[u] / as);
+            put_pair(sy, ldy, 2, il, cb[u] / bs);
+            put_pair(sy, ldy, 4, il, cg[u] / cs);
         }
-        put_pair(sy, RW, 0, il, a / as);
-        put_pair(sy, RW, 2, il, ao / bs);
-        put_pair(sy, RW, 4, il, gz / cs);
     }
-    row_consts<NT>(pq, r, wr.t0, lane, inv_tau, kmin, kmax, scm);
+    // row constants from q (load_rows zeroed q past the wave's rows; rows of
+    // other waves only feed discarded tiles)
+    const bool fast = put_row_consts<NT, RPL>(qr, lane, 16 * wr.nt, inv_tau, kmin, kmax, scm);
     if (W > 1) __syncthreads();
     else __builtin_amdgcn_wave_barrier();
 
     f32x4_t acc[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int chunk = 0, j0 = 0; j0 < rpad; j0 += 32, ++chunk) {
-        const int jj = j0 + 8 * g;
-        float kv[8];
-        *(u32x4_t*)kv = *(const u32x4_t*)(sk + jj);
-        *(u32x4_t*)(kv + 4) = *(const u32x4_t*)(sk + jj + 4);
-        const f16x8_t ax = xfrag(sx, rpad, n, 4, jj);
-        f32x4_t col[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-        for (int p = 0; p < NT / 2; ++p) {
-            {
-                // the wave's LDS operations run in order, so this pair's writes
-                // follow the previous pair's transposed reads of the same block
+    auto chunks = [&](auto fast_c) {
+        constexpr bool FAST = decltype(fast_c)::value;
+        for (int chunk = 0, j0 = 0; j0 < rpad; j0 += 32, ++chunk) {
+            float kv[8];
+            f16x4_t k0, k1;
+            if (FAST) {
+                k0 = key_frag(sk[j0 + n], g);
+                k1 = key_frag(sk[j0 + 16 + n], g);
+            } else {
+                keys_perm(sk, j0, g, kv);
+            }
+            const f16x8_t ax = xfrag_perm(sx, ldx, n, 4, j0, g);
+            // operands of this chunk's column epilogue, loaded now so the loads overlap the chunk
+            float ev[2], eg[2];
+    #pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int j = W == 1 ? j0 + 16 * h + n : j0 + (lane & 31);
+                const int jc = j < r ? j : r - 1;
+                ev[h] = pv[jc];
+                eg[h] = gh[jc];
+            }
+            f32x4_t col[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
+    #pragma unroll
+            for (int p = 0; p < NT / 2; ++p) {
+                // the wave's LDS operations run in order, so this pair's writes follow
+                // the previous pair's transposed reads of the same block
                 __builtin_amdgcn_wave_barrier();
-                _Float16* eb = se;
-#pragma unroll
+    #pragma unroll
                 for (int q = 0; q < 2; ++q) {
                     const int t = 2 * p + q;
-                    const float2 cm = scm[16 * t + n];
-                    const u32x4_t e = efrag(cm.x, cm.y, kv);
-                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax, __builtin_bit_cast(f16x8_t, e), acc[t], 0,
-                                                                    0, 0);
-                    const int row = 16 * q + n;
-                    *(u32x4_t*)(eb + row * 32 + ((g ^ ((row >> 2) & 3)) * 8)) = e;
+                    u32x4_t e;
+                    if (FAST) {
+                        e = efrag_mfma(k0, k1, *(const f16x4_t*)(scm + 16 * t + n));
+                    } else {
+                        const float2 cm = scm[16 * t + n];
+                        e = efrag(cm.x, cm.y, kv);
+                    }
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax, __builtin_bit_cast(f16x8_t, e), acc[t], 0, 0, 0);
+                    // keys 4 g .. +3 and 16 + 4 g .. +3 of row 16 q + n, into their block chunks
+                    const int row = 16 * q + n, sw = (row >> 2) & 3;
+                    typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+                    *(u32x2_t*)(se + row * 32 + (((g >> 1) ^ sw) * 8) + 4 * (g & 1)) = u32x2_t{e.x, e.y};
+                    *(u32x2_t*)(se + row * 32 + (((2 + (g >> 1)) ^ sw) * 8) + 4 * (g & 1)) = u32x2_t{e.z, e.w};
                 }
-                const f16x8_t ay = xfrag(sy, RW, n, 6, 32 * p + 8 * g);
-#pragma unroll
+                const f16x8_t ay = xfrag(sy, ldy, n, 6, 32 * p + 8 * g);
+    #pragma unroll
                 for (int h = 0; h < 2; ++h)
-                    col[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ay, e_transposed(eb, h, lane), col[h], 0, 0, 0);
+                    col[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ay, e_transposed(se, h, lane), col[h], 0, 0, 0);
             }
-        }
-        // lanes 0..15: (a hi, a lo, a o hi, a o lo) of key n (+16 h); lanes 16..31: (go/Z hi, lo)
-        if (W == 1) {
-            if (lane < 32) {
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const int j = j0 + 16 * h + n;
-                    if (j < r) {
-                        if (lane < 16) {
-                            const float c1 = (col[h].x + col[h].y) * as, c2 = (col[h].z + col[h].w) * bs;
-                            st<T>::store(GP + b * ldgp + 2 * r + j, pv[j] * c1 - c2);
-                        } else {
-                            st<T>::store(GP + b * ldgp + j, beta * gh[j] + (col[h].x + col[h].y) * cs);
+            // lanes 0..15: (a hi, a lo, a o hi, a o lo) of key n (+16 h); lanes 16..31: (go/Z hi, lo)
+            if (W == 1) {
+                if (lane < 32) {
+    #pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int j = j0 + 16 * h + n;
+                        if (j < r) {
+                            if (lane < 16) {
+                                const float c1 = (col[h].x + col[h].y) * as, c2 = (col[h].z + col[h].w) * bs;
+                                st<T>::store(GP + b * ldgp + 2 * r + j, ev[h] * c1 - c2);
+                            } else {
+                                st<T>::store(GP + b * ldgp + j, beta * eg[h] + (col[h].x + col[h].y) * cs);
+                            }
                         }
                     }
                 }
-            }
-        } else {
-            float* sl = slot + (chunk & 1) * 96;
-            if (lane < 32) {
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    if (lane < 16) {
-                        sl[16 * h + n] = (col[h].x + col[h].y) * as;
-                        sl[32 + 16 * h + n] = (col[h].z + col[h].w) * bs;
-                    } else {
-                        sl[64 + 16 * h + n] = (col[h].x + col[h].y) * cs;
+            } else {
+                float* sl = slot + (chunk & 1) * 96;
+                if (lane < 32) {
+    #pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        if (lane < 16) {
+                            sl[16 * h + n] = (col[h].x + col[h].y) * as;
+                            sl[32 + 16 * h + n] = (col[h].z + col[h].w) * bs;
+                        } else {
+                            sl[64 + 16 * h + n] = (col[h].x + col[h].y) * cs;
+                        }
+                    }
+                }
+                __syncthreads();
+                // the sample's first wave adds the W partials in wave order
+                if (live && wr.w == 0 && lane < 32) {
+                    const int j = j0 + lane;
+                    float c1 = 0.f, c2 = 0.f, c3 = 0.f;
+    #pragma unroll
+                    for (int w = 0; w < W; ++w) {
+                        const float* so2 = smem + (4 / W) * attn_bwd_sample_floats(rpad) +
+                                           (wave + w) * attn_bwd_wave_floats(W) + attn_bwd_slot_offset() + (chunk & 1) * 96;
+                        c1 += so2[lane];
+                        c2 += so2[32 + lane];
+                        c3 += so2[64 + lane];
+                    }
+                    if (j < r) {
+                        st<T>::store(GP + b * ldgp + 2 * r + j, ev[0] * c1 - c2);
+                        st<T>::store(GP + b * ldgp + j, beta * eg[0] + c3);
                     }
                 }
             }
-            __syncthreads();
-            // the sample's first wave adds the W partials in wave order
-            if (live && wr.w == 0 && lane < 32) {
-                const int j = j0 + lane;
-                float c1 = 0.f, c2 = 0.f, c3 = 0.f;
-#pragma unroll
-                for (int w = 0; w < W; ++w) {
-                    const float* so2 = smem + (4 / W) * attn_bwd_sample_floats(rpad) +
-                                       (wave + w) * attn_bwd_wave_floats(W) + attn_bwd_slot_offset() + (chunk & 1) * 96;
-                    c1 += so2[lane];
-                    c2 += so2[32 + lane];
-                    c3 += so2[64 + lane];
-                }
-                if (j < r) {
-                    st<T>::store(GP + b * ldgp + 2 * r + j, pv[j] * c1 - c2);
-                    st<T>::store(GP + b * ldgp + j, beta * gh[j] + c3);
-                }
-            }
         }
-    }
+    };
+    if (fast) chunks(std::true_type{});
+    else chunks(std::false_type{});
     if (live && lane < 16) {
+        float gi[NT], oi[NT], zi[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {  // all loads first
+            const int i = (wr.t0 + t) * 16 + lane, ic = i < r ? i : r - 1;
+            gi[t] = gh[ic];
+            oi[t] = so[ic];
+            zi[t] = so[r + ic];
+        }
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             const int i = (wr.t0 + t) * 16 + lane;
             if (t < wr.nt && i < r) {
                 const float w1 = (acc[t].x + acc[t].y) * vks, w2 = (acc[t].z + acc[t].w) * ks;
-                const float go = alpha * gh[i], rz = 1.0f / so[r + i];
-                st<T>::store(GP + b * ldgp + r + i, go * rz * inv_tau * (w1 - so[i] * w2));
+                const float go = alpha * gi[t], rz = 1.0f / zi[t];
+                st<T>::store(GP + b * ldgp + r + i, go * rz * inv_tau * (w1 - oi[t] * w2));
             }
         }
     }
@@ -592,13 +787,14 @@ hipError_t launch_attn_fwd(int64_t B, int r, float alpha, float beta, float tau,
         const int NT = attn_tiles(rpad, W);
         const int64_t blocks = (B * W + 3) / 4;
         const size_t lds = 4 * sizeof(float) * (size_t)attn_fwd_wave_floats(rpad);
-#define RDCN_AFWD(NTV)                                                                                          \
-    hipLaunchKernelGGL((k_attn_fwd_mfma<bf16_t, NTV>), dim3((unsigned)blocks), dim3(256), lds, s, B, r, rpad, W, \
+#define RDCN_AFWD(NTV, KBV)                                                                                          \
+    hipLaunchKernelGGL((k_attn_fwd_mfma<bf16_t, NTV, KBV>), dim3((unsigned)blocks), dim3(256), lds, s, B, r, rpad, W, \
                        alpha, beta, 1.0f / tau, (const float*)P, ldp, (bf16_t*)H, (bf16_t*)H2, ldh, stats)
-        if (NT == 2) RDCN_AFWD(2);
-        else if (NT == 4) RDCN_AFWD(4);
-        else if (NT == 8) RDCN_AFWD(8);
-        else RDCN_AFWD(16);
+        if (NT == 2) RDCN_AFWD(2, 1);
+        else if (NT == 4) RDCN_AFWD(4, 1);
+        else if (NT == 8) RDCN_AFWD(8, 1);
+        else if (W == 1) RDCN_AFWD(16, 1);
+        else RDCN_AFWD(16, 4);
 #undef RDCN_AFWD
         return hipGetLastError();
     }

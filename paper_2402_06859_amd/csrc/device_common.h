@@ -27,6 +27,7 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) { return f32
 template <typename T> struct st;
 template <> struct st<float> {
     static constexpr int vec = 4;  // elements per 16-byte vector
+    __device__ static __forceinline__ float round(float v) { return v; }  // the value a store keeps
     __device__ static __forceinline__ float load(const float* p) { return *p; }
     __device__ static __forceinline__ void store(float* p, float v) { *p = v; }
     // 16-byte vector <-> 4 floats
@@ -40,6 +41,7 @@ template <> struct st<float> {
 };
 template <> struct st<bf16_t> {
     static constexpr int vec = 8;
+    __device__ static __forceinline__ float round(float v) { return bf16_to_f32(f32_to_bf16(v)); }
     __device__ static __forceinline__ float load(const bf16_t* p) { return bf16_to_f32(*p); }
     __device__ static __forceinline__ void store(bf16_t* p, float v) { *p = (bf16_t)f32_to_bf16(v); }
     __device__ static __forceinline__ void unpack(const u32x4_t& w, float* v) {
