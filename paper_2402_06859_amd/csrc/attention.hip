@@ -450,14 +450,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     float vmax = 0.f;
 #pragma unroll
     for (int u = 0; u < KPL; ++u) vmax = fmaxf(vmax, fabsf(vr[u]));
-    const float vs = pow2_ceil(wave_max(vmax));
+    const float vs = pow2_ceil(wave_max(vmax)), ivs = 1.0f / vs;  // exact: vs is a power of two
     const int ldx = rpad;
 #pragma unroll
     for (int u = 0; u < KPL; ++u) {
         const int j = 64 * u + lane;
         if (j < rpad) {
             sk[j] = kr[u];
-            put_pair(sx, ldx, 0, j, vr[u] / vs);
+            put_pair(sx, ldx, 0, j, vr[u] * ivs);
             sx[xoff(2, j, ldx)] = (_Float16)(j < r ? 1.f : 0.f);
         }
     }
@@ -507,7 +507,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             const int i = (wr.t0 + t) * 16 + lane;
             if (t < wr.nt && i < r) {
                 const float z = acc[t].z;
-                const float o = (acc[t].x + acc[t].y) * vs / z;
+                const float o = (acc[t].x + acc[t].y) * vs * __builtin_amdgcn_rcpf(z);
                 const float hv = beta * vi[t] + alpha * o;
                 st<T>::store(H + wr.b * ldh + i, hv);
                 if (H2) st<T>::store(H2 + wr.b * ldh + i, hv - st<T>::round(hv));
@@ -593,13 +593,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         mk = fmaxf(mk, fabsf(kr[u]));
     }
     const float vks = pow2_ceil(wave_max(mvk)), ks = pow2_ceil(wave_max(mk));
+    const float ivks = 1.0f / vks, iks = 1.0f / ks;  // exact: powers of two
 #pragma unroll
     for (int u = 0; u < KPL; ++u) {
         const int j = 64 * u + lane;
         if (j < rpad && u % W == wr.w) {
             sk[j] = kr[u];
-            put_pair(sx, ldx, 0, j, vr[u] * kr[u] / vks);
-            put_pair(sx, ldx, 2, j, kr[u] / ks);
+            put_pair(sx, ldx, 0, j, vr[u] * kr[u] * ivks);
+            put_pair(sx, ldx, 2, j, kr[u] * iks);
         }
     }
     // per-row coefficients of the wave's rows (zero past its rows)
@@ -607,7 +608,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     float ma = 0.f, mb = 0.f, mc = 0.f;
 #pragma unroll
     for (int u = 0; u < RPL; ++u) {
-        const float go = alpha * ghr[u], rz = zr[u] != 0.f ? 1.0f / zr[u] : 0.f;
+        const float go = alpha * ghr[u], rz = zr[u] != 0.f ? __builtin_amdgcn_rcpf(zr[u]) : 0.f;
         ca[u] = go * qr[u] * rz * inv_tau;
         cb[u] = ca[u] * orr[u];
         cg[u] = go * rz;
@@ -616,13 +617,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         mc = fmaxf(mc, fabsf(cg[u]));
     }
     const float as = pow2_ceil(wave_max(ma)), bs = pow2_ceil(wave_max(mb)), cs = pow2_ceil(wave_max(mc));
+    const float ias = 1.0f / as, ibs = 1.0f / bs, ics = 1.0f / cs;  // exact: powers of two
 #pragma unroll
     for (int u = 0; u < RPL; ++u) {
         const int il = 64 * u + lane;
         if (il < 16 * NT) {
-            put_pair(sy, ldy, 0, il, ca[u] / as);
-            put_pair(sy, ldy, 2, il, cb[u] / bs);
-            put_pair(sy, ldy, 4, il, cg[u] / cs);
+            put_pair(sy, ldy, 0, il, ca[u] * ias);
+            put_pair(sy, ldy, 2, il, cb[u] * ibs);
+            put_pair(sy, ldy, 4, il, cg[u] * ics);
         }
     }
     // row constants from q (load_rows zeroed q past the wave's rows; rows of
@@ -749,7 +751,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             const int i = (wr.t0 + t) * 16 + lane;
             if (t < wr.nt && i < r) {
                 const float w1 = (acc[t].x + acc[t].y) * vks, w2 = (acc[t].z + acc[t].w) * ks;
-                const float go = alpha * gi[t], rz = 1.0f / zi[t];
+                const float go = alpha * gi[t], rz = __builtin_amdgcn_rcpf(zi[t]);
                 st<T>::store(GP + b * ldgp + r + i, go * rz * inv_tau * (w1 - oi[t] * w2));
             }
         }
