@@ -57,6 +57,13 @@ def lib():
         L.orc_embed_backward.argtypes = [i64, i64, i64, i64, i64, i64, i64, ctypes.c_int, vp, vp, vp, vp, vp,
                                          vp, vp]
         L.orc_embed_backward.restype = i64
+        L.orc_quantize_rows.argtypes = [i64, i64, vp, vp, vp]
+        L.orc_quantize_rows.restype = ctypes.c_int
+        L.orc_dequantize_rows.argtypes = [i64, i64, vp, vp, vp]
+        L.orc_dequantize_rows.restype = ctypes.c_int
+        L.orc_gather_q8.argtypes = [i64, i64, i64, i64, i64, i64, i64, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp,
+                                    vp, vp, vp, vp]
+        L.orc_gather_q8.restype = i64
         _lib = L
     return _lib
 
@@ -176,3 +183,42 @@ def embed_backward(B: int, F: int, D: int, Nd: int, vocab: int, rows_q: int, m: 
     if bad < 0:
         raise ValueError("orc_embed_backward: bad arguments")
     return gq, gr, int(bad)
+
+
+def quantize_rows(x):
+    """Middle-max 8-bit row-wise quantization of x [rows, D] (float32 values):
+    (codes int8 [rows, D], params float32 [rows, 2] = (middle, scale))."""
+    x = _np(x, np.float32)
+    rows, D = x.shape
+    codes = np.empty((rows, D), np.int8)
+    params = np.empty((rows, 2), np.float32)
+    if lib().orc_quantize_rows(rows, D, _p(x), _p(codes), _p(params)) != 0:
+        raise ValueError("orc_quantize_rows: bad arguments")
+    return codes, params
+
+
+def dequantize_rows(codes, params):
+    codes = _c(codes, np.int8)
+    params = _c(params, np.float32)
+    rows, D = codes.shape
+    x = np.empty((rows, D), np.float32)
+    if lib().orc_dequantize_rows(rows, D, _p(codes), _p(params), _p(x)) != 0:
+        raise ValueError("orc_dequantize_rows: bad arguments")
+    return x
+
+
+def gather_q8(B: int, F: int, D: int, Nd: int, vocab: int, rows_q: int, m: int, combine: str, bf16: bool,
+              ids, offsets, q_codes, q_params, r_codes, r_params, dense):
+    """Serving gather from quantized tables (codes [F*rows, D] int8, params [F*rows, 2]):
+    x0 [B, F*D+Nd] float32 and the out-of-range id count."""
+    ids = _np(ids, np.int64)
+    offsets = _np(offsets, np.int64)
+    qc, rc = _c(q_codes, np.int8), _c(r_codes, np.int8)
+    qp, rp = _c(q_params, np.float32), _c(r_params, np.float32)
+    dn = _np(dense, np.float32)
+    x0 = np.empty((B, F * D + Nd), np.float32)
+    bad = lib().orc_gather_q8(B, F, D, Nd, vocab, rows_q, m, COMBINE[combine], int(bf16), _p(ids), _p(offsets),
+                              _p(qc), _p(qp), _p(rc), _p(rp), _p(dn), _p(x0))
+    if bad < 0:
+        raise ValueError("orc_gather_q8: bad arguments")
+    return x0, int(bad)

@@ -438,3 +438,76 @@ int64_t orc_embed_backward(int64_t B, int64_t F, int64_t D, int64_t Nd, int64_t 
     }
     return bad;
 }
+
+/* ------------------------------------------- middle-max 8-bit table quantization */
+
+/*
+ * Section "Embedding Table Quantization": post-training row-wise quantization
+ * of an embedding table X with bits = 8. For row i with minimum mn and
+ * maximum mx:
+ *   middle = (mx * 2^(bits-1) + mn * (2^(bits-1) - 1)) / (2^bits - 1)
+ *   scale  = (mx - mn) / (2^bits - 1)
+ *   code   = round((x - middle) / scale)          (lands in [-128, 127])
+ *   value  = middle + code * scale                (dequantization)
+ * In float, one rounding per operation in the order written: middle =
+ * (mx*128 + mn*127) / 255, scale = (mx - mn) / 255, code = rint((x - middle) /
+ * scale) with ties to even, clamped to [-128, 127]. A constant row (mx == mn)
+ * has scale 0 and all codes 0. Dequantization is middle + code*scale with a
+ * single rounding (fused multiply-add).
+ *
+ * x [rows, D] (storage values as float) -> codes [rows, D], params [rows, 2] =
+ * (middle, scale).
+ */
+int orc_quantize_rows(int64_t rows, int64_t D, const float* x, int8_t* codes, float* params) {
+    if (rows < 0 || D <= 0) return -1;
+    for (int64_t i = 0; i < rows; ++i) {
+        const float* row = x + i * D;
+        float mn = row[0], mx = row[0];
+        for (int64_t c = 1; c < D; ++c) {
+            if (row[c] < mn) mn = row[c];
+            if (row[c] > mx) mx = row[c];
+        }
+        const float middle = (mx * 128.0f + mn * 127.0f) / 255.0f;
+        const float scale = (mx - mn) / 255.0f;
+        params[2 * i] = middle;
+        params[2 * i + 1] = scale;
+        for (int64_t c = 0; c < D; ++c) {
+            float q = 0.0f;
+            if (scale > 0.0f) {
+                q = rintf((row[c] - middle) / scale);
+                if (q < -128.0f) q = -128.0f;
+                if (q > 127.0f) q = 127.0f;
+            }
+            codes[i * D + c] = (int8_t)q;
+        }
+    }
+    return 0;
+}
+
+/* Dequantized table: value[i, c] = fma(code[i, c], scale_i, middle_i). */
+int orc_dequantize_rows(int64_t rows, int64_t D, const int8_t* codes, const float* params, float* x) {
+    if (rows < 0 || D <= 0) return -1;
+    for (int64_t i = 0; i < rows; ++i)
+        for (int64_t c = 0; c < D; ++c) x[i * D + c] = fmaf((float)codes[i * D + c], params[2 * i + 1], params[2 * i]);
+    return 0;
+}
+
+/*
+ * Serving gather from quantized tables: exactly orc_gather with every table
+ * value replaced by its dequantized value (the combine, pooling and rounding
+ * are those of the gather).
+ */
+int64_t orc_gather_q8(int64_t B, int64_t F, int64_t D, int64_t Nd, int64_t vocab, int64_t rows_q, int64_t m,
+                      int combine, int round_bf16, const int64_t* ids, const int64_t* offsets,
+                      const int8_t* q_codes, const float* q_params, const int8_t* r_codes, const float* r_params,
+                      const float* dense, float* x0) {
+    if (B < 0 || F < 0 || D <= 0 || Nd < 0 || m <= 0 || rows_q <= 0) return -1;
+    float* qt = (float*)malloc(sizeof(float) * (size_t)(F * rows_q * D + 1));
+    float* rt = (float*)malloc(sizeof(float) * (size_t)(F * m * D + 1));
+    orc_dequantize_rows(F * rows_q, D, q_codes, q_params, qt);
+    orc_dequantize_rows(F * m, D, r_codes, r_params, rt);
+    int64_t bad = orc_gather(B, F, D, Nd, vocab, rows_q, m, combine, round_bf16, ids, offsets, qt, rt, dense, x0);
+    free(qt);
+    free(rt);
+    return bad;
+}

@@ -39,8 +39,17 @@ MUTATIONS = {
     "bwd_value_skip_dropped": ("grad", "dv[j] = beta * dh[j] + s;", "dv[j] = s;"),
     "bwd_final_input_term_dropped": ("grad", "grad_x0[b * d + c] = gx0[c] + g[c];", "grad_x0[b * d + c] = gx0[c];"),
     "emb_product_rule_wrong_row": ("grad", "gq[c] += g[c] * (double)rrow[c];", "gq[c] += g[c] * (double)qrow[c];"),
+    "quant_middle_weights_swapped": ("quant", "(mx * 128.0f + mn * 127.0f) / 255.0f", "(mx * 127.0f + mn * 128.0f) / 255.0f"),
+    "quant_scale_over_256": ("quant", "(mx - mn) / 255.0f", "(mx - mn) / 256.0f"),
+    "quant_truncating_round": ("quant", "q = rintf((row[c] - middle) / scale);", "q = truncf((row[c] - middle) / scale);"),
+    "quant_ties_away": ("quant", "q = rintf((row[c] - middle) / scale);", "q = roundf((row[c] - middle) / scale);"),
+    "quant_dequant_minus": ("quant", "fmaf((float)codes[i * D + c], params[2 * i + 1], params[2 * i])",
+                            "fmaf((float)codes[i * D + c], -params[2 * i + 1], params[2 * i])"),
+    "quant_dequant_two_roundings": ("quant", "fmaf((float)codes[i * D + c], params[2 * i + 1], params[2 * i])",
+                                    "(float)codes[i * D + c] * params[2 * i + 1] + params[2 * i]"),
 }
-PIN_FILE = {"gather": "test_oracle_gather.py", "dcn": "test_oracle_dcn.py", "grad": "test_oracle_grad.py"}
+PIN_FILE = {"gather": "test_oracle_gather.py", "dcn": "test_oracle_dcn.py", "grad": "test_oracle_grad.py",
+            "quant": "test_oracle_quant.py"}
 
 
 @pytest.mark.parametrize("name", list(MUTATIONS))
