@@ -451,7 +451,8 @@ int64_t orc_embed_backward(int64_t B, int64_t F, int64_t D, int64_t Nd, int64_t 
  *   value  = middle + code * scale                (dequantization)
  * In float, one rounding per operation in the order written: middle =
  * (mx*128 + mn*127) / 255, scale = (mx - mn) / 255, code = rint((x - middle) /
- * scale) with ties to even, clamped to [-128, 127]. A constant row (mx == mn)
+ * scale) with ties to even, clamped to [-128, 127]; an extreme that is a zero is
+ * taken as +0 (the paper is silent on signed zeros). A constant row (mx == mn)
  * has scale 0 and all codes 0. Dequantization is middle + code*scale with a
  * single rounding (fused multiply-add).
  *
@@ -467,6 +468,8 @@ int orc_quantize_rows(int64_t rows, int64_t D, const float* x, int8_t* codes, fl
             if (row[c] < mn) mn = row[c];
             if (row[c] > mx) mx = row[c];
         }
+        mn += 0.0f;  /* a zero extreme counts as +0 whichever zero was met first */
+        mx += 0.0f;
         const float middle = (mx * 128.0f + mn * 127.0f) / 255.0f;
         const float scale = (mx - mn) / 255.0f;
         params[2 * i] = middle;

@@ -105,6 +105,13 @@ def test_dequantization_error_at_most_half_step():
     assert np.all(err <= bound)
 
 
+def test_signed_zero_extremes_are_positive_zero():
+    x = np.array([[-0.0, 0.0, -0.0, 0.0], [0.0, -0.0, -0.0, -0.0], [-0.0] * 4, [-1.0, -0.0, -0.5, 0.0]], np.float32)
+    codes, params = oracle.quantize_rows(x)
+    assert not np.signbit(params[:3, 0]).any() and np.all(params[:3, 1] == 0)
+    assert params[3, 1] == np.float32(1.0) / np.float32(255.0)
+
+
 def test_constant_row():
     x = np.full((3, 8), 0.3, np.float32)
     x[1] = -2.0
