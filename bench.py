@@ -85,6 +85,8 @@ def kernel_work(wl, B: int) -> dict:
     w["emb_keys"] = (0.0, nnz * 8 + 2 * nnz * 8 + (nnz * 4 if wl.multi_hot else 0), 0.0)
     w["emb_sort"] = (0.0, passes * 2 * nnz * (4 + 8 + 8), 0.0)  # histogram read + scatter read/write per pass
     w["emb_reduce"] = (0.0, 2 * nnz * (8 + D * 4) + 2 * F * wl.table_rows * D * 8, 0.0)
+    # serving gather from 8-bit tables: codes (1 byte per value) and each row's (middle, scale)
+    w["gather_q8"] = (0.0, B * (F * hot * 8 + 2 * F * hot * (D + 8) + F * D * eb + 2 * Nd * eb), 0.0)
     return w
 
 
@@ -177,6 +179,35 @@ def _oracle_step(wl, rows: int) -> float:
     oracle.embed_backward(rows, wl.num_cat, wl.emb_dim, wl.num_dense, wl.vocab, wl.table_rows, wl.table_rows,
                           wl.combine, inp["ids"], inp["offsets"], inp["q_tables"], inp["r_tables"], gx0)
     return time.perf_counter() - t0
+
+
+def time_gather_q8(db, q8_bytes: float, bytes16: float, launches: int = 20) -> dict:
+    """Serving-path gather from middle-max 8-bit tables (quantized once here), timed
+    with HIP events on its launch stream; the storage-type gather on the same batch
+    beside it."""
+    import torch
+    lib, D = db.lib, db.wl.emb_dim
+    qs = []
+    for t in (db.q_tables, db.r_tables):
+        rows = t.numel() // D
+        codes = torch.empty((rows, D), dtype=torch.int8, device=t.device)
+        params = torch.empty((rows, 2), dtype=torch.float32, device=t.device)
+        lib.qr_quantize_tables(rows, t, codes, params)
+        qs += [codes, params]
+    x0 = torch.empty_like(db.x0)
+    res = {}
+    for name in ("gather_q8", "gather"):
+        lib.profile_start(launches, [name])
+        for _ in range(launches):
+            if name == "gather_q8":
+                lib.qr_embed_gather_q8(db.B, db.ids, db.offsets, qs[0], qs[1], qs[2], qs[3], db.dense, x0)
+            else:
+                lib.qr_embed_gather(db.B, db.ids, db.offsets, db.q_tables, db.r_tables, db.dense, x0)
+        ms, n = lib.profile_stop()[name]
+        res[name] = ms / n * 1e3
+    return {"avg_us": res["gather_q8"], "gbps": q8_bytes / (res["gather_q8"] * 1e-6) / 1e9,
+            "table_bytes_per_value": 1, "storage_gather_avg_us": res["gather"],
+            "storage_gather_gbps": bytes16 / (res["gather"] * 1e-6) / 1e9}
 
 
 def main():
@@ -284,6 +315,8 @@ def main():
         "gather_gbps": (work["gather"][1] / gather_s / 1e9) if gather_s > 0 else None,
         "kernels": kernels,
     }
+    if wl.num_cat > 0:
+        out["gather_q8"] = time_gather_q8(db, work["gather_q8"][1], work["gather"][1])
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(out), flush=True)

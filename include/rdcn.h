@@ -150,6 +150,35 @@ rdcn_status qr_embed_gather(rdcn_handle* h, int64_t batch, const void* ids, cons
                             void* stream);
 
 /*
+ * Middle-max 8-bit row-wise quantization of QR tables, section "Embedding
+ * Table Quantization" (post-training, for serving). For each of the `rows`
+ * rows of `tables` ([rows, emb_dim] in the storage dtype: all quotient tables
+ * [F * qr_rows_q, D] or all remainder tables [F * m, D] of the handle's model)
+ * with row minimum mn and maximum mx (a zero extreme counts as +0):
+ *   middle = (mx * 128 + mn * 127) / 255,  scale = (mx - mn) / 255,
+ *   code   = round((x - middle) / scale)   ties to even, in [-128, 127]
+ * each a single IEEE float operation in that order; a constant row has scale 0
+ * and codes 0. Outputs: codes [rows, D] int8 and params [rows, 2] float
+ * (middle, scale). codes must be 8-byte aligned for bf16 models (4 for float),
+ * params 8-byte aligned (RDCN_ERR_ARG otherwise); rows >= 2^32 gives
+ * RDCN_ERR_UNSUPPORTED.
+ */
+rdcn_status qr_quantize_tables(rdcn_handle* h, int64_t rows, const void* tables, int8_t* codes, float* params,
+                               void* stream);
+
+/*
+ * QR embedding gather from quantized tables (serving path): exactly
+ * qr_embed_gather with every table value replaced by its dequantized value
+ * middle + code * scale, computed with one rounding (fused multiply-add).
+ * q_codes [F, qr_rows_q, D] and r_codes [F, m, D] int8, q_params / r_params
+ * [F, rows, 2] float as written by qr_quantize_tables; ids, offsets, dense and
+ * x0 as in qr_embed_gather. Alignment as for qr_quantize_tables.
+ */
+rdcn_status qr_embed_gather_q8(rdcn_handle* h, int64_t batch, const void* ids, const int64_t* offsets,
+                               const int8_t* q_codes, const float* q_params, const int8_t* r_codes,
+                               const float* r_params, const void* dense, void* x0, void* stream);
+
+/*
  * Scratch bytes qr_embed_backward needs for `batch` samples holding `nnz` ids
  * in total (single-hot: nnz = batch * F).
  */
@@ -234,7 +263,9 @@ typedef enum rdcn_kernel {
     RDCN_KERNEL_EMB_KEYS = 12,      /* embedding backward: row keys */
     RDCN_KERNEL_EMB_SORT = 13,      /* embedding backward: stable radix sort */
     RDCN_KERNEL_EMB_REDUCE = 14,    /* embedding backward: segmented reduction + fix-up */
-    RDCN_KERNEL_COUNT = 15
+    RDCN_KERNEL_GATHER_Q8 = 15,     /* qr_embed_gather_q8 */
+    RDCN_KERNEL_QUANTIZE = 16,      /* qr_quantize_tables */
+    RDCN_KERNEL_COUNT = 17
 } rdcn_kernel;
 
 /*

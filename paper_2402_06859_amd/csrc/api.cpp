@@ -170,6 +170,40 @@ hipError_t gemm_weight_grad(rdcn_handle* h, int kind, GemmArgs g, float* out, fl
     return launch_splitk_reduce(splitk, p.splits, g.M * g.N, out, s);
 }
 
+rdcn_status gather_args(rdcn_handle* h, int64_t batch, const void* ids, const int64_t* offsets,
+                               const void* q_tables, const void* r_tables, const void* dense, void* x0,
+                               GatherArgs& a) {
+    const rdcn_config& c = h->cfg;
+    if (!x0 || (c.num_cat > 0 && (!ids || !q_tables || !r_tables)) || (c.num_dense > 0 && !dense))
+        return RDCN_ERR_ARG;
+    a.batch = batch;
+    a.F = c.num_cat;
+    a.D = c.emb_dim;
+    a.Nd = c.num_dense;
+    a.rows_q = c.qr_rows_q;
+    a.m = (uint32_t)c.qr_rows_r;
+    a.vocab = (uint64_t)c.vocab;
+    a.magic = h->magic;
+    a.shift = h->shift;
+    a.combine = c.combine == RDCN_COMBINE_MUL ? 0 : 1;
+    a.ids = ids;
+    a.offsets = offsets;
+    a.q_tables = q_tables;
+    a.r_tables = r_tables;
+    a.q_params = nullptr;
+    a.r_params = nullptr;
+    a.dense = dense;
+    a.x0 = x0;
+    a.err = h->err;
+    return RDCN_OK;
+}
+
+// codes: 8 (bf16 models) or 4 (float) codes per lane load; params: float2 loads
+bool q8_aligned(const rdcn_handle* h, const void* codes, const void* params) {
+    const uintptr_t cm = h->bf16 ? 7u : 3u;
+    return (((uintptr_t)codes) & cm) == 0 && (((uintptr_t)params) & 7u) == 0;
+}
+
 }  // namespace
 
 extern "C" {
@@ -266,28 +300,38 @@ rdcn_status qr_embed_gather(rdcn_handle* h, int64_t batch, const void* ids, cons
     const rdcn_config& c = h->cfg;
     if ((offsets != nullptr) != (c.multi_hot != 0)) return RDCN_ERR_ARG;
     if (batch == 0) return RDCN_OK;
-    if (!x0 || (c.num_cat > 0 && (!ids || !q_tables || !r_tables)) || (c.num_dense > 0 && !dense))
-        return RDCN_ERR_ARG;
     GatherArgs a;
-    a.batch = batch;
-    a.F = c.num_cat;
-    a.D = c.emb_dim;
-    a.Nd = c.num_dense;
-    a.rows_q = c.qr_rows_q;
-    a.m = (uint32_t)c.qr_rows_r;
-    a.vocab = (uint64_t)c.vocab;
-    a.magic = h->magic;
-    a.shift = h->shift;
-    a.combine = c.combine == RDCN_COMBINE_MUL ? 0 : 1;
-    a.ids = ids;
-    a.offsets = offsets;
-    a.q_tables = q_tables;
-    a.r_tables = r_tables;
-    a.dense = dense;
-    a.x0 = x0;
-    a.err = h->err;
+    if ((st = gather_args(h, batch, ids, offsets, q_tables, r_tables, dense, x0, a)) != RDCN_OK) return st;
     ProfScope ps(h, RDCN_KERNEL_GATHER, (hipStream_t)stream);
     return hip_status(launch_qr_gather(a, h->bf16, h->ids64, (hipStream_t)stream));
+}
+
+rdcn_status qr_quantize_tables(rdcn_handle* h, int64_t rows, const void* tables, int8_t* codes, float* params,
+                               void* stream) {
+    if (!h || rows < 0) return RDCN_ERR_ARG;
+    if (rows >= ((int64_t)1 << 32)) return RDCN_ERR_UNSUPPORTED;
+    if (rows == 0) return RDCN_OK;
+    if (!tables || !codes || !params || !q8_aligned(h, codes, params)) return RDCN_ERR_ARG;
+    ProfScope ps(h, RDCN_KERNEL_QUANTIZE, (hipStream_t)stream);
+    return hip_status(launch_quantize_rows(rows, h->cfg.emb_dim, tables, codes, params, h->bf16, (hipStream_t)stream));
+}
+
+rdcn_status qr_embed_gather_q8(rdcn_handle* h, int64_t batch, const void* ids, const int64_t* offsets,
+                               const int8_t* q_codes, const float* q_params, const int8_t* r_codes,
+                               const float* r_params, const void* dense, void* x0, void* stream) {
+    rdcn_status st = check_batch(h, batch);
+    if (st != RDCN_OK) return st;
+    if ((offsets != nullptr) != (h->cfg.multi_hot != 0)) return RDCN_ERR_ARG;
+    if (batch == 0) return RDCN_OK;
+    GatherArgs a;
+    if ((st = gather_args(h, batch, ids, offsets, q_codes, r_codes, dense, x0, a)) != RDCN_OK) return st;
+    if (h->cfg.num_cat > 0 && (!q_params || !r_params || !q8_aligned(h, q_codes, q_params) ||
+                               !q8_aligned(h, r_codes, r_params)))
+        return RDCN_ERR_ARG;
+    a.q_params = q_params;
+    a.r_params = r_params;
+    ProfScope ps(h, RDCN_KERNEL_GATHER_Q8, (hipStream_t)stream);
+    return hip_status(launch_qr_gather_q8(a, h->bf16, h->ids64, (hipStream_t)stream));
 }
 
 rdcn_status qr_embed_backward_workspace(const rdcn_handle* h, int64_t batch, int64_t nnz, size_t* scratch_bytes) {

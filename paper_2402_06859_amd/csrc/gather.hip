@@ -41,7 +41,67 @@ __device__ __forceinline__ bool qr_split(ID id_raw, const GatherArgs& a, uint32_
 
 constexpr int GATHER_ROWS = 4;  // rows per wave (their loads are issued together)
 
-template <typename T, typename ID, bool BAGS>
+// Table rows in the storage type: a lane's V values are one 16-byte vector.
+template <typename T>
+struct StorageRows {
+    static constexpr int V = st<T>::vec;
+    struct Raw {
+        u32x4_t w;
+    };
+    const T* q;  // the lane's columns in row 0 of feature f's quotient table
+    const T* r;
+    int64_t D;
+    __device__ __forceinline__ StorageRows(const GatherArgs& a, int f, int cc)
+        : q((const T*)a.q_tables + (int64_t)f * a.rows_q * a.D + cc * V),
+          r((const T*)a.r_tables + (int64_t)f * a.m * a.D + cc * V), D(a.D) {}
+    __device__ __forceinline__ Raw load_q(uint32_t i) const { return Raw{*(const u32x4_t*)(q + (int64_t)i * D)}; }
+    __device__ __forceinline__ Raw load_r(uint32_t i) const { return Raw{*(const u32x4_t*)(r + (int64_t)i * D)}; }
+    __device__ __forceinline__ static void values(const Raw& x, float* v) { st<T>::unpack(x.w, v); }
+};
+
+// Middle-max 8-bit rows (section "Embedding Table Quantization"): a lane's V codes
+// and the row's (middle, scale); value = middle + code * scale with one rounding.
+template <typename T>
+struct Q8Rows {
+    static constexpr int V = st<T>::vec;  // output values per lane (8 for bf16 x0, 4 for float)
+    struct Raw {
+        uint32_t c[V / 4];
+        float2 p;
+    };
+    const int8_t* q;
+    const int8_t* r;
+    const float2* qp;
+    const float2* rp;
+    int64_t D;
+    __device__ __forceinline__ Q8Rows(const GatherArgs& a, int f, int cc)
+        : q((const int8_t*)a.q_tables + (int64_t)f * a.rows_q * a.D + cc * V),
+          r((const int8_t*)a.r_tables + (int64_t)f * a.m * a.D + cc * V),
+          qp((const float2*)a.q_params + (int64_t)f * a.rows_q), rp((const float2*)a.r_params + (int64_t)f * a.m),
+          D(a.D) {}
+    __device__ __forceinline__ static Raw load(const int8_t* codes, const float2* params, uint32_t i, int64_t D) {
+        Raw x;
+        if (V == 8) {
+            const uint2 w = *(const uint2*)(codes + (int64_t)i * D);
+            x.c[0] = w.x;
+            x.c[V / 4 - 1] = w.y;
+        } else {
+            x.c[0] = *(const uint32_t*)(codes + (int64_t)i * D);
+        }
+        x.p = params[i];
+        return x;
+    }
+    __device__ __forceinline__ Raw load_q(uint32_t i) const { return load(q, qp, i, D); }
+    __device__ __forceinline__ Raw load_r(uint32_t i) const { return load(r, rp, i, D); }
+    __device__ __forceinline__ static void values(const Raw& x, float* v) {
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            const int code = (int)(int8_t)((x.c[e / 4] >> (8 * (e % 4))) & 0xffu);
+            v[e] = __builtin_fmaf((float)code, x.p.y, x.p.x);
+        }
+    }
+};
+
+template <typename T, typename ID, bool BAGS, class Rows>
 __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a) {
 #pragma clang fp contract(off)
     constexpr int V = st<T>::vec;
@@ -50,16 +110,13 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a) {
     const int cpr = emb_vecs + a.Nd / V;     // vectors per x0 row
     const int c = blockIdx.x * 64 + (threadIdx.x & 63);
     if (c >= cpr) return;
-    const T* qt = (const T*)a.q_tables;
-    const T* rt = (const T*)a.r_tables;
     const ID* ids = (const ID*)a.ids;
     T* x0 = (T*)a.x0;
     const int64_t d = (int64_t)a.F * a.D + a.Nd;
     const bool emb = c < emb_vecs;
     const int f = emb ? c / cpf : 0;
     const int cc = emb ? c - f * cpf : 0;
-    const T* qbase = qt + (int64_t)f * a.rows_q * a.D + cc * V;
-    const T* rbase = rt + (int64_t)f * a.m * a.D + cc * V;
+    const Rows rows(a, f, cc);
     const int64_t row_step = (int64_t)gridDim.y * 4 * GATHER_ROWS;
     for (int64_t b0 = ((int64_t)blockIdx.y * 4 + (threadIdx.x >> 6)) * GATHER_ROWS; b0 < a.batch; b0 += row_step) {
         const int nr = a.batch - b0 < GATHER_ROWS ? (int)(a.batch - b0) : GATHER_ROWS;
@@ -73,21 +130,21 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a) {
 #pragma unroll
             for (int u = 0; u < GATHER_ROWS; ++u) id[u] = ids[(b0 + (u < nr ? u : 0)) * a.F + f];
             bool ok[GATHER_ROWS];
-            u32x4_t qw[GATHER_ROWS], rw[GATHER_ROWS];
+            typename Rows::Raw qw[GATHER_ROWS], rw[GATHER_ROWS];
 #pragma unroll
             for (int u = 0; u < GATHER_ROWS; ++u) {
                 uint32_t qi = 0, ri = 0;
                 ok[u] = qr_split<ID>(id[u], a, qi, ri);
                 if (!ok[u]) qi = ri = 0;
-                qw[u] = *(const u32x4_t*)(qbase + (int64_t)qi * a.D);
-                rw[u] = *(const u32x4_t*)(rbase + (int64_t)ri * a.D);
+                qw[u] = rows.load_q(qi);
+                rw[u] = rows.load_r(ri);
             }
             bool bad = false;
 #pragma unroll
             for (int u = 0; u < GATHER_ROWS; ++u) {
                 float qv[V], rv[V], acc[V];
-                st<T>::unpack(qw[u], qv);
-                st<T>::unpack(rw[u], rv);
+                Rows::values(qw[u], qv);
+                Rows::values(rw[u], rv);
 #pragma unroll
                 for (int e = 0; e < V; ++e) acc[e] = ok[u] ? (a.combine == 0 ? qv[e] * rv[e] : qv[e] + rv[e]) : 0.0f;
                 out[u] = st<T>::pack(acc);
@@ -114,8 +171,8 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a) {
                         continue;
                     }
                     float qv[V], rv[V];
-                    st<T>::unpack(*(const u32x4_t*)(qbase + (int64_t)qi * a.D), qv);
-                    st<T>::unpack(*(const u32x4_t*)(rbase + (int64_t)ri * a.D), rv);
+                    Rows::values(rows.load_q(qi), qv);
+                    Rows::values(rows.load_r(ri), rv);
 #pragma unroll
                     for (int e = 0; e < V; ++e) {
                         const float x = a.combine == 0 ? qv[e] * rv[e] : qv[e] + rv[e];
@@ -137,7 +194,49 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a) {
     }
 }
 
-hipError_t launch_qr_gather(const GatherArgs& a, bool bf16, bool ids64, hipStream_t s) {
+// Middle-max quantization of one row per wave (D <= 256: lane holds columns
+// lane + 64 u). Every operation is one IEEE float operation in the order the
+// definition writes it (no contraction), rounding to nearest even.
+template <typename T>
+__global__ __launch_bounds__(256) void k_quantize_rows(int64_t rows, int D, const T* __restrict__ x,
+                                                       int8_t* __restrict__ codes, float2* __restrict__ params) {
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const T* xr = x + row * D;
+    float v[4];
+    float mn = INFINITY, mx = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int c = lane + 64 * u;
+        v[u] = c < D ? st<T>::load(xr + c) : 0.0f;
+        if (c < D) {
+            mn = fminf(mn, v[u]);
+            mx = fmaxf(mx, v[u]);
+        }
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+        mn = fminf(mn, __shfl_xor(mn, off));
+        mx = fmaxf(mx, __shfl_xor(mx, off));
+    }
+    mn = __fadd_rn(mn, 0.0f);  // a zero extreme counts as +0
+    mx = __fadd_rn(mx, 0.0f);
+    const float middle = __fdiv_rn(__fadd_rn(__fmul_rn(mx, 128.0f), __fmul_rn(mn, 127.0f)), 255.0f);
+    const float scale = __fdiv_rn(__fsub_rn(mx, mn), 255.0f);
+    if (lane == 0) params[row] = make_float2(middle, scale);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int c = lane + 64 * u;
+        if (c < D) {
+            float q = 0.0f;
+            if (scale > 0.0f) q = fminf(fmaxf(__builtin_rintf(__fdiv_rn(__fsub_rn(v[u], middle), scale)), -128.0f), 127.0f);
+            codes[row * D + c] = (int8_t)(int)q;
+        }
+    }
+}
+
+template <template <typename> class R>
+hipError_t launch_gather_rows(const GatherArgs& a, bool bf16, bool ids64, hipStream_t s) {
     const int V = bf16 ? 8 : 4;
     const int64_t cpr = (a.F * (int64_t)a.D + a.Nd) / V;
     if (a.batch == 0 || cpr == 0) return hipSuccess;
@@ -147,7 +246,7 @@ hipError_t launch_qr_gather(const GatherArgs& a, bool bf16, bool ids64, hipStrea
     const dim3 grid((unsigned)((cpr + 63) / 64), (unsigned)ygroups);
     const int threads = 256;
     const bool bags = a.offsets != nullptr;
-#define RDCN_GATHER(T, ID, BG) hipLaunchKernelGGL((k_qr_gather<T, ID, BG>), grid, dim3(threads), 0, s, a)
+#define RDCN_GATHER(T, ID, BG) hipLaunchKernelGGL((k_qr_gather<T, ID, BG, R<T>>), grid, dim3(threads), 0, s, a)
     if (bf16) {
         if (ids64) { if (bags) RDCN_GATHER(bf16_t, int64_t, true); else RDCN_GATHER(bf16_t, int64_t, false); }
         else       { if (bags) RDCN_GATHER(bf16_t, int32_t, true); else RDCN_GATHER(bf16_t, int32_t, false); }
@@ -156,6 +255,27 @@ hipError_t launch_qr_gather(const GatherArgs& a, bool bf16, bool ids64, hipStrea
         else       { if (bags) RDCN_GATHER(float, int32_t, true); else RDCN_GATHER(float, int32_t, false); }
     }
 #undef RDCN_GATHER
+    return hipGetLastError();
+}
+
+hipError_t launch_qr_gather(const GatherArgs& a, bool bf16, bool ids64, hipStream_t s) {
+    return launch_gather_rows<StorageRows>(a, bf16, ids64, s);
+}
+
+hipError_t launch_qr_gather_q8(const GatherArgs& a, bool bf16, bool ids64, hipStream_t s) {
+    return launch_gather_rows<Q8Rows>(a, bf16, ids64, s);
+}
+
+hipError_t launch_quantize_rows(int64_t rows, int D, const void* tables, int8_t* codes, float* params, bool bf16,
+                                hipStream_t s) {
+    if (rows == 0) return hipSuccess;
+    const dim3 grid((unsigned)((rows + 3) / 4));
+    if (bf16)
+        hipLaunchKernelGGL(k_quantize_rows<bf16_t>, grid, dim3(256), 0, s, rows, D, (const bf16_t*)tables, codes,
+                           (float2*)params);
+    else
+        hipLaunchKernelGGL(k_quantize_rows<float>, grid, dim3(256), 0, s, rows, D, (const float*)tables, codes,
+                           (float2*)params);
     return hipGetLastError();
 }
 

@@ -15,13 +15,20 @@ struct GatherArgs {
     int combine;            // 0 = product, 1 = sum
     const void* ids;        // int32 or int64
     const int64_t* offsets; // NULL = single-hot
-    const void* q_tables;
+    const void* q_tables;   // storage-type tables, or int8 codes for the quantized gather
     const void* r_tables;
+    const float* q_params;  // quantized gather: (middle, scale) per table row
+    const float* r_params;
     const void* dense;
     void* x0;
     int* err;
 };
 hipError_t launch_qr_gather(const GatherArgs& a, bool bf16, bool ids64, hipStream_t s);
+// Same gather from middle-max 8-bit tables (codes in q_tables / r_tables, row parameters in q_params / r_params).
+hipError_t launch_qr_gather_q8(const GatherArgs& a, bool bf16, bool ids64, hipStream_t s);
+// Middle-max 8-bit row-wise quantization of `rows` table rows of width D.
+hipError_t launch_quantize_rows(int64_t rows, int D, const void* tables, int8_t* codes, float* params, bool bf16,
+                                hipStream_t s);
 
 }  // namespace rdcn
 

@@ -23,11 +23,12 @@ COMBINE_MUL, COMBINE_SUM = 0, 1
 
 EXPORTS = ["rdcn_create", "rdcn_destroy", "rdcn_dim", "rdcn_workspace_bytes", "qr_embed_gather",
            "qr_embed_backward_workspace", "qr_embed_backward", "rdcn_forward", "rdcn_backward",
-           "rdcn_check_device_errors", "rdcn_status_string", "rdcn_profile_start", "rdcn_profile_stop"]
+           "rdcn_check_device_errors", "rdcn_status_string", "rdcn_profile_start", "rdcn_profile_stop",
+           "qr_quantize_tables", "qr_embed_gather_q8"]
 
 KERNELS = ["gather", "fwd_down_gemm", "fwd_attention", "fwd_up_gemm", "bwd_pointwise", "bwd_bias", "bwd_gu_gemm",
            "bwd_gh_gemm", "bwd_attention", "bwd_gw_gemm", "bwd_gx_gemm", "splitk_reduce", "emb_keys", "emb_sort",
-           "emb_reduce"]
+           "emb_reduce", "gather_q8", "quantize"]
 
 
 class RdcnConfig(ctypes.Structure):
@@ -73,6 +74,8 @@ def load(build_if_missing: bool = True):
     L.rdcn_dim.argtypes = [vp, ctypes.POINTER(i64)]
     L.rdcn_workspace_bytes.argtypes = [vp, i64, ctypes.POINTER(sz), ctypes.POINTER(sz)]
     L.qr_embed_gather.argtypes = [vp, i64, vp, vp, vp, vp, vp, vp, vp]
+    L.qr_quantize_tables.argtypes = [vp, i64, vp, vp, vp, vp]
+    L.qr_embed_gather_q8.argtypes = [vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.qr_embed_backward_workspace.argtypes = [vp, i64, i64, ctypes.POINTER(sz)]
     L.qr_embed_backward.argtypes = [vp, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.rdcn_forward.argtypes = [vp, i64, vp, ctypes.POINTER(RdcnWeights), vp, vp, vp, vp]
@@ -177,6 +180,15 @@ class Rdcn:
     def qr_embed_gather(self, batch, ids, offsets, q_tables, r_tables, dense, x0, stream=None):
         _check("qr_embed_gather", load().qr_embed_gather(self.h, batch, _ptr(ids), _ptr(offsets), _ptr(q_tables),
                                                          _ptr(r_tables), _ptr(dense), _ptr(x0), _stream(stream)))
+
+    def qr_quantize_tables(self, rows, tables, codes, params, stream=None):
+        _check("qr_quantize_tables", load().qr_quantize_tables(self.h, rows, _ptr(tables), _ptr(codes), _ptr(params),
+                                                               _stream(stream)))
+
+    def qr_embed_gather_q8(self, batch, ids, offsets, q_codes, q_params, r_codes, r_params, dense, x0, stream=None):
+        _check("qr_embed_gather_q8", load().qr_embed_gather_q8(
+            self.h, batch, _ptr(ids), _ptr(offsets), _ptr(q_codes), _ptr(q_params), _ptr(r_codes), _ptr(r_params),
+            _ptr(dense), _ptr(x0), _stream(stream)))
 
     def qr_embed_backward(self, batch, nnz, ids, offsets, q_tables, r_tables, grad_x0, grad_q, grad_r, scratch,
                           stream=None):

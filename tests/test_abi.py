@@ -102,3 +102,9 @@ def test_entry_points_reject_null_handle():
                            None) == rdcn.RDCN_ERR_ARG
     assert L.rdcn_check_device_errors(None, None) == rdcn.RDCN_ERR_ARG
     assert L.rdcn_destroy(None) == rdcn.RDCN_OK
+
+
+def test_quantization_entry_points_reject_null_handle():
+    L = rdcn.load()
+    assert L.qr_quantize_tables(None, 4, None, None, None, None) == rdcn.RDCN_ERR_ARG
+    assert L.qr_embed_gather_q8(None, 4, None, None, None, None, None, None, None, None, None) == rdcn.RDCN_ERR_ARG
