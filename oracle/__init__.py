@@ -50,9 +50,10 @@ def lib():
         L.orc_gather.restype = i64
         L.orc_attention.argtypes = [i64, dbl, dbl, dbl, vp, vp, vp, vp, vp, vp]
         L.orc_attention.restype = None
-        L.orc_forward.argtypes = [i64, i64, i64, i64, dbl, dbl, dbl, vp, vp, vp, vp, vp]
+        L.orc_forward.argtypes = [i64, i64, i64, i64, dbl, dbl, dbl, ctypes.c_int, vp, vp, vp, vp, vp]
         L.orc_forward.restype = ctypes.c_int
-        L.orc_backward.argtypes = [i64, i64, i64, i64, dbl, dbl, dbl, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.orc_backward.argtypes = [i64, i64, i64, i64, dbl, dbl, dbl, ctypes.c_int, vp, vp, vp, vp, vp, vp, vp, vp,
+                                   vp]
         L.orc_backward.restype = ctypes.c_int
         L.orc_embed_backward.argtypes = [i64, i64, i64, i64, i64, i64, i64, ctypes.c_int, vp, vp, vp, vp, vp,
                                          vp, vp]
@@ -134,34 +135,42 @@ def _stack(ws: Sequence, dtype=np.float64) -> np.ndarray:
     return _c(np.stack([_np(w, np.float64) for w in ws]), dtype)
 
 
-def forward(x0, w_down: Sequence, u: Sequence, bias: Sequence, alpha: float, beta: float, tau: float = 1.0):
-    """x_L [B, d] in float64 from storage values (x0, weights as float arrays / torch tensors)."""
+def _rank(U, parallel: bool) -> int:
+    return U.shape[2] // (2 if parallel else 1)
+
+
+def forward(x0, w_down: Sequence, u: Sequence, bias: Sequence, alpha: float, beta: float, tau: float = 1.0,
+            parallel: bool = False):
+    """x_L [B, d] in float64 from storage values (x0, weights as float arrays / torch tensors).
+    parallel: a plain and an attention low-rank cross net with their own weights per layer
+    (w_down [4r, d] = V1, V2, Q, K; u [d, 2r] = [U1 | U2])."""
     x0 = _np(x0, np.float64)
     B, d = x0.shape
     L = len(w_down)
     W, U, b = _stack(w_down), _stack(u), _stack(bias)
-    r = U.shape[2]
+    r = _rank(U, parallel)
     out = np.empty((B, d))
-    rc = lib().orc_forward(B, d, r, L, alpha, beta, tau, _p(x0), _p(W), _p(U), _p(b), _p(out))
+    rc = lib().orc_forward(B, d, r, L, alpha, beta, tau, int(parallel), _p(x0), _p(W), _p(U), _p(b), _p(out))
     if rc != 0:
         raise ValueError("orc_forward: bad arguments")
     return out
 
 
 def backward(x0, w_down: Sequence, u: Sequence, bias: Sequence, grad_out, alpha: float, beta: float,
-             tau: float = 1.0):
-    """(grad_x0 [B, d], g_w_down [L, n*r, d], g_u [L, d, r], g_bias [L, d]) in float64."""
+             tau: float = 1.0, parallel: bool = False):
+    """(grad_x0 [B, d], g_w_down [L, n*r, d], g_u [L, d, hr], g_bias [L, d]) in float64."""
     x0 = _np(x0, np.float64)
     G = _np(grad_out, np.float64)
     B, d = x0.shape
     L = len(w_down)
     W, U, b = _stack(w_down), _stack(u), _stack(bias)
-    r = U.shape[2]
+    r = _rank(U, parallel)
     gx0 = np.empty((B, d))
     gW = np.empty_like(W)
     gU = np.empty_like(U)
     gb = np.empty_like(b)
-    rc = lib().orc_backward(B, d, r, L, alpha, beta, tau, _p(x0), _p(W), _p(U), _p(b), _p(G), _p(gx0), _p(gW),
+    rc = lib().orc_backward(B, d, r, L, alpha, beta, tau, int(parallel), _p(x0), _p(W), _p(U), _p(b), _p(G),
+                            _p(gx0), _p(gW),
                             _p(gU), _p(gb))
     if rc != 0:
         raise ValueError("orc_backward: bad arguments")

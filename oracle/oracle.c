@@ -194,12 +194,12 @@ void orc_attention(int64_t r, double alpha, double beta, double tau, const doubl
 /* Per-layer intermediates of one sample, kept for the backward pass. */
 typedef struct {
     double* x;  /* [L+1][d]  x_0 .. x_L */
-    double* v;  /* [L][r] */
+    double* v;  /* [L][r]   value of the attention (or of the only branch) */
     double* q;  /* [L][r]   (attention only) */
     double* k;  /* [L][r] */
     double* A;  /* [L][r][r] */
     double* o;  /* [L][r] */
-    double* h;  /* [L][r] */
+    double* h;  /* [L][hr]  input of the up projection (hr = 2r with parallel branches) */
     double* t;  /* [L][d] */
 } orc_tape;
 
@@ -207,7 +207,7 @@ static int tape_alloc(orc_tape* tp, int64_t L, int64_t d, int64_t r, int attn) {
     memset(tp, 0, sizeof *tp);
     tp->x = (double*)calloc((size_t)((L + 1) * d), sizeof(double));
     tp->v = (double*)calloc((size_t)(L * r), sizeof(double));
-    tp->h = (double*)calloc((size_t)(L * r), sizeof(double));
+    tp->h = (double*)calloc((size_t)(L * 2 * r), sizeof(double));
     tp->t = (double*)calloc((size_t)(L * d), sizeof(double));
     if (attn) {
         tp->q = (double*)calloc((size_t)(L * r), sizeof(double));
@@ -227,27 +227,42 @@ static void tape_free(orc_tape* tp) {
  * Forward pass of one sample through L layers. Weights per layer l:
  *   w_down + l*n*r*d : [n*r, d], rows 0..r-1 = V^T, r..2r-1 = Q^T, 2r..3r-1 = K^T (n = 3 when
  *                      alpha != 0, else n = 1 and only V^T is present)
- *   u + l*d*r        : [d, r]
+ *   u + l*d*hr       : [d, hr]
  *   bias + l*d       : [d]
+ * With parallel branches (par != 0, alpha != 0) a plain low-rank cross net and an
+ * attention low-rank cross net with their own weights run side by side: n = 4,
+ * rows 0..r-1 = V1^T (plain branch), then V2^T, Q^T, K^T (attention branch);
+ * h = [V1^T x | beta v2 + alpha A v2] has hr = 2r entries and U = [U1 | U2].
  */
-static void sample_forward(int64_t d, int64_t r, int64_t L, double alpha, double beta, double tau,
+static void sample_forward(int64_t d, int64_t r, int64_t L, double alpha, double beta, double tau, int par,
                            const double* x0, const double* w_down, const double* u, const double* bias,
                            orc_tape* tp) {
     const int attn = alpha != 0.0;
-    const int64_t n = attn ? 3 : 1;
+    par = par && attn;
+    const int64_t n = attn ? (par ? 4 : 3) : 1;
+    const int64_t hr = par ? 2 * r : r;
     memcpy(tp->x, x0, sizeof(double) * (size_t)d);
     for (int64_t l = 0; l < L; ++l) {
         const double* W = w_down + l * n * r * d;
-        const double* U = u + l * d * r;
+        const double* U = u + l * d * hr;
         const double* bl = bias + l * d;
         const double* xl = tp->x + l * d;
         double* v = tp->v + l * r;
-        double* h = tp->h + l * r;
+        double* h = tp->h + l * hr;
         double* t = tp->t + l * d;
         double* xn = tp->x + (l + 1) * d;
+        if (par) {  /* plain branch: h[0..r) = V1^T x_l */
+            for (int64_t i = 0; i < r; ++i) {
+                double s = 0.0;
+                for (int64_t c = 0; c < d; ++c) s += W[i * d + c] * xl[c];
+                h[i] = s;
+            }
+        }
+        const double* Wa = par ? W + r * d : W;  /* value, query, key rows of the attention branch */
+        double* ha = par ? h + r : h;
         for (int64_t i = 0; i < r; ++i) {
             double s = 0.0;
-            for (int64_t c = 0; c < d; ++c) s += W[i * d + c] * xl[c];
+            for (int64_t c = 0; c < d; ++c) s += Wa[i * d + c] * xl[c];
             v[i] = s;
         }
         if (attn) {
@@ -256,19 +271,19 @@ static void sample_forward(int64_t d, int64_t r, int64_t L, double alpha, double
             for (int64_t i = 0; i < r; ++i) {
                 double sq = 0.0, sk = 0.0;
                 for (int64_t c = 0; c < d; ++c) {
-                    sq += W[(r + i) * d + c] * xl[c];
-                    sk += W[(2 * r + i) * d + c] * xl[c];
+                    sq += Wa[(r + i) * d + c] * xl[c];
+                    sk += Wa[(2 * r + i) * d + c] * xl[c];
                 }
                 q[i] = sq;
                 k[i] = sk;
             }
-            orc_attention(r, alpha, beta, tau, q, k, v, tp->A + l * r * r, tp->o + l * r, h);
+            orc_attention(r, alpha, beta, tau, q, k, v, tp->A + l * r * r, tp->o + l * r, ha);
         } else {
             for (int64_t i = 0; i < r; ++i) h[i] = beta * v[i];
         }
         for (int64_t c = 0; c < d; ++c) {
             double s = bl[c];
-            for (int64_t i = 0; i < r; ++i) s += U[c * r + i] * h[i];
+            for (int64_t i = 0; i < hr; ++i) s += U[c * hr + i] * h[i];
             t[c] = s;
             xn[c] = x0[c] * s + xl[c];
         }
@@ -276,13 +291,13 @@ static void sample_forward(int64_t d, int64_t r, int64_t L, double alpha, double
 }
 
 /* x_out[b] = x_L of sample b. x0 [B, d], x_out [B, d]. */
-int orc_forward(int64_t B, int64_t d, int64_t r, int64_t L, double alpha, double beta, double tau,
+int orc_forward(int64_t B, int64_t d, int64_t r, int64_t L, double alpha, double beta, double tau, int par,
                 const double* x0, const double* w_down, const double* u, const double* bias, double* x_out) {
     if (B < 0 || d <= 0 || r <= 0 || L <= 0 || tau <= 0.0) return -1;
     orc_tape tp;
     if (!tape_alloc(&tp, L, d, r, alpha != 0.0)) { tape_free(&tp); return -1; }
     for (int64_t b = 0; b < B; ++b) {
-        sample_forward(d, r, L, alpha, beta, tau, x0 + b * d, w_down, u, bias, &tp);
+        sample_forward(d, r, L, alpha, beta, tau, par, x0 + b * d, w_down, u, bias, &tp);
         memcpy(x_out + b * d, tp.x + L * d, sizeof(double) * (size_t)d);
     }
     tape_free(&tp);
@@ -298,24 +313,29 @@ int orc_forward(int64_t B, int64_t d, int64_t r, int64_t L, double alpha, double
  *   attention: do = alpha dh;  dv = beta dh + A^T do;  dS_ij = A_ij do_i (v_j - o_i);
  *              dq_i = sum_j dS_ij k_j / tau;  dk_j = sum_i dS_ij q_i / tau
  *   plain:     dv = beta dh
- *   g_W += [dv; dq; dk] x_l^T;  g <- g + W^T [dv; dq; dk]
+ *   parallel branches: dh = [dh1 | dh2]; the plain branch's value gradient is dh1
+ *              itself and the attention branch takes dh2 as above
+ *   g_W += [dv; dq; dk] x_l^T;  g <- g + W^T [dv; dq; dk]   (with [dv1; dv2; dq; dk] in parallel)
  * and finally grad_x0 = gx0 + g (x0 is both the multiplier of every layer and the first input).
+ * g_u is [L, d, hr].
  */
-int orc_backward(int64_t B, int64_t d, int64_t r, int64_t L, double alpha, double beta, double tau,
+int orc_backward(int64_t B, int64_t d, int64_t r, int64_t L, double alpha, double beta, double tau, int par,
                  const double* x0, const double* w_down, const double* u, const double* bias,
                  const double* grad_out, double* grad_x0, double* g_w_down, double* g_u, double* g_bias) {
     if (B < 0 || d <= 0 || r <= 0 || L <= 0 || tau <= 0.0) return -1;
     const int attn = alpha != 0.0;
-    const int64_t n = attn ? 3 : 1;
+    par = par && attn;
+    const int64_t n = attn ? (par ? 4 : 3) : 1;
+    const int64_t hr = par ? 2 * r : r;
     memset(g_w_down, 0, sizeof(double) * (size_t)(L * n * r * d));
-    memset(g_u, 0, sizeof(double) * (size_t)(L * d * r));
+    memset(g_u, 0, sizeof(double) * (size_t)(L * d * hr));
     memset(g_bias, 0, sizeof(double) * (size_t)(L * d));
     orc_tape tp;
     double* g = (double*)malloc(sizeof(double) * (size_t)d);
     double* gn = (double*)malloc(sizeof(double) * (size_t)d);
     double* gx0 = (double*)malloc(sizeof(double) * (size_t)d);
     double* dt = (double*)malloc(sizeof(double) * (size_t)d);
-    double* dh = (double*)malloc(sizeof(double) * (size_t)r);
+    double* dh = (double*)malloc(sizeof(double) * (size_t)hr);
     double* dP = (double*)malloc(sizeof(double) * (size_t)(n * r));
     double* dS = (double*)malloc(sizeof(double) * (size_t)(r * r));
     int ok = tape_alloc(&tp, L, d, r, attn) && g && gn && gx0 && dt && dh && dP && dS;
@@ -325,45 +345,49 @@ int orc_backward(int64_t B, int64_t d, int64_t r, int64_t L, double alpha, doubl
     }
     for (int64_t b = 0; b < B; ++b) {
         const double* xb0 = x0 + b * d;
-        sample_forward(d, r, L, alpha, beta, tau, xb0, w_down, u, bias, &tp);
+        sample_forward(d, r, L, alpha, beta, tau, par, xb0, w_down, u, bias, &tp);
         memcpy(g, grad_out + b * d, sizeof(double) * (size_t)d);
         memset(gx0, 0, sizeof(double) * (size_t)d);
         for (int64_t l = L - 1; l >= 0; --l) {
             const double* W = w_down + l * n * r * d;
-            const double* U = u + l * d * r;
+            const double* U = u + l * d * hr;
             const double* xl = tp.x + l * d;
-            const double* h = tp.h + l * r;
+            const double* h = tp.h + l * hr;
             const double* t = tp.t + l * d;
             double* gW = g_w_down + l * n * r * d;
-            double* gU = g_u + l * d * r;
+            double* gU = g_u + l * d * hr;
             double* gb = g_bias + l * d;
             for (int64_t c = 0; c < d; ++c) {
                 dt[c] = g[c] * xb0[c];
                 gx0[c] += g[c] * t[c];
                 gb[c] += dt[c];
-                for (int64_t i = 0; i < r; ++i) gU[c * r + i] += dt[c] * h[i];
+                for (int64_t i = 0; i < hr; ++i) gU[c * hr + i] += dt[c] * h[i];
             }
-            for (int64_t i = 0; i < r; ++i) {
+            for (int64_t i = 0; i < hr; ++i) {
                 double s = 0.0;
-                for (int64_t c = 0; c < d; ++c) s += U[c * r + i] * dt[c];
+                for (int64_t c = 0; c < d; ++c) s += U[c * hr + i] * dt[c];
                 dh[i] = s;
             }
+            if (par)  /* plain branch: h1 = v1 */
+                for (int64_t i = 0; i < r; ++i) dP[i] = dh[i];
             if (attn) {
+                const double* dha = par ? dh + r : dh;
+                double* dPa = par ? dP + r : dP;
                 const double* A = tp.A + l * r * r;
                 const double* v = tp.v + l * r;
                 const double* q = tp.q + l * r;
                 const double* k = tp.k + l * r;
                 const double* o = tp.o + l * r;
-                double* dv = dP;
-                double* dq = dP + r;
-                double* dk = dP + 2 * r;
+                double* dv = dPa;
+                double* dq = dPa + r;
+                double* dk = dPa + 2 * r;
                 for (int64_t j = 0; j < r; ++j) {
                     double s = 0.0;
-                    for (int64_t i = 0; i < r; ++i) s += A[i * r + j] * alpha * dh[i];
-                    dv[j] = beta * dh[j] + s;
+                    for (int64_t i = 0; i < r; ++i) s += A[i * r + j] * alpha * dha[i];
+                    dv[j] = beta * dha[j] + s;
                 }
                 for (int64_t i = 0; i < r; ++i)
-                    for (int64_t j = 0; j < r; ++j) dS[i * r + j] = A[i * r + j] * alpha * dh[i] * (v[j] - o[i]);
+                    for (int64_t j = 0; j < r; ++j) dS[i * r + j] = A[i * r + j] * alpha * dha[i] * (v[j] - o[i]);
                 for (int64_t i = 0; i < r; ++i) {
                     double s = 0.0;
                     for (int64_t j = 0; j < r; ++j) s += dS[i * r + j] * k[j];

@@ -28,15 +28,15 @@ MUTATIONS = {
     "temperature_inverted": ("dcn", "row[j] = q[i] * k[j] / tau;", "row[j] = q[i] * k[j] * tau;"),
     "softmax_over_queries": ("dcn", "row[j] = q[i] * k[j] / tau;", "row[j] = q[j] * k[i] / tau;"),
     "skip_dropped": ("dcn", "h[i] = beta * v[i] + alpha * oi;", "h[i] = alpha * oi;"),
-    "up_projection_transposed": ("dcn", "for (int64_t i = 0; i < r; ++i) s += U[c * r + i] * h[i];",
-                                 "for (int64_t i = 0; i < r; ++i) s += U[(i * d + c) % (d * r)] * h[i];"),
+    "up_projection_transposed": ("dcn", "for (int64_t i = 0; i < hr; ++i) s += U[c * hr + i] * h[i];",
+                                 "for (int64_t i = 0; i < hr; ++i) s += U[(i * d + c) % (d * hr)] * h[i];"),
     "bias_dropped": ("dcn", "double s = bl[c];", "double s = 0.0;"),
     "residual_dropped": ("dcn", "xn[c] = x0[c] * s + xl[c];", "xn[c] = x0[c] * s;"),
     "multiplier_x_l_not_x0": ("dcn", "xn[c] = x0[c] * s + xl[c];", "xn[c] = xl[c] * s + xl[c];"),
     "bwd_x0_term_dropped": ("grad", "gx0[c] += g[c] * t[c];", "gx0[c] += 0.0;"),
     "bwd_score_sign": ("grad", "* (v[j] - o[i]);", "* (o[i] - v[j]);"),
     "bwd_key_temperature": ("grad", "dk[j] = s / tau;", "dk[j] = s;"),
-    "bwd_value_skip_dropped": ("grad", "dv[j] = beta * dh[j] + s;", "dv[j] = s;"),
+    "bwd_value_skip_dropped": ("grad", "dv[j] = beta * dha[j] + s;", "dv[j] = s;"),
     "bwd_final_input_term_dropped": ("grad", "grad_x0[b * d + c] = gx0[c] + g[c];", "grad_x0[b * d + c] = gx0[c];"),
     "emb_product_rule_wrong_row": ("grad", "gq[c] += g[c] * (double)rrow[c];", "gq[c] += g[c] * (double)qrow[c];"),
     "quant_middle_weights_swapped": ("quant", "(mx * 128.0f + mn * 127.0f) / 255.0f", "(mx * 127.0f + mn * 128.0f) / 255.0f"),
@@ -47,9 +47,14 @@ MUTATIONS = {
                             "fmaf((float)codes[i * D + c], -params[2 * i + 1], params[2 * i])"),
     "quant_dequant_two_roundings": ("quant", "fmaf((float)codes[i * D + c], params[2 * i + 1], params[2 * i])",
                                     "(float)codes[i * D + c] * params[2 * i + 1] + params[2 * i]"),
+    "par_plain_grad_dropped": ("parallel", "for (int64_t i = 0; i < r; ++i) dP[i] = dh[i];",
+                               "for (int64_t i = 0; i < r; ++i) dP[i] = 0.0;"),
+    "par_attention_reads_plain_rows": ("parallel", "const double* Wa = par ? W + r * d : W;", "const double* Wa = W;"),
+    "par_plain_branch_scaled_by_skip": ("parallel", "                h[i] = s;\n            }\n        }",
+                                        "                h[i] = beta * s;\n            }\n        }"),
 }
 PIN_FILE = {"gather": "test_oracle_gather.py", "dcn": "test_oracle_dcn.py", "grad": "test_oracle_grad.py",
-            "quant": "test_oracle_quant.py"}
+            "quant": "test_oracle_quant.py", "parallel": "test_oracle_parallel.py"}
 
 
 @pytest.mark.parametrize("name", list(MUTATIONS))
