@@ -58,24 +58,27 @@ def kernel_work(wl, B: int) -> dict:
     F, D, Nd = wl.num_cat, wl.emb_dim, wl.num_dense
     hot = wl.bag_mean if wl.multi_hot else 1.0
     L = wl.num_layers
+    hr = wl.h_width          # width of the up projection's input
+    dl = 2 if wl.parallel else 1  # launches of the down and gh GEMMs per layer (plain branch apart)
     w = {}
     # gather: ids, both table rows per id, x0 write, dense read
     w["gather"] = (0.0, B * (F * hot * 8 + 2 * F * hot * D * eb + F * D * eb + 2 * Nd * eb), 0.0)
-    w["fwd_down_gemm"] = (2.0 * B * nr * d, B * d * eb + nr * d * eb + B * nr * pb, 0.0)
+    w["fwd_down_gemm"] = (2.0 * B * nr * d / dl, (dl * B * d * eb + nr * d * eb + B * nr * pb) / dl, 0.0)
     exp_f = 2.0 * EXP_SLOTS
     pair_fwd = (2.0 + exp_f + 1.0) if wl.dtype == "bf16" else (2.0 + exp_f + 3.0)
     pair_bwd = (2.0 + exp_f + 1.0) if wl.dtype == "bf16" else (2 * (2.0 + exp_f) + 11.0)
     stats = 2 * r * 4 if wl.dtype == "bf16" else 0  # saved (o, Z) per row
     w["fwd_attention"] = (0.0, B * (3 * r * 4 + r * eb + stats), pair_fwd * B * r * r)
     # up projection + cross epilogue: h, U, bias, x0, x_l in; t, x_{l+1} out
-    w["fwd_up_gemm"] = (2.0 * B * d * r, B * r * eb + d * r * eb + d * eb + 4 * B * d * eb, 0.0)
+    w["fwd_up_gemm"] = (2.0 * B * d * hr, B * hr * eb + d * hr * eb + d * eb + 4 * B * d * eb, 0.0)
     # average over layers of: g in (storage on the top layer, float below), x0, t, grad_x0 (rmw below top), gt out
     gin = (eb + (L - 1) * 4) / L
     gx = (4 + (L - 1) * 8) / L
     w["bwd_pointwise"] = (0.0, B * d * (gin + 2 * eb + gx + eb), 0.0)
     w["bwd_bias"] = (0.0, -(-B // 128) * d * 4 + d * 4, 0.0)
-    w["bwd_gu_gemm"] = (2.0 * d * r * B, B * d * eb + B * r * eb + d * r * 4, 0.0)
-    w["bwd_gh_gemm"] = (2.0 * B * r * d, B * d * eb + d * r * eb + B * r * (4 if wl.attention else eb), 0.0)
+    w["bwd_gu_gemm"] = (2.0 * d * hr * B, B * d * eb + B * hr * eb + d * hr * 4, 0.0)
+    w["bwd_gh_gemm"] = (2.0 * B * hr * d / dl, (dl * B * d * eb + d * hr * eb + B * hr * (4 if wl.attention else eb)) / dl,
+                        0.0)
     w["bwd_attention"] = (0.0, B * (3 * r * 4 + r * 4 + stats + 3 * r * eb), pair_bwd * B * r * r)
     w["bwd_gw_gemm"] = (2.0 * nr * d * B, B * nr * eb + B * d * eb + nr * d * 4, 0.0)
     w["bwd_gx_gemm"] = (2.0 * B * d * nr, B * nr * eb + nr * d * eb + 2 * B * d * 4, 0.0)
@@ -218,6 +221,8 @@ def main():
     ap.add_argument("--workload", default="small")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle time budget for cpu_baseline (0 = skip)")
     ap.add_argument("--id-mode", default="scatter", choices=["scatter", "rank"])
+    ap.add_argument("--parallel-branch", action="store_true",
+                    help="plain and attention low-rank cross nets with their own weights in every layer")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device-to-device a few times (known traffic, to scale HBM counters)")
     args = ap.parse_args()
@@ -243,6 +248,11 @@ def main():
     from paper_2402_06859_amd.synth import WORKLOADS, make_inputs
 
     wl = WORKLOADS[args.workload]
+    if args.parallel_branch:
+        if not wl.attention:
+            print("--parallel-branch needs a workload with the attention term", file=sys.stderr)
+            sys.exit(2)
+        wl = wl.with_(parallel=True)
     torch.cuda.set_device(0)
     inp = make_inputs(wl, id_mode=args.id_mode)
     db = DeviceBatch(wl, inp)
@@ -306,9 +316,10 @@ def main():
         "dtype": wl.dtype,
         "data": "synthetic (seeded Zipf ids, N(0,1) dense, Xavier weights); inputs resident in HBM",
         "config": {"workload": "%s: batch %d, %d single-hot features (vocab %d, QR tables %dx%d, %s combine), "
-                               "%d dense, d=%d, %d Residual-DCN layers rank %d, attention %s"
+                               "%d dense, d=%d, %d Residual-DCN layers rank %d, attention %s%s"
                                % (wl.name, B, wl.num_cat, wl.vocab, wl.table_rows, wl.emb_dim, wl.combine,
-                                  wl.num_dense, wl.d, wl.num_layers, wl.rank, "on" if wl.attention else "off"),
+                                  wl.num_dense, wl.d, wl.num_layers, wl.rank, "on" if wl.attention else "off",
+                                  ", parallel plain branch" if wl.parallel else ""),
                    "global_batch": B, "id_mode": args.id_mode},
         "roofline": roof,
         "gemm_mfma_frac": (gemm_flops / gemm_s / 1e12 / PEAK_BF16_TFLOPS) if gemm_s > 0 else None,

@@ -66,7 +66,9 @@ typedef enum rdcn_combine { RDCN_COMBINE_MUL = 0, RDCN_COMBINE_SUM = 1 } rdcn_co
 
 /*
  * Model and batch description. d = num_cat * emb_dim + num_dense is derived.
- * n = 3 projections per layer (value, query, key) when attn_alpha != 0, else 1.
+ * n = 3 projections per layer (value, query, key) when attn_alpha != 0, else 1;
+ * n = 4 with parallel branches (plain value, attention value, query, key).
+ * hr = 2r with parallel branches, else r: the width of the up projection's input.
  */
 typedef struct rdcn_config {
     int64_t batch_max;    /* largest batch any call will pass */
@@ -88,13 +90,17 @@ typedef struct rdcn_config {
     float attn_alpha;     /* alpha: weight of the attention path (0 = plain low-rank DCNv2) */
     float skip_beta;      /* beta: weight of the skip (value) path */
     float temperature;    /* tau > 0: scores are q_i k_j / tau */
-    int32_t reserved1;    /* must be 0 */
+    int32_t parallel_branch; /* 0 or 1 (needs attn_alpha != 0): a plain low-rank cross net and the
+                                attention low-rank cross net run side by side with their own
+                                weights (section "Residual DCN", last sentences of the second
+                                paragraph): t = U1 V1^T x + U2 (beta v2 + alpha A v2) + b */
 } rdcn_config;
 
 /*
  * Per-layer weight pointers (entries at index >= num_layers are ignored).
- *   w_down[l] : [n*r, d]  rows 0..r-1 = V_l^T (value), r..2r-1 = Q_l^T, 2r..3r-1 = K_l^T
- *   u[l]      : [d, r]    up projection U_l
+ *   w_down[l] : [n*r, d]  rows 0..r-1 = V_l^T (value), r..2r-1 = Q_l^T, 2r..3r-1 = K_l^T;
+ *                         with parallel branches V1^T (plain branch), V2^T, Q^T, K^T
+ *   u[l]      : [d, hr]   up projection U_l ([U1 | U2] with parallel branches)
  *   bias[l]   : [d]       b_l
  * Weights are in the storage dtype; gradients use the same struct with float pointers.
  */

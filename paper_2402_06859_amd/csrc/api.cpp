@@ -15,8 +15,9 @@
 struct rdcn_handle {
     rdcn_config cfg;
     int64_t d;
-    int n;  // projections per layer (3 with the attention term, else 1)
-    bool bf16, ids64, attn, split;
+    int n;   // projections per layer (3 with the attention term, 4 with parallel branches, else 1)
+    int hr;  // width of the up projection's input (2r with parallel branches, else r)
+    bool bf16, ids64, attn, split, par;
     uint32_t magic, shift;
     int* err;  // device error word
     // per-kernel timing (rdcn_profile_start / rdcn_profile_stop)
@@ -96,9 +97,11 @@ SavedLayout saved_layout(const rdcn_handle* h, int64_t B) {
     size_t off = 0;
     for (int l = 0; l < h->cfg.num_layers; ++l) {
         const bool more = l + 1 < h->cfg.num_layers;
-        s.P[l] = off; off += al(B * n * r * (h->attn ? 4 : e));  // float [v|q|k] feeds the attention
+        // float [v|q|k] feeds the attention (with parallel branches the plain branch's
+        // value goes straight into the first half of H instead)
+        s.P[l] = off; off += al(B * (h->par ? 3 : n) * r * (h->attn ? 4 : e));
         s.P2[l] = off; off += (sp && !h->attn) ? al(B * r * e) : 0;
-        s.H[l] = off; off += h->attn ? al(B * r * e) : 0;
+        s.H[l] = off; off += h->attn ? al(B * (size_t)h->hr * e) : 0;
         s.H2[l] = off; off += (sp && h->attn) ? al(B * r * e) : 0;
         s.A[l] = off; off += (h->attn && h->bf16) ? al(B * 2 * r * 4) : 0;
         s.T[l] = off; off += al(B * d * e);
@@ -115,11 +118,11 @@ struct ScratchLayout {
 };
 
 int64_t splitk_elems(const rdcn_handle* h, int64_t B) {
-    const int64_t d = h->d, r = h->cfg.rank, nr = (int64_t)h->n * r;
-    const GemmPlan pu = plan_gemm(d, r, B, h->bf16, true);
+    const int64_t d = h->d, r = h->cfg.rank, nr = (int64_t)h->n * r, hr = h->hr;
+    const GemmPlan pu = plan_gemm(d, hr, B, h->bf16, true);
     const GemmPlan pw = plan_gemm(nr, d, B, h->bf16, true);
     int64_t m = 0;
-    if (pu.splits > 1) m = pu.splits * d * r;
+    if (pu.splits > 1) m = pu.splits * d * hr;
     if (pw.splits > 1 && pw.splits * nr * d > m) m = pw.splits * nr * d;
     return m;
 }
@@ -230,7 +233,7 @@ rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
         (c.combine != RDCN_COMBINE_MUL && c.combine != RDCN_COMBINE_SUM) || (c.multi_hot != 0 && c.multi_hot != 1) ||
         (c.id_type != RDCN_I32 && c.id_type != RDCN_I64) || (c.dtype != RDCN_F32 && c.dtype != RDCN_BF16) ||
         c.vocab <= 0 || !(c.temperature > 0.0f) || (c.split_activations != 0 && c.split_activations != 1) ||
-        c.reserved1 != 0 ||
+        (c.parallel_branch != 0 && c.parallel_branch != 1) || (c.parallel_branch && c.attn_alpha == 0.0f) ||
         c.attn_alpha != c.attn_alpha || c.skip_beta != c.skip_beta)
         return RDCN_ERR_ARG;
     if ((int64_t)c.qr_rows_q * (int64_t)c.qr_rows_r < c.vocab) return RDCN_ERR_SHAPE;
@@ -243,6 +246,7 @@ rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
     if ((int64_t)c.num_cat * ((int64_t)c.qr_rows_q + c.qr_rows_r) >= (int64_t)1 << 31) return RDCN_ERR_UNSUPPORTED;
     if (c.attn_alpha != 0.0f && c.rank > 1024) return RDCN_ERR_UNSUPPORTED;  // one sample's attention staged in LDS (<= 64 KiB)
     if (c.split_activations && c.dtype != RDCN_BF16) return RDCN_ERR_UNSUPPORTED;  // float storage has nothing to split
+    if (c.split_activations && c.parallel_branch) return RDCN_ERR_UNSUPPORTED;
     (void)n;
 
     rdcn_handle* h = new (std::nothrow) rdcn_handle();
@@ -250,7 +254,9 @@ rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
     h->cfg = c;
     h->d = d;
     h->attn = c.attn_alpha != 0.0f;
-    h->n = h->attn ? 3 : 1;
+    h->par = c.parallel_branch != 0;
+    h->n = h->attn ? (h->par ? 4 : 3) : 1;
+    h->hr = h->par ? 2 * c.rank : c.rank;
     h->bf16 = c.dtype == RDCN_BF16;
     h->ids64 = c.id_type == RDCN_I64;
     h->split = c.split_activations != 0;
@@ -421,16 +427,31 @@ rdcn_status rdcn_forward(rdcn_handle* h, int64_t batch, const void* x0, const rd
     for (int l = 0; l < c.num_layers; ++l) {
         const bool more = l + 1 < c.num_layers;
         void* P = sv + S.P[l];
+        const int64_t hr = h->hr;
+        // parallel branches: the plain branch's value V1^T x_l goes straight into the
+        // first half of H; the attention branch's [v2|q|k] into P as usual
+        const int64_t pr = h->par ? 3 * r : nr;  // width of P
+        const char* wv = (const char*)w->w_down[l] + (h->par ? r * d * (int64_t)eb(h) : 0);
+        if (h->par) {
+            GemmArgs g{};
+            g.M = B; g.N = r; g.K = d;
+            g.a = xcur; g.lda = d;
+            g.b = w->w_down[l]; g.ldb = d;
+            g.epi = EPI_STORE; g.scale = 1.0f;
+            g.c = sv + S.H[l]; g.ldc = hr;
+            ProfScope ps(h, RDCN_KERNEL_FWD_DOWN_GEMM, s);
+            RDCN_TRY(launch_gemm(g, plan_gemm(B, r, d, h->bf16, false), h->bf16, s));
+        }
         GemmArgs g{};
-        g.M = B; g.N = nr; g.K = d;
+        g.M = B; g.N = pr; g.K = d;
         g.a = xcur; g.a2 = xcur2; g.lda = d;
-        g.b = w->w_down[l]; g.ldb = d;
+        g.b = wv; g.ldb = d;
         g.epi = h->attn ? EPI_STORE_F32 : EPI_STORE; g.scale = 1.0f;
-        g.c = P; g.ldc = nr;
+        g.c = P; g.ldc = pr;
         if (h->split && !h->attn) g.c2 = sv + S.P2[l];  // v as hi + lo for the up projection
         {
             ProfScope ps(h, RDCN_KERNEL_FWD_DOWN_GEMM, s);
-            RDCN_TRY(launch_gemm(g, plan_gemm(B, nr, d, h->bf16, false), h->bf16, s));
+            RDCN_TRY(launch_gemm(g, plan_gemm(B, pr, d, h->bf16, false), h->bf16, s));
         }
         const void* hsrc = P;
         const void* hsrc2 = g.c2;
@@ -439,25 +460,26 @@ rdcn_status rdcn_forward(rdcn_handle* h, int64_t batch, const void* x0, const rd
         if (h->attn) {
             void* H = sv + S.H[l];
             void* H2 = h->split ? (void*)(sv + S.H2[l]) : nullptr;
+            void* Ha = (char*)H + (h->par ? r * (int64_t)eb(h) : 0);  // attention output columns of H
             ProfScope ps(h, RDCN_KERNEL_FWD_ATTENTION, s);
-            RDCN_TRY(launch_attn_fwd(B, (int)r, c.attn_alpha, c.skip_beta, c.temperature, P, nr, H, H2, r,
+            RDCN_TRY(launch_attn_fwd(B, (int)r, c.attn_alpha, c.skip_beta, c.temperature, P, pr, Ha, H2, hr,
                                      (float*)(sv + S.A[l]), h->bf16, s));
             hsrc = H;
             hsrc2 = H2;
-            ldh = r;
+            ldh = hr;
             scale = 1.0f;
         }
         void* xnext = more ? (void*)(sv + S.X[l]) : x_out;
         GemmArgs u{};
-        u.M = B; u.N = d; u.K = r;
+        u.M = B; u.N = d; u.K = hr;
         u.a = hsrc; u.a2 = hsrc2; u.lda = ldh;
-        u.b = w->u[l]; u.ldb = r;
+        u.b = w->u[l]; u.ldb = hr;
         u.epi = EPI_CROSS; u.scale = scale;
         u.c = xnext; u.c2 = (h->split && more) ? (void*)(sv + S.X2[l]) : nullptr; u.ldc = d;
         u.bias = w->bias[l]; u.x0 = x0; u.xl = xcur; u.xl2 = xcur2; u.t_out = sv + S.T[l]; u.ldx = d;
         {
             ProfScope ps(h, RDCN_KERNEL_FWD_UP_GEMM, s);
-            RDCN_TRY(launch_gemm(u, plan_gemm(B, d, r, h->bf16, false), h->bf16, s));
+            RDCN_TRY(launch_gemm(u, plan_gemm(B, d, hr, h->bf16, false), h->bf16, s));
         }
         xcur = xnext;
         xcur2 = u.c2;
@@ -511,23 +533,35 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
             RDCN_TRY(launch_colsum(part, W.nrb, d, (float*)grads->bias[l], s));
         }
         const void* hsrc = h->attn ? (const void*)(sv + S.H[l]) : P;
-        const int64_t ldh = h->attn ? r : nr;
+        const int64_t hr = h->hr;
+        const int64_t ldh = h->attn ? hr : nr;
         const float hscale = h->attn ? 1.0f : c.skip_beta;
-        // gU = gt^T h      [d, r], K = batch
+        const int64_t e = (int64_t)eb(h);
+        // gU = gt^T h      [d, hr], K = batch
         {
             GemmArgs g1{};
-            g1.M = d; g1.N = r; g1.K = B;
+            g1.M = d; g1.N = hr; g1.K = B;
             g1.a = gt; g1.lda = d; g1.a_kstrided = true;
             g1.b = hsrc; g1.ldb = ldh; g1.b_kstrided = true;
             g1.scale = hscale;
             RDCN_TRY(gemm_weight_grad(h, RDCN_KERNEL_BWD_GU_GEMM, g1, (float*)grads->u[l], splitk, s));
         }
-        // gh = gt U         [B, r]
+        // gh = gt U         [B, hr]; with parallel branches the plain branch's part is its
+        // value gradient and goes straight into the first columns of gP
+        if (h->par) {
+            GemmArgs g2{};
+            g2.M = B; g2.N = r; g2.K = d;
+            g2.a = gt; g2.lda = d;
+            g2.b = w->u[l]; g2.ldb = hr; g2.b_kstrided = true;
+            g2.epi = EPI_STORE; g2.scale = 1.0f; g2.c = gP; g2.ldc = nr;
+            ProfScope ps(h, RDCN_KERNEL_BWD_GH_GEMM, s);
+            RDCN_TRY(launch_gemm(g2, plan_gemm(B, r, d, h->bf16, false), h->bf16, s));
+        }
         {
             GemmArgs g2{};
             g2.M = B; g2.N = r; g2.K = d;
             g2.a = gt; g2.lda = d;
-            g2.b = w->u[l]; g2.ldb = r; g2.b_kstrided = true;
+            g2.b = (const char*)w->u[l] + (h->par ? r * e : 0); g2.ldb = hr; g2.b_kstrided = true;
             if (h->attn) {
                 g2.epi = EPI_STORE_F32; g2.scale = 1.0f; g2.c = gh; g2.ldc = r;
             } else {
@@ -537,9 +571,11 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
             RDCN_TRY(launch_gemm(g2, plan_gemm(B, r, d, h->bf16, false), h->bf16, s));
         }
         if (h->attn) {
+            const int64_t pr = h->par ? 3 * r : nr;
             ProfScope ps(h, RDCN_KERNEL_BWD_ATTENTION, s);
-            RDCN_TRY(launch_attn_bwd(B, (int)r, c.attn_alpha, c.skip_beta, c.temperature, P, nr,
-                                     (const float*)(sv + S.A[l]), gh, r, gP, nr, h->bf16, s));
+            RDCN_TRY(launch_attn_bwd(B, (int)r, c.attn_alpha, c.skip_beta, c.temperature, P, pr,
+                                     (const float*)(sv + S.A[l]), gh, r, (char*)gP + (h->par ? r * e : 0), nr,
+                                     h->bf16, s));
         }
         // gW = gP^T x_l    [n r, d], K = batch
         {

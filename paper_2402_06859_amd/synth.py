@@ -48,6 +48,7 @@ class Workload:
     temperature: float = 1.0
     skip_beta: float = 1.0
     split_activations: bool = False  # activations as hi + lo bf16 pairs (deep attention stacks)
+    parallel: bool = False           # plain + attention low-rank cross nets with their own weights
 
     @property
     def d(self) -> int:
@@ -68,7 +69,12 @@ class Workload:
 
     @property
     def n_proj(self) -> int:
-        return 3 if self.attention else 1
+        return (4 if self.parallel else 3) if self.attention else 1
+
+    @property
+    def h_width(self) -> int:
+        """Width of the up projection's input (2r with parallel branches)."""
+        return 2 * self.rank if (self.parallel and self.attention) else self.rank
 
     def with_(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)
@@ -196,7 +202,8 @@ def make_inputs(wl: Workload, seed: Optional[int] = None, id_mode: str = "scatte
 
 
 def make_weights(wl: Workload, rng: np.random.Generator, bias_std: float = 0.0) -> dict:
-    """Xavier-normal projections (std sqrt(2/(d+r))), bias N(0, bias_std^2) (0 by default)."""
+    """Xavier-normal projections (std sqrt(2/(d+r))), bias N(0, bias_std^2) (0 by default).
+    With parallel branches w_down stacks (V1, V2, Q, K) and u is [U1 | U2]."""
     d, r, n = wl.d, wl.rank, wl.n_proj
     std = math.sqrt(2.0 / (d + r))
     w_down: List = []
@@ -204,7 +211,7 @@ def make_weights(wl: Workload, rng: np.random.Generator, bias_std: float = 0.0) 
     bias: List = []
     for _ in range(wl.num_layers):
         w_down.append(to_storage(rng.standard_normal((n * r, d), dtype=np.float32) * std, wl.dtype))
-        u.append(to_storage(rng.standard_normal((d, r), dtype=np.float32) * std, wl.dtype))
+        u.append(to_storage(rng.standard_normal((d, wl.h_width), dtype=np.float32) * std, wl.dtype))
         b = rng.standard_normal(d, dtype=np.float32) * bias_std if bias_std > 0 else np.zeros(d, np.float32)
         bias.append(to_storage(b, wl.dtype))
     return {"w_down": w_down, "u": u, "bias": bias}

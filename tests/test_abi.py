@@ -108,3 +108,17 @@ def test_quantization_entry_points_reject_null_handle():
     L = rdcn.load()
     assert L.qr_quantize_tables(None, 4, None, None, None, None) == rdcn.RDCN_ERR_ARG
     assert L.qr_embed_gather_q8(None, 4, None, None, None, None, None, None, None, None, None) == rdcn.RDCN_ERR_ARG
+
+
+def test_parallel_branch_validation():
+    L = rdcn.load()
+    h = ctypes.c_void_p()
+    c = good()
+    c.parallel_branch = 2
+    assert L.rdcn_create(ctypes.byref(c), ctypes.byref(h)) == rdcn.RDCN_ERR_ARG
+    c = good()
+    c.parallel_branch, c.attn_alpha = 1, 0.0
+    assert L.rdcn_create(ctypes.byref(c), ctypes.byref(h)) == rdcn.RDCN_ERR_ARG
+    c = good()
+    c.parallel_branch, c.split_activations = 1, 1
+    assert L.rdcn_create(ctypes.byref(c), ctypes.byref(h)) == rdcn.RDCN_ERR_UNSUPPORTED

@@ -42,13 +42,14 @@ def run_full_compare(wl: Workload, seed=None, grad_rows=None, fwd_rows=None, bia
     x0_ref = oracle_x0(wl, inp)
     W, U, b = host_weights(inp)
     rows = np.arange(B) if fwd_rows is None else fwd_rows
-    xL = oracle.forward(x0_ref[rows], W, U, b, wl.alpha, wl.beta, wl.temperature)
+    xL = oracle.forward(x0_ref[rows], W, U, b, wl.alpha, wl.beta, wl.temperature, parallel=wl.parallel)
     tol = FWD_TOL[wl.dtype] if fwd_tol is None else fwd_tol
     e_fwd = relerr(to_np(db.x_out)[rows], xL)
     assert e_fwd <= tol, "forward rel err %.3g > %.3g" % (e_fwd, tol)
     grows = np.arange(B) if grad_rows is None else grad_rows
     G = inp["grad_out"].float().numpy()
-    gx0, gW, gU, gb = oracle.backward(x0_ref[grows], W, U, b, G[grows], wl.alpha, wl.beta, wl.temperature)
+    gx0, gW, gU, gb = oracle.backward(x0_ref[grows], W, U, b, G[grows], wl.alpha, wl.beta, wl.temperature,
+                                      parallel=wl.parallel)
     gtol = (1e-4 if wl.dtype == "f32" else GRAD_TOL) if grad_tol is None else grad_tol
     got_gx0 = to_np(db.grad_x0)
     errs = {"grad_x0": relerr(got_gx0[grows], gx0)}
@@ -97,6 +98,29 @@ def test_attention_multiwave_ragged(rank, batch):
     need_gpu()
     wl = Workload("multiwave", 15, batch, 4, 20_000, 150, 16, 64, 2, rank, True, "bf16", "sum", 1.1)
     run_full_compare(wl)
+
+
+@pytest.mark.parametrize("tau,beta", [(1.0, 1.0), (0.25, 0.5), (4.0, 0.0)])
+def test_parallel_branches_ragged(tau, beta):
+    """Plain and attention low-rank cross nets with their own weights: batch 300, d = 160,
+    r = 40 (no tile multiples), two layers."""
+    need_gpu()
+    wl = Workload("parallel", 16, 300, 5, 50_000, 250, 24, 40, 2, 40, True, "bf16", "sum", 1.1, temperature=tau,
+                  parallel=True)
+    run_full_compare(wl.with_(skip_beta=beta))
+
+
+def test_parallel_branches_fp32_ragged():
+    need_gpu()
+    wl = Workload("parallel32", 17, 130, 3, 10_000, 100, 16, 12, 3, 20, True, "f32", "mul", 1.1, parallel=True)
+    run_full_compare(wl)
+
+
+def test_parallel_branches_small_full_batch_sampled():
+    need_gpu()
+    wl = WORKLOADS["small"].with_(parallel=True)
+    rows = sample_rows(wl.batch, 24)
+    run_full_compare(wl, grad_rows=rows, fwd_rows=rows)
 
 
 def test_fp32_attention_ragged():
