@@ -500,7 +500,7 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
     if (batch == 0) {  // gradients of an empty batch are zero
         for (int l = 0; l < c.num_layers; ++l) {
             RDCN_TRY(launch_fill_zero((float*)grads->w_down[l], nr * d, s));
-            RDCN_TRY(launch_fill_zero((float*)grads->u[l], d * r, s));
+            RDCN_TRY(launch_fill_zero((float*)grads->u[l], d * (int64_t)h->hr, s));
             RDCN_TRY(launch_fill_zero((float*)grads->bias[l], d, s));
         }
         return RDCN_OK;
