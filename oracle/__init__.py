@@ -65,6 +65,17 @@ def lib():
         L.orc_gather_q8.argtypes = [i64, i64, i64, i64, i64, i64, i64, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp,
                                     vp, vp, vp, vp]
         L.orc_gather_q8.restype = i64
+        u64 = ctypes.c_uint64
+        L.orc_murmur64a.argtypes = [vp, i64, u64]
+        L.orc_murmur64a.restype = u64
+        L.orc_hash_ids.argtypes = [vp, i64, u64, vp]
+        L.orc_hash_ids.restype = None
+        L.orc_gather_hashed.argtypes = [i64, i64, i64, i64, i64, i64, ctypes.c_int, ctypes.c_int, u64, vp, vp, vp, vp,
+                                        vp, vp]
+        L.orc_gather_hashed.restype = i64
+        L.orc_embed_backward_hashed.argtypes = [i64, i64, i64, i64, i64, i64, ctypes.c_int, u64, vp, vp, vp, vp, vp,
+                                                vp, vp]
+        L.orc_embed_backward_hashed.restype = i64
         _lib = L
     return _lib
 
@@ -231,3 +242,50 @@ def gather_q8(B: int, F: int, D: int, Nd: int, vocab: int, rows_q: int, m: int, 
     if bad < 0:
         raise ValueError("orc_gather_q8: bad arguments")
     return x0, int(bad)
+
+
+def murmur64a(data: bytes, seed: int = 0) -> int:
+    """MurmurHash64A of a byte string."""
+    buf = ctypes.create_string_buffer(bytes(data), max(len(data), 1))
+    return int(lib().orc_murmur64a(buf, len(data), seed))
+
+
+def hash_ids(ids, seed: int = 0) -> np.ndarray:
+    """uint64 MurmurHash64A of each id's 8 little-endian bytes."""
+    ids = _np(ids, np.int64).reshape(-1)
+    out = np.empty(ids.size, np.uint64)
+    lib().orc_hash_ids(_p(ids), ids.size, seed, _p(out))
+    return out
+
+
+def gather_hashed(B: int, F: int, D: int, Nd: int, rows_q: int, m: int, combine: str, bf16: bool, seed: int,
+                  ids, offsets, q_tables, r_tables, dense):
+    """x0 [B, F*D+Nd] float32 of the hashed front-end (tables [F, 2, rows, D])."""
+    ids = _np(ids, np.int64)
+    offsets = _np(offsets, np.int64)
+    qt = _np(q_tables, np.float32)
+    rt = _np(r_tables, np.float32)
+    dn = _np(dense, np.float32)
+    x0 = np.empty((B, F * D + Nd), np.float32)
+    rc = lib().orc_gather_hashed(B, F, D, Nd, rows_q, m, COMBINE[combine], int(bf16), seed, _p(ids), _p(offsets),
+                                 _p(qt), _p(rt), _p(dn), _p(x0))
+    if rc < 0:
+        raise ValueError("orc_gather_hashed: bad arguments")
+    return x0
+
+
+def embed_backward_hashed(B: int, F: int, D: int, Nd: int, rows_q: int, m: int, combine: str, seed: int, ids,
+                          offsets, q_tables, r_tables, grad_x0):
+    """Table gradients (float64 [F, 2, rows, D]) of the hashed front-end."""
+    ids = _np(ids, np.int64)
+    offsets = _np(offsets, np.int64)
+    qt = _np(q_tables, np.float32)
+    rt = _np(r_tables, np.float32)
+    g = _np(grad_x0, np.float64)
+    gq = np.zeros((F, 2, rows_q, D))
+    gr = np.zeros((F, 2, m, D))
+    rc = lib().orc_embed_backward_hashed(B, F, D, Nd, rows_q, m, COMBINE[combine], seed, _p(ids), _p(offsets),
+                                         _p(qt), _p(rt), _p(g), _p(gq), _p(gr))
+    if rc < 0:
+        raise ValueError("orc_embed_backward_hashed: bad arguments")
+    return gq, gr

@@ -538,3 +538,149 @@ int64_t orc_gather_q8(int64_t B, int64_t F, int64_t D, int64_t Nd, int64_t vocab
     free(rt);
     return bad;
 }
+
+/* ------------------------------------------------------- hashed front-end */
+
+/*
+ * Appendix "Vocabulary Compression" and section "Model Dictionary Compression":
+ * a raw id is mapped by a stateless collision-resistant hash (Murmur) to int64,
+ * the 64 bits are reinterpreted as two 32-bit numbers B (low half) and C (high
+ * half), and each indexes its own set of QR tables. The hash here is
+ * MurmurHash64A (the 64-bit member of Austin Appleby's MurmurHash2 family),
+ * written from its published description: 8-byte little-endian blocks mixed by
+ * multiply / xor-shift with m = 0xc6a4a7935bd1e995 and r = 47, a tail of up to 7
+ * bytes folded in, then a final xor-shift / multiply / xor-shift.
+ */
+uint64_t orc_murmur64a(const void* key, int64_t len, uint64_t seed) {
+    const uint64_t m = 0xc6a4a7935bd1e995ull;
+    const int r = 47;
+    const uint8_t* p = (const uint8_t*)key;
+    uint64_t h = seed ^ ((uint64_t)len * m);
+    const int64_t nblocks = len / 8;
+    for (int64_t i = 0; i < nblocks; ++i) {
+        uint64_t k = 0;
+        for (int b = 7; b >= 0; --b) k = (k << 8) | p[8 * i + b];
+        k *= m;
+        k ^= k >> r;
+        k *= m;
+        h ^= k;
+        h *= m;
+    }
+    const uint8_t* t = p + 8 * nblocks;
+    const int rest = (int)(len & 7);
+    if (rest > 0) {
+        for (int b = rest - 1; b >= 0; --b) h ^= (uint64_t)t[b] << (8 * b);
+        h *= m;
+    }
+    h ^= h >> r;
+    h *= m;
+    h ^= h >> r;
+    return h;
+}
+
+/* Hash of every id: its 8 bytes in little-endian order. */
+void orc_hash_ids(const int64_t* ids, int64_t n, uint64_t seed, uint64_t* out) {
+    for (int64_t i = 0; i < n; ++i) {
+        uint8_t bytes[8];
+        uint64_t v = (uint64_t)ids[i];
+        for (int b = 0; b < 8; ++b) bytes[b] = (uint8_t)(v >> (8 * b));
+        out[i] = orc_murmur64a(bytes, 8, seed);
+    }
+}
+
+/*
+ * Gather with the hashed front-end. q_tables [F, 2, rows_q, D] and r_tables
+ * [F, 2, m, D]: pair 0 serves the low half B, pair 1 the high half C of each
+ * id's hash; each half x in [0, 2^32) is QR-split (qi = x / m, ri = x mod m; needs
+ * rows_q * m >= 2^32). The element of one id is (Q0[qi_B] op R0[ri_B]) + (Q1[qi_C]
+ * op R1[ri_C]) in float: each combine one float operation, the two halves summed
+ * (the paper does not say how the two look-ups are aggregated; the sum is the
+ * aggregation it found best for QR). Bags pool as in orc_gather. Every id is valid.
+ */
+int64_t orc_gather_hashed(int64_t B, int64_t F, int64_t D, int64_t Nd, int64_t rows_q, int64_t m, int combine,
+                          int round_bf16, uint64_t seed, const int64_t* ids, const int64_t* offsets,
+                          const float* q_tables, const float* r_tables, const float* dense, float* x0) {
+    if (B < 0 || F < 0 || D <= 0 || Nd < 0 || m <= 0 || rows_q <= 0) return -1;
+    if ((uint64_t)rows_q * (uint64_t)m < ((uint64_t)1 << 32)) return -1;
+    const int64_t d = F * D + Nd;
+    float* acc = (float*)malloc(sizeof(float) * (size_t)D);
+    for (int64_t b = 0; b < B; ++b) {
+        for (int64_t f = 0; f < F; ++f) {
+            int64_t begin = offsets ? offsets[b * F + f] : b * F + f;
+            int64_t end = offsets ? offsets[b * F + f + 1] : begin + 1;
+            int started = 0;
+            for (int64_t p = begin; p < end; ++p) {
+                uint64_t hsh;
+                orc_hash_ids(&ids[p], 1, seed, &hsh);
+                const uint64_t half[2] = {hsh & 0xffffffffull, hsh >> 32};
+                const float* qrow[2];
+                const float* rrow[2];
+                for (int s = 0; s < 2; ++s) {
+                    const uint64_t qi = half[s] / (uint64_t)m, ri = half[s] % (uint64_t)m;
+                    qrow[s] = q_tables + ((f * 2 + s) * rows_q + (int64_t)qi) * D;
+                    rrow[s] = r_tables + ((f * 2 + s) * m + (int64_t)ri) * D;
+                }
+                for (int64_t c = 0; c < D; ++c) {
+                    float e0 = (combine == ORC_COMBINE_MUL) ? qrow[0][c] * rrow[0][c] : qrow[0][c] + rrow[0][c];
+                    float e1 = (combine == ORC_COMBINE_MUL) ? qrow[1][c] * rrow[1][c] : qrow[1][c] + rrow[1][c];
+                    float e = e0 + e1;
+                    acc[c] = started ? acc[c] + e : e;
+                }
+                started = 1;
+            }
+            float* dst = x0 + b * d + f * D;
+            for (int64_t c = 0; c < D; ++c) {
+                float v = started ? acc[c] : 0.0f;
+                dst[c] = round_bf16 ? orc_round_bf16(v) : v;
+            }
+        }
+        for (int64_t j = 0; j < Nd; ++j) x0[b * d + F * D + j] = dense[b * Nd + j];
+    }
+    free(acc);
+    return 0;
+}
+
+/*
+ * Table gradients of the hashed gather (accumulated, in (b, p) order), g =
+ * grad_x0[b, f*D : (f+1)*D], for both halves s of every id:
+ *   sum combine:      gQs[qi_s] += g,               gRs[ri_s] += g
+ *   product combine:  gQs[qi_s] += g * Rs[ri_s],    gRs[ri_s] += g * Qs[qi_s]
+ * grad_q [F, 2, rows_q, D], grad_r [F, 2, m, D].
+ */
+int64_t orc_embed_backward_hashed(int64_t B, int64_t F, int64_t D, int64_t Nd, int64_t rows_q, int64_t m,
+                                  int combine, uint64_t seed, const int64_t* ids, const int64_t* offsets,
+                                  const float* q_tables, const float* r_tables, const double* grad_x0,
+                                  double* grad_q, double* grad_r) {
+    if (B < 0 || F < 0 || D <= 0 || Nd < 0 || m <= 0 || rows_q <= 0) return -1;
+    if ((uint64_t)rows_q * (uint64_t)m < ((uint64_t)1 << 32)) return -1;
+    const int64_t d = F * D + Nd;
+    for (int64_t b = 0; b < B; ++b) {
+        for (int64_t f = 0; f < F; ++f) {
+            int64_t begin = offsets ? offsets[b * F + f] : b * F + f;
+            int64_t end = offsets ? offsets[b * F + f + 1] : begin + 1;
+            const double* g = grad_x0 + b * d + f * D;
+            for (int64_t p = begin; p < end; ++p) {
+                uint64_t hsh;
+                orc_hash_ids(&ids[p], 1, seed, &hsh);
+                for (int s = 0; s < 2; ++s) {
+                    const uint64_t x = s ? hsh >> 32 : hsh & 0xffffffffull;
+                    const int64_t qi = (int64_t)(x / (uint64_t)m), ri = (int64_t)(x % (uint64_t)m);
+                    double* gq = grad_q + ((f * 2 + s) * rows_q + qi) * D;
+                    double* gr = grad_r + ((f * 2 + s) * m + ri) * D;
+                    const float* qrow = q_tables + ((f * 2 + s) * rows_q + qi) * D;
+                    const float* rrow = r_tables + ((f * 2 + s) * m + ri) * D;
+                    for (int64_t c = 0; c < D; ++c) {
+                        if (combine == ORC_COMBINE_MUL) {
+                            gq[c] += g[c] * (double)rrow[c];
+                            gr[c] += g[c] * (double)qrow[c];
+                        } else {
+                            gq[c] += g[c];
+                            gr[c] += g[c];
+                        }
+                    }
+                }
+            }
+        }
+    }
+    return 0;
+}

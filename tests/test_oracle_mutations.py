@@ -52,9 +52,24 @@ MUTATIONS = {
     "par_attention_reads_plain_rows": ("parallel", "const double* Wa = par ? W + r * d : W;", "const double* Wa = W;"),
     "par_plain_branch_scaled_by_skip": ("parallel", "                h[i] = s;\n            }\n        }",
                                         "                h[i] = beta * s;\n            }\n        }"),
+    "hash_shift_46": ("hash", "const int r = 47;", "const int r = 46;"),
+    "hash_final_mix_dropped": ("hash", "    h ^= h >> r;\n    h *= m;\n    h ^= h >> r;\n    return h;",
+                               "    h ^= h >> r;\n    h *= m;\n    return h;"),
+    "hash_big_endian_blocks": ("hash", "for (int b = 7; b >= 0; --b) k = (k << 8) | p[8 * i + b];",
+                               "for (int b = 0; b < 8; ++b) k = (k << 8) | p[8 * i + b];"),
+    "hash_halves_swapped": ("hash", "const uint64_t half[2] = {hsh & 0xffffffffull, hsh >> 32};",
+                            "const uint64_t half[2] = {hsh >> 32, hsh & 0xffffffffull};"),
+    "hash_bwd_other_row": ("hash", "                            gq[c] += g[c] * (double)rrow[c];\n"
+                           "                            gr[c] += g[c] * (double)qrow[c];\n                        } else {\n"
+                           "                            gq[c] += g[c];\n                            gr[c] += g[c];\n"
+                           "                        }\n                    }\n                }",
+                           "                            gq[c] += g[c] * (double)qrow[c];\n"
+                           "                            gr[c] += g[c] * (double)qrow[c];\n                        } else {\n"
+                           "                            gq[c] += g[c];\n                            gr[c] += g[c];\n"
+                           "                        }\n                    }\n                }"),
 }
 PIN_FILE = {"gather": "test_oracle_gather.py", "dcn": "test_oracle_dcn.py", "grad": "test_oracle_grad.py",
-            "quant": "test_oracle_quant.py", "parallel": "test_oracle_parallel.py"}
+            "quant": "test_oracle_quant.py", "parallel": "test_oracle_parallel.py", "hash": "test_oracle_hash.py"}
 
 
 @pytest.mark.parametrize("name", list(MUTATIONS))
