@@ -94,6 +94,15 @@ typedef struct rdcn_config {
                                 attention low-rank cross net run side by side with their own
                                 weights (section "Residual DCN", last sentences of the second
                                 paragraph): t = U1 V1^T x + U2 (beta v2 + alpha A v2) + b */
+    int32_t hashed;       /* 0 or 1: hashed front-end (appendix "Vocabulary Compression"): every
+                             raw id is hashed with MurmurHash64A (its 8 little-endian bytes,
+                             seed hash_seed); the low 32 bits B and the high 32 bits C each
+                             index their own QR table pair, and the two combined rows are
+                             summed. Tables become [F, 2, rows, D] (pair 0 for B, 1 for C),
+                             vocab must be 0 (every id is valid), and qr_rows_q * m must
+                             reach 2^32 */
+    int32_t reserved2;    /* must be 0 */
+    uint64_t hash_seed;   /* seed of the hashed front-end */
 } rdcn_config;
 
 /*

@@ -189,6 +189,8 @@ rdcn_status gather_args(rdcn_handle* h, int64_t batch, const void* ids, const in
     a.magic = h->magic;
     a.shift = h->shift;
     a.combine = c.combine == RDCN_COMBINE_MUL ? 0 : 1;
+    a.hashed = c.hashed;
+    a.seed = c.hash_seed;
     a.ids = ids;
     a.offsets = offsets;
     a.q_tables = q_tables;
@@ -232,18 +234,22 @@ rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
         c.num_layers < 1 || c.num_layers > RDCN_MAX_LAYERS || c.qr_rows_q <= 0 || c.qr_rows_r <= 0 ||
         (c.combine != RDCN_COMBINE_MUL && c.combine != RDCN_COMBINE_SUM) || (c.multi_hot != 0 && c.multi_hot != 1) ||
         (c.id_type != RDCN_I32 && c.id_type != RDCN_I64) || (c.dtype != RDCN_F32 && c.dtype != RDCN_BF16) ||
-        c.vocab <= 0 || !(c.temperature > 0.0f) || (c.split_activations != 0 && c.split_activations != 1) ||
+        (c.hashed != 0 && c.hashed != 1) || c.reserved2 != 0 || (c.hashed ? c.vocab != 0 : c.vocab <= 0) ||
+        !(c.temperature > 0.0f) || (c.split_activations != 0 && c.split_activations != 1) ||
         (c.parallel_branch != 0 && c.parallel_branch != 1) || (c.parallel_branch && c.attn_alpha == 0.0f) ||
         c.attn_alpha != c.attn_alpha || c.skip_beta != c.skip_beta)
         return RDCN_ERR_ARG;
-    if ((int64_t)c.qr_rows_q * (int64_t)c.qr_rows_r < c.vocab) return RDCN_ERR_SHAPE;
+    // ids in [0, vocab) (hashed: both 32-bit hash halves) must reach only existing rows
+    const int64_t id_space = c.hashed ? ((int64_t)1 << 32) : c.vocab;
+    if ((int64_t)c.qr_rows_q * (int64_t)c.qr_rows_r < id_space) return RDCN_ERR_SHAPE;
     const int64_t d = (int64_t)c.num_cat * c.emb_dim + c.num_dense;
     if (d <= 0) return RDCN_ERR_SHAPE;
     const int vec = c.dtype == RDCN_BF16 ? 8 : 4;
     if (c.emb_dim % vec || c.num_dense % vec || c.rank % vec || c.emb_dim > 256) return RDCN_ERR_UNSUPPORTED;
     const int n = c.attn_alpha != 0.0f ? 3 : 1;
     // sort keys and occurrence indices are 32-bit
-    if ((int64_t)c.num_cat * ((int64_t)c.qr_rows_q + c.qr_rows_r) >= (int64_t)1 << 31) return RDCN_ERR_UNSUPPORTED;
+    if ((int64_t)c.num_cat * (c.hashed ? 2 : 1) * ((int64_t)c.qr_rows_q + c.qr_rows_r) >= (int64_t)1 << 31)
+        return RDCN_ERR_UNSUPPORTED;
     if (c.attn_alpha != 0.0f && c.rank > 1024) return RDCN_ERR_UNSUPPORTED;  // one sample's attention staged in LDS (<= 64 KiB)
     if (c.split_activations && c.dtype != RDCN_BF16) return RDCN_ERR_UNSUPPORTED;  // float storage has nothing to split
     if (c.split_activations && c.parallel_branch) return RDCN_ERR_UNSUPPORTED;
@@ -345,10 +351,10 @@ rdcn_status qr_embed_backward_workspace(const rdcn_handle* h, int64_t batch, int
     if (st != RDCN_OK) return st;
     if (!scratch_bytes || nnz < 0) return RDCN_ERR_ARG;
     if (!h->cfg.multi_hot && nnz != batch * h->cfg.num_cat) return RDCN_ERR_SHAPE;
-    if (2 * nnz >= ((int64_t)1 << 31)) return RDCN_ERR_UNSUPPORTED;
+    if (emb_pairs(nnz, h->cfg.hashed != 0) >= ((int64_t)1 << 31)) return RDCN_ERR_UNSUPPORTED;
     const EmbedBwdLayout L =
         embed_bwd_layout(nnz, h->cfg.num_cat, h->cfg.qr_rows_q, h->cfg.qr_rows_r, h->cfg.emb_dim, h->cfg.multi_hot,
-                         h->cfg.combine == RDCN_COMBINE_MUL);
+                         h->cfg.combine == RDCN_COMBINE_MUL, h->cfg.hashed != 0);
     *scratch_bytes = al(L.total);
     return RDCN_OK;
 }
@@ -377,6 +383,8 @@ rdcn_status qr_embed_backward(rdcn_handle* h, int64_t batch, int64_t nnz, const 
     a.m = (uint32_t)c.qr_rows_r;
     a.vocab = (uint64_t)c.vocab;
     a.combine = c.combine == RDCN_COMBINE_MUL ? 0 : 1;
+    a.hashed = c.hashed;
+    a.seed = c.hash_seed;
     a.ids = ids;
     a.offsets = offsets;
     a.q_tables = q_tables;

@@ -70,4 +70,20 @@ __device__ __forceinline__ uint32_t div_magic(uint32_t n, const DivMagic& dm) {
     return (t + ((n - t) >> 1)) >> dm.shift;
 }
 
+// MurmurHash64A (Austin Appleby, MurmurHash2 family) of one 8-byte key, from the
+// published description: the key's little-endian bytes are one block.
+__device__ __forceinline__ uint64_t murmur64a_8(uint64_t key, uint64_t seed) {
+    const uint64_t m = 0xc6a4a7935bd1e995ull;
+    uint64_t h = seed ^ (8ull * m);
+    uint64_t k = key * m;
+    k ^= k >> 47;
+    k *= m;
+    h ^= k;
+    h *= m;
+    h ^= h >> 47;
+    h *= m;
+    h ^= h >> 47;
+    return h;
+}
+
 }  // namespace rdcn

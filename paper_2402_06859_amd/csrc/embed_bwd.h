@@ -11,6 +11,8 @@ struct EmbedBwdArgs {
     uint32_t m;
     uint64_t vocab;
     int combine;             // 0 = product, 1 = sum
+    int hashed;              // 1: hashed front-end, two (Q, R) pairs per feature and four keys per id
+    uint64_t seed;           // hash seed
     const void* ids;
     const int64_t* offsets;  // NULL = single-hot
     const void* q_tables;
@@ -27,7 +29,9 @@ struct EmbedBwdLayout {
     int bits, passes, dbits;
 };
 
-EmbedBwdLayout embed_bwd_layout(int64_t nnz, int F, int rows_q, int m, int D, bool bags, bool mul);
+// (key, occurrence) pairs the embedding backward sorts: two per id, four when hashed
+inline int64_t emb_pairs(int64_t nnz, bool hashed) { return (hashed ? 4 : 2) * nnz; }
+EmbedBwdLayout embed_bwd_layout(int64_t nnz, int F, int rows_q, int m, int D, bool bags, bool mul, bool hashed);
 hipError_t launch_emb_keys(const EmbedBwdArgs& a, bool ids64, void* scratch, hipStream_t s);
 hipError_t launch_emb_sort(const EmbedBwdArgs& a, void* scratch, hipStream_t s);
 // grad_x0, grad_q and grad_r must be 16-byte aligned (checked by the caller).

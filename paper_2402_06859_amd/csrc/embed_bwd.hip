@@ -9,7 +9,10 @@
 // occurrences, so the sum is not formed with atomics. Instead:
 //   1. keys: each occurrence gets two keys, its row in the concatenation of
 //      all quotient tables followed by all remainder tables; the value is the
-//      occurrence index (ids outside [0, V) get a sentinel key that sorts last);
+//      occurrence index (ids outside [0, V) get a sentinel key that sorts last).
+//      With the hashed front-end each feature has two table pairs (one per
+//      32-bit half of the id's hash) and an occurrence gets four keys; the value
+//      is then occurrence + half * nnz;
 //   2. a stable LSD radix sort of (key, occurrence) pairs groups equal rows
 //      while keeping occurrence order inside each group;
 //   3. a segmented reduction walks the sorted pairs in fixed tiles, one wave
@@ -49,13 +52,14 @@ __device__ __forceinline__ bool split_id(ID raw, const EmbedBwdArgs& a, uint32_t
 // 1. keys. Single-hot: thread per occurrence o = b*F + f. Bags: thread per bag.
 // With the product combine each occurrence also records its quotient and
 // remainder rows (the reduction multiplies by the row of the other table).
-template <typename ID, bool BAGS, bool MUL>
+template <typename ID, bool BAGS, bool MUL, bool HASHED>
 __global__ __launch_bounds__(256) void k_emb_keys(EmbedBwdArgs a, uint32_t* __restrict__ keys,
                                                   uint32_t* __restrict__ vals, uint32_t* __restrict__ bag_of,
                                                   uint32_t* __restrict__ qrow, uint32_t* __restrict__ rrow) {
     const ID* ids = (const ID*)a.ids;
-    const uint32_t sentinel = (uint32_t)a.F * (a.rows_q + a.m);
-    const uint32_t rbase = (uint32_t)a.F * a.rows_q;
+    const uint32_t pairs = HASHED ? 2u : 1u;  // table pairs per feature
+    const uint32_t sentinel = (uint32_t)a.F * pairs * (a.rows_q + a.m);
+    const uint32_t rbase = (uint32_t)a.F * pairs * a.rows_q;
     const int64_t nunits = BAGS ? a.batch * a.F : a.nnz;
     for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < nunits;
          u += (int64_t)gridDim.x * blockDim.x) {
@@ -63,6 +67,27 @@ __global__ __launch_bounds__(256) void k_emb_keys(EmbedBwdArgs a, uint32_t* __re
         const int64_t begin = BAGS ? a.offsets[u] : u;
         const int64_t end = BAGS ? a.offsets[u + 1] : u + 1;
         for (int64_t p = begin; p < end && p < a.nnz; ++p) {
+            if (HASHED) {  // keys [q of half 0 | r of half 0 | q of half 1 | r of half 1], value p + s * nnz
+                const uint64_t h = murmur64a_8((uint64_t)(int64_t)ids[p], a.seed);
+                const DivMagic dm{a.magic_m, a.shift_m, a.m};
+#pragma unroll
+                for (int s = 0; s < 2; ++s) {
+                    const uint32_t x = (uint32_t)(s ? h >> 32 : h);
+                    const uint32_t qi = div_magic(x, dm), ri = x - qi * a.m;
+                    const uint32_t tbl = 2u * (uint32_t)f + (uint32_t)s;
+                    const int64_t o = p + s * a.nnz;
+                    keys[2 * s * a.nnz + p] = tbl * a.rows_q + qi;
+                    keys[(2 * s + 1) * a.nnz + p] = rbase + tbl * a.m + ri;
+                    vals[2 * s * a.nnz + p] = (uint32_t)o;
+                    vals[(2 * s + 1) * a.nnz + p] = (uint32_t)o;
+                    if (MUL) {
+                        qrow[o] = qi;
+                        rrow[o] = ri;
+                    }
+                }
+                if (BAGS) bag_of[p] = (uint32_t)u;
+                continue;
+            }
             uint32_t qi = 0, ri = 0, kq = sentinel, kr = sentinel;
             if (split_id<ID>(ids[p], a, qi, ri)) {
                 kq = (uint32_t)f * a.rows_q + qi;
@@ -235,17 +260,20 @@ struct SegCtx {
         const uint32_t kk0 = ok ? k : 0u;
         const bool isq = kk0 < rbase;
         const uint32_t kk = isq ? kk0 : kk0 - rbase;
-        const uint32_t f = isq ? div_magic(kk, DivMagic{a.magic_q, a.shift_q, (uint32_t)a.rows_q})
-                               : div_magic(kk, DivMagic{a.magic_m, a.shift_m, a.m});
+        // table pair of the key (the feature, or 2 * feature + hash half)
+        const uint32_t tbl = isq ? div_magic(kk, DivMagic{a.magic_q, a.shift_q, (uint32_t)a.rows_q})
+                                 : div_magic(kk, DivMagic{a.magic_m, a.shift_m, a.m});
+        const uint32_t f = a.hashed ? tbl >> 1 : tbl;
         const uint32_t oo = ok ? o : 0u;
+        const uint32_t occ = oo >= (uint32_t)a.nnz ? oo - (uint32_t)a.nnz : oo;  // value = occurrence + half * nnz
         const int cc = ok ? c : 0;
-        const uint32_t bag = BAGS ? bag_of[oo] : oo;
+        const uint32_t bag = BAGS ? bag_of[occ] : occ;
         const int64_t b = div_magic(bag, DivMagic{a.magic_f, a.shift_f, (uint32_t)a.F});
         const f32x4_t w = *(const f32x4_t*)(a.grad_x0 + b * a.d + (int64_t)f * a.D + cc);
         Cols4 out = {{w.x, w.y, w.z, w.w}};
         if (MUL) {
-            const T* other = isq ? (const T*)a.r_tables + ((int64_t)f * a.m + rrow[oo]) * a.D + cc
-                                 : (const T*)a.q_tables + ((int64_t)f * a.rows_q + qrow[oo]) * a.D + cc;
+            const T* other = isq ? (const T*)a.r_tables + ((int64_t)tbl * a.m + rrow[oo]) * a.D + cc
+                                 : (const T*)a.q_tables + ((int64_t)tbl * a.rows_q + qrow[oo]) * a.D + cc;
 #pragma unroll
             for (int e = 0; e < 4; ++e) out.v[e] *= st<T>::load(other + e);
         }
@@ -442,8 +470,8 @@ hipError_t launch_reduce(const EmbedBwdArgs& a, const RedPtrs& p, uint32_t n, hi
     s.qrow = p.qrow;
     s.rrow = p.rrow;
     s.n = n;
-    s.sentinel = (uint32_t)a.F * (a.rows_q + a.m);
-    s.rbase = (uint32_t)a.F * a.rows_q;
+    s.sentinel = (uint32_t)a.F * (a.hashed ? 2u : 1u) * (a.rows_q + a.m);
+    s.rbase = (uint32_t)a.F * (a.hashed ? 2u : 1u) * a.rows_q;
     const uint32_t ntiles = (n + SEG_TILE - 1) / SEG_TILE;
     const unsigned blocks = (ntiles + 3) / 4;
     hipLaunchKernelGGL((k_seg_reduce<T, L, MUL, BAGS>), dim3(blocks), dim3(256), 0, st, s, p.carry_head,
@@ -474,11 +502,11 @@ inline int key_bits(uint32_t maxkey) {
 
 }  // namespace
 
-EmbedBwdLayout embed_bwd_layout(int64_t nnz, int F, int rows_q, int m, int D, bool bags, bool mul) {
+EmbedBwdLayout embed_bwd_layout(int64_t nnz, int F, int rows_q, int m, int D, bool bags, bool mul, bool hashed) {
     EmbedBwdLayout L;
-    const uint64_t n = 2 * (uint64_t)nnz;
+    const uint64_t n = (uint64_t)emb_pairs(nnz, hashed);
     const uint64_t ntiles = (n + RS_TILE - 1) / RS_TILE;
-    const int bits = key_bits((uint32_t)F * (uint32_t)(rows_q + m));
+    const int bits = key_bits((uint32_t)F * (hashed ? 2u : 1u) * (uint32_t)(rows_q + m));
     const int passes = (bits + RS_MAX_BITS - 1) / RS_MAX_BITS;
     const int dbits = (bits + passes - 1) / passes;
     const uint64_t hist = ((uint64_t)1 << dbits) * (ntiles ? ntiles : 1);
@@ -491,8 +519,8 @@ EmbedBwdLayout embed_bwd_layout(int64_t nnz, int F, int rows_q, int m, int D, bo
     L.keys1 = off; off += al(4 * n);
     L.vals1 = off; off += al(4 * n);
     L.bag_of = off; off += bags ? al(4 * (uint64_t)nnz) : 0;
-    L.qrow = off; off += mul ? al(4 * (uint64_t)nnz) : 0;
-    L.rrow = off; off += mul ? al(4 * (uint64_t)nnz) : 0;
+    L.qrow = off; off += mul ? al(4 * (hashed ? 2 : 1) * (uint64_t)nnz) : 0;  // per (occurrence, half)
+    L.rrow = off; off += mul ? al(4 * (hashed ? 2 : 1) * (uint64_t)nnz) : 0;
     L.hist = off; off += al(4 * hist);
     L.sums = off; off += al(4 * sums);
     L.carry_head = off; off += al(4 * segtiles * (uint64_t)D);
@@ -520,7 +548,7 @@ static EmbPtrs emb_ptrs(const EmbedBwdArgs& a, void* scratch) {
     EmbPtrs p;
     const bool bags = a.offsets != nullptr;
     const bool mul = a.combine == 0;
-    p.L = embed_bwd_layout(a.nnz, a.F, a.rows_q, a.m, a.D, bags, mul);
+    p.L = embed_bwd_layout(a.nnz, a.F, a.rows_q, a.m, a.D, bags, mul, a.hashed != 0);
     char* base = (char*)scratch;
     p.keys[0] = (uint32_t*)(base + p.L.keys0);
     p.keys[1] = (uint32_t*)(base + p.L.keys1);
@@ -544,8 +572,14 @@ hipError_t launch_emb_keys(const EmbedBwdArgs& a, bool ids64, void* scratch, hip
     int64_t blocks = (units + 255) / 256;
     if (blocks > 65536) blocks = 65536;
 #define RDCN_KEYS(ID, BG, MU)                                                                                   \
-    hipLaunchKernelGGL((k_emb_keys<ID, BG, MU>), dim3((unsigned)blocks), dim3(256), 0, st, a, P.keys[0], P.vals[0], \
-                       P.bag_of, P.qrow, P.rrow)
+    do {                                                                                                        \
+        if (a.hashed)                                                                                           \
+            hipLaunchKernelGGL((k_emb_keys<ID, BG, MU, true>), dim3((unsigned)blocks), dim3(256), 0, st, a,     \
+                               P.keys[0], P.vals[0], P.bag_of, P.qrow, P.rrow);                                 \
+        else                                                                                                    \
+            hipLaunchKernelGGL((k_emb_keys<ID, BG, MU, false>), dim3((unsigned)blocks), dim3(256), 0, st, a,    \
+                               P.keys[0], P.vals[0], P.bag_of, P.qrow, P.rrow);                                 \
+    } while (0)
 #define RDCN_KEYS_M(ID, BG) do { if (a.combine == 0) RDCN_KEYS(ID, BG, true); else RDCN_KEYS(ID, BG, false); } while (0)
     if (ids64) { if (bags) RDCN_KEYS_M(int64_t, true); else RDCN_KEYS_M(int64_t, false); }
     else       { if (bags) RDCN_KEYS_M(int32_t, true); else RDCN_KEYS_M(int32_t, false); }
@@ -558,7 +592,7 @@ hipError_t launch_emb_keys(const EmbedBwdArgs& a, bool ids64, void* scratch, hip
 hipError_t launch_emb_sort(const EmbedBwdArgs& a, void* scratch, hipStream_t st) {
     if (a.nnz == 0 || a.F == 0) return hipSuccess;
     const EmbPtrs P = emb_ptrs(a, scratch);
-    const uint32_t n = (uint32_t)(2 * a.nnz);
+    const uint32_t n = (uint32_t)emb_pairs(a.nnz, a.hashed != 0);
     const int ntiles = (int)((n + RS_TILE - 1) / RS_TILE);
     int cur = 0;
     for (int pass = 0; pass < P.L.passes; ++pass) {
@@ -581,7 +615,7 @@ hipError_t launch_emb_sort(const EmbedBwdArgs& a, void* scratch, hipStream_t st)
 hipError_t launch_emb_reduce(const EmbedBwdArgs& a, bool bf16, void* scratch, hipStream_t st) {
     if (a.nnz == 0 || a.F == 0) return hipSuccess;
     const EmbPtrs P = emb_ptrs(a, scratch);
-    const uint32_t n = (uint32_t)(2 * a.nnz);
+    const uint32_t n = (uint32_t)emb_pairs(a.nnz, a.hashed != 0);
     const int cur = P.L.passes & 1;
     const RedPtrs rp = {P.keys[cur], P.vals[cur], P.bag_of, P.qrow, P.rrow, P.carry_head, P.carry_tail};
     const bool mul = a.combine == 0, bags = a.offsets != nullptr;

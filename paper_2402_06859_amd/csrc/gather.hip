@@ -101,7 +101,19 @@ struct Q8Rows {
     }
 };
 
-template <typename T, typename ID, bool BAGS, class Rows>
+// Hashed front-end: the two 32-bit halves of an id's 64-bit hash, each QR-split by m.
+__device__ __forceinline__ void hash_split(int64_t id, const GatherArgs& a, uint32_t (&qi)[2], uint32_t (&ri)[2]) {
+    const uint64_t h = murmur64a_8((uint64_t)id, a.seed);
+    const DivMagic dm{a.magic, a.shift, a.m};
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        const uint32_t x = (uint32_t)(s ? h >> 32 : h);
+        qi[s] = div_magic(x, dm);
+        ri[s] = x - qi[s] * a.m;
+    }
+}
+
+template <typename T, typename ID, bool BAGS, class Rows, bool HASHED>
 __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a) {
 #pragma clang fp contract(off)
     constexpr int V = st<T>::vec;
@@ -116,7 +128,9 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a) {
     const bool emb = c < emb_vecs;
     const int f = emb ? c / cpf : 0;
     const int cc = emb ? c - f * cpf : 0;
-    const Rows rows(a, f, cc);
+    // table pair(s) of feature f: pair f, or pairs 2f (low hash half) and 2f + 1 (high)
+    const Rows rows(a, HASHED ? 2 * f : f, cc);
+    const Rows rows1(a, HASHED ? 2 * f + 1 : f, cc);
     const int64_t row_step = (int64_t)gridDim.y * 4 * GATHER_ROWS;
     for (int64_t b0 = ((int64_t)blockIdx.y * 4 + (threadIdx.x >> 6)) * GATHER_ROWS; b0 < a.batch; b0 += row_step) {
         const int nr = a.batch - b0 < GATHER_ROWS ? (int)(a.batch - b0) : GATHER_ROWS;
@@ -125,6 +139,35 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a) {
 #pragma unroll
             for (int u = 0; u < GATHER_ROWS; ++u)
                 if (u < nr) out[u] = *(const u32x4_t*)((const T*)a.dense + (b0 + u) * a.Nd + (c - emb_vecs) * V);
+        } else if (!BAGS && HASHED) {
+            ID id[GATHER_ROWS];
+#pragma unroll
+            for (int u = 0; u < GATHER_ROWS; ++u) id[u] = ids[(b0 + (u < nr ? u : 0)) * a.F + f];
+            typename Rows::Raw q0[GATHER_ROWS], r0[GATHER_ROWS], q1[GATHER_ROWS], r1[GATHER_ROWS];
+#pragma unroll
+            for (int u = 0; u < GATHER_ROWS; ++u) {
+                uint32_t qi[2], ri[2];
+                hash_split((int64_t)id[u], a, qi, ri);
+                q0[u] = rows.load_q(qi[0]);
+                r0[u] = rows.load_r(ri[0]);
+                q1[u] = rows1.load_q(qi[1]);
+                r1[u] = rows1.load_r(ri[1]);
+            }
+#pragma unroll
+            for (int u = 0; u < GATHER_ROWS; ++u) {
+                float qa[V], ra[V], qb[V], rb[V], acc[V];
+                Rows::values(q0[u], qa);
+                Rows::values(r0[u], ra);
+                Rows::values(q1[u], qb);
+                Rows::values(r1[u], rb);
+#pragma unroll
+                for (int e = 0; e < V; ++e) {
+                    const float e0 = a.combine == 0 ? qa[e] * ra[e] : qa[e] + ra[e];
+                    const float e1 = a.combine == 0 ? qb[e] * rb[e] : qb[e] + rb[e];
+                    acc[e] = e0 + e1;
+                }
+                out[u] = st<T>::pack(acc);
+            }
         } else if (!BAGS) {
             ID id[GATHER_ROWS];
 #pragma unroll
@@ -165,19 +208,35 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a) {
                 float acc[V];
                 bool started = false;
                 for (int64_t p = beg[u]; p < end[u]; ++p) {
-                    uint32_t qi, ri;
-                    if (!qr_split<ID>(ids[p], a, qi, ri)) {
-                        bad = true;
-                        continue;
-                    }
-                    float qv[V], rv[V];
-                    Rows::values(rows.load_q(qi), qv);
-                    Rows::values(rows.load_r(ri), rv);
+                    float x[V];
+                    if (HASHED) {
+                        uint32_t qi[2], ri[2];
+                        hash_split((int64_t)ids[p], a, qi, ri);
+                        float qa[V], ra[V], qb[V], rb[V];
+                        Rows::values(rows.load_q(qi[0]), qa);
+                        Rows::values(rows.load_r(ri[0]), ra);
+                        Rows::values(rows1.load_q(qi[1]), qb);
+                        Rows::values(rows1.load_r(ri[1]), rb);
 #pragma unroll
-                    for (int e = 0; e < V; ++e) {
-                        const float x = a.combine == 0 ? qv[e] * rv[e] : qv[e] + rv[e];
-                        acc[e] = started ? acc[e] + x : x;
+                        for (int e = 0; e < V; ++e) {
+                            const float e0 = a.combine == 0 ? qa[e] * ra[e] : qa[e] + ra[e];
+                            const float e1 = a.combine == 0 ? qb[e] * rb[e] : qb[e] + rb[e];
+                            x[e] = e0 + e1;
+                        }
+                    } else {
+                        uint32_t qi, ri;
+                        if (!qr_split<ID>(ids[p], a, qi, ri)) {
+                            bad = true;
+                            continue;
+                        }
+                        float qv[V], rv[V];
+                        Rows::values(rows.load_q(qi), qv);
+                        Rows::values(rows.load_r(ri), rv);
+#pragma unroll
+                        for (int e = 0; e < V; ++e) x[e] = a.combine == 0 ? qv[e] * rv[e] : qv[e] + rv[e];
                     }
+#pragma unroll
+                    for (int e = 0; e < V; ++e) acc[e] = started ? acc[e] + x[e] : x[e];
                     started = true;
                 }
                 if (!started) {
@@ -246,7 +305,11 @@ hipError_t launch_gather_rows(const GatherArgs& a, bool bf16, bool ids64, hipStr
     const dim3 grid((unsigned)((cpr + 63) / 64), (unsigned)ygroups);
     const int threads = 256;
     const bool bags = a.offsets != nullptr;
-#define RDCN_GATHER(T, ID, BG) hipLaunchKernelGGL((k_qr_gather<T, ID, BG, R<T>>), grid, dim3(threads), 0, s, a)
+#define RDCN_GATHER(T, ID, BG)                                                                         \
+    do {                                                                                               \
+        if (a.hashed) hipLaunchKernelGGL((k_qr_gather<T, ID, BG, R<T>, true>), grid, dim3(threads), 0, s, a);  \
+        else hipLaunchKernelGGL((k_qr_gather<T, ID, BG, R<T>, false>), grid, dim3(threads), 0, s, a);          \
+    } while (0)
     if (bf16) {
         if (ids64) { if (bags) RDCN_GATHER(bf16_t, int64_t, true); else RDCN_GATHER(bf16_t, int64_t, false); }
         else       { if (bags) RDCN_GATHER(bf16_t, int32_t, true); else RDCN_GATHER(bf16_t, int32_t, false); }

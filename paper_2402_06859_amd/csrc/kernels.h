@@ -13,6 +13,8 @@ struct GatherArgs {
     uint64_t vocab;
     uint32_t magic, shift;  // 32-bit division by m (valid when vocab <= 2^32)
     int combine;            // 0 = product, 1 = sum
+    int hashed;             // 1: hashed front-end (tables [F, 2, rows, D]; every id valid)
+    uint64_t seed;          // hash seed
     const void* ids;        // int32 or int64
     const int64_t* offsets; // NULL = single-hot
     const void* q_tables;   // storage-type tables, or int8 codes for the quantized gather

@@ -37,7 +37,8 @@ class RdcnConfig(ctypes.Structure):
                 ("qr_rows_q", ctypes.c_int32), ("qr_rows_r", ctypes.c_int32), ("combine", ctypes.c_int32),
                 ("multi_hot", ctypes.c_int32), ("id_type", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("split_activations", ctypes.c_int32), ("vocab", ctypes.c_int64), ("attn_alpha", ctypes.c_float),
-                ("skip_beta", ctypes.c_float), ("temperature", ctypes.c_float), ("parallel_branch", ctypes.c_int32)]
+                ("skip_beta", ctypes.c_float), ("temperature", ctypes.c_float), ("parallel_branch", ctypes.c_int32),
+                ("hashed", ctypes.c_int32), ("reserved2", ctypes.c_int32), ("hash_seed", ctypes.c_uint64)]
 
 
 class RdcnWeights(ctypes.Structure):
@@ -114,7 +115,7 @@ def make_config(batch_max: int, num_cat: int, emb_dim: int, num_dense: int, rank
                 qr_rows_q: int, qr_rows_r: int, vocab: int, combine: str = "sum", multi_hot: bool = False,
                 id_type: str = "i64", dtype: str = "bf16", attn_alpha: float = 0.0, skip_beta: float = 1.0,
                 temperature: float = 1.0, split_activations: bool = False,
-                parallel_branch: bool = False) -> RdcnConfig:
+                parallel_branch: bool = False, hashed: bool = False, hash_seed: int = 0) -> RdcnConfig:
     c = RdcnConfig()
     c.batch_max, c.num_cat, c.emb_dim, c.num_dense = batch_max, num_cat, emb_dim, num_dense
     c.rank, c.num_layers, c.qr_rows_q, c.qr_rows_r = rank, num_layers, qr_rows_q, qr_rows_r
@@ -126,14 +127,17 @@ def make_config(batch_max: int, num_cat: int, emb_dim: int, num_dense: int, rank
     c.attn_alpha, c.skip_beta, c.temperature = attn_alpha, skip_beta, temperature
     c.split_activations = int(split_activations)
     c.parallel_branch = int(parallel_branch)
+    c.hashed = int(hashed)
+    c.hash_seed = hash_seed
     return c
 
 
 def config_for(wl, batch_max: Optional[int] = None, id_type: str = "i64") -> RdcnConfig:
     """Config of a synthetic workload (paper_2402_06859_amd.synth.Workload)."""
     return make_config(batch_max or wl.batch, wl.num_cat, wl.emb_dim, wl.num_dense, wl.rank, wl.num_layers,
-                       wl.table_rows, wl.table_rows, wl.vocab, wl.combine, wl.multi_hot, id_type, wl.dtype,
-                       wl.alpha, wl.beta, wl.temperature, wl.split_activations, wl.parallel)
+                       wl.table_rows, wl.table_rows, 0 if wl.hashed else wl.vocab, wl.combine, wl.multi_hot, id_type,
+                       wl.dtype, wl.alpha, wl.beta, wl.temperature, wl.split_activations, wl.parallel, wl.hashed,
+                       wl.hash_seed)
 
 
 def _weights(w_down: Sequence[torch.Tensor], u: Sequence[torch.Tensor], bias: Sequence[torch.Tensor]) -> RdcnWeights:

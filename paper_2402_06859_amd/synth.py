@@ -49,10 +49,16 @@ class Workload:
     skip_beta: float = 1.0
     split_activations: bool = False  # activations as hi + lo bf16 pairs (deep attention stacks)
     parallel: bool = False           # plain + attention low-rank cross nets with their own weights
+    hashed: bool = False             # Murmur front-end: two QR table pairs per feature, rows*rows >= 2^32
+    hash_seed: int = 0
 
     @property
     def d(self) -> int:
         return self.num_cat * self.emb_dim + self.num_dense
+
+    @property
+    def table_pairs(self) -> int:
+        return 2 if self.hashed else 1
 
     @property
     def quotient_rows_used(self) -> int:
@@ -186,8 +192,9 @@ def make_inputs(wl: Workload, seed: Optional[int] = None, id_mode: str = "scatte
     # tables: N(0, sigma^2); sigma = 1 for the multiplicative combine, 1/sqrt(2) for the additive one
     sigma = 1.0 if wl.combine == "mul" else 1.0 / math.sqrt(2.0)
     tg = st["tables"]
-    out["q_tables"] = to_storage(tg.standard_normal((F, m, D), dtype=np.float32) * sigma, wl.dtype)
-    out["r_tables"] = to_storage(tg.standard_normal((F, m, D), dtype=np.float32) * sigma, wl.dtype)
+    shape = (F, 2, m, D) if wl.hashed else (F, m, D)  # hashed: one (Q, R) pair per hash half
+    out["q_tables"] = to_storage(tg.standard_normal(shape, dtype=np.float32) * sigma, wl.dtype)
+    out["r_tables"] = to_storage(tg.standard_normal(shape, dtype=np.float32) * sigma, wl.dtype)
 
     dense = st["dense"].standard_normal((B, wl.num_dense), dtype=np.float32)
     if wl.dense_zero_frac > 0:

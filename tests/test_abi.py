@@ -122,3 +122,19 @@ def test_parallel_branch_validation():
     c = good()
     c.parallel_branch, c.split_activations = 1, 1
     assert L.rdcn_create(ctypes.byref(c), ctypes.byref(h)) == rdcn.RDCN_ERR_UNSUPPORTED
+
+
+def test_hashed_front_end_validation():
+    L = rdcn.load()
+    h = ctypes.c_void_p()
+    c = good()
+    c.hashed = 1  # vocab must be 0
+    assert L.rdcn_create(ctypes.byref(c), ctypes.byref(h)) == rdcn.RDCN_ERR_ARG
+    c.vocab = 0   # 25 * 25 rows do not cover a 32-bit hash half
+    assert L.rdcn_create(ctypes.byref(c), ctypes.byref(h)) == rdcn.RDCN_ERR_SHAPE
+    c = good()
+    c.hashed = 2
+    assert L.rdcn_create(ctypes.byref(c), ctypes.byref(h)) == rdcn.RDCN_ERR_ARG
+    c = good()
+    c.reserved2 = 1
+    assert L.rdcn_create(ctypes.byref(c), ctypes.byref(h)) == rdcn.RDCN_ERR_ARG
