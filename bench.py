@@ -61,8 +61,9 @@ def kernel_work(wl, B: int) -> dict:
     hr = wl.h_width          # width of the up projection's input
     dl = 2 if wl.parallel else 1  # launches of the down and gh GEMMs per layer (plain branch apart)
     w = {}
-    # gather: ids, both table rows per id, x0 write, dense read
-    w["gather"] = (0.0, B * (F * hot * 8 + 2 * F * hot * D * eb + F * D * eb + 2 * Nd * eb), 0.0)
+    tp = wl.table_pairs  # QR table pairs per feature (2 with the hashed front-end)
+    # gather: ids, both table rows of every pair per id, x0 write, dense read
+    w["gather"] = (0.0, B * (F * hot * 8 + 2 * tp * F * hot * D * eb + F * D * eb + 2 * Nd * eb), 0.0)
     w["fwd_down_gemm"] = (2.0 * B * nr * d / dl, (dl * B * d * eb + nr * d * eb + B * nr * pb) / dl, 0.0)
     exp_f = 2.0 * EXP_SLOTS
     pair_fwd = (2.0 + exp_f + 1.0) if wl.dtype == "bf16" else (2.0 + exp_f + 3.0)
@@ -84,12 +85,12 @@ def kernel_work(wl, B: int) -> dict:
     w["bwd_gx_gemm"] = (2.0 * B * d * nr, B * nr * eb + nr * d * eb + 2 * B * d * 4, 0.0)
     # embedding backward: nnz ids, 2 (key, occurrence) pairs of 4 + 4 bytes per id
     nnz = B * F * hot
-    passes = _radix_passes(F * (2 * wl.table_rows))
-    w["emb_keys"] = (0.0, nnz * 8 + 2 * nnz * 8 + (nnz * 4 if wl.multi_hot else 0), 0.0)
-    w["emb_sort"] = (0.0, passes * 2 * nnz * (4 + 8 + 8), 0.0)  # histogram read + scatter read/write per pass
-    w["emb_reduce"] = (0.0, 2 * nnz * (8 + D * 4) + 2 * F * wl.table_rows * D * 8, 0.0)
+    passes = _radix_passes(F * tp * (2 * wl.table_rows))
+    w["emb_keys"] = (0.0, nnz * 8 + 2 * tp * nnz * 8 + (nnz * 4 if wl.multi_hot else 0), 0.0)
+    w["emb_sort"] = (0.0, passes * 2 * tp * nnz * (4 + 8 + 8), 0.0)  # histogram read + scatter read/write per pass
+    w["emb_reduce"] = (0.0, 2 * tp * nnz * (8 + D * 4) + 2 * tp * F * wl.table_rows * D * 8, 0.0)
     # serving gather from 8-bit tables: codes (1 byte per value) and each row's (middle, scale)
-    w["gather_q8"] = (0.0, B * (F * hot * 8 + 2 * F * hot * (D + 8) + F * D * eb + 2 * Nd * eb), 0.0)
+    w["gather_q8"] = (0.0, B * (F * hot * 8 + 2 * tp * F * hot * (D + 8) + F * D * eb + 2 * Nd * eb), 0.0)
     return w
 
 
@@ -173,14 +174,22 @@ def _oracle_step(wl, rows: int) -> float:
     W = [x.float().numpy() for x in inp["w_down"]]
     U = [x.float().numpy() for x in inp["u"]]
     b = [x.float().numpy() for x in inp["bias"]]
+    F, D, Nd, m, bf16 = wl.num_cat, wl.emb_dim, wl.num_dense, wl.table_rows, wl.dtype == "bf16"
     t0 = time.perf_counter()
-    x0, _ = oracle.gather(rows, wl.num_cat, wl.emb_dim, wl.num_dense, wl.vocab, wl.table_rows, wl.table_rows,
-                          wl.combine, wl.dtype == "bf16", inp["ids"], inp["offsets"], inp["q_tables"],
-                          inp["r_tables"], inp["dense"])
-    oracle.forward(x0, W, U, b, wl.alpha, wl.beta, wl.temperature)
-    gx0 = oracle.backward(x0, W, U, b, inp["grad_out"], wl.alpha, wl.beta, wl.temperature)[0]
-    oracle.embed_backward(rows, wl.num_cat, wl.emb_dim, wl.num_dense, wl.vocab, wl.table_rows, wl.table_rows,
-                          wl.combine, inp["ids"], inp["offsets"], inp["q_tables"], inp["r_tables"], gx0)
+    if wl.hashed:
+        x0 = oracle.gather_hashed(rows, F, D, Nd, m, m, wl.combine, bf16, wl.hash_seed, inp["ids"], inp["offsets"],
+                                  inp["q_tables"], inp["r_tables"], inp["dense"])
+    else:
+        x0, _ = oracle.gather(rows, F, D, Nd, wl.vocab, m, m, wl.combine, bf16, inp["ids"], inp["offsets"],
+                              inp["q_tables"], inp["r_tables"], inp["dense"])
+    oracle.forward(x0, W, U, b, wl.alpha, wl.beta, wl.temperature, parallel=wl.parallel)
+    gx0 = oracle.backward(x0, W, U, b, inp["grad_out"], wl.alpha, wl.beta, wl.temperature, parallel=wl.parallel)[0]
+    if wl.hashed:
+        oracle.embed_backward_hashed(rows, F, D, Nd, m, m, wl.combine, wl.hash_seed, inp["ids"], inp["offsets"],
+                                     inp["q_tables"], inp["r_tables"], gx0)
+    else:
+        oracle.embed_backward(rows, F, D, Nd, wl.vocab, m, m, wl.combine, inp["ids"], inp["offsets"],
+                              inp["q_tables"], inp["r_tables"], gx0)
     return time.perf_counter() - t0
 
 
@@ -221,6 +230,8 @@ def main():
     ap.add_argument("--workload", default="small")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle time budget for cpu_baseline (0 = skip)")
     ap.add_argument("--id-mode", default="scatter", choices=["scatter", "rank"])
+    ap.add_argument("--hashed", action="store_true",
+                    help="Murmur-hashed front-end: raw ids hashed, two QR table pairs of 2^16 + 2^16 rows per feature")
     ap.add_argument("--parallel-branch", action="store_true",
                     help="plain and attention low-rank cross nets with their own weights in every layer")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -253,6 +264,8 @@ def main():
             print("--parallel-branch needs a workload with the attention term", file=sys.stderr)
             sys.exit(2)
         wl = wl.with_(parallel=True)
+    if args.hashed:
+        wl = wl.with_(hashed=True, table_rows=1 << 16)
     torch.cuda.set_device(0)
     inp = make_inputs(wl, id_mode=args.id_mode)
     db = DeviceBatch(wl, inp)
@@ -319,7 +332,9 @@ def main():
                                "%d dense, d=%d, %d Residual-DCN layers rank %d, attention %s%s"
                                % (wl.name, B, wl.num_cat, wl.vocab, wl.table_rows, wl.emb_dim, wl.combine,
                                   wl.num_dense, wl.d, wl.num_layers, wl.rank, "on" if wl.attention else "off",
-                                  ", parallel plain branch" if wl.parallel else ""),
+                                  ", parallel plain branch" if wl.parallel else "")
+                               + (", Murmur-hashed ids (two QR pairs of 2^16 x 2^16 rows per feature)"
+                                  if wl.hashed else ""),
                    "global_batch": B, "id_mode": args.id_mode},
         "roofline": roof,
         "gemm_mfma_frac": (gemm_flops / gemm_s / 1e12 / PEAK_BF16_TFLOPS) if gemm_s > 0 else None,
