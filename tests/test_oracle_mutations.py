@@ -1,6 +1,6 @@
 """The oracle's pins must catch plausible mistakes.
 
-Each case plants one mistake in a copy of oracle.c (a dropped term, a wrong
+Each case plants one mistake in a copy of oracle.c or head.py (a dropped term, a wrong
 sign, a swapped index, a transposed operand, a wrong rounding), builds it into
 a temporary directory and runs the pin file that should notice; the pins must
 fail. Runs on the CPU only; the real oracle is never modified.
@@ -67,20 +67,38 @@ MUTATIONS = {
                            "                            gr[c] += g[c] * (double)qrow[c];\n                        } else {\n"
                            "                            gq[c] += g[c];\n                            gr[c] += g[c];\n"
                            "                        }\n                    }\n                }"),
+    "head_gate_derivative_missing_one_minus": ("head", "g_s = g_rho * rho * (1.0 - rho)", "g_s = g_rho * rho", "head.py"),
+    "head_gate_input_gradient_dropped": ("head", "ga = ga + np.outer(g_s, Gl)", "ga = ga", "head.py"),
+    "head_relu_gradient_ungated": ("head", "g_z = g_relu * (z > 0.0)", "g_z = ga * (z > 0.0)", "head.py"),
+    "head_bias_gradient_before_mask": ("head", "gb[l] = g_z.sum(axis=0)", "gb[l] = g_relu.sum(axis=0)", "head.py"),
+    "head_bucket_remainder_off_by_one": ("head", "v[here, i] = t[here] - step * k[here]",
+                                         "v[here, i] = t[here] - step * (k[here] + 1)", "head.py"),
+    "head_bucket_bound_inclusive": ("head", "k += (t32 > bound).astype(np.int64)",
+                                    "k += (t32 >= bound).astype(np.int64)", "head.py"),
+    "head_slope_ignores_embedding": ("head", "np.sum(np.maximum(e + w, 0.0) * v, axis=1)",
+                                     "np.sum(np.maximum(w, 0.0) * v, axis=1)", "head.py"),
+    "head_logit_gradient_next_bucket": ("head", "np.maximum(pre[rows, k], 0.0)",
+                                        "np.maximum(pre[rows, np.minimum(k + 1, K - 1)], 0.0)", "head.py"),
+    "head_logloss_sign": ("head", "return softplus(y_cal) - label * y_cal, sigmoid(y_cal) - label",
+                          "return softplus(y_cal) - label * y_cal, label - sigmoid(y_cal)", "head.py"),
+    "head_output_weight_gradient_uncalibrated": ("head", "g_wout = g_y @ aL", "g_wout = np.asarray(g_cal) @ aL",
+                                                 "head.py"),
 }
 PIN_FILE = {"gather": "test_oracle_gather.py", "dcn": "test_oracle_dcn.py", "grad": "test_oracle_grad.py",
-            "quant": "test_oracle_quant.py", "parallel": "test_oracle_parallel.py", "hash": "test_oracle_hash.py"}
+            "quant": "test_oracle_quant.py", "parallel": "test_oracle_parallel.py", "hash": "test_oracle_hash.py",
+            "head": "test_oracle_head.py"}
 
 
 @pytest.mark.parametrize("name", list(MUTATIONS))
 def test_pins_catch_planted_mistake(name, tmp_path):
-    which, old, new = MUTATIONS[name]
-    src = open(os.path.join(ROOT, "oracle", "oracle.c")).read()
+    which, old, new = MUTATIONS[name][:3]
+    fname = MUTATIONS[name][3] if len(MUTATIONS[name]) > 3 else "oracle.c"
+    src = open(os.path.join(ROOT, "oracle", fname)).read()
     assert src.count(old) >= 1, "mutation anchor not found: " + name
     for sub in ("oracle", "tests", "paper_2402_06859_amd"):
         shutil.copytree(os.path.join(ROOT, sub), tmp_path / sub,
                         ignore=shutil.ignore_patterns("*.so", "__pycache__", "_build*"))
-    (tmp_path / "oracle" / "oracle.c").write_text(src.replace(old, new, 1))
+    (tmp_path / "oracle" / fname).write_text(src.replace(old, new, 1))
     r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
                         os.path.join("tests", PIN_FILE[which])], cwd=tmp_path, capture_output=True, text=True)
     assert r.returncode == 1, "planted mistake %r was not caught:\n%s" % (name, r.stdout[-2000:])
