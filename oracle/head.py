@@ -29,10 +29,15 @@ Readings where the paper is silent (each is a choice of this library):
   - e is an input [B, K] (the calibration-feature embedding made upstream);
     its gradient is returned;
   - loss_b = softplus(y_cal) - label * y_cal, its gradient sigmoid(y_cal) - label.
+
+ReLU masks and the bucket index are decisions taken by floating point. To take
+them on the same values as a device that keeps its hidden activations in a
+narrower storage type, `round_act` (optional) is applied to every stored hidden
+activation a_1 .. a_L; everything else stays float64.
 """
 from __future__ import annotations
 
-from typing import List, Optional, Sequence
+from typing import Callable, List, Optional, Sequence
 
 import numpy as np
 
@@ -56,10 +61,12 @@ def softplus(z):
 # Gated MLP
 # ---------------------------------------------------------------------------
 
-def mlp_forward(x, W: Sequence, b: Sequence, G: Optional[Sequence] = None, c: Optional[Sequence] = None):
+def mlp_forward(x, W: Sequence, b: Sequence, G: Optional[Sequence] = None, c: Optional[Sequence] = None,
+                round_act: Optional[Callable] = None):
     """a_0 = x; a_l = ReLU(a_{l-1} W_l^T + b_l) [* sigmoid(a_{l-1} g_l + c_l)].
 
-    x [B, n_0]; W[l] [n_l, n_{l-1}]; b[l] [n_l]; G[l] [n_{l-1}]; c[l] scalar.
+    x [B, n_0]; W[l] [n_l, n_{l-1}]; b[l] [n_l]; G[l] [n_{l-1}]; c[l] scalar;
+    round_act(a) -> a, applied to each a_l (l >= 1) before it is used or returned.
     Returns (a, s): activations a_0 .. a_L and gate logits s_1 .. s_L (empty when ungated).
     """
     a = [np.asarray(x, dtype=np.float64)]
@@ -72,6 +79,8 @@ def mlp_forward(x, W: Sequence, b: Sequence, G: Optional[Sequence] = None, c: Op
             sl = prev @ np.asarray(G[l], dtype=np.float64) + float(c[l])
             act = act * sigmoid(sl)[:, None]
             s.append(sl)
+        if round_act is not None:
+            act = np.asarray(round_act(act), dtype=np.float64)
         a.append(act)
     return a, s
 
@@ -176,18 +185,19 @@ def logloss(y_cal, label):
 # The whole head
 # ---------------------------------------------------------------------------
 
-def head_forward(x, p: dict):
+def head_forward(x, p: dict, round_act: Optional[Callable] = None):
     """p: W, b, (G, c when gated), w_out, b_out, cal_w, cal_b, lo, step; plus e [B, K].
     Returns dict(a, s, y, y_cal)."""
-    a, s = mlp_forward(x, p["W"], p["b"], p.get("G"), p.get("c"))
+    a, s = mlp_forward(x, p["W"], p["b"], p.get("G"), p.get("c"), round_act)
     y = a[-1] @ np.asarray(p["w_out"], dtype=np.float64) + float(p["b_out"])
     y_cal = calibrate(y, p["e"], p["cal_w"], p["cal_b"], p["lo"], p["step"])
     return {"a": a, "s": s, "y": y, "y_cal": y_cal}
 
 
-def head_backward(x, p: dict, g_cal):
-    """Gradients of every input and parameter of head_forward given dLoss/dy_cal."""
-    f = head_forward(x, p)
+def head_backward(x, p: dict, g_cal, round_act: Optional[Callable] = None):
+    """Gradients of every input and parameter of head_forward given dLoss/dy_cal
+    (with round_act, the gradients at the rounded activations)."""
+    f = head_forward(x, p, round_act)
     g_y, g_e, g_w, g_bc = calibrate_backward(f["y"], p["e"], p["cal_w"], p["lo"], p["step"], g_cal)
     aL = f["a"][-1]
     w_out = np.asarray(p["w_out"], dtype=np.float64)

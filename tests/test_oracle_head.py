@@ -295,3 +295,21 @@ def test_head_backward_finite_differences(gated):
         assert out["w_out"][j] == pytest.approx((f(w_out=wo + d) - f(w_out=wo - d)) / (2 * h), rel=1e-5, abs=1e-7)
     assert out["b_out"] == pytest.approx((f(b_out=p["b_out"] + h) - f(b_out=p["b_out"] - h)) / (2 * h), rel=1e-5)
     assert out["cal_b"] == pytest.approx(g.sum(), rel=1e-14)
+
+
+def test_rounded_activations_only_change_the_stored_values():
+    """round_act is applied to the stored activations only: with an identity rounding
+    the results are unchanged, and with bf16 rounding every a_l is a bf16 value and the
+    backward's masks follow the rounded activations (z recomputed from them)."""
+    import oracle
+    rng = np.random.default_rng(12)
+    p = _params(rng, [16, 8], True, 4, 8)
+    x = rng.standard_normal((5, 8))
+    a0, _ = H.mlp_forward(x, p["W"], p["b"], p["G"], p["c"])
+    a1, _ = H.mlp_forward(x, p["W"], p["b"], p["G"], p["c"], round_act=lambda v: v)
+    for u, v in zip(a0, a1):
+        np.testing.assert_array_equal(u, v)
+    ar, _ = H.mlp_forward(x, p["W"], p["b"], p["G"], p["c"], round_act=oracle.round_bf16)
+    for l in (1, 2):
+        np.testing.assert_array_equal(ar[l], oracle.round_bf16(ar[l]).astype(np.float64))
+        assert np.max(np.abs(ar[l] - a0[l])) <= 2.0 ** -8 * np.max(np.abs(a0[l])) * 2
