@@ -280,8 +280,109 @@ typedef enum rdcn_kernel {
     RDCN_KERNEL_EMB_REDUCE = 14,    /* embedding backward: segmented reduction + fix-up */
     RDCN_KERNEL_GATHER_Q8 = 15,     /* qr_embed_gather_q8 */
     RDCN_KERNEL_QUANTIZE = 16,      /* qr_quantize_tables */
-    RDCN_KERNEL_COUNT = 17
+    RDCN_KERNEL_HEAD_GATE = 17,     /* head: gate logits s_l = g_l . a_{l-1} + c_l */
+    RDCN_KERNEL_HEAD_FWD_GEMM = 18, /* head: a_l = ReLU(a_{l-1} W_l^T + b_l) * sigmoid(s_l) */
+    RDCN_KERNEL_HEAD_OUT = 19,      /* head: logit and isotonic calibration */
+    RDCN_KERNEL_HEAD_LOSS = 20,     /* rdcn_head_logloss */
+    RDCN_KERNEL_HEAD_OUT_BWD = 21,  /* head backward: calibration and logit gradients, top layer's G */
+    RDCN_KERNEL_HEAD_GW_GEMM = 22,  /* head backward: gW_l = G_l^T a_{l-1} (plus split-K reduce) */
+    RDCN_KERNEL_HEAD_GX_GEMM = 23,  /* head backward: G_{l-1} (or grad_x) from G_l W_l */
+    RDCN_KERNEL_HEAD_GATE_BWD = 24, /* head backward: gate-logit gradients from the row partials */
+    RDCN_KERNEL_HEAD_COLSUM = 25,   /* head backward: bias, gate and calibration gradients (column sums) */
+    RDCN_KERNEL_COUNT = 26
 } rdcn_kernel;
+
+/*
+ * ---------------------------------------------------------------------------
+ * Head: the layers after the cross stack, for a Feed-style tower.
+ *   - section "Dense Gating and Large MLP": wide ReLU layers on x = x_L, each
+ *     hidden layer gated. Gate (a reading: the paper gives the idea, from
+ *     GateNet, and its cost, negligible extra matrix work, not a formula): one
+ *     scalar per sample and layer from the layer's own input,
+ *       a_l = ReLU(W_l a_{l-1} + b_l) * sigmoid(g_l . a_{l-1} + c_l),  a_0 = x;
+ *   - logit y = w_out . a_L + b_out;
+ *   - section "Isotonic Calibration Layer", equation (calibration): with
+ *     t = y - lo, bucket k = the largest j in [0, K-1] with t - step*j > 0 (0 if
+ *     none; decided in float, each bound step*j rounded to float), v_i = step for
+ *     i < k, v_k = t - step*k:
+ *       y_cal = cal_b + sum_{i <= k} ReLU(e_i + cal_w_i) * v_i
+ *     (below lo and above lo + K*step the first and last buckets extend
+ *     linearly); e [batch, K] float is the per-sample calibration embedding,
+ *     made upstream. y_cal is monotone non-decreasing in y.
+ * bf16 models only. Activations a_l are kept in bf16, gate logits, y and y_cal
+ * in float.
+ * ---------------------------------------------------------------------------
+ */
+#define RDCN_HEAD_MAX_HIDDEN 8
+
+typedef struct rdcn_head_config {
+    int32_t num_hidden;                    /* hidden layers, 1 .. RDCN_HEAD_MAX_HIDDEN */
+    int32_t hidden[RDCN_HEAD_MAX_HIDDEN];  /* widths n_1 .. n_L, multiples of 8 (a width that is
+                                              not one is run exactly by zero rows of padding) */
+    int32_t gated;                         /* 0 or 1 */
+    int32_t num_buckets;                   /* K, 1 .. 65536 */
+    float bucket_lo;                       /* lo, finite */
+    float bucket_step;                     /* step > 0, finite */
+} rdcn_head_config;
+
+/*
+ * Head weights (entries at index >= num_hidden are ignored). n_0 = d.
+ *   w[l]      : [n_l, n_{l-1}]  bf16       b[l]      : [n_l]  bf16
+ *   gate_w[l] : [n_{l-1}]       bf16       gate_b[l] : [1]    bf16   (gated only)
+ *   w_out     : [n_L] bf16,  b_out : [1] bf16
+ *   cal_w     : [K] float,   cal_b : [1] float
+ * Vector operands (w, b, gate_w, w_out) must be 16-byte aligned. Gradients use
+ * the same struct with float buffers of the same shapes (overwritten).
+ */
+typedef struct rdcn_head_weights {
+    void* w[RDCN_HEAD_MAX_HIDDEN];
+    void* b[RDCN_HEAD_MAX_HIDDEN];
+    void* gate_w[RDCN_HEAD_MAX_HIDDEN];
+    void* gate_b[RDCN_HEAD_MAX_HIDDEN];
+    void* w_out;
+    void* b_out;
+    void* cal_w;
+    void* cal_b;
+} rdcn_head_weights;
+
+/*
+ * Attach a head to the handle (replacing any earlier one); its input width is
+ * the handle's d. RDCN_ERR_ARG for values out of range, RDCN_ERR_UNSUPPORTED
+ * for a float model or a batch_max above 8388480.
+ */
+rdcn_status rdcn_head_configure(rdcn_handle* h, const rdcn_head_config* cfg);
+
+/* Saved and scratch bytes of the head for `batch` samples (256-byte aligned buffers). */
+rdcn_status rdcn_head_workspace_bytes(const rdcn_handle* h, int64_t batch, size_t* saved_bytes,
+                                      size_t* scratch_bytes);
+
+/*
+ * Head forward: x [batch, d] bf16 (16-byte aligned; normally x_L of
+ * rdcn_forward), e_cal [batch, K] float -> y_logit [batch] and y_cal [batch]
+ * float. `saved` (rdcn_head_workspace_bytes) keeps the activations, gate logits
+ * and logits for rdcn_head_backward.
+ */
+rdcn_status rdcn_head_forward(rdcn_handle* h, int64_t batch, const void* x, const float* e_cal,
+                              const rdcn_head_weights* w, float* y_logit, float* y_cal, void* saved, void* stream);
+
+/*
+ * Log loss of a binary task on the calibrated logit z = y_cal, per sample:
+ * loss = softplus(z) - label * z, grad = (sigmoid(z) - label) * scale (pass
+ * scale = 1/batch for a mean loss). labels in [0, 1]; loss or grad may be NULL.
+ */
+rdcn_status rdcn_head_logloss(rdcn_handle* h, int64_t batch, const float* y_cal, const float* labels, float scale,
+                              float* loss, float* grad, void* stream);
+
+/*
+ * Head backward for dLoss/dy_cal = grad_ycal [batch] float. Writes grad_x
+ * [batch, d] bf16 (16-byte aligned; feeds rdcn_backward as grad_out), grad_e
+ * [batch, K] float and every parameter gradient in `grads` (float, overwritten,
+ * summed over the batch in a fixed order: deterministic). x, e_cal, w and saved
+ * must be those of the matching rdcn_head_forward. ReLU'(0) = 0.
+ */
+rdcn_status rdcn_head_backward(rdcn_handle* h, int64_t batch, const void* x, const float* e_cal,
+                               const rdcn_head_weights* w, const void* saved, const float* grad_ycal, void* grad_x,
+                               float* grad_e, const rdcn_head_weights* grads, void* scratch, void* stream);
 
 /*
  * Per-kernel timing with HIP events on the stream each kernel is launched on.

@@ -3,6 +3,8 @@
 // gather, the Residual-DCN forward and backward, and the embedding backward.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <cmath>
 #include <new>
 #include <string.h>
 #include <vector>
@@ -10,6 +12,7 @@
 #include "../../include/rdcn.h"
 #include "embed_bwd.h"
 #include "gemm.h"
+#include "head.h"
 #include "kernels.h"
 
 struct rdcn_handle {
@@ -20,6 +23,8 @@ struct rdcn_handle {
     bool bf16, ids64, attn, split, par;
     uint32_t magic, shift;
     int* err;  // device error word
+    bool head_on = false;
+    rdcn_head_config head{};
     // per-kernel timing (rdcn_profile_start / rdcn_profile_stop)
     bool prof_on = false;
     uint32_t prof_mask = 0;
@@ -207,6 +212,82 @@ rdcn_status gather_args(rdcn_handle* h, int64_t batch, const void* ids, const in
 bool q8_aligned(const rdcn_handle* h, const void* codes, const void* params) {
     const uintptr_t cm = h->bf16 ? 7u : 3u;
     return (((uintptr_t)codes) & cm) == 0 && (((uintptr_t)params) & 7u) == 0;
+}
+
+// ---------------------------------------------------------------------------
+// Head layouts. Saved: per hidden layer a_l [B, n_l] bf16 and (gated) s_l [B]
+// float, then y [B] float. Scratch: two G planes [B, n_max] bf16 (the current
+// layer's pre-activation gradient and the next one's), gy [B], two gs [B], the
+// gate row partials, column-sum partials and split-K partials.
+// ---------------------------------------------------------------------------
+inline int64_t head_in(const rdcn_handle* h, int l) { return l == 0 ? h->d : h->head.hidden[l - 1]; }
+
+struct HeadSaved {
+    size_t A[RDCN_HEAD_MAX_HIDDEN], S[RDCN_HEAD_MAX_HIDDEN], Y, total;
+};
+
+HeadSaved head_saved_layout(const rdcn_handle* h, int64_t B) {
+    HeadSaved s;
+    size_t off = 0;
+    for (int l = 0; l < h->head.num_hidden; ++l) {
+        s.A[l] = off; off += al((size_t)B * h->head.hidden[l] * 2);
+        s.S[l] = off; off += h->head.gated ? al((size_t)B * 4) : 0;
+    }
+    s.Y = off; off += al((size_t)B * 4);
+    s.total = off;
+    return s;
+}
+
+struct HeadScratch {
+    size_t G[2], gy, gs[2], rowpart, colpart, splitk, total;
+};
+
+HeadScratch head_scratch_layout(const rdcn_handle* h, int64_t B) {
+    const rdcn_head_config& c = h->head;
+    int64_t nmax = 0, tiles = 0, split = 0, widest = std::max<int64_t>(h->d, c.num_buckets);
+    for (int l = 0; l < c.num_hidden; ++l) {
+        const int64_t nin = head_in(h, l), nout = c.hidden[l];
+        nmax = std::max<int64_t>(nmax, nout);
+        widest = std::max<int64_t>(widest, nout);
+        if (l > 0) tiles = std::max<int64_t>(tiles, gemm_tiles_n(nin, plan_gemm(B, nin, nout, true, false)));
+        const GemmPlan pw = plan_gemm(nout, nin, B, true, true);
+        if (pw.splits > 1) split = std::max<int64_t>(split, pw.splits * nout * nin);
+    }
+    HeadScratch s;
+    size_t off = 0;
+    for (int i = 0; i < 2; ++i) { s.G[i] = off; off += al((size_t)B * nmax * 2); }
+    s.gy = off; off += al((size_t)B * 4);
+    for (int i = 0; i < 2; ++i) { s.gs[i] = off; off += al((size_t)B * 4); }
+    s.rowpart = off; off += c.gated ? al((size_t)tiles * B * 4) : 0;
+    s.colpart = off; off += al((size_t)colsum_chunks(B) * widest * 4);
+    s.splitk = off; off += al((size_t)split * 4);
+    s.total = off;
+    return s;
+}
+
+bool a16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+rdcn_status check_head_weights(const rdcn_handle* h, const rdcn_head_weights* w, bool grads) {
+    if (!w) return RDCN_ERR_ARG;
+    const rdcn_head_config& c = h->head;
+    for (int l = 0; l < c.num_hidden; ++l) {
+        if (!w->w[l] || !w->b[l] || !a16(w->w[l]) || !a16(w->b[l])) return RDCN_ERR_ARG;
+        if (c.gated && (!w->gate_w[l] || !w->gate_b[l] || !a16(w->gate_w[l]))) return RDCN_ERR_ARG;
+    }
+    if (!w->w_out || !w->b_out || !w->cal_w || !w->cal_b || !a16(w->w_out)) return RDCN_ERR_ARG;
+    (void)grads;
+    return RDCN_OK;
+}
+
+CalArgs cal_args(const rdcn_handle* h, const rdcn_head_weights* w, const float* e) {
+    CalArgs c;
+    c.K = h->head.num_buckets;
+    c.lo = h->head.bucket_lo;
+    c.step = h->head.bucket_step;
+    c.w = (const float*)w->cal_w;
+    c.b = (const float*)w->cal_b;
+    c.e = e;
+    return c;
 }
 
 }  // namespace
@@ -607,6 +688,175 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
             ProfScope ps(h, RDCN_KERNEL_BWD_GX_GEMM, s);
             RDCN_TRY(launch_gemm(g4, plan_gemm(B, d, nr, h->bf16, false), h->bf16, s));
         }
+    }
+    return RDCN_OK;
+}
+
+rdcn_status rdcn_head_configure(rdcn_handle* h, const rdcn_head_config* cfg) {
+    if (!h || !cfg) return RDCN_ERR_ARG;
+    const rdcn_head_config& c = *cfg;
+    if (c.num_hidden < 1 || c.num_hidden > RDCN_HEAD_MAX_HIDDEN || (c.gated != 0 && c.gated != 1) ||
+        c.num_buckets < 1 || c.num_buckets > 65536 || !std::isfinite(c.bucket_lo) || !std::isfinite(c.bucket_step) ||
+        !(c.bucket_step > 0.0f))
+        return RDCN_ERR_ARG;
+    for (int l = 0; l < c.num_hidden; ++l)
+        if (c.hidden[l] <= 0 || c.hidden[l] % 8) return RDCN_ERR_ARG;
+    if (!h->bf16) return RDCN_ERR_UNSUPPORTED;
+    if (h->cfg.batch_max > (int64_t)65535 * 128) return RDCN_ERR_UNSUPPORTED;  // column-sum chunks per launch
+    h->head = c;
+    for (int l = c.num_hidden; l < RDCN_HEAD_MAX_HIDDEN; ++l) h->head.hidden[l] = 0;
+    h->head_on = true;
+    return RDCN_OK;
+}
+
+rdcn_status rdcn_head_workspace_bytes(const rdcn_handle* h, int64_t batch, size_t* saved_bytes,
+                                      size_t* scratch_bytes) {
+    rdcn_status st = check_batch(h, batch);
+    if (st != RDCN_OK) return st;
+    if (!h->head_on) return RDCN_ERR_ARG;
+    if (!saved_bytes || !scratch_bytes) return RDCN_ERR_ARG;
+    *saved_bytes = head_saved_layout(h, batch).total;
+    *scratch_bytes = head_scratch_layout(h, batch).total;
+    return RDCN_OK;
+}
+
+rdcn_status rdcn_head_forward(rdcn_handle* h, int64_t batch, const void* x, const float* e_cal,
+                              const rdcn_head_weights* w, float* y_logit, float* y_cal, void* saved, void* stream) {
+    rdcn_status st = check_batch(h, batch);
+    if (st != RDCN_OK) return st;
+    if (!h->head_on) return RDCN_ERR_ARG;
+    if ((st = check_head_weights(h, w, false)) != RDCN_OK) return st;
+    if (batch == 0) return RDCN_OK;
+    if (!x || !a16(x) || !e_cal || !y_logit || !y_cal || !saved) return RDCN_ERR_ARG;
+    if (!aligned256(saved)) return RDCN_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    const rdcn_head_config& c = h->head;
+    const int64_t B = batch;
+    const HeadSaved S = head_saved_layout(h, B);
+    char* sv = (char*)saved;
+    for (int l = 0; l < c.num_hidden; ++l) {
+        const int64_t nin = head_in(h, l), nout = c.hidden[l];
+        const void* in = l == 0 ? x : (const void*)(sv + S.A[l - 1]);
+        float* sl = c.gated ? (float*)(sv + S.S[l]) : nullptr;
+        if (c.gated) {
+            ProfScope ps(h, RDCN_KERNEL_HEAD_GATE, s);
+            RDCN_TRY(launch_gate_logit(B, (int)nin, in, nin, w->gate_w[l], w->gate_b[l], sl, s));
+        }
+        GemmArgs g{};
+        g.M = B; g.N = nout; g.K = nin;
+        g.a = in; g.lda = nin;
+        g.b = w->w[l]; g.ldb = nin;
+        g.epi = EPI_MLP_FWD; g.scale = 1.0f;
+        g.bias = w->b[l];
+        g.rowv = sl;
+        g.c = sv + S.A[l]; g.ldc = nout;
+        ProfScope ps(h, RDCN_KERNEL_HEAD_FWD_GEMM, s);
+        RDCN_TRY(launch_gemm(g, plan_gemm(B, nout, nin, true, false), true, s));
+    }
+    const int L = c.num_hidden;
+    ProfScope ps(h, RDCN_KERNEL_HEAD_OUT, s);
+    return hip_status(launch_head_out(B, c.hidden[L - 1], sv + S.A[L - 1], w->w_out, w->b_out, cal_args(h, w, e_cal),
+                                      (float*)(sv + S.Y), y_logit, y_cal, s));
+}
+
+rdcn_status rdcn_head_logloss(rdcn_handle* h, int64_t batch, const float* y_cal, const float* labels, float scale,
+                              float* loss, float* grad, void* stream) {
+    rdcn_status st = check_batch(h, batch);
+    if (st != RDCN_OK) return st;
+    if (batch == 0) return RDCN_OK;
+    if (!y_cal || !labels || !std::isfinite(scale)) return RDCN_ERR_ARG;
+    ProfScope ps(h, RDCN_KERNEL_HEAD_LOSS, (hipStream_t)stream);
+    return hip_status(launch_logloss(batch, y_cal, labels, scale, loss, grad, (hipStream_t)stream));
+}
+
+rdcn_status rdcn_head_backward(rdcn_handle* h, int64_t batch, const void* x, const float* e_cal,
+                               const rdcn_head_weights* w, const void* saved, const float* grad_ycal, void* grad_x,
+                               float* grad_e, const rdcn_head_weights* grads, void* scratch, void* stream) {
+    rdcn_status st = check_batch(h, batch);
+    if (st != RDCN_OK) return st;
+    if (!h->head_on) return RDCN_ERR_ARG;
+    if ((st = check_head_weights(h, w, false)) != RDCN_OK) return st;
+    if ((st = check_head_weights(h, grads, true)) != RDCN_OK) return st;
+    if (!scratch || !aligned256(scratch)) return RDCN_ERR_WORKSPACE;
+    if (batch > 0) {
+        if (!x || !a16(x) || !e_cal || !saved || !grad_ycal || !grad_x || !a16(grad_x) || !grad_e)
+            return RDCN_ERR_ARG;
+        if (!aligned256(saved)) return RDCN_ERR_WORKSPACE;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    const rdcn_head_config& c = h->head;
+    const int64_t B = batch;
+    const int L = c.num_hidden;
+    const HeadSaved S = head_saved_layout(h, B);
+    const HeadScratch W = head_scratch_layout(h, B);
+    const char* sv = (const char*)saved;
+    char* sc = (char*)scratch;
+    float* gy = (float*)(sc + W.gy);
+    float* colpart = (float*)(sc + W.colpart);
+    auto colsum = [&](int64_t n, const void* X, int64_t ldx, bool xbf16, const float* wgt, void* out) -> hipError_t {
+        ProfScope ps(h, RDCN_KERNEL_HEAD_COLSUM, s);
+        return launch_colsum_w(B, n, X, ldx, xbf16, wgt, colpart, (float*)out, s);
+    };
+    const void* aL = B > 0 ? (const void*)(sv + S.A[L - 1]) : nullptr;
+    int cur = 0;
+    {
+        ProfScope ps(h, RDCN_KERNEL_HEAD_OUT_BWD, s);
+        RDCN_TRY(launch_head_out_bwd(B, c.hidden[L - 1], aL, c.gated && B > 0 ? (const float*)(sv + S.S[L - 1]) : nullptr,
+                                     w->w_out, B > 0 ? (const float*)(sv + S.Y) : nullptr, cal_args(h, w, e_cal),
+                                     grad_ycal, grad_e, gy, sc + W.G[cur], (float*)(sc + W.gs[cur]), s));
+    }
+    RDCN_TRY(colsum(c.hidden[L - 1], aL, c.hidden[L - 1], true, gy, grads->w_out));
+    RDCN_TRY(colsum(1, gy, 1, false, nullptr, grads->b_out));
+    RDCN_TRY(colsum(c.num_buckets, grad_e, c.num_buckets, false, nullptr, grads->cal_w));
+    RDCN_TRY(colsum(1, grad_ycal, 1, false, nullptr, grads->cal_b));
+    for (int l = L - 1; l >= 0; --l) {
+        const int64_t nin = head_in(h, l), nout = c.hidden[l];
+        const void* in = l == 0 ? x : (const void*)(sv + S.A[l - 1]);
+        const void* G = sc + W.G[cur];
+        const float* gsl = (const float*)(sc + W.gs[cur]);
+        RDCN_TRY(colsum(nout, G, nout, true, nullptr, grads->b[l]));
+        if (c.gated) {
+            RDCN_TRY(colsum(nin, in, nin, true, gsl, grads->gate_w[l]));
+            RDCN_TRY(colsum(1, gsl, 1, false, nullptr, grads->gate_b[l]));
+        }
+        {
+            GemmArgs g{};
+            g.M = nout; g.N = nin; g.K = B;
+            g.a = G; g.lda = nout; g.a_kstrided = true;
+            g.b = in; g.ldb = nin; g.b_kstrided = true;
+            g.scale = 1.0f;
+            RDCN_TRY(gemm_weight_grad(h, RDCN_KERNEL_HEAD_GW_GEMM, g, (float*)grads->w[l], (float*)(sc + W.splitk), s));
+        }
+        GemmArgs g{};
+        g.M = B; g.N = nin; g.K = nout;
+        g.a = G; g.lda = nout;
+        g.b = w->w[l]; g.ldb = nin; g.b_kstrided = true;
+        g.epi = EPI_MLP_BWD; g.scale = 1.0f;
+        if (c.gated) {
+            g.colv = w->gate_w[l];
+            g.rowv = gsl;
+        }
+        const GemmPlan p = plan_gemm(B, nin, nout, true, false);
+        if (l > 0) {
+            g.act = sv + S.A[l - 1]; g.ldx = nin;
+            g.c = sc + W.G[1 - cur]; g.ldc = nin;
+            if (c.gated) {
+                g.rowg = (const float*)(sv + S.S[l - 1]);
+                g.rowpart = (float*)(sc + W.rowpart);
+            }
+        } else {
+            g.c = grad_x; g.ldc = nin;
+        }
+        {
+            ProfScope ps(h, RDCN_KERNEL_HEAD_GX_GEMM, s);
+            RDCN_TRY(launch_gemm(g, p, true, s));
+        }
+        if (l > 0 && c.gated) {
+            ProfScope ps(h, RDCN_KERNEL_HEAD_GATE_BWD, s);
+            RDCN_TRY(launch_gate_finalize(B, (int)gemm_tiles_n(nin, p), (const float*)(sc + W.rowpart),
+                                          (const float*)(sv + S.S[l - 1]), (float*)(sc + W.gs[1 - cur]), s));
+        }
+        cur = 1 - cur;
     }
     return RDCN_OK;
 }

@@ -12,7 +12,13 @@ enum GemmEpi {
     EPI_CROSS = 3,      // t = scale*acc + bias[n]; c = x0 * t + xl; t_out = t   (storage type;
                         // xl2 / c2: lo planes of a hi + lo bf16 input / output)
     EPI_RESID = 4,      // c (float) = gin + scale * acc
-    EPI_RESID_X0 = 5    // c (float) += gin + scale * acc
+    EPI_RESID_X0 = 5,   // c (float) += gin + scale * acc
+    // MLP layers (bf16 storage, A K-contiguous):
+    EPI_MLP_FWD = 6,    // c = ReLU(scale*acc + bias[n]) * (rowv ? sigmoid(rowv[m]) : 1)
+    EPI_MLP_BWD = 7     // v = scale*acc + (colv ? rowv[m] * colv[n] : 0);
+                        // act == NULL: c = v;
+                        // else c = v * [act[m, n] > 0] * (rowg ? sigmoid(rowg[m]) : 1), and with
+                        // rowpart: rowpart[(n0 / BN) * M + m] = sum over the tile's columns of v * act
 };
 
 struct GemmArgs {
@@ -37,6 +43,12 @@ struct GemmArgs {
     const void* gin;
     bool gin_f32;
     int64_t ldx;
+    // MLP epilogue operands (act has row stride ldx)
+    const float* rowv;
+    const void* colv;
+    const float* rowg;
+    const void* act;
+    float* rowpart;
 };
 
 struct GemmPlan {
@@ -47,6 +59,8 @@ struct GemmPlan {
 
 GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool bf16, bool allow_split);
 hipError_t launch_gemm(const GemmArgs& g, const GemmPlan& p, bool bf16, hipStream_t s);
+// Column tiles of an MLP GEMM under plan p (the rowpart partials per row).
+inline int64_t gemm_tiles_n(int64_t N, const GemmPlan& p) { return (N + p.bn - 1) / p.bn; }
 hipError_t launch_splitk_reduce(const float* part, int splits, int64_t MN, float* out, hipStream_t s);
 
 }  // namespace rdcn

@@ -21,6 +21,7 @@
 // and stores are 8- or 16-byte vectors along the rows of x0, x_l, t and g.
 #include "device_common.h"
 #include "gemm.h"
+#include "mlp_common.h"
 
 namespace rdcn {
 
@@ -207,6 +208,46 @@ __device__ __forceinline__ void epilogue8(const GemmArgs& g, int64_t m, int64_t 
             break;
         }
     }
+}
+
+// MLP epilogues on eight consecutive columns n .. n+7 of row m (n + 7 < N); returns
+// this thread's share of the row dot product sum(v * act) (EPI_MLP_BWD with act).
+template <typename T>
+__device__ __forceinline__ float mlp_epilogue8(const GemmArgs& g, int64_t m, int64_t n, float* v) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] *= g.scale;
+    T* out = (T*)g.c + m * g.ldc + n;
+    if (g.epi == EPI_MLP_FWD) {
+        float b[8];
+        load8<T>((const T*)g.bias + n, b);
+        const float gate = g.rowv ? sigmoid_f(g.rowv[m]) : 1.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = relu_f(v[e] + b[e]) * gate;
+        store8<T>(out, v);
+        return 0.f;
+    }
+    if (g.colv) {  // the gate's rank-one term
+        float cv[8];
+        load8<T>((const T*)g.colv + n, cv);
+        const float r = g.rowv[m];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = fmaf(r, cv[e], v[e]);
+    }
+    if (!g.act) {
+        store8<T>(out, v);
+        return 0.f;
+    }
+    float a[8];
+    load8<T>((const T*)g.act + m * g.ldx + n, a);
+    const float rho = g.rowg ? sigmoid_f(g.rowg[m]) : 1.f;
+    float dot = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        dot = fmaf(v[e], a[e], dot);
+        v[e] = a[e] > 0.f ? rho * v[e] : 0.f;
+    }
+    store8<T>(out, v);
+    return dot;
 }
 
 __device__ __forceinline__ int xcd_remap(int id, int n) {
@@ -409,7 +450,7 @@ struct Pipe {
 };
 
 // C = A B^T with an ST-stage direct-to-LDS pipeline (see layouts above).
-template <int BM, int BN, bool AKS, bool BKS, int ST, typename T>
+template <int BM, int BN, bool AKS, bool BKS, int ST, typename T, bool MLP>
 __global__ __launch_bounds__(256, ST == 2 ? 2 : 1) void k_gemm_mfma(GemmArgs g) {
     using P = Pipe<BM, BN, AKS, BKS, ST>;
     // one buffer: the stage ring during the K loop, the C staging area afterwards
@@ -485,11 +526,26 @@ __global__ __launch_bounds__(256, ST == 2 ? 2 : 1) void k_gemm_mfma(GemmArgs g) 
         for (int q = tid; q < CH * (BN / 8); q += 256) {
             const int row = q / (BN / 8), col = (q % (BN / 8)) * 8;
             const int64_t m = c.m0 + h * CH + row, n = c.n0 + col;
-            if (m >= g.M || n >= g.N) continue;
-            float v[8];
-            *(f32x4_t*)v = *(const f32x4_t*)(cs + row * CP + col);
-            *(f32x4_t*)(v + 4) = *(const f32x4_t*)(cs + row * CP + col + 4);
-            epilogue8<T>(g, m, n, z, v);
+            if (!MLP) {
+                if (m >= g.M || n >= g.N) continue;
+                float v[8];
+                *(f32x4_t*)v = *(const f32x4_t*)(cs + row * CP + col);
+                *(f32x4_t*)(v + 4) = *(const f32x4_t*)(cs + row * CP + col + 4);
+                epilogue8<T>(g, m, n, z, v);
+            } else {
+                float part = 0.f;
+                if (m < g.M && n < g.N) {
+                    float v[8];
+                    *(f32x4_t*)v = *(const f32x4_t*)(cs + row * CP + col);
+                    *(f32x4_t*)(v + 4) = *(const f32x4_t*)(cs + row * CP + col + 4);
+                    part = mlp_epilogue8<T>(g, m, n, v);
+                }
+                if (g.rowpart) {  // uniform: the BN / 8 threads of one row are an aligned lane group
+#pragma unroll
+                    for (int o = 1; o < BN / 8; o <<= 1) part += __shfl_xor(part, o);
+                    if (col == 0 && m < g.M) g.rowpart[(int64_t)(c.n0 / BN) * g.M + m] = part;
+                }
+            }
         }
     }
 }
@@ -560,11 +616,16 @@ template <int BM, int BN, int ST, typename T>
 hipError_t launch_tile(const GemmArgs& g, int splits, hipStream_t s) {
     const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
     dim3 grid((unsigned)tiles, 1, (unsigned)splits);
-#define RDCN_GEMM(AK, BKS) hipLaunchKernelGGL((k_gemm_mfma<BM, BN, AK, BKS, ST, T>), grid, dim3(256), 0, s, g)
-    if (g.a_kstrided) {
-        if (g.b_kstrided) RDCN_GEMM(true, true); else RDCN_GEMM(true, false);
+#define RDCN_GEMM(AK, BKS, MLP) \
+    hipLaunchKernelGGL((k_gemm_mfma<BM, BN, AK, BKS, ST, T, MLP>), grid, dim3(256), 0, s, g)
+    if (g.epi == EPI_MLP_FWD || g.epi == EPI_MLP_BWD) {
+        // MLP layers: forward (both K-contiguous) and input gradient (B K-strided), no split-K
+        if (g.a_kstrided || splits != 1) return hipErrorInvalidValue;
+        if (g.b_kstrided) RDCN_GEMM(false, true, true); else RDCN_GEMM(false, false, true);
+    } else if (g.a_kstrided) {
+        if (g.b_kstrided) RDCN_GEMM(true, true, false); else RDCN_GEMM(true, false, false);
     } else {
-        if (g.b_kstrided) RDCN_GEMM(false, true); else RDCN_GEMM(false, false);
+        if (g.b_kstrided) RDCN_GEMM(false, true, false); else RDCN_GEMM(false, false, false);
     }
 #undef RDCN_GEMM
     return hipGetLastError();
@@ -602,6 +663,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool bf16, bool allow_split)
 
 hipError_t launch_gemm(const GemmArgs& g, const GemmPlan& p, bool bf16, hipStream_t s) {
     if (g.M == 0 || g.N == 0) return hipSuccess;
+    if (!bf16 && (g.epi == EPI_MLP_FWD || g.epi == EPI_MLP_BWD)) return hipErrorInvalidValue;
     if (!bf16) {
         const int64_t tiles = ((g.M + 63) / 64) * ((g.N + 63) / 64);
         hipLaunchKernelGGL(k_gemm_f32, dim3((unsigned)tiles, 1, (unsigned)p.splits), dim3(256), 0, s, g);

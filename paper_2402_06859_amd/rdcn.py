@@ -24,11 +24,14 @@ COMBINE_MUL, COMBINE_SUM = 0, 1
 EXPORTS = ["rdcn_create", "rdcn_destroy", "rdcn_dim", "rdcn_workspace_bytes", "qr_embed_gather",
            "qr_embed_backward_workspace", "qr_embed_backward", "rdcn_forward", "rdcn_backward",
            "rdcn_check_device_errors", "rdcn_status_string", "rdcn_profile_start", "rdcn_profile_stop",
-           "qr_quantize_tables", "qr_embed_gather_q8"]
+           "qr_quantize_tables", "qr_embed_gather_q8", "rdcn_head_configure", "rdcn_head_workspace_bytes",
+           "rdcn_head_forward", "rdcn_head_logloss", "rdcn_head_backward"]
 
 KERNELS = ["gather", "fwd_down_gemm", "fwd_attention", "fwd_up_gemm", "bwd_pointwise", "bwd_bias", "bwd_gu_gemm",
            "bwd_gh_gemm", "bwd_attention", "bwd_gw_gemm", "bwd_gx_gemm", "splitk_reduce", "emb_keys", "emb_sort",
-           "emb_reduce", "gather_q8", "quantize"]
+           "emb_reduce", "gather_q8", "quantize", "head_gate", "head_fwd_gemm", "head_out", "head_loss",
+           "head_out_bwd", "head_gw_gemm", "head_gx_gemm", "head_gate_bwd", "head_colsum"]
+MAX_HIDDEN = 8
 
 
 class RdcnConfig(ctypes.Structure):
@@ -44,6 +47,40 @@ class RdcnConfig(ctypes.Structure):
 class RdcnWeights(ctypes.Structure):
     _fields_ = [("w_down", ctypes.c_void_p * MAX_LAYERS), ("u", ctypes.c_void_p * MAX_LAYERS),
                 ("bias", ctypes.c_void_p * MAX_LAYERS)]
+
+
+class RdcnHeadConfig(ctypes.Structure):
+    _fields_ = [("num_hidden", ctypes.c_int32), ("hidden", ctypes.c_int32 * MAX_HIDDEN), ("gated", ctypes.c_int32),
+                ("num_buckets", ctypes.c_int32), ("bucket_lo", ctypes.c_float), ("bucket_step", ctypes.c_float)]
+
+
+class RdcnHeadWeights(ctypes.Structure):
+    _fields_ = [("w", ctypes.c_void_p * MAX_HIDDEN), ("b", ctypes.c_void_p * MAX_HIDDEN),
+                ("gate_w", ctypes.c_void_p * MAX_HIDDEN), ("gate_b", ctypes.c_void_p * MAX_HIDDEN),
+                ("w_out", ctypes.c_void_p), ("b_out", ctypes.c_void_p), ("cal_w", ctypes.c_void_p),
+                ("cal_b", ctypes.c_void_p)]
+
+
+def make_head_config(hidden: Sequence[int], gated: bool, num_buckets: int, bucket_lo: float,
+                     bucket_step: float) -> RdcnHeadConfig:
+    c = RdcnHeadConfig()
+    c.num_hidden = len(hidden)
+    for i, n in enumerate(hidden):
+        c.hidden[i] = n
+    c.gated, c.num_buckets, c.bucket_lo, c.bucket_step = int(gated), num_buckets, bucket_lo, bucket_step
+    return c
+
+
+def head_weights(p: dict) -> RdcnHeadWeights:
+    """p: W, b, (G, c), w_out, b_out, cal_w, cal_b (device tensors; G and c only when gated)."""
+    w = RdcnHeadWeights()
+    for l in range(len(p["W"])):
+        w.w[l], w.b[l] = p["W"][l].data_ptr(), p["b"][l].data_ptr()
+        if p.get("G") is not None:
+            w.gate_w[l], w.gate_b[l] = p["G"][l].data_ptr(), p["c"][l].data_ptr()
+    w.w_out, w.b_out = p["w_out"].data_ptr(), p["b_out"].data_ptr()
+    w.cal_w, w.cal_b = p["cal_w"].data_ptr(), p["cal_b"].data_ptr()
+    return w
 
 
 class RdcnError(RuntimeError):
@@ -83,6 +120,12 @@ def load(build_if_missing: bool = True):
     L.rdcn_backward.argtypes = [vp, i64, vp, ctypes.POINTER(RdcnWeights), vp, vp, vp, ctypes.POINTER(RdcnWeights),
                                 vp, vp]
     L.rdcn_check_device_errors.argtypes = [vp, vp]
+    L.rdcn_head_configure.argtypes = [vp, ctypes.POINTER(RdcnHeadConfig)]
+    L.rdcn_head_workspace_bytes.argtypes = [vp, i64, ctypes.POINTER(sz), ctypes.POINTER(sz)]
+    L.rdcn_head_forward.argtypes = [vp, i64, vp, vp, ctypes.POINTER(RdcnHeadWeights), vp, vp, vp, vp]
+    L.rdcn_head_logloss.argtypes = [vp, i64, vp, vp, ctypes.c_float, vp, vp, vp]
+    L.rdcn_head_backward.argtypes = [vp, i64, vp, vp, ctypes.POINTER(RdcnHeadWeights), vp, vp, vp, vp,
+                                     ctypes.POINTER(RdcnHeadWeights), vp, vp]
     L.rdcn_profile_start.argtypes = [vp, ctypes.c_int32, ctypes.c_uint32]
     L.rdcn_profile_stop.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
     for name in EXPORTS:
@@ -214,6 +257,35 @@ class Rdcn:
         _check("rdcn_backward", load().rdcn_backward(self.h, batch, _ptr(x0), ctypes.byref(w), _ptr(saved),
                                                      _ptr(grad_out), _ptr(grad_x0), ctypes.byref(g), _ptr(scratch),
                                                      _stream(stream)))
+
+    # ---- head (layers after the cross stack)
+    def head_configure(self, cfg: RdcnHeadConfig):
+        _check("rdcn_head_configure", load().rdcn_head_configure(self.h, ctypes.byref(cfg)))
+        self.head_cfg = cfg
+
+    def head_workspace_bytes(self, batch: int):
+        s, t = ctypes.c_size_t(), ctypes.c_size_t()
+        _check("rdcn_head_workspace_bytes",
+               load().rdcn_head_workspace_bytes(self.h, batch, ctypes.byref(s), ctypes.byref(t)))
+        return s.value, t.value
+
+    def head_forward(self, batch, x, e_cal, params: dict, y_logit, y_cal, saved, stream=None):
+        w = head_weights(params)
+        _check("rdcn_head_forward", load().rdcn_head_forward(self.h, batch, _ptr(x), _ptr(e_cal), ctypes.byref(w),
+                                                             _ptr(y_logit), _ptr(y_cal), _ptr(saved),
+                                                             _stream(stream)))
+
+    def head_logloss(self, batch, y_cal, labels, scale, loss=None, grad=None, stream=None):
+        _check("rdcn_head_logloss", load().rdcn_head_logloss(self.h, batch, _ptr(y_cal), _ptr(labels), scale,
+                                                             _ptr(loss), _ptr(grad), _stream(stream)))
+
+    def head_backward(self, batch, x, e_cal, params: dict, saved, grad_ycal, grad_x, grad_e, grads: dict, scratch,
+                      stream=None):
+        w = head_weights(params)
+        g = head_weights(grads)
+        _check("rdcn_head_backward", load().rdcn_head_backward(
+            self.h, batch, _ptr(x), _ptr(e_cal), ctypes.byref(w), _ptr(saved), _ptr(grad_ycal), _ptr(grad_x),
+            _ptr(grad_e), ctypes.byref(g), _ptr(scratch), _stream(stream)))
 
     def profile_start(self, max_launches: int = 8192, kernels=None):
         """Time the launches of `kernels` (names from KERNELS; all when None)."""

@@ -76,3 +76,61 @@ class DeviceBatch:
         self.forward(stream)
         self.backward(stream=stream)
         self.embed_backward(stream=stream)
+
+
+class DeviceHead:
+    """Device buffers of the head after the cross stack (gated MLP, logit, isotonic
+    calibration, log loss) on the handle `lib`, and its call order."""
+
+    def __init__(self, lib: Rdcn, head, hinp: dict, B: int, device: str = "cuda"):
+        from .rdcn import make_head_config
+        dev = torch.device(device)
+        self.lib = lib
+        self.head = head
+        self.B = B
+        lib.head_configure(make_head_config(head.widths, head.gated, head.buckets, head.lo, head.step))
+        keys = ["W", "b"] + (["G", "c"] if head.gated else [])
+        self.params = {k: [t.contiguous().to(dev) for t in hinp[k]] for k in keys}
+        for k in ("w_out", "b_out", "cal_w", "cal_b"):
+            self.params[k] = hinp[k].contiguous().to(dev)
+        self.e = hinp["e"].contiguous().to(dev)
+        self.labels = hinp["labels"].contiguous().to(dev)
+        self.g_cal_in = hinp["g_cal"].contiguous().to(dev) if "g_cal" in hinp else None
+        self.x = hinp["x"].contiguous().to(dev) if "x" in hinp else None
+        saved_b, scratch_b = lib.head_workspace_bytes(B)
+        self.saved = torch.empty(max(saved_b, 1), dtype=torch.uint8, device=dev)
+        self.scratch = torch.empty(max(scratch_b, 1), dtype=torch.uint8, device=dev)
+        self.y = torch.empty(B, dtype=torch.float32, device=dev)
+        self.y_cal = torch.empty(B, dtype=torch.float32, device=dev)
+        self.loss = torch.empty(B, dtype=torch.float32, device=dev)
+        self.g_cal = torch.empty(B, dtype=torch.float32, device=dev)
+        self.grad_x = torch.empty((B, lib.d), dtype=torch.bfloat16, device=dev)
+        self.grad_e = torch.empty(self.e.shape, dtype=torch.float32, device=dev)
+        self.grads = {k: [torch.empty(t.shape, dtype=torch.float32, device=dev) for t in self.params[k]]
+                      for k in keys}
+        for k in ("w_out", "b_out", "cal_w", "cal_b"):
+            self.grads[k] = torch.empty(self.params[k].shape, dtype=torch.float32, device=dev)
+
+    def forward(self, x: Optional[torch.Tensor] = None, stream=None):
+        self.lib.head_forward(self.B, self.x if x is None else x, self.e, self.params, self.y, self.y_cal,
+                              self.saved, stream)
+
+    def logloss(self, stream=None):
+        """Mean log loss over the batch: per-sample losses and dLoss/dy_cal = (sigmoid - label) / B."""
+        self.lib.head_logloss(self.B, self.y_cal, self.labels, 1.0 / max(self.B, 1), self.loss, self.g_cal, stream)
+
+    def backward(self, x: Optional[torch.Tensor] = None, g_cal: Optional[torch.Tensor] = None, stream=None):
+        self.lib.head_backward(self.B, self.x if x is None else x, self.e, self.params, self.saved,
+                               self.g_cal if g_cal is None else g_cal, self.grad_x, self.grad_e, self.grads,
+                               self.scratch, stream)
+
+    def tower_step(self, db: "DeviceBatch", stream=None):
+        """One training step of a Feed-style tower: gather -> cross stack -> head ->
+        log loss -> head backward -> cross-stack backward -> embedding backward."""
+        db.gather(stream)
+        db.forward(stream)
+        self.forward(db.x_out, stream)
+        self.logloss(stream)
+        self.backward(db.x_out, stream=stream)
+        db.backward(self.grad_x, stream)
+        db.embed_backward(stream=stream)

@@ -229,3 +229,80 @@ def grad_x0_like(wl: Workload, B: int, seed: int):
     import torch
     rng = np.random.Generator(np.random.PCG64(seed))
     return torch.from_numpy(rng.standard_normal((B, wl.d), dtype=np.float32))
+
+
+# ---------------------------------------------------------------------------
+# Head after the cross stack (section "Dense Gating and Large MLP", section
+# "Isotonic Calibration Layer"): gated wide ReLU layers, a logit, calibration.
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class HeadSpec:
+    name: str
+    hidden: tuple            # logical widths (the Feed "Large MLP" is 4 x 3500)
+    gated: bool = True
+    buckets: int = 32        # K calibration buckets over [lo, lo + K*step]
+    lo: float = -4.0
+    step: float = 0.25
+    gate_bias: float = 1.0   # initial gate logit offset (gates start mostly open)
+    e_std: float = 0.1       # per-sample calibration embedding values
+    label_rate: float = 0.1  # positive rate of the synthetic binary labels
+
+    @property
+    def widths(self) -> tuple:
+        """Stored widths: each logical width rounded up to a multiple of 8; the extra
+        units have zero weights and biases, so the model is exactly the logical one."""
+        return tuple(-(-n // 8) * 8 for n in self.hidden)
+
+
+HEADS: Dict[str, HeadSpec] = {
+    "lmlp": HeadSpec("lmlp", (3500, 3500, 3500, 3500)),
+    "small": HeadSpec("small", (256, 128)),
+}
+
+
+def make_head_inputs(wl: Workload, head: HeadSpec, batch: Optional[int] = None, seed: Optional[int] = None,
+                     with_x: bool = True, bias_std: float = 0.05) -> dict:
+    """Seeded head parameters and per-sample inputs (torch CPU tensors).
+
+    W[l] [n_l, n_{l-1}] bf16 He-normal (std sqrt(2/n_{l-1}) over the logical fan-in),
+    b[l] N(0, bias_std^2), gate weights G[l] [n_{l-1}] N(0, 1/n_{l-1}) and gate bias
+    c[l] [1] = gate_bias, w_out N(0, 1/n_L), b_out 0, cal_w U(0.5, 1.5) float, cal_b 0;
+    e [B, K] N(0, e_std^2) float, labels Bernoulli(label_rate) float, g_cal [B] N(0, 1)
+    float (an upstream gradient for tests); x [B, d] bf16 N(0, 1) when with_x. Units
+    beyond a logical width have zero weights, biases, gate and output weights."""
+    B = wl.batch if batch is None else batch
+    base = SEED_BASE + 1000 + wl.index if seed is None else seed
+    ss = np.random.SeedSequence(base).spawn(4)
+    rw, rc, rx, rg = (np.random.Generator(np.random.PCG64(s)) for s in ss)
+    logical = (wl.d,) + tuple(head.hidden)
+    stored = (wl.d,) + head.widths
+    W, b, G, c = [], [], [], []
+    for l in range(len(head.hidden)):
+        nin, nout = stored[l], stored[l + 1]
+        w = np.zeros((nout, nin), np.float32)
+        w[:logical[l + 1], :logical[l]] = rw.standard_normal((logical[l + 1], logical[l]), dtype=np.float32) * \
+            math.sqrt(2.0 / logical[l])
+        bv = np.zeros(nout, np.float32)
+        bv[:logical[l + 1]] = rw.standard_normal(logical[l + 1], dtype=np.float32) * bias_std
+        g = np.zeros(nin, np.float32)
+        g[:logical[l]] = rw.standard_normal(logical[l], dtype=np.float32) / math.sqrt(logical[l])
+        W.append(to_storage(w, "bf16"))
+        b.append(to_storage(bv, "bf16"))
+        G.append(to_storage(g, "bf16"))
+        c.append(to_storage(np.array([head.gate_bias], np.float32), "bf16"))
+    wo = np.zeros(stored[-1], np.float32)
+    wo[:logical[-1]] = rw.standard_normal(logical[-1], dtype=np.float32) / math.sqrt(logical[-1])
+    K = head.buckets
+    import torch
+    out = {"W": W, "b": b, "w_out": to_storage(wo, "bf16"), "b_out": to_storage(np.zeros(1, np.float32), "bf16"),
+           "cal_w": torch.from_numpy(rc.uniform(0.5, 1.5, K).astype(np.float32)),
+           "cal_b": torch.zeros(1, dtype=torch.float32),
+           "e": torch.from_numpy(rc.standard_normal((B, K), dtype=np.float32) * head.e_std),
+           "labels": torch.from_numpy((rc.random(B) < head.label_rate).astype(np.float32)),
+           "g_cal": torch.from_numpy(rg.standard_normal(B, dtype=np.float32))}
+    if head.gated:
+        out["G"], out["c"] = G, c
+    if with_x:
+        out["x"] = to_storage(rx.standard_normal((B, wl.d), dtype=np.float32), "bf16")
+    return out

@@ -138,3 +138,32 @@ def test_hashed_front_end_validation():
     c = good()
     c.reserved2 = 1
     assert L.rdcn_create(ctypes.byref(c), ctypes.byref(h)) == rdcn.RDCN_ERR_ARG
+
+
+def test_head_struct_layout_matches_c(tmp_path):
+    prog = tmp_path / "hlayout.c"
+    prog.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "rdcn.h"\n'
+                    'int main(void){printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(rdcn_head_config),'
+                    ' offsetof(rdcn_head_config, gated), offsetof(rdcn_head_config, bucket_step),'
+                    ' sizeof(rdcn_head_weights), offsetof(rdcn_head_weights, w_out), offsetof(rdcn_head_weights, cal_b));'
+                    'return 0;}\n')
+    exe = tmp_path / "hlayout"
+    subprocess.check_call(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), str(prog), "-o", str(exe)])
+    vals = [int(v) for v in subprocess.check_output([str(exe)]).split()]
+    C, W = rdcn.RdcnHeadConfig, rdcn.RdcnHeadWeights
+    assert vals == [ctypes.sizeof(C), C.gated.offset, C.bucket_step.offset, ctypes.sizeof(W), W.w_out.offset,
+                    W.cal_b.offset]
+    assert len(rdcn.KERNELS) == 26  # RDCN_KERNEL_COUNT: rdcn_profile_stop writes that many entries
+
+
+def test_head_calls_reject_null_handle():
+    L = rdcn.load()
+    cfg = rdcn.make_head_config([16], True, 4, -1.0, 0.5)
+    s, t = ctypes.c_size_t(), ctypes.c_size_t()
+    w = rdcn.RdcnHeadWeights()
+    assert L.rdcn_head_configure(None, ctypes.byref(cfg)) == rdcn.RDCN_ERR_ARG
+    assert L.rdcn_head_workspace_bytes(None, 4, ctypes.byref(s), ctypes.byref(t)) == rdcn.RDCN_ERR_ARG
+    assert L.rdcn_head_forward(None, 4, None, None, ctypes.byref(w), None, None, None, None) == rdcn.RDCN_ERR_ARG
+    assert L.rdcn_head_logloss(None, 4, None, None, 1.0, None, None, None) == rdcn.RDCN_ERR_ARG
+    assert L.rdcn_head_backward(None, 4, None, None, ctypes.byref(w), None, None, None, None, ctypes.byref(w), None,
+                                None) == rdcn.RDCN_ERR_ARG
