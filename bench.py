@@ -94,6 +94,36 @@ def kernel_work(wl, B: int) -> dict:
     return w
 
 
+def head_work(wl, head, B: int) -> dict:
+    """Algorithmic work per launch of the head kernels (averaged over the launches of a
+    step where layers differ): flops of the logical widths (the zero padding to a
+    multiple of 8 is not counted), bytes of each operand read once and each result
+    written once (bf16 activations, weights and G; float gate logits, logits and
+    calibration data)."""
+    n = [wl.d] + list(head.hidden)
+    L = len(head.hidden)
+    K = head.buckets
+    lay = range(1, L + 1)
+    w = {}
+    w["head_gate"] = (0.0, sum(B * n[l - 1] * 2 + B * 4 for l in lay) / L, 0.0)
+    w["head_fwd_gemm"] = (sum(2.0 * B * n[l] * n[l - 1] for l in lay) / L,
+                          sum(B * n[l - 1] * 2 + n[l] * n[l - 1] * 2 + B * n[l] * 2 + n[l] * 2 for l in lay) / L, 0.0)
+    w["head_out"] = (0.0, B * n[L] * 2 + B * K * 4 + 3 * B * 4, 0.0)
+    w["head_loss"] = (0.0, 4 * B * 4, 0.0)
+    w["head_out_bwd"] = (0.0, 2 * B * n[L] * 2 + 2 * B * K * 4 + 5 * B * 4, 0.0)
+    w["head_gw_gemm"] = (sum(2.0 * n[l] * n[l - 1] * B for l in lay) / L,
+                         sum(B * n[l] * 2 + B * n[l - 1] * 2 + n[l] * n[l - 1] * 4 for l in lay) / L, 0.0)
+    # G_l W_l: G and W in, the layer below's activations in (l > 1), its G (or grad_x) out
+    w["head_gx_gemm"] = (sum(2.0 * B * n[l - 1] * n[l] for l in lay) / L,
+                         sum(B * n[l] * 2 + n[l] * n[l - 1] * 2 + (B * n[l - 1] * 2 if l > 1 else 0)
+                             + B * n[l - 1] * 2 for l in lay) / L, 0.0)
+    w["head_gate_bwd"] = (0.0, B * 4 * 3, 0.0)
+    col = (B * n[L] * 2 + B * 4) + B * 4 + B * K * 4 + B * 4 + sum(B * n[l] * 2 + B * n[l - 1] * 2 + 2 * B * 4
+                                                                  for l in lay)
+    w["head_colsum"] = (0.0, col / (4 + 3 * L), 0.0)
+    return w
+
+
 def _radix_passes(maxkey: int) -> int:
     bits = max(1, int(maxkey).bit_length())
     return -(-bits // 10)
@@ -154,20 +184,23 @@ def measured_traffic(kernel: str, workload: str):
     return None
 
 
-def cpu_baseline(wl, target_s: float) -> dict:
-    """The oracle (plain single-threaded C) timed on a sub-batch sized to about
-    `target_s` seconds: one step = gather + forward + backward (which recomputes
-    its forward) + embedding backward."""
+def cpu_baseline(wl, target_s: float, head=None) -> dict:
+    """The oracle timed on a sub-batch sized to about `target_s` seconds, single-threaded
+    (the C oracle is; numpy's BLAS is held to one thread): one step = gather + forward
+    + backward (which recomputes its forward) + embedding backward, and with a head its
+    forward and backward (numpy float64) between the cross stack's."""
+    from threadpoolctl import threadpool_limits
     probe = 8
-    t = _oracle_step(wl, probe)
-    rows = int(max(16, min(wl.batch, round(probe * target_s / max(t, 1e-6)))))
-    dt = _oracle_step(wl, rows)
+    with threadpool_limits(limits=1):
+        t = _oracle_step(wl, probe, head)
+        rows = int(max(16, min(wl.batch, round(probe * target_s / max(t, 1e-6)))))
+        dt = _oracle_step(wl, rows, head)
     return {"value": rows / dt, "unit": "samples/s", "cores": 1, "kind": "oracle",
-            "sample": "%d samples of the %s workload (gather + forward + backward + embedding backward), "
-                      "%.1f s, single-threaded" % (rows, wl.name, dt)}
+            "sample": "%d samples of the %s workload (gather + forward + backward + embedding backward%s), "
+                      "%.1f s, single-threaded" % (rows, wl.name, " + head" if head is not None else "", dt)}
 
 
-def _oracle_step(wl, rows: int) -> float:
+def _oracle_step(wl, rows: int, head=None) -> float:
     import oracle
     from paper_2402_06859_amd.synth import make_inputs
     inp = make_inputs(wl, batch=rows, bias_std=0.0)
@@ -175,6 +208,17 @@ def _oracle_step(wl, rows: int) -> float:
     U = [x.float().numpy() for x in inp["u"]]
     b = [x.float().numpy() for x in inp["bias"]]
     F, D, Nd, m, bf16 = wl.num_cat, wl.emb_dim, wl.num_dense, wl.table_rows, wl.dtype == "bf16"
+    if head is not None:
+        from paper_2402_06859_amd.synth import make_head_inputs
+        hinp = make_head_inputs(wl, head, batch=rows, with_x=False)
+        f64 = lambda t: t.float().numpy().astype("float64")
+        hp = {"W": [f64(w) for w in hinp["W"]], "b": [f64(v) for v in hinp["b"]], "w_out": f64(hinp["w_out"]),
+              "b_out": float(hinp["b_out"].float()[0]), "cal_w": f64(hinp["cal_w"]), "cal_b": 0.0,
+              "lo": head.lo, "step": head.step, "e": f64(hinp["e"])}
+        if head.gated:
+            hp["G"] = [f64(g) for g in hinp["G"]]
+            hp["c"] = [float(c.float()[0]) for c in hinp["c"]]
+        labels = f64(hinp["labels"])
     t0 = time.perf_counter()
     if wl.hashed:
         x0 = oracle.gather_hashed(rows, F, D, Nd, m, m, wl.combine, bf16, wl.hash_seed, inp["ids"], inp["offsets"],
@@ -182,8 +226,15 @@ def _oracle_step(wl, rows: int) -> float:
     else:
         x0, _ = oracle.gather(rows, F, D, Nd, wl.vocab, m, m, wl.combine, bf16, inp["ids"], inp["offsets"],
                               inp["q_tables"], inp["r_tables"], inp["dense"])
-    oracle.forward(x0, W, U, b, wl.alpha, wl.beta, wl.temperature, parallel=wl.parallel)
-    gx0 = oracle.backward(x0, W, U, b, inp["grad_out"], wl.alpha, wl.beta, wl.temperature, parallel=wl.parallel)[0]
+    xL = oracle.forward(x0, W, U, b, wl.alpha, wl.beta, wl.temperature, parallel=wl.parallel)
+    g_out = inp["grad_out"]
+    if head is not None:
+        from oracle import head as OH
+        p = hp
+        f = OH.head_forward(xL, p)
+        _, g_cal = OH.logloss(f["y_cal"], labels)
+        g_out = OH.head_backward(xL, p, g_cal / rows)["x"]
+    gx0 = oracle.backward(x0, W, U, b, g_out, wl.alpha, wl.beta, wl.temperature, parallel=wl.parallel)[0]
     if wl.hashed:
         oracle.embed_backward_hashed(rows, F, D, Nd, m, m, wl.combine, wl.hash_seed, inp["ids"], inp["offsets"],
                                      inp["q_tables"], inp["r_tables"], gx0)
@@ -234,6 +285,10 @@ def main():
                     help="Murmur-hashed front-end: raw ids hashed, two QR table pairs of 2^16 + 2^16 rows per feature")
     ap.add_argument("--parallel-branch", action="store_true",
                     help="plain and attention low-rank cross nets with their own weights in every layer")
+    ap.add_argument("--head", default=None, metavar="NAME",
+                    help="train a Feed-style tower: the cross stack's output goes through a head (lmlp: gated "
+                         "4 x 3500 ReLU layers, logit, isotonic calibration, log loss) whose input gradient "
+                         "drives the cross-stack backward")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device-to-device a few times (known traffic, to scale HBM counters)")
     args = ap.parse_args()
@@ -255,8 +310,8 @@ def main():
 
     import torch
     from paper_2402_06859_amd import rdcn
-    from paper_2402_06859_amd.step import DeviceBatch
-    from paper_2402_06859_amd.synth import WORKLOADS, make_inputs
+    from paper_2402_06859_amd.step import DeviceBatch, DeviceHead
+    from paper_2402_06859_amd.synth import HEADS, WORKLOADS, make_head_inputs, make_inputs
 
     wl = WORKLOADS[args.workload]
     if args.parallel_branch:
@@ -270,17 +325,25 @@ def main():
     inp = make_inputs(wl, id_mode=args.id_mode)
     db = DeviceBatch(wl, inp)
     B = db.B
+    head = HEADS[args.head] if args.head else None
+    if head is not None:
+        dh = DeviceHead(db.lib, head, make_head_inputs(wl, head, with_x=False), B)
+        step = lambda: dh.tower_step(db)
+    else:
+        step = db.step
     for _ in range(args.warmup):
-        db.step()
+        step()
     torch.cuda.synchronize()
     if db.lib.check_device_errors() != rdcn.RDCN_OK:
         raise RuntimeError("device error flag raised during warm-up")
 
     # find the kernel with the largest share of a step (all launch sites timed, untimed step)
     db.lib.profile_start(4096)
-    db.step()
+    step()
     prof = db.lib.profile_stop()
     work = kernel_work(wl, B)
+    if head is not None:
+        work.update(head_work(wl, head, B))
     dominant = max((k for k in prof if k in work), key=lambda k: prof[k][0])
 
     # timed region: only the dominant kernel's launches carry events
@@ -291,7 +354,7 @@ def main():
     w0 = time.perf_counter()
     e0.record(stream)
     for _ in range(args.steps):
-        db.step()
+        step()
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
@@ -334,7 +397,11 @@ def main():
                                   wl.num_dense, wl.d, wl.num_layers, wl.rank, "on" if wl.attention else "off",
                                   ", parallel plain branch" if wl.parallel else "")
                                + (", Murmur-hashed ids (two QR pairs of 2^16 x 2^16 rows per feature)"
-                                  if wl.hashed else ""),
+                                  if wl.hashed else "")
+                               + ("; head: %s%d x %s ReLU layers, logit, isotonic calibration (%d buckets), log loss"
+                                  % ("gated " if head.gated else "", len(head.hidden),
+                                     "/".join(str(v) for v in sorted(set(head.hidden))), head.buckets)
+                                  if head is not None else ""),
                    "global_batch": B, "id_mode": args.id_mode},
         "roofline": roof,
         "gemm_mfma_frac": (gemm_flops / gemm_s / 1e12 / PEAK_BF16_TFLOPS) if gemm_s > 0 else None,
@@ -344,7 +411,7 @@ def main():
     if wl.num_cat > 0:
         out["gather_q8"] = time_gather_q8(db, work["gather_q8"][1], work["gather"][1])
     if args.cpu_seconds > 0:
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, head)
     print(json.dumps(out), flush=True)
 
 

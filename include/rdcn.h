@@ -348,7 +348,7 @@ typedef struct rdcn_head_weights {
 /*
  * Attach a head to the handle (replacing any earlier one); its input width is
  * the handle's d. RDCN_ERR_ARG for values out of range, RDCN_ERR_UNSUPPORTED
- * for a float model or a batch_max above 8388480.
+ * for a float model or a batch_max above 4194240.
  */
 rdcn_status rdcn_head_configure(rdcn_handle* h, const rdcn_head_config* cfg);
 

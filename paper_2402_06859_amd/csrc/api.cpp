@@ -702,7 +702,7 @@ rdcn_status rdcn_head_configure(rdcn_handle* h, const rdcn_head_config* cfg) {
     for (int l = 0; l < c.num_hidden; ++l)
         if (c.hidden[l] <= 0 || c.hidden[l] % 8) return RDCN_ERR_ARG;
     if (!h->bf16) return RDCN_ERR_UNSUPPORTED;
-    if (h->cfg.batch_max > (int64_t)65535 * 128) return RDCN_ERR_UNSUPPORTED;  // column-sum chunks per launch
+    if (h->cfg.batch_max > (int64_t)65535 * 64) return RDCN_ERR_UNSUPPORTED;  // column-sum chunks per launch
     h->head = c;
     for (int l = c.num_hidden; l < RDCN_HEAD_MAX_HIDDEN; ++l) h->head.hidden[l] = 0;
     h->head_on = true;

@@ -165,38 +165,50 @@ __global__ __launch_bounds__(256) void k_gate_finalize(int64_t B, int ntiles, co
                                                        const float* __restrict__ s, float* __restrict__ gs) {
     for (int64_t m = (int64_t)blockIdx.x * 256 + threadIdx.x; m < B; m += (int64_t)gridDim.x * 256) {
         float acc = 0.f;
+#pragma unroll 8
         for (int t = 0; t < ntiles; ++t) acc += part[(int64_t)t * B + m];
         gs[m] = (1.f - sigmoid_f(s[m])) * acc;
     }
 }
 
-constexpr int COLSUM_ROWS = 128;  // rows per chunk
+constexpr int COLSUM_ROWS = 64;  // rows per chunk (16 per wave)
 
-// part[chunk, j] = sum over the chunk's rows (in order) of X[b, j] * wgt[b]; VEC consecutive
-// columns per thread (VEC = 8: 16-byte loads), one 64-lane wave per block.
+// part[chunk, j] = sum over the chunk's rows of X[b, j] * wgt[b]. A block of four
+// waves covers 64 * VEC columns (VEC = 8: 16-byte loads); wave w takes rows
+// w, w + 4, ... of the chunk, and the four wave sums are added in wave order.
 template <typename T, int VEC>
-__global__ __launch_bounds__(64) void k_colsum_w(int64_t B, int64_t n, const T* __restrict__ X, int64_t ldx,
-                                                 const float* __restrict__ wgt, float* __restrict__ part) {
-    const int64_t j = ((int64_t)blockIdx.x * 64 + threadIdx.x) * VEC;
-    if (j >= n) return;
+__global__ __launch_bounds__(256) void k_colsum_w(int64_t B, int64_t n, const T* __restrict__ X, int64_t ldx,
+                                                  const float* __restrict__ wgt, float* __restrict__ part) {
+    __shared__ float red[4][64 * VEC];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t j = ((int64_t)blockIdx.x * 64 + lane) * VEC;
     const int64_t b0 = (int64_t)blockIdx.y * COLSUM_ROWS;
     const int64_t b1 = b0 + COLSUM_ROWS < B ? b0 + COLSUM_ROWS : B;
     float acc[VEC];
 #pragma unroll
     for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
-    for (int64_t b = b0; b < b1; ++b) {
-        const float wv = wgt ? wgt[b] : 1.f;
-        float v[VEC];
-        if constexpr (VEC == 8) {
-            ld8(X + b * ldx + j, v);
-        } else {
-            v[0] = st<T>::load(X + b * ldx + j);
-        }
+    if (j < n) {
+        for (int64_t b = b0 + wave; b < b1; b += 4) {
+            const float wv = wgt ? wgt[b] : 1.f;
+            float v[VEC];
+            if constexpr (VEC == 8) {
+                ld8(X + b * ldx + j, v);
+            } else {
+                v[0] = st<T>::load(X + b * ldx + j);
+            }
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[e] = fmaf(v[e], wv, acc[e]);
+            for (int e = 0; e < VEC; ++e) acc[e] = fmaf(v[e], wv, acc[e]);
+        }
     }
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) part[(int64_t)blockIdx.y * n + j + e] = acc[e];
+    for (int e = 0; e < VEC; ++e) red[wave][lane * VEC + e] = acc[e];
+    __syncthreads();
+    if (wave == 0 && j < n) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            part[(int64_t)blockIdx.y * n + j + e] =
+                ((red[0][lane * VEC + e] + red[1][lane * VEC + e]) + red[2][lane * VEC + e]) + red[3][lane * VEC + e];
+    }
 }
 
 // out[j] = sum over chunks of part[chunk, j]: four slices of the chunks summed in
@@ -274,11 +286,11 @@ hipError_t launch_colsum_w(int64_t B, int64_t n, const void* X, int64_t ldx, boo
     const int64_t cols_per_block = 64 * (vec ? 8 : 1);
     const dim3 grid((unsigned)((n + cols_per_block - 1) / cols_per_block), (unsigned)nch);
     if (x_bf16) {
-        if (vec) hipLaunchKernelGGL((k_colsum_w<bf16_t, 8>), grid, dim3(64), 0, st, B, n, (const bf16_t*)X, ldx, wgt, part);
-        else hipLaunchKernelGGL((k_colsum_w<bf16_t, 1>), grid, dim3(64), 0, st, B, n, (const bf16_t*)X, ldx, wgt, part);
+        if (vec) hipLaunchKernelGGL((k_colsum_w<bf16_t, 8>), grid, dim3(256), 0, st, B, n, (const bf16_t*)X, ldx, wgt, part);
+        else hipLaunchKernelGGL((k_colsum_w<bf16_t, 1>), grid, dim3(256), 0, st, B, n, (const bf16_t*)X, ldx, wgt, part);
     } else {
-        if (vec) hipLaunchKernelGGL((k_colsum_w<float, 8>), grid, dim3(64), 0, st, B, n, (const float*)X, ldx, wgt, part);
-        else hipLaunchKernelGGL((k_colsum_w<float, 1>), grid, dim3(64), 0, st, B, n, (const float*)X, ldx, wgt, part);
+        if (vec) hipLaunchKernelGGL((k_colsum_w<float, 8>), grid, dim3(256), 0, st, B, n, (const float*)X, ldx, wgt, part);
+        else hipLaunchKernelGGL((k_colsum_w<float, 1>), grid, dim3(256), 0, st, B, n, (const float*)X, ldx, wgt, part);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
