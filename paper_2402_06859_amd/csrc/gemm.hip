@@ -11,14 +11,18 @@
 //            gU    = gt^T h         both K-strided (split-K over the batch)
 //            gW    = gP^T x_l       both K-strided (split-K over the batch)
 //
-// Tiling: 256 threads = 4 waves in a 2 x 2 grid; a wave owns a (BM/2) x (BN/2)
-// block of 16 x 16 MFMA tiles (v_mfma_f32_16x16x32_bf16). Each K step of 64 is
-// one stage of a 3-stage ring in LDS, filled by direct global-to-LDS loads two
-// steps ahead of the multiply; K-strided operands stay [k][m] in LDS and are
+// Tiling: 64 x 64 and 128 x 128 blocks use 256 threads = 4 waves in a 2 x 2 grid,
+// each wave owning a (BM/2) x (BN/2) block of 16 x 16 MFMA tiles
+// (v_mfma_f32_16x16x32_bf16); large products use 256 x 256 or 256 x 128 blocks of
+// 8 waves with 32 x 32 tiles (v_mfma_f32_32x32x16_bf16). Each K step of 64 is one
+// stage of a 2- or 3-stage ring in LDS, filled by direct global-to-LDS loads one or
+// two steps ahead of the multiply; K-strided operands stay [k][m] in LDS and are
 // transposed on the way out by ds_read_b64_tr_b16, so no operand is ever
 // transposed in memory. The MFMA is issued with B as its first operand, so each
 // lane ends up with four consecutive output columns of one row: epilogue loads
 // and stores are 8- or 16-byte vectors along the rows of x0, x_l, t and g.
+#include <type_traits>
+
 #include "device_common.h"
 #include "gemm.h"
 #include "mlp_common.h"
@@ -293,15 +297,17 @@ __device__ __forceinline__ uint32_t lds_addr(const bf16_t* p) { return (uint32_t
 
 template <int ROWS>
 __device__ __forceinline__ int kstr_swz(int k) {
-    // ROWS = 128: 8 slots of 32 B per k-row; ROWS = 64: 4 slots, two k-rows per 256 B window
-    return ROWS == 128 ? (((k & 3) << 1) | ((k >> 3) & 1)) : ((((k >> 1) & 1) << 1) | ((k >> 3) & 1));
+    // ROWS = 128: 8 slots of 32 B per k-row; ROWS = 256: 16 slots, two 256 B windows per
+    // k-row (the XOR spreads the k-rows of one read over all 8 slot positions of a window);
+    // ROWS = 64: 4 slots, two k-rows per 256 B window
+    return ROWS >= 128 ? (((k & 3) << 1) | ((k >> 3) & 1)) : ((((k >> 1) & 1) << 1) | ((k >> 3) & 1));
 }
 
-// Issue this thread's direct-to-LDS loads of one stage for one operand.
-template <int ROWS, bool KS>
+// Issue this thread's direct-to-LDS loads of one stage for one operand (NW waves).
+template <int ROWS, bool KS, int NW>
 __device__ __forceinline__ void stage_load(const bf16_t* __restrict__ base, int64_t ld, int64_t rows, int64_t row0,
                                            int64_t k0, int64_t kend, bf16_t* lds, int wave, int lane) {
-    constexpr int NI = ROWS / 32;  // wave-instructions per thread (ROWS * 8 chunks / 64 lanes / 4 waves)
+    constexpr int NI = ROWS / (8 * NW);  // wave-instructions per thread (ROWS * 8 chunks / 64 lanes / NW waves)
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
         const int blk = wave * NI + j;  // 1 KiB block index within the stage
@@ -315,7 +321,7 @@ __device__ __forceinline__ void stage_load(const bf16_t* __restrict__ base, int6
             if (gk >= kend) gk = kend - 8;
             dma16(base + gr * ld + gk, lds_addr(lds) + (uint32_t)__builtin_amdgcn_readfirstlane(blk) * 1024u);
         } else {
-            constexpr int RPB = ROWS == 128 ? 4 : 8;  // k-rows per 1 KiB block
+            constexpr int RPB = ROWS == 256 ? 2 : (ROWS == 128 ? 4 : 8);  // k-rows per 1 KiB block
             constexpr int QPR = 64 / RPB;             // 16-byte pieces per k-row
             const int kr = blk * RPB + lane / QPR;
             const int q = lane % QPR;
@@ -329,18 +335,18 @@ __device__ __forceinline__ void stage_load(const bf16_t* __restrict__ base, int6
     }
 }
 
-// Zero the k positions >= kvalid of one stage (tail tile of a K range).
-template <int ROWS, bool KS>
+// Zero the k positions >= kvalid of one stage (tail tile of a K range); NT threads.
+template <int ROWS, bool KS, int NT>
 __device__ __forceinline__ void stage_zero_tail(bf16_t* lds, int kvalid, int tid) {
     if (!KS) {
         const int nch = 8 - kvalid / 8;  // chunks per row to clear
-        for (int e = tid; e < ROWS * nch; e += 256) {
+        for (int e = tid; e < ROWS * nch; e += NT) {
             const int r = e / nch, kc = kvalid / 8 + e % nch;
             *(u32x4_t*)(lds + r * 64 + ((kc ^ ((r >> 1) & 7)) * 8)) = u32x4_t{0, 0, 0, 0};
         }
     } else {
         const int n = (64 - kvalid) * ROWS / 8;  // 16-byte pieces in the k-rows to clear
-        for (int e = tid; e < n; e += 256)
+        for (int e = tid; e < n; e += NT)
             *(u32x4_t*)(lds + kvalid * ROWS + e * 8) = u32x4_t{0, 0, 0, 0};
     }
 }
@@ -372,6 +378,39 @@ __device__ __forceinline__ bf16x8_t load_frag(const bf16_t* lds, int rt, int ks,
     }
 }
 
+// MFMA fragment (32 rows x 16 k) for v_mfma_f32_32x32x16_bf16: lane l holds row
+// rt + l % 32 and the 8 k values ks + 8 (l / 32) .. + 7. K-strided operands use the
+// same transposing reads as above, each 16-lane group G supplying row chunk
+// rt / 16 + (G & 1) and k rows from ks + 8 (G >> 1).
+template <int ROWS, bool KS>
+__device__ __forceinline__ bf16x8_t load_frag32(const bf16_t* lds, int rt, int ks, int lane) {
+    if (!KS) {
+        const int r = rt + (lane & 31);
+        const int kc = ks / 8 + (lane >> 5);
+        return __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(lds + r * 64 + ((kc ^ ((r >> 1) & 7)) * 8)));
+    } else {
+        const int i = lane & 15, G = lane >> 4;
+        const int c = rt / 16 + (G & 1);
+        const int kb = ks + 8 * (G >> 1);
+        s16x4_t lo, hi;
+        {
+            const int kr = kb + (i >> 2);
+            const int off = kr * ROWS + ((c ^ kstr_swz<ROWS>(kr)) * 16) + (i & 3) * 4;
+            lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4_t*)(lds + off));
+        }
+        {
+            const int kr = kb + 4 + (i >> 2);
+            const int off = kr * ROWS + ((c ^ kstr_swz<ROWS>(kr)) * 16) + (i & 3) * 4;
+            hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4_t*)(lds + off));
+        }
+        typedef short s16x8_t __attribute__((ext_vector_type(8)));
+        const s16x8_t v = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        return __builtin_bit_cast(bf16x8_t, v);
+    }
+}
+
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
 __device__ __forceinline__ void wait_vmcnt(int n) {
     // s_waitcnt with vmcnt = n (n <= 63), expcnt and lgkmcnt left at their maxima
     switch (n) {
@@ -391,11 +430,17 @@ __device__ __forceinline__ void wait_lgkm0() {
     __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (0 << 8));
 }
 
-template <int BM, int BN, bool AKS, bool BKS, int ST>
+// Block tile BM x BN over WM x WN waves; each wave owns a (BM/WM) x (BN/WN) block of
+// MFMA tiles: 16 x 16 (v_mfma_f32_16x16x32_bf16) or, with M32, 32 x 32
+// (v_mfma_f32_32x32x16_bf16, twice the flops per clock).
+template <int BM, int BN, bool AKS, bool BKS, int ST, int WM, int WN, bool M32>
 struct Pipe {
-    static constexpr int TM = BM / 32, TN = BN / 32;  // 16x16 MFMA tiles per wave
-    static constexpr int LOADS = BM / 32 + BN / 32;   // load instructions per thread per stage
+    static constexpr int NW = WM * WN, THREADS = 64 * NW;
+    static constexpr int MT = M32 ? 32 : 16;
+    static constexpr int TM = BM / WM / MT, TN = BN / WN / MT;  // MFMA tiles per wave
+    static constexpr int LOADS = (BM + BN) / (8 * NW);          // load instructions per thread per stage
     static constexpr int STAGE_ELEMS = (BM + BN) * BK;
+    using acc_t = typename std::conditional<M32, f32x16_t, f32x4_t>::type;
 
     struct Ctx {
         const GemmArgs* g;
@@ -412,47 +457,65 @@ struct Pipe {
         const int plane = t >= c.nk;
         const int64_t k0 = c.kbeg + (int64_t)(t - plane * c.nk) * BK;
         const bf16_t* a = (const bf16_t*)(plane ? c.g->a2 : c.g->a);
-        stage_load<BM, AKS>(a, c.g->lda, c.g->M, c.m0, k0, c.kend, buf, wave, lane);
-        stage_load<BN, BKS>((const bf16_t*)c.g->b, c.g->ldb, c.g->N, c.n0, k0, c.kend, buf + BM * BK, wave, lane);
+        stage_load<BM, AKS, NW>(a, c.g->lda, c.g->M, c.m0, k0, c.kend, buf, wave, lane);
+        stage_load<BN, BKS, NW>((const bf16_t*)c.g->b, c.g->ldb, c.g->N, c.n0, k0, c.kend, buf + BM * BK, wave, lane);
     }
 
     // One step on tile kt held in `cur`; prefetch tile kt + ST - 1 into `nxt`.
     // Every step issues the same number of loads (past the last tile they re-read
     // it), so "all but the newest ST - 2 stages" is a fixed count on every path.
     __device__ __forceinline__ static void step(const Ctx& c, bf16_t* cur, bf16_t* nxt, int kt,
-                                                f32x4_t (&acc)[TM][TN]) {
-        const int lane = c.tid & 63, wave = c.tid >> 6, wm = wave >> 1, wn = wave & 1;
+                                                acc_t (&acc)[TM][TN]) {
+        const int lane = c.tid & 63, wave = c.tid >> 6, wm = wave / WN, wn = wave % WN;
         wait_vmcnt(LOADS * (ST - 2));
         __builtin_amdgcn_s_barrier();
         issue(c, kt + ST - 1, nxt);
         const int kk = kt >= c.nk ? kt - c.nk : kt;
         const int64_t kv = c.kend - (c.kbeg + (int64_t)kk * BK);
         if (kv < BK) {  // tail tile: clear k positions past the range
-            stage_zero_tail<BM, AKS>(cur, (int)kv, c.tid);
-            stage_zero_tail<BN, BKS>(cur + BM * BK, (int)kv, c.tid);
+            stage_zero_tail<BM, AKS, THREADS>(cur, (int)kv, c.tid);
+            stage_zero_tail<BN, BKS, THREADS>(cur + BM * BK, (int)kv, c.tid);
             wait_lgkm0();
             __builtin_amdgcn_s_barrier();
         }
+        if constexpr (M32) {
 #pragma unroll
-        for (int ks = 0; ks < BK; ks += 32) {
-            bf16x8_t af[TM], bfr[TN];
+            for (int ks = 0; ks < BK; ks += 16) {
+                bf16x8_t af[TM], bfr[TN];
 #pragma unroll
-            for (int i = 0; i < TM; ++i) af[i] = load_frag<BM, AKS>(cur, wm * (BM / 2) + i * 16, ks, lane);
-#pragma unroll
-            for (int j = 0; j < TN; ++j) bfr[j] = load_frag<BN, BKS>(cur + BM * BK, wn * (BN / 2) + j * 16, ks, lane);
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
+                for (int i = 0; i < TM; ++i) af[i] = load_frag32<BM, AKS>(cur, wm * (BM / WM) + i * 32, ks, lane);
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+                    bfr[j] = load_frag32<BN, BKS>(cur + BM * BK, wn * (BN / WN) + j * 32, ks, lane);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+            }
+        } else {
+#pragma unroll
+            for (int ks = 0; ks < BK; ks += 32) {
+                bf16x8_t af[TM], bfr[TN];
+#pragma unroll
+                for (int i = 0; i < TM; ++i) af[i] = load_frag<BM, AKS>(cur, wm * (BM / WM) + i * 16, ks, lane);
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    bfr[j] = load_frag<BN, BKS>(cur + BM * BK, wn * (BN / WN) + j * 16, ks, lane);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+            }
         }
     }
 };
 
 // C = A B^T with an ST-stage direct-to-LDS pipeline (see layouts above).
-template <int BM, int BN, bool AKS, bool BKS, int ST, typename T, bool MLP>
-__global__ __launch_bounds__(256, ST == 2 ? 2 : 1) void k_gemm_mfma(GemmArgs g) {
-    using P = Pipe<BM, BN, AKS, BKS, ST>;
+template <int BM, int BN, bool AKS, bool BKS, int ST, int WM, int WN, bool M32, typename T, bool MLP>
+__global__ __launch_bounds__(64 * WM * WN, (ST == 2 && WM * WN == 4) ? 2 : 1) void k_gemm_mfma(GemmArgs g) {
+    using P = Pipe<BM, BN, AKS, BKS, ST, WM, WN, M32>;
     // one buffer: the stage ring during the K loop, the C staging area afterwards
     __shared__ __attribute__((aligned(1024))) bf16_t smem[ST * P::STAGE_ELEMS];
     bf16_t* lds0 = smem;
@@ -460,7 +523,7 @@ __global__ __launch_bounds__(256, ST == 2 ? 2 : 1) void k_gemm_mfma(GemmArgs g) 
     bf16_t* lds2 = smem + (ST == 3 ? 2 : 0) * P::STAGE_ELEMS;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WN, wn = wave % WN;
     const int tiles_n = (int)((g.N + BN - 1) / BN);
     const int ntiles = (int)(((g.M + BM - 1) / BM) * tiles_n);
     const int t = xcd_remap(blockIdx.x, ntiles);
@@ -477,11 +540,13 @@ __global__ __launch_bounds__(256, ST == 2 ? 2 : 1) void k_gemm_mfma(GemmArgs g) 
     c.nk = c.kbeg < c.kend ? (int)((c.kend - c.kbeg + BK - 1) / BK) : 0;
     c.ntot = c.nk * (g.a2 ? 2 : 1);
 
-    f32x4_t acc[P::TM][P::TN];
+    typename P::acc_t acc[P::TM][P::TN];
 #pragma unroll
     for (int i = 0; i < P::TM; ++i)
 #pragma unroll
-        for (int j = 0; j < P::TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < P::TN; ++j)
+#pragma unroll
+            for (int e = 0; e < (M32 ? 16 : 4); ++e) acc[i][j][e] = 0.f;
 
     if (c.ntot > 0) {
         P::issue(c, 0, lds0);
@@ -514,16 +579,31 @@ __global__ __launch_bounds__(256, ST == 2 ? 2 : 1) void k_gemm_mfma(GemmArgs g) 
 #pragma unroll
     for (int h = 0; h < BM / CH; ++h) {
         __syncthreads();
+        if constexpr (M32) {
+            // lane holds C[m = tile_m + lane % 32][n = tile_n + 8 q + 4 (lane / 32) + e] in acc[4 q + e]
 #pragma unroll
-        for (int i = 0; i < P::TM; ++i) {
-            const int row = wm * (BM / 2) + i * 16 + (lane & 15) - h * CH;
-            if (row < 0 || row >= CH) continue;
+            for (int i = 0; i < P::TM; ++i) {
+                const int row = wm * (BM / WM) + i * 32 + (lane & 31) - h * CH;
+                if (row < 0 || row >= CH) continue;
 #pragma unroll
-            for (int j = 0; j < P::TN; ++j)
-                *(f32x4_t*)(cs + row * CP + wn * (BN / 2) + j * 16 + 4 * (lane >> 4)) = acc[i][j];
+                for (int j = 0; j < P::TN; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        *(f32x4_t*)(cs + row * CP + wn * (BN / WN) + j * 32 + 8 * q + 4 * (lane >> 5)) =
+                            f32x4_t{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < P::TM; ++i) {
+                const int row = wm * (BM / WM) + i * 16 + (lane & 15) - h * CH;
+                if (row < 0 || row >= CH) continue;
+#pragma unroll
+                for (int j = 0; j < P::TN; ++j)
+                    *(f32x4_t*)(cs + row * CP + wn * (BN / WN) + j * 16 + 4 * (lane >> 4)) = acc[i][j];
+            }
         }
         __syncthreads();
-        for (int q = tid; q < CH * (BN / 8); q += 256) {
+        for (int q = tid; q < CH * (BN / 8); q += P::THREADS) {
             const int row = q / (BN / 8), col = (q % (BN / 8)) * 8;
             const int64_t m = c.m0 + h * CH + row, n = c.n0 + col;
             if (!MLP) {
@@ -612,12 +692,12 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float* part, int sp
     }
 }
 
-template <int BM, int BN, int ST, typename T>
+template <int BM, int BN, int ST, int WM, int WN, bool M32, typename T>
 hipError_t launch_tile(const GemmArgs& g, int splits, hipStream_t s) {
     const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
     dim3 grid((unsigned)tiles, 1, (unsigned)splits);
 #define RDCN_GEMM(AK, BKS, MLP) \
-    hipLaunchKernelGGL((k_gemm_mfma<BM, BN, AK, BKS, ST, T, MLP>), grid, dim3(256), 0, s, g)
+    hipLaunchKernelGGL((k_gemm_mfma<BM, BN, AK, BKS, ST, WM, WN, M32, T, MLP>), grid, dim3(64 * WM * WN), 0, s, g)
     if (g.epi == EPI_MLP_FWD || g.epi == EPI_MLP_BWD) {
         // MLP layers: forward (both K-contiguous) and input gradient (B K-strided), no split-K
         if (g.a_kstrided || splits != 1) return hipErrorInvalidValue;
@@ -658,6 +738,22 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool bf16, bool allow_split)
     // overlaps one tile's loads and epilogue with the other's multiplies; this beats
     // a third stage (one workgroup per CU) at every K measured.
     p.stages = p.bm == 128 ? 2 : 3;
+    // Large products (bound by the MFMA rate rather than by L2 -> LDS loads): eight
+    // waves on 256-row blocks with 32 x 32 x 16 MFMAs, which halve the bytes loaded
+    // per flop; 256 x 256 blocks when they still cover the chip, else 256 x 128.
+    if (bf16 && (double)M * (double)N * (double)K >= 8.0e9) {
+        const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256), t128 = ((M + 255) / 256) * ((N + 127) / 128);
+        if (t256 >= 240) {
+            p.bm = p.bn = 256;
+            p.splits = 1;
+            p.stages = 2;
+        } else if (t128 >= 200) {
+            p.bm = 256;
+            p.bn = 128;
+            p.splits = 1;
+            p.stages = 3;
+        }
+    }
     return p;
 }
 
@@ -669,12 +765,16 @@ hipError_t launch_gemm(const GemmArgs& g, const GemmPlan& p, bool bf16, hipStrea
         hipLaunchKernelGGL(k_gemm_f32, dim3((unsigned)tiles, 1, (unsigned)p.splits), dim3(256), 0, s, g);
         return hipGetLastError();
     }
-    if (p.bm == 128) {
-        if (p.stages == 2) return launch_tile<128, 128, 2, bf16_t>(g, p.splits, s);
-        return launch_tile<128, 128, 3, bf16_t>(g, p.splits, s);
+    if (p.bm == 256) {
+        if (p.bn == 256) return launch_tile<256, 256, 2, 2, 4, true, bf16_t>(g, p.splits, s);
+        return launch_tile<256, 128, 3, 4, 2, true, bf16_t>(g, p.splits, s);
     }
-    if (p.stages == 2) return launch_tile<64, 64, 2, bf16_t>(g, p.splits, s);
-    return launch_tile<64, 64, 3, bf16_t>(g, p.splits, s);
+    if (p.bm == 128) {
+        if (p.stages == 2) return launch_tile<128, 128, 2, 2, 2, false, bf16_t>(g, p.splits, s);
+        return launch_tile<128, 128, 3, 2, 2, false, bf16_t>(g, p.splits, s);
+    }
+    if (p.stages == 2) return launch_tile<64, 64, 2, 2, 2, false, bf16_t>(g, p.splits, s);
+    return launch_tile<64, 64, 3, 2, 2, false, bf16_t>(g, p.splits, s);
 }
 
 hipError_t launch_splitk_reduce(const float* part, int splits, int64_t MN, float* out, hipStream_t s) {
