@@ -21,6 +21,7 @@
 // transposed in memory. The MFMA is issued with B as its first operand, so each
 // lane ends up with four consecutive output columns of one row: epilogue loads
 // and stores are 8- or 16-byte vectors along the rows of x0, x_l, t and g.
+#include <cmath>
 #include <type_traits>
 
 #include "device_common.h"
@@ -479,19 +480,30 @@ struct Pipe {
             __builtin_amdgcn_s_barrier();
         }
         if constexpr (M32) {
+            // fragments double-buffered: the reads of substep s + 1 are issued before the
+            // MFMAs of substep s, so LDS latency hides behind the matrix cores
+            bf16x8_t af[2][TM], bfr[2][TN];
+            auto frags = [&](int buf, int ks) {
 #pragma unroll
-            for (int ks = 0; ks < BK; ks += 16) {
-                bf16x8_t af[TM], bfr[TN];
-#pragma unroll
-                for (int i = 0; i < TM; ++i) af[i] = load_frag32<BM, AKS>(cur, wm * (BM / WM) + i * 32, ks, lane);
+                for (int i = 0; i < TM; ++i)
+                    af[buf][i] = load_frag32<BM, AKS>(cur, wm * (BM / WM) + i * 32, ks, lane);
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    bfr[j] = load_frag32<BN, BKS>(cur + BM * BK, wn * (BN / WN) + j * 32, ks, lane);
+                    bfr[buf][j] = load_frag32<BN, BKS>(cur + BM * BK, wn * (BN / WN) + j * 32, ks, lane);
+            };
+            frags(0, 0);
+#pragma unroll
+            for (int s = 0; s < BK / 16; ++s) {
+                if (s + 1 < BK / 16) frags((s + 1) & 1, (s + 1) * 16);
+                // keep the compiler from sinking those reads below the MFMAs
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
                     for (int j = 0; j < TN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+                        acc[i][j] =
+                            __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[s & 1][j], af[s & 1][i], acc[i][j], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
             }
         } else {
 #pragma unroll
@@ -514,7 +526,8 @@ struct Pipe {
 
 // C = A B^T with an ST-stage direct-to-LDS pipeline (see layouts above).
 template <int BM, int BN, bool AKS, bool BKS, int ST, int WM, int WN, bool M32, typename T, bool MLP>
-__global__ __launch_bounds__(64 * WM * WN, (ST == 2 && WM * WN == 4) ? 2 : 1) void k_gemm_mfma(GemmArgs g) {
+__global__ __launch_bounds__(64 * WM * WN, (ST == 2 && WM * WN == 4) ? 2 : 1)
+__attribute__((amdgpu_waves_per_eu(WM * WN == 8 ? 2 : 1, WM * WN == 8 ? 2 : 8))) void k_gemm_mfma(GemmArgs g) {
     using P = Pipe<BM, BN, AKS, BKS, ST, WM, WN, M32>;
     // one buffer: the stage ring during the K loop, the C staging area afterwards
     __shared__ __attribute__((aligned(1024))) bf16_t smem[ST * P::STAGE_ELEMS];
@@ -742,12 +755,21 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool bf16, bool allow_split)
     // waves on 256-row blocks with 32 x 32 x 16 MFMAs, which halve the bytes loaded
     // per flop; 256 x 256 blocks when they still cover the chip, else 256 x 128.
     if (bf16 && (double)M * (double)N * (double)K >= 8.0e9) {
-        const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256), t128 = ((M + 255) / 256) * ((N + 127) / 128);
-        if (t256 >= 240) {
+        // Per 64-deep K step a block needs max(MFMA time, load time): MFMA at ~3600
+        // flop/clk per CU, loads at the ~24 B/clk per CU that L2 -> LDS sustains here.
+        // A launch takes ceil(tiles / 256) rounds of that (one block per CU).
+        auto cost = [&](int bm, int bn) {
+            const double tiles = (double)((M + bm - 1) / bm) * (double)((N + bn - 1) / bn);
+            const double mfma = 2.0 * bm * bn * 64 / 3600.0, load = (bm + bn) * 64 * 2 / 24.0;
+            return std::ceil(tiles / 256.0) * (mfma > load ? mfma : load);
+        };
+        const double c256 = cost(256, 256), c128 = cost(256, 128);
+        const int64_t t128 = ((M + 255) / 256) * ((N + 127) / 128);
+        if (c256 <= c128) {
             p.bm = p.bn = 256;
             p.splits = 1;
             p.stages = 2;
-        } else if (t128 >= 200) {
+        } else if (t128 >= 128) {
             p.bm = 256;
             p.bn = 128;
             p.splits = 1;
