@@ -154,6 +154,10 @@ KERNEL_SOURCES = {
 }
 for _k in ("fwd_down_gemm", "fwd_up_gemm", "bwd_gu_gemm", "bwd_gh_gemm", "bwd_gw_gemm", "bwd_gx_gemm"):
     KERNEL_SOURCES[_k] = ["gemm.hip", "gemm.h", "device_common.h"]
+for _k in ("head_fwd_gemm", "head_gw_gemm", "head_gx_gemm"):
+    KERNEL_SOURCES[_k] = ["gemm.hip", "gemm.h", "device_common.h", "mlp_common.h"]
+for _k in ("head_gate", "head_out", "head_loss", "head_out_bwd", "head_gate_bwd", "head_colsum"):
+    KERNEL_SOURCES[_k] = ["head.hip", "head.h", "device_common.h", "mlp_common.h"]
 
 
 def sources_sha256(kernel: str) -> str:
@@ -368,7 +372,7 @@ def main():
     avg_s = dom[0] / dom[1] / 1e3
     roof = roofline_for(dominant, work[dominant], avg_s, wl.dtype == "bf16")
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = measured_traffic(dominant, wl.name)
+    roof["traffic"] = measured_traffic(dominant, wl.name + ("+" + head.name if head is not None else ""))
     roof["kernel"] = dominant
     roof["avg_us"] = avg_s * 1e6
     roof["launches"] = dom[1]
