@@ -239,7 +239,7 @@ HeadSaved head_saved_layout(const rdcn_handle* h, int64_t B) {
 }
 
 struct HeadScratch {
-    size_t G[2], gy, gs[2], rowpart, colpart, splitk, total;
+    size_t G[2], gy, gs, rowpart, colpart, splitk, total;  // gs: one [B] vector per layer
 };
 
 HeadScratch head_scratch_layout(const rdcn_handle* h, int64_t B) {
@@ -257,7 +257,7 @@ HeadScratch head_scratch_layout(const rdcn_handle* h, int64_t B) {
     size_t off = 0;
     for (int i = 0; i < 2; ++i) { s.G[i] = off; off += al((size_t)B * nmax * 2); }
     s.gy = off; off += al((size_t)B * 4);
-    for (int i = 0; i < 2; ++i) { s.gs[i] = off; off += al((size_t)B * 4); }
+    s.gs = off; off += (size_t)c.num_hidden * al((size_t)B * 4);
     s.rowpart = off; off += c.gated ? al((size_t)tiles * B * 4) : 0;
     s.colpart = off; off += al((size_t)colsum_chunks(B) * widest * 4);
     s.splitk = off; off += al((size_t)split * 4);
@@ -793,6 +793,13 @@ rdcn_status rdcn_head_backward(rdcn_handle* h, int64_t batch, const void* x, con
     char* sc = (char*)scratch;
     float* gy = (float*)(sc + W.gy);
     float* colpart = (float*)(sc + W.colpart);
+    auto gs_of = [&](int l) { return (float*)(sc + W.gs + (size_t)l * al((size_t)B * 4)); };
+    VecSums sums{};  // the scalar gradients, summed in one launch at the end
+    auto add_sum = [&](const float* x, void* out) {
+        sums.x[sums.n] = x;
+        sums.out[sums.n] = (float*)out;
+        ++sums.n;
+    };
     auto colsum = [&](int64_t n, const void* X, int64_t ldx, bool xbf16, const float* wgt, void* out) -> hipError_t {
         ProfScope ps(h, RDCN_KERNEL_HEAD_COLSUM, s);
         return launch_colsum_w(B, n, X, ldx, xbf16, wgt, colpart, (float*)out, s);
@@ -803,21 +810,21 @@ rdcn_status rdcn_head_backward(rdcn_handle* h, int64_t batch, const void* x, con
         ProfScope ps(h, RDCN_KERNEL_HEAD_OUT_BWD, s);
         RDCN_TRY(launch_head_out_bwd(B, c.hidden[L - 1], aL, c.gated && B > 0 ? (const float*)(sv + S.S[L - 1]) : nullptr,
                                      w->w_out, B > 0 ? (const float*)(sv + S.Y) : nullptr, cal_args(h, w, e_cal),
-                                     grad_ycal, grad_e, gy, sc + W.G[cur], (float*)(sc + W.gs[cur]), s));
+                                     grad_ycal, grad_e, gy, sc + W.G[cur], gs_of(L - 1), s));
     }
     RDCN_TRY(colsum(c.hidden[L - 1], aL, c.hidden[L - 1], true, gy, grads->w_out));
-    RDCN_TRY(colsum(1, gy, 1, false, nullptr, grads->b_out));
     RDCN_TRY(colsum(c.num_buckets, grad_e, c.num_buckets, false, nullptr, grads->cal_w));
-    RDCN_TRY(colsum(1, grad_ycal, 1, false, nullptr, grads->cal_b));
+    add_sum(gy, grads->b_out);
+    add_sum(grad_ycal, grads->cal_b);
     for (int l = L - 1; l >= 0; --l) {
         const int64_t nin = head_in(h, l), nout = c.hidden[l];
         const void* in = l == 0 ? x : (const void*)(sv + S.A[l - 1]);
         const void* G = sc + W.G[cur];
-        const float* gsl = (const float*)(sc + W.gs[cur]);
+        const float* gsl = gs_of(l);
         RDCN_TRY(colsum(nout, G, nout, true, nullptr, grads->b[l]));
         if (c.gated) {
             RDCN_TRY(colsum(nin, in, nin, true, gsl, grads->gate_w[l]));
-            RDCN_TRY(colsum(1, gsl, 1, false, nullptr, grads->gate_b[l]));
+            add_sum(gsl, grads->gate_b[l]);
         }
         {
             GemmArgs g{};
@@ -854,11 +861,12 @@ rdcn_status rdcn_head_backward(rdcn_handle* h, int64_t batch, const void* x, con
         if (l > 0 && c.gated) {
             ProfScope ps(h, RDCN_KERNEL_HEAD_GATE_BWD, s);
             RDCN_TRY(launch_gate_finalize(B, (int)gemm_tiles_n(nin, p), (const float*)(sc + W.rowpart),
-                                          (const float*)(sv + S.S[l - 1]), (float*)(sc + W.gs[1 - cur]), s));
+                                          (const float*)(sv + S.S[l - 1]), gs_of(l - 1), s));
         }
         cur = 1 - cur;
     }
-    return RDCN_OK;
+    ProfScope ps(h, RDCN_KERNEL_HEAD_COLSUM, s);
+    return hip_status(launch_vec_sums(B, sums, s));
 }
 
 rdcn_status rdcn_profile_start(rdcn_handle* h, int32_t max_launches, uint32_t kernel_mask) {

@@ -38,4 +38,14 @@ int64_t colsum_chunks(int64_t B);
 hipError_t launch_colsum_w(int64_t B, int64_t n, const void* X, int64_t ldx, bool x_bf16, const float* wgt,
                            float* part, float* out, hipStream_t st);
 
+// out_i = sum over b < B of x_i[b] (float vectors), for up to VEC_SUMS_MAX vectors in one
+// launch; each sum is taken in a fixed order (deterministic).
+constexpr int VEC_SUMS_MAX = 16;
+struct VecSums {
+    int n;
+    const float* x[VEC_SUMS_MAX];
+    float* out[VEC_SUMS_MAX];
+};
+hipError_t launch_vec_sums(int64_t B, const VecSums& v, hipStream_t st);
+
 }  // namespace rdcn

@@ -226,7 +226,31 @@ __global__ __launch_bounds__(256) void k_chunk_reduce(int64_t nchunks, int64_t n
     if (ty == 0 && j < n) out[j] = ((red[0][tx] + red[1][tx]) + red[2][tx]) + red[3][tx];
 }
 
+// One block per vector: 256 threads take rows t, t + 256, ...; the thread sums are
+// added in a fixed tree order.
+__global__ __launch_bounds__(256) void k_vec_sums(int64_t B, VecSums v) {
+    __shared__ float red[256];
+    const int i = blockIdx.x, t = threadIdx.x;
+    const float* x = v.x[i];
+    float acc = 0.f;
+    for (int64_t b = t; b < B; b += 256) acc += x[b];
+    red[t] = acc;
+    __syncthreads();
+    for (int o = 128; o >= 1; o >>= 1) {
+        if (t < o) red[t] += red[t + o];
+        __syncthreads();
+    }
+    if (t == 0) *v.out[i] = red[0];
+}
+
 }  // namespace
+
+hipError_t launch_vec_sums(int64_t B, const VecSums& v, hipStream_t st) {
+    if (v.n <= 0) return hipSuccess;
+    if (v.n > VEC_SUMS_MAX) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_vec_sums, dim3((unsigned)v.n), dim3(256), 0, st, B, v);
+    return hipGetLastError();
+}
 
 hipError_t launch_gate_logit(int64_t B, int n, const void* x, int64_t ldx, const void* g, const void* c, float* s,
                              hipStream_t st) {
