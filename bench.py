@@ -36,6 +36,8 @@ PEAK_HBM_GBS = 8000.0
 # Issue cost of one v_exp_f32 in FMA slots (measured on MI355X: an exp + add chain
 # runs at ~14.7 T/s against ~39 T FMA slots/s, i.e. about two slots per exp).
 EXP_SLOTS = 2.0
+# Measured v_exp_f32 throughput on MI355X (an exp + add chain over all CUs).
+EXP_PEAK_PER_S = 14.7e12
 
 
 def kernel_work(wl, B: int) -> dict:
@@ -186,6 +188,39 @@ def measured_traffic(kernel: str, workload: str):
                 if rec.get("kernel") == kernel and rec.get("workload") == workload and rec.get("sha256") == sha:
                     return float(rec["bytes_per_launch"])
     return None
+
+
+def phase_rooflines(work: dict, prof: dict, bf16: bool) -> dict:
+    """Every timed kernel against its own bound: {kernel: {bound, achieved, unit, frac}}."""
+    out = {}
+    for k, (ms, n) in prof.items():
+        if not n or k not in work:
+            continue
+        r = roofline_for(k, work[k], ms / n / 1e3, bf16)
+        out[k] = {"bound": r["bound"], "achieved": r["achieved"], "unit": r["unit"], "frac": r["achieved"] / r["peak"]}
+    return out
+
+
+def gather_counter_gbps(wl, prof: dict):
+    """HBM bytes of the gather from the FETCH_SIZE / WRITE_SIZE summaries under profiles/
+    (while its sources are unchanged) over its measured launch time."""
+    t = measured_traffic("gather", wl.name)
+    ms, n = prof.get("gather", (0.0, 0))
+    return t / (ms / n / 1e3) / 1e9 if (t is not None and n) else None
+
+
+def attention_exp_rate(wl, B: int, prof: dict):
+    """Exponentials per second of the attention kernels (one per (query, key) pair in the
+    forward and one in the backward) and the fraction of the measured v_exp_f32 rate."""
+    if not wl.attention:
+        return None
+    out = {}
+    for k in ("fwd_attention", "bwd_attention"):
+        ms, n = prof.get(k, (0.0, 0))
+        if n:
+            rate = B * wl.rank * wl.rank / (ms / n / 1e3)
+            out[k] = {"exp_per_s": rate, "frac_of_measured_peak": rate / EXP_PEAK_PER_S}
+    return out
 
 
 def cpu_baseline(wl, target_s: float, head=None) -> dict:
@@ -410,6 +445,10 @@ def main():
         "roofline": roof,
         "gemm_mfma_frac": (gemm_flops / gemm_s / 1e12 / PEAK_BF16_TFLOPS) if gemm_s > 0 else None,
         "gather_gbps": (work["gather"][1] / gather_s / 1e9) if gather_s > 0 else None,
+        "gather_hbm_frac": (work["gather"][1] / gather_s / 1e9 / PEAK_HBM_GBS) if gather_s > 0 else None,
+        "gather_counter_gbps": gather_counter_gbps(wl, prof),
+        "attention_exp_per_s": attention_exp_rate(wl, B, prof),
+        "phases": phase_rooflines(work, prof, wl.dtype == "bf16"),
         "kernels": kernels,
     }
     if wl.num_cat > 0:
