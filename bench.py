@@ -239,10 +239,34 @@ def cpu_baseline(wl, target_s: float, head=None) -> dict:
                       "%.1f s, single-threaded" % (rows, wl.name, " + head" if head is not None else "", dt)}
 
 
-def _oracle_step(wl, rows: int, head=None) -> float:
+def _oracle_worker(wl, rows: int, head, seed: int) -> float:
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(limits=1):
+        return _oracle_step(wl, rows, head, seed)
+
+
+def cpu_baseline_parallel(wl, target_s: float, head, single: dict) -> dict:
+    """The same oracle step in one single-threaded process per host core (at most 16),
+    each on its own sub-batch of about `target_s` seconds of work; samples/s is the
+    total over the wall time of the pool (the table gradients stay per process)."""
+    import multiprocessing as mp
+    workers = max(1, min(16, os.cpu_count() or 1))
+    rows = int(max(16, min(wl.batch, round(single["value"] * target_s))))
+    ctx = mp.get_context("spawn")
+    with ctx.Pool(workers) as pool:
+        pool.starmap(_oracle_worker, [(wl, 8, head, i) for i in range(workers)])  # import and build once
+        t0 = time.perf_counter()
+        pool.starmap(_oracle_worker, [(wl, rows, head, i) for i in range(workers)])
+        wall = time.perf_counter() - t0
+    return {"value": workers * rows / wall, "unit": "samples/s", "cores": workers, "kind": "oracle",
+            "sample": "%d processes x %d samples of the %s workload%s, %.1f s wall, one oracle per core"
+                      % (workers, rows, wl.name, " + head" if head is not None else "", wall)}
+
+
+def _oracle_step(wl, rows: int, head=None, seed=None) -> float:
     import oracle
     from paper_2402_06859_amd.synth import make_inputs
-    inp = make_inputs(wl, batch=rows, bias_std=0.0)
+    inp = make_inputs(wl, batch=rows, bias_std=0.0, seed=None if seed is None else 1000 + seed)
     W = [x.float().numpy() for x in inp["w_down"]]
     U = [x.float().numpy() for x in inp["u"]]
     b = [x.float().numpy() for x in inp["bias"]]
@@ -360,11 +384,17 @@ def main():
         wl = wl.with_(parallel=True)
     if args.hashed:
         wl = wl.with_(hashed=True, table_rows=1 << 16)
+    head = HEADS[args.head] if args.head else None
+    # the CPU baselines run before anything touches the GPU (their worker processes
+    # are started from a process that has not initialised it)
+    cpu = cpu_par = None
+    if args.cpu_seconds > 0:
+        cpu = cpu_baseline(wl, args.cpu_seconds, head)
+        cpu_par = cpu_baseline_parallel(wl, args.cpu_seconds, head, cpu)
     torch.cuda.set_device(0)
     inp = make_inputs(wl, id_mode=args.id_mode)
     db = DeviceBatch(wl, inp)
     B = db.B
-    head = HEADS[args.head] if args.head else None
     if head is not None:
         dh = DeviceHead(db.lib, head, make_head_inputs(wl, head, with_x=False), B)
         step = lambda: dh.tower_step(db)
@@ -453,8 +483,9 @@ def main():
     }
     if wl.num_cat > 0:
         out["gather_q8"] = time_gather_q8(db, work["gather_q8"][1], work["gather"][1])
-    if args.cpu_seconds > 0:
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, head)
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
+        out["cpu_baseline_all_cores"] = cpu_par
     print(json.dumps(out), flush=True)
 
 
