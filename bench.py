@@ -307,6 +307,33 @@ def _oracle_step(wl, rows: int, head=None, seed=None) -> float:
     return time.perf_counter() - t0
 
 
+def time_graph_replays(step, steps: int, B: int) -> dict:
+    """The step captured once in a HIP graph (torch.cuda.CUDAGraph; the library issues
+    kernel launches only), then `steps` replays timed with events on the replay stream."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for _ in range(3):
+        graph.replay()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        graph.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    return {"ms_per_step": ms, "samples_per_s": B / (ms / 1e3), "replays": steps}
+
+
 def time_gather_q8(db, q8_bytes: float, bytes16: float, launches: int = 20) -> dict:
     """Serving-path gather from middle-max 8-bit tables (quantized once here), timed
     with HIP events on its launch stream; the storage-type gather on the same batch
@@ -352,6 +379,8 @@ def main():
                     help="train a Feed-style tower: the cross stack's output goes through a head (lmlp: gated "
                          "4 x 3500 ReLU layers, logit, isotonic calibration, log loss) whose input gradient "
                          "drives the cross-stack backward")
+    ap.add_argument("--graph", action="store_true",
+                    help="also capture the step in a HIP graph and time its replays (graph_ms_per_step)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device-to-device a few times (known traffic, to scale HBM counters)")
     args = ap.parse_args()
@@ -483,6 +512,8 @@ def main():
     }
     if wl.num_cat > 0:
         out["gather_q8"] = time_gather_q8(db, work["gather_q8"][1], work["gather"][1])
+    if args.graph:
+        out["graph"] = time_graph_replays(step, args.steps, B)
     if cpu is not None:
         out["cpu_baseline"] = cpu
         out["cpu_baseline_all_cores"] = cpu_par
