@@ -491,10 +491,13 @@ struct Pipe {
                 for (int j = 0; j < TN; ++j)
                     bfr[buf][j] = load_frag32<BN, BKS>(cur + BM * BK, wn * (BN / WN) + j * 32, ks, lane);
             };
+            // (not with a K-strided A and eight accumulator tiles: that variant would spill)
+            constexpr bool DB = !(AKS && TM * TN > 4);
             frags(0, 0);
 #pragma unroll
             for (int s = 0; s < BK / 16; ++s) {
-                if (s + 1 < BK / 16) frags((s + 1) & 1, (s + 1) * 16);
+                if (!DB && s > 0) frags(s & 1, s * 16);
+                if (DB && s + 1 < BK / 16) frags((s + 1) & 1, (s + 1) * 16);
                 // keep the compiler from sinking those reads below the MFMAs
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
