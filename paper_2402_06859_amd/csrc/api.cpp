@@ -267,7 +267,7 @@ HeadScratch head_scratch_layout(const rdcn_handle* h, int64_t B) {
 
 bool a16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-rdcn_status check_head_weights(const rdcn_handle* h, const rdcn_head_weights* w, bool grads) {
+rdcn_status check_head_weights(const rdcn_handle* h, const rdcn_head_weights* w) {
     if (!w) return RDCN_ERR_ARG;
     const rdcn_head_config& c = h->head;
     for (int l = 0; l < c.num_hidden; ++l) {
@@ -275,7 +275,6 @@ rdcn_status check_head_weights(const rdcn_handle* h, const rdcn_head_weights* w,
         if (c.gated && (!w->gate_w[l] || !w->gate_b[l] || !a16(w->gate_w[l]))) return RDCN_ERR_ARG;
     }
     if (!w->w_out || !w->b_out || !w->cal_w || !w->cal_b || !a16(w->w_out)) return RDCN_ERR_ARG;
-    (void)grads;
     return RDCN_OK;
 }
 
@@ -725,7 +724,7 @@ rdcn_status rdcn_head_forward(rdcn_handle* h, int64_t batch, const void* x, cons
     rdcn_status st = check_batch(h, batch);
     if (st != RDCN_OK) return st;
     if (!h->head_on) return RDCN_ERR_ARG;
-    if ((st = check_head_weights(h, w, false)) != RDCN_OK) return st;
+    if ((st = check_head_weights(h, w)) != RDCN_OK) return st;
     if (batch == 0) return RDCN_OK;
     if (!x || !a16(x) || !e_cal || !y_logit || !y_cal || !saved) return RDCN_ERR_ARG;
     if (!aligned256(saved)) return RDCN_ERR_WORKSPACE;
@@ -775,8 +774,8 @@ rdcn_status rdcn_head_backward(rdcn_handle* h, int64_t batch, const void* x, con
     rdcn_status st = check_batch(h, batch);
     if (st != RDCN_OK) return st;
     if (!h->head_on) return RDCN_ERR_ARG;
-    if ((st = check_head_weights(h, w, false)) != RDCN_OK) return st;
-    if ((st = check_head_weights(h, grads, true)) != RDCN_OK) return st;
+    if ((st = check_head_weights(h, w)) != RDCN_OK) return st;
+    if ((st = check_head_weights(h, grads)) != RDCN_OK) return st;
     if (!scratch || !aligned256(scratch)) return RDCN_ERR_WORKSPACE;
     if (batch > 0) {
         if (!x || !a16(x) || !e_cal || !saved || !grad_ycal || !grad_x || !a16(grad_x) || !grad_e)

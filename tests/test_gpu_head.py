@@ -205,6 +205,15 @@ def test_deterministic_rerun():
         assert torch.equal(a, b)
 
 
+def test_head_needs_a_bf16_model():
+    need_gpu()
+    from paper_2402_06859_amd.rdcn import RDCN_ERR_UNSUPPORTED
+    lib = Rdcn(config_for(WORKLOADS["tiny"], 8))  # float storage
+    with pytest.raises(RdcnError) as ei:
+        lib.head_configure(make_head_config([16], True, 4, 0.0, 1.0))
+    assert ei.value.status == RDCN_ERR_UNSUPPORTED
+
+
 def test_head_argument_errors():
     need_gpu()
     lib = Rdcn(config_for(RAGGED, 8))
