@@ -91,6 +91,12 @@ def kernel_work(wl, B: int) -> dict:
     w["emb_keys"] = (0.0, nnz * 8 + 2 * tp * nnz * 8 + (nnz * 4 if wl.multi_hot else 0), 0.0)
     w["emb_sort"] = (0.0, passes * 2 * tp * nnz * (4 + 8 + 8), 0.0)  # histogram read + scatter read/write per pass
     w["emb_reduce"] = (0.0, 2 * tp * nnz * (8 + D * 4) + 2 * tp * F * wl.table_rows * D * 8, 0.0)
+    # one-kernel path: ids (and bag offsets), each feature's gradient slab once, every table row
+    # read and written once (+ the other table once with the product combine); the per-occurrence
+    # re-reads of gradient slices are served by L2
+    w["emb_fused"] = (0.0, nnz * 8 + (B * F * 8 if wl.multi_hot else 0) + B * F * D * 4
+                      + 2 * F * wl.table_rows * D * 8 + (2 * F * wl.table_rows * D * eb if wl.combine == "mul" else 0),
+                      0.0)
     # serving gather from 8-bit tables: codes (1 byte per value) and each row's (middle, scale)
     w["gather_q8"] = (0.0, B * (F * hot * 8 + 2 * tp * F * hot * (D + 8) + F * D * eb + 2 * Nd * eb), 0.0)
     return w
@@ -153,6 +159,7 @@ KERNEL_SOURCES = {
     "emb_keys": ["embed_bwd.hip", "device_common.h"],
     "emb_sort": ["embed_bwd.hip", "device_common.h"],
     "emb_reduce": ["embed_bwd.hip", "device_common.h"],
+    "emb_fused": ["embed_bwd.hip", "device_common.h"],
 }
 for _k in ("fwd_down_gemm", "fwd_up_gemm", "bwd_gu_gemm", "bwd_gh_gemm", "bwd_gw_gemm", "bwd_gx_gemm"):
     KERNEL_SOURCES[_k] = ["gemm.hip", "gemm.h", "device_common.h"]

@@ -195,7 +195,8 @@ rdcn_status qr_embed_gather_q8(rdcn_handle* h, int64_t batch, const void* ids, c
 
 /*
  * Scratch bytes qr_embed_backward needs for `batch` samples holding `nnz` ids
- * in total (single-hot: nnz = batch * F).
+ * in total (single-hot: nnz = batch * F). 0 for unhashed ids with tables of
+ * at most 16384 rows (qr_rows_q and m), which take a one-kernel path.
  */
 rdcn_status qr_embed_backward_workspace(const rdcn_handle* h, int64_t batch, int64_t nnz, size_t* scratch_bytes);
 
@@ -206,10 +207,11 @@ rdcn_status qr_embed_backward_workspace(const rdcn_handle* h, int64_t batch, int
  * valid id of bag (b, f) and g = grad_x0[b, f*D : (f+1)*D]:
  *   sum combine:     gQ_f[qi] += g,            gR_f[ri] += g
  *   product combine: gQ_f[qi] += g * R_f[ri],  gR_f[ri] += g * Q_f[qi]
- * The contributions to one table row are added in (b, position-in-bag) order,
- * so the result is deterministic. ids/offsets/tables as in qr_embed_gather;
- * nnz = number of ids (batch * F when single-hot). scratch must hold
- * qr_embed_backward_workspace() bytes. grad_x0, grad_q_tables and
+ * No atomics: the order in which a row's contributions are added depends only
+ * on the inputs and the configuration, so the result is deterministic.
+ * ids/offsets/tables as in qr_embed_gather; nnz = number of ids (batch * F
+ * when single-hot). scratch must hold qr_embed_backward_workspace() bytes (it
+ * may be NULL when that is 0). grad_x0, grad_q_tables and
  * grad_r_tables must be 16-byte aligned (RDCN_ERR_ARG otherwise).
  */
 rdcn_status qr_embed_backward(rdcn_handle* h, int64_t batch, int64_t nnz, const void* ids, const int64_t* offsets,
@@ -289,7 +291,8 @@ typedef enum rdcn_kernel {
     RDCN_KERNEL_HEAD_GX_GEMM = 23,  /* head backward: G_{l-1} (or grad_x) from G_l W_l */
     RDCN_KERNEL_HEAD_GATE_BWD = 24, /* head backward: gate-logit gradients from the row partials */
     RDCN_KERNEL_HEAD_COLSUM = 25,   /* head backward: bias, gate and calibration gradients (column sums) */
-    RDCN_KERNEL_COUNT = 26
+    RDCN_KERNEL_EMB_FUSED = 26,     /* embedding backward in one kernel (per-slice sort + sums in LDS) */
+    RDCN_KERNEL_COUNT = 27
 } rdcn_kernel;
 
 /*

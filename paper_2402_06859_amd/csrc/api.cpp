@@ -432,6 +432,10 @@ rdcn_status qr_embed_backward_workspace(const rdcn_handle* h, int64_t batch, int
     if (!scratch_bytes || nnz < 0) return RDCN_ERR_ARG;
     if (!h->cfg.multi_hot && nnz != batch * h->cfg.num_cat) return RDCN_ERR_SHAPE;
     if (emb_pairs(nnz, h->cfg.hashed != 0) >= ((int64_t)1 << 31)) return RDCN_ERR_UNSUPPORTED;
+    if (emb_fused_ok(h->cfg.qr_rows_q, h->cfg.qr_rows_r, h->cfg.emb_dim, h->cfg.hashed != 0)) {
+        *scratch_bytes = 0;  // the one-kernel path needs no workspace
+        return RDCN_OK;
+    }
     const EmbedBwdLayout L =
         embed_bwd_layout(nnz, h->cfg.num_cat, h->cfg.qr_rows_q, h->cfg.qr_rows_r, h->cfg.emb_dim, h->cfg.multi_hot,
                          h->cfg.combine == RDCN_COMBINE_MUL, h->cfg.hashed != 0);
@@ -449,9 +453,9 @@ rdcn_status qr_embed_backward(rdcn_handle* h, int64_t batch, int64_t nnz, const 
     const rdcn_config& c = h->cfg;
     if ((offsets != nullptr) != (c.multi_hot != 0)) return RDCN_ERR_ARG;
     if (batch == 0 || nnz == 0 || c.num_cat == 0) return RDCN_OK;
-    if (!ids || !q_tables || !r_tables || !grad_x0 || !grad_q_tables || !grad_r_tables || !scratch)
+    if (!ids || !q_tables || !r_tables || !grad_x0 || !grad_q_tables || !grad_r_tables || (need > 0 && !scratch))
         return RDCN_ERR_ARG;
-    if (scratch_bytes < need || !aligned256(scratch)) return RDCN_ERR_WORKSPACE;
+    if (need > 0 && (scratch_bytes < need || !aligned256(scratch))) return RDCN_ERR_WORKSPACE;
     if ((((uintptr_t)grad_x0) | ((uintptr_t)grad_q_tables) | ((uintptr_t)grad_r_tables)) & 15) return RDCN_ERR_ARG;
     EmbedBwdArgs a;
     a.batch = batch;
@@ -477,6 +481,10 @@ rdcn_status qr_embed_backward(rdcn_handle* h, int64_t batch, int64_t nnz, const 
     a.magic_m = h->magic;
     a.shift_m = h->shift;
     hipStream_t s = (hipStream_t)stream;
+    if (need == 0) {
+        ProfScope ps(h, RDCN_KERNEL_EMB_FUSED, s);
+        return hip_status(launch_emb_fused(a, h->bf16, h->ids64, s));
+    }
     {
         ProfScope ps(h, RDCN_KERNEL_EMB_KEYS, s);
         RDCN_TRY(launch_emb_keys(a, h->ids64, scratch, s));

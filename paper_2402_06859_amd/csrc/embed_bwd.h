@@ -36,5 +36,9 @@ hipError_t launch_emb_keys(const EmbedBwdArgs& a, bool ids64, void* scratch, hip
 hipError_t launch_emb_sort(const EmbedBwdArgs& a, void* scratch, hipStream_t s);
 // grad_x0, grad_q and grad_r must be 16-byte aligned (checked by the caller).
 hipError_t launch_emb_reduce(const EmbedBwdArgs& a, bool bf16, void* scratch, hipStream_t s);
+// One-kernel embedding backward without scratch, for unhashed ids and tables of at most
+// 16384 rows (emb_fused_ok); the same sums in the same per-row order of occurrences.
+bool emb_fused_ok(int rows_q, int m, int D, bool hashed);
+hipError_t launch_emb_fused(const EmbedBwdArgs& a, bool bf16, bool ids64, hipStream_t s);
 
 }  // namespace rdcn

@@ -22,6 +22,8 @@
 //      tile and summed in tile order by a fix-up pass.
 // The result is deterministic: each row's contributions are added in
 // (b, position-in-bag) order, irrespective of scheduling.
+// Unhashed ids with tables of at most 16384 rows take the one-kernel path of
+// step 4 instead (no scratch, no global sort).
 #include "device_common.h"
 #include "embed_bwd.h"
 
@@ -252,11 +254,14 @@ struct SegCtx {
     uint32_t n;
     uint32_t sentinel, rbase;
 
-    // contribution of sorted pair (k, o) to the row of key k, columns c .. c+3.
-    // Every load is issued unconditionally (ok = false reads row 0 / occurrence 0
-    // and returns zeros), so the loads of many pairs can be in flight together.
+    // loads for the contribution of sorted pair (k, o) to the row of key k, columns
+    // c .. c+3: the gradient slice into g and, with the product combine, the other
+    // table's row into r (the contribution is g * r). Every load is issued
+    // unconditionally (ok = false reads row 0 / occurrence 0; the caller masks the
+    // result when it uses it), and nothing writes the loaded registers before that
+    // use, so the loads of many pairs are in flight together.
     template <bool MUL, bool BAGS>
-    __device__ __forceinline__ Cols4 contrib(uint32_t k, uint32_t o, int c, bool ok) const {
+    __device__ __forceinline__ void contrib(uint32_t k, uint32_t o, int c, bool ok, Cols4& g, Cols4& r) const {
         const uint32_t kk0 = ok ? k : 0u;
         const bool isq = kk0 < rbase;
         const uint32_t kk = isq ? kk0 : kk0 - rbase;
@@ -270,15 +275,13 @@ struct SegCtx {
         const uint32_t bag = BAGS ? bag_of[occ] : occ;
         const int64_t b = div_magic(bag, DivMagic{a.magic_f, a.shift_f, (uint32_t)a.F});
         const f32x4_t w = *(const f32x4_t*)(a.grad_x0 + b * a.d + (int64_t)f * a.D + cc);
-        Cols4 out = {{w.x, w.y, w.z, w.w}};
+        g = Cols4{{w.x, w.y, w.z, w.w}};
         if (MUL) {
             const T* other = isq ? (const T*)a.r_tables + ((int64_t)tbl * a.m + rrow[oo]) * a.D + cc
                                  : (const T*)a.q_tables + ((int64_t)tbl * a.rows_q + qrow[oo]) * a.D + cc;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) out.v[e] *= st<T>::load(other + e);
+            for (int e = 0; e < 4; ++e) r.v[e] = st<T>::load(other + e);
         }
-        if (!ok) out = Cols4{{0.f, 0.f, 0.f, 0.f}};
-        return out;
     }
 
     __device__ __forceinline__ float* row_of(uint32_t k) const {
@@ -352,11 +355,11 @@ __global__ __launch_bounds__(256) void k_seg_reduce(SegCtx<T> s, float* __restri
             }
             dst[u] = d;
         }
-        Cols4 x[U], old[U];
+        Cols4 x[U], o4[U], old[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const bool ok = key[u] != SEG_PAD && key[u] != s.sentinel && colok;
-            x[u] = s.template contrib<MUL, BAGS>(key[u], val[u], c, ok);
+            s.template contrib<MUL, BAGS>(key[u], val[u], c, ok, x[u], o4[u]);
             old[u] = load4(s.row_of(dst[u] == DST_ROW ? key[u] : 0u) + (colok ? c : 0));
         }
 #pragma unroll
@@ -364,7 +367,10 @@ __global__ __launch_bounds__(256) void k_seg_reduce(SegCtx<T> s, float* __restri
             const uint32_t k = key[u];
             const uint32_t kprev = __shfl_up(k, L);
             bool head = grp == 0 ? k != carry_key : k != kprev;
-            Cols4 v = x[u];
+            const bool ok = k != SEG_PAD && k != s.sentinel && colok;
+            Cols4 v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v.v[e] = ok ? (MUL ? x[u].v[e] * o4[u].v[e] : x[u].v[e]) : 0.f;
 #pragma unroll
             for (int off = 1; off < E; off <<= 1) {
                 Cols4 y;
@@ -455,6 +461,319 @@ __global__ __launch_bounds__(256) void k_seg_fixup(const uint32_t* __restrict__ 
     }
 }
 
+// 4. Fused path (unhashed ids, tables of at most FU_ROWS * FU_MAX_SLICES rows):
+// one workgroup per (feature, table, row slice) replaces steps 1-3. It walks the
+// feature's occurrences in (bag, position) order, CAP at a time, keeps those whose
+// row falls in its slice and sorts them by row in LDS (a counting sort over at most
+// FU_ROWS rows: each wave ranks its quarter of the chunk with ballots, a scan over
+// the rows gives every (row, wave) run its start). The sorted chunk is split into
+// equal parts, one per lane group (L lanes of four columns each, 64 / L groups per
+// wave); a group adds its part's contributions one after another, and a segment
+// that crosses parts is finished by the group in which it starts, from per-part
+// head and tail pieces in LDS, after a barrier. The rows of a slice belong to one workgroup, so
+// each chunk's row sums are added straight into the table gradient (+=), chunk after
+// chunk. Summation order is fixed by the data: deterministic.
+// The workgroups of one feature are given block indices with equal residue mod 8 so
+// that they run on one XCD and share its L2 copy of the feature's gradient slab.
+constexpr int FU_CAP = 4096;            // occurrences per chunk
+constexpr int FU_QW = FU_CAP / 4;       // per wave
+constexpr int FU_ROWS = 1024;           // rows per slice
+constexpr int FU_MAX_SLICES = 16;
+constexpr int FU_TARGET_BLOCKS = 256;   // workgroups the slice count aims for (fewer slices: less repeated id work)
+constexpr int FU_BAGS = 1024;           // bags per block (bag front-end), four per thread
+constexpr uint32_t FU_SKIP = 0xffffffffu;
+
+struct FusedArgs {
+    EmbedBwdArgs a;
+    int ids64;
+    int slices;                // row slices per table
+    uint32_t rps_q, rps_r;     // rows per slice of the quotient / remainder tables
+};
+
+template <typename T, int L, bool MUL, bool BAGS>
+__global__ __launch_bounds__(256) void k_emb_fused(FusedArgs fa) {
+    constexpr int E = 64 / L;                // lane groups per wave
+    constexpr int NP = 4 * E;                // parts of a sorted chunk, one per lane group
+    constexpr int U = MUL ? 8 : 16;          // elements of a part whose loads are in flight together
+    __shared__ uint32_t key_e[FU_CAP];       // per chunk element: row << 16 | rank in its wave's run, or FU_SKIP
+    __shared__ uint32_t sorted[FU_CAP];      // row << 12 | element, in (row, element) order
+    __shared__ uint32_t whist[4][FU_ROWS];   // per wave row counts, then run starts
+    __shared__ float carry[2][NP][4 * L];    // per part head / tail pieces
+    __shared__ uint16_t bag_e[BAGS ? FU_CAP : 1];
+    __shared__ uint16_t other_e[MUL ? FU_CAP : 1];
+    __shared__ uint32_t bstart[BAGS ? FU_BAGS : 1];
+    __shared__ int64_t boff[BAGS ? FU_BAGS : 1];
+    __shared__ uint32_t sh[4];
+    __shared__ uint32_t nkept;
+
+    const EmbedBwdArgs& a = fa.a;
+    const int per_f = 2 * fa.slices;
+    const int j = (int)(blockIdx.x >> 3);
+    const int f = (j / per_f) * 8 + (int)(blockIdx.x & 7);
+    if (f >= a.F) return;
+    const int sub = j % per_f;
+    const bool isq = sub < fa.slices;
+    const uint32_t rps = isq ? fa.rps_q : fa.rps_r;
+    const uint32_t r0 = (uint32_t)(isq ? sub : sub - fa.slices) * rps;
+    const uint32_t rows = isq ? (uint32_t)a.rows_q : a.m;
+    if (r0 >= rows) return;
+    const uint32_t nr = rows - r0 < rps ? rows - r0 : rps;
+    const int nbits = nr > 1 ? 32 - __clz((int)(nr - 1)) : 0;
+    const int D = a.D;
+    float* gtab = isq ? a.grad_q + ((int64_t)f * a.rows_q + r0) * D : a.grad_r + ((int64_t)f * a.m + r0) * D;
+    const T* otab = isq ? (const T*)a.r_tables + (int64_t)f * a.m * D : (const T*)a.q_tables + (int64_t)f * a.rows_q * D;
+    const float* gx = a.grad_x0 + (int64_t)f * D;
+
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int grp = lane / L, sub4 = lane % L, c = 4 * sub4;
+    const bool colok = c < D;
+    const uint64_t lt = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+    for (int i = threadIdx.x; i < 4 * FU_ROWS; i += 256) (&whist[0][0])[i] = 0u;
+
+    const int64_t step_b = BAGS ? FU_BAGS : FU_CAP;
+    for (int64_t b0 = 0; b0 < a.batch; b0 += step_b) {
+        const uint32_t nb = (uint32_t)(a.batch - b0 < step_b ? a.batch - b0 : step_b);
+        uint32_t total = nb;  // occurrences of this block of bags
+        if (BAGS) {
+            uint32_t len[4], s4 = 0;
+            int64_t beg[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t t = 4 * threadIdx.x + k;
+                len[k] = 0;
+                beg[k] = 0;
+                if (t < nb) {
+                    const int64_t u = (b0 + t) * a.F + f;
+                    int64_t s = a.offsets[u], e = a.offsets[u + 1];
+                    s = s < 0 ? 0 : (s > a.nnz ? a.nnz : s);
+                    e = e < s ? s : (e > a.nnz ? a.nnz : e);
+                    beg[k] = s;
+                    len[k] = (uint32_t)(e - s);
+                }
+                s4 += len[k];
+            }
+            uint32_t run = block_exclusive_scan(s4, sh, total);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                bstart[4 * threadIdx.x + k] = run;
+                boff[4 * threadIdx.x + k] = beg[k];
+                run += len[k];
+            }
+        }
+        __syncthreads();
+        for (uint32_t c0 = 0; c0 < total; c0 += FU_CAP) {
+            const uint32_t n = total - c0 < (uint32_t)FU_CAP ? total - c0 : (uint32_t)FU_CAP;
+            // A. rows of this wave's quarter (all id loads first, then the ranking); the
+            // rank of each kept element among the wave's earlier elements of its row
+            constexpr int NIT = FU_QW / 64;
+            int64_t pv[NIT];
+            uint32_t bagv[NIT];
+            if (BAGS) {
+                // last bag of the block whose start is <= the element: a branch-free search,
+                // all elements in lockstep (entries past the block's bags hold the total,
+                // which exceeds every element, so they are never taken)
+                uint32_t vv[NIT];
+#pragma unroll
+                for (int it = 0; it < NIT; ++it) {
+                    const uint32_t e = (uint32_t)(wv * FU_QW + it * 64 + lane);
+                    vv[it] = c0 + (e < n ? e : 0u);
+                    bagv[it] = 0;
+                }
+#pragma unroll
+                for (uint32_t sstep = FU_BAGS / 2; sstep > 0; sstep >>= 1) {
+#pragma unroll
+                    for (int it = 0; it < NIT; ++it) {
+                        const uint32_t t = bagv[it] + sstep;
+                        bagv[it] = bstart[t] <= vv[it] ? t : bagv[it];
+                    }
+                }
+#pragma unroll
+                for (int it = 0; it < NIT; ++it) pv[it] = boff[bagv[it]] + (int64_t)(vv[it] - bstart[bagv[it]]);
+            } else {
+#pragma unroll
+                for (int it = 0; it < NIT; ++it) {
+                    const uint32_t e = (uint32_t)(wv * FU_QW + it * 64 + lane);
+                    pv[it] = (b0 + (e < n ? e : 0u)) * a.F + f;
+                    bagv[it] = 0;
+                }
+            }
+            // every load is issued (element 0 stands in past the chunk end), so all are in flight together
+            int64_t idv[NIT];
+            if (fa.ids64) {
+#pragma unroll
+                for (int it = 0; it < NIT; ++it) idv[it] = ((const int64_t*)a.ids)[pv[it]];
+            } else {
+#pragma unroll
+                for (int it = 0; it < NIT; ++it) idv[it] = (int64_t)((const int32_t*)a.ids)[pv[it]];
+            }
+            const DivMagic dm{a.magic_m, a.shift_m, a.m};
+#pragma unroll
+            for (int it = 0; it < NIT; ++it) {
+                const uint32_t e = (uint32_t)(wv * FU_QW + it * 64 + lane);
+                // ids below vocab <= rows_q * m <= 2^28 here: the 32-bit split is exact
+                const int64_t id = idv[it];
+                const uint32_t x = (uint32_t)id;
+                const uint32_t qi = div_magic(x, dm), ri = x - qi * a.m;
+                const uint32_t r = (isq ? qi : ri) - r0;
+                const bool kept = e < n && id >= 0 && (uint64_t)id < a.vocab && qi < (uint32_t)a.rows_q && r < nr;
+                const uint32_t row = kept ? r : 0u;
+                uint64_t peers = __ballot(kept);
+                for (int bb = 0; bb < nbits; ++bb) {
+                    const bool bit = (row >> bb) & 1u;
+                    const uint64_t m = __ballot(bit);
+                    peers &= bit ? m : ~m;
+                }
+                const uint32_t before = whist[wv][row];
+                const uint32_t rank = (uint32_t)__popcll(peers & lt);
+                key_e[e] = kept ? (row << 16) | (before + rank) : FU_SKIP;
+                if (BAGS) bag_e[e] = (uint16_t)bagv[it];
+                if (MUL) other_e[e] = (uint16_t)(isq ? ri : qi);
+                if (kept && rank == 0) whist[wv][row] = before + (uint32_t)__popcll(peers);
+            }
+            __syncthreads();
+            // B. run starts: rows in order, inside a row the waves in order
+            {
+                uint32_t cnt[4][4], s4 = 0;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const uint32_t r = 4 * threadIdx.x + k;
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) {
+                        cnt[k][w] = r < nr ? whist[w][r] : 0u;
+                        s4 += cnt[k][w];
+                    }
+                }
+                uint32_t tot;
+                uint32_t run = block_exclusive_scan(s4, sh, tot);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const uint32_t r = 4 * threadIdx.x + k;
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) {
+                        if (r < nr) whist[w][r] = run;
+                        run += cnt[k][w];
+                    }
+                }
+                if (threadIdx.x == 0) nkept = tot;
+            }
+            __syncthreads();
+            // C. placement
+            for (int it = 0; it < FU_QW / 64; ++it) {
+                const uint32_t e = (uint32_t)(wv * FU_QW + it * 64 + lane);
+                const uint32_t kv = key_e[e];
+                if (kv != FU_SKIP) {
+                    const uint32_t row = kv >> 16;
+                    sorted[whist[wv][row] + (kv & 0xffffu)] = (row << 12) | e;
+                }
+            }
+            __syncthreads();
+            for (int i = threadIdx.x; i < 4 * FU_ROWS; i += 256) (&whist[0][0])[i] = 0u;
+            // D. sums in sorted order: lane group g of wave w takes part P = w * E + g, an
+            // equal share of the sorted chunk, and adds its elements one after another
+            const uint32_t nk = nkept;
+            const int P = wv * E + grp;
+            const uint32_t lo = (uint32_t)(((uint64_t)nk * P) / NP), hi = (uint32_t)(((uint64_t)nk * (P + 1)) / NP);
+            uint32_t first_key = SEG_PAD, last_key = SEG_PAD;
+            bool head_cont = false, tail_cont = false;
+            if (lo < hi) {
+                first_key = sorted[lo] >> 12;
+                last_key = sorted[hi - 1] >> 12;
+                head_cont = lo > 0 && (sorted[lo - 1] >> 12) == first_key;
+                tail_cont = hi < nk && (sorted[hi] >> 12) == last_key;
+            }
+            const uint32_t cnt = hi - lo;
+            const uint32_t cmax = (nk + NP - 1) / NP;  // longest part (uniform loop bound)
+            Cols4 acc = {{0.f, 0.f, 0.f, 0.f}};
+            uint32_t acc_key = SEG_PAD;
+            for (uint32_t s0 = 0; s0 < cmax; s0 += U) {
+                uint32_t key[U], el[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const uint32_t i = s0 + u;
+                    const uint32_t v = i < cnt ? sorted[lo + i] : 0u;
+                    key[u] = i < cnt ? v >> 12 : SEG_PAD;
+                    el[u] = v & 0xfffu;
+                }
+                const uint32_t key_after = s0 + U < cnt ? sorted[lo + s0 + U] >> 12 : SEG_PAD;
+                // where each segment that ends here goes: the table row, or this part's head /
+                // tail piece when the segment runs on into the previous / next part
+                int dst[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const uint32_t k = key[u];
+                    const uint32_t knext = u + 1 < U ? key[u + 1 < U ? u + 1 : u] : key_after;
+                    int d = DST_NONE;
+                    if (k != SEG_PAD && colok && knext != k) {
+                        if (head_cont && k == first_key) d = DST_HEAD;
+                        else if (tail_cont && k == last_key) d = DST_TAIL;
+                        else d = DST_ROW;
+                    }
+                    dst[u] = d;
+                }
+                // all loads first (padding lanes read bag b0 / row 0 and are masked when used):
+                // a load's registers are not written again before use, so none waits for another
+                Cols4 x[U], o4[U], old[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const bool ok = key[u] != SEG_PAD && colok;
+                    const int cc = colok ? c : 0;
+                    const uint32_t ee = ok ? el[u] : 0u;
+                    const int64_t b = b0 + (ok ? (BAGS ? (int64_t)bag_e[ee] : (int64_t)ee) : 0);
+                    x[u] = load4(gx + b * a.d + cc);
+                    if (MUL) {
+                        const T* o = otab + (int64_t)(ok ? other_e[ee] : 0u) * D + cc;
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) o4[u].v[q] = st<T>::load(o + q);
+                    }
+                    old[u] = load4(gtab + (int64_t)(dst[u] == DST_ROW ? key[u] : 0u) * D + cc);
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const uint32_t k = key[u];
+                    const bool ok = k != SEG_PAD && colok;
+                    const bool cont = k == acc_key;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const float v = ok ? (MUL ? x[u].v[q] * o4[u].v[q] : x[u].v[q]) : 0.f;
+                        acc.v[q] = cont ? acc.v[q] + v : v;
+                    }
+                    acc_key = k;
+                    if (dst[u] == DST_ROW) {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) old[u].v[q] += acc.v[q];
+                        store4(gtab + (int64_t)k * D + c, old[u]);
+                    } else if (dst[u] != DST_NONE) {
+                        float* cp = &carry[dst[u] == DST_HEAD ? 0 : 1][P][c];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) cp[q] = acc.v[q];
+                    }
+                }
+            }
+            __syncthreads();
+            // E. a segment that runs on into later parts is finished by the part where it
+            // starts: its tail piece, then the head pieces of the parts it covers, in order
+            if (lo < hi && tail_cont && !(head_cont && first_key == last_key) && colok) {
+                Cols4 tot = {{carry[1][P][c], carry[1][P][c + 1], carry[1][P][c + 2], carry[1][P][c + 3]}};
+                for (int p2 = P + 1; p2 < NP; ++p2) {
+                    const uint32_t lo2 = (uint32_t)(((uint64_t)nk * p2) / NP);
+                    const uint32_t hi2 = (uint32_t)(((uint64_t)nk * (p2 + 1)) / NP);
+                    if (lo2 == hi2) continue;
+                    if ((sorted[lo2] >> 12) != last_key) break;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) tot.v[q] += carry[0][p2][c + q];
+                    if ((sorted[hi2 - 1] >> 12) != last_key) break;
+                }
+                float* dstp = gtab + (int64_t)last_key * D + c;
+                Cols4 old = load4(dstp);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) old.v[q] += tot.v[q];
+                store4(dstp, old);
+            }
+            __syncthreads();
+        }
+    }
+}
+
 struct RedPtrs {
     const uint32_t *keys, *vals, *bag_of, *qrow, *rrow;
     float *carry_head, *carry_tail;
@@ -492,6 +811,19 @@ hipError_t launch_reduce_d(const EmbedBwdArgs& a, const RedPtrs& p, uint32_t n, 
     if (q <= 16) return launch_reduce<T, 16, MUL, BAGS>(a, p, n, st);
     if (q <= 32) return launch_reduce<T, 32, MUL, BAGS>(a, p, n, st);
     return launch_reduce<T, 64, MUL, BAGS>(a, p, n, st);
+}
+
+template <typename T, bool MUL, bool BAGS>
+hipError_t launch_fused_d(const FusedArgs& fa, unsigned blocks, hipStream_t st) {
+    const int q = (fa.a.D + 3) / 4;
+#define RDCN_FUSED(L) hipLaunchKernelGGL((k_emb_fused<T, L, MUL, BAGS>), dim3(blocks), dim3(256), 0, st, fa)
+    if (q <= 4) RDCN_FUSED(4);
+    else if (q <= 8) RDCN_FUSED(8);
+    else if (q <= 16) RDCN_FUSED(16);
+    else if (q <= 32) RDCN_FUSED(32);
+    else RDCN_FUSED(64);
+#undef RDCN_FUSED
+    return hipGetLastError();
 }
 
 inline int key_bits(uint32_t maxkey) {
@@ -626,6 +958,39 @@ hipError_t launch_emb_reduce(const EmbedBwdArgs& a, bool bf16, void* scratch, hi
     if (bf16) RDCN_RED(bf16_t);
     RDCN_RED(float);
 #undef RDCN_RED
+}
+
+bool emb_fused_ok(int rows_q, int m, int D, bool hashed) {
+    return !hashed && D > 0 && D <= 256 && rows_q > 0 && m > 0 && rows_q <= FU_ROWS * FU_MAX_SLICES &&
+           m <= FU_ROWS * FU_MAX_SLICES;
+}
+
+hipError_t launch_emb_fused(const EmbedBwdArgs& a, bool bf16, bool ids64, hipStream_t st) {
+    if (a.nnz == 0 || a.F == 0 || a.batch == 0) return hipSuccess;
+    if (!emb_fused_ok(a.rows_q, (int)a.m, a.D, a.hashed != 0)) return hipErrorInvalidValue;
+    FusedArgs fa;
+    fa.a = a;
+    fa.ids64 = ids64 ? 1 : 0;
+    const int rmax = a.rows_q > (int)a.m ? a.rows_q : (int)a.m;
+    // enough slices for the row limit, and for about FU_TARGET_BLOCKS workgroups
+    int S = (rmax + FU_ROWS - 1) / FU_ROWS;
+    const int want = (FU_TARGET_BLOCKS + 2 * a.F - 1) / (2 * a.F);
+    if (want > S) S = want;
+    if (S > FU_MAX_SLICES) S = FU_MAX_SLICES;
+    if (S > rmax) S = rmax;
+    fa.slices = S;
+    fa.rps_q = (uint32_t)((a.rows_q + S - 1) / S);
+    fa.rps_r = (a.m + (uint32_t)S - 1) / (uint32_t)S;
+    const unsigned blocks = 8u * (unsigned)((a.F + 7) / 8) * 2u * (unsigned)S;
+    const bool mul = a.combine == 0, bags = a.offsets != nullptr;
+#define RDCN_FU(T)                                                                                           \
+    do {                                                                                                     \
+        if (mul) return bags ? launch_fused_d<T, true, true>(fa, blocks, st) : launch_fused_d<T, true, false>(fa, blocks, st); \
+        return bags ? launch_fused_d<T, false, true>(fa, blocks, st) : launch_fused_d<T, false, false>(fa, blocks, st);       \
+    } while (0)
+    if (bf16) RDCN_FU(bf16_t);
+    RDCN_FU(float);
+#undef RDCN_FU
 }
 
 }  // namespace rdcn

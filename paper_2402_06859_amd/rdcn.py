@@ -30,7 +30,7 @@ EXPORTS = ["rdcn_create", "rdcn_destroy", "rdcn_dim", "rdcn_workspace_bytes", "q
 KERNELS = ["gather", "fwd_down_gemm", "fwd_attention", "fwd_up_gemm", "bwd_pointwise", "bwd_bias", "bwd_gu_gemm",
            "bwd_gh_gemm", "bwd_attention", "bwd_gw_gemm", "bwd_gx_gemm", "splitk_reduce", "emb_keys", "emb_sort",
            "emb_reduce", "gather_q8", "quantize", "head_gate", "head_fwd_gemm", "head_out", "head_loss",
-           "head_out_bwd", "head_gw_gemm", "head_gx_gemm", "head_gate_bwd", "head_colsum"]
+           "head_out_bwd", "head_gw_gemm", "head_gx_gemm", "head_gate_bwd", "head_colsum", "emb_fused"]
 MAX_HIDDEN = 8
 
 

@@ -153,7 +153,7 @@ def test_head_struct_layout_matches_c(tmp_path):
     C, W = rdcn.RdcnHeadConfig, rdcn.RdcnHeadWeights
     assert vals == [ctypes.sizeof(C), C.gated.offset, C.bucket_step.offset, ctypes.sizeof(W), W.w_out.offset,
                     W.cal_b.offset]
-    assert len(rdcn.KERNELS) == 26  # RDCN_KERNEL_COUNT: rdcn_profile_stop writes that many entries
+    assert len(rdcn.KERNELS) == 27  # RDCN_KERNEL_COUNT: rdcn_profile_stop writes that many entries
 
 
 def test_head_calls_reject_null_handle():

@@ -30,6 +30,30 @@ def run(wl, inp, gx0, id_type="i64", reps=1):
     return gq.cpu(), gr.cpu(), status
 
 
+def unreached(wl, inp):
+    """Rows of the quotient / remainder tables that no valid id reaches, [F, rows] masks."""
+    F, V, m = wl.num_cat, wl.vocab, wl.table_rows
+    ids = inp["ids"].numpy().astype(np.int64)
+    if inp["offsets"] is None:
+        feat = np.tile(np.arange(F), inp["batch"])
+        ids = ids.reshape(-1)
+    else:
+        lens = np.diff(inp["offsets"].numpy())
+        feat = np.repeat(np.tile(np.arange(F), inp["batch"]), lens)
+    ok = (ids >= 0) & (ids < V)
+    q = np.ones((F, m), dtype=bool)
+    r = np.ones((F, m), dtype=bool)
+    q[feat[ok], ids[ok] // m] = False
+    r[feat[ok], ids[ok] % m] = False
+    return q, r
+
+
+def assert_unreached_zero(wl, inp, gq, gr):
+    """Rows that no id reaches stay exactly zero (a reached row may still sum to 0)."""
+    uq, ur = unreached(wl, inp)
+    assert not np.any(gq.numpy()[uq]) and not np.any(gr.numpy()[ur])
+
+
 def ref(wl, inp, gx0):
     gq, gr, bad = oracle.embed_backward(inp["batch"], wl.num_cat, wl.emb_dim, wl.num_dense, wl.vocab,
                                         wl.table_rows, wl.table_rows, wl.combine, inp["ids"], inp["offsets"],
@@ -53,8 +77,7 @@ def test_embed_backward_full_batch(name, mode):
     print("rel err", e, flush=True)
     tol = 1e-5 if wl.dtype == "f32" else 1e-5  # float sums of float inputs: only summation rounding differs
     assert max(e) <= tol
-    # rows that no id reaches stay exactly zero
-    assert np.array_equal(gq.numpy() == 0, rq == 0) and np.array_equal(gr.numpy() == 0, rr == 0)
+    assert_unreached_zero(wl, inp, gq, gr)
 
 
 @pytest.mark.parametrize("name", ["small", "multihot"])
@@ -94,4 +117,83 @@ def test_embed_backward_skips_bad_ids():
     gq, gr, _ = run(wl, inp, gx0)
     rq, rr, bad = ref(wl, inp, gx0)
     assert bad == 2
+    assert max(relerr(gq.numpy(), rq), relerr(gr.numpy(), rr)) <= 1e-5
+
+
+def test_embed_backward_sort_path_large_tables():
+    """Tables of more than 16384 rows take the keys / radix sort / segmented-reduce path
+    (scratch > 0); tables of at most 16384 rows the one-kernel path (no scratch)."""
+    need_gpu()
+    wl = WORKLOADS["small"].with_(batch=2048, vocab=400_000_000, table_rows=20_000)
+    inp = make_inputs(wl, id_mode="rank", with_weights=False, with_grad=False)
+    lib = rdcn.Rdcn(rdcn.config_for(wl, inp["batch"]))
+    assert lib.embed_backward_workspace(inp["batch"], inp["ids"].numel()) > 0
+    small = rdcn.Rdcn(rdcn.config_for(WORKLOADS["small"], 4096))
+    assert small.embed_backward_workspace(4096, 4096 * 50) == 0
+    gx0 = grad_x0_like(wl, inp["batch"], 9)
+    print("embed_bwd sort path", flush=True)
+    gq, gr, status = run(wl, inp, gx0)
+    assert status == rdcn.RDCN_OK
+    rq, rr, _ = ref(wl, inp, gx0)
+    assert max(relerr(gq.numpy(), rq), relerr(gr.numpy(), rr)) <= 1e-5
+
+
+@pytest.mark.parametrize("batch,mode", [(9000, "rank"), (4097, "scatter"), (1, "rank")])
+def test_embed_backward_single_hot_chunks(batch, mode):
+    """Single-hot batches over several 4096-occurrence chunks, ragged last chunk, and one
+    sample; rank-order ids put most occurrences on one quotient row (a segment across
+    all four wave parts of every chunk)."""
+    need_gpu()
+    wl = WORKLOADS["small"].with_(batch=batch, num_cat=5)
+    inp = make_inputs(wl, id_mode=mode, with_weights=False, with_grad=False)
+    gx0 = grad_x0_like(wl, batch, 10)
+    print("embed_bwd single-hot", batch, mode, flush=True)
+    gq, gr, status = run(wl, inp, gx0)
+    assert status == rdcn.RDCN_OK
+    rq, rr, _ = ref(wl, inp, gx0)
+    assert max(relerr(gq.numpy(), rq), relerr(gr.numpy(), rr)) <= 1e-5
+    assert_unreached_zero(wl, inp, gq, gr)
+
+
+@pytest.mark.parametrize("combine", ["sum", "mul"])
+def test_embed_backward_bag_edges(combine):
+    """Bags: empty bags, a bag longer than a chunk (5000 ids), bags of one, and a hot id
+    that takes half of all occurrences; both combines."""
+    need_gpu()
+    F, B = 3, 700
+    wl = WORKLOADS["multihot"].with_(batch=B, num_cat=F, combine=combine, emb_dim=32, num_dense=16)
+    inp = make_inputs(wl, with_weights=False, with_grad=False)
+    rng = np.random.Generator(np.random.PCG64(11))
+    lens = rng.integers(0, 12, size=(B, F))
+    lens[rng.random((B, F)) < 0.2] = 0      # empty bags
+    lens[5, 1] = 5000                       # longer than one chunk
+    lens[600, 2] = 4500
+    lens[7, :] = 1
+    offsets = np.zeros(B * F + 1, dtype=np.int64)
+    np.cumsum(lens.reshape(-1), out=offsets[1:])
+    nnz = int(offsets[-1])
+    ids = rng.integers(0, wl.vocab, size=nnz)
+    ids[rng.random(nnz) < 0.5] = 123_457   # hot id: one long segment per table
+    inp["ids"] = torch.from_numpy(ids.astype(np.int64))
+    inp["offsets"] = torch.from_numpy(offsets)
+    gx0 = grad_x0_like(wl, B, 12)
+    print("embed_bwd bag edges", combine, "nnz", nnz, flush=True)
+    gq, gr, status = run(wl, inp, gx0)
+    assert status == rdcn.RDCN_OK
+    rq, rr, _ = ref(wl, inp, gx0)
+    assert max(relerr(gq.numpy(), rq), relerr(gr.numpy(), rr)) <= 1e-5
+    assert_unreached_zero(wl, inp, gq, gr)
+
+
+@pytest.mark.parametrize("D,dtype", [(4, "f32"), (48, "bf16"), (256, "bf16")])
+def test_embed_backward_widths(D, dtype):
+    """Table widths from one column group to 256 (one pair per step)."""
+    need_gpu()
+    wl = WORKLOADS["tiny"].with_(emb_dim=D, combine="sum", dtype=dtype)
+    inp = make_inputs(wl, id_mode="rank", with_weights=False, with_grad=False)
+    gx0 = grad_x0_like(wl, inp["batch"], 13)
+    print("embed_bwd width", D, flush=True)
+    gq, gr, status = run(wl, inp, gx0)
+    assert status == rdcn.RDCN_OK
+    rq, rr, _ = ref(wl, inp, gx0)
     assert max(relerr(gq.numpy(), rq), relerr(gr.numpy(), rr)) <= 1e-5
