@@ -217,6 +217,11 @@ __device__ __forceinline__ float pow2_ceil(float m) {
     return ldexpf(1.f, e);
 }
 
+// A wave-uniform float (the same value in every lane) moved to a scalar register.
+__device__ __forceinline__ float uniform_f(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, x)));
+}
+
 __device__ __forceinline__ float wave_max(float x) {
     for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
     return x;
@@ -450,7 +455,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     float vmax = 0.f;
 #pragma unroll
     for (int u = 0; u < KPL; ++u) vmax = fmaxf(vmax, fabsf(vr[u]));
-    const float vs = pow2_ceil(wave_max(vmax)), ivs = 1.0f / vs;  // exact: vs is a power of two
+    const float vs = uniform_f(pow2_ceil(wave_max(vmax))), ivs = 1.0f / vs;  // exact: vs is a power of two
     const int ldx = rpad;
 #pragma unroll
     for (int u = 0; u < KPL; ++u) {
@@ -592,7 +597,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         mvk = fmaxf(mvk, fabsf(vr[u] * kr[u]));
         mk = fmaxf(mk, fabsf(kr[u]));
     }
-    const float vks = pow2_ceil(wave_max(mvk)), ks = pow2_ceil(wave_max(mk));
+    const float vks = uniform_f(pow2_ceil(wave_max(mvk))), ks = uniform_f(pow2_ceil(wave_max(mk)));
     const float ivks = 1.0f / vks, iks = 1.0f / ks;  // exact: powers of two
 #pragma unroll
     for (int u = 0; u < KPL; ++u) {
@@ -616,7 +621,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         mb = fmaxf(mb, fabsf(cb[u]));
         mc = fmaxf(mc, fabsf(cg[u]));
     }
-    const float as = pow2_ceil(wave_max(ma)), bs = pow2_ceil(wave_max(mb)), cs = pow2_ceil(wave_max(mc));
+    const float as = uniform_f(pow2_ceil(wave_max(ma))), bs = uniform_f(pow2_ceil(wave_max(mb)));
+    const float cs = uniform_f(pow2_ceil(wave_max(mc)));
     const float ias = 1.0f / as, ibs = 1.0f / bs, ics = 1.0f / cs;  // exact: powers of two
 #pragma unroll
     for (int u = 0; u < RPL; ++u) {
