@@ -80,6 +80,19 @@ def test_ragged_small_shapes(attn, tau, beta):
     run_full_compare(wl.with_(skip_beta=beta))
 
 
+@pytest.mark.parametrize("rank", [40, 256])
+def test_attention_extreme_logits(rank):
+    """tau = 1e-4 puts the exponent coefficients beyond f16 range, so the attention kernels
+    compute the exponent arguments with FMAs instead of on the matrix cores (both the
+    paired-tile form of waves with up to 8 tiles and the 16-tile form). One layer: its q
+    and k come from bf16 inputs exactly, so the nearly one-hot softmax picks the same
+    keys as the float64 oracle (with more layers, rounding the stored activations to
+    bf16 moves near-ties)."""
+    need_gpu()
+    wl = Workload("extreme", 16, 200, 5, 50_000, 250, 24, 40, 1, rank, True, "bf16", "sum", 1.1, temperature=1e-4)
+    run_full_compare(wl)
+
+
 @pytest.mark.parametrize("attn", [True, False])
 def test_split_activations_ragged(attn):
     """hi + lo activations: the projections see ~16-bit activations, so the forward is
