@@ -87,7 +87,7 @@ size_t eb(const rdcn_handle* h) { return h->bf16 ? 2 : 4; }
 
 // Per layer: [v|q|k] (float with the attention term, else storage; plus a lo plane
 // of v when split), h and its lo plane (attention only), the attention row
-// statistics [o | Z] (float, bf16 storage with attention), t, x_{l+1} and its lo
+// statistics [o | Z | W1 | W2] (float, bf16 storage with attention), t, x_{l+1} and its lo
 // plane (l < L-1). Lo planes exist only with split_activations.
 struct SavedLayout {
     size_t P[RDCN_MAX_LAYERS], P2[RDCN_MAX_LAYERS], H[RDCN_MAX_LAYERS], H2[RDCN_MAX_LAYERS], A[RDCN_MAX_LAYERS],
@@ -108,7 +108,7 @@ SavedLayout saved_layout(const rdcn_handle* h, int64_t B) {
         s.P2[l] = off; off += (sp && !h->attn) ? al(B * r * e) : 0;
         s.H[l] = off; off += h->attn ? al(B * (size_t)h->hr * e) : 0;
         s.H2[l] = off; off += (sp && h->attn) ? al(B * r * e) : 0;
-        s.A[l] = off; off += (h->attn && h->bf16) ? al(B * 2 * r * 4) : 0;
+        s.A[l] = off; off += (h->attn && h->bf16) ? al(B * 4 * r * 4) : 0;
         s.T[l] = off; off += al(B * d * e);
         s.X[l] = off; off += more ? al(B * d * e) : 0;  // x_{l+1}
         s.X2[l] = off; off += (sp && more) ? al(B * d * e) : 0;

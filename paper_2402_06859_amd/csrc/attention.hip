@@ -183,17 +183,18 @@ __global__ __launch_bounds__(256) void k_attn_bwd(int64_t B, int r, float alpha,
 // 2^-11); all sums of one row use the same rounded e, so the normalisation by Z
 // is consistent. Output lane l holds quantities 4 (l / 16) .. +3 of row l % 16.
 //
-// One wave owns up to ATT_NT 16-row tiles of one sample and loops over all keys,
-// so row sums never leave its registers and the setup needs no workgroup
-// barrier; a sample with more rows is split over W = ceil(tiles / ATT_NT) waves
-// of one workgroup.
+// In the forward one wave owns up to ATT_NT 16-row tiles of one sample and loops
+// over all keys, so row sums never leave its registers; a sample with more rows
+// is split over W = ceil(tiles / ATT_NT) waves of one workgroup, which share the
+// sample's keys and X^T in LDS.
 //
-// The forward saves each row's o_i and Z_i. The backward then needs every e_ij
-// only once: the row sums (over keys) take e in the layout above, and the column
-// sums (over rows, weighted by per-row coefficients that depend on o_i and Z_i)
-// take the same values transposed: the wave writes its 32-row x 32-key block of
-// e to LDS and reads it back with ds_read_b64_tr_b16, which delivers the B
-// operand with K running over rows.
+// The forward saves each row's o_i and Z_i and, from the same MFMAs (four more
+// rows of X^T), the two row sums the query gradient needs. The backward is then
+// left with column sums only (over rows, weighted by per-row coefficients that
+// depend on o_i and Z_i): it computes the exponent arguments with the forward's
+// product transposed (row records as the A operand, key fragments as B), which
+// hands every lane the e values of one key for 8 rows: the B operand with K
+// running over rows. No e_ij is stored or exchanged between lanes.
 // ---------------------------------------------------------------------------
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
@@ -399,21 +400,114 @@ __device__ __forceinline__ void key_range(const float (&k)[KPL], int r, int lane
     kmax = wave_max(hi);
 }
 
-// (c_i, m_i) = (q_i log2(e) / tau, -c_i k*_i) of rows il = 64 u + lane < 16 NT into
-// scm[il] (rows past r: c = m = 0; q holds zeros there): as floats, or, when every
-// c, m of rows il < nrows and every key fits f16 (returned, wave-uniform), as the
-// f16 record row_rec of the matrix-core path.
-template <int NT, int RPL>
-__device__ __forceinline__ bool put_row_consts(const float (&q)[RPL], int lane, int nrows, float inv_tau,
-                                               float kmin, float kmax, float2* scm) {
-    float c[RPL], m[RPL], big = fmaxf(fabsf(kmin), fabsf(kmax));
+// (c_i, m_i) = (q_i log2(e) / tau, -c_i k*_i) of rows 64 u + lane (rows past r hold
+// q = 0, so c = m = 0), and the largest |c|, |m| over rows below nrows together with
+// the key range (wave-uniform). The exponent arguments go through the matrix cores
+// when that maximum stays below ATT_F16_SAFE.
+template <int RPL>
+__device__ __forceinline__ float row_consts(const float (&q)[RPL], int lane, int nrows, float inv_tau, float kmin,
+                                            float kmax, float (&c)[RPL], float (&m)[RPL]) {
+    float big = fmaxf(fabsf(kmin), fabsf(kmax));
 #pragma unroll
     for (int u = 0; u < RPL; ++u) {
         c[u] = q[u] * (LOG2E * inv_tau);
         m[u] = -(c[u] * (c[u] >= 0.f ? kmax : kmin));
         if (64 * u + lane < nrows) big = fmaxf(big, fmaxf(fabsf(c[u]), fabsf(m[u])));
     }
-    const bool fast = wave_max(big) < ATT_F16_SAFE;  // false for NaN too
+    return wave_max(big);
+}
+
+// Largest of the W per-wave values in the sample's slots (each wave wrote slot[k] of
+// its own area at stride `stride` floats; slot0 is the first wave's area).
+template <int W>
+__device__ __forceinline__ float sample_max(const float* slot0, int stride, int k) {
+    float x = slot0[k];
+#pragma unroll
+    for (int w = 1; w < W; ++w) x = fmaxf(x, slot0[w * stride + k]);
+    return x;
+}
+
+// X^T of the forward: f16 hi + lo pairs of quantities summed against e, row stride
+// rpad. Quantity rows (the MFMA's M index): 0, 1: v / vs; 2: 1 for the real keys;
+// 3: zero (not stored); 4, 5: v k / vks; 6, 7: k / ks. Output lanes 0-15 get
+// (sum e v, sum e) for o and Z, lanes 16-31 the backward's row sums
+// W1 = sum_j e v_j k_j and W2 = sum_j e k_j, from the same MFMAs.
+constexpr int ATT_XROWS = 7;
+__device__ __forceinline__ int xrow(int n) { return n < 3 ? n : n - 1; }
+__device__ __forceinline__ f16x8_t xfrag_fwd(const _Float16* sx, int ld, int n, int j0, int g) {
+    if (n == 3 || n > 7) return f16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    return xfrag_perm(sx, ld, xrow(n), ATT_XROWS, j0, g);
+}
+
+// LDS of the forward. Per sample (shared by its W waves): keys, X^T. Per wave: row
+// constants and one slot for the range check.
+__host__ __device__ constexpr int attn_fwd_sample_floats(int rpad) { return rpad + ATT_XROWS * rpad / 2; }
+__host__ __device__ constexpr int attn_fwd_wave_floats() { return 2 * 16 * ATT_NT + 4; }
+__host__ __device__ constexpr int attn_fwd_block_floats(int rpad, int W) {
+    return (4 / W) * attn_fwd_sample_floats(rpad) + 4 * attn_fwd_wave_floats();
+}
+
+// NT: tiles computed per wave (a power of two >= the tiles it owns; the extra ones
+// are computed on harmless row constants and discarded).
+// KB: 256-key batches a lane's registers cover (4 KB >= rpad / 64).
+// stats: [o | Z | W1 | W2] per sample, row stride 4 r.
+template <typename T, int W, int NT, int KB>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_attn_fwd_mfma(int64_t B, int r, int rpad, float alpha, float beta,
+                                                      float inv_tau, const float* __restrict__ P, int64_t ldp,
+                                                      T* __restrict__ H, T* __restrict__ H2, int64_t ldh,
+                                                      float* __restrict__ stats) {
+    extern __shared__ __attribute__((aligned(16))) float smem[];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int ntile = rpad / 16;
+    const WaveRows wr = wave_rows(W, ntile);
+    const bool live = wr.b < B;
+    if (W == 1 && !live) return;  // with W > 1 every wave takes part in the barriers
+    float* sk = smem + (wave / W) * attn_fwd_sample_floats(rpad);  // [rpad] keys (shared by the sample's waves)
+    _Float16* sx = (_Float16*)(sk + rpad);                           // X^T (ATT_XROWS stored rows)
+    float* pw = smem + (4 / W) * attn_fwd_sample_floats(rpad);
+    float2* scm = (float2*)(pw + wave * attn_fwd_wave_floats());   // [16 ATT_NT] row constants
+    float* slot = pw + wave * attn_fwd_wave_floats() + 2 * 16 * ATT_NT;
+    const int64_t b = live ? wr.b : 0;
+    const float* pv = P + b * ldp;
+    constexpr int KPL = 4 * KB;
+    constexpr int RPL = RowsPerLane<NT>::value;
+    float kr[KPL], vr[KPL], qr[RPL];
+    load_keys<KPL>(pv, pv + 2 * r, r, lane, kr, vr);
+    load_rows<RPL>(pv + r, r, wr.t0, 16 * NT, lane, qr);
+    float kmin, kmax;
+    key_range<KPL>(kr, r, lane, kmin, kmax);
+    float vmax = 0.f, mvk = 0.f, mk = 0.f;
+#pragma unroll
+    for (int u = 0; u < KPL; ++u) {
+        vmax = fmaxf(vmax, fabsf(vr[u]));
+        mvk = fmaxf(mvk, fabsf(vr[u] * kr[u]));
+        mk = fmaxf(mk, fabsf(kr[u]));
+    }
+    // exact scalings: powers of two, identical in every wave of the sample (all see all keys)
+    const float vs = uniform_f(pow2_ceil(wave_max(vmax))), ivs = 1.0f / vs;
+    const float vks = uniform_f(pow2_ceil(wave_max(mvk))), ivks = 1.0f / vks;
+    const float ks = uniform_f(pow2_ceil(wave_max(mk))), iks = 1.0f / ks;
+    const int ldx = rpad;
+#pragma unroll
+    for (int u = 0; u < KPL; ++u) {
+        const int j = 64 * u + lane;
+        if (j < rpad && u % W == wr.w) {
+            sk[j] = kr[u];
+            put_pair(sx, ldx, 0, j, vr[u] * ivs);
+            sx[xoff(2, j, ldx)] = (_Float16)(j < r ? 1.f : 0.f);
+            put_pair(sx, ldx, xrow(4), j, vr[u] * kr[u] * ivks);
+            put_pair(sx, ldx, xrow(6), j, kr[u] * iks);
+        }
+    }
+    float c[RPL], m[RPL];
+    float big = row_consts<RPL>(qr, lane, 16 * wr.nt, inv_tau, kmin, kmax, c, m);
+    if (W > 1) {  // one decision per sample, as in the backward
+        if (lane == 0) slot[0] = big;
+        __syncthreads();
+        big = uniform_f(sample_max<W>(pw + (wave - wr.w) * attn_fwd_wave_floats() + 2 * 16 * ATT_NT,
+                                      attn_fwd_wave_floats(), 0));
+    }
+    const bool fast = big < ATT_F16_SAFE;  // false for NaN too
 #pragma unroll
     for (int u = 0; u < RPL; ++u) {
         const int il = 64 * u + lane;
@@ -422,52 +516,8 @@ __device__ __forceinline__ bool put_row_consts(const float (&q)[RPL], int lane, 
             else scm[il] = make_float2(c[u], m[u]);
         }
     }
-    return fast;
-}
-
-// LDS words per wave of the forward: keys, row constants, X^T (3 rows).
-__host__ __device__ constexpr int attn_fwd_wave_floats(int rpad) { return rpad + 2 * 16 * ATT_NT + 3 * rpad / 2; }
-
-// NT: tiles computed per wave (a power of two >= the tiles it owns; the extra ones
-// are computed on harmless row constants and discarded).
-// KB: 256-key batches a lane's registers cover (4 KB >= rpad / 64).
-template <typename T, int NT, int KB>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_attn_fwd_mfma(int64_t B, int r, int rpad, int W, float alpha, float beta,
-                                                      float inv_tau, const float* __restrict__ P, int64_t ldp,
-                                                      T* __restrict__ H, T* __restrict__ H2, int64_t ldh,
-                                                      float* __restrict__ stats) {
-    extern __shared__ __attribute__((aligned(16))) float smem[];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int ntile = rpad / 16;
-    const WaveRows wr = wave_rows(W, ntile);
-    if (wr.b >= B) return;
-    float* sk = smem + wave * attn_fwd_wave_floats(rpad);  // [rpad] keys
-    float2* scm = (float2*)(sk + rpad);                       // [16 ATT_NT] row constants
-    _Float16* sx = (_Float16*)(scm + 16 * ATT_NT);            // X^T: 3 rows x rpad (v hi, v lo, 1)
-    const float* pv = P + wr.b * ldp;
-    constexpr int KPL = 4 * KB;
-    constexpr int RPL = RowsPerLane<NT>::value;
-    float kr[KPL], vr[KPL], qr[RPL];
-    load_keys<KPL>(pv, pv + 2 * r, r, lane, kr, vr);
-    load_rows<RPL>(pv + r, r, wr.t0, 16 * NT, lane, qr);
-    float kmin, kmax;
-    key_range<KPL>(kr, r, lane, kmin, kmax);
-    float vmax = 0.f;
-#pragma unroll
-    for (int u = 0; u < KPL; ++u) vmax = fmaxf(vmax, fabsf(vr[u]));
-    const float vs = uniform_f(pow2_ceil(wave_max(vmax))), ivs = 1.0f / vs;  // exact: vs is a power of two
-    const int ldx = rpad;
-#pragma unroll
-    for (int u = 0; u < KPL; ++u) {
-        const int j = 64 * u + lane;
-        if (j < rpad) {
-            sk[j] = kr[u];
-            put_pair(sx, ldx, 0, j, vr[u] * ivs);
-            sx[xoff(2, j, ldx)] = (_Float16)(j < r ? 1.f : 0.f);
-        }
-    }
-    const bool fast = put_row_consts<NT, RPL>(qr, lane, 16 * wr.nt, inv_tau, kmin, kmax, scm);
-    __builtin_amdgcn_wave_barrier();
+    if (W > 1) __syncthreads();
+    else __builtin_amdgcn_wave_barrier();
     const int g = lane >> 4, n = lane & 15;
     f32x4_t acc[NT];
 #pragma unroll
@@ -483,7 +533,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             } else {
                 keys_perm(sk, j0, g, kv);
             }
-            const f16x8_t a = xfrag_perm(sx, ldx, n, 3, j0, g);
+            const f16x8_t a = xfrag_fwd(sx, ldx, n, j0, g);
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
                 u32x4_t e;
@@ -499,60 +549,54 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     };
     if (fast) chunks(std::true_type{});
     else chunks(std::false_type{});
-    if (lane < 16) {
-        float* so = stats + wr.b * 2 * (int64_t)r;
+    if (live && lane < 32) {
+        // lanes 0-15: (sum e v, sum e) of row n -> h, o, Z; lanes 16-31: (W1, W2) of row n
+        float* so = stats + b * 4 * (int64_t)r;
+        const bool lo = lane < 16;
         float vi[NT];
 #pragma unroll
         for (int t = 0; t < NT; ++t) {  // all loads first
-            const int i = (wr.t0 + t) * 16 + lane;
+            const int i = (wr.t0 + t) * 16 + n;
             vi[t] = pv[i < r ? i : r - 1];
         }
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            const int i = (wr.t0 + t) * 16 + lane;
+            const int i = (wr.t0 + t) * 16 + n;
             if (t < wr.nt && i < r) {
-                const float z = acc[t].z;
-                const float o = (acc[t].x + acc[t].y) * vs * __builtin_amdgcn_rcpf(z);
-                const float hv = beta * vi[t] + alpha * o;
-                st<T>::store(H + wr.b * ldh + i, hv);
-                if (H2) st<T>::store(H2 + wr.b * ldh + i, hv - st<T>::round(hv));
-                so[i] = o;
-                so[r + i] = z;
+                const float s01 = acc[t].x + acc[t].y, z = acc[t].z;
+                const float o = s01 * vs * __builtin_amdgcn_rcpf(z);
+                if (lo) {
+                    const float hv = beta * vi[t] + alpha * o;
+                    st<T>::store(H + b * ldh + i, hv);
+                    if (H2) st<T>::store(H2 + b * ldh + i, hv - st<T>::round(hv));
+                }
+                so[(lo ? 0 : 2 * r) + i] = lo ? o : s01 * vks;
+                so[(lo ? r : 3 * r) + i] = lo ? z : (z + acc[t].w) * ks;
             }
         }
     }
 }
 
-// LDS of the backward. Per sample (shared by its W waves): keys and X^T (4 rows).
-// Per wave: row constants, Y^T (6 rows of the wave's rows), one 32 x 32 f16 block
-// of e, and (W > 1) two column-partial slots.
-__host__ __device__ constexpr int attn_bwd_sample_floats(int rpad) { return 3 * rpad; }
-__host__ __device__ constexpr int attn_bwd_slot_offset() { return 2 * 16 * ATT_NT + 3 * (16 * ATT_NT) + 512; }
-__host__ __device__ constexpr int attn_bwd_wave_floats(int W) { return attn_bwd_slot_offset() + (W > 1 ? 2 * 96 : 0); }
+// LDS of the backward, per sample (shared by its W waves): keys, row constants (8
+// bytes per row), Y^T (6 rows of f16, row stride rpad); per wave four slots for the
+// range check and the three scales.
+__host__ __device__ constexpr int attn_bwd_sample_floats(int rpad) { return rpad + 2 * rpad + 3 * rpad; }
+__host__ __device__ constexpr int attn_bwd_wave_floats() { return 4; }
 __host__ __device__ constexpr int attn_bwd_block_floats(int rpad, int W) {
-    return (4 / W) * attn_bwd_sample_floats(rpad) + 4 * attn_bwd_wave_floats(W);
+    return (4 / W) * attn_bwd_sample_floats(rpad) + 4 * attn_bwd_wave_floats();
 }
 
-// ds_read_b64_tr_b16 of the e block: lane (g, i) receives e[8 g + t][16 h + i]
-// for t = 0..7 (rows t < 4 from the first read, t >= 4 from the second). Block
-// rows hold 32 keys as four 16-byte chunks, chunk index XOR ((row >> 2) & 3).
-__device__ __forceinline__ f16x8_t e_transposed(const _Float16* se, int h, int lane) {
-    const int g = lane >> 4, i = lane & 15;
-    const int chunk = 2 * h + ((i & 3) >> 1);
-    const int r0 = 8 * g + (i >> 2), r1 = r0 + 4;
-    const int o0 = r0 * 32 + ((chunk ^ ((r0 >> 2) & 3)) * 8) + 4 * (i & 1);
-    const int o1 = r1 * 32 + ((chunk ^ ((r1 >> 2) & 3)) * 8) + 4 * (i & 1);
-    const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4_t*)(se + o0));
-    const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS s16x4_t*)(se + o1));
-    const s16x8_t v = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-    return __builtin_bit_cast(f16x8_t, v);
-}
-
-// Backward. Row sums W1_i = sum_j e v_j k_j, W2_i = sum_j e k_j give
-// dq_i = go_i / (Z_i tau) (W1_i - o_i W2_i); column sums C1_j = sum_i e a_i,
-// C2_j = sum_i e a_i o_i, C3_j = sum_i e go_i / Z_i with a_i = go_i q_i / (Z_i tau)
-// give dk_j = v_j C1_j - C2_j and dv_j = beta gh_j + C3_j (go = alpha gh).
-template <typename T, int W, int NT>
+// Backward. With the forward's row sums W1 and W2, dq_i = go_i / (Z_i tau) (W1_i - o_i W2_i)
+// needs no exponentials. The column sums C1_j = sum_i e_ij a_i, C2_j = sum_i e_ij a_i o_i,
+// C3_j = sum_i e_ij go_i / Z_i (a_i = go_i q_i / (Z_i tau)) give dk_j = v_j C1_j - C2_j and
+// dv_j = beta gh_j + C3_j (go = alpha gh). They run on the matrix cores with K over rows:
+// the exponent arguments come out of v_mfma_f32_16x16x16_f16 with the row records as A
+// and the key fragments as B (the forward's product with its operands swapped, so each
+// e_ij is computed exactly as in the forward), which leaves lane (g, n) holding e of
+// key n for rows 4 g .. +3 and 16 + 4 g .. +3 of a 32-row block: the B operand of
+// v_mfma_f32_16x16x32_f16 against Y^T (rows: a hi, a lo, a o hi, a o lo, go/Z hi, lo).
+// A sample's waves split its keys (32 at a time); every wave runs over all rows.
+template <typename T, int W, int KB>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_attn_bwd_mfma(int64_t B, int r, int rpad, float alpha, float beta,
                                                       float inv_tau, const float* __restrict__ P, int64_t ldp,
                                                       const float* __restrict__ stats,
@@ -560,208 +604,190 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                                                       T* __restrict__ GP, int64_t ldgp) {
     extern __shared__ __attribute__((aligned(16))) float smem[];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int ntile = rpad / 16;
-    const WaveRows wr = wave_rows(W, ntile);
-    const bool live = wr.b < B;
+    const int64_t gw = (int64_t)blockIdx.x * 4 + wave;
+    const int64_t bsm = gw / W;
+    const int w = __builtin_amdgcn_readfirstlane((int)(gw - bsm * W));
+    const bool live = bsm < B;
     if (W == 1 && !live) return;  // with W > 1 every wave takes part in the barriers
-    constexpr int RW = 16 * ATT_NT;
-    float* sk = smem + (wave / W) * attn_bwd_sample_floats(rpad);  // [rpad] keys (shared by the sample's waves)
-    _Float16* sx = (_Float16*)(sk + rpad);                           // 4 rows: v k hi/lo, k hi/lo
-    float* pw = smem + (4 / W) * attn_bwd_sample_floats(rpad) + wave * attn_bwd_wave_floats(W);
-    float2* scm = (float2*)pw;                   // [RW] row constants
-    _Float16* sy = (_Float16*)(scm + RW);        // 6 rows: a hi/lo, a o hi/lo, go/Z hi/lo
-    _Float16* se = sy + 6 * RW;                  // 32 x 32 e block
-    const int ldx = rpad, ldy = RW;
-    float* slot = pw + attn_bwd_slot_offset();   // 2 x 96 column partials (W > 1)
-    const int g = lane >> 4, n = lane & 15;
-    const int64_t b = live ? wr.b : 0;
+    const int64_t b = live ? bsm : 0;
+    float* sk = smem + (wave / W) * attn_bwd_sample_floats(rpad);  // [rpad] keys
+    float2* scm = (float2*)(sk + rpad);                              // [rpad] row constants
+    _Float16* sy = (_Float16*)(scm + rpad);                          // Y^T, 6 rows
+    float* slots = smem + (4 / W) * attn_bwd_sample_floats(rpad);
+    float* slot = slots + wave * attn_bwd_wave_floats();
+    const int ldy = rpad;
     const float* pv = P + b * ldp;
     const float* pq = pv + r;
     const float* pk = pv + 2 * r;
     const float* gh = GH + b * ldg;
-    const float* so = stats + b * 2 * (int64_t)r;
-    constexpr int KPL = W == 1 ? 4 : 16;
-    constexpr int RPL = RowsPerLane<NT>::value;
-    float kr[KPL], vr[KPL], qr[RPL], ghr[RPL], orr[RPL], zr[RPL];
-    load_keys<KPL>(pv, pk, r, lane, kr, vr);
-    load_rows<RPL>(pq, r, wr.t0, 16 * wr.nt, lane, qr);
-    load_rows<RPL>(gh, r, wr.t0, 16 * wr.nt, lane, ghr);
-    load_rows<RPL>(so, r, wr.t0, 16 * wr.nt, lane, orr);
-    load_rows<RPL>(so + r, r, wr.t0, 16 * wr.nt, lane, zr);
-    // every wave reduces over all keys; each writes its share of the sample's key arrays
-    float kmin, kmax;
-    key_range<KPL>(kr, r, lane, kmin, kmax);
-    float mvk = 0.f, mk = 0.f;
-#pragma unroll
-    for (int u = 0; u < KPL; ++u) {
-        mvk = fmaxf(mvk, fabsf(vr[u] * kr[u]));
-        mk = fmaxf(mk, fabsf(kr[u]));
-    }
-    const float vks = uniform_f(pow2_ceil(wave_max(mvk))), ks = uniform_f(pow2_ceil(wave_max(mk)));
-    const float ivks = 1.0f / vks, iks = 1.0f / ks;  // exact: powers of two
+    const float* so = stats + b * 4 * (int64_t)r;
+    constexpr int KPL = 4 * KB;      // keys (and rows) per lane: 64 KPL >= rpad
+    constexpr int RPW = KPL / W;     // rows per lane of this wave's share: 64 (s W + w) + lane
+    float kr[KPL];
 #pragma unroll
     for (int u = 0; u < KPL; ++u) {
         const int j = 64 * u + lane;
-        if (j < rpad && u % W == wr.w) {
-            sk[j] = kr[u];
-            put_pair(sx, ldx, 0, j, vr[u] * kr[u] * ivks);
-            put_pair(sx, ldx, 2, j, kr[u] * iks);
-        }
+        kr[u] = pk[j < r ? j : r - 1];
     }
-    // per-row coefficients of the wave's rows (zero past its rows)
-    float ca[RPL], cb[RPL], cg[RPL];
-    float ma = 0.f, mb = 0.f, mc = 0.f;
 #pragma unroll
-    for (int u = 0; u < RPL; ++u) {
-        const float go = alpha * ghr[u], rz = zr[u] != 0.f ? __builtin_amdgcn_rcpf(zr[u]) : 0.f;
-        ca[u] = go * qr[u] * rz * inv_tau;
-        cb[u] = ca[u] * orr[u];
-        cg[u] = go * rz;
-        ma = fmaxf(ma, fabsf(ca[u]));
-        mb = fmaxf(mb, fabsf(cb[u]));
-        mc = fmaxf(mc, fabsf(cg[u]));
+    for (int u = 0; u < KPL; ++u)
+        if (64 * u + lane >= r) kr[u] = 0.f;
+    float kmin, kmax;
+    key_range<KPL>(kr, r, lane, kmin, kmax);
+    // this wave's rows: the forward's statistics, dq, and the column-sum coefficients
+    float qr[RPW], ghr[RPW], orr[RPW], zr[RPW], w1[RPW], w2[RPW];
+#pragma unroll
+    for (int s = 0; s < RPW; ++s) {
+        const int i = 64 * (s * W + w) + lane, ic = i < r ? i : r - 1;
+        qr[s] = pq[ic];
+        ghr[s] = gh[ic];
+        orr[s] = so[ic];
+        zr[s] = so[r + ic];
+        w1[s] = so[2 * r + ic];
+        w2[s] = so[3 * r + ic];
     }
-    const float as = uniform_f(pow2_ceil(wave_max(ma))), bs = uniform_f(pow2_ceil(wave_max(mb)));
-    const float cs = uniform_f(pow2_ceil(wave_max(mc)));
+    float ca[RPW], cb[RPW], cg[RPW], c[RPW], m[RPW];
+    float big = fmaxf(fabsf(kmin), fabsf(kmax)), ma = 0.f, mb = 0.f, mc = 0.f;
+#pragma unroll
+    for (int s = 0; s < RPW; ++s) {
+        const int i = 64 * (s * W + w) + lane;
+        const bool ok = i < r;
+        const float q = ok ? qr[s] : 0.f, go = ok ? alpha * ghr[s] : 0.f;
+        const float rz = ok && zr[s] != 0.f ? __builtin_amdgcn_rcpf(zr[s]) : 0.f;
+        if (live && ok) st<T>::store(GP + b * ldgp + r + i, go * rz * inv_tau * (w1[s] - orr[s] * w2[s]));
+        ca[s] = go * q * rz * inv_tau;
+        cb[s] = ca[s] * orr[s];
+        cg[s] = go * rz;
+        c[s] = q * (LOG2E * inv_tau);
+        m[s] = -(c[s] * (c[s] >= 0.f ? kmax : kmin));
+        if (ok) big = fmaxf(big, fmaxf(fabsf(c[s]), fabsf(m[s])));
+        ma = fmaxf(ma, fabsf(ca[s]));
+        mb = fmaxf(mb, fabsf(cb[s]));
+        mc = fmaxf(mc, fabsf(cg[s]));
+    }
+    big = wave_max(big);
+    ma = wave_max(ma);
+    mb = wave_max(mb);
+    mc = wave_max(mc);
+    if (W > 1) {  // maxima over the sample's rows
+        if (lane == 0) {
+            slot[0] = big;
+            slot[1] = ma;
+            slot[2] = mb;
+            slot[3] = mc;
+        }
+        __syncthreads();
+        const float* s0 = slots + (wave - w) * attn_bwd_wave_floats();
+        big = sample_max<W>(s0, attn_bwd_wave_floats(), 0);
+        ma = sample_max<W>(s0, attn_bwd_wave_floats(), 1);
+        mb = sample_max<W>(s0, attn_bwd_wave_floats(), 2);
+        mc = sample_max<W>(s0, attn_bwd_wave_floats(), 3);
+    }
+    const bool fast = uniform_f(big) < ATT_F16_SAFE;  // the forward's decision (false for NaN too)
+    const float as = uniform_f(pow2_ceil(ma)), bs = uniform_f(pow2_ceil(mb)), cs = uniform_f(pow2_ceil(mc));
     const float ias = 1.0f / as, ibs = 1.0f / bs, ics = 1.0f / cs;  // exact: powers of two
 #pragma unroll
-    for (int u = 0; u < RPL; ++u) {
-        const int il = 64 * u + lane;
-        if (il < 16 * NT) {
-            put_pair(sy, ldy, 0, il, ca[u] * ias);
-            put_pair(sy, ldy, 2, il, cb[u] * ibs);
-            put_pair(sy, ldy, 4, il, cg[u] * ics);
+    for (int u = 0; u < KPL; ++u) {
+        const int j = 64 * u + lane;
+        if (j < rpad && u % W == w) sk[j] = kr[u];
+    }
+#pragma unroll
+    for (int s = 0; s < RPW; ++s) {
+        const int i = 64 * (s * W + w) + lane;
+        if (i < rpad) {
+            if (fast) *(f16x4_t*)(scm + i) = row_rec(c[s], m[s]);
+            else scm[i] = make_float2(c[s], m[s]);
+            put_pair(sy, ldy, 0, i, ca[s] * ias);
+            put_pair(sy, ldy, 2, i, cb[s] * ibs);
+            put_pair(sy, ldy, 4, i, cg[s] * ics);
         }
     }
-    // row constants from q (load_rows zeroed q past the wave's rows; rows of
-    // other waves only feed discarded tiles)
-    const bool fast = put_row_consts<NT, RPL>(qr, lane, 16 * wr.nt, inv_tau, kmin, kmax, scm);
     if (W > 1) __syncthreads();
     else __builtin_amdgcn_wave_barrier();
+    if (!live) return;
 
-    f32x4_t acc[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    auto chunks = [&](auto fast_c) {
+    const int g = lane >> 4, n = lane & 15;
+    auto keys = [&](auto fast_c) {
         constexpr bool FAST = decltype(fast_c)::value;
-        for (int chunk = 0, j0 = 0; j0 < rpad; j0 += 32, ++chunk) {
-            float kv[8];
-            f16x4_t k0, k1;
+        for (int j0 = 32 * w; j0 < rpad; j0 += 32 * W) {
+            // keys j0 + n and j0 + 16 + n of this lane; their epilogue operands, loaded now
+            f16x4_t kf0, kf1;
+            float kv0 = 0.f, kv1 = 0.f;
             if (FAST) {
-                k0 = key_frag(sk[j0 + n], g);
-                k1 = key_frag(sk[j0 + 16 + n], g);
+                kf0 = key_frag(sk[j0 + n], g);
+                kf1 = key_frag(sk[j0 + 16 + n], g);
             } else {
-                keys_perm(sk, j0, g, kv);
+                kv0 = sk[j0 + n];
+                kv1 = sk[j0 + 16 + n];
             }
-            const f16x8_t ax = xfrag_perm(sx, ldx, n, 4, j0, g);
-            // operands of this chunk's column epilogue, loaded now so the loads overlap the chunk
             float ev[2], eg[2];
-    #pragma unroll
+#pragma unroll
             for (int h = 0; h < 2; ++h) {
-                const int j = W == 1 ? j0 + 16 * h + n : j0 + (lane & 31);
-                const int jc = j < r ? j : r - 1;
+                const int j = j0 + 16 * h + n, jc = j < r ? j : r - 1;
                 ev[h] = pv[jc];
                 eg[h] = gh[jc];
             }
-            f32x4_t col[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
-    #pragma unroll
-            for (int p = 0; p < NT / 2; ++p) {
-                // the wave's LDS operations run in order, so this pair's writes follow
-                // the previous pair's transposed reads of the same block
-                __builtin_amdgcn_wave_barrier();
-    #pragma unroll
-                for (int q = 0; q < 2; ++q) {
-                    const int t = 2 * p + q;
-                    u32x4_t e;
-                    if (FAST) {
-                        e = efrag_mfma(k0, k1, *(const f16x4_t*)(scm + 16 * t + n));
-                    } else {
-                        const float2 cm = scm[16 * t + n];
-                        e = efrag(cm.x, cm.y, kv);
+            f32x4_t col0 = {0.f, 0.f, 0.f, 0.f}, col1 = {0.f, 0.f, 0.f, 0.f};
+            for (int i0 = 0; i0 < rpad; i0 += 32) {
+                const f16x8_t ay = xfrag_perm(sy, ldy, n, 6, i0, g);
+                u32x4_t e0, e1;
+                if (FAST) {
+                    const f16x4_t ra = *(const f16x4_t*)(scm + i0 + n);
+                    const f16x4_t rb = *(const f16x4_t*)(scm + i0 + 16 + n);
+                    const f32x4_t z = {0.f, 0.f, 0.f, 0.f};
+                    const f32x4_t x00 = __builtin_amdgcn_mfma_f32_16x16x16f16(ra, kf0, z, 0, 0, 0);
+                    const f32x4_t x01 = __builtin_amdgcn_mfma_f32_16x16x16f16(rb, kf0, z, 0, 0, 0);
+                    const f32x4_t x10 = __builtin_amdgcn_mfma_f32_16x16x16f16(ra, kf1, z, 0, 0, 0);
+                    const f32x4_t x11 = __builtin_amdgcn_mfma_f32_16x16x16f16(rb, kf1, z, 0, 0, 0);
+                    float e[8], f[8];
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        e[t] = __builtin_amdgcn_exp2f(x00[t]);
+                        e[4 + t] = __builtin_amdgcn_exp2f(x01[t]);
+                        f[t] = __builtin_amdgcn_exp2f(x10[t]);
+                        f[4 + t] = __builtin_amdgcn_exp2f(x11[t]);
                     }
-                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ax, __builtin_bit_cast(f16x8_t, e), acc[t], 0, 0, 0);
-                    // keys 4 g .. +3 and 16 + 4 g .. +3 of row 16 q + n, into their block chunks
-                    const int row = 16 * q + n, sw = (row >> 2) & 3;
-                    typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-                    *(u32x2_t*)(se + row * 32 + (((g >> 1) ^ sw) * 8) + 4 * (g & 1)) = u32x2_t{e.x, e.y};
-                    *(u32x2_t*)(se + row * 32 + (((2 + (g >> 1)) ^ sw) * 8) + 4 * (g & 1)) = u32x2_t{e.z, e.w};
+                    e0 = pack_e(e);
+                    e1 = pack_e(f);
+                } else {
+                    // rows i0 + 4 g + t and i0 + 16 + 4 g + t (t < 4) of this lane's keys
+                    float2 cm[8];
+                    *(f32x4_t*)&cm[0] = *(const f32x4_t*)(scm + i0 + 4 * g);
+                    *(f32x4_t*)&cm[2] = *(const f32x4_t*)(scm + i0 + 4 * g + 2);
+                    *(f32x4_t*)&cm[4] = *(const f32x4_t*)(scm + i0 + 16 + 4 * g);
+                    *(f32x4_t*)&cm[6] = *(const f32x4_t*)(scm + i0 + 16 + 4 * g + 2);
+                    float e[8], f[8];
+#pragma unroll
+                    for (int t = 0; t < 8; ++t) {
+                        e[t] = __builtin_amdgcn_exp2f(fmaf(cm[t].x, kv0, cm[t].y));
+                        f[t] = __builtin_amdgcn_exp2f(fmaf(cm[t].x, kv1, cm[t].y));
+                    }
+                    e0 = pack_e(e);
+                    e1 = pack_e(f);
                 }
-                const f16x8_t ay = xfrag(sy, ldy, n, 6, 32 * p + 8 * g);
-    #pragma unroll
-                for (int h = 0; h < 2; ++h)
-                    col[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ay, e_transposed(se, h, lane), col[h], 0, 0, 0);
+                col0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ay, __builtin_bit_cast(f16x8_t, e0), col0, 0, 0, 0);
+                col1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ay, __builtin_bit_cast(f16x8_t, e1), col1, 0, 0, 0);
             }
             // lanes 0..15: (a hi, a lo, a o hi, a o lo) of key n (+16 h); lanes 16..31: (go/Z hi, lo)
-            if (W == 1) {
-                if (lane < 32) {
-    #pragma unroll
-                    for (int h = 0; h < 2; ++h) {
-                        const int j = j0 + 16 * h + n;
-                        if (j < r) {
-                            if (lane < 16) {
-                                const float c1 = (col[h].x + col[h].y) * as, c2 = (col[h].z + col[h].w) * bs;
-                                st<T>::store(GP + b * ldgp + 2 * r + j, ev[h] * c1 - c2);
-                            } else {
-                                st<T>::store(GP + b * ldgp + j, beta * eg[h] + (col[h].x + col[h].y) * cs);
-                            }
-                        }
-                    }
-                }
-            } else {
-                float* sl = slot + (chunk & 1) * 96;
-                if (lane < 32) {
-    #pragma unroll
-                    for (int h = 0; h < 2; ++h) {
-                        if (lane < 16) {
-                            sl[16 * h + n] = (col[h].x + col[h].y) * as;
-                            sl[32 + 16 * h + n] = (col[h].z + col[h].w) * bs;
-                        } else {
-                            sl[64 + 16 * h + n] = (col[h].x + col[h].y) * cs;
-                        }
-                    }
-                }
-                __syncthreads();
-                // the sample's first wave adds the W partials in wave order
-                if (live && wr.w == 0 && lane < 32) {
-                    const int j = j0 + lane;
-                    float c1 = 0.f, c2 = 0.f, c3 = 0.f;
-    #pragma unroll
-                    for (int w = 0; w < W; ++w) {
-                        const float* so2 = smem + (4 / W) * attn_bwd_sample_floats(rpad) +
-                                           (wave + w) * attn_bwd_wave_floats(W) + attn_bwd_slot_offset() + (chunk & 1) * 96;
-                        c1 += so2[lane];
-                        c2 += so2[32 + lane];
-                        c3 += so2[64 + lane];
-                    }
+            if (lane < 32) {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const f32x4_t col = h ? col1 : col0;
+                    const int j = j0 + 16 * h + n;
                     if (j < r) {
-                        st<T>::store(GP + b * ldgp + 2 * r + j, ev[0] * c1 - c2);
-                        st<T>::store(GP + b * ldgp + j, beta * eg[0] + c3);
+                        if (lane < 16) {
+                            const float c1 = (col.x + col.y) * as, c2 = (col.z + col.w) * bs;
+                            st<T>::store(GP + b * ldgp + 2 * r + j, ev[h] * c1 - c2);
+                        } else {
+                            st<T>::store(GP + b * ldgp + j, beta * eg[h] + (col.x + col.y) * cs);
+                        }
                     }
                 }
             }
         }
     };
-    if (fast) chunks(std::true_type{});
-    else chunks(std::false_type{});
-    if (live && lane < 16) {
-        float gi[NT], oi[NT], zi[NT];
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {  // all loads first
-            const int i = (wr.t0 + t) * 16 + lane, ic = i < r ? i : r - 1;
-            gi[t] = gh[ic];
-            oi[t] = so[ic];
-            zi[t] = so[r + ic];
-        }
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const int i = (wr.t0 + t) * 16 + lane;
-            if (t < wr.nt && i < r) {
-                const float w1 = (acc[t].x + acc[t].y) * vks, w2 = (acc[t].z + acc[t].w) * ks;
-                const float go = alpha * gi[t], rz = __builtin_amdgcn_rcpf(zi[t]);
-                st<T>::store(GP + b * ldgp + r + i, go * rz * inv_tau * (w1 - oi[t] * w2));
-            }
-        }
-    }
+    if (fast) keys(std::true_type{});
+    else keys(std::false_type{});
 }
 
 int attn_threads(int r) {
@@ -794,15 +820,20 @@ hipError_t launch_attn_fwd(int64_t B, int r, float alpha, float beta, float tau,
         const int W = attn_waves(rpad);
         const int NT = attn_tiles(rpad, W);
         const int64_t blocks = (B * W + 3) / 4;
-        const size_t lds = 4 * sizeof(float) * (size_t)attn_fwd_wave_floats(rpad);
-#define RDCN_AFWD(NTV, KBV)                                                                                          \
-    hipLaunchKernelGGL((k_attn_fwd_mfma<bf16_t, NTV, KBV>), dim3((unsigned)blocks), dim3(256), lds, s, B, r, rpad, W, \
+        const size_t lds = sizeof(float) * (size_t)attn_fwd_block_floats(rpad, W);
+#define RDCN_AFWD(WV, NTV, KBV)                                                                                     \
+    hipLaunchKernelGGL((k_attn_fwd_mfma<bf16_t, WV, NTV, KBV>), dim3((unsigned)blocks), dim3(256), lds, s, B, r, rpad, \
                        alpha, beta, 1.0f / tau, (const float*)P, ldp, (bf16_t*)H, (bf16_t*)H2, ldh, stats)
-        if (NT == 2) RDCN_AFWD(2, 1);
-        else if (NT == 4) RDCN_AFWD(4, 1);
-        else if (NT == 8) RDCN_AFWD(8, 1);
-        else if (W == 1) RDCN_AFWD(16, 1);
-        else RDCN_AFWD(16, 4);
+        if (W == 1) {
+            if (NT == 2) RDCN_AFWD(1, 2, 1);
+            else if (NT == 4) RDCN_AFWD(1, 4, 1);
+            else if (NT == 8) RDCN_AFWD(1, 8, 1);
+            else RDCN_AFWD(1, 16, 1);
+        } else if (W == 2) {
+            RDCN_AFWD(2, 16, 4);
+        } else {
+            RDCN_AFWD(4, 16, 4);
+        }
 #undef RDCN_AFWD
         return hipGetLastError();
     }
@@ -821,24 +852,14 @@ hipError_t launch_attn_bwd(int64_t B, int r, float alpha, float beta, float tau,
         if (r > 4 * 16 * ATT_NT || !stats) return hipErrorInvalidValue;
         const int rpad = (r + 31) / 32 * 32;
         const int W = attn_waves(rpad);
-        const int NT = attn_tiles(rpad, W);
         const int64_t blocks = (B * W + 3) / 4;
         const size_t lds = sizeof(float) * (size_t)attn_bwd_block_floats(rpad, W);
-#define RDCN_ABWD(WV, NTV)                                                                                          \
-    hipLaunchKernelGGL((k_attn_bwd_mfma<bf16_t, WV, NTV>), dim3((unsigned)blocks), dim3(256), lds, s, B, r, rpad,     \
+#define RDCN_ABWD(WV, KBV)                                                                                          \
+    hipLaunchKernelGGL((k_attn_bwd_mfma<bf16_t, WV, KBV>), dim3((unsigned)blocks), dim3(256), lds, s, B, r, rpad,     \
                        alpha, beta, 1.0f / tau, (const float*)P, ldp, stats, GH, ldg, (bf16_t*)GP, ldgp)
-        if (W == 1) {
-            if (NT == 2) RDCN_ABWD(1, 2);
-            else if (NT == 4) RDCN_ABWD(1, 4);
-            else if (NT == 8) RDCN_ABWD(1, 8);
-            else RDCN_ABWD(1, 16);
-        } else if (W == 2) {
-            if (NT == 8) RDCN_ABWD(2, 8);
-            else RDCN_ABWD(2, 16);
-        } else {
-            if (NT == 8) RDCN_ABWD(4, 8);
-            else RDCN_ABWD(4, 16);
-        }
+        if (W == 1) RDCN_ABWD(1, 1);
+        else if (W == 2) RDCN_ABWD(2, 4);
+        else RDCN_ABWD(4, 4);
 #undef RDCN_ABWD
         return hipGetLastError();
     }

@@ -36,8 +36,9 @@ hipError_t launch_quantize_rows(int64_t rows, int D, const void* tables, int8_t*
 
 namespace rdcn {
 
-// bf16 storage: the forward writes o_i and Z_i of every row to stats ([o | Z] per
-// sample, row stride 2 r) and the backward reads them back.
+// bf16 storage: the forward writes o_i, Z_i and the row sums W1_i = sum_j e_ij v_j k_j,
+// W2_i = sum_j e_ij k_j of every row to stats ([o | Z | W1 | W2] per sample, row
+// stride 4 r) and the backward reads them back.
 hipError_t launch_attn_fwd(int64_t B, int r, float alpha, float beta, float tau, const void* P, int64_t ldp, void* H,
                            void* H2, int64_t ldh, float* stats, bool bf16, hipStream_t s);
 hipError_t launch_attn_bwd(int64_t B, int r, float alpha, float beta, float tau, const void* P, int64_t ldp,
