@@ -203,6 +203,9 @@ typedef short s16x8_t __attribute__((ext_vector_type(8)));
 #define LDS_AS __attribute__((address_space(3)))
 
 constexpr int ATT_NT = 16;  // 16-row tiles per wave
+// 16-key tiles the backward carries through one pass over a sample's rows (four:
+// the row records and Y^T fragment read per 32-row block serve 64 keys; eight spill)
+constexpr int ATT_BWD_KT = 4;
 
 __device__ __forceinline__ uint32_t pk_f16(float a, float b) {
     const f16x2_t v = {(_Float16)a, (_Float16)b};
@@ -595,7 +598,7 @@ __host__ __device__ constexpr int attn_bwd_block_floats(int rpad, int W) {
 // e_ij is computed exactly as in the forward), which leaves lane (g, n) holding e of
 // key n for rows 4 g .. +3 and 16 + 4 g .. +3 of a 32-row block: the B operand of
 // v_mfma_f32_16x16x32_f16 against Y^T (rows: a hi, a lo, a o hi, a o lo, go/Z hi, lo).
-// A sample's waves split its keys (32 at a time); every wave runs over all rows.
+// A sample's waves split its keys (16 ATT_BWD_KT at a time); every wave runs over all rows.
 template <typename T, int W, int KB>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_attn_bwd_mfma(int64_t B, int r, int rpad, float alpha, float beta,
                                                       float inv_tau, const float* __restrict__ P, int64_t ldp,
@@ -707,48 +710,48 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     if (!live) return;
 
     const int g = lane >> 4, n = lane & 15;
+    constexpr int KT = ATT_BWD_KT;
     auto keys = [&](auto fast_c) {
         constexpr bool FAST = decltype(fast_c)::value;
-        for (int j0 = 32 * w; j0 < rpad; j0 += 32 * W) {
-            // keys j0 + n and j0 + 16 + n of this lane; their epilogue operands, loaded now
-            f16x4_t kf0, kf1;
-            float kv0 = 0.f, kv1 = 0.f;
-            if (FAST) {
-                kf0 = key_frag(sk[j0 + n], g);
-                kf1 = key_frag(sk[j0 + 16 + n], g);
-            } else {
-                kv0 = sk[j0 + n];
-                kv1 = sk[j0 + 16 + n];
-            }
-            float ev[2], eg[2];
+        for (int j0 = 16 * KT * w; j0 < rpad; j0 += 16 * KT * W) {
+            // keys j0 + 16 q + n of this lane (q < KT; past rpad the last key stands in and
+            // nothing is stored); their epilogue operands, loaded now
+            f16x4_t kf[KT];
+            float kv[KT], ev[KT], eg[KT];
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int j = j0 + 16 * h + n, jc = j < r ? j : r - 1;
-                ev[h] = pv[jc];
-                eg[h] = gh[jc];
+            for (int q = 0; q < KT; ++q) {
+                const int j = j0 + 16 * q + n, jp = j < rpad ? j : rpad - 1, jc = j < r ? j : r - 1;
+                kv[q] = sk[jp];
+                if (FAST) kf[q] = key_frag(kv[q], g);
+                ev[q] = pv[jc];
+                eg[q] = gh[jc];
             }
-            f32x4_t col0 = {0.f, 0.f, 0.f, 0.f}, col1 = {0.f, 0.f, 0.f, 0.f};
+            f32x4_t col[KT];
+#pragma unroll
+            for (int q = 0; q < KT; ++q) col[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
             for (int i0 = 0; i0 < rpad; i0 += 32) {
                 const f16x8_t ay = xfrag_perm(sy, ldy, n, 6, i0, g);
-                u32x4_t e0, e1;
+                u32x4_t e[KT];
                 if (FAST) {
                     const f16x4_t ra = *(const f16x4_t*)(scm + i0 + n);
                     const f16x4_t rb = *(const f16x4_t*)(scm + i0 + 16 + n);
                     const f32x4_t z = {0.f, 0.f, 0.f, 0.f};
-                    const f32x4_t x00 = __builtin_amdgcn_mfma_f32_16x16x16f16(ra, kf0, z, 0, 0, 0);
-                    const f32x4_t x01 = __builtin_amdgcn_mfma_f32_16x16x16f16(rb, kf0, z, 0, 0, 0);
-                    const f32x4_t x10 = __builtin_amdgcn_mfma_f32_16x16x16f16(ra, kf1, z, 0, 0, 0);
-                    const f32x4_t x11 = __builtin_amdgcn_mfma_f32_16x16x16f16(rb, kf1, z, 0, 0, 0);
-                    float e[8], f[8];
+                    f32x4_t x0[KT], x1[KT];
 #pragma unroll
-                    for (int t = 0; t < 4; ++t) {
-                        e[t] = __builtin_amdgcn_exp2f(x00[t]);
-                        e[4 + t] = __builtin_amdgcn_exp2f(x01[t]);
-                        f[t] = __builtin_amdgcn_exp2f(x10[t]);
-                        f[4 + t] = __builtin_amdgcn_exp2f(x11[t]);
+                    for (int q = 0; q < KT; ++q) {
+                        x0[q] = __builtin_amdgcn_mfma_f32_16x16x16f16(ra, kf[q], z, 0, 0, 0);
+                        x1[q] = __builtin_amdgcn_mfma_f32_16x16x16f16(rb, kf[q], z, 0, 0, 0);
                     }
-                    e0 = pack_e(e);
-                    e1 = pack_e(f);
+#pragma unroll
+                    for (int q = 0; q < KT; ++q) {
+                        float ex[8];
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) {
+                            ex[t] = __builtin_amdgcn_exp2f(x0[q][t]);
+                            ex[4 + t] = __builtin_amdgcn_exp2f(x1[q][t]);
+                        }
+                        e[q] = pack_e(ex);
+                    }
                 } else {
                     // rows i0 + 4 g + t and i0 + 16 + 4 g + t (t < 4) of this lane's keys
                     float2 cm[8];
@@ -756,30 +759,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                     *(f32x4_t*)&cm[2] = *(const f32x4_t*)(scm + i0 + 4 * g + 2);
                     *(f32x4_t*)&cm[4] = *(const f32x4_t*)(scm + i0 + 16 + 4 * g);
                     *(f32x4_t*)&cm[6] = *(const f32x4_t*)(scm + i0 + 16 + 4 * g + 2);
-                    float e[8], f[8];
 #pragma unroll
-                    for (int t = 0; t < 8; ++t) {
-                        e[t] = __builtin_amdgcn_exp2f(fmaf(cm[t].x, kv0, cm[t].y));
-                        f[t] = __builtin_amdgcn_exp2f(fmaf(cm[t].x, kv1, cm[t].y));
+                    for (int q = 0; q < KT; ++q) {
+                        float ex[8];
+#pragma unroll
+                        for (int t = 0; t < 8; ++t) ex[t] = __builtin_amdgcn_exp2f(fmaf(cm[t].x, kv[q], cm[t].y));
+                        e[q] = pack_e(ex);
                     }
-                    e0 = pack_e(e);
-                    e1 = pack_e(f);
                 }
-                col0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ay, __builtin_bit_cast(f16x8_t, e0), col0, 0, 0, 0);
-                col1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ay, __builtin_bit_cast(f16x8_t, e1), col1, 0, 0, 0);
+#pragma unroll
+                for (int q = 0; q < KT; ++q)
+                    col[q] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ay, __builtin_bit_cast(f16x8_t, e[q]), col[q], 0, 0, 0);
             }
-            // lanes 0..15: (a hi, a lo, a o hi, a o lo) of key n (+16 h); lanes 16..31: (go/Z hi, lo)
+            // lanes 0..15: (a hi, a lo, a o hi, a o lo) of key n (+16 q); lanes 16..31: (go/Z hi, lo)
             if (lane < 32) {
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const f32x4_t col = h ? col1 : col0;
-                    const int j = j0 + 16 * h + n;
+                for (int q = 0; q < KT; ++q) {
+                    const int j = j0 + 16 * q + n;
                     if (j < r) {
                         if (lane < 16) {
-                            const float c1 = (col.x + col.y) * as, c2 = (col.z + col.w) * bs;
-                            st<T>::store(GP + b * ldgp + 2 * r + j, ev[h] * c1 - c2);
+                            const float c1 = (col[q].x + col[q].y) * as, c2 = (col[q].z + col[q].w) * bs;
+                            st<T>::store(GP + b * ldgp + 2 * r + j, ev[q] * c1 - c2);
                         } else {
-                            st<T>::store(GP + b * ldgp + j, beta * eg[h] + (col.x + col.y) * cs);
+                            st<T>::store(GP + b * ldgp + j, beta * eg[q] + (col[q].x + col[q].y) * cs);
                         }
                     }
                 }
