@@ -35,55 +35,106 @@ __device__ __forceinline__ void st4<bf16_t>(bf16_t* p, const float* v) {
     *(uint2*)p = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
 }
 
-// Block = 16 column groups of 4 columns x 16 row slices. Thread (ty, tx) handles
-// columns c .. c+3 and rows b0 + ty, b0 + ty + 16, ...; its column sums are then
-// added over ty in fixed order, giving one partial row per block.
-constexpr int PW_ROWS = 128;  // rows per block
+// 8 consecutive values at p (float: as two halves, the second at p + off4, where off4
+// is 4, or 0 when only the first half lies inside the row; bf16 rows have a multiple
+// of 8 columns, so their 16 bytes are always inside).
+template <typename T>
+__device__ __forceinline__ void ld8(const T* p, int off4, float* v);
+template <>
+__device__ __forceinline__ void ld8<float>(const float* p, int off4, float* v) {
+    ld4<float>(p, v);
+    ld4<float>(p + off4, v + 4);
+}
+template <>
+__device__ __forceinline__ void ld8<bf16_t>(const bf16_t* p, int, float* v) {
+    const u32x4_t w = *(const u32x4_t*)p;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+        v[2 * h] = __uint_as_float(w[h] << 16);
+        v[2 * h + 1] = __uint_as_float(w[h] & 0xffff0000u);
+    }
+}
+
+// Store 8 values (float: the second half only when has4; bf16: all 16 bytes).
+template <typename T>
+__device__ __forceinline__ void st8(T* p, bool has4, const float* v);
+template <>
+__device__ __forceinline__ void st8<float>(float* p, bool has4, const float* v) {
+    st4<float>(p, v);
+    if (has4) st4<float>(p + 4, v + 4);
+}
+template <>
+__device__ __forceinline__ void st8<bf16_t>(bf16_t* p, bool, const float* v) {
+    *(u32x4_t*)p = u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                           pack_bf16x2(v[6], v[7])};
+}
+
+// Block = 8 column groups of 8 columns x 32 row slices. Thread (ty, tx) handles
+// columns c .. c+7 (two 4-column halves; d is a multiple of 4) of rows
+// b0 + ty + 32 k, k < PW_RPT: every load of its rows is issued before any of them
+// is used. Its column sums are then added over ty in fixed order, giving one
+// partial row per block.
+constexpr int PW_ROWS = 128;            // rows per block
+constexpr int PW_RPT = PW_ROWS / 32;    // rows per thread
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_bwd_pointwise(int64_t B, int64_t d, const void* gin, int gin_f32,
                                                        const T* __restrict__ x0, const T* __restrict__ t,
                                                        float* __restrict__ gx0, int first, T* __restrict__ gt,
                                                        float* __restrict__ part) {
-    __shared__ float red[16][64 + 4];
-    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-    const int64_t c = (int64_t)blockIdx.x * 64 + tx * 4;
+    __shared__ float red[32][64 + 4];
+    const int tx = threadIdx.x & 7, ty = threadIdx.x >> 3;
+    const int64_t c = (int64_t)blockIdx.x * 64 + tx * 8;
     const int64_t b0 = (int64_t)blockIdx.y * PW_ROWS;
-    int64_t b1 = b0 + PW_ROWS;
-    if (b1 > B) b1 = B;
-    float cs[4] = {0.f, 0.f, 0.f, 0.f};
+    float cs[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if (c < d) {
-        for (int64_t b = b0 + ty; b < b1; b += 16) {
-            const int64_t i = b * d + c;
-            float g[4], xv[4], tv[4], acc[4], gtv[4];
-            if (gin_f32) ld4<float>((const float*)gin + i, g);
-            else ld4<T>((const T*)gin + i, g);
-            ld4<T>(x0 + i, xv);
-            ld4<T>(t + i, tv);
-            if (first) {
-                acc[0] = acc[1] = acc[2] = acc[3] = 0.f;
-            } else {
-                ld4<float>(gx0 + i, acc);
-            }
+        // (float) the second half past d re-reads the first; nothing of it is stored
+        const int off4 = c + 4 < d ? 4 : 0;
+        float g[PW_RPT][8], xv[PW_RPT][8], tv[PW_RPT][8], acc[PW_RPT][8];
+        int64_t row[PW_RPT];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                gtv[e] = g[e] * xv[e];
-                acc[e] = fmaf(g[e], tv[e], acc[e]);
+        for (int k = 0; k < PW_RPT; ++k) {
+            const int64_t b = b0 + ty + 32 * k;
+            row[k] = (b < B ? b : b0) * d;  // rows past B re-read row b0 and are not stored
+        }
+        if (gin_f32) {
+#pragma unroll
+            for (int k = 0; k < PW_RPT; ++k) ld8<float>((const float*)gin + row[k] + c, off4, g[k]);
+        } else {
+#pragma unroll
+            for (int k = 0; k < PW_RPT; ++k) ld8<T>((const T*)gin + row[k] + c, off4, g[k]);
+        }
+#pragma unroll
+        for (int k = 0; k < PW_RPT; ++k) {
+            ld8<T>(x0 + row[k] + c, off4, xv[k]);
+            ld8<T>(t + row[k] + c, off4, tv[k]);
+            if (!first) ld8<float>(gx0 + row[k] + c, off4, acc[k]);
+        }
+#pragma unroll
+        for (int k = 0; k < PW_RPT; ++k) {
+            if (b0 + ty + 32 * k >= B) continue;
+            float gtv[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float a = first ? 0.f : acc[k][e];
+                gtv[e] = g[k][e] * xv[k][e];
+                acc[k][e] = fmaf(g[k][e], tv[k][e], a);
                 cs[e] += gtv[e];
             }
-            st4<T>(gt + i, gtv);
-            st4<float>(gx0 + i, acc);
+            st8<T>(gt + row[k] + c, off4 != 0, gtv);
+            st8<float>(gx0 + row[k] + c, off4 != 0, acc[k]);
         }
     }
 #pragma unroll
-    for (int e = 0; e < 4; ++e) red[ty][tx * 4 + e] = cs[e];
+    for (int e = 0; e < 8; ++e) red[ty][tx * 8 + e] = cs[e];
     __syncthreads();
-    if (ty == 0 && c < d) {
-        float s[4] = {red[0][tx * 4], red[0][tx * 4 + 1], red[0][tx * 4 + 2], red[0][tx * 4 + 3]};
-        for (int y = 1; y < 16; ++y)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) s[e] += red[y][tx * 4 + e];
-        st4<float>(part + (int64_t)blockIdx.y * d + c, s);
+    // 64 threads finish the block's 64 columns, each adding the 32 row slices in order
+    if (threadIdx.x < 64) {
+        const int col = threadIdx.x;
+        const int64_t cc = (int64_t)blockIdx.x * 64 + col;
+        float s = red[0][col];
+        for (int y = 1; y < 32; ++y) s += red[y][col];
+        if (cc < d) part[(int64_t)blockIdx.y * d + cc] = s;
     }
 }
 
