@@ -148,6 +148,29 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
     return wofs + x - v;
 }
 
+// Exclusive scan of one value per thread over a workgroup of NW waves.
+template <int NW>
+__device__ __forceinline__ uint32_t block_exclusive_scan_nw(uint32_t v, uint32_t* sh, uint32_t& total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint32_t x = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t y = __shfl_up(x, off);
+        if (lane >= off) x += y;
+    }
+    if (lane == 63) sh[wave] = x;
+    __syncthreads();
+    uint32_t wofs = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+        if (w < wave) wofs += sh[w];
+        tot += sh[w];
+    }
+    total = tot;
+    __syncthreads();
+    return wofs + x - v;
+}
+
 // Per digit d (one workgroup per digit): exclusive prefix over the tiles of
 // hist[d][*] in place, 256 tiles per round; digit total into tot[d].
 __global__ __launch_bounds__(256) void k_digit_scan(uint32_t* __restrict__ hist, int ntiles,
@@ -465,7 +488,7 @@ __global__ __launch_bounds__(256) void k_seg_fixup(const uint32_t* __restrict__ 
 // one workgroup per (feature, table, row slice) replaces steps 1-3. It walks the
 // feature's occurrences in (bag, position) order, CAP at a time, keeps those whose
 // row falls in its slice and sorts them by row in LDS (a counting sort over at most
-// FU_ROWS rows: each wave ranks its quarter of the chunk with ballots, a scan over
+// FU_ROWS rows: each wave ranks its share of the chunk with ballots, a scan over
 // the rows gives every (row, wave) run its start). The sorted chunk is split into
 // equal parts, one per lane group (L lanes of four columns each, 64 / L groups per
 // wave); a group adds its part's contributions one after another, and a segment
@@ -476,11 +499,15 @@ __global__ __launch_bounds__(256) void k_seg_fixup(const uint32_t* __restrict__ 
 // The workgroups of one feature are given block indices with equal residue mod 8 so
 // that they run on one XCD and share its L2 copy of the feature's gradient slab.
 constexpr int FU_CAP = 4096;            // occurrences per chunk
-constexpr int FU_QW = FU_CAP / 4;       // per wave
+constexpr int FU_WAVES = 8;             // waves per workgroup
+constexpr int FU_THREADS = 64 * FU_WAVES;
+constexpr int FU_QW = FU_CAP / FU_WAVES;  // chunk elements per wave
 constexpr int FU_ROWS = 1024;           // rows per slice
 constexpr int FU_MAX_SLICES = 16;
 constexpr int FU_TARGET_BLOCKS = 256;   // workgroups the slice count aims for (fewer slices: less repeated id work)
-constexpr int FU_BAGS = 1024;           // bags per block (bag front-end), four per thread
+constexpr int FU_BAGS = 1024;           // bags per block (bag front-end)
+constexpr int FU_BPT = FU_BAGS / FU_THREADS;  // bags per thread
+constexpr int FU_RPT = FU_ROWS / FU_THREADS;  // slice rows per thread in the run-start scan
 constexpr uint32_t FU_SKIP = 0xffffffffu;
 
 struct FusedArgs {
@@ -491,19 +518,19 @@ struct FusedArgs {
 };
 
 template <typename T, int L, bool MUL, bool BAGS>
-__global__ __launch_bounds__(256) void k_emb_fused(FusedArgs fa) {
+__global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
     constexpr int E = 64 / L;                // lane groups per wave
-    constexpr int NP = 4 * E;                // parts of a sorted chunk, one per lane group
-    constexpr int U = MUL ? 8 : 16;          // elements of a part whose loads are in flight together
+    constexpr int NP = FU_WAVES * E;         // parts of a sorted chunk, one per lane group
+    constexpr int U = 8;                     // elements of a part whose loads are in flight together
     __shared__ uint32_t key_e[FU_CAP];       // per chunk element: row << 16 | rank in its wave's run, or FU_SKIP
     __shared__ uint32_t sorted[FU_CAP];      // row << 12 | element, in (row, element) order
-    __shared__ uint32_t whist[4][FU_ROWS];   // per wave row counts, then run starts
+    __shared__ uint16_t whist[FU_WAVES][FU_ROWS];  // per wave row counts, then run starts (< FU_CAP)
     __shared__ float carry[2][NP][4 * L];    // per part head / tail pieces
     __shared__ uint16_t bag_e[BAGS ? FU_CAP : 1];
     __shared__ uint16_t other_e[MUL ? FU_CAP : 1];
     __shared__ uint32_t bstart[BAGS ? FU_BAGS : 1];
     __shared__ int64_t boff[BAGS ? FU_BAGS : 1];
-    __shared__ uint32_t sh[4];
+    __shared__ uint32_t sh[FU_WAVES];
     __shared__ uint32_t nkept;
 
     const EmbedBwdArgs& a = fa.a;
@@ -528,18 +555,18 @@ __global__ __launch_bounds__(256) void k_emb_fused(FusedArgs fa) {
     const int grp = lane / L, sub4 = lane % L, c = 4 * sub4;
     const bool colok = c < D;
     const uint64_t lt = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-    for (int i = threadIdx.x; i < 4 * FU_ROWS; i += 256) (&whist[0][0])[i] = 0u;
+    for (int i = threadIdx.x; i < FU_WAVES * FU_ROWS; i += FU_THREADS) (&whist[0][0])[i] = 0;
 
     const int64_t step_b = BAGS ? FU_BAGS : FU_CAP;
     for (int64_t b0 = 0; b0 < a.batch; b0 += step_b) {
         const uint32_t nb = (uint32_t)(a.batch - b0 < step_b ? a.batch - b0 : step_b);
         uint32_t total = nb;  // occurrences of this block of bags
         if (BAGS) {
-            uint32_t len[4], s4 = 0;
-            int64_t beg[4];
+            uint32_t len[FU_BPT], s4 = 0;
+            int64_t beg[FU_BPT];
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const uint32_t t = 4 * threadIdx.x + k;
+            for (int k = 0; k < FU_BPT; ++k) {
+                const uint32_t t = FU_BPT * threadIdx.x + k;
                 len[k] = 0;
                 beg[k] = 0;
                 if (t < nb) {
@@ -552,18 +579,18 @@ __global__ __launch_bounds__(256) void k_emb_fused(FusedArgs fa) {
                 }
                 s4 += len[k];
             }
-            uint32_t run = block_exclusive_scan(s4, sh, total);
+            uint32_t run = block_exclusive_scan_nw<FU_WAVES>(s4, sh, total);
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                bstart[4 * threadIdx.x + k] = run;
-                boff[4 * threadIdx.x + k] = beg[k];
+            for (int k = 0; k < FU_BPT; ++k) {
+                bstart[FU_BPT * threadIdx.x + k] = run;
+                boff[FU_BPT * threadIdx.x + k] = beg[k];
                 run += len[k];
             }
         }
         __syncthreads();
         for (uint32_t c0 = 0; c0 < total; c0 += FU_CAP) {
             const uint32_t n = total - c0 < (uint32_t)FU_CAP ? total - c0 : (uint32_t)FU_CAP;
-            // A. rows of this wave's quarter (all id loads first, then the ranking); the
+            // A. rows of this wave's share (all id loads first, then the ranking); the
             // rank of each kept element among the wave's earlier elements of its row
             constexpr int NIT = FU_QW / 64;
             int64_t pv[NIT];
@@ -628,29 +655,29 @@ __global__ __launch_bounds__(256) void k_emb_fused(FusedArgs fa) {
                 key_e[e] = kept ? (row << 16) | (before + rank) : FU_SKIP;
                 if (BAGS) bag_e[e] = (uint16_t)bagv[it];
                 if (MUL) other_e[e] = (uint16_t)(isq ? ri : qi);
-                if (kept && rank == 0) whist[wv][row] = before + (uint32_t)__popcll(peers);
+                if (kept && rank == 0) whist[wv][row] = (uint16_t)(before + (uint32_t)__popcll(peers));
             }
             __syncthreads();
             // B. run starts: rows in order, inside a row the waves in order
             {
-                uint32_t cnt[4][4], s4 = 0;
+                uint32_t cnt[FU_RPT][FU_WAVES], s4 = 0;
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const uint32_t r = 4 * threadIdx.x + k;
+                for (int k = 0; k < FU_RPT; ++k) {
+                    const uint32_t r = FU_RPT * threadIdx.x + k;
 #pragma unroll
-                    for (int w = 0; w < 4; ++w) {
+                    for (int w = 0; w < FU_WAVES; ++w) {
                         cnt[k][w] = r < nr ? whist[w][r] : 0u;
                         s4 += cnt[k][w];
                     }
                 }
                 uint32_t tot;
-                uint32_t run = block_exclusive_scan(s4, sh, tot);
+                uint32_t run = block_exclusive_scan_nw<FU_WAVES>(s4, sh, tot);
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const uint32_t r = 4 * threadIdx.x + k;
+                for (int k = 0; k < FU_RPT; ++k) {
+                    const uint32_t r = FU_RPT * threadIdx.x + k;
 #pragma unroll
-                    for (int w = 0; w < 4; ++w) {
-                        if (r < nr) whist[w][r] = run;
+                    for (int w = 0; w < FU_WAVES; ++w) {
+                        if (r < nr) whist[w][r] = (uint16_t)run;
                         run += cnt[k][w];
                     }
                 }
@@ -667,7 +694,7 @@ __global__ __launch_bounds__(256) void k_emb_fused(FusedArgs fa) {
                 }
             }
             __syncthreads();
-            for (int i = threadIdx.x; i < 4 * FU_ROWS; i += 256) (&whist[0][0])[i] = 0u;
+            for (int i = threadIdx.x; i < FU_WAVES * FU_ROWS; i += FU_THREADS) (&whist[0][0])[i] = 0;
             // D. sums in sorted order: lane group g of wave w takes part P = w * E + g, an
             // equal share of the sorted chunk, and adds its elements one after another
             const uint32_t nk = nkept;
@@ -816,7 +843,7 @@ hipError_t launch_reduce_d(const EmbedBwdArgs& a, const RedPtrs& p, uint32_t n, 
 template <typename T, bool MUL, bool BAGS>
 hipError_t launch_fused_d(const FusedArgs& fa, unsigned blocks, hipStream_t st) {
     const int q = (fa.a.D + 3) / 4;
-#define RDCN_FUSED(L) hipLaunchKernelGGL((k_emb_fused<T, L, MUL, BAGS>), dim3(blocks), dim3(256), 0, st, fa)
+#define RDCN_FUSED(L) hipLaunchKernelGGL((k_emb_fused<T, L, MUL, BAGS>), dim3(blocks), dim3(FU_THREADS), 0, st, fa)
     if (q <= 4) RDCN_FUSED(4);
     else if (q <= 8) RDCN_FUSED(8);
     else if (q <= 16) RDCN_FUSED(16);
