@@ -504,7 +504,7 @@ constexpr int FU_THREADS = 64 * FU_WAVES;
 constexpr int FU_QW = FU_CAP / FU_WAVES;  // chunk elements per wave
 constexpr int FU_ROWS = 1024;           // rows per slice
 constexpr int FU_MAX_SLICES = 16;
-constexpr int FU_TARGET_BLOCKS = 256;   // workgroups the slice count aims for (fewer slices: less repeated id work)
+constexpr int FU_TARGET_BLOCKS = 128;   // workgroups the slice count aims for (fewer slices: less repeated id work)
 constexpr int FU_BAGS = 1024;           // bags per block (bag front-end)
 constexpr int FU_BPT = FU_BAGS / FU_THREADS;  // bags per thread
 constexpr int FU_RPT = FU_ROWS / FU_THREADS;  // slice rows per thread in the run-start scan
