@@ -243,6 +243,12 @@ rdcn_status rdcn_forward(rdcn_handle* h, int64_t batch, const void* x0, const rd
  * and the float weight gradients in `grads` (same shapes as the weights,
  * summed over the batch). x0, w and saved must be those of the matching
  * rdcn_forward call.
+ * The weight-gradient products (and the bias sums) run on a second stream that
+ * the handle owns (default priority), forked from `stream` after each layer's
+ * attention and joined back to `stream` with events before the call returns:
+ * work enqueued on `stream` after the call sees every output, and capturing
+ * `stream` in a HIP graph captures both streams. Two calls on one handle must
+ * not run concurrently on different streams.
  */
 rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const rdcn_weights* w, const void* saved,
                           const void* grad_out, float* grad_x0, const rdcn_weights* grads, void* scratch,

@@ -22,6 +22,10 @@ struct rdcn_handle {
     int hr;  // width of the up projection's input (2r with parallel branches, else r)
     bool bf16, ids64, attn, split, par;
     uint32_t magic, shift;
+    // the backward's weight-gradient products run on `side`, forked from and joined
+    // back to the caller's stream with these events (no timing)
+    hipStream_t side = nullptr;
+    hipEvent_t ev_att = nullptr, ev_side[2] = {nullptr, nullptr};
     int* err;  // device error word
     bool head_on = false;
     rdcn_head_config head{};
@@ -117,8 +121,10 @@ SavedLayout saved_layout(const rdcn_handle* h, int64_t B) {
     return s;
 }
 
+// gt, gP and part alternate between two copies by layer parity: the side stream
+// still reads layer l's copies while the main stream computes layer l - 1.
 struct ScratchLayout {
-    size_t g, gt, gh, gP, part, splitk, total;
+    size_t g, gt[2], gh, gP[2], part[2], splitk, total;
     int nrb;
 };
 
@@ -136,12 +142,21 @@ ScratchLayout scratch_layout(const rdcn_handle* h, int64_t B) {
     ScratchLayout s;
     const size_t e = eb(h), d = (size_t)h->d, r = (size_t)h->cfg.rank, n = (size_t)h->n;
     s.nrb = B > 0 ? (int)((B + pointwise_rows_per_block(B, d) - 1) / pointwise_rows_per_block(B, d)) : 0;
+    const int copies = h->cfg.num_layers > 1 ? 2 : 1;
     size_t off = 0;
     s.g = off; off += al(B * d * 4);
-    s.gt = off; off += al(B * d * e);
     s.gh = off; off += h->attn ? al(B * r * 4) : 0;
-    s.gP = off; off += al(B * n * r * e);
-    s.part = off; off += al((size_t)s.nrb * d * 4);
+    for (int k = 0; k < 2; ++k) {
+        if (k >= copies) {
+            s.gt[k] = s.gt[0];
+            s.gP[k] = s.gP[0];
+            s.part[k] = s.part[0];
+            continue;
+        }
+        s.gt[k] = off; off += al(B * d * e);
+        s.gP[k] = off; off += al(B * n * r * e);
+        s.part[k] = off; off += al((size_t)s.nrb * d * 4);
+    }
     s.splitk = off; off += al((size_t)splitk_elems(h, B) * 4);
     s.total = off;
     return s;
@@ -352,9 +367,13 @@ rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
         delete h;
         return RDCN_ERR_HIP;
     }
-    if (hipMemset(h->err, 0, sizeof(int)) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
-        (void)hipFree(h->err);
-        delete h;
+    bool ok = hipMemset(h->err, 0, sizeof(int)) == hipSuccess && hipDeviceSynchronize() == hipSuccess;
+    ok = ok && hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking) == hipSuccess;  // default priority
+    for (hipEvent_t* e : {&h->ev_att, &h->ev_side[0], &h->ev_side[1]})
+        ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
+    if (!ok) {
+        (void)hipGetLastError();
+        (void)rdcn_destroy(h);
         return RDCN_ERR_HIP;
     }
     *out = h;
@@ -365,6 +384,9 @@ rdcn_status rdcn_destroy(rdcn_handle* h) {
     if (!h) return RDCN_OK;
     rdcn_status s = RDCN_OK;
     for (hipEvent_t e : h->prof_ev) (void)hipEventDestroy(e);
+    for (hipEvent_t e : {h->ev_att, h->ev_side[0], h->ev_side[1]})
+        if (e && hipEventDestroy(e) != hipSuccess) s = RDCN_ERR_HIP;
+    if (h->side && hipStreamDestroy(h->side) != hipSuccess) s = RDCN_ERR_HIP;
     if (h->err && hipFree(h->err) != hipSuccess) s = RDCN_ERR_HIP;
     delete h;
     return s;
@@ -608,14 +630,23 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
     const char* sv = (const char*)saved;
     char* sc = (char*)scratch;
     float* g = (float*)(sc + W.g);
-    void* gt = sc + W.gt;
     float* gh = (float*)(sc + W.gh);
-    void* gP = sc + W.gP;
-    float* part = (float*)(sc + W.part);
     float* splitk = (float*)(sc + W.splitk);
+    hipStream_t side = h->side;
 
+    // Main stream: pointwise -> gh -> attention -> gx, the chain from one layer's
+    // gradient to the next. Side stream, once the layer's attention is done: the bias
+    // column sums and the weight gradients gU and gW (with their split-K reductions),
+    // which nothing later in the backward reads; they overlap gx and the next layer's
+    // pointwise and gh (started earlier, they slow the attention more than they gain).
     for (int l = c.num_layers - 1; l >= 0; --l) {
         const bool top = l == c.num_layers - 1;
+        const int par = l & 1;
+        void* gt = sc + W.gt[par];
+        void* gP = sc + W.gP[par];
+        float* part = (float*)(sc + W.part[par]);
+        // this parity's copies were last read by the side stream's work of layer l + 2
+        if (l + 2 < c.num_layers) RDCN_TRY(hipStreamWaitEvent(s, h->ev_side[par], 0));
         const void* gin = top ? grad_out : (const void*)g;
         const void* P = sv + S.P[l];
         const void* xl = l == 0 ? x0 : (const void*)(sv + S.X[l - 1]);
@@ -624,24 +655,11 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
             ProfScope ps(h, RDCN_KERNEL_BWD_POINTWISE, s);
             RDCN_TRY(launch_bwd_pointwise(B, d, gin, !top, x0, sv + S.T[l], grad_x0, top, gt, part, h->bf16, s));
         }
-        {
-            ProfScope ps(h, RDCN_KERNEL_BWD_BIAS, s);
-            RDCN_TRY(launch_colsum(part, W.nrb, d, (float*)grads->bias[l], s));
-        }
         const void* hsrc = h->attn ? (const void*)(sv + S.H[l]) : P;
         const int64_t hr = h->hr;
         const int64_t ldh = h->attn ? hr : nr;
         const float hscale = h->attn ? 1.0f : c.skip_beta;
         const int64_t e = (int64_t)eb(h);
-        // gU = gt^T h      [d, hr], K = batch
-        {
-            GemmArgs g1{};
-            g1.M = d; g1.N = hr; g1.K = B;
-            g1.a = gt; g1.lda = d; g1.a_kstrided = true;
-            g1.b = hsrc; g1.ldb = ldh; g1.b_kstrided = true;
-            g1.scale = hscale;
-            RDCN_TRY(gemm_weight_grad(h, RDCN_KERNEL_BWD_GU_GEMM, g1, (float*)grads->u[l], splitk, s));
-        }
         // gh = gt U         [B, hr]; with parallel branches the plain branch's part is its
         // value gradient and goes straight into the first columns of gP
         if (h->par) {
@@ -673,6 +691,21 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
                                      (const float*)(sv + S.A[l]), gh, r, (char*)gP + (h->par ? r * e : 0), nr,
                                      h->bf16, s));
         }
+        RDCN_TRY(hipEventRecord(h->ev_att, s));
+        RDCN_TRY(hipStreamWaitEvent(side, h->ev_att, 0));
+        {
+            ProfScope ps(h, RDCN_KERNEL_BWD_BIAS, side);
+            RDCN_TRY(launch_colsum(part, W.nrb, d, (float*)grads->bias[l], side));
+        }
+        // gU = gt^T h      [d, hr], K = batch
+        {
+            GemmArgs g1{};
+            g1.M = d; g1.N = hr; g1.K = B;
+            g1.a = gt; g1.lda = d; g1.a_kstrided = true;
+            g1.b = hsrc; g1.ldb = ldh; g1.b_kstrided = true;
+            g1.scale = hscale;
+            RDCN_TRY(gemm_weight_grad(h, RDCN_KERNEL_BWD_GU_GEMM, g1, (float*)grads->u[l], splitk, side));
+        }
         // gW = gP^T x_l    [n r, d], K = batch
         {
             GemmArgs g3{};
@@ -680,8 +713,9 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
             g3.a = gP; g3.lda = nr; g3.a_kstrided = true;
             g3.b = xl; g3.ldb = d; g3.b_kstrided = true;
             g3.scale = 1.0f;
-            RDCN_TRY(gemm_weight_grad(h, RDCN_KERNEL_BWD_GW_GEMM, g3, (float*)grads->w_down[l], splitk, s));
+            RDCN_TRY(gemm_weight_grad(h, RDCN_KERNEL_BWD_GW_GEMM, g3, (float*)grads->w_down[l], splitk, side));
         }
+        RDCN_TRY(hipEventRecord(h->ev_side[par], side));
         // g_l = g_{l+1} + gP W   (layer 0: grad_x0 += g_1 + gP W)
         {
             GemmArgs g4{};
@@ -696,6 +730,8 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
             RDCN_TRY(launch_gemm(g4, plan_gemm(B, d, nr, h->bf16, false), h->bf16, s));
         }
     }
+    // join: the side stream's last work (layer 0) completes before anything later on `s`
+    RDCN_TRY(hipStreamWaitEvent(s, h->ev_side[0], 0));
     return RDCN_OK;
 }
 
