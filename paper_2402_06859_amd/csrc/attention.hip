@@ -284,19 +284,6 @@ __device__ __forceinline__ f16x4_t row_rec(float c, float m) {
     return f16x4_t{ch, (_Float16)(c - (float)ch), mh, (_Float16)(m - (float)mh)};
 }
 
-__device__ __forceinline__ u32x4_t efrag_mfma(const f16x4_t& k0, const f16x4_t& k1, const f16x4_t& rec) {
-    const f32x4_t z = {0.f, 0.f, 0.f, 0.f};
-    const f32x4_t x0 = __builtin_amdgcn_mfma_f32_16x16x16f16(k0, rec, z, 0, 0, 0);
-    const f32x4_t x1 = __builtin_amdgcn_mfma_f32_16x16x16f16(k1, rec, z, 0, 0, 0);
-    float e[8];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        e[t] = __builtin_amdgcn_exp2f(x0[t]);
-        e[4 + t] = __builtin_amdgcn_exp2f(x1[t]);
-    }
-    return pack_e(e);
-}
-
 // X^T fragment of row n (< nx, else zero) for the chunk at j0, keys in the order above.
 __device__ __forceinline__ f16x8_t xfrag_perm(const _Float16* sx, int ld, int n, int nx, int j0, int g) {
     if (n >= nx) return f16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
@@ -304,6 +291,8 @@ __device__ __forceinline__ f16x8_t xfrag_perm(const _Float16* sx, int ld, int n,
     const f16x4_t hi = *(const f16x4_t*)(sx + xoff(n, j0 + 16 + 4 * g, ld));
     return f16x8_t{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
 }
+
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // The lane's 8 keys (order above) from the float key array.
 __device__ __forceinline__ void keys_perm(const float* sk, int j0, int g, float (&kv)[8]) {
@@ -442,6 +431,22 @@ __device__ __forceinline__ f16x8_t xfrag_fwd(const _Float16* sx, int ld, int n, 
     return xfrag_perm(sx, ld, xrow(n), ATT_XROWS, j0, g);
 }
 
+// Exponent arguments of 32 keys x 32 rows from one v_mfma_f32_32x32x8_f16 (the key
+// and row records of key_frag / row_rec use only 8 K slots): lane l gets row l % 32 and
+// keys 8 a + 4 (l / 32) + t in element 4 a + t. Elements 8 p .. 8 p + 7 are the B
+// operand of a 16x16x32 weighted sum over keys 16 p .. 16 p + 15 whose columns are
+// rows n (lanes 0-15, 32-47) and n + 16 (lanes 16-31, 48-63): xfrag32 gives the
+// quantities of row n to output slots 0-7 and those of row n + 16 to slots 8-15.
+// X^T fragment for such a sum at keys jb .. jb + 15: lane (g4, q) with q % 8 a
+// quantity row (row 3 and rows of the other half read as zero).
+__device__ __forceinline__ f16x8_t xfrag32(const _Float16* sx, int ld, int lane, int jb) {
+    const int qs = lane & 15, g4 = lane >> 4, q = qs & 7, h = g4 >> 1;
+    if ((qs >> 3) != (g4 & 1) || q == 3) return f16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    const f16x4_t lo = *(const f16x4_t*)(sx + xoff(xrow(q), jb + 4 * h, ld));
+    const f16x4_t hi = *(const f16x4_t*)(sx + xoff(xrow(q), jb + 8 + 4 * h, ld));
+    return f16x8_t{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+}
+
 // LDS of the forward. Per sample (shared by its W waves): keys, X^T. Per wave: row
 // constants and one slot for the range check.
 __host__ __device__ constexpr int attn_fwd_sample_floats(int rpad) { return rpad + ATT_XROWS * rpad / 2; }
@@ -528,44 +533,60 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     auto chunks = [&](auto fast_c) {
         constexpr bool FAST = decltype(fast_c)::value;
         for (int j0 = 0; j0 < rpad; j0 += 32) {
-            float kv[8];
-            f16x4_t k0, k1;
             if (FAST) {
-                k0 = key_frag(sk[j0 + n], g);
-                k1 = key_frag(sk[j0 + 16 + n], g);
-            } else {
-                keys_perm(sk, j0, g, kv);
-            }
-            const f16x8_t a = xfrag_fwd(sx, ldx, n, j0, g);
+                // 32-row tiles: acc[tt] holds rows 32 tt + n (lanes 0-31) and 32 tt + 16 + n
+                const f16x4_t kf = key_frag(sk[j0 + (lane & 31)], lane >> 5);
+                const f16x8_t a0 = xfrag32(sx, ldx, lane, j0), a1 = xfrag32(sx, ldx, lane, j0 + 16);
+                const f32x16_t z16 = {};
 #pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                u32x4_t e;
-                if (FAST) {
-                    e = efrag_mfma(k0, k1, *(const f16x4_t*)(scm + 16 * t + n));
-                } else {
-                    const float2 cm = scm[16 * t + n];
-                    e = efrag(cm.x, cm.y, kv);
+                for (int tt = 0; tt < NT / 2; ++tt) {
+                    const f16x4_t rec = *(const f16x4_t*)(scm + 32 * tt + (lane & 31));
+                    const f32x16_t x = __builtin_amdgcn_mfma_f32_32x32x8f16(kf, rec, z16, 0, 0, 0);
+                    float e0[8], e1[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        e0[u] = __builtin_amdgcn_exp2f(x[u]);
+                        e1[u] = __builtin_amdgcn_exp2f(x[8 + u]);
+                    }
+                    acc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, __builtin_bit_cast(f16x8_t, pack_e(e0)), acc[tt], 0, 0, 0);
+                    acc[tt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, __builtin_bit_cast(f16x8_t, pack_e(e1)), acc[tt], 0, 0, 0);
                 }
-                acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, __builtin_bit_cast(f16x8_t, e), acc[t], 0, 0, 0);
+            } else {
+                float kv[8];
+                keys_perm(sk, j0, g, kv);
+                const f16x8_t a = xfrag_fwd(sx, ldx, n, j0, g);
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    const float2 cm = scm[16 * t + n];
+                    const u32x4_t e = efrag(cm.x, cm.y, kv);
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, __builtin_bit_cast(f16x8_t, e), acc[t], 0, 0, 0);
+                }
             }
         }
     };
     if (fast) chunks(std::true_type{});
     else chunks(std::false_type{});
-    if (live && lane < 32) {
-        // lanes 0-15: (sum e v, sum e) of row n -> h, o, Z; lanes 16-31: (W1, W2) of row n
+    // Which row and quantities each lane's accumulators hold. Fast path: 32-row tiles,
+    // lane (g4, n) has quantities 4 (g4 & 1) .. +3 of row 16 (2 t + g4 / 2) + n. Slow
+    // path: 16-row tiles, lanes 0-31 only, quantities 4 (lane / 16) .. +3 of row 16 t + n.
+    const int na = fast ? NT / 2 : NT;
+    const bool act = fast || lane < 32;
+    const bool lo = fast ? ((lane >> 4) & 1) == 0 : lane < 16;
+    if (live && act) {
+        // lo lanes: (sum e v, sum e) of their row -> h, o, Z; the others: (W1, W2)
         float* so = stats + b * 4 * (int64_t)r;
-        const bool lo = lane < 16;
         float vi[NT];
 #pragma unroll
         for (int t = 0; t < NT; ++t) {  // all loads first
-            const int i = (wr.t0 + t) * 16 + n;
+            const int t16 = fast ? 2 * t + (lane >> 5) : t;
+            const int i = (wr.t0 + t16) * 16 + n;
             vi[t] = pv[i < r ? i : r - 1];
         }
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            const int i = (wr.t0 + t) * 16 + n;
-            if (t < wr.nt && i < r) {
+            const int t16 = fast ? 2 * t + (lane >> 5) : t;
+            const int i = (wr.t0 + t16) * 16 + n;
+            if (t < na && t16 < wr.nt && i < r) {
                 const float s01 = acc[t].x + acc[t].y, z = acc[t].z;
                 const float o = s01 * vs * __builtin_amdgcn_rcpf(z);
                 if (lo) {
