@@ -173,15 +173,17 @@ __global__ __launch_bounds__(256) void k_attn_bwd(int64_t B, int r, float alpha,
 
 // ---------------------------------------------------------------------------
 // bf16 models: the exponentials are computed on the vector ALU, every weighted
-// sum over them runs on the matrix cores. For a 16-row x 32-key block of one
-// sample, each lane computes the 8 values e_ij of its row i = lane % 16 for keys
-// 8 (lane / 16) .. +7, which is exactly the B-operand layout of
-// v_mfma_f32_16x16x32_f16 with K running over keys; the A operand is a small
+// sum over them runs on the matrix cores. For a 32-row x 32-key block of one
+// sample, one v_mfma_f32_32x32x8_f16 leaves each lane 16 values e_ij of its row
+// i = lane % 32, 8 of which form the B operand of a v_mfma_f32_16x16x32_f16 with
+// K running over 16 keys (rows n and n + 16 share its columns and go to output
+// slots 0-7 and 8-15; the A operand is zero in the other half); the A operand is a small
 // per-sample matrix X^T whose rows are the quantities summed against e (v, 1,
 // v k, k), each stored as an f16 hi + lo pair scaled by a power of two so the
 // pair keeps about 21 significant bits. e itself is rounded to f16 (relative
 // 2^-11); all sums of one row use the same rounded e, so the normalisation by Z
-// is consistent. Output lane l holds quantities 4 (l / 16) .. +3 of row l % 16.
+// is consistent. Output lane l holds quantities 4 (l / 16 % 2) .. +3 of row
+// l % 16 (+16 for l >= 32).
 //
 // In the forward one wave owns up to ATT_NT 16-row tiles of one sample and loops
 // over all keys, so row sums never leave its registers; a sample with more rows
@@ -193,7 +195,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd(int64_t B, int r, float alpha,
 // left with column sums only (over rows, weighted by per-row coefficients that
 // depend on o_i and Z_i): it computes the exponent arguments with the forward's
 // product transposed (row records as the A operand, key fragments as B), which
-// hands every lane the e values of one key for 8 rows: the B operand with K
+// hands every lane the e values of one key for 16 rows: B operands with K
 // running over rows. No e_ij is stored or exchanged between lanes.
 // ---------------------------------------------------------------------------
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
@@ -246,11 +248,10 @@ __device__ __forceinline__ f16x8_t xfrag(const _Float16* sx, int ld, int n, int 
     return __builtin_bit_cast(f16x8_t, *(const u32x4_t*)(sx + xoff(n, j0, ld)));
 }
 
-// Key order inside one 32-key chunk. Lane (g, n)'s 8 K slots of a fragment hold
-// keys j0 + 4 g + t (t < 4) and j0 + 16 + 4 g + (t - 4) (t >= 4): the layout in
-// which two 16x16x16 MFMA outputs (keys j0 .. +15 and j0 + 16 .. +31) leave the
-// exponent arguments. Everything indexed by key within a chunk (X^T fragments,
-// the LDS e block) follows it; sums over K do not depend on the order.
+// Key order inside one 32-key chunk of the FMA (slow) path. Lane (g, n)'s 8 K slots
+// of a fragment hold keys j0 + 4 g + t (t < 4) and j0 + 16 + 4 g + (t - 4) (t >= 4).
+// Everything indexed by key within a chunk (X^T fragments, the lane's keys) follows
+// it; sums over K do not depend on the order.
 typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ u32x4_t pack_e(const float (&e)[8]) {
@@ -266,10 +267,10 @@ __device__ __forceinline__ u32x4_t efrag(float c, float m, const float* kv) {
     return pack_e(e);
 }
 
-// Exponent arguments on the matrix cores: x = c k + m as a 16 (keys) x 16 (rows)
-// product with K = 5 of 16 slots used, from f16 hi + lo parts of c, k and m:
-//   keys (A, lane (g, n), key n):   g = 0: (k_hi, k_hi, 1, 1)   g = 1: (k_lo, 0, 0, 0)
-//   rows (B, lane (g, n), row n):   (c_hi, c_lo, m_hi, m_lo) for every g
+// Exponent arguments on the matrix cores: x = c k + m as a 32 (keys) x 32 (rows)
+// product with K = 5 of 8 slots used, from f16 hi + lo parts of c, k and m:
+//   keys (lane half g, key l % 32):   g = 0: (k_hi, k_hi, 1, 1)   g = 1: (k_lo, 0, 0, 0)
+//   rows (lane half g, row l % 32):   (c_hi, c_lo, m_hi, m_lo) for both halves
 // giving c_hi k_hi + c_lo k_hi + m_hi + m_lo + c_hi k_lo: every product is exact in
 // the float accumulator and only c_lo k_lo (relative 2^-22 of c k) is left out.
 __device__ __forceinline__ f16x4_t key_frag(float k, int g) {
@@ -435,15 +436,19 @@ __device__ __forceinline__ f16x8_t xfrag_fwd(const _Float16* sx, int ld, int n, 
 // and row records of key_frag / row_rec use only 8 K slots): lane l gets row l % 32 and
 // keys 8 a + 4 (l / 32) + t in element 4 a + t. Elements 8 p .. 8 p + 7 are the B
 // operand of a 16x16x32 weighted sum over keys 16 p .. 16 p + 15 whose columns are
-// rows n (lanes 0-15, 32-47) and n + 16 (lanes 16-31, 48-63): xfrag32 gives the
+// rows n (lanes 0-15, 32-47) and n + 16 (lanes 16-31, 48-63): frag32 gives the
 // quantities of row n to output slots 0-7 and those of row n + 16 to slots 8-15.
 // X^T fragment for such a sum at keys jb .. jb + 15: lane (g4, q) with q % 8 a
 // quantity row (row 3 and rows of the other half read as zero).
-__device__ __forceinline__ f16x8_t xfrag32(const _Float16* sx, int ld, int lane, int jb) {
+// The backward's Y^T fragment is the same with K over rows and its 6 quantity rows
+// stored as they are (fwd = false).
+template <bool FWD>
+__device__ __forceinline__ f16x8_t frag32(const _Float16* sx, int ld, int lane, int jb) {
     const int qs = lane & 15, g4 = lane >> 4, q = qs & 7, h = g4 >> 1;
-    if ((qs >> 3) != (g4 & 1) || q == 3) return f16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-    const f16x4_t lo = *(const f16x4_t*)(sx + xoff(xrow(q), jb + 4 * h, ld));
-    const f16x4_t hi = *(const f16x4_t*)(sx + xoff(xrow(q), jb + 8 + 4 * h, ld));
+    if ((qs >> 3) != (g4 & 1) || (FWD ? q == 3 : q >= 6)) return f16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    const int row = FWD ? xrow(q) : q;
+    const f16x4_t lo = *(const f16x4_t*)(sx + xoff(row, jb + 4 * h, ld));
+    const f16x4_t hi = *(const f16x4_t*)(sx + xoff(row, jb + 8 + 4 * h, ld));
     return f16x8_t{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
 }
 
@@ -536,7 +541,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             if (FAST) {
                 // 32-row tiles: acc[tt] holds rows 32 tt + n (lanes 0-31) and 32 tt + 16 + n
                 const f16x4_t kf = key_frag(sk[j0 + (lane & 31)], lane >> 5);
-                const f16x8_t a0 = xfrag32(sx, ldx, lane, j0), a1 = xfrag32(sx, ldx, lane, j0 + 16);
+                const f16x8_t a0 = frag32<true>(sx, ldx, lane, j0), a1 = frag32<true>(sx, ldx, lane, j0 + 16);
                 const f32x16_t z16 = {};
 #pragma unroll
                 for (int tt = 0; tt < NT / 2; ++tt) {
@@ -614,11 +619,12 @@ __host__ __device__ constexpr int attn_bwd_block_floats(int rpad, int W) {
 // needs no exponentials. The column sums C1_j = sum_i e_ij a_i, C2_j = sum_i e_ij a_i o_i,
 // C3_j = sum_i e_ij go_i / Z_i (a_i = go_i q_i / (Z_i tau)) give dk_j = v_j C1_j - C2_j and
 // dv_j = beta gh_j + C3_j (go = alpha gh). They run on the matrix cores with K over rows:
-// the exponent arguments come out of v_mfma_f32_16x16x16_f16 with the row records as A
+// the exponent arguments come out of v_mfma_f32_32x32x8_f16 with the row records as A
 // and the key fragments as B (the forward's product with its operands swapped, so each
-// e_ij is computed exactly as in the forward), which leaves lane (g, n) holding e of
-// key n for rows 4 g .. +3 and 16 + 4 g .. +3 of a 32-row block: the B operand of
-// v_mfma_f32_16x16x32_f16 against Y^T (rows: a hi, a lo, a o hi, a o lo, go/Z hi, lo).
+// e_ij is computed exactly as in the forward), which leaves lane l holding e of key
+// l % 32 for 16 rows of a 32-row block: the B operands of two v_mfma_f32_16x16x32_f16
+// against Y^T (rows: a hi, a lo, a o hi, a o lo, go/Z hi, lo), keys n and n + 16 in
+// output slots 0-7 and 8-15 (frag32).
 // A sample's waves split its keys (16 ATT_BWD_KT at a time); every wave runs over all rows.
 template <typename T, int W, int KB>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_attn_bwd_mfma(int64_t B, int r, int rpad, float alpha, float beta,
@@ -732,18 +738,70 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 
     const int g = lane >> 4, n = lane & 15;
     constexpr int KT = ATT_BWD_KT;
-    auto keys = [&](auto fast_c) {
-        constexpr bool FAST = decltype(fast_c)::value;
+    // Fast path: 32-key blocks. Arguments of 32 rows x 32 keys from one 32x32x8 MFMA
+    // (row records as A, key records as B: lane l gets key l % 32), then two column
+    // sums per block whose output lane (g4, n) holds quantities 4 (g4 & 1) .. +3 of
+    // key n + 16 (g4 / 2).
+    auto keys32 = [&]() {
+        constexpr int KB2 = KT / 2;
+        for (int j0 = 16 * KT * w; j0 < rpad; j0 += 16 * KT * W) {
+            f16x4_t kf[KB2];
+            float ev[KB2], eg[KB2];
+#pragma unroll
+            for (int q = 0; q < KB2; ++q) {
+                const int jl = j0 + 32 * q + (lane & 31), jp = jl < rpad ? jl : rpad - 1;
+                kf[q] = key_frag(sk[jp], lane >> 5);
+                const int j = j0 + 32 * q + n + 16 * (lane >> 5), jc = j < r ? j : r - 1;
+                ev[q] = pv[jc];
+                eg[q] = gh[jc];
+            }
+            f32x4_t col[KB2];
+#pragma unroll
+            for (int q = 0; q < KB2; ++q) col[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            const f32x16_t z16 = {};
+            for (int i0 = 0; i0 < rpad; i0 += 32) {
+                const f16x4_t rec = *(const f16x4_t*)(scm + i0 + (lane & 31));
+                const f16x8_t y0 = frag32<false>(sy, ldy, lane, i0), y1 = frag32<false>(sy, ldy, lane, i0 + 16);
+                f32x16_t x[KB2];
+#pragma unroll
+                for (int q = 0; q < KB2; ++q) x[q] = __builtin_amdgcn_mfma_f32_32x32x8f16(rec, kf[q], z16, 0, 0, 0);
+#pragma unroll
+                for (int q = 0; q < KB2; ++q) {
+                    float e0[8], e1[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        e0[u] = __builtin_amdgcn_exp2f(x[q][u]);
+                        e1[u] = __builtin_amdgcn_exp2f(x[q][8 + u]);
+                    }
+                    col[q] = __builtin_amdgcn_mfma_f32_16x16x32_f16(y0, __builtin_bit_cast(f16x8_t, pack_e(e0)), col[q], 0, 0, 0);
+                    col[q] = __builtin_amdgcn_mfma_f32_16x16x32_f16(y1, __builtin_bit_cast(f16x8_t, pack_e(e1)), col[q], 0, 0, 0);
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < KB2; ++q) {
+                const int j = j0 + 32 * q + n + 16 * (lane >> 5);
+                if (j < r) {
+                    if (((lane >> 4) & 1) == 0) {
+                        const float c1 = (col[q].x + col[q].y) * as, c2 = (col[q].z + col[q].w) * bs;
+                        st<T>::store(GP + b * ldgp + 2 * r + j, ev[q] * c1 - c2);
+                    } else {
+                        st<T>::store(GP + b * ldgp + j, beta * eg[q] + (col[q].x + col[q].y) * cs);
+                    }
+                }
+            }
+        }
+    };
+    // Slow path (arguments by FMA): 16-key tiles, lane (g, n) holds e of key n for
+    // rows 4 g .. +3 and 16 + 4 g .. +3 of each 32-row block.
+    auto keys_fma = [&]() {
         for (int j0 = 16 * KT * w; j0 < rpad; j0 += 16 * KT * W) {
             // keys j0 + 16 q + n of this lane (q < KT; past rpad the last key stands in and
             // nothing is stored); their epilogue operands, loaded now
-            f16x4_t kf[KT];
             float kv[KT], ev[KT], eg[KT];
 #pragma unroll
             for (int q = 0; q < KT; ++q) {
                 const int j = j0 + 16 * q + n, jp = j < rpad ? j : rpad - 1, jc = j < r ? j : r - 1;
                 kv[q] = sk[jp];
-                if (FAST) kf[q] = key_frag(kv[q], g);
                 ev[q] = pv[jc];
                 eg[q] = gh[jc];
             }
@@ -753,27 +811,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             for (int i0 = 0; i0 < rpad; i0 += 32) {
                 const f16x8_t ay = xfrag_perm(sy, ldy, n, 6, i0, g);
                 u32x4_t e[KT];
-                if (FAST) {
-                    const f16x4_t ra = *(const f16x4_t*)(scm + i0 + n);
-                    const f16x4_t rb = *(const f16x4_t*)(scm + i0 + 16 + n);
-                    const f32x4_t z = {0.f, 0.f, 0.f, 0.f};
-                    f32x4_t x0[KT], x1[KT];
-#pragma unroll
-                    for (int q = 0; q < KT; ++q) {
-                        x0[q] = __builtin_amdgcn_mfma_f32_16x16x16f16(ra, kf[q], z, 0, 0, 0);
-                        x1[q] = __builtin_amdgcn_mfma_f32_16x16x16f16(rb, kf[q], z, 0, 0, 0);
-                    }
-#pragma unroll
-                    for (int q = 0; q < KT; ++q) {
-                        float ex[8];
-#pragma unroll
-                        for (int t = 0; t < 4; ++t) {
-                            ex[t] = __builtin_amdgcn_exp2f(x0[q][t]);
-                            ex[4 + t] = __builtin_amdgcn_exp2f(x1[q][t]);
-                        }
-                        e[q] = pack_e(ex);
-                    }
-                } else {
+                {
                     // rows i0 + 4 g + t and i0 + 16 + 4 g + t (t < 4) of this lane's keys
                     float2 cm[8];
                     *(f32x4_t*)&cm[0] = *(const f32x4_t*)(scm + i0 + 4 * g);
@@ -809,8 +847,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             }
         }
     };
-    if (fast) keys(std::true_type{});
-    else keys(std::false_type{});
+    if (fast) keys32();
+    else keys_fma();
 }
 
 int attn_threads(int r) {
