@@ -25,7 +25,7 @@ struct rdcn_handle {
     // the backward's weight-gradient products run on `side`, forked from and joined
     // back to the caller's stream with these events (no timing)
     hipStream_t side = nullptr;
-    hipEvent_t ev_att = nullptr, ev_side[2] = {nullptr, nullptr};
+    hipEvent_t ev_pw = nullptr, ev_att = nullptr, ev_side[2] = {nullptr, nullptr};
     int* err;  // device error word
     bool head_on = false;
     rdcn_head_config head{};
@@ -369,7 +369,7 @@ rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
     }
     bool ok = hipMemset(h->err, 0, sizeof(int)) == hipSuccess && hipDeviceSynchronize() == hipSuccess;
     ok = ok && hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking) == hipSuccess;  // default priority
-    for (hipEvent_t* e : {&h->ev_att, &h->ev_side[0], &h->ev_side[1]})
+    for (hipEvent_t* e : {&h->ev_pw, &h->ev_att, &h->ev_side[0], &h->ev_side[1]})
         ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
     if (!ok) {
         (void)hipGetLastError();
@@ -384,7 +384,7 @@ rdcn_status rdcn_destroy(rdcn_handle* h) {
     if (!h) return RDCN_OK;
     rdcn_status s = RDCN_OK;
     for (hipEvent_t e : h->prof_ev) (void)hipEventDestroy(e);
-    for (hipEvent_t e : {h->ev_att, h->ev_side[0], h->ev_side[1]})
+    for (hipEvent_t e : {h->ev_pw, h->ev_att, h->ev_side[0], h->ev_side[1]})
         if (e && hipEventDestroy(e) != hipSuccess) s = RDCN_ERR_HIP;
     if (h->side && hipStreamDestroy(h->side) != hipSuccess) s = RDCN_ERR_HIP;
     if (h->err && hipFree(h->err) != hipSuccess) s = RDCN_ERR_HIP;
@@ -638,7 +638,8 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
     // gradient to the next. Side stream, once the layer's attention is done: the bias
     // column sums and the weight gradients gU and gW (with their split-K reductions),
     // which nothing later in the backward reads; they overlap gx and the next layer's
-    // pointwise and gh (started earlier, they slow the attention more than they gain).
+    // pointwise and gh (started earlier, they slow the attention more than they gain;
+    // layer 0, the last, starts its bias sums and gU after its pointwise kernel).
     for (int l = c.num_layers - 1; l >= 0; --l) {
         const bool top = l == c.num_layers - 1;
         const int par = l & 1;
@@ -660,6 +661,31 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
         const int64_t ldh = h->attn ? hr : nr;
         const float hscale = h->attn ? 1.0f : c.skip_beta;
         const int64_t e = (int64_t)eb(h);
+        // bias sums and gU on the side stream
+        auto side_bias_gu = [&]() -> rdcn_status {
+            {
+                ProfScope ps(h, RDCN_KERNEL_BWD_BIAS, side);
+                RDCN_TRY(launch_colsum(part, W.nrb, d, (float*)grads->bias[l], side));
+            }
+            // gU = gt^T h      [d, hr], K = batch
+            {
+                GemmArgs g1{};
+                g1.M = d; g1.N = hr; g1.K = B;
+                g1.a = gt; g1.lda = d; g1.a_kstrided = true;
+                g1.b = hsrc; g1.ldb = ldh; g1.b_kstrided = true;
+                g1.scale = hscale;
+                RDCN_TRY(gemm_weight_grad(h, RDCN_KERNEL_BWD_GU_GEMM, g1, (float*)grads->u[l], splitk, side));
+            }
+            return RDCN_OK;
+        };
+        // Layer 0 forks its bias sums and gU right after the pointwise kernel: nothing
+        // follows its gx on the main stream, so side work left until after the attention
+        // would run alone while the main stream waits to join.
+        if (l == 0) {
+            RDCN_TRY(hipEventRecord(h->ev_pw, s));
+            RDCN_TRY(hipStreamWaitEvent(side, h->ev_pw, 0));
+            if ((st = side_bias_gu()) != RDCN_OK) return st;
+        }
         // gh = gt U         [B, hr]; with parallel branches the plain branch's part is its
         // value gradient and goes straight into the first columns of gP
         if (h->par) {
@@ -693,19 +719,7 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
         }
         RDCN_TRY(hipEventRecord(h->ev_att, s));
         RDCN_TRY(hipStreamWaitEvent(side, h->ev_att, 0));
-        {
-            ProfScope ps(h, RDCN_KERNEL_BWD_BIAS, side);
-            RDCN_TRY(launch_colsum(part, W.nrb, d, (float*)grads->bias[l], side));
-        }
-        // gU = gt^T h      [d, hr], K = batch
-        {
-            GemmArgs g1{};
-            g1.M = d; g1.N = hr; g1.K = B;
-            g1.a = gt; g1.lda = d; g1.a_kstrided = true;
-            g1.b = hsrc; g1.ldb = ldh; g1.b_kstrided = true;
-            g1.scale = hscale;
-            RDCN_TRY(gemm_weight_grad(h, RDCN_KERNEL_BWD_GU_GEMM, g1, (float*)grads->u[l], splitk, side));
-        }
+        if (l > 0 && (st = side_bias_gu()) != RDCN_OK) return st;
         // gW = gP^T x_l    [n r, d], K = batch
         {
             GemmArgs g3{};
