@@ -57,7 +57,10 @@ struct GemmPlan {
     int stages = 3;  // LDS ring depth (2 lets two workgroups share a CU)
 };
 
-GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool bf16, bool allow_split);
+// split_blocks: with split-K allowed, the workgroup count the K split aims for when
+// the output tiles alone are fewer than 256 (a product that runs beside other
+// kernels does better with fewer, longer splits).
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool bf16, bool allow_split, int split_blocks = 384);
 hipError_t launch_gemm(const GemmArgs& g, const GemmPlan& p, bool bf16, hipStream_t s);
 // Column tiles of an MLP GEMM under plan p (the rowpart partials per row).
 inline int64_t gemm_tiles_n(int64_t N, const GemmPlan& p) { return (N + p.bn - 1) / p.bn; }

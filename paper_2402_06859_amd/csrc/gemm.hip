@@ -729,7 +729,7 @@ hipError_t launch_tile(const GemmArgs& g, int splits, hipStream_t s) {
 
 }  // namespace
 
-GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool bf16, bool allow_split) {
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool bf16, bool allow_split, int split_blocks) {
     GemmPlan p;
     if (!bf16) {
         p.bm = p.bn = 64;
@@ -743,7 +743,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool bf16, bool allow_split)
     const int64_t tiles = ((M + p.bm - 1) / p.bm) * ((N + p.bn - 1) / p.bn);
     p.splits = 1;
     if (allow_split && tiles < 256) {
-        int64_t s = (384 + tiles - 1) / tiles;
+        int64_t s = (split_blocks + tiles - 1) / tiles;
         const int64_t kmax = K / 512;  // keep >= 8 K steps of 64 per split
         if (s > kmax) s = kmax;
         if (s > 16) s = 16;
