@@ -129,16 +129,19 @@ struct ScratchLayout {
 };
 
 // Split-K target of the backward's weight-gradient GEMMs, which run on the side
-// stream beside the main chain: fewer splits leave more of the chip to the main
-// stream and shrink the partials the reduction reads (384, the full-chip target:
-// 0.749 ms per small step; 192: 0.733; 128: 0.726; 64: slower again, the GEMMs
-// themselves grow too long).
-constexpr int BWD_SPLIT_BLOCKS = 128;
+// stream beside the main chain. Below 8e9 multiply-adds fewer splits leave more of
+// the chip to the main stream and shrink the partials the reduction reads (384, the
+// full-chip target: 0.749 ms per small step; 192: 0.733; 128: 0.726; 64: slower
+// again); larger products (feed: 3.7e10) outlast the main chain with fewer splits
+// (4.23 -> 4.81 ms per feed step at 128) and keep 384.
+int bwd_split_blocks(int64_t M, int64_t N, int64_t K) {
+    return (double)M * (double)N * (double)K < 8.0e9 ? 128 : 384;
+}
 
 int64_t splitk_elems(const rdcn_handle* h, int64_t B) {
     const int64_t d = h->d, r = h->cfg.rank, nr = (int64_t)h->n * r, hr = h->hr;
-    const GemmPlan pu = plan_gemm(d, hr, B, h->bf16, true, BWD_SPLIT_BLOCKS);
-    const GemmPlan pw = plan_gemm(nr, d, B, h->bf16, true, BWD_SPLIT_BLOCKS);
+    const GemmPlan pu = plan_gemm(d, hr, B, h->bf16, true, bwd_split_blocks(d, hr, B));
+    const GemmPlan pw = plan_gemm(nr, d, B, h->bf16, true, bwd_split_blocks(nr, d, B));
     int64_t m = 0;
     if (pu.splits > 1) m = pu.splits * d * hr;
     if (pw.splits > 1 && pw.splits * nr * d > m) m = pw.splits * nr * d;
@@ -682,7 +685,8 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
                 g1.a = gt; g1.lda = d; g1.a_kstrided = true;
                 g1.b = hsrc; g1.ldb = ldh; g1.b_kstrided = true;
                 g1.scale = hscale;
-                RDCN_TRY(gemm_weight_grad(h, RDCN_KERNEL_BWD_GU_GEMM, g1, (float*)grads->u[l], splitk, side, BWD_SPLIT_BLOCKS));
+                RDCN_TRY(gemm_weight_grad(h, RDCN_KERNEL_BWD_GU_GEMM, g1, (float*)grads->u[l], splitk, side,
+                                          bwd_split_blocks(g1.M, g1.N, g1.K)));
             }
             return RDCN_OK;
         };
@@ -735,7 +739,8 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
             g3.a = gP; g3.lda = nr; g3.a_kstrided = true;
             g3.b = xl; g3.ldb = d; g3.b_kstrided = true;
             g3.scale = 1.0f;
-            RDCN_TRY(gemm_weight_grad(h, RDCN_KERNEL_BWD_GW_GEMM, g3, (float*)grads->w_down[l], splitk, side, BWD_SPLIT_BLOCKS));
+            RDCN_TRY(gemm_weight_grad(h, RDCN_KERNEL_BWD_GW_GEMM, g3, (float*)grads->w_down[l], splitk, side,
+                                      bwd_split_blocks(g3.M, g3.N, g3.K)));
         }
         RDCN_TRY(hipEventRecord(h->ev_side[par], side));
         // g_l = g_{l+1} + gP W   (layer 0: grad_x0 += g_1 + gP W)
