@@ -1,18 +1,21 @@
 """Benchmark: samples/s of one training step of the QR-embedding + Residual-DCN path.
 
 One step = qr_embed_gather -> rdcn_forward -> rdcn_backward -> qr_embed_backward
-on one synthetic batch already resident in HBM (the "small" workload: batch
-4096, 50 single-hot features QR-hashed into 1000 x 32 tables, 256 dense
-features, d = 1856, 3 Residual-DCN layers of rank 256 with the attention term,
-bf16 storage with float accumulation).
+on one synthetic batch already resident in HBM. The default workload is the
+largest one that fits one GPU ("large": batch 32768, 200 single-hot features
+QR-hashed into 4473 x 48 tables, 1024 dense features, d = 10624, 6 Residual-DCN
+layers of rank 1024 with the attention term, bf16 weights and storage with float
+accumulation, activations x_l and h held in f16).
 
-Prints ONE JSON line. Besides throughput it carries:
-  roofline      -- the kernel with the largest share of the timed region:
-                   algorithmic work per launch / average launch time, measured
-                   with HIP events on the launch stream during the timed steps
-  cpu_baseline  -- the CPU oracle (oracle/, single-threaded C) timed on a
-                   bounded sub-batch of the same workload on this host
-  kernels       -- average microseconds per launch and launches per step
+Prints ONE JSON line. Besides throughput (timed over the steps alone, no
+per-kernel events) it carries:
+  roofline      -- the kernel with the largest share of a step: algorithmic work
+                   per launch / average launch time, measured with HIP events on
+                   the launch stream over as many steps again, run after the timed
+                   region with every kernel alone on the stream
+  cpu_baseline  -- the CPU oracle (oracle/: plain C loops) timed on this host on a
+                   bounded sub-batch of the same workload, one process per core
+  kernels, phases -- per-kernel average times and each against its own bound
 """
 from __future__ import annotations
 
@@ -36,8 +39,13 @@ PEAK_HBM_GBS = 8000.0
 # Issue cost of one v_exp_f32 in FMA slots (measured on MI355X: an exp + add chain
 # runs at ~14.7 T/s against ~39 T FMA slots/s, i.e. about two slots per exp).
 EXP_SLOTS = 2.0
-# Measured v_exp_f32 throughput on MI355X (an exp + add chain over all CUs).
-EXP_PEAK_PER_S = 14.7e12
+# Exponential rate of the chip: one wave-wide v_exp_f32 issues every 8 clocks per SIMD
+# (measured: 8.1 clk; half the rate of a plain VALU op), so 256 CUs x 4 SIMDs x 8 lanes
+# per clock x 2.4 GHz = 19.66 T exp/s. The attention kernels' roofline is this rate.
+EXP_PEAK_PER_S = 256 * 4 * 8 * 2.4e9
+# Measured rate of independent exp + add pairs over all CUs (an exponential and one
+# more VALU op per pair, as a softmax needs at least): a practical ceiling beside the peak.
+EXP_ADD_MEASURED_PER_S = 14.7e12
 
 
 def kernel_work(wl, B: int) -> dict:
@@ -139,6 +147,10 @@ def _radix_passes(maxkey: int) -> int:
 
 def roofline_for(name: str, work: tuple, avg_s: float, bf16: bool) -> dict:
     flops, nbytes, alu = work
+    if bf16 and name in ("fwd_attention", "bwd_attention"):
+        # exponential-bound: one exp per (query, key) pair; alu holds 7 FMA-equivalent flops per pair
+        exps = alu / 7.0
+        return {"bound": "exp", "achieved": exps / avg_s / 1e12, "peak": EXP_PEAK_PER_S / 1e12, "unit": "Texp/s"}
     if alu > 0:
         return {"bound": "alu", "achieved": alu / avg_s / 1e12, "peak": PEAK_F32_UNPACKED_TFLOPS, "unit": "TFLOP/s"}
     peak_f = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
@@ -210,15 +222,42 @@ def phase_rooflines(work: dict, prof: dict, bf16: bool) -> dict:
 
 def gather_counter_gbps(wl, prof: dict):
     """HBM bytes of the gather from the FETCH_SIZE / WRITE_SIZE summaries under profiles/
-    (while its sources are unchanged) over its measured launch time."""
+    (while its sources are unchanged) over its measured launch time; None without a
+    matching counter record."""
     t = measured_traffic("gather", wl.name)
     ms, n = prof.get("gather", (0.0, 0))
     return t / (ms / n / 1e3) / 1e9 if (t is not None and n) else None
 
 
+def mfma_counter_rates(wl, tag: str, prof: dict) -> dict:
+    """Matrix-core flops per launch of each GEMM phase from the MFMA counter summaries
+    under profiles/ (lines 'mfma: {json}' with SQ_INSTS_VALU_MFMA_MOPS_BF16 / _F16 x 512
+    flops, while the GEMM sources are unchanged) over the phase's measured launch time:
+    {phase: {"tflops", "frac", "busy"}} (busy: SQ_VALU_MFMA_BUSY_CYCLES over SQ_BUSY_CU_CYCLES
+    when recorded)."""
+    import glob
+    out = {}
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        with open(path) as fh:
+            for line in fh:
+                if not line.startswith("mfma: "):
+                    continue
+                rec = json.loads(line[len("mfma: "):])
+                k = rec.get("kernel")
+                if rec.get("workload") != tag or k not in KERNEL_SOURCES or rec.get("sha256") != sources_sha256(k):
+                    continue
+                ms, n = prof.get(k, (0.0, 0))
+                if not n:
+                    continue
+                tf = rec["flops_per_launch"] / (ms / n / 1e3) / 1e12
+                out[k] = {"tflops": tf, "frac": tf / PEAK_BF16_TFLOPS, "busy": rec.get("mfma_busy")}
+    return out
+
+
 def attention_exp_rate(wl, B: int, prof: dict):
     """Exponentials per second of the attention kernels (one per (query, key) pair in the
-    forward and one in the backward) and the fraction of the measured v_exp_f32 rate."""
+    forward and one in the backward) against the chip's exponential rate and against the
+    measured exp + add rate."""
     if not wl.attention:
         return None
     out = {}
@@ -226,58 +265,112 @@ def attention_exp_rate(wl, B: int, prof: dict):
         ms, n = prof.get(k, (0.0, 0))
         if n:
             rate = B * wl.rank * wl.rank / (ms / n / 1e3)
-            out[k] = {"exp_per_s": rate, "frac_of_measured_peak": rate / EXP_PEAK_PER_S}
+            out[k] = {"exp_per_s": rate, "frac_of_peak": rate / EXP_PEAK_PER_S,
+                      "frac_of_measured_exp_add_rate": rate / EXP_ADD_MEASURED_PER_S}
     return out
 
 
-def cpu_baseline(wl, target_s: float, head=None) -> dict:
-    """The oracle timed on a sub-batch sized to about `target_s` seconds, single-threaded
-    (the C oracle is; numpy's BLAS is held to one thread): one step = gather + forward
-    + backward (which recomputes its forward) + embedding backward, and with a head its
-    forward and backward (numpy float64) between the cross stack's."""
+def host_info() -> dict:
+    """The host's logical CPU count, CPU model and available memory (for the CPU baseline)."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    avail = None
+    try:
+        with open("/proc/meminfo") as fh:
+            for line in fh:
+                if line.startswith("MemAvailable:"):
+                    avail = int(line.split()[1]) * 1024
+                    break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "cpu_model": model, "mem_available_bytes": avail}
+
+
+def oracle_worker_bytes(wl) -> float:
+    """Host memory one oracle process needs: the weights and their gradients in float64 (the
+    C oracle's working copies), the storage-type and float32 copies of the inputs, and the
+    tables (an upper estimate; the large workload measured 6.4 GB for 8.4 GB estimated)."""
+    d, r, n, L = wl.d, wl.rank, wl.n_proj, wl.num_layers
+    params = L * (n * r * d + d * wl.h_width + d)
+    tables = 2 * wl.table_pairs * wl.num_cat * wl.table_rows * wl.emb_dim
+    return params * (8 * 2 + 4 + 2 + 8) + tables * 14 + (1 << 30)
+
+
+def _oracle_proc(wl, rows: int, head, seed: int, barrier, queue) -> None:
+    """One baseline worker: draw its inputs, wait for the others, then time its oracle step
+    (start and end on the system-wide monotonic clock)."""
     from threadpoolctl import threadpool_limits
-    probe = 8
+    with threadpool_limits(limits=1):
+        state = _oracle_prepare(wl, rows, head, seed)
+        barrier.wait()
+        t0 = time.perf_counter()
+        _oracle_run(state)
+        queue.put((t0, time.perf_counter()))
+
+
+def cpu_baseline(wl, target_s: float, head=None) -> dict:
+    """The oracle (oracle/: plain C loops, single-threaded, plus numpy float64 for a head)
+    timed on this host: one step = gather + forward + backward (which recomputes its
+    forward) + embedding backward on a sub-batch, in one single-threaded process per
+    host core (at most 16, and no more than half the available memory holds). Each
+    worker's sub-batch is sized from a single-threaded probe (8 rows, or 1 row on
+    workloads with more than 2e7 cross-stack weights) to about `target_s` seconds. The
+    workers draw their inputs, wait for each other, then time their steps; the value is
+    the total rows over the span from the first start to the last end, and
+    `single_thread_value` is the workers' mean own rate."""
+    import multiprocessing as mp
+    from threadpoolctl import threadpool_limits
+    info = host_info()
+    per_worker = oracle_worker_bytes(wl)
+    workers = max(1, min(16, info["nproc"] or 1))
+    if info["mem_available_bytes"]:
+        workers = max(1, min(workers, int(0.5 * info["mem_available_bytes"] // per_worker)))
+    probe = 1 if wl.d * wl.rank * wl.num_layers > 2e7 else 8
     with threadpool_limits(limits=1):
         t = _oracle_step(wl, probe, head)
-        rows = int(max(16, min(wl.batch, round(probe * target_s / max(t, 1e-6)))))
-        dt = _oracle_step(wl, rows, head)
-    return {"value": rows / dt, "unit": "samples/s", "cores": 1, "kind": "oracle",
-            "sample": "%d samples of the %s workload (gather + forward + backward + embedding backward%s), "
-                      "%.1f s, single-threaded" % (rows, wl.name, " + head" if head is not None else "", dt)}
-
-
-def _oracle_worker(wl, rows: int, head, seed: int) -> float:
-    from threadpoolctl import threadpool_limits
-    with threadpool_limits(limits=1):
-        return _oracle_step(wl, rows, head, seed)
-
-
-def cpu_baseline_parallel(wl, target_s: float, head, single: dict) -> dict:
-    """The same oracle step in one single-threaded process per host core (at most 16),
-    each on its own sub-batch of about `target_s` seconds of work; samples/s is the
-    total over the wall time of the pool (the table gradients stay per process)."""
-    import multiprocessing as mp
-    workers = max(1, min(16, os.cpu_count() or 1))
-    rows = int(max(16, min(wl.batch, round(single["value"] * target_s))))
+    rows = int(max(1, min(wl.batch, round(probe * target_s / max(t, 1e-6)))))
     ctx = mp.get_context("spawn")
-    with ctx.Pool(workers) as pool:
-        pool.starmap(_oracle_worker, [(wl, 8, head, i) for i in range(workers)])  # import and build once
-        t0 = time.perf_counter()
-        pool.starmap(_oracle_worker, [(wl, rows, head, i) for i in range(workers)])
-        wall = time.perf_counter() - t0
+    barrier, queue = ctx.Barrier(workers), ctx.Queue()
+    procs = [ctx.Process(target=_oracle_proc, args=(wl, rows, head, i, barrier, queue)) for i in range(workers)]
+    for p in procs:
+        p.start()
+    spans = [queue.get() for _ in procs]
+    for p in procs:
+        p.join()
+        if p.exitcode != 0:
+            raise RuntimeError("oracle baseline worker failed (exit code %s)" % p.exitcode)
+    wall = max(e for _, e in spans) - min(b for b, _ in spans)
+    times = [e - b for b, e in spans]
     return {"value": workers * rows / wall, "unit": "samples/s", "cores": workers, "kind": "oracle",
-            "sample": "%d processes x %d samples of the %s workload%s, %.1f s wall, one oracle per core"
-                      % (workers, rows, wl.name, " + head" if head is not None else "", wall)}
+            "sample": "%d processes x %d sample%s of the %s workload (gather + forward + backward + embedding "
+                      "backward%s), %.1f s wall, one single-threaded oracle per core"
+                      % (workers, rows, "" if rows == 1 else "s", wl.name, " + head" if head is not None else "",
+                         wall),
+            "single_thread_value": rows / (sum(times) / len(times)),
+            "nproc": info["nproc"], "cpu_model": info["cpu_model"],
+            "worker_memory_bytes_estimate": per_worker}
 
 
 def _oracle_step(wl, rows: int, head=None, seed=None) -> float:
+    return _oracle_run(_oracle_prepare(wl, rows, head, seed))
+
+
+def _oracle_prepare(wl, rows: int, head=None, seed=None) -> dict:
+    """Inputs of one oracle step (drawn, not timed)."""
     import oracle
     from paper_2402_06859_amd.synth import make_inputs
+    oracle.lib()  # load the C oracle before anything is timed
     inp = make_inputs(wl, batch=rows, bias_std=0.0, seed=None if seed is None else 1000 + seed)
     W = [x.float().numpy() for x in inp["w_down"]]
     U = [x.float().numpy() for x in inp["u"]]
     b = [x.float().numpy() for x in inp["bias"]]
-    F, D, Nd, m, bf16 = wl.num_cat, wl.emb_dim, wl.num_dense, wl.table_rows, wl.dtype == "bf16"
     if head is not None:
         from paper_2402_06859_amd.synth import make_head_inputs
         hinp = make_head_inputs(wl, head, batch=rows, with_x=False)
@@ -289,6 +382,18 @@ def _oracle_step(wl, rows: int, head=None, seed=None) -> float:
             hp["G"] = [f64(g) for g in hinp["G"]]
             hp["c"] = [float(c.float()[0]) for c in hinp["c"]]
         labels = f64(hinp["labels"])
+    else:
+        hp = labels = None
+    return {"wl": wl, "rows": rows, "head": head, "inp": inp, "W": W, "U": U, "b": b, "hp": hp, "labels": labels}
+
+
+def _oracle_run(state: dict) -> float:
+    """Seconds of one oracle step: gather, forward, (head forward, loss and backward),
+    backward (which recomputes its forward), embedding backward."""
+    import oracle
+    wl, rows, head, inp = state["wl"], state["rows"], state["head"], state["inp"]
+    W, U, b, hp, labels = state["W"], state["U"], state["b"], state["hp"], state["labels"]
+    F, D, Nd, m, bf16 = wl.num_cat, wl.emb_dim, wl.num_dense, wl.table_rows, wl.dtype == "bf16"
     t0 = time.perf_counter()
     if wl.hashed:
         x0 = oracle.gather_hashed(rows, F, D, Nd, m, m, wl.combine, bf16, wl.hash_seed, inp["ids"], inp["offsets"],
@@ -375,8 +480,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="small")
+    ap.add_argument("--workload", default="large",
+                    help="tiny, small, feed, multihot or large (the default: the largest single-GPU one)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle time budget for cpu_baseline (0 = skip)")
+    ap.add_argument("--side-stream", default="on", choices=["on", "off"],
+                    help="run the backward's weight-gradient work on a second stream during the timed steps")
+    ap.add_argument("--no-q8", action="store_true", help="skip the 8-bit serving-gather comparison")
     ap.add_argument("--id-mode", default="scatter", choices=["scatter", "rank"])
     ap.add_argument("--hashed", action="store_true",
                     help="Murmur-hashed front-end: raw ids hashed, two QR table pairs of 2^16 + 2^16 rows per feature")
@@ -421,16 +530,15 @@ def main():
     if args.hashed:
         wl = wl.with_(hashed=True, table_rows=1 << 16)
     head = HEADS[args.head] if args.head else None
-    # the CPU baselines run before anything touches the GPU (their worker processes
-    # are started from a process that has not initialised it)
-    cpu = cpu_par = None
-    if args.cpu_seconds > 0:
-        cpu = cpu_baseline(wl, args.cpu_seconds, head)
-        cpu_par = cpu_baseline_parallel(wl, args.cpu_seconds, head, cpu)
+    # the CPU baseline runs before anything touches the GPU (its worker processes are
+    # started from a process that has not initialised it)
+    cpu = cpu_baseline(wl, args.cpu_seconds, head) if args.cpu_seconds > 0 else None
     torch.cuda.set_device(0)
     inp = make_inputs(wl, id_mode=args.id_mode)
     db = DeviceBatch(wl, inp)
     B = db.B
+    side_on = args.side_stream == "on"
+    db.lib.set_side_stream(side_on)
     if head is not None:
         dh = DeviceHead(db.lib, head, make_head_inputs(wl, head, with_x=False), B)
         step = lambda: dh.tower_step(db)
@@ -442,17 +550,7 @@ def main():
     if db.lib.check_device_errors() != rdcn.RDCN_OK:
         raise RuntimeError("device error flag raised during warm-up")
 
-    # find the kernel with the largest share of a step (all launch sites timed, untimed step)
-    db.lib.profile_start(4096)
-    step()
-    prof = db.lib.profile_stop()
-    work = kernel_work(wl, B)
-    if head is not None:
-        work.update(head_work(wl, head, B))
-    dominant = max((k for k in prof if k in work), key=lambda k: prof[k][0])
-
-    # timed region: only the dominant kernel's launches carry events
-    db.lib.profile_start(4 * args.steps * 64, [dominant])
+    # timed region: the steps alone, no per-kernel events
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -464,24 +562,47 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     ms = e0.elapsed_time(e1)
-    dom = db.lib.profile_stop()[dominant]
-    status = db.lib.check_device_errors()
-    if status != rdcn.RDCN_OK:
+    if db.lib.check_device_errors() != rdcn.RDCN_OK:
         raise RuntimeError("device error flag raised during the timed steps")
+
+    # per-kernel times, measured after the timed region with every kernel running alone
+    # (the backward's weight-gradient work on the caller's stream): one step with events
+    # around every launch finds the kernel with the largest share, then `steps` steps with
+    # events around that kernel's launches only give its roofline
+    db.lib.set_side_stream(False)
+    db.lib.profile_start(4096)
+    step()
+    prof = db.lib.profile_stop()
+    work = kernel_work(wl, B)
+    if head is not None:
+        work.update(head_work(wl, head, B))
+    dominant = max((k for k in prof if k in work), key=lambda k: prof[k][0])
+    db.lib.profile_start(4 * args.steps * 64, [dominant])
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    dom = db.lib.profile_stop()[dominant]
+    db.lib.set_side_stream(side_on)
 
     ms_step = ms / args.steps
     avg_s = dom[0] / dom[1] / 1e3
     roof = roofline_for(dominant, work[dominant], avg_s, wl.dtype == "bf16")
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = measured_traffic(dominant, wl.name + ("+" + head.name if head is not None else ""))
+    tag = wl.name + ("+" + head.name if head is not None else "")
+    roof["traffic"] = measured_traffic(dominant, tag)
     roof["kernel"] = dominant
     roof["avg_us"] = avg_s * 1e6
     roof["launches"] = dom[1]
+    roof["measured"] = "HIP events on the launch stream, %d steps after the timed region, kernels run alone" \
+                       % args.steps
+    if roof["bound"] == "exp":
+        roof["frac_of_measured_exp_add_rate"] = roof["achieved"] * 1e12 / EXP_ADD_MEASURED_PER_S
 
     kernels = {k: {"avg_us": (v[0] / v[1] * 1e3) if v[1] else 0.0, "per_step": v[1]} for k, v in prof.items() if v[1]}
     gemm_flops = sum(work[k][0] * prof[k][1] for k in work if k.endswith("_gemm") and k in prof)
     gemm_s = sum(prof[k][0] for k in prof if k.endswith("_gemm")) / 1e3
-    gather_s = prof["gather"][0] / 1e3 if prof["gather"][1] else 0.0
+    gather_s = prof["gather"][0] / prof["gather"][1] / 1e3 if prof["gather"][1] else 0.0
+    counter_gbps = gather_counter_gbps(wl, prof)
     out = {
         "metric": METRIC,
         "value": B * args.steps / (ms / 1e3),
@@ -496,35 +617,46 @@ def main():
         "vs_baseline": None,
         "dtype": wl.dtype,
         "data": "synthetic (seeded Zipf ids, N(0,1) dense, Xavier weights); inputs resident in HBM",
-        "config": {"workload": "%s: batch %d, %d single-hot features (vocab %d, QR tables %dx%d, %s combine), "
-                               "%d dense, d=%d, %d Residual-DCN layers rank %d, attention %s%s"
-                               % (wl.name, B, wl.num_cat, wl.vocab, wl.table_rows, wl.emb_dim, wl.combine,
-                                  wl.num_dense, wl.d, wl.num_layers, wl.rank, "on" if wl.attention else "off",
-                                  ", parallel plain branch" if wl.parallel else "")
-                               + (", Murmur-hashed ids (two QR pairs of 2^16 x 2^16 rows per feature)"
-                                  if wl.hashed else "")
-                               + ("; head: %s%d x %s ReLU layers, logit, isotonic calibration (%d buckets), log loss"
-                                  % ("gated " if head.gated else "", len(head.hidden),
-                                     "/".join(str(v) for v in sorted(set(head.hidden))), head.buckets)
-                                  if head is not None else ""),
-                   "global_batch": B, "id_mode": args.id_mode},
+        "config": {"workload": workload_description(wl, B, head), "global_batch": B, "id_mode": args.id_mode,
+                   "side_stream": args.side_stream},
         "roofline": roof,
         "gemm_mfma_frac": (gemm_flops / gemm_s / 1e12 / PEAK_BF16_TFLOPS) if gemm_s > 0 else None,
-        "gather_gbps": (work["gather"][1] / gather_s / 1e9) if gather_s > 0 else None,
-        "gather_hbm_frac": (work["gather"][1] / gather_s / 1e9 / PEAK_HBM_GBS) if gather_s > 0 else None,
-        "gather_counter_gbps": gather_counter_gbps(wl, prof),
+        "gemm_phases_tflops": {k: work[k][0] / (prof[k][0] / prof[k][1] / 1e3) / 1e12
+                               for k in work if k.endswith("_gemm") and prof.get(k, (0, 0))[1]},
+        "gather_hbm_frac": counter_gbps / PEAK_HBM_GBS if counter_gbps is not None else None,
+        "gather_counter_gbps": counter_gbps,
+        "gather_model_gbps": (work["gather"][1] / gather_s / 1e9) if gather_s > 0 else None,
+        "gather_model_frac": (work["gather"][1] / gather_s / 1e9 / PEAK_HBM_GBS) if gather_s > 0 else None,
         "attention_exp_per_s": attention_exp_rate(wl, B, prof),
         "phases": phase_rooflines(work, prof, wl.dtype == "bf16"),
         "kernels": kernels,
     }
-    if wl.num_cat > 0:
+    mfma = mfma_counter_rates(wl, tag, prof)
+    if mfma:
+        out["gemm_counter_tflops"] = mfma
+    if wl.num_cat > 0 and not args.no_q8:
         out["gather_q8"] = time_gather_q8(db, work["gather_q8"][1], work["gather"][1])
     if args.graph:
         out["graph"] = time_graph_replays(step, args.steps, B)
     if cpu is not None:
         out["cpu_baseline"] = cpu
-        out["cpu_baseline_all_cores"] = cpu_par
     print(json.dumps(out), flush=True)
+
+
+def workload_description(wl, B: int, head) -> str:
+    hot = ("%d multi-hot features (bags ~Poisson(%g) in [%d, %d])" % (wl.num_cat, wl.bag_mean, wl.bag_min, wl.bag_max)
+           if wl.multi_hot else "%d single-hot features" % wl.num_cat)
+    act = {"storage": "", "hilo": ", activations as bf16 hi + lo pairs",
+           "f16": ", activations x_l and h held in f16 (bf16 weights and storage)"}[wl.act_mode]
+    return ("%s: batch %d, %s (vocab %d, QR tables %dx%d, %s combine), %d dense, d=%d, %d Residual-DCN layers "
+            "rank %d, attention %s%s%s" % (wl.name, B, hot, wl.vocab, wl.table_rows, wl.emb_dim, wl.combine,
+                                          wl.num_dense, wl.d, wl.num_layers, wl.rank,
+                                          "on" if wl.attention else "off",
+                                          ", parallel plain branch" if wl.parallel else "", act)
+            + (", Murmur-hashed ids (two QR pairs of 2^16 x 2^16 rows per feature)" if wl.hashed else "")
+            + ("; head: %s%d x %s ReLU layers, logit, isotonic calibration (%d buckets), log loss"
+               % ("gated " if head.gated else "", len(head.hidden),
+                  "/".join(str(v) for v in sorted(set(head.hidden))), head.buckets) if head is not None else ""))
 
 
 if __name__ == "__main__":

@@ -55,12 +55,32 @@ typedef enum rdcn_status {
     RDCN_ERR_INDEX = 3,        /* an id outside [0, vocab) was met on the device */
     RDCN_ERR_UNSUPPORTED = 4,  /* valid but not supported here (see rdcn_create) */
     RDCN_ERR_WORKSPACE = 5,    /* a workspace or buffer argument is too small */
-    RDCN_ERR_HIP = 6           /* a HIP runtime call or kernel launch failed */
+    RDCN_ERR_HIP = 6,          /* a HIP runtime call or kernel launch failed */
+    RDCN_ERR_RANGE = 7         /* an activation kept as f16 (activation mode 2) was beyond the
+                                  f16 range (|x| >= 65520) and became infinite */
 } rdcn_status;
 
 typedef enum rdcn_dtype { RDCN_F32 = 0, RDCN_BF16 = 1 } rdcn_dtype;
 typedef enum rdcn_idtype { RDCN_I32 = 0, RDCN_I64 = 1 } rdcn_idtype;
 typedef enum rdcn_combine { RDCN_COMBINE_MUL = 0, RDCN_COMBINE_SUM = 1 } rdcn_combine;
+
+/*
+ * Precision of the activations the projections read (bf16 models; float models
+ * keep everything in float). The paper fixes no precision for the cross stack;
+ * deep attention stacks whose softmax ends close to one-hot amplify any rounding of
+ * x_l and h, so the library offers three ways to hold them:
+ *   RDCN_ACT_STORAGE: x_l and h in bf16, the storage type (one bf16 MFMA pass each)
+ *   RDCN_ACT_HILO:    x_l (l >= 1) and h as bf16 hi + lo pairs whose sum carries about
+ *                     16 significant bits; the down and up projections run two bf16
+ *                     MFMA passes over them against the exact bf16 weights
+ *   RDCN_ACT_F16:     x_l (l >= 1) and h in f16 (11 significant bits; |x| < 65520, else
+ *                     RDCN_ERR_RANGE is flagged); the down (l >= 1) and up projections
+ *                     run one f16 MFMA pass against f16 copies of the weights that
+ *                     rdcn_forward makes in its scratch (bf16 weights of magnitude
+ *                     >= 2^-17 convert exactly); bf16 copies of x_l and h feed the
+ *                     weight gradients
+ */
+typedef enum rdcn_act_mode { RDCN_ACT_STORAGE = 0, RDCN_ACT_HILO = 1, RDCN_ACT_F16 = 2 } rdcn_act_mode;
 
 #define RDCN_MAX_LAYERS 16
 
@@ -83,9 +103,8 @@ typedef struct rdcn_config {
     int32_t multi_hot;    /* 0: one id per (sample, feature); 1: CSR bags, sum pooling */
     int32_t id_type;      /* rdcn_idtype of the id array */
     int32_t dtype;        /* rdcn_dtype of tables, dense, x0, activations and weights */
-    int32_t split_activations; /* 0 or 1, bf16 only: keep x_l (l >= 1) and h as hi + lo bf16
-                                  pairs (about 16 significant bits) and run the down and
-                                  up projections as two bf16 MFMA passes over them */
+    int32_t activation_mode; /* rdcn_act_mode; modes 1 and 2 need a bf16 model without
+                                parallel branches */
     int64_t vocab;        /* V: valid ids are [0, V); requires qr_rows_q * qr_rows_r >= V */
     float attn_alpha;     /* alpha: weight of the attention path (0 = plain low-rank DCNv2) */
     float skip_beta;      /* beta: weight of the skip (value) path */
@@ -123,7 +142,13 @@ typedef struct rdcn_handle rdcn_handle;
 
 /*
  * Validate `cfg` and create a handle (host metadata plus one device error word
- * on the current device). Returns RDCN_ERR_ARG for null pointers or values out
+ * on the current device). The configuration is the paper's statement of the
+ * model: categorical ids QR-hashed into per-feature quotient and remainder
+ * tables (section "Model Dictionary Compression"), their embeddings
+ * concatenated with the dense features (appendix "Feed Ranking Sparse ID
+ * features"), and a stack of num_layers Residual DCN layers of rank r with the
+ * attention term and skip weight (section "Residual DCN").
+ * Returns RDCN_ERR_ARG for null pointers or values out
  * of range, RDCN_ERR_SHAPE if qr_rows_q * qr_rows_r < vocab, and
  * RDCN_ERR_UNSUPPORTED when a bf16 model has emb_dim, num_dense or rank not a
  * multiple of 8 (fp32: multiple of 4), which the vector loads need, when
@@ -203,6 +228,12 @@ rdcn_status qr_embed_backward_workspace(const rdcn_handle* h, int64_t batch, int
 /*
  * QR embedding backward: table gradients from the x0 gradient, ACCUMULATED (+=)
  * into grad_q_tables [F, qr_rows_q, D] and grad_r_tables [F, m, D] (float).
+ * This is the chain rule through the look-up and combine of section "Model
+ * Dictionary Compression" (each id reads one quotient and one remainder row, so
+ * its x0 gradient slice flows back to exactly those two rows). Besides the
+ * arguments of qr_embed_gather it takes nnz (the id count, which sizes the sort
+ * path) and the size of the caller's scratch, so that a too small workspace is an
+ * error rather than an overrun.
  * grad_x0 is [batch, d] float (only its embedding columns are read). For every
  * valid id of bag (b, f) and g = grad_x0[b, f*D : (f+1)*D]:
  *   sum combine:     gQ_f[qi] += g,            gR_f[ri] += g
@@ -225,30 +256,33 @@ rdcn_status qr_embed_backward(rdcn_handle* h, int64_t batch, int64_t nnz, const 
  * float accumulate); if alpha != 0, per sample S_ij = q_i k_j / tau, A = row
  * softmax of S, o = A v; h = beta v + alpha o; t = U_l h + b_l;
  * x_{l+1} = x0 * t + x_l. `saved` (saved_bytes) receives what rdcn_backward
- * needs and must stay untouched until then; `scratch` holds scratch_bytes.
- * With the attention term on, [v; q; k] are kept in float (they feed the
- * softmax, whose sharpness amplifies any rounding of q and k); h, t and x_l
- * are kept in the storage dtype, or, with split_activations, x_l (l >= 1) and
- * h as hi + lo bf16 pairs whose sum carries about 16 significant bits: the
- * projections then see the activations at that precision (two MFMA passes
- * against the exact bf16 weights). Deep stacks whose attention is close to
- * one-hot need this to keep gradients within a few percent of exact.
+ * needs and must stay untouched until then; `scratch` holds scratch_bytes (in
+ * activation mode 2 the forward keeps one layer's f16 weight copies there; it
+ * may be NULL in the other modes). With the attention term on, [v; q; k] are
+ * kept in float (they feed the softmax, whose sharpness amplifies any rounding
+ * of q and k); t is kept in the storage dtype and x_l and h as the activation
+ * mode says (rdcn_act_mode). Deep stacks whose attention is close to one-hot
+ * need mode 1 or 2 to keep gradients within a few percent of exact. In mode 2
+ * the weights must be 16-byte aligned (RDCN_ERR_ARG otherwise).
  */
 rdcn_status rdcn_forward(rdcn_handle* h, int64_t batch, const void* x0, const rdcn_weights* w, void* x_out,
                          void* saved, void* scratch, void* stream);
 
 /*
  * Residual-DCN backward for the loss whose gradient w.r.t. x_L is grad_out
- * [batch, d] (storage dtype). Writes (overwrites) grad_x0 [batch, d] (float)
- * and the float weight gradients in `grads` (same shapes as the weights,
- * summed over the batch). x0, w and saved must be those of the matching
- * rdcn_forward call.
- * The weight-gradient products (and the bias sums) run on a second stream that
- * the handle owns (default priority), forked from `stream` after each layer's
- * attention and joined back to `stream` with events before the call returns:
- * work enqueued on `stream` after the call sees every output, and capturing
- * `stream` in a HIP graph captures both streams. Two calls on one handle must
- * not run concurrently on different streams.
+ * [batch, d] (storage dtype): the chain rule through the layer of section
+ * "Residual DCN" (cross layer, attention between the two low-rank maps, skip
+ * connection), which the paper states for the forward only. Writes
+ * (overwrites) grad_x0 [batch, d] (float) and the float weight gradients in
+ * `grads` (same shapes as the weights, summed over the batch). x0, w and saved
+ * must be those of the matching rdcn_forward call.
+ * The weight-gradient products (and the bias sums) may run on a second stream
+ * that the handle owns (default priority; rdcn_set_side_stream can turn it off), forked from
+ * `stream` after each layer's attention (layer 0, the last one, forks its bias
+ * sums and gU after its pointwise kernel) and joined back to `stream` with events
+ * before the call returns, on error returns too: work enqueued on `stream` after
+ * the call sees every output, and capturing `stream` in a HIP graph captures both
+ * streams. Two calls on one handle must not run concurrently on different streams.
  */
 rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const rdcn_weights* w, const void* saved,
                           const void* grad_out, float* grad_x0, const rdcn_weights* grads, void* scratch,
@@ -257,9 +291,20 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
 /*
  * Wait for `stream`, then read and clear the device error word:
  * RDCN_ERR_INDEX if any id outside [0, vocab) was met since the last check,
+ * else RDCN_ERR_RANGE if an f16 activation overflowed (activation mode 2),
  * RDCN_ERR_HIP on a runtime error, RDCN_OK otherwise.
  */
 rdcn_status rdcn_check_device_errors(rdcn_handle* h, void* stream);
+
+/*
+ * Where rdcn_backward runs its bias sums and weight-gradient GEMMs (a scheduling
+ * choice, not part of the paper's method): enable = 1 (the default) on the
+ * handle's second stream beside the main chain, enable = 0 on `stream` itself,
+ * so that every kernel runs alone and its measured time is its own (per-kernel
+ * profiling). Results are bitwise the same either way. RDCN_ERR_ARG for a null
+ * handle or another value.
+ */
+rdcn_status rdcn_set_side_stream(rdcn_handle* h, int32_t enable);
 
 /* Static description of a status code. */
 const char* rdcn_status_string(rdcn_status s);

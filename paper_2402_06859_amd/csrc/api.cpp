@@ -20,12 +20,15 @@ struct rdcn_handle {
     int64_t d;
     int n;   // projections per layer (3 with the attention term, 4 with parallel branches, else 1)
     int hr;  // width of the up projection's input (2r with parallel branches, else r)
-    bool bf16, ids64, attn, split, par;
+    bool bf16, ids64, attn, par;
+    bool split;  // activation mode 1: x_l (l >= 1) and h as bf16 hi + lo pairs
+    bool f16;    // activation mode 2: x_l (l >= 1) and h as f16 (plus bf16 copies for the weight gradients)
+    bool side_enabled = true;  // rdcn_set_side_stream
     uint32_t magic, shift;
     // the backward's weight-gradient products run on `side`, forked from and joined
     // back to the caller's stream with these events (no timing)
     hipStream_t side = nullptr;
-    hipEvent_t ev_pw = nullptr, ev_att = nullptr, ev_side[2] = {nullptr, nullptr};
+    hipEvent_t ev_pw = nullptr, ev_att = nullptr, ev_side[2] = {nullptr, nullptr}, ev_join = nullptr;
     int* err;  // device error word
     bool head_on = false;
     rdcn_head_config head{};
@@ -89,10 +92,13 @@ void div_magic_host(uint32_t m, uint32_t& magic, uint32_t& shift) {
 
 size_t eb(const rdcn_handle* h) { return h->bf16 ? 2 : 4; }
 
-// Per layer: [v|q|k] (float with the attention term, else storage; plus a lo plane
-// of v when split), h and its lo plane (attention only), the attention row
-// statistics [o | Z | W1 | W2] (float, bf16 storage with attention), t, x_{l+1} and its lo
-// plane (l < L-1). Lo planes exist only with split_activations.
+// Per layer: [v|q|k] (float with the attention term, else storage; plus a second
+// plane of v without it), h and its second plane (attention only), the attention row
+// statistics [o | Z | W1 | W2] (float, bf16 storage with attention), t, x_{l+1} and its
+// second plane (l < L-1). Second planes exist with activation modes 1 (the lo part of a
+// bf16 hi + lo pair) and 2: x_{l+1} is then f16 in X and its bf16 copy (the weight
+// gradient's operand) in X2, h is bf16 in H and f16 in H2, and v (no attention) bf16 in
+// P and f16 in P2.
 struct SavedLayout {
     size_t P[RDCN_MAX_LAYERS], P2[RDCN_MAX_LAYERS], H[RDCN_MAX_LAYERS], H2[RDCN_MAX_LAYERS], A[RDCN_MAX_LAYERS],
         T[RDCN_MAX_LAYERS], X[RDCN_MAX_LAYERS], X2[RDCN_MAX_LAYERS];
@@ -102,7 +108,7 @@ struct SavedLayout {
 SavedLayout saved_layout(const rdcn_handle* h, int64_t B) {
     SavedLayout s;
     const size_t e = eb(h), d = (size_t)h->d, r = (size_t)h->cfg.rank, n = (size_t)h->n;
-    const bool sp = h->split;
+    const bool sp = h->split || h->f16;
     size_t off = 0;
     for (int l = 0; l < h->cfg.num_layers; ++l) {
         const bool more = l + 1 < h->cfg.num_layers;
@@ -170,6 +176,22 @@ ScratchLayout scratch_layout(const rdcn_handle* h, int64_t B) {
     s.splitk = off; off += al((size_t)splitk_elems(h, B) * 4);
     s.total = off;
     return s;
+}
+
+// Forward scratch (activation mode 2 only): one layer's weights converted to f16, the
+// operands of the f16 projections (reused layer after layer).
+struct FwdScratchLayout {
+    size_t w16, u16, total;
+};
+
+FwdScratchLayout fwd_scratch_layout(const rdcn_handle* h) {
+    FwdScratchLayout f{0, 0, 0};
+    if (!h->f16) return f;
+    const size_t d = (size_t)h->d;
+    f.w16 = 0;
+    f.u16 = al((size_t)h->n * h->cfg.rank * d * 2);
+    f.total = f.u16 + al(d * (size_t)h->hr * 2);
+    return f;
 }
 
 bool aligned256(const void* p) { return ((uintptr_t)p & 255u) == 0; }
@@ -328,6 +350,7 @@ const char* rdcn_status_string(rdcn_status s) {
         case RDCN_ERR_UNSUPPORTED: return "unsupported configuration";
         case RDCN_ERR_WORKSPACE: return "workspace too small or misaligned";
         case RDCN_ERR_HIP: return "HIP runtime error";
+        case RDCN_ERR_RANGE: return "f16 activation beyond range";
     }
     return "unknown status";
 }
@@ -341,7 +364,7 @@ rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
         (c.combine != RDCN_COMBINE_MUL && c.combine != RDCN_COMBINE_SUM) || (c.multi_hot != 0 && c.multi_hot != 1) ||
         (c.id_type != RDCN_I32 && c.id_type != RDCN_I64) || (c.dtype != RDCN_F32 && c.dtype != RDCN_BF16) ||
         (c.hashed != 0 && c.hashed != 1) || c.reserved2 != 0 || (c.hashed ? c.vocab != 0 : c.vocab <= 0) ||
-        !(c.temperature > 0.0f) || (c.split_activations != 0 && c.split_activations != 1) ||
+        !(c.temperature > 0.0f) || c.activation_mode < RDCN_ACT_STORAGE || c.activation_mode > RDCN_ACT_F16 ||
         (c.parallel_branch != 0 && c.parallel_branch != 1) || (c.parallel_branch && c.attn_alpha == 0.0f) ||
         c.attn_alpha != c.attn_alpha || c.skip_beta != c.skip_beta)
         return RDCN_ERR_ARG;
@@ -357,8 +380,8 @@ rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
     if ((int64_t)c.num_cat * (c.hashed ? 2 : 1) * ((int64_t)c.qr_rows_q + c.qr_rows_r) >= (int64_t)1 << 31)
         return RDCN_ERR_UNSUPPORTED;
     if (c.attn_alpha != 0.0f && c.rank > 1024) return RDCN_ERR_UNSUPPORTED;  // one sample's attention staged in LDS (<= 64 KiB)
-    if (c.split_activations && c.dtype != RDCN_BF16) return RDCN_ERR_UNSUPPORTED;  // float storage has nothing to split
-    if (c.split_activations && c.parallel_branch) return RDCN_ERR_UNSUPPORTED;
+    if (c.activation_mode != RDCN_ACT_STORAGE && c.dtype != RDCN_BF16) return RDCN_ERR_UNSUPPORTED;  // float storage is exact
+    if (c.activation_mode != RDCN_ACT_STORAGE && c.parallel_branch) return RDCN_ERR_UNSUPPORTED;
     (void)n;
 
     rdcn_handle* h = new (std::nothrow) rdcn_handle();
@@ -371,7 +394,8 @@ rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
     h->hr = h->par ? 2 * c.rank : c.rank;
     h->bf16 = c.dtype == RDCN_BF16;
     h->ids64 = c.id_type == RDCN_I64;
-    h->split = c.split_activations != 0;
+    h->split = c.activation_mode == RDCN_ACT_HILO;
+    h->f16 = c.activation_mode == RDCN_ACT_F16;
     div_magic_host((uint32_t)c.qr_rows_r, h->magic, h->shift);
     if (hipMalloc((void**)&h->err, sizeof(int)) != hipSuccess) {
         (void)hipGetLastError();
@@ -380,7 +404,7 @@ rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
     }
     bool ok = hipMemset(h->err, 0, sizeof(int)) == hipSuccess && hipDeviceSynchronize() == hipSuccess;
     ok = ok && hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking) == hipSuccess;  // default priority
-    for (hipEvent_t* e : {&h->ev_pw, &h->ev_att, &h->ev_side[0], &h->ev_side[1]})
+    for (hipEvent_t* e : {&h->ev_pw, &h->ev_att, &h->ev_side[0], &h->ev_side[1], &h->ev_join})
         ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
     if (!ok) {
         (void)hipGetLastError();
@@ -395,7 +419,7 @@ rdcn_status rdcn_destroy(rdcn_handle* h) {
     if (!h) return RDCN_OK;
     rdcn_status s = RDCN_OK;
     for (hipEvent_t e : h->prof_ev) (void)hipEventDestroy(e);
-    for (hipEvent_t e : {h->ev_pw, h->ev_att, h->ev_side[0], h->ev_side[1]})
+    for (hipEvent_t e : {h->ev_pw, h->ev_att, h->ev_side[0], h->ev_side[1], h->ev_join})
         if (e && hipEventDestroy(e) != hipSuccess) s = RDCN_ERR_HIP;
     if (h->side && hipStreamDestroy(h->side) != hipSuccess) s = RDCN_ERR_HIP;
     if (h->err && hipFree(h->err) != hipSuccess) s = RDCN_ERR_HIP;
@@ -414,7 +438,7 @@ rdcn_status rdcn_workspace_bytes(const rdcn_handle* h, int64_t batch, size_t* sa
     if (st != RDCN_OK) return st;
     if (!saved_bytes || !scratch_bytes) return RDCN_ERR_ARG;
     *saved_bytes = saved_layout(h, batch).total;
-    *scratch_bytes = scratch_layout(h, batch).total;
+    *scratch_bytes = std::max(scratch_layout(h, batch).total, fwd_scratch_layout(h).total);
     return RDCN_OK;
 }
 
@@ -530,6 +554,17 @@ rdcn_status qr_embed_backward(rdcn_handle* h, int64_t batch, int64_t nnz, const 
     return hip_status(launch_emb_reduce(a, h->bf16, scratch, s));
 }
 
+// Once the backward has forked work onto the side stream, every return joins it back:
+// nothing enqueued on the caller's stream afterwards can overlap work still running there.
+struct SideJoin {
+    rdcn_handle* h;
+    hipStream_t s;
+    bool forked;
+    ~SideJoin() {
+        if (forked && hipEventRecord(h->ev_join, h->side) == hipSuccess) (void)hipStreamWaitEvent(s, h->ev_join, 0);
+    }
+};
+
 static rdcn_status check_weights(const rdcn_handle* h, const rdcn_weights* w) {
     if (!w) return RDCN_ERR_ARG;
     for (int l = 0; l < h->cfg.num_layers; ++l)
@@ -545,22 +580,34 @@ rdcn_status rdcn_forward(rdcn_handle* h, int64_t batch, const void* x0, const rd
     if (batch == 0) return RDCN_OK;
     if (!x0 || !x_out || !saved) return RDCN_ERR_ARG;
     if (!aligned256(saved)) return RDCN_ERR_WORKSPACE;
-    (void)scratch;
+    const FwdScratchLayout FS = fwd_scratch_layout(h);
+    if (FS.total > 0 && (!scratch || !aligned256(scratch))) return RDCN_ERR_WORKSPACE;
+    if (h->f16) {  // the f16 copies of the weights use 16-byte vector accesses
+        for (int l = 0; l < h->cfg.num_layers; ++l)
+            if (!a16(w->w_down[l]) || !a16(w->u[l])) return RDCN_ERR_ARG;
+    }
     hipStream_t s = (hipStream_t)stream;
     const rdcn_config& c = h->cfg;
     const int64_t B = batch, d = h->d, r = c.rank, nr = (int64_t)h->n * r;
     const SavedLayout S = saved_layout(h, B);
     char* sv = (char*)saved;
-    const void* xcur = x0;     // x_l (hi plane when split)
-    const void* xcur2 = nullptr;  // lo plane of x_l (x0 is exact in bf16: none)
+    void* w16 = FS.total ? (char*)scratch + FS.w16 : nullptr;  // f16 W_l (activation mode 2)
+    void* u16 = FS.total ? (char*)scratch + FS.u16 : nullptr;  // f16 U_l
+    const void* xcur = x0;        // x_l (hi plane when split, f16 in mode 2; x0 itself is bf16)
+    const void* xcur2 = nullptr;  // lo plane of x_l when split (x0 is exact in bf16: none)
     for (int l = 0; l < c.num_layers; ++l) {
         const bool more = l + 1 < c.num_layers;
+        const bool xf16 = h->f16 && l > 0;  // x_l held as f16
         void* P = sv + S.P[l];
         const int64_t hr = h->hr;
         // parallel branches: the plain branch's value V1^T x_l goes straight into the
         // first half of H; the attention branch's [v2|q|k] into P as usual
         const int64_t pr = h->par ? 3 * r : nr;  // width of P
         const char* wv = (const char*)w->w_down[l] + (h->par ? r * d * (int64_t)eb(h) : 0);
+        if (h->f16) {  // this layer's weights as f16 operands (W only when x_l is f16)
+            if (xf16) RDCN_TRY(launch_bf16_to_f16(w->w_down[l], w16, nr * d, h->err, s));
+            RDCN_TRY(launch_bf16_to_f16(w->u[l], u16, d * hr, h->err, s));
+        }
         if (h->par) {
             GemmArgs g{};
             g.M = B; g.N = r; g.K = d;
@@ -574,27 +621,33 @@ rdcn_status rdcn_forward(rdcn_handle* h, int64_t batch, const void* x0, const rd
         GemmArgs g{};
         g.M = B; g.N = pr; g.K = d;
         g.a = xcur; g.a2 = xcur2; g.lda = d;
-        g.b = wv; g.ldb = d;
+        g.b = xf16 ? w16 : wv; g.ldb = d;
+        g.ops_f16 = xf16;
         g.epi = h->attn ? EPI_STORE_F32 : EPI_STORE; g.scale = 1.0f;
         g.c = P; g.ldc = pr;
-        if (h->split && !h->attn) g.c2 = sv + S.P2[l];  // v as hi + lo for the up projection
+        g.err = h->err;
+        if (!h->attn && (h->split || h->f16)) {  // v as hi + lo, or its f16 copy, for the up projection
+            g.c2 = sv + S.P2[l];
+            g.c2_kind = h->f16 ? C2_F16 : C2_LO;
+        }
         {
             ProfScope ps(h, RDCN_KERNEL_FWD_DOWN_GEMM, s);
             RDCN_TRY(launch_gemm(g, plan_gemm(B, pr, d, h->bf16, false), h->bf16, s));
         }
         const void* hsrc = P;
-        const void* hsrc2 = g.c2;
+        const void* hsrc2 = h->split ? g.c2 : nullptr;
         int64_t ldh = nr;
         float scale = c.skip_beta;
+        if (h->f16 && !h->attn) hsrc = g.c2;  // the f16 copy of v
         if (h->attn) {
             void* H = sv + S.H[l];
-            void* H2 = h->split ? (void*)(sv + S.H2[l]) : nullptr;
+            void* H2 = (h->split || h->f16) ? (void*)(sv + S.H2[l]) : nullptr;
             void* Ha = (char*)H + (h->par ? r * (int64_t)eb(h) : 0);  // attention output columns of H
             ProfScope ps(h, RDCN_KERNEL_FWD_ATTENTION, s);
-            RDCN_TRY(launch_attn_fwd(B, (int)r, c.attn_alpha, c.skip_beta, c.temperature, P, pr, Ha, H2, hr,
-                                     (float*)(sv + S.A[l]), h->bf16, s));
-            hsrc = H;
-            hsrc2 = H2;
+            RDCN_TRY(launch_attn_fwd(B, (int)r, c.attn_alpha, c.skip_beta, c.temperature, P, pr, Ha, H2, h->f16, hr,
+                                     (float*)(sv + S.A[l]), h->err, h->bf16, s));
+            hsrc = h->f16 ? H2 : H;
+            hsrc2 = h->split ? H2 : nullptr;
             ldh = hr;
             scale = 1.0f;
         }
@@ -602,16 +655,24 @@ rdcn_status rdcn_forward(rdcn_handle* h, int64_t batch, const void* x0, const rd
         GemmArgs u{};
         u.M = B; u.N = d; u.K = hr;
         u.a = hsrc; u.a2 = hsrc2; u.lda = ldh;
-        u.b = w->u[l]; u.ldb = hr;
+        u.b = h->f16 ? u16 : w->u[l]; u.ldb = hr;
+        u.ops_f16 = h->f16;
         u.epi = EPI_CROSS; u.scale = scale;
-        u.c = xnext; u.c2 = (h->split && more) ? (void*)(sv + S.X2[l]) : nullptr; u.ldc = d;
-        u.bias = w->bias[l]; u.x0 = x0; u.xl = xcur; u.xl2 = xcur2; u.t_out = sv + S.T[l]; u.ldx = d;
+        u.c = xnext; u.ldc = d;
+        u.err = h->err;
+        if (more && (h->split || h->f16)) {  // x_{l+1}: hi + lo pair, or f16 with a bf16 copy
+            u.c2 = sv + S.X2[l];
+            u.c2_kind = h->f16 ? C2_BF16 : C2_LO;
+            u.c_f16 = h->f16;
+        }
+        u.bias = w->bias[l]; u.x0 = x0; u.xl = xcur; u.xl2 = xcur2; u.xl_f16 = xf16;
+        u.t_out = sv + S.T[l]; u.ldx = d;
         {
             ProfScope ps(h, RDCN_KERNEL_FWD_UP_GEMM, s);
             RDCN_TRY(launch_gemm(u, plan_gemm(B, d, hr, h->bf16, false), h->bf16, s));
         }
         xcur = xnext;
-        xcur2 = u.c2;
+        xcur2 = h->split ? u.c2 : nullptr;
     }
     return RDCN_OK;
 }
@@ -643,7 +704,9 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
     float* g = (float*)(sc + W.g);
     float* gh = (float*)(sc + W.gh);
     float* splitk = (float*)(sc + W.splitk);
-    hipStream_t side = h->side;
+    const bool use_side = h->side_enabled;
+    hipStream_t side = use_side ? h->side : s;
+    SideJoin join{h, s, false};
 
     // Main stream: pointwise -> gh -> attention -> gx, the chain from one layer's
     // gradient to the next. Side stream, once the layer's attention is done: the bias
@@ -658,10 +721,11 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
         void* gP = sc + W.gP[par];
         float* part = (float*)(sc + W.part[par]);
         // this parity's copies were last read by the side stream's work of layer l + 2
-        if (l + 2 < c.num_layers) RDCN_TRY(hipStreamWaitEvent(s, h->ev_side[par], 0));
+        if (use_side && l + 2 < c.num_layers) RDCN_TRY(hipStreamWaitEvent(s, h->ev_side[par], 0));
         const void* gin = top ? grad_out : (const void*)g;
         const void* P = sv + S.P[l];
-        const void* xl = l == 0 ? x0 : (const void*)(sv + S.X[l - 1]);
+        // x_l as the weight gradient's bf16 operand (the hi plane, or the bf16 copy of an f16 x_l)
+        const void* xl = l == 0 ? x0 : (const void*)(sv + (h->f16 ? S.X2[l - 1] : S.X[l - 1]));
         // gt = g * x0, grad_x0 (+)= g * t_l, bias partials
         {
             ProfScope ps(h, RDCN_KERNEL_BWD_POINTWISE, s);
@@ -694,8 +758,11 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
         // follows its gx on the main stream, so side work left until after the attention
         // would run alone while the main stream waits to join.
         if (l == 0) {
-            RDCN_TRY(hipEventRecord(h->ev_pw, s));
-            RDCN_TRY(hipStreamWaitEvent(side, h->ev_pw, 0));
+            if (use_side) {
+                RDCN_TRY(hipEventRecord(h->ev_pw, s));
+                RDCN_TRY(hipStreamWaitEvent(side, h->ev_pw, 0));
+                join.forked = true;
+            }
             if ((st = side_bias_gu()) != RDCN_OK) return st;
         }
         // gh = gt U         [B, hr]; with parallel branches the plain branch's part is its
@@ -729,8 +796,11 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
                                      (const float*)(sv + S.A[l]), gh, r, (char*)gP + (h->par ? r * e : 0), nr,
                                      h->bf16, s));
         }
-        RDCN_TRY(hipEventRecord(h->ev_att, s));
-        RDCN_TRY(hipStreamWaitEvent(side, h->ev_att, 0));
+        if (use_side) {
+            RDCN_TRY(hipEventRecord(h->ev_att, s));
+            RDCN_TRY(hipStreamWaitEvent(side, h->ev_att, 0));
+            join.forked = true;
+        }
         if (l > 0 && (st = side_bias_gu()) != RDCN_OK) return st;
         // gW = gP^T x_l    [n r, d], K = batch
         {
@@ -742,7 +812,7 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
             RDCN_TRY(gemm_weight_grad(h, RDCN_KERNEL_BWD_GW_GEMM, g3, (float*)grads->w_down[l], splitk, side,
                                       bwd_split_blocks(g3.M, g3.N, g3.K)));
         }
-        RDCN_TRY(hipEventRecord(h->ev_side[par], side));
+        if (use_side) RDCN_TRY(hipEventRecord(h->ev_side[par], side));
         // g_l = g_{l+1} + gP W   (layer 0: grad_x0 += g_1 + gP W)
         {
             GemmArgs g4{};
@@ -758,7 +828,10 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
         }
     }
     // join: the side stream's last work (layer 0) completes before anything later on `s`
-    RDCN_TRY(hipStreamWaitEvent(s, h->ev_side[0], 0));
+    if (use_side) {
+        join.forked = false;
+        RDCN_TRY(hipStreamWaitEvent(s, h->ev_side[0], 0));
+    }
     return RDCN_OK;
 }
 
@@ -988,8 +1061,14 @@ rdcn_status rdcn_check_device_errors(rdcn_handle* h, void* stream) {
     if (v != 0) {
         const int zero = 0;
         if (hipMemcpy(h->err, &zero, sizeof(int), hipMemcpyHostToDevice) != hipSuccess) return RDCN_ERR_HIP;
-        return RDCN_ERR_INDEX;
+        return (v & 1) ? RDCN_ERR_INDEX : RDCN_ERR_RANGE;
     }
+    return RDCN_OK;
+}
+
+rdcn_status rdcn_set_side_stream(rdcn_handle* h, int32_t enable) {
+    if (!h || (enable != 0 && enable != 1)) return RDCN_ERR_ARG;
+    h->side_enabled = enable != 0;
     return RDCN_OK;
 }
 

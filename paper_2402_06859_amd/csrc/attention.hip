@@ -467,8 +467,8 @@ __host__ __device__ constexpr int attn_fwd_block_floats(int rpad, int W) {
 template <typename T, int W, int NT, int KB>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_attn_fwd_mfma(int64_t B, int r, int rpad, float alpha, float beta,
                                                       float inv_tau, const float* __restrict__ P, int64_t ldp,
-                                                      T* __restrict__ H, T* __restrict__ H2, int64_t ldh,
-                                                      float* __restrict__ stats) {
+                                                      T* __restrict__ H, void* __restrict__ H2, int64_t ldh,
+                                                      bool h2_f16, float* __restrict__ stats, int* err) {
     extern __shared__ __attribute__((aligned(16))) float smem[];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int ntile = rpad / 16;
@@ -597,7 +597,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 if (lo) {
                     const float hv = beta * vi[t] + alpha * o;
                     st<T>::store(H + b * ldh + i, hv);
-                    if (H2) st<T>::store(H2 + b * ldh + i, hv - st<T>::round(hv));
+                    if (H2 && h2_f16) {  // h as f16, the up projection's operand
+                        ((_Float16*)H2)[b * ldh + i] = (_Float16)hv;
+                        if (fabsf(hv) >= F16_OVERFLOW) atomicOr(err, 2);  // f16 range bit of the error word
+                    } else if (H2) {     // lo part of a hi + lo pair
+                        st<T>::store((T*)H2 + b * ldh + i, hv - st<T>::round(hv));
+                    }
                 }
                 so[(lo ? 0 : 2 * r) + i] = lo ? o : s01 * vks;
                 so[(lo ? r : 3 * r) + i] = lo ? z : (z + acc[t].w) * ks;
@@ -873,7 +878,7 @@ static int attn_tiles(int rpad, int W) {
 }
 
 hipError_t launch_attn_fwd(int64_t B, int r, float alpha, float beta, float tau, const void* P, int64_t ldp, void* H,
-                           void* H2, int64_t ldh, float* stats, bool bf16, hipStream_t s) {
+                           void* H2, bool h2_f16, int64_t ldh, float* stats, int* err, bool bf16, hipStream_t s) {
     if (B == 0) return hipSuccess;
     if (bf16) {
         if (r > 4 * 16 * ATT_NT || !stats) return hipErrorInvalidValue;
@@ -884,7 +889,7 @@ hipError_t launch_attn_fwd(int64_t B, int r, float alpha, float beta, float tau,
         const size_t lds = sizeof(float) * (size_t)attn_fwd_block_floats(rpad, W);
 #define RDCN_AFWD(WV, NTV, KBV)                                                                                     \
     hipLaunchKernelGGL((k_attn_fwd_mfma<bf16_t, WV, NTV, KBV>), dim3((unsigned)blocks), dim3(256), lds, s, B, r, rpad, \
-                       alpha, beta, 1.0f / tau, (const float*)P, ldp, (bf16_t*)H, (bf16_t*)H2, ldh, stats)
+                       alpha, beta, 1.0f / tau, (const float*)P, ldp, (bf16_t*)H, H2, ldh, h2_f16, stats, err)
         if (W == 1) {
             if (NT == 2) RDCN_AFWD(1, 2, 1);
             else if (NT == 4) RDCN_AFWD(1, 4, 1);
@@ -898,6 +903,7 @@ hipError_t launch_attn_fwd(int64_t B, int r, float alpha, float beta, float tau,
 #undef RDCN_AFWD
         return hipGetLastError();
     }
+    if (h2_f16) return hipErrorInvalidValue;  // float models have no f16 activations
     const size_t lds = sizeof(float) * (2 * (size_t)r + 32);
     const int th = attn_threads(r);
     hipLaunchKernelGGL(k_attn_fwd<float>, dim3((unsigned)B), dim3(th), lds, s, B, r, alpha, beta, 1.0f / tau,

@@ -10,7 +10,36 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
+typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+
 __device__ __forceinline__ float bf16_to_f32(uint32_t raw16) { return __uint_as_float(raw16 << 16); }
+
+// Values at or beyond this magnitude round to infinity when converted to f16.
+constexpr float F16_OVERFLOW = 65520.f;
+
+// 8 floats -> one 16-byte vector of 8 f16 (round to nearest, ties to even); `ovf` is
+// set when a value is beyond the f16 range (it becomes infinity).
+__device__ __forceinline__ u32x4_t pack_f16x8(const float* v, bool& ovf) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const half2_t p = {(_Float16)v[2 * i], (_Float16)v[2 * i + 1]};
+        w[i] = __builtin_bit_cast(uint32_t, p);
+        ovf |= fabsf(v[2 * i]) >= F16_OVERFLOW || fabsf(v[2 * i + 1]) >= F16_OVERFLOW;
+    }
+    return u32x4_t{w[0], w[1], w[2], w[3]};
+}
+
+__device__ __forceinline__ void unpack_f16x8(const u32x4_t& w, float* v) {
+    const uint32_t x[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const half2_t p = __builtin_bit_cast(half2_t, x[i]);
+        v[2 * i] = (float)p.x;
+        v[2 * i + 1] = (float)p.y;
+    }
+}
 
 // float -> bfloat16 bits, round to nearest, ties to even (NaN kept quiet).
 __device__ __forceinline__ uint32_t f32_to_bf16(float x) {

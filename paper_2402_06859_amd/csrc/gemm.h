@@ -6,11 +6,12 @@
 namespace rdcn {
 
 enum GemmEpi {
-    EPI_STORE = 0,      // c[m, n] (storage type) = scale * acc; with c2: bf16 hi in c, lo in c2
+    EPI_STORE = 0,      // c[m, n] (storage type, or f16 with c_f16) = scale * acc; c2 as c2_kind says
     EPI_STORE_F32 = 1,  // c[m, n] (float) = scale * acc
     EPI_PARTIAL = 2,    // c[z, m, n] (float) = scale * acc   (split-K partials, z = split)
     EPI_CROSS = 3,      // t = scale*acc + bias[n]; c = x0 * t + xl; t_out = t   (storage type;
-                        // xl2 / c2: lo planes of a hi + lo bf16 input / output)
+                        // xl2: lo plane of a hi + lo bf16 x_l; xl_f16: x_l held as f16;
+                        // c_f16: c written as f16; c2 as c2_kind says)
     EPI_RESID = 4,      // c (float) = gin + scale * acc
     EPI_RESID_X0 = 5,   // c (float) += gin + scale * acc
     // MLP layers (bf16 storage, A K-contiguous):
@@ -21,6 +22,16 @@ enum GemmEpi {
                         // rowpart: rowpart[(n0 / BN) * M + m] = sum over the tile's columns of v * act
 };
 
+// What an optional second output plane c2 receives (same row stride as c).
+enum GemmC2 {
+    C2_LO = 0,    // c is bf16 hi = bf16(v), c2 the lo part bf16(v - hi): the pair carries ~16 bits
+    C2_BF16 = 1,  // a bf16 copy of v (c holds v as f16)
+    C2_F16 = 2    // an f16 copy of v (c holds v in the storage type)
+};
+
+// Bit of the device error word set when a value written as f16 is beyond its range.
+constexpr int ERR_BIT_F16_RANGE = 2;
+
 struct GemmArgs {
     int64_t M, N, K;
     const void* a;      // A(m, k) = a[m*lda + k], or a[k*lda + m] when a_kstrided
@@ -29,16 +40,21 @@ struct GemmArgs {
     const void* b;      // B(n, k) = b[n*ldb + k], or b[k*ldb + n] when b_kstrided
     int64_t ldb;
     bool a_kstrided, b_kstrided;
+    bool ops_f16;       // A and B hold f16 values (f16 MFMAs; both K-contiguous, no MLP epilogue)
     int epi;
     float scale;
     void* c;            // output (see GemmEpi)
-    void* c2;           // optional lo plane of a hi + lo bf16 output
+    void* c2;           // optional second output plane (see GemmC2)
+    int c2_kind;
+    bool c_f16;         // EPI_STORE / EPI_CROSS: c is written as f16
+    int* err;           // device error word (needed with c_f16 or c2_kind == C2_F16)
     int64_t ldc;
     // cross / residual epilogue operands, row stride ldx
     const void* bias;
     const void* x0;
     const void* xl;
     const void* xl2;    // optional lo plane of x_l
+    bool xl_f16;        // x_l is f16
     void* t_out;
     const void* gin;
     bool gin_f32;
@@ -65,5 +81,8 @@ hipError_t launch_gemm(const GemmArgs& g, const GemmPlan& p, bool bf16, hipStrea
 // Column tiles of an MLP GEMM under plan p (the rowpart partials per row).
 inline int64_t gemm_tiles_n(int64_t N, const GemmPlan& p) { return (N + p.bn - 1) / p.bn; }
 hipError_t launch_splitk_reduce(const float* part, int splits, int64_t MN, float* out, hipStream_t s);
+// dst = f16(src) for n bf16 values (n % 8 == 0, 16-byte aligned); sets ERR_BIT_F16_RANGE
+// in err when a value is beyond the f16 range.
+hipError_t launch_bf16_to_f16(const void* src, void* dst, int64_t n, int* err, hipStream_t s);
 
 }  // namespace rdcn

@@ -157,16 +157,29 @@ __device__ __forceinline__ void store_split8(T* hi, T* lo, const float* v) {
     store_split4<T>(hi + 4, lo + 4, v + 4);
 }
 
-// Epilogue on eight consecutive columns n .. n+7 of row m (n + 7 < N guaranteed):
-// 16-byte accesses along the rows of x0, x_l, t and g.
+// Output of eight values v at element offset off of c (and of c2, as c2_kind says).
 template <typename T>
-__device__ __forceinline__ void epilogue8(const GemmArgs& g, int64_t m, int64_t n, int z, float* v) {
+__device__ __forceinline__ void store_out8(const GemmArgs& g, int64_t off, const float* v, bool& ovf) {
+    if (g.c_f16) *(u32x4_t*)((_Float16*)g.c + off) = pack_f16x8(v, ovf);
+    else if (g.c2 && g.c2_kind == C2_LO) {
+        store_split8((T*)g.c + off, (T*)g.c2 + off, v);
+        return;
+    } else store8<T>((T*)g.c + off, v);
+    if (!g.c2) return;
+    if (g.c2_kind == C2_F16) *(u32x4_t*)((_Float16*)g.c2 + off) = pack_f16x8(v, ovf);
+    else store8<bf16_t>((bf16_t*)g.c2 + off, v);
+}
+
+// Epilogue on eight consecutive columns n .. n+7 of row m (n + 7 < N guaranteed):
+// 16-byte accesses along the rows of x0, x_l, t and g. `ovf` collects f16 range
+// overflows of the outputs written as f16.
+template <typename T>
+__device__ __forceinline__ void epilogue8(const GemmArgs& g, int64_t m, int64_t n, int z, float* v, bool& ovf) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] *= g.scale;
     switch (g.epi) {
         case EPI_STORE:
-            if (g.c2) store_split8((T*)g.c + m * g.ldc + n, (T*)g.c2 + m * g.ldc + n, v);
-            else store8<T>((T*)g.c + m * g.ldc + n, v);
+            store_out8<T>(g, m * g.ldc + n, v, ovf);
             break;
         case EPI_STORE_F32:
             store8<float>((float*)g.c + m * g.ldc + n, v);
@@ -178,7 +191,8 @@ __device__ __forceinline__ void epilogue8(const GemmArgs& g, int64_t m, int64_t 
             float b[8], x0[8], xl[8], xn[8];
             load8<T>((const T*)g.bias + n, b);
             load8<T>((const T*)g.x0 + m * g.ldx + n, x0);
-            load8<T>((const T*)g.xl + m * g.ldx + n, xl);
+            if (g.xl_f16) unpack_f16x8(*(const u32x4_t*)((const _Float16*)g.xl + m * g.ldx + n), xl);
+            else load8<T>((const T*)g.xl + m * g.ldx + n, xl);
             if (g.xl2) {
                 float lo[8];
                 load8<T>((const T*)g.xl2 + m * g.ldx + n, lo);
@@ -191,8 +205,7 @@ __device__ __forceinline__ void epilogue8(const GemmArgs& g, int64_t m, int64_t 
                 xn[e] = x0[e] * v[e] + xl[e];
             }
             store8<T>((T*)g.t_out + m * g.ldx + n, v);
-            if (g.c2) store_split8((T*)g.c + m * g.ldc + n, (T*)g.c2 + m * g.ldc + n, xn);
-            else store8<T>((T*)g.c + m * g.ldc + n, xn);
+            store_out8<T>(g, m * g.ldc + n, xn, ovf);
             break;
         }
         case EPI_RESID:
@@ -431,10 +444,27 @@ __device__ __forceinline__ void wait_lgkm0() {
     __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (0 << 8));
 }
 
+// The two MFMA shapes for bf16 or f16 operands (the same bit patterns either way: the
+// LDS layout and fragment reads do not depend on the element type).
+template <bool F16>
+__device__ __forceinline__ f32x16_t mfma32x32x16(const bf16x8_t& b, const bf16x8_t& a, const f32x16_t& c) {
+    if constexpr (F16)
+        return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(half8_t, b), __builtin_bit_cast(half8_t, a),
+                                                      c, 0, 0, 0);
+    else return __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, a, c, 0, 0, 0);
+}
+template <bool F16>
+__device__ __forceinline__ f32x4_t mfma16x16x32(const bf16x8_t& b, const bf16x8_t& a, const f32x4_t& c) {
+    if constexpr (F16)
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8_t, b), __builtin_bit_cast(half8_t, a),
+                                                      c, 0, 0, 0);
+    else return __builtin_amdgcn_mfma_f32_16x16x32_bf16(b, a, c, 0, 0, 0);
+}
+
 // Block tile BM x BN over WM x WN waves; each wave owns a (BM/WM) x (BN/WN) block of
 // MFMA tiles: 16 x 16 (v_mfma_f32_16x16x32_bf16) or, with M32, 32 x 32
 // (v_mfma_f32_32x32x16_bf16, twice the flops per clock).
-template <int BM, int BN, bool AKS, bool BKS, int ST, int WM, int WN, bool M32>
+template <int BM, int BN, bool AKS, bool BKS, int ST, int WM, int WN, bool M32, bool F16>
 struct Pipe {
     static constexpr int NW = WM * WN, THREADS = 64 * NW;
     static constexpr int MT = M32 ? 32 : 16;
@@ -505,7 +535,7 @@ struct Pipe {
 #pragma unroll
                     for (int j = 0; j < TN; ++j)
                         acc[i][j] =
-                            __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[s & 1][j], af[s & 1][i], acc[i][j], 0, 0, 0);
+                            mfma32x32x16<F16>(bfr[s & 1][j], af[s & 1][i], acc[i][j]);
                 __builtin_amdgcn_sched_barrier(0);
             }
         } else {
@@ -521,17 +551,17 @@ struct Pipe {
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
                     for (int j = 0; j < TN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+                        acc[i][j] = mfma16x16x32<F16>(bfr[j], af[i], acc[i][j]);
             }
         }
     }
 };
 
 // C = A B^T with an ST-stage direct-to-LDS pipeline (see layouts above).
-template <int BM, int BN, bool AKS, bool BKS, int ST, int WM, int WN, bool M32, typename T, bool MLP>
+template <int BM, int BN, bool AKS, bool BKS, int ST, int WM, int WN, bool M32, typename T, bool MLP, bool F16>
 __global__ __launch_bounds__(64 * WM * WN, (ST == 2 && WM * WN == 4) ? 2 : 1)
 __attribute__((amdgpu_waves_per_eu(WM * WN == 8 ? 2 : 1, WM * WN == 8 ? 2 : 8))) void k_gemm_mfma(GemmArgs g) {
-    using P = Pipe<BM, BN, AKS, BKS, ST, WM, WN, M32>;
+    using P = Pipe<BM, BN, AKS, BKS, ST, WM, WN, M32, F16>;
     // one buffer: the stage ring during the K loop, the C staging area afterwards
     __shared__ __attribute__((aligned(1024))) bf16_t smem[ST * P::STAGE_ELEMS];
     bf16_t* lds0 = smem;
@@ -588,6 +618,7 @@ __attribute__((amdgpu_waves_per_eu(WM * WN == 8 ? 2 : 1, WM * WN == 8 ? 2 : 8)))
     // Epilogue through LDS: lane holds C[m = tile_m + (lane & 15)][n = tile_n + 4 (lane >> 4) + e];
     // the tile is staged row-major (64 rows at a time), then each thread applies the
     // epilogue to 8 consecutive columns of a row.
+    bool ovf = false;                      // an output written as f16 overflowed
     constexpr int CH = 64;                 // rows staged per pass
     constexpr int CP = BN + 4;             // float pitch of a staged row
     static_assert(CH * CP * 4 <= ST * P::STAGE_ELEMS * 2, "C staging must fit the stage ring");
@@ -627,7 +658,7 @@ __attribute__((amdgpu_waves_per_eu(WM * WN == 8 ? 2 : 1, WM * WN == 8 ? 2 : 8)))
                 float v[8];
                 *(f32x4_t*)v = *(const f32x4_t*)(cs + row * CP + col);
                 *(f32x4_t*)(v + 4) = *(const f32x4_t*)(cs + row * CP + col + 4);
-                epilogue8<T>(g, m, n, z, v);
+                epilogue8<T>(g, m, n, z, v, ovf);
             } else {
                 float part = 0.f;
                 if (m < g.M && n < g.N) {
@@ -644,6 +675,7 @@ __attribute__((amdgpu_waves_per_eu(WM * WN == 8 ? 2 : 1, WM * WN == 8 ? 2 : 8)))
             }
         }
     }
+    if (ovf) atomicOr(g.err, ERR_BIT_F16_RANGE);
 }
 
 // Float VALU GEMM (float-storage models): 64 x 64 tile, 4 x 4 outputs per
@@ -713,8 +745,14 @@ hipError_t launch_tile(const GemmArgs& g, int splits, hipStream_t s) {
     const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
     dim3 grid((unsigned)tiles, 1, (unsigned)splits);
 #define RDCN_GEMM(AK, BKS, MLP) \
-    hipLaunchKernelGGL((k_gemm_mfma<BM, BN, AK, BKS, ST, WM, WN, M32, T, MLP>), grid, dim3(64 * WM * WN), 0, s, g)
-    if (g.epi == EPI_MLP_FWD || g.epi == EPI_MLP_BWD) {
+    hipLaunchKernelGGL((k_gemm_mfma<BM, BN, AK, BKS, ST, WM, WN, M32, T, MLP, false>), grid, dim3(64 * WM * WN), 0, s, g)
+    if (g.ops_f16) {
+        // f16 operands: the forward projections over f16 activations (both K-contiguous)
+        if (g.a_kstrided || g.b_kstrided || g.epi == EPI_MLP_FWD || g.epi == EPI_MLP_BWD || g.a2)
+            return hipErrorInvalidValue;
+        hipLaunchKernelGGL((k_gemm_mfma<BM, BN, false, false, ST, WM, WN, M32, T, false, true>), grid,
+                           dim3(64 * WM * WN), 0, s, g);
+    } else if (g.epi == EPI_MLP_FWD || g.epi == EPI_MLP_BWD) {
         // MLP layers: forward (both K-contiguous) and input gradient (B K-strided), no split-K
         if (g.a_kstrided || splits != 1) return hipErrorInvalidValue;
         if (g.b_kstrided) RDCN_GEMM(false, true, true); else RDCN_GEMM(false, false, true);
@@ -800,6 +838,28 @@ hipError_t launch_gemm(const GemmArgs& g, const GemmPlan& p, bool bf16, hipStrea
     }
     if (p.stages == 2) return launch_tile<64, 64, 2, 2, 2, false, bf16_t>(g, p.splits, s);
     return launch_tile<64, 64, 3, 2, 2, false, bf16_t>(g, p.splits, s);
+}
+
+// dst = f16(src), 8 values per thread and step; err bit on values beyond the f16 range.
+__global__ __launch_bounds__(256) void k_bf16_to_f16(const bf16_t* __restrict__ src, _Float16* __restrict__ dst,
+                                                     int64_t n8, int* err) {
+    bool ovf = false;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n8; i += (int64_t)gridDim.x * blockDim.x) {
+        float v[8];
+        st<bf16_t>::unpack(*(const u32x4_t*)(src + 8 * i), v);
+        *(u32x4_t*)(dst + 8 * i) = pack_f16x8(v, ovf);
+    }
+    if (ovf) atomicOr(err, ERR_BIT_F16_RANGE);
+}
+
+hipError_t launch_bf16_to_f16(const void* src, void* dst, int64_t n, int* err, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    if (n % 8 || ((uintptr_t)src & 15) || ((uintptr_t)dst & 15)) return hipErrorInvalidValue;
+    int64_t blocks = (n / 8 + 255) / 256;
+    if (blocks > 2048) blocks = 2048;
+    hipLaunchKernelGGL(k_bf16_to_f16, dim3((unsigned)blocks), dim3(256), 0, s, (const bf16_t*)src, (_Float16*)dst,
+                       n / 8, err);
+    return hipGetLastError();
 }
 
 hipError_t launch_splitk_reduce(const float* part, int splits, int64_t MN, float* out, hipStream_t s) {

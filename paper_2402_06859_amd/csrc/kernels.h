@@ -39,8 +39,10 @@ namespace rdcn {
 // bf16 storage: the forward writes o_i, Z_i and the row sums W1_i = sum_j e_ij v_j k_j,
 // W2_i = sum_j e_ij k_j of every row to stats ([o | Z | W1 | W2] per sample, row
 // stride 4 r) and the backward reads them back.
+// H2: optional second plane of h: its f16 value (h2_f16) or the lo part of a bf16
+// hi + lo pair; f16 values beyond range set bit 2 of *err.
 hipError_t launch_attn_fwd(int64_t B, int r, float alpha, float beta, float tau, const void* P, int64_t ldp, void* H,
-                           void* H2, int64_t ldh, float* stats, bool bf16, hipStream_t s);
+                           void* H2, bool h2_f16, int64_t ldh, float* stats, int* err, bool bf16, hipStream_t s);
 hipError_t launch_attn_bwd(int64_t B, int r, float alpha, float beta, float tau, const void* P, int64_t ldp,
                            const float* stats, const float* GH, int64_t ldg, void* GP, int64_t ldgp, bool bf16,
                            hipStream_t s);

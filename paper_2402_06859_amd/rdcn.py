@@ -16,16 +16,18 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "librdcn.so")
 MAX_LAYERS = 16
 
-RDCN_OK, RDCN_ERR_ARG, RDCN_ERR_SHAPE, RDCN_ERR_INDEX, RDCN_ERR_UNSUPPORTED, RDCN_ERR_WORKSPACE, RDCN_ERR_HIP = range(7)
+(RDCN_OK, RDCN_ERR_ARG, RDCN_ERR_SHAPE, RDCN_ERR_INDEX, RDCN_ERR_UNSUPPORTED, RDCN_ERR_WORKSPACE, RDCN_ERR_HIP,
+ RDCN_ERR_RANGE) = range(8)
 F32, BF16 = 0, 1
 I32, I64 = 0, 1
 COMBINE_MUL, COMBINE_SUM = 0, 1
+ACT_MODES = {"storage": 0, "hilo": 1, "f16": 2}   # rdcn_act_mode
 
 EXPORTS = ["rdcn_create", "rdcn_destroy", "rdcn_dim", "rdcn_workspace_bytes", "qr_embed_gather",
            "qr_embed_backward_workspace", "qr_embed_backward", "rdcn_forward", "rdcn_backward",
            "rdcn_check_device_errors", "rdcn_status_string", "rdcn_profile_start", "rdcn_profile_stop",
            "qr_quantize_tables", "qr_embed_gather_q8", "rdcn_head_configure", "rdcn_head_workspace_bytes",
-           "rdcn_head_forward", "rdcn_head_logloss", "rdcn_head_backward"]
+           "rdcn_head_forward", "rdcn_head_logloss", "rdcn_head_backward", "rdcn_set_side_stream"]
 
 KERNELS = ["gather", "fwd_down_gemm", "fwd_attention", "fwd_up_gemm", "bwd_pointwise", "bwd_bias", "bwd_gu_gemm",
            "bwd_gh_gemm", "bwd_attention", "bwd_gw_gemm", "bwd_gx_gemm", "splitk_reduce", "emb_keys", "emb_sort",
@@ -39,7 +41,7 @@ class RdcnConfig(ctypes.Structure):
                 ("num_dense", ctypes.c_int32), ("rank", ctypes.c_int32), ("num_layers", ctypes.c_int32),
                 ("qr_rows_q", ctypes.c_int32), ("qr_rows_r", ctypes.c_int32), ("combine", ctypes.c_int32),
                 ("multi_hot", ctypes.c_int32), ("id_type", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("split_activations", ctypes.c_int32), ("vocab", ctypes.c_int64), ("attn_alpha", ctypes.c_float),
+                ("activation_mode", ctypes.c_int32), ("vocab", ctypes.c_int64), ("attn_alpha", ctypes.c_float),
                 ("skip_beta", ctypes.c_float), ("temperature", ctypes.c_float), ("parallel_branch", ctypes.c_int32),
                 ("hashed", ctypes.c_int32), ("reserved2", ctypes.c_int32), ("hash_seed", ctypes.c_uint64)]
 
@@ -127,6 +129,7 @@ def load(build_if_missing: bool = True):
     L.rdcn_head_backward.argtypes = [vp, i64, vp, vp, ctypes.POINTER(RdcnHeadWeights), vp, vp, vp, vp,
                                      ctypes.POINTER(RdcnHeadWeights), vp, vp]
     L.rdcn_profile_start.argtypes = [vp, ctypes.c_int32, ctypes.c_uint32]
+    L.rdcn_set_side_stream.argtypes = [vp, ctypes.c_int32]
     L.rdcn_profile_stop.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
     for name in EXPORTS:
         if name != "rdcn_status_string":
@@ -157,7 +160,7 @@ def _stream(stream=None):
 def make_config(batch_max: int, num_cat: int, emb_dim: int, num_dense: int, rank: int, num_layers: int,
                 qr_rows_q: int, qr_rows_r: int, vocab: int, combine: str = "sum", multi_hot: bool = False,
                 id_type: str = "i64", dtype: str = "bf16", attn_alpha: float = 0.0, skip_beta: float = 1.0,
-                temperature: float = 1.0, split_activations: bool = False,
+                temperature: float = 1.0, activation_mode: str = "storage",
                 parallel_branch: bool = False, hashed: bool = False, hash_seed: int = 0) -> RdcnConfig:
     c = RdcnConfig()
     c.batch_max, c.num_cat, c.emb_dim, c.num_dense = batch_max, num_cat, emb_dim, num_dense
@@ -168,7 +171,7 @@ def make_config(batch_max: int, num_cat: int, emb_dim: int, num_dense: int, rank
     c.dtype = BF16 if dtype == "bf16" else F32
     c.vocab = vocab
     c.attn_alpha, c.skip_beta, c.temperature = attn_alpha, skip_beta, temperature
-    c.split_activations = int(split_activations)
+    c.activation_mode = ACT_MODES[activation_mode]
     c.parallel_branch = int(parallel_branch)
     c.hashed = int(hashed)
     c.hash_seed = hash_seed
@@ -179,7 +182,7 @@ def config_for(wl, batch_max: Optional[int] = None, id_type: str = "i64") -> Rdc
     """Config of a synthetic workload (paper_2402_06859_amd.synth.Workload)."""
     return make_config(batch_max or wl.batch, wl.num_cat, wl.emb_dim, wl.num_dense, wl.rank, wl.num_layers,
                        wl.table_rows, wl.table_rows, 0 if wl.hashed else wl.vocab, wl.combine, wl.multi_hot, id_type,
-                       wl.dtype, wl.alpha, wl.beta, wl.temperature, wl.split_activations, wl.parallel, wl.hashed,
+                       wl.dtype, wl.alpha, wl.beta, wl.temperature, wl.act_mode, wl.parallel, wl.hashed,
                        wl.hash_seed)
 
 
@@ -300,6 +303,11 @@ class Rdcn:
         _check("rdcn_profile_stop", load().rdcn_profile_stop(self.h, ms, cnt))
         return {k: (ms[i], cnt[i]) for i, k in enumerate(KERNELS)}
 
+    def set_side_stream(self, enable: bool):
+        """Run the backward's weight-gradient work on the handle's second stream (default) or not."""
+        _check("rdcn_set_side_stream", load().rdcn_set_side_stream(self.h, int(enable)))
+
     def check_device_errors(self, stream=None) -> int:
-        """Synchronise and return (and clear) the device error status (RDCN_OK or RDCN_ERR_INDEX)."""
+        """Synchronise and return (and clear) the device error status (RDCN_OK, RDCN_ERR_INDEX or
+        RDCN_ERR_RANGE)."""
         return load().rdcn_check_device_errors(self.h, _stream(stream))

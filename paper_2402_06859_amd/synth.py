@@ -47,7 +47,7 @@ class Workload:
     dense_zero_frac: float = 0.0
     temperature: float = 1.0
     skip_beta: float = 1.0
-    split_activations: bool = False  # activations as hi + lo bf16 pairs (deep attention stacks)
+    act_mode: str = "storage"        # x_l and h: storage type, "hilo" bf16 pairs or "f16" (deep attention stacks)
     parallel: bool = False           # plain + attention low-rank cross nets with their own weights
     hashed: bool = False             # Murmur front-end: two QR table pairs per feature, rows*rows >= 2^32
     hash_seed: int = 0
@@ -94,7 +94,7 @@ WORKLOADS: Dict[str, Workload] = {
     "multihot": Workload("multihot", 3, 8192, 64, 10_000_000, 3163, 64, 256, 3, 512, False, "bf16", "sum", 1.1,
                          multi_hot=True),
     "large": Workload("large", 4, 32768, 200, 20_000_000, 4473, 48, 1024, 6, 1024, True, "bf16", "sum", 1.1,
-                      split_activations=True),
+                      act_mode="f16"),
 }
 
 

@@ -46,8 +46,8 @@ def test_struct_layout_matches_c(tmp_path):
 
 
 def test_status_strings():
-    for s in range(7):
-        assert rdcn.status_string(s)
+    for s in range(8):
+        assert rdcn.status_string(s) != "unknown status"
     assert rdcn.status_string(99) == "unknown status"
 
 
@@ -60,7 +60,7 @@ def good():
     ("emb_dim", 0, rdcn.RDCN_ERR_ARG), ("num_cat", -1, rdcn.RDCN_ERR_ARG), ("batch_max", -1, rdcn.RDCN_ERR_ARG),
     ("combine", 7, rdcn.RDCN_ERR_ARG), ("dtype", 3, rdcn.RDCN_ERR_ARG), ("id_type", 2, rdcn.RDCN_ERR_ARG),
     ("temperature", 0.0, rdcn.RDCN_ERR_ARG), ("temperature", -1.0, rdcn.RDCN_ERR_ARG), ("vocab", 0, rdcn.RDCN_ERR_ARG),
-    ("split_activations", 2, rdcn.RDCN_ERR_ARG), ("multi_hot", 2, rdcn.RDCN_ERR_ARG),
+    ("activation_mode", 3, rdcn.RDCN_ERR_ARG), ("activation_mode", -1, rdcn.RDCN_ERR_ARG), ("multi_hot", 2, rdcn.RDCN_ERR_ARG),
     ("vocab", 626, rdcn.RDCN_ERR_SHAPE),                      # 25 * 25 < 626: ids would not fit the tables
     ("emb_dim", 12, rdcn.RDCN_ERR_UNSUPPORTED), ("num_dense", 4, rdcn.RDCN_ERR_UNSUPPORTED),
     ("rank", 12, rdcn.RDCN_ERR_UNSUPPORTED), ("emb_dim", 264, rdcn.RDCN_ERR_UNSUPPORTED),
@@ -73,11 +73,17 @@ def test_create_rejects_bad_config_before_hip(field, value, expect):
     assert not h.value
 
 
-def test_split_needs_bf16():
+@pytest.mark.parametrize("mode", [1, 2])
+def test_activation_modes_need_bf16(mode):
     c = good()
-    c.dtype, c.emb_dim, c.num_dense, c.rank, c.split_activations = rdcn.F32, 16, 32, 8, 1
+    c.dtype, c.emb_dim, c.num_dense, c.rank, c.activation_mode = rdcn.F32, 16, 32, 8, mode
     h = ctypes.c_void_p()
     assert rdcn.load().rdcn_create(ctypes.byref(c), ctypes.byref(h)) == rdcn.RDCN_ERR_UNSUPPORTED
+
+
+def test_side_stream_switch_rejects_null_handle():
+    assert rdcn.load().rdcn_set_side_stream(None, 0) == rdcn.RDCN_ERR_ARG
+    assert rdcn.load().rdcn_set_side_stream(None, 1) == rdcn.RDCN_ERR_ARG
 
 
 def test_create_null_arguments():
@@ -120,8 +126,9 @@ def test_parallel_branch_validation():
     c.parallel_branch, c.attn_alpha = 1, 0.0
     assert L.rdcn_create(ctypes.byref(c), ctypes.byref(h)) == rdcn.RDCN_ERR_ARG
     c = good()
-    c.parallel_branch, c.split_activations = 1, 1
-    assert L.rdcn_create(ctypes.byref(c), ctypes.byref(h)) == rdcn.RDCN_ERR_UNSUPPORTED
+    for mode in (1, 2):
+        c.parallel_branch, c.activation_mode = 1, mode
+        assert L.rdcn_create(ctypes.byref(c), ctypes.byref(h)) == rdcn.RDCN_ERR_UNSUPPORTED
 
 
 def test_hashed_front_end_validation():

@@ -93,14 +93,15 @@ def test_attention_extreme_logits(rank):
     run_full_compare(wl)
 
 
+@pytest.mark.parametrize("mode,tol", [("hilo", 2e-3), ("f16", 5e-3)])
 @pytest.mark.parametrize("attn", [True, False])
-def test_split_activations_ragged(attn):
-    """hi + lo activations: the projections see ~16-bit activations, so the forward is
-    an order of magnitude closer to the float64 oracle than plain bf16 operands."""
+def test_activation_modes_ragged(attn, mode, tol):
+    """hi + lo activations (~16 significant bits) and f16 activations (11 bits): the
+    projections see the activations at that precision, so the forward is several times
+    closer to the float64 oracle than with plain bf16 operands (8 significant bits)."""
     need_gpu()
-    wl = Workload("ragged_split", 14, 300, 5, 50_000, 250, 24, 40, 3, 40, attn, "bf16", "sum", 1.1,
-                  split_activations=True)
-    run_full_compare(wl, fwd_tol=2e-3)
+    wl = Workload("ragged_act", 14, 300, 5, 50_000, 250, 24, 40, 3, 40, attn, "bf16", "sum", 1.1, act_mode=mode)
+    run_full_compare(wl, fwd_tol=tol)
 
 
 @pytest.mark.parametrize("rank,batch", [(296, 77), (600, 37)])
