@@ -251,6 +251,24 @@ rdcn_status qr_embed_backward(rdcn_handle* h, int64_t batch, int64_t nnz, const 
                               void* stream);
 
 /*
+ * qr_embed_backward without a caller-provided workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). Same arguments, results and errors as
+ * qr_embed_backward, minus scratch: the sort path (hashed ids, or tables of more
+ * than 16384 rows) uses a library-owned static device array of
+ * RDCN_EMBED_STATIC_SCRATCH_BYTES per GPU, which the library holds from
+ * rdcn_create until the process ends. RDCN_ERR_WORKSPACE (before any launch)
+ * when qr_embed_backward_workspace() exceeds that size. The call allocates and
+ * frees nothing. Every call on one GPU shares that GPU's array: calls that
+ * overlap in time on one GPU (two streams, two host threads, two handles) race
+ * and give wrong results; calls ordered on one stream are safe.
+ */
+#define RDCN_EMBED_STATIC_SCRATCH_BYTES (64ull << 20)
+rdcn_status qr_embed_backward_static(rdcn_handle* h, int64_t batch, int64_t nnz, const void* ids,
+                                     const int64_t* offsets, const void* q_tables, const void* r_tables,
+                                     const float* grad_x0, float* grad_q_tables, float* grad_r_tables, void* stream);
+
+/*
  * Residual-DCN forward, section "Residual DCN". x0 [batch, d] -> x_out = x_L
  * [batch, d], storage dtype. For each layer: [v; q; k] = W_l x_l (bf16 MFMA,
  * float accumulate); if alpha != 0, per sample S_ij = q_i k_j / tau, A = row

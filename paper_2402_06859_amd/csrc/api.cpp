@@ -30,6 +30,7 @@ struct rdcn_handle {
     hipStream_t side = nullptr;
     hipEvent_t ev_pw = nullptr, ev_att = nullptr, ev_side[2] = {nullptr, nullptr}, ev_join = nullptr;
     int* err;  // device error word
+    void* static_scratch = nullptr;  // this device's qr_embed_backward_static workspace
     bool head_on = false;
     rdcn_head_config head{};
     // per-kernel timing (rdcn_profile_start / rdcn_profile_stop)
@@ -339,6 +340,9 @@ CalArgs cal_args(const rdcn_handle* h, const rdcn_head_weights* w, const float* 
 
 }  // namespace
 
+static_assert(RDCN_EMBED_STATIC_SCRATCH_BYTES == rdcn::EMB_STATIC_SCRATCH_BYTES,
+              "the header states the static workspace size");
+
 extern "C" {
 
 const char* rdcn_status_string(rdcn_status s) {
@@ -404,6 +408,7 @@ rdcn_status rdcn_create(const rdcn_config* cfg, rdcn_handle** out) {
     }
     bool ok = hipMemset(h->err, 0, sizeof(int)) == hipSuccess && hipDeviceSynchronize() == hipSuccess;
     ok = ok && hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking) == hipSuccess;  // default priority
+    ok = ok && emb_static_scratch(&h->static_scratch) == hipSuccess;
     for (hipEvent_t* e : {&h->ev_pw, &h->ev_att, &h->ev_side[0], &h->ev_side[1], &h->ev_join})
         ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
     if (!ok) {
@@ -564,6 +569,18 @@ struct SideJoin {
         if (forked && hipEventRecord(h->ev_join, h->side) == hipSuccess) (void)hipStreamWaitEvent(s, h->ev_join, 0);
     }
 };
+
+rdcn_status qr_embed_backward_static(rdcn_handle* h, int64_t batch, int64_t nnz, const void* ids,
+                                     const int64_t* offsets, const void* q_tables, const void* r_tables,
+                                     const float* grad_x0, float* grad_q_tables, float* grad_r_tables, void* stream) {
+    size_t need = 0;
+    rdcn_status st = qr_embed_backward_workspace(h, batch, nnz, &need);
+    if (st != RDCN_OK) return st;
+    if (need > RDCN_EMBED_STATIC_SCRATCH_BYTES) return RDCN_ERR_WORKSPACE;
+    if (need > 0 && !h->static_scratch) return RDCN_ERR_HIP;
+    return qr_embed_backward(h, batch, nnz, ids, offsets, q_tables, r_tables, grad_x0, grad_q_tables, grad_r_tables,
+                             need > 0 ? h->static_scratch : nullptr, need, stream);
+}
 
 static rdcn_status check_weights(const rdcn_handle* h, const rdcn_weights* w) {
     if (!w) return RDCN_ERR_ARG;

@@ -41,4 +41,9 @@ hipError_t launch_emb_reduce(const EmbedBwdArgs& a, bool bf16, void* scratch, hi
 bool emb_fused_ok(int rows_q, int m, int D, bool hashed);
 hipError_t launch_emb_fused(const EmbedBwdArgs& a, bool bf16, bool ids64, hipStream_t s);
 
+// Size of the library-owned workspace of qr_embed_backward_static (per device).
+constexpr uint64_t EMB_STATIC_SCRATCH_BYTES = 64ull << 20;
+// Device address of that workspace on the current device (looked up once per device).
+hipError_t emb_static_scratch(void** out);
+
 }  // namespace rdcn

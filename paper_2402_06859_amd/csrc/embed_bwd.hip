@@ -24,6 +24,8 @@
 // (b, position-in-bag) order, irrespective of scheduling.
 // Unhashed ids with tables of at most 16384 rows take the one-kernel path of
 // step 4 instead (no scratch, no global sort).
+#include <mutex>
+
 #include "device_common.h"
 #include "embed_bwd.h"
 
@@ -1018,6 +1020,37 @@ hipError_t launch_emb_fused(const EmbedBwdArgs& a, bool bf16, bool ids64, hipStr
     if (bf16) RDCN_FU(bf16_t);
     RDCN_FU(float);
 #undef RDCN_FU
+}
+
+// ---------------------------------------------------------------------------
+// Workspace of the allocation-free embedding backward (qr_embed_backward_static):
+// a file-scope device array, one copy on every GPU the library runs on, held until
+// the process ends. Its name is a host-side stand-in in host code; kernels get the
+// device address that hipGetSymbolAddress returns for the current device.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[EMB_STATIC_SCRATCH_BYTES];
+
+namespace {
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
+}  // namespace
+
+hipError_t emb_static_scratch(void** out) {
+    *out = nullptr;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= MAX_DEVICES) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
 }
 
 }  // namespace rdcn

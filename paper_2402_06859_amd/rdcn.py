@@ -27,7 +27,9 @@ EXPORTS = ["rdcn_create", "rdcn_destroy", "rdcn_dim", "rdcn_workspace_bytes", "q
            "qr_embed_backward_workspace", "qr_embed_backward", "rdcn_forward", "rdcn_backward",
            "rdcn_check_device_errors", "rdcn_status_string", "rdcn_profile_start", "rdcn_profile_stop",
            "qr_quantize_tables", "qr_embed_gather_q8", "rdcn_head_configure", "rdcn_head_workspace_bytes",
-           "rdcn_head_forward", "rdcn_head_logloss", "rdcn_head_backward", "rdcn_set_side_stream"]
+           "rdcn_head_forward", "rdcn_head_logloss", "rdcn_head_backward", "rdcn_set_side_stream",
+           "qr_embed_backward_static"]
+EMBED_STATIC_SCRATCH_BYTES = 64 << 20
 
 KERNELS = ["gather", "fwd_down_gemm", "fwd_attention", "fwd_up_gemm", "bwd_pointwise", "bwd_bias", "bwd_gu_gemm",
            "bwd_gh_gemm", "bwd_attention", "bwd_gw_gemm", "bwd_gx_gemm", "splitk_reduce", "emb_keys", "emb_sort",
@@ -118,6 +120,7 @@ def load(build_if_missing: bool = True):
     L.qr_embed_gather_q8.argtypes = [vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.qr_embed_backward_workspace.argtypes = [vp, i64, i64, ctypes.POINTER(sz)]
     L.qr_embed_backward.argtypes = [vp, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.qr_embed_backward_static.argtypes = [vp, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp]
     L.rdcn_forward.argtypes = [vp, i64, vp, ctypes.POINTER(RdcnWeights), vp, vp, vp, vp]
     L.rdcn_backward.argtypes = [vp, i64, vp, ctypes.POINTER(RdcnWeights), vp, vp, vp, ctypes.POINTER(RdcnWeights),
                                 vp, vp]
@@ -247,6 +250,12 @@ class Rdcn:
         _check("qr_embed_backward", load().qr_embed_backward(
             self.h, batch, nnz, _ptr(ids), _ptr(offsets), _ptr(q_tables), _ptr(r_tables), _ptr(grad_x0),
             _ptr(grad_q), _ptr(grad_r), _ptr(scratch), scratch.numel() * scratch.element_size(), _stream(stream)))
+
+    def qr_embed_backward_static(self, batch, nnz, ids, offsets, q_tables, r_tables, grad_x0, grad_q, grad_r,
+                                 stream=None):
+        _check("qr_embed_backward_static", load().qr_embed_backward_static(
+            self.h, batch, nnz, _ptr(ids), _ptr(offsets), _ptr(q_tables), _ptr(r_tables), _ptr(grad_x0),
+            _ptr(grad_q), _ptr(grad_r), _stream(stream)))
 
     def rdcn_forward(self, batch, x0, w_down, u, bias, x_out, saved, scratch=None, stream=None):
         w = _weights(w_down, u, bias)
