@@ -16,7 +16,9 @@
 // (v_mfma_f32_16x16x32_bf16); large products use 256 x 256 or 256 x 128 blocks of
 // 8 waves with 32 x 32 tiles (v_mfma_f32_32x32x16_bf16). Each K step of 64 is one
 // stage of a 2- or 3-stage ring in LDS, filled by direct global-to-LDS loads one or
-// two steps ahead of the multiply; K-strided operands stay [k][m] in LDS and are
+// two steps ahead of the multiply (a scalar base advanced along K plus per-lane offsets
+// computed once per block; a tail stage's positions past K are loaded from a block of
+// zeros, so every stage runs the same multiplies); K-strided operands stay [k][m] in LDS and are
 // transposed on the way out by ds_read_b64_tr_b16, so no operand is ever
 // transposed in memory. The MFMA is issued with B as its first operand, so each
 // lane ends up with four consecutive output columns of one row: epilogue loads
@@ -278,10 +280,11 @@ __device__ __forceinline__ int xcd_remap(int id, int n) {
 }
 
 // ---------------------------------------------------------------------------
-// LDS layouts (one stage = one BK = 64 slice of A and of B):
-//  K-contiguous operand, ROWS x 64 bf16: row r holds 8 chunks of 16 bytes; the
-//    chunk of logical k-block kc sits in slot kc ^ ((r >> 1) & 7). Two rows share
-//    a 256-byte bank window, so 16 consecutive rows reading the same kc hit 16
+// LDS layouts (one stage = one KB-deep slice of A and of B; KB = 64 in every launch,
+// the layouts also hold for KB = 32):
+//  K-contiguous operand, ROWS x KB bf16: row r holds KB/8 chunks of 16 bytes; the
+//    chunk of logical k-block kc sits in slot kc ^ kc_swz(r) (((r >> 1) & 7) for KB = 64).
+//    Two rows share a 256-byte bank window, so 16 consecutive rows reading the same kc hit 16
 //    distinct 16-byte bank groups (ds_read_b128 without conflicts).
 //  K-strided operand, 64 k-rows x ROWS bf16 (rows contiguous along m): a k-row
 //    holds ROWS/16 chunks of 32 bytes (16 m values); chunk c sits in slot
@@ -309,6 +312,14 @@ __device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
 
 __device__ __forceinline__ uint32_t lds_addr(const bf16_t* p) { return (uint32_t)(uintptr_t)((LDS_AS const char*)p); }
 
+// Slot XOR of row r of a K-contiguous operand stage of KB bf16 per row: KB = 64 (8 slots
+// of 16 bytes, two rows per 256-byte bank window) or 32 (4 slots, four rows per window);
+// 16 consecutive rows reading one slot hit 16 distinct 16-byte bank groups.
+template <int KB>
+__device__ __forceinline__ int kc_swz(int r) {
+    return KB == 64 ? ((r >> 1) & 7) : ((r >> 2) & 3);
+}
+
 template <int ROWS>
 __device__ __forceinline__ int kstr_swz(int k) {
     // ROWS = 128: 8 slots of 32 B per k-row; ROWS = 256: 16 slots, two 256 B windows per
@@ -317,23 +328,32 @@ __device__ __forceinline__ int kstr_swz(int k) {
     return ROWS >= 128 ? (((k & 3) << 1) | ((k >> 3) & 1)) : ((((k >> 1) & 1) << 1) | ((k >> 3) & 1));
 }
 
-// Issue this thread's direct-to-LDS loads of one stage for one operand (NW waves).
-template <int ROWS, bool KS, int NW>
+// 16 zero bytes in device memory: the source of the direct-to-LDS loads of K positions
+// past a range, so a tail stage arrives in LDS already zero-padded.
+__device__ __align__(16) const uint32_t kZero16[4] = {0u, 0u, 0u, 0u};
+
+// Issue this thread's direct-to-LDS loads of one stage (KB deep) for one operand (NW waves).
+// Rows past `rows` re-read the last row (their results are discarded); K positions at
+// or past kend read zeros. K-contiguous operands need kend - k0 to be a multiple of 8
+// (a 16-byte piece never straddles kend: K is a multiple of 8 for bf16 models).
+template <int ROWS, bool KS, int NW, int KB>
 __device__ __forceinline__ void stage_load(const bf16_t* __restrict__ base, int64_t ld, int64_t rows, int64_t row0,
                                            int64_t k0, int64_t kend, bf16_t* lds, int wave, int lane) {
-    constexpr int NI = ROWS / (8 * NW);  // wave-instructions per thread (ROWS * 8 chunks / 64 lanes / NW waves)
+    constexpr int NI = ROWS * KB / (512 * NW);  // wave-instructions per thread (1 KiB each)
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
         const int blk = wave * NI + j;  // 1 KiB block index within the stage
         int64_t gr, gk;
         if (!KS) {
-            const int r = blk * 8 + (lane >> 3);
-            const int kc = (lane & 7) ^ ((r >> 1) & 7);
+            constexpr int CPR = KB / 8;    // 16-byte chunks per row
+            constexpr int RPB = 64 / CPR;  // rows per 1 KiB block
+            const int r = blk * RPB + lane / CPR;
+            const int kc = (lane % CPR) ^ kc_swz<KB>(r);
             gr = row0 + r;
             gk = k0 + kc * 8;
             if (gr >= rows) gr = rows - 1;
-            if (gk >= kend) gk = kend - 8;
-            dma16(base + gr * ld + gk, lds_addr(lds) + (uint32_t)__builtin_amdgcn_readfirstlane(blk) * 1024u);
+            const void* src = gk < kend ? (const void*)(base + gr * ld + gk) : (const void*)kZero16;
+            dma16(src, lds_addr(lds) + (uint32_t)__builtin_amdgcn_readfirstlane(blk) * 1024u);
         } else {
             constexpr int RPB = ROWS == 256 ? 2 : (ROWS == 128 ? 4 : 8);  // k-rows per 1 KiB block
             constexpr int QPR = 64 / RPB;             // 16-byte pieces per k-row
@@ -342,37 +362,69 @@ __device__ __forceinline__ void stage_load(const bf16_t* __restrict__ base, int6
             const int c = (q >> 1) ^ kstr_swz<ROWS>(kr);
             gk = k0 + kr;
             gr = row0 + c * 16 + (q & 1) * 8;
-            if (gk >= kend) gk = kend - 1;
             if (gr >= rows) gr = rows - 8;
-            dma16(base + gk * ld + gr, lds_addr(lds) + (uint32_t)__builtin_amdgcn_readfirstlane(blk) * 1024u);
+            const void* src = gk < kend ? (const void*)(base + gk * ld + gr) : (const void*)kZero16;
+            dma16(src, lds_addr(lds) + (uint32_t)__builtin_amdgcn_readfirstlane(blk) * 1024u);
         }
     }
 }
 
-// Zero the k positions >= kvalid of one stage (tail tile of a K range); NT threads.
-template <int ROWS, bool KS, int NT>
-__device__ __forceinline__ void stage_zero_tail(bf16_t* lds, int kvalid, int tid) {
-    if (!KS) {
-        const int nch = 8 - kvalid / 8;  // chunks per row to clear
-        for (int e = tid; e < ROWS * nch; e += NT) {
-            const int r = e / nch, kc = kvalid / 8 + e % nch;
-            *(u32x4_t*)(lds + r * 64 + ((kc ^ ((r >> 1) & 7)) * 8)) = u32x4_t{0, 0, 0, 0};
+// The same loads with the address split into a scalar base (wave-uniform, advanced by
+// BK along K every step) and a loop-invariant per-lane 32-bit byte offset, computed
+// once per block by stage_offsets: no address arithmetic between the barrier and the
+// multiplies of a step.
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+    const uint64_t v = (uint64_t)(uintptr_t)p;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(v >> 32));
+    return (const void*)(uintptr_t)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ void dma16_s(uint32_t voff, const void* sbase, uint32_t lds_base) {
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(voff), "s"(sbase), "s"(lds_base)
+                 : "memory");
+}
+
+// Per-lane byte offsets of stage_load's loads relative to element (row_base, k0) of a
+// K-contiguous operand ([rows][ld]) or (k0, row_base) of a K-strided one ([K][ld]),
+// with rows clamped as stage_load clamps them; row_base <= every clamped row.
+template <int ROWS, bool KS, int NW, int KB>
+__device__ __forceinline__ void stage_offsets(int64_t ld, int64_t rows, int64_t row0, int64_t row_base, int wave,
+                                              int lane, uint32_t (&off)[ROWS * KB / (512 * NW)]) {
+    constexpr int NI = ROWS * KB / (512 * NW);
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+        const int blk = wave * NI + j;
+        if (!KS) {
+            constexpr int CPR = KB / 8, RPB = 64 / CPR;
+            const int r = blk * RPB + lane / CPR;
+            const int kc = (lane % CPR) ^ kc_swz<KB>(r);
+            int64_t gr = row0 + r;
+            if (gr >= rows) gr = rows - 1;
+            off[j] = (uint32_t)(((gr - row_base) * ld + kc * 8) * 2);
+        } else {
+            constexpr int RPB = ROWS == 256 ? 2 : (ROWS == 128 ? 4 : 8);
+            constexpr int QPR = 64 / RPB;
+            const int kr = blk * RPB + lane / QPR;
+            const int q = lane % QPR;
+            const int c = (q >> 1) ^ kstr_swz<ROWS>(kr);
+            int64_t gr = row0 + c * 16 + (q & 1) * 8;
+            if (gr >= rows) gr = rows - 8;
+            off[j] = (uint32_t)((kr * ld + (gr - row_base)) * 2);
         }
-    } else {
-        const int n = (64 - kvalid) * ROWS / 8;  // 16-byte pieces in the k-rows to clear
-        for (int e = tid; e < n; e += NT)
-            *(u32x4_t*)(lds + kvalid * ROWS + e * 8) = u32x4_t{0, 0, 0, 0};
     }
 }
 
 // MFMA fragment (16 rows x 32 k) of an operand tile at row offset rt, k offset ks.
-template <int ROWS, bool KS>
+template <int ROWS, bool KS, int KB>
 __device__ __forceinline__ bf16x8_t load_frag(const bf16_t* lds, int rt, int ks, int lane) {
     const int i = lane & 15, g = lane >> 4;
     if (!KS) {
         const int r = rt + i;
         const int kc = ks / 8 + g;
-        return __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(lds + r * 64 + ((kc ^ ((r >> 1) & 7)) * 8)));
+        return __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(lds + r * KB + ((kc ^ kc_swz<KB>(r)) * 8)));
     } else {
         const int c = rt / 16;
         s16x4_t lo, hi;
@@ -396,12 +448,12 @@ __device__ __forceinline__ bf16x8_t load_frag(const bf16_t* lds, int rt, int ks,
 // rt + l % 32 and the 8 k values ks + 8 (l / 32) .. + 7. K-strided operands use the
 // same transposing reads as above, each 16-lane group G supplying row chunk
 // rt / 16 + (G & 1) and k rows from ks + 8 (G >> 1).
-template <int ROWS, bool KS>
+template <int ROWS, bool KS, int KB>
 __device__ __forceinline__ bf16x8_t load_frag32(const bf16_t* lds, int rt, int ks, int lane) {
     if (!KS) {
         const int r = rt + (lane & 31);
         const int kc = ks / 8 + (lane >> 5);
-        return __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(lds + r * 64 + ((kc ^ ((r >> 1) & 7)) * 8)));
+        return __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(lds + r * KB + ((kc ^ kc_swz<KB>(r)) * 8)));
     } else {
         const int i = lane & 15, G = lane >> 4;
         const int c = rt / 16 + (G & 1);
@@ -464,14 +516,16 @@ __device__ __forceinline__ f32x4_t mfma16x16x32(const bf16x8_t& b, const bf16x8_
 // Block tile BM x BN over WM x WN waves; each wave owns a (BM/WM) x (BN/WN) block of
 // MFMA tiles: 16 x 16 (v_mfma_f32_16x16x32_bf16) or, with M32, 32 x 32
 // (v_mfma_f32_32x32x16_bf16, twice the flops per clock).
-template <int BM, int BN, bool AKS, bool BKS, int ST, int WM, int WN, bool M32, bool F16>
+template <int BM, int BN, bool AKS, bool BKS, int ST, int WM, int WN, bool M32, bool F16, int KB>
 struct Pipe {
     static constexpr int NW = WM * WN, THREADS = 64 * NW;
     static constexpr int MT = M32 ? 32 : 16;
     static constexpr int TM = BM / WM / MT, TN = BN / WN / MT;  // MFMA tiles per wave
-    static constexpr int LOADS = (BM + BN) / (8 * NW);          // load instructions per thread per stage
-    static constexpr int STAGE_ELEMS = (BM + BN) * BK;
+    static constexpr int LOADS = (BM + BN) * KB / (512 * NW);   // load instructions per thread per stage
+    static constexpr int STAGE_ELEMS = (BM + BN) * KB;
     using acc_t = typename std::conditional<M32, f32x16_t, f32x4_t>::type;
+
+    static constexpr int NIA = BM * KB / (512 * NW), NIB = BN * KB / (512 * NW);  // loads per thread per stage
 
     struct Ctx {
         const GemmArgs* g;
@@ -479,36 +533,63 @@ struct Pipe {
         int ntot;        // nk * planes
         int64_t kbeg, kend, m0, n0;
         int tid;
+        bool fast;                  // per-lane offsets fit 32 bits: loads use scalar base + offset
+        int64_t abase, bbase;       // first row of each operand the offsets are taken from
+        uint32_t aoff[NIA], boff[NIB];
     };
+
+    // Per-block setup of the scalar-base loads.
+    __device__ __forceinline__ static void prepare(Ctx& c) {
+        const GemmArgs& g = *c.g;
+        const int lane = c.tid & 63, wave = c.tid >> 6;
+        // K-strided rows clamp to rows - 8, possibly below the block's first row
+        c.abase = AKS ? (c.m0 + 8 <= g.M ? c.m0 : (g.M >= 8 ? g.M - 8 : 0)) : c.m0;
+        c.bbase = BKS ? (c.n0 + 8 <= g.N ? c.n0 : (g.N >= 8 ? g.N - 8 : 0)) : c.n0;
+        // largest offset: a block's rows (or its BK k-rows) times the stride, plus a row
+        const double amax = ((AKS ? KB : BM) + 1.0) * (double)g.lda * 2.0 + BM * 2.0;
+        const double bmax = ((BKS ? KB : BN) + 1.0) * (double)g.ldb * 2.0 + BN * 2.0;
+        c.fast = amax < 2.0e9 && bmax < 2.0e9 && g.M >= 8 && g.N >= 8 && g.K >= 8;
+        if (c.fast) {
+            stage_offsets<BM, AKS, NW, KB>(g.lda, g.M, c.m0, c.abase, wave, lane, c.aoff);
+            stage_offsets<BN, BKS, NW, KB>(g.ldb, g.N, c.n0, c.bbase, wave, lane, c.boff);
+        }
+    }
 
     // Loads of tile `t` (clamped to the last tile; planes follow each other) into `buf`.
     __device__ __forceinline__ static void issue(const Ctx& c, int t, bf16_t* buf) {
         const int lane = c.tid & 63, wave = c.tid >> 6;
         if (t > c.ntot - 1) t = c.ntot - 1;
         const int plane = t >= c.nk;
-        const int64_t k0 = c.kbeg + (int64_t)(t - plane * c.nk) * BK;
+        const int64_t k0 = c.kbeg + (int64_t)(t - plane * c.nk) * KB;
         const bf16_t* a = (const bf16_t*)(plane ? c.g->a2 : c.g->a);
-        stage_load<BM, AKS, NW>(a, c.g->lda, c.g->M, c.m0, k0, c.kend, buf, wave, lane);
-        stage_load<BN, BKS, NW>((const bf16_t*)c.g->b, c.g->ldb, c.g->N, c.n0, k0, c.kend, buf + BM * BK, wave, lane);
+        const bf16_t* b = (const bf16_t*)c.g->b;
+        if (c.fast && k0 + KB <= c.kend) {  // a whole stage: no clamp along K
+            const void* sa = uniform_ptr(AKS ? a + k0 * c.g->lda + c.abase : a + c.abase * c.g->lda + k0);
+            const void* sb = uniform_ptr(BKS ? b + k0 * c.g->ldb + c.bbase : b + c.bbase * c.g->ldb + k0);
+            const uint32_t la = lds_addr(buf), lb = lds_addr(buf + BM * KB);
+#pragma unroll
+            for (int j = 0; j < NIA; ++j)
+                dma16_s(c.aoff[j], sa, la + (uint32_t)__builtin_amdgcn_readfirstlane(wave * NIA + j) * 1024u);
+#pragma unroll
+            for (int j = 0; j < NIB; ++j)
+                dma16_s(c.boff[j], sb, lb + (uint32_t)__builtin_amdgcn_readfirstlane(wave * NIB + j) * 1024u);
+            return;
+        }
+        stage_load<BM, AKS, NW, KB>(a, c.g->lda, c.g->M, c.m0, k0, c.kend, buf, wave, lane);
+        stage_load<BN, BKS, NW, KB>(b, c.g->ldb, c.g->N, c.n0, k0, c.kend, buf + BM * KB, wave, lane);
     }
 
     // One step on tile kt held in `cur`; prefetch tile kt + ST - 1 into `nxt`.
     // Every step issues the same number of loads (past the last tile they re-read
-    // it), so "all but the newest ST - 2 stages" is a fixed count on every path.
+    // it), so "all but the newest ST - 2 stages" is a fixed count on every path. A tail
+    // tile's positions past the K range arrive as zeros (stage_load), so every step
+    // runs the same multiplies.
     __device__ __forceinline__ static void step(const Ctx& c, bf16_t* cur, bf16_t* nxt, int kt,
                                                 acc_t (&acc)[TM][TN]) {
         const int lane = c.tid & 63, wave = c.tid >> 6, wm = wave / WN, wn = wave % WN;
         wait_vmcnt(LOADS * (ST - 2));
         __builtin_amdgcn_s_barrier();
         issue(c, kt + ST - 1, nxt);
-        const int kk = kt >= c.nk ? kt - c.nk : kt;
-        const int64_t kv = c.kend - (c.kbeg + (int64_t)kk * BK);
-        if (kv < BK) {  // tail tile: clear k positions past the range
-            stage_zero_tail<BM, AKS, THREADS>(cur, (int)kv, c.tid);
-            stage_zero_tail<BN, BKS, THREADS>(cur + BM * BK, (int)kv, c.tid);
-            wait_lgkm0();
-            __builtin_amdgcn_s_barrier();
-        }
         if constexpr (M32) {
             // fragments double-buffered: the reads of substep s + 1 are issued before the
             // MFMAs of substep s, so LDS latency hides behind the matrix cores
@@ -516,18 +597,18 @@ struct Pipe {
             auto frags = [&](int buf, int ks) {
 #pragma unroll
                 for (int i = 0; i < TM; ++i)
-                    af[buf][i] = load_frag32<BM, AKS>(cur, wm * (BM / WM) + i * 32, ks, lane);
+                    af[buf][i] = load_frag32<BM, AKS, KB>(cur, wm * (BM / WM) + i * 32, ks, lane);
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    bfr[buf][j] = load_frag32<BN, BKS>(cur + BM * BK, wn * (BN / WN) + j * 32, ks, lane);
+                    bfr[buf][j] = load_frag32<BN, BKS, KB>(cur + BM * KB, wn * (BN / WN) + j * 32, ks, lane);
             };
             // (not with a K-strided A and eight accumulator tiles: that variant would spill)
             constexpr bool DB = !(AKS && TM * TN > 4);
             frags(0, 0);
 #pragma unroll
-            for (int s = 0; s < BK / 16; ++s) {
+            for (int s = 0; s < KB / 16; ++s) {
                 if (!DB && s > 0) frags(s & 1, s * 16);
-                if (DB && s + 1 < BK / 16) frags((s + 1) & 1, (s + 1) * 16);
+                if (DB && s + 1 < KB / 16) frags((s + 1) & 1, (s + 1) * 16);
                 // keep the compiler from sinking those reads below the MFMAs
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -540,13 +621,13 @@ struct Pipe {
             }
         } else {
 #pragma unroll
-            for (int ks = 0; ks < BK; ks += 32) {
+            for (int ks = 0; ks < KB; ks += 32) {
                 bf16x8_t af[TM], bfr[TN];
 #pragma unroll
-                for (int i = 0; i < TM; ++i) af[i] = load_frag<BM, AKS>(cur, wm * (BM / WM) + i * 16, ks, lane);
+                for (int i = 0; i < TM; ++i) af[i] = load_frag<BM, AKS, KB>(cur, wm * (BM / WM) + i * 16, ks, lane);
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    bfr[j] = load_frag<BN, BKS>(cur + BM * BK, wn * (BN / WN) + j * 16, ks, lane);
+                    bfr[j] = load_frag<BN, BKS, KB>(cur + BM * KB, wn * (BN / WN) + j * 16, ks, lane);
 #pragma unroll
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -557,83 +638,33 @@ struct Pipe {
     }
 };
 
-// C = A B^T with an ST-stage direct-to-LDS pipeline (see layouts above).
-template <int BM, int BN, bool AKS, bool BKS, int ST, int WM, int WN, bool M32, typename T, bool MLP, bool F16>
-__global__ __launch_bounds__(64 * WM * WN, (ST == 2 && WM * WN == 4) ? 2 : 1)
-__attribute__((amdgpu_waves_per_eu(WM * WN == 8 ? 2 : 1, WM * WN == 8 ? 2 : 8))) void k_gemm_mfma(GemmArgs g) {
-    using P = Pipe<BM, BN, AKS, BKS, ST, WM, WN, M32, F16>;
-    // one buffer: the stage ring during the K loop, the C staging area afterwards
-    __shared__ __attribute__((aligned(1024))) bf16_t smem[ST * P::STAGE_ELEMS];
-    bf16_t* lds0 = smem;
-    bf16_t* lds1 = smem + P::STAGE_ELEMS;
-    bf16_t* lds2 = smem + (ST == 3 ? 2 : 0) * P::STAGE_ELEMS;
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// Epilogue of a BM x BN block through LDS (`smem`, the stage ring of `ring_elems` bf16
+// elements, reused once the K loop is done). With 16 x 16 tiles lane holds
+// C[m = tile_m + (lane & 15)][n = tile_n + 4 (lane >> 4) + e]; with 32 x 32 tiles
+// C[m = tile_m + lane % 32][n = tile_n + 8 q + 4 (lane / 32) + e] in acc[4 q + e]. The
+// block is staged row-major, 64 rows at a time, then each thread applies the epilogue
+// to 8 consecutive columns of a row.
+template <int BM, int BN, int WM, int WN, bool M32, typename T, bool MLP, int THREADS, int RING, typename Acc,
+          int TM, int TN>
+__device__ __forceinline__ void block_epilogue(const GemmArgs& g, int64_t m0, int64_t n0, int z, Acc (&acc)[TM][TN],
+                                               bf16_t* smem, int tid) {
+    const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
-    const int tiles_n = (int)((g.N + BN - 1) / BN);
-    const int ntiles = (int)(((g.M + BM - 1) / BM) * tiles_n);
-    const int t = xcd_remap(blockIdx.x, ntiles);
-
-    typename P::Ctx c;
-    c.g = &g;
-    c.tid = tid;
-    c.m0 = (int64_t)(t / tiles_n) * BM;
-    c.n0 = (int64_t)(t % tiles_n) * BN;
-    const int z = blockIdx.z;
-    const int64_t kchunk = ((g.K + (int64_t)gridDim.z * BK - 1) / ((int64_t)gridDim.z * BK)) * BK;
-    c.kbeg = z * kchunk;
-    c.kend = c.kbeg + kchunk < g.K ? c.kbeg + kchunk : g.K;
-    c.nk = c.kbeg < c.kend ? (int)((c.kend - c.kbeg + BK - 1) / BK) : 0;
-    c.ntot = c.nk * (g.a2 ? 2 : 1);
-
-    typename P::acc_t acc[P::TM][P::TN];
-#pragma unroll
-    for (int i = 0; i < P::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < P::TN; ++j)
-#pragma unroll
-            for (int e = 0; e < (M32 ? 16 : 4); ++e) acc[i][j][e] = 0.f;
-
-    if (c.ntot > 0) {
-        P::issue(c, 0, lds0);
-        if (ST == 3) {
-            P::issue(c, 1, lds1);
-            for (int kt = 0; kt < c.ntot; kt += 3) {
-                P::step(c, lds0, lds2, kt, acc);
-                if (kt + 1 >= c.ntot) break;
-                P::step(c, lds1, lds0, kt + 1, acc);
-                if (kt + 2 >= c.ntot) break;
-                P::step(c, lds2, lds1, kt + 2, acc);
-            }
-        } else {
-            for (int kt = 0; kt < c.ntot; kt += 2) {
-                P::step(c, lds0, lds1, kt, acc);
-                if (kt + 1 >= c.ntot) break;
-                P::step(c, lds1, lds0, kt + 1, acc);
-            }
-        }
-        wait_vmcnt(0);  // the trailing re-read loads land before the workgroup ends
-    }
-
-    // Epilogue through LDS: lane holds C[m = tile_m + (lane & 15)][n = tile_n + 4 (lane >> 4) + e];
-    // the tile is staged row-major (64 rows at a time), then each thread applies the
-    // epilogue to 8 consecutive columns of a row.
     bool ovf = false;                      // an output written as f16 overflowed
     constexpr int CH = 64;                 // rows staged per pass
     constexpr int CP = BN + 4;             // float pitch of a staged row
-    static_assert(CH * CP * 4 <= ST * P::STAGE_ELEMS * 2, "C staging must fit the stage ring");
+    static_assert(CH * CP * 4 <= RING * 2, "C staging must fit the stage ring");
     float* cs = (float*)smem;
 #pragma unroll
     for (int h = 0; h < BM / CH; ++h) {
         __syncthreads();
         if constexpr (M32) {
-            // lane holds C[m = tile_m + lane % 32][n = tile_n + 8 q + 4 (lane / 32) + e] in acc[4 q + e]
 #pragma unroll
-            for (int i = 0; i < P::TM; ++i) {
+            for (int i = 0; i < TM; ++i) {
                 const int row = wm * (BM / WM) + i * 32 + (lane & 31) - h * CH;
                 if (row < 0 || row >= CH) continue;
 #pragma unroll
-                for (int j = 0; j < P::TN; ++j)
+                for (int j = 0; j < TN; ++j)
 #pragma unroll
                     for (int q = 0; q < 4; ++q)
                         *(f32x4_t*)(cs + row * CP + wn * (BN / WN) + j * 32 + 8 * q + 4 * (lane >> 5)) =
@@ -641,18 +672,18 @@ __attribute__((amdgpu_waves_per_eu(WM * WN == 8 ? 2 : 1, WM * WN == 8 ? 2 : 8)))
             }
         } else {
 #pragma unroll
-            for (int i = 0; i < P::TM; ++i) {
+            for (int i = 0; i < TM; ++i) {
                 const int row = wm * (BM / WM) + i * 16 + (lane & 15) - h * CH;
                 if (row < 0 || row >= CH) continue;
 #pragma unroll
-                for (int j = 0; j < P::TN; ++j)
+                for (int j = 0; j < TN; ++j)
                     *(f32x4_t*)(cs + row * CP + wn * (BN / WN) + j * 16 + 4 * (lane >> 4)) = acc[i][j];
             }
         }
         __syncthreads();
-        for (int q = tid; q < CH * (BN / 8); q += P::THREADS) {
+        for (int q = tid; q < CH * (BN / 8); q += THREADS) {
             const int row = q / (BN / 8), col = (q % (BN / 8)) * 8;
-            const int64_t m = c.m0 + h * CH + row, n = c.n0 + col;
+            const int64_t m = m0 + h * CH + row, n = n0 + col;
             if (!MLP) {
                 if (m >= g.M || n >= g.N) continue;
                 float v[8];
@@ -670,12 +701,82 @@ __attribute__((amdgpu_waves_per_eu(WM * WN == 8 ? 2 : 1, WM * WN == 8 ? 2 : 8)))
                 if (g.rowpart) {  // uniform: the BN / 8 threads of one row are an aligned lane group
 #pragma unroll
                     for (int o = 1; o < BN / 8; o <<= 1) part += __shfl_xor(part, o);
-                    if (col == 0 && m < g.M) g.rowpart[(int64_t)(c.n0 / BN) * g.M + m] = part;
+                    if (col == 0 && m < g.M) g.rowpart[(int64_t)(n0 / BN) * g.M + m] = part;
                 }
             }
         }
     }
     if (ovf) atomicOr(g.err, ERR_BIT_F16_RANGE);
+}
+
+// C = A B^T with an ST-stage direct-to-LDS pipeline of KB-deep stages (see layouts above).
+template <int BM, int BN, bool AKS, bool BKS, int ST, int WM, int WN, bool M32, typename T, bool MLP, bool F16, int KB>
+__global__ __launch_bounds__(64 * WM * WN, (ST == 2 && WM * WN == 4) ? 2 : 1)
+__attribute__((amdgpu_waves_per_eu(WM * WN == 8 ? 2 : 1, WM * WN == 8 ? 2 : 8))) void k_gemm_mfma(GemmArgs g) {
+    using P = Pipe<BM, BN, AKS, BKS, ST, WM, WN, M32, F16, KB>;
+    // one buffer: the stage ring during the K loop, the C staging area afterwards
+    __shared__ __attribute__((aligned(1024))) bf16_t smem[ST * P::STAGE_ELEMS];
+
+    const int tid = threadIdx.x;
+    const int tiles_n = (int)((g.N + BN - 1) / BN);
+    const int ntiles = (int)(((g.M + BM - 1) / BM) * tiles_n);
+    const int t = xcd_remap(blockIdx.x, ntiles);
+
+    typename P::Ctx c;
+    c.g = &g;
+    c.tid = tid;
+    c.m0 = (int64_t)(t / tiles_n) * BM;
+    c.n0 = (int64_t)(t % tiles_n) * BN;
+    const int z = blockIdx.z;
+    // split-K ranges are multiples of BK (itself a multiple of every KB)
+    const int64_t kchunk = ((g.K + (int64_t)gridDim.z * BK - 1) / ((int64_t)gridDim.z * BK)) * BK;
+    c.kbeg = z * kchunk;
+    c.kend = c.kbeg + kchunk < g.K ? c.kbeg + kchunk : g.K;
+    c.nk = c.kbeg < c.kend ? (int)((c.kend - c.kbeg + KB - 1) / KB) : 0;
+    c.ntot = c.nk * (g.a2 ? 2 : 1);
+    P::prepare(c);
+
+    typename P::acc_t acc[P::TM][P::TN];
+#pragma unroll
+    for (int i = 0; i < P::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < P::TN; ++j)
+#pragma unroll
+            for (int e = 0; e < (M32 ? 16 : 4); ++e) acc[i][j][e] = 0.f;
+
+    if (c.ntot > 0) {
+        // ring of ST stages: step kt multiplies stage kt and fills slot (kt + ST - 1) % ST
+        bf16_t* const s0 = smem;
+        bf16_t* const s1 = smem + P::STAGE_ELEMS;
+        bf16_t* const s2 = smem + (ST >= 3 ? 2 : 0) * P::STAGE_ELEMS;
+#pragma unroll
+        for (int u = 0; u < ST - 1; ++u) P::issue(c, u, smem + u * P::STAGE_ELEMS);
+        if constexpr (ST == 2) {  // unrolled: fixed buffer pointers in each step
+            for (int kt = 0; kt < c.ntot; kt += 2) {
+                P::step(c, s0, s1, kt, acc);
+                if (kt + 1 >= c.ntot) break;
+                P::step(c, s1, s0, kt + 1, acc);
+            }
+        } else if constexpr (ST == 3) {
+            for (int kt = 0; kt < c.ntot; kt += 3) {
+                P::step(c, s0, s2, kt, acc);
+                if (kt + 1 >= c.ntot) break;
+                P::step(c, s1, s0, kt + 1, acc);
+                if (kt + 2 >= c.ntot) break;
+                P::step(c, s2, s1, kt + 2, acc);
+            }
+        } else {
+            int cur = 0;
+            for (int kt = 0; kt < c.ntot; ++kt) {
+                const int nxt = cur == 0 ? ST - 1 : cur - 1;  // (kt + ST - 1) % ST
+                P::step(c, smem + cur * P::STAGE_ELEMS, smem + nxt * P::STAGE_ELEMS, kt, acc);
+                cur = cur + 1 == ST ? 0 : cur + 1;
+            }
+        }
+        wait_vmcnt(0);  // the trailing re-read loads land before the workgroup ends
+    }
+
+    block_epilogue<BM, BN, WM, WN, M32, T, MLP, P::THREADS, ST * P::STAGE_ELEMS>(g, c.m0, c.n0, z, acc, smem, tid);
 }
 
 // Float VALU GEMM (float-storage models): 64 x 64 tile, 4 x 4 outputs per
@@ -740,17 +841,17 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float* part, int sp
     }
 }
 
-template <int BM, int BN, int ST, int WM, int WN, bool M32, typename T>
+template <int BM, int BN, int ST, int WM, int WN, bool M32, typename T, int KB = 64>
 hipError_t launch_tile(const GemmArgs& g, int splits, hipStream_t s) {
     const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
     dim3 grid((unsigned)tiles, 1, (unsigned)splits);
 #define RDCN_GEMM(AK, BKS, MLP) \
-    hipLaunchKernelGGL((k_gemm_mfma<BM, BN, AK, BKS, ST, WM, WN, M32, T, MLP, false>), grid, dim3(64 * WM * WN), 0, s, g)
+    hipLaunchKernelGGL((k_gemm_mfma<BM, BN, AK, BKS, ST, WM, WN, M32, T, MLP, false, KB>), grid, dim3(64 * WM * WN), 0, s, g)
     if (g.ops_f16) {
         // f16 operands: the forward projections over f16 activations (both K-contiguous)
         if (g.a_kstrided || g.b_kstrided || g.epi == EPI_MLP_FWD || g.epi == EPI_MLP_BWD || g.a2)
             return hipErrorInvalidValue;
-        hipLaunchKernelGGL((k_gemm_mfma<BM, BN, false, false, ST, WM, WN, M32, T, false, true>), grid,
+        hipLaunchKernelGGL((k_gemm_mfma<BM, BN, false, false, ST, WM, WN, M32, T, false, true, KB>), grid,
                            dim3(64 * WM * WN), 0, s, g);
     } else if (g.epi == EPI_MLP_FWD || g.epi == EPI_MLP_BWD) {
         // MLP layers: forward (both K-contiguous) and input gradient (B K-strided), no split-K
