@@ -1,10 +1,12 @@
 """GPU head (gated MLP, logit, isotonic calibration, log loss) vs the float64 oracle.
 
-The oracle takes the same bf16 parameters and inputs and rounds its stored
-hidden activations to bf16 (oracle.round_bf16) so that ReLU masks and the
-calibration bucket are decided on the values the device keeps; all its
-arithmetic is float64. The device keeps the pre-activation gradients G in bf16,
-which bounds the parameter gradients' agreement at a few 1e-3.
+Two oracles. The plain one is the definition in float64 throughout (the same bf16
+parameters and inputs, no rounding of anything it computes); the device must match
+it within the bars of the bf16 cross stack (2e-2 forward, 5e-2 gradients). The
+emulating one rounds its stored hidden activations to bf16 (oracle.round_bf16), so
+that ReLU masks and the calibration bucket are decided on the values the device
+keeps (all its arithmetic is float64); against it the bars are tighter (2e-3
+forward, 1e-2 gradients: the device keeps the pre-activation gradients G in bf16).
 
 Small shapes are compared in full; the Feed-sized head (4 x 3500, stored as
 4 x 3504 with zero padding) runs at the full batch in the launch configuration
@@ -27,6 +29,7 @@ pytestmark = pytest.mark.gpu
 Y_TOL = 2e-3      # logits / calibrated logits (bf16 rounding of activations on both sides)
 GRAD_TOL = 1e-2   # parameter and input gradients (device G in bf16)
 CAL_TOL = 1e-5    # the calibration bias gradient (a float sum of the upstream gradient)
+PLAIN_Y_TOL, PLAIN_GRAD_TOL = 2e-2, 5e-2  # against the plain float64 definition
 
 
 def oracle_params(hinp: dict, head: HeadSpec) -> dict:
@@ -40,8 +43,9 @@ def oracle_params(hinp: dict, head: HeadSpec) -> dict:
     return p
 
 
-def run_head(wl: Workload, head: HeadSpec, B: int, rows=None, seed=None, hinp=None):
-    """Device forward + backward with upstream g_cal (zero outside `rows`), oracle on `rows`."""
+def run_head(wl: Workload, head: HeadSpec, B: int, rows=None, seed=None, hinp=None, round_act=oracle.round_bf16):
+    """Device forward + backward with upstream g_cal (zero outside `rows`), oracle on `rows`
+    (round_act=None: the plain float64 definition)."""
     print("head", head.name, head.hidden, "gated", head.gated, "K", head.buckets, "B", B, "d", wl.d, flush=True)
     hinp = make_head_inputs(wl, head, batch=B, seed=seed) if hinp is None else hinp
     rows = np.arange(B) if rows is None else rows
@@ -57,19 +61,19 @@ def run_head(wl: Workload, head: HeadSpec, B: int, rows=None, seed=None, hinp=No
     x = hinp["x"].float().numpy().astype(np.float64)
     p_rows = dict(p, e=p["e"][rows])
     g64 = g.numpy().astype(np.float64)
-    ref = OH.head_backward(x[rows], p_rows, g64[rows], round_act=oracle.round_bf16)
-    ref["scale"] = sum_scale(x, p, g64, rows)
+    ref = OH.head_backward(x[rows], p_rows, g64[rows], round_act=round_act)
+    ref["scale"] = sum_scale(x, p, g64, rows, round_act)
     return dh, ref, rows, p
 
 
-def sum_scale(x, p, g, rows) -> dict:
+def sum_scale(x, p, g, rows, round_act=oracle.round_bf16) -> dict:
     """Sum over rows of |per-row contribution| of each scalar gradient (gate biases, b_out):
     the scale of the summation error bound. A scalar gradient can be a nearly cancelling
     sum (0.01 out of terms whose magnitudes add up to 14 on the ragged case), so it is
     compared against this scale rather than against its own size."""
     acc = None
     for r in rows:
-        o = OH.head_backward(x[r:r + 1], dict(p, e=p["e"][r:r + 1]), g[r:r + 1], round_act=oracle.round_bf16)
+        o = OH.head_backward(x[r:r + 1], dict(p, e=p["e"][r:r + 1]), g[r:r + 1], round_act=round_act)
         v = {"b_out": abs(o["b_out"])}
         if o["c"] is not None:
             for l, c in enumerate(o["c"]):
@@ -78,10 +82,10 @@ def sum_scale(x, p, g, rows) -> dict:
     return acc
 
 
-def compare(dh: DeviceHead, ref: dict, rows, gated: bool, grad_tol=GRAD_TOL):
+def compare(dh: DeviceHead, ref: dict, rows, gated: bool, grad_tol=GRAD_TOL, y_tol=Y_TOL):
     scale = ref["scale"]
     errs = {"y": relerr(to_np(dh.y)[rows], ref["y"]), "y_cal": relerr(to_np(dh.y_cal)[rows], ref["y_cal"])}
-    assert errs["y"] <= Y_TOL and errs["y_cal"] <= Y_TOL, errs
+    assert errs["y"] <= y_tol and errs["y_cal"] <= y_tol, errs
     gerr = {"x": relerr(to_np(dh.grad_x)[rows], ref["x"]), "e": relerr(to_np(dh.grad_e)[rows], ref["e"]),
             "w_out": relerr(to_np(dh.grads["w_out"]), ref["w_out"]),
             "b_out": abs(float(to_np(dh.grads["b_out"])[0]) - ref["b_out"]) / scale["b_out"],
@@ -96,7 +100,7 @@ def compare(dh: DeviceHead, ref: dict, rows, gated: bool, grad_tol=GRAD_TOL):
     print("y %.3g  y_cal %.3g  max grad %.3g (%s)" % (errs["y"], errs["y_cal"], max(gerr.values()),
                                                       max(gerr, key=gerr.get)), flush=True)
     # cal_b sums g_cal alone; grad_e and cal_w carry v_k = t - step*k and so the logit's error
-    assert gerr["cal_b"] <= CAL_TOL and gerr["e"] <= Y_TOL and gerr["cal_w"] <= Y_TOL, gerr
+    assert gerr["cal_b"] <= CAL_TOL and gerr["e"] <= y_tol and gerr["cal_w"] <= y_tol, gerr
     bad = {k: v for k, v in gerr.items() if not v <= grad_tol}
     assert not bad, "gradient rel err above %.3g: %s" % (grad_tol, bad)
     if len(rows) < dh.B:
@@ -147,6 +151,22 @@ def test_large_mlp_full_batch_sampled():
     for l, n in enumerate(HEADS["lmlp"].hidden):
         gW = to_np(dh.grads["W"][l])
         assert not np.any(gW[n:]) and not np.any(to_np(dh.grads["b"][l])[n:])
+
+
+@pytest.mark.parametrize("case", ["ragged_gated", "ragged_plain"])
+def test_head_against_plain_float64_definition(case):
+    """The device against the head computed in float64 from the same bf16 parameters and
+    inputs with nothing rounded, at the bf16 bars (2e-2 forward, 5e-2 gradients): the
+    ragged head, gated and plain (many logits outside the bucket range)."""
+    need_gpu()
+    if case == "lmlp":
+        wl, head, B = WORKLOADS["small"], HEADS["lmlp"], WORKLOADS["small"].batch
+        rows = sample_rows(B, 64)
+    else:
+        wl, B, rows = RAGGED, 300, None
+        head = HeadSpec("ragged", (40, 24), gated=case == "ragged_gated", buckets=9, lo=-0.5, step=0.1)
+    dh, ref, rows, _ = run_head(wl, head, B, rows=rows, round_act=None)
+    compare(dh, ref, rows, head.gated, grad_tol=PLAIN_GRAD_TOL, y_tol=PLAIN_Y_TOL)
 
 
 def test_logloss_matches_oracle():
