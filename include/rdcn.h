@@ -56,7 +56,8 @@ typedef enum rdcn_status {
     RDCN_ERR_UNSUPPORTED = 4,  /* valid but not supported here (see rdcn_create) */
     RDCN_ERR_WORKSPACE = 5,    /* a workspace or buffer argument is too small */
     RDCN_ERR_HIP = 6,          /* a HIP runtime call or kernel launch failed */
-    RDCN_ERR_RANGE = 7         /* an activation kept as f16 (activation mode 2) was beyond the
+    RDCN_ERR_RANGE = 7         /* an activation kept as f16 (activation mode 2, or a head's
+                                  hidden activations) or an f16 weight copy was beyond the
                                   f16 range (|x| >= 65520) and became infinite */
 } rdcn_status;
 
@@ -309,7 +310,8 @@ rdcn_status rdcn_backward(rdcn_handle* h, int64_t batch, const void* x0, const r
 /*
  * Wait for `stream`, then read and clear the device error word:
  * RDCN_ERR_INDEX if any id outside [0, vocab) was met since the last check,
- * else RDCN_ERR_RANGE if an f16 activation overflowed (activation mode 2),
+ * else RDCN_ERR_RANGE if an f16 activation or weight copy overflowed
+ * (activation mode 2, the head's hidden layers),
  * RDCN_ERR_HIP on a runtime error, RDCN_OK otherwise.
  */
 rdcn_status rdcn_check_device_errors(rdcn_handle* h, void* stream);
@@ -381,8 +383,12 @@ typedef enum rdcn_kernel {
  *     (below lo and above lo + K*step the first and last buckets extend
  *     linearly); e [batch, K] float is the per-sample calibration embedding,
  *     made upstream. y_cal is monotone non-decreasing in y.
- * bf16 models only. Activations a_l are kept in bf16, gate logits, y and y_cal
- * in float.
+ * bf16 models only. Each hidden activation a_l is kept twice: in f16, which
+ * the next layer (an f16 MFMA product against an f16 copy of W_{l+1} made in
+ * `saved`), the gate logits, the logit and the column sums of the output and
+ * gate weight gradients read, and in bf16, which the weight-gradient products
+ * and the ReLU masks read (|a_l| and |W_l| < 65520, else RDCN_ERR_RANGE is
+ * flagged; rdcn_check_device_errors). Gate logits, y and y_cal are float.
  * ---------------------------------------------------------------------------
  */
 #define RDCN_HEAD_MAX_HIDDEN 8

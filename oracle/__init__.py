@@ -115,6 +115,13 @@ def round_bf16(x) -> np.ndarray:
     return y
 
 
+def round_f16(x) -> np.ndarray:
+    """x (as float32) rounded to the nearest IEEE binary16 value, ties to even,
+    |x| >= 65520 to infinity, returned as float32: the rounding of an activation
+    kept in f16. numpy's float16 cast is the rounding step."""
+    return np.asarray(x, np.float32).astype(np.float16).astype(np.float32)
+
+
 def gather(B: int, F: int, D: int, Nd: int, vocab: int, rows_q: int, m: int, combine: str, bf16: bool,
            ids, offsets, q_tables, r_tables, dense):
     """x0 [B, F*D+Nd] float32 (bf16-rounded values when bf16) and the out-of-range id count."""

@@ -264,25 +264,32 @@ bool q8_aligned(const rdcn_handle* h, const void* codes, const void* params) {
 }
 
 // ---------------------------------------------------------------------------
-// Head layouts. Saved: per hidden layer a_l [B, n_l] bf16 and (gated) s_l [B]
-// float, then y [B] float. Scratch: two G planes [B, n_max] bf16 (the current
-// layer's pre-activation gradient and the next one's), gy [B], two gs [B], the
-// gate row partials, column-sum partials and split-K partials.
+// Head layouts. Saved: per hidden layer a_l [B, n_l] twice, as bf16 (the weight
+// gradients' operand and the ReLU masks) and as f16 (what the next layer, the gate
+// logits and the logit read: three more mantissa bits keep the ReLU masks of the
+// deeper layers close to those of the exact activations), (gated) s_l [B] float,
+// then y [B] float and an f16 copy of the widest W_l (l >= 1) for the forward's
+// f16 products. Scratch: two G planes [B, n_max] bf16 (the current layer's
+// pre-activation gradient and the next one's), gy [B], two gs [B], the gate row
+// partials, column-sum partials and split-K partials.
 // ---------------------------------------------------------------------------
 inline int64_t head_in(const rdcn_handle* h, int l) { return l == 0 ? h->d : h->head.hidden[l - 1]; }
 
 struct HeadSaved {
-    size_t A[RDCN_HEAD_MAX_HIDDEN], S[RDCN_HEAD_MAX_HIDDEN], Y, total;
+    size_t A[RDCN_HEAD_MAX_HIDDEN], A16[RDCN_HEAD_MAX_HIDDEN], S[RDCN_HEAD_MAX_HIDDEN], Y, W16, total;
 };
 
 HeadSaved head_saved_layout(const rdcn_handle* h, int64_t B) {
     HeadSaved s;
-    size_t off = 0;
+    size_t off = 0, w16 = 0;
     for (int l = 0; l < h->head.num_hidden; ++l) {
         s.A[l] = off; off += al((size_t)B * h->head.hidden[l] * 2);
+        s.A16[l] = off; off += al((size_t)B * h->head.hidden[l] * 2);
         s.S[l] = off; off += h->head.gated ? al((size_t)B * 4) : 0;
+        if (l > 0) w16 = std::max(w16, (size_t)h->head.hidden[l] * h->head.hidden[l - 1] * 2);
     }
     s.Y = off; off += al((size_t)B * 4);
+    s.W16 = off; off += al(w16);
     s.total = off;
     return s;
 }
@@ -896,27 +903,35 @@ rdcn_status rdcn_head_forward(rdcn_handle* h, int64_t batch, const void* x, cons
     char* sv = (char*)saved;
     for (int l = 0; l < c.num_hidden; ++l) {
         const int64_t nin = head_in(h, l), nout = c.hidden[l];
-        const void* in = l == 0 ? x : (const void*)(sv + S.A[l - 1]);
+        // layer 0 reads the bf16 input, the others the f16 copy of a_{l-1}
+        const void* in = l == 0 ? x : (const void*)(sv + S.A16[l - 1]);
         float* sl = c.gated ? (float*)(sv + S.S[l]) : nullptr;
         if (c.gated) {
             ProfScope ps(h, RDCN_KERNEL_HEAD_GATE, s);
-            RDCN_TRY(launch_gate_logit(B, (int)nin, in, nin, w->gate_w[l], w->gate_b[l], sl, s));
+            RDCN_TRY(launch_gate_logit(B, (int)nin, in, l > 0, nin, w->gate_w[l], w->gate_b[l], sl, s));
         }
         GemmArgs g{};
         g.M = B; g.N = nout; g.K = nin;
         g.a = in; g.lda = nin;
         g.b = w->w[l]; g.ldb = nin;
+        if (l > 0) {
+            g.b = sv + S.W16;
+            g.ops_f16 = true;
+            RDCN_TRY(launch_bf16_to_f16(w->w[l], sv + S.W16, nout * nin, h->err, s));
+        }
         g.epi = EPI_MLP_FWD; g.scale = 1.0f;
         g.bias = w->b[l];
         g.rowv = sl;
         g.c = sv + S.A[l]; g.ldc = nout;
+        g.c2 = sv + S.A16[l]; g.c2_kind = C2_F16;
+        g.err = h->err;
         ProfScope ps(h, RDCN_KERNEL_HEAD_FWD_GEMM, s);
         RDCN_TRY(launch_gemm(g, plan_gemm(B, nout, nin, true, false), true, s));
     }
     const int L = c.num_hidden;
     ProfScope ps(h, RDCN_KERNEL_HEAD_OUT, s);
-    return hip_status(launch_head_out(B, c.hidden[L - 1], sv + S.A[L - 1], w->w_out, w->b_out, cal_args(h, w, e_cal),
-                                      (float*)(sv + S.Y), y_logit, y_cal, s));
+    return hip_status(launch_head_out(B, c.hidden[L - 1], sv + S.A16[L - 1], w->w_out, w->b_out,
+                                      cal_args(h, w, e_cal), (float*)(sv + S.Y), y_logit, y_cal, s));
 }
 
 rdcn_status rdcn_head_logloss(rdcn_handle* h, int64_t batch, const float* y_cal, const float* labels, float scale,
@@ -960,11 +975,12 @@ rdcn_status rdcn_head_backward(rdcn_handle* h, int64_t batch, const void* x, con
         sums.out[sums.n] = (float*)out;
         ++sums.n;
     };
-    auto colsum = [&](int64_t n, const void* X, int64_t ldx, bool xbf16, const float* wgt, void* out) -> hipError_t {
+    auto colsum = [&](int64_t n, const void* X, int64_t ldx, ColType xt, const float* wgt, void* out) -> hipError_t {
         ProfScope ps(h, RDCN_KERNEL_HEAD_COLSUM, s);
-        return launch_colsum_w(B, n, X, ldx, xbf16, wgt, colpart, (float*)out, s);
+        return launch_colsum_w(B, n, X, ldx, xt, wgt, colpart, (float*)out, s);
     };
-    const void* aL = B > 0 ? (const void*)(sv + S.A[L - 1]) : nullptr;
+    // the top layer's activations as the forward's logit read them (f16)
+    const void* aL = B > 0 ? (const void*)(sv + S.A16[L - 1]) : nullptr;
     int cur = 0;
     {
         ProfScope ps(h, RDCN_KERNEL_HEAD_OUT_BWD, s);
@@ -972,8 +988,8 @@ rdcn_status rdcn_head_backward(rdcn_handle* h, int64_t batch, const void* x, con
                                      w->w_out, B > 0 ? (const float*)(sv + S.Y) : nullptr, cal_args(h, w, e_cal),
                                      grad_ycal, grad_e, gy, sc + W.G[cur], gs_of(L - 1), s));
     }
-    RDCN_TRY(colsum(c.hidden[L - 1], aL, c.hidden[L - 1], true, gy, grads->w_out));
-    RDCN_TRY(colsum(c.num_buckets, grad_e, c.num_buckets, false, nullptr, grads->cal_w));
+    RDCN_TRY(colsum(c.hidden[L - 1], aL, c.hidden[L - 1], COL_F16, gy, grads->w_out));
+    RDCN_TRY(colsum(c.num_buckets, grad_e, c.num_buckets, COL_F32, nullptr, grads->cal_w));
     add_sum(gy, grads->b_out);
     add_sum(grad_ycal, grads->cal_b);
     for (int l = L - 1; l >= 0; --l) {
@@ -981,9 +997,11 @@ rdcn_status rdcn_head_backward(rdcn_handle* h, int64_t batch, const void* x, con
         const void* in = l == 0 ? x : (const void*)(sv + S.A[l - 1]);
         const void* G = sc + W.G[cur];
         const float* gsl = gs_of(l);
-        RDCN_TRY(colsum(nout, G, nout, true, nullptr, grads->b[l]));
+        RDCN_TRY(colsum(nout, G, nout, COL_BF16, nullptr, grads->b[l]));
         if (c.gated) {
-            RDCN_TRY(colsum(nin, in, nin, true, gsl, grads->gate_w[l]));
+            // the gate logit's input as the forward read it (bf16 x, f16 a_{l-1})
+            if (l == 0) RDCN_TRY(colsum(nin, in, nin, COL_BF16, gsl, grads->gate_w[l]));
+            else RDCN_TRY(colsum(nin, sv + S.A16[l - 1], nin, COL_F16, gsl, grads->gate_w[l]));
             add_sum(gsl, grads->gate_b[l]);
         }
         {

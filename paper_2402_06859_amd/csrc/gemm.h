@@ -15,7 +15,8 @@ enum GemmEpi {
     EPI_RESID = 4,      // c (float) = gin + scale * acc
     EPI_RESID_X0 = 5,   // c (float) += gin + scale * acc
     // MLP layers (bf16 storage, A K-contiguous):
-    EPI_MLP_FWD = 6,    // c = ReLU(scale*acc + bias[n]) * (rowv ? sigmoid(rowv[m]) : 1)
+    EPI_MLP_FWD = 6,    // c = ReLU(scale*acc + bias[n]) * (rowv ? sigmoid(rowv[m]) : 1);
+                        // with c2: an f16 copy of c (c2_kind C2_F16, err needed)
     EPI_MLP_BWD = 7     // v = scale*acc + (colv ? rowv[m] * colv[n] : 0);
                         // act == NULL: c = v;
                         // else c = v * [act[m, n] > 0] * (rowg ? sigmoid(rowg[m]) : 1), and with
@@ -40,7 +41,7 @@ struct GemmArgs {
     const void* b;      // B(n, k) = b[n*ldb + k], or b[k*ldb + n] when b_kstrided
     int64_t ldb;
     bool a_kstrided, b_kstrided;
-    bool ops_f16;       // A and B hold f16 values (f16 MFMAs; both K-contiguous, no MLP epilogue)
+    bool ops_f16;       // A and B hold f16 values (f16 MFMAs; both K-contiguous, not EPI_MLP_BWD)
     int epi;
     float scale;
     void* c;            // output (see GemmEpi)

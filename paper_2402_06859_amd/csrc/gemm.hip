@@ -232,8 +232,9 @@ __device__ __forceinline__ void epilogue8(const GemmArgs& g, int64_t m, int64_t 
 
 // MLP epilogues on eight consecutive columns n .. n+7 of row m (n + 7 < N); returns
 // this thread's share of the row dot product sum(v * act) (EPI_MLP_BWD with act).
+// EPI_MLP_FWD with c2 (c2_kind C2_F16) also writes an f16 copy of the activations.
 template <typename T>
-__device__ __forceinline__ float mlp_epilogue8(const GemmArgs& g, int64_t m, int64_t n, float* v) {
+__device__ __forceinline__ float mlp_epilogue8(const GemmArgs& g, int64_t m, int64_t n, float* v, bool& ovf) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] *= g.scale;
     T* out = (T*)g.c + m * g.ldc + n;
@@ -244,6 +245,7 @@ __device__ __forceinline__ float mlp_epilogue8(const GemmArgs& g, int64_t m, int
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = relu_f(v[e] + b[e]) * gate;
         store8<T>(out, v);
+        if (g.c2) *(u32x4_t*)((_Float16*)g.c2 + m * g.ldc + n) = pack_f16x8(v, ovf);
         return 0.f;
     }
     if (g.colv) {  // the gate's rank-one term
@@ -696,7 +698,7 @@ __device__ __forceinline__ void block_epilogue(const GemmArgs& g, int64_t m0, in
                     float v[8];
                     *(f32x4_t*)v = *(const f32x4_t*)(cs + row * CP + col);
                     *(f32x4_t*)(v + 4) = *(const f32x4_t*)(cs + row * CP + col + 4);
-                    part = mlp_epilogue8<T>(g, m, n, v);
+                    part = mlp_epilogue8<T>(g, m, n, v, ovf);
                 }
                 if (g.rowpart) {  // uniform: the BN / 8 threads of one row are an aligned lane group
 #pragma unroll
@@ -848,11 +850,17 @@ hipError_t launch_tile(const GemmArgs& g, int splits, hipStream_t s) {
 #define RDCN_GEMM(AK, BKS, MLP) \
     hipLaunchKernelGGL((k_gemm_mfma<BM, BN, AK, BKS, ST, WM, WN, M32, T, MLP, false, KB>), grid, dim3(64 * WM * WN), 0, s, g)
     if (g.ops_f16) {
-        // f16 operands: the forward projections over f16 activations (both K-contiguous)
-        if (g.a_kstrided || g.b_kstrided || g.epi == EPI_MLP_FWD || g.epi == EPI_MLP_BWD || g.a2)
-            return hipErrorInvalidValue;
-        hipLaunchKernelGGL((k_gemm_mfma<BM, BN, false, false, ST, WM, WN, M32, T, false, true, KB>), grid,
-                           dim3(64 * WM * WN), 0, s, g);
+        // f16 operands: the forward products over f16 activations (both K-contiguous;
+        // the cross projections and the MLP layers, no split-K for the latter)
+        if (g.a_kstrided || g.b_kstrided || g.epi == EPI_MLP_BWD || g.a2) return hipErrorInvalidValue;
+        if (g.epi == EPI_MLP_FWD) {
+            if (splits != 1) return hipErrorInvalidValue;
+            hipLaunchKernelGGL((k_gemm_mfma<BM, BN, false, false, ST, WM, WN, M32, T, true, true, KB>), grid,
+                               dim3(64 * WM * WN), 0, s, g);
+        } else {
+            hipLaunchKernelGGL((k_gemm_mfma<BM, BN, false, false, ST, WM, WN, M32, T, false, true, KB>), grid,
+                               dim3(64 * WM * WN), 0, s, g);
+        }
     } else if (g.epi == EPI_MLP_FWD || g.epi == EPI_MLP_BWD) {
         // MLP layers: forward (both K-contiguous) and input gradient (B K-strided), no split-K
         if (g.a_kstrided || splits != 1) return hipErrorInvalidValue;

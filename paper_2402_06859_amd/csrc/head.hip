@@ -33,6 +33,7 @@ __device__ __forceinline__ int wave_sum_i(int v) {
 }
 
 __device__ __forceinline__ void ld8(const bf16_t* p, float* v) { st<bf16_t>::unpack(*(const u32x4_t*)p, v); }
+__device__ __forceinline__ void ld8(const _Float16* p, float* v) { unpack_f16x8(*(const u32x4_t*)p, v); }
 __device__ __forceinline__ void ld8(const float* p, float* v) {
     st<float>::unpack(*(const u32x4_t*)p, v);
     st<float>::unpack(*(const u32x4_t*)(p + 4), v + 4);
@@ -53,14 +54,15 @@ inline unsigned row_blocks(int64_t B) {
     return (unsigned)(b > 0 ? b : 1);
 }
 
-__global__ __launch_bounds__(256) void k_gate_logit(int64_t B, int n, const bf16_t* __restrict__ x, int64_t ldx,
+template <typename TX>
+__global__ __launch_bounds__(256) void k_gate_logit(int64_t B, int n, const TX* __restrict__ x, int64_t ldx,
                                                     const bf16_t* __restrict__ g, const bf16_t* __restrict__ c,
                                                     float* __restrict__ s) {
     const int lane = threadIdx.x & 63;
     const float cb = bf16_to_f32(*c);
     for (int64_t row = (int64_t)blockIdx.x * ROWS_PER_BLOCK + (threadIdx.x >> 6); row < B;
          row += (int64_t)gridDim.x * ROWS_PER_BLOCK) {
-        const bf16_t* xr = x + row * ldx;
+        const TX* xr = x + row * ldx;
         float acc = 0.f;
         for (int col = lane * 8; col < n; col += 512) {
             float xv[8], gv[8];
@@ -74,7 +76,8 @@ __global__ __launch_bounds__(256) void k_gate_logit(int64_t B, int n, const bf16
     }
 }
 
-__global__ __launch_bounds__(256) void k_head_out(int64_t B, int n, const bf16_t* __restrict__ aL,
+template <typename TA>
+__global__ __launch_bounds__(256) void k_head_out(int64_t B, int n, const TA* __restrict__ aL,
                                                   const bf16_t* __restrict__ w_out, const bf16_t* __restrict__ b_out,
                                                   CalArgs c, float* __restrict__ y, float* __restrict__ y2,
                                                   float* __restrict__ y_cal) {
@@ -82,7 +85,7 @@ __global__ __launch_bounds__(256) void k_head_out(int64_t B, int n, const bf16_t
     const float bo = bf16_to_f32(*b_out), cb = *c.b;
     for (int64_t row = (int64_t)blockIdx.x * ROWS_PER_BLOCK + (threadIdx.x >> 6); row < B;
          row += (int64_t)gridDim.x * ROWS_PER_BLOCK) {
-        const bf16_t* ar = aL + row * n;
+        const TA* ar = aL + row * n;
         float acc = 0.f;
         for (int col = lane * 8; col < n; col += 512) {
             float av[8], wv[8];
@@ -117,7 +120,8 @@ __global__ __launch_bounds__(256) void k_logloss(int64_t B, const float* __restr
     }
 }
 
-__global__ __launch_bounds__(256) void k_head_out_bwd(int64_t B, int n, const bf16_t* __restrict__ aL,
+template <typename TA>
+__global__ __launch_bounds__(256) void k_head_out_bwd(int64_t B, int n, const TA* __restrict__ aL,
                                                       const float* __restrict__ sL,
                                                       const bf16_t* __restrict__ w_out, const float* __restrict__ y,
                                                       CalArgs c, const float* __restrict__ g_cal,
@@ -138,7 +142,7 @@ __global__ __launch_bounds__(256) void k_head_out_bwd(int64_t B, int n, const bf
         }
         const float gy = gc * relu_f(er[k] + c.w[k]);
         const float rho = sL ? sigmoid_f(sL[row]) : 1.f;
-        const bf16_t* ar = aL + row * n;
+        const TA* ar = aL + row * n;
         bf16_t* gr = G + row * n;
         float dot = 0.f;
         for (int col = lane * 8; col < n; col += 512) {
@@ -252,18 +256,22 @@ hipError_t launch_vec_sums(int64_t B, const VecSums& v, hipStream_t st) {
     return hipGetLastError();
 }
 
-hipError_t launch_gate_logit(int64_t B, int n, const void* x, int64_t ldx, const void* g, const void* c, float* s,
-                             hipStream_t st) {
+hipError_t launch_gate_logit(int64_t B, int n, const void* x, bool x_f16, int64_t ldx, const void* g, const void* c,
+                             float* s, hipStream_t st) {
     if (B == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_gate_logit, dim3(row_blocks(B)), dim3(256), 0, st, B, n, (const bf16_t*)x, ldx,
-                       (const bf16_t*)g, (const bf16_t*)c, s);
+    if (x_f16)
+        hipLaunchKernelGGL(k_gate_logit<_Float16>, dim3(row_blocks(B)), dim3(256), 0, st, B, n, (const _Float16*)x, ldx,
+                           (const bf16_t*)g, (const bf16_t*)c, s);
+    else
+        hipLaunchKernelGGL(k_gate_logit<bf16_t>, dim3(row_blocks(B)), dim3(256), 0, st, B, n, (const bf16_t*)x, ldx,
+                           (const bf16_t*)g, (const bf16_t*)c, s);
     return hipGetLastError();
 }
 
 hipError_t launch_head_out(int64_t B, int n, const void* aL, const void* w_out, const void* b_out, const CalArgs& c,
                            float* y, float* y2, float* y_cal, hipStream_t st) {
     if (B == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_head_out, dim3(row_blocks(B)), dim3(256), 0, st, B, n, (const bf16_t*)aL,
+    hipLaunchKernelGGL(k_head_out<_Float16>, dim3(row_blocks(B)), dim3(256), 0, st, B, n, (const _Float16*)aL,
                        (const bf16_t*)w_out, (const bf16_t*)b_out, c, y, y2, y_cal);
     return hipGetLastError();
 }
@@ -281,7 +289,7 @@ hipError_t launch_head_out_bwd(int64_t B, int n, const void* aL, const float* sL
                                const CalArgs& c, const float* g_cal, float* grad_e, float* gy, void* G, float* gs,
                                hipStream_t st) {
     if (B == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_head_out_bwd, dim3(row_blocks(B)), dim3(256), 0, st, B, n, (const bf16_t*)aL, sL,
+    hipLaunchKernelGGL(k_head_out_bwd<_Float16>, dim3(row_blocks(B)), dim3(256), 0, st, B, n, (const _Float16*)aL, sL,
                        (const bf16_t*)w_out, y, c, g_cal, grad_e, gy, (bf16_t*)G, gs);
     return hipGetLastError();
 }
@@ -297,7 +305,7 @@ hipError_t launch_gate_finalize(int64_t B, int ntiles, const float* part, const 
 
 int64_t colsum_chunks(int64_t B) { return B > 0 ? (B + COLSUM_ROWS - 1) / COLSUM_ROWS : 1; }
 
-hipError_t launch_colsum_w(int64_t B, int64_t n, const void* X, int64_t ldx, bool x_bf16, const float* wgt,
+hipError_t launch_colsum_w(int64_t B, int64_t n, const void* X, int64_t ldx, ColType xt, const float* wgt,
                            float* part, float* out, hipStream_t st) {
     if (n == 0) return hipSuccess;
     const int64_t nch = colsum_chunks(B);
@@ -309,7 +317,10 @@ hipError_t launch_colsum_w(int64_t B, int64_t n, const void* X, int64_t ldx, boo
     const bool vec = n % 8 == 0 && ldx % 8 == 0;
     const int64_t cols_per_block = 64 * (vec ? 8 : 1);
     const dim3 grid((unsigned)((n + cols_per_block - 1) / cols_per_block), (unsigned)nch);
-    if (x_bf16) {
+    if (xt == COL_F16) {
+        if (!vec) return hipErrorInvalidValue;
+        hipLaunchKernelGGL((k_colsum_w<_Float16, 8>), grid, dim3(256), 0, st, B, n, (const _Float16*)X, ldx, wgt, part);
+    } else if (xt == COL_BF16) {
         if (vec) hipLaunchKernelGGL((k_colsum_w<bf16_t, 8>), grid, dim3(256), 0, st, B, n, (const bf16_t*)X, ldx, wgt, part);
         else hipLaunchKernelGGL((k_colsum_w<bf16_t, 1>), grid, dim3(256), 0, st, B, n, (const bf16_t*)X, ldx, wgt, part);
     } else {

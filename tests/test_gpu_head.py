@@ -3,10 +3,11 @@
 Two oracles. The plain one is the definition in float64 throughout (the same bf16
 parameters and inputs, no rounding of anything it computes); the device must match
 it within the bars of the bf16 cross stack (2e-2 forward, 5e-2 gradients). The
-emulating one rounds its stored hidden activations to bf16 (oracle.round_bf16), so
-that ReLU masks and the calibration bucket are decided on the values the device
-keeps (all its arithmetic is float64); against it the bars are tighter (2e-3
-forward, 1e-2 gradients: the device keeps the pre-activation gradients G in bf16).
+emulating one rounds its hidden activations to f16 (oracle.round_f16), the copy the
+device's forward reads, so that ReLU masks and the calibration bucket are decided
+on the values the device uses (all its arithmetic is float64); against it the bars
+are tighter (2e-3 forward, 1e-2 gradients: the device keeps the pre-activation
+gradients G in bf16, and its weight-gradient products read bf16 activations).
 
 Small shapes are compared in full; the Feed-sized head (4 x 3500, stored as
 4 x 3504 with zero padding) runs at the full batch in the launch configuration
@@ -26,7 +27,7 @@ from paper_2402_06859_amd.synth import HEADS, WORKLOADS, HeadSpec, Workload, mak
 
 pytestmark = pytest.mark.gpu
 
-Y_TOL = 2e-3      # logits / calibrated logits (bf16 rounding of activations on both sides)
+Y_TOL = 2e-3      # logits / calibrated logits (f16 rounding of activations on both sides)
 GRAD_TOL = 1e-2   # parameter and input gradients (device G in bf16)
 CAL_TOL = 1e-5    # the calibration bias gradient (a float sum of the upstream gradient)
 PLAIN_Y_TOL, PLAIN_GRAD_TOL = 2e-2, 5e-2  # against the plain float64 definition
@@ -43,7 +44,7 @@ def oracle_params(hinp: dict, head: HeadSpec) -> dict:
     return p
 
 
-def run_head(wl: Workload, head: HeadSpec, B: int, rows=None, seed=None, hinp=None, round_act=oracle.round_bf16):
+def run_head(wl: Workload, head: HeadSpec, B: int, rows=None, seed=None, hinp=None, round_act=oracle.round_f16):
     """Device forward + backward with upstream g_cal (zero outside `rows`), oracle on `rows`
     (round_act=None: the plain float64 definition)."""
     print("head", head.name, head.hidden, "gated", head.gated, "K", head.buckets, "B", B, "d", wl.d, flush=True)
@@ -66,7 +67,7 @@ def run_head(wl: Workload, head: HeadSpec, B: int, rows=None, seed=None, hinp=No
     return dh, ref, rows, p
 
 
-def sum_scale(x, p, g, rows, round_act=oracle.round_bf16) -> dict:
+def sum_scale(x, p, g, rows, round_act=oracle.round_f16) -> dict:
     """Sum over rows of |per-row contribution| of each scalar gradient (gate biases, b_out):
     the scale of the summation error bound. A scalar gradient can be a nearly cancelling
     sum (0.01 out of terms whose magnitudes add up to 14 on the ragged case), so it is
@@ -153,11 +154,15 @@ def test_large_mlp_full_batch_sampled():
         assert not np.any(gW[n:]) and not np.any(to_np(dh.grads["b"][l])[n:])
 
 
-@pytest.mark.parametrize("case", ["ragged_gated", "ragged_plain"])
+@pytest.mark.parametrize("case", ["ragged_gated", "ragged_plain", "lmlp"])
 def test_head_against_plain_float64_definition(case):
     """The device against the head computed in float64 from the same bf16 parameters and
     inputs with nothing rounded, at the bf16 bars (2e-2 forward, 5e-2 gradients): the
-    ragged head, gated and plain (many logits outside the bucket range)."""
+    ragged head, gated and plain (many logits outside the bucket range), and Feed's
+    Large MLP (4 x 3500, gated) on 64 sampled rows of a 4096 batch. On the latter,
+    activations rounded to bf16 would flip enough ReLU masks in the deeper layers to
+    move the gradients by about 6% from the definition; with the f16 copies the
+    float64 emulation of the device's rounding is 2.2% away (x and W0 gradients)."""
     need_gpu()
     if case == "lmlp":
         wl, head, B = WORKLOADS["small"], HEADS["lmlp"], WORKLOADS["small"].batch

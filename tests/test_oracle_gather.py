@@ -31,6 +31,27 @@ def test_round_bf16_matches_torch():
     assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
 
 
+def test_round_f16_against_the_binary16_format():
+    """Values fixed by the binary16 format itself (11 significant bits, exponents
+    -14 .. 15, subnormals down to 2^-24, round to nearest with ties to even), then a
+    sweep against torch's half conversion."""
+    cases = [(1.0 / 3.0, 1365 / 4096),               # 1.0101010101 x 2^-2, next bit 0
+             (0.1, 1638 / 16384), (-0.1, -1638 / 16384),
+             (1 + 2 ** -11, 1.0),                    # tie, even neighbour 1
+             (1 + 3 * 2 ** -11, 1 + 2 ** -9),        # tie, even neighbour 1 + 2^-9
+             (1 + 2 ** -11 + 2 ** -20, 1 + 2 ** -10),  # just above the tie
+             (65504.0, 65504.0), (65519.0, 65504.0), (65520.0, np.inf), (-70000.0, -np.inf),
+             (2.0 ** -14, 2.0 ** -14), (2.0 ** -24, 2.0 ** -24), (2.0 ** -25, 0.0),
+             (3 * 2.0 ** -26, 2.0 ** -24), (5 * 2.0 ** -25, 2 * 2.0 ** -24)]
+    x = np.array([c[0] for c in cases], np.float32)
+    want = np.array([c[1] for c in cases], np.float32)
+    assert np.array_equal(oracle.round_f16(x), want)
+    rng = np.random.default_rng(1)
+    y = (rng.standard_normal(100_000) * 10.0 ** rng.integers(-9, 6, 100_000)).astype(np.float32)
+    ref = torch.from_numpy(y).to(torch.float16).float().numpy()
+    assert np.array_equal(oracle.round_f16(y).view(np.uint32), ref.view(np.uint32))
+
+
 def test_gather_tiny_mul_vs_onehot():
     wl = WORKLOADS["tiny"]
     inp = make_inputs(wl, with_weights=False, with_grad=False)
