@@ -66,12 +66,14 @@ struct GemmArgs {
     const float* rowg;
     const void* act;
     float* rowpart;
+    int group_m;        // set from GemmPlan::group_m by launch_gemm
 };
 
 struct GemmPlan {
     int bm = 128, bn = 128;
     int splits = 1;
     int stages = 3;  // LDS ring depth (2 lets two workgroups share a CU)
+    int group_m = 0; // > 1: tiles walked in groups of group_m tile rows, column by column
 };
 
 // split_blocks: with split-K allowed, the workgroup count the K split aims for when

@@ -721,14 +721,27 @@ __attribute__((amdgpu_waves_per_eu(WM * WN == 8 ? 2 : 1, WM * WN == 8 ? 2 : 8)))
 
     const int tid = threadIdx.x;
     const int tiles_n = (int)((g.N + BN - 1) / BN);
-    const int ntiles = (int)(((g.M + BM - 1) / BM) * tiles_n);
-    const int t = xcd_remap(blockIdx.x, ntiles);
+    const int tiles_m = (int)((g.M + BM - 1) / BM);
+    const int t = xcd_remap(blockIdx.x, tiles_m * tiles_n);
+    int tm, tn;
+    if (g.group_m > 1) {
+        // groups of group_m tile rows, walked column by column: the blocks that run
+        // together on one XCD share group_m A panels and a few B panels in its L2
+        const int per = g.group_m * tiles_n, grp = t / per, first = grp * g.group_m;
+        const int rows = tiles_m - first < g.group_m ? tiles_m - first : g.group_m;
+        const int r = t - grp * per;
+        tm = first + r % rows;
+        tn = r / rows;
+    } else {
+        tm = t / tiles_n;
+        tn = t % tiles_n;
+    }
 
     typename P::Ctx c;
     c.g = &g;
     c.tid = tid;
-    c.m0 = (int64_t)(t / tiles_n) * BM;
-    c.n0 = (int64_t)(t % tiles_n) * BN;
+    c.m0 = (int64_t)tm * BM;
+    c.n0 = (int64_t)tn * BN;
     const int z = blockIdx.z;
     // split-K ranges are multiples of BK (itself a multiple of every KB)
     const int64_t kchunk = ((g.K + (int64_t)gridDim.z * BK - 1) / ((int64_t)gridDim.z * BK)) * BK;
@@ -915,15 +928,20 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, bool bf16, bool allow_split,
         };
         const double c256 = cost(256, 256), c128 = cost(256, 128);
         const int64_t t128 = ((M + 255) / 256) * ((N + 127) / 128);
+        // Tiles in groups of four tile rows: the 32 blocks an XCD runs at once then
+        // read 4 A panels and 8 B panels instead of 1-3 A panels and up to 32 B panels
+        // (measured on the large workload's six products: 2-8% faster, none slower).
         if (c256 <= c128) {
             p.bm = p.bn = 256;
             p.splits = 1;
             p.stages = 2;
+            p.group_m = 4;
         } else if (t128 >= 128) {
             p.bm = 256;
             p.bn = 128;
             p.splits = 1;
             p.stages = 3;
+            p.group_m = 4;
         }
     }
     return p;
@@ -937,16 +955,18 @@ hipError_t launch_gemm(const GemmArgs& g, const GemmPlan& p, bool bf16, hipStrea
         hipLaunchKernelGGL(k_gemm_f32, dim3((unsigned)tiles, 1, (unsigned)p.splits), dim3(256), 0, s, g);
         return hipGetLastError();
     }
+    GemmArgs ga = g;
+    ga.group_m = p.group_m;
     if (p.bm == 256) {
-        if (p.bn == 256) return launch_tile<256, 256, 2, 2, 4, true, bf16_t>(g, p.splits, s);
-        return launch_tile<256, 128, 3, 4, 2, true, bf16_t>(g, p.splits, s);
+        if (p.bn == 256) return launch_tile<256, 256, 2, 2, 4, true, bf16_t>(ga, p.splits, s);
+        return launch_tile<256, 128, 3, 4, 2, true, bf16_t>(ga, p.splits, s);
     }
     if (p.bm == 128) {
-        if (p.stages == 2) return launch_tile<128, 128, 2, 2, 2, false, bf16_t>(g, p.splits, s);
-        return launch_tile<128, 128, 3, 2, 2, false, bf16_t>(g, p.splits, s);
+        if (p.stages == 2) return launch_tile<128, 128, 2, 2, 2, false, bf16_t>(ga, p.splits, s);
+        return launch_tile<128, 128, 3, 2, 2, false, bf16_t>(ga, p.splits, s);
     }
-    if (p.stages == 2) return launch_tile<64, 64, 2, 2, 2, false, bf16_t>(g, p.splits, s);
-    return launch_tile<64, 64, 3, 2, 2, false, bf16_t>(g, p.splits, s);
+    if (p.stages == 2) return launch_tile<64, 64, 2, 2, 2, false, bf16_t>(ga, p.splits, s);
+    return launch_tile<64, 64, 3, 2, 2, false, bf16_t>(ga, p.splits, s);
 }
 
 // dst = f16(src), 8 values per thread and step; err bit on values beyond the f16 range.
