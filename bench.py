@@ -46,6 +46,12 @@ EXP_PEAK_PER_S = 256 * 4 * 8 * 2.4e9
 # Measured rate of independent exp + add pairs over all CUs (an exponential and one
 # more VALU op per pair, as a softmax needs at least): a practical ceiling beside the peak.
 EXP_ADD_MEASURED_PER_S = 14.7e12
+# Measured rates of the attention inner loop's instruction mix run alone (per lane: 16
+# exponentials, 8 packed conversions to f16, one 32x32x8 and two 16x16x32 f16 MFMAs,
+# 8 waves per SIMD), and of exponentials alone: what the exponent loop can reach
+# without loads, barriers or per-sample set-up.
+EXP_LOOP_MIX_MEASURED_PER_S = 13.5e12
+EXP_ONLY_MEASURED_PER_S = 17.4e12
 
 
 def kernel_work(wl, B: int) -> dict:
@@ -209,6 +215,23 @@ def measured_traffic(kernel: str, workload: str):
     return None
 
 
+def counter_record(prefix: str, kernel: str, workload: str):
+    """The '<prefix>: {json}' record of `kernel` on `workload` under profiles/ taken on the
+    kernel's current sources, or None."""
+    import glob
+    if kernel not in KERNEL_SOURCES:
+        return None
+    sha = sources_sha256(kernel)
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        with open(path) as fh:
+            for line in fh:
+                if line.startswith(prefix + ": "):
+                    rec = json.loads(line[len(prefix) + 2:])
+                    if rec.get("kernel") == kernel and rec.get("workload") == workload and rec.get("sha256") == sha:
+                        return rec
+    return None
+
+
 def phase_rooflines(work: dict, prof: dict, bf16: bool) -> dict:
     """Every timed kernel against its own bound: {kernel: {bound, achieved, unit, frac}}."""
     out = {}
@@ -266,7 +289,13 @@ def attention_exp_rate(wl, B: int, prof: dict):
         if n:
             rate = B * wl.rank * wl.rank / (ms / n / 1e3)
             out[k] = {"exp_per_s": rate, "frac_of_peak": rate / EXP_PEAK_PER_S,
-                      "frac_of_measured_exp_add_rate": rate / EXP_ADD_MEASURED_PER_S}
+                      "frac_of_measured_exp_add_rate": rate / EXP_ADD_MEASURED_PER_S,
+                      "frac_of_measured_loop_mix_rate": rate / EXP_LOOP_MIX_MEASURED_PER_S}
+            rec = counter_record("trans", k, wl.name)
+            if rec is not None:  # SQ_INSTS_VALU_TRANS_F32 x 64 of the same kernel and workload
+                out[k]["counter_exps_per_launch"] = rec["exps_per_launch"]
+                out[k]["counter_exps_over_pairs"] = rec["exps_per_launch"] / (B * wl.rank * wl.rank)
+                out[k]["valu_instr_per_exp_lane"] = rec["valu_instr_per_launch"] * 64 / rec["exps_per_launch"]
     return out
 
 
@@ -597,6 +626,7 @@ def main():
                        % args.steps
     if roof["bound"] == "exp":
         roof["frac_of_measured_exp_add_rate"] = roof["achieved"] * 1e12 / EXP_ADD_MEASURED_PER_S
+        roof["frac_of_measured_loop_mix_rate"] = roof["achieved"] * 1e12 / EXP_LOOP_MIX_MEASURED_PER_S
 
     kernels = {k: {"avg_us": (v[0] / v[1] * 1e3) if v[1] else 0.0, "per_step": v[1]} for k, v in prof.items() if v[1]}
     gemm_flops = sum(work[k][0] * prof[k][1] for k in work if k.endswith("_gemm") and k in prof)
