@@ -215,6 +215,13 @@ def measured_traffic(kernel: str, workload: str):
     return None
 
 
+def profile_tag(wl, head=None) -> str:
+    """The workload key of the counter records under profiles/: the workload's name, then
+    the variant and the head (e.g. 'small+hashed', 'feed+lmlp')."""
+    return (wl.name + ("+hashed" if wl.hashed else "") + ("+parallel" if wl.parallel else "")
+            + ("+" + head.name if head is not None else ""))
+
+
 def counter_record(prefix: str, kernel: str, workload: str):
     """The '<prefix>: {json}' record of `kernel` on `workload` under profiles/ taken on the
     kernel's current sources, or None."""
@@ -243,11 +250,11 @@ def phase_rooflines(work: dict, prof: dict, bf16: bool) -> dict:
     return out
 
 
-def gather_counter_gbps(wl, prof: dict):
+def gather_counter_gbps(tag: str, prof: dict):
     """HBM bytes of the gather from the FETCH_SIZE / WRITE_SIZE summaries under profiles/
     (while its sources are unchanged) over its measured launch time; None without a
     matching counter record."""
-    t = measured_traffic("gather", wl.name)
+    t = measured_traffic("gather", tag)
     ms, n = prof.get("gather", (0.0, 0))
     return t / (ms / n / 1e3) / 1e9 if (t is not None and n) else None
 
@@ -277,7 +284,7 @@ def mfma_counter_rates(wl, tag: str, prof: dict) -> dict:
     return out
 
 
-def attention_exp_rate(wl, B: int, prof: dict):
+def attention_exp_rate(wl, tag: str, B: int, prof: dict):
     """Exponentials per second of the attention kernels (one per (query, key) pair in the
     forward and one in the backward) against the chip's exponential rate and against the
     measured exp + add rate."""
@@ -291,7 +298,7 @@ def attention_exp_rate(wl, B: int, prof: dict):
             out[k] = {"exp_per_s": rate, "frac_of_peak": rate / EXP_PEAK_PER_S,
                       "frac_of_measured_exp_add_rate": rate / EXP_ADD_MEASURED_PER_S,
                       "frac_of_measured_loop_mix_rate": rate / EXP_LOOP_MIX_MEASURED_PER_S}
-            rec = counter_record("trans", k, wl.name)
+            rec = counter_record("trans", k, tag)
             if rec is not None:  # SQ_INSTS_VALU_TRANS_F32 x 64 of the same kernel and workload
                 out[k]["counter_exps_per_launch"] = rec["exps_per_launch"]
                 out[k]["counter_exps_over_pairs"] = rec["exps_per_launch"] / (B * wl.rank * wl.rank)
@@ -617,7 +624,7 @@ def main():
     avg_s = dom[0] / dom[1] / 1e3
     roof = roofline_for(dominant, work[dominant], avg_s, wl.dtype == "bf16")
     roof["frac"] = roof["achieved"] / roof["peak"]
-    tag = wl.name + ("+" + head.name if head is not None else "")
+    tag = profile_tag(wl, head)
     roof["traffic"] = measured_traffic(dominant, tag)
     roof["kernel"] = dominant
     roof["avg_us"] = avg_s * 1e6
@@ -632,7 +639,7 @@ def main():
     gemm_flops = sum(work[k][0] * prof[k][1] for k in work if k.endswith("_gemm") and k in prof)
     gemm_s = sum(prof[k][0] for k in prof if k.endswith("_gemm")) / 1e3
     gather_s = prof["gather"][0] / prof["gather"][1] / 1e3 if prof["gather"][1] else 0.0
-    counter_gbps = gather_counter_gbps(wl, prof)
+    counter_gbps = gather_counter_gbps(profile_tag(wl, head), prof)
     out = {
         "metric": METRIC,
         "value": B * args.steps / (ms / 1e3),
@@ -657,7 +664,7 @@ def main():
         "gather_counter_gbps": counter_gbps,
         "gather_model_gbps": (work["gather"][1] / gather_s / 1e9) if gather_s > 0 else None,
         "gather_model_frac": (work["gather"][1] / gather_s / 1e9 / PEAK_HBM_GBS) if gather_s > 0 else None,
-        "attention_exp_per_s": attention_exp_rate(wl, B, prof),
+        "attention_exp_per_s": attention_exp_rate(wl, profile_tag(wl, head), B, prof),
         "phases": phase_rooflines(work, prof, wl.dtype == "bf16"),
         "kernels": kernels,
     }
