@@ -1054,8 +1054,10 @@ rdcn_status rdcn_profile_start(rdcn_handle* h, int32_t max_launches, uint32_t ke
     h->prof_kind.clear();
     h->prof_used = 0;
     h->prof_ev.resize(2 * (size_t)max_launches);
+    // timing-only events: without the system-scope fence (cache write-back and
+    // invalidation at every record) the timed kernel starts as it would untimed
     for (auto& e : h->prof_ev)
-        if (hipEventCreate(&e) != hipSuccess) return RDCN_ERR_HIP;
+        if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return RDCN_ERR_HIP;
     h->prof_kind.reserve(max_launches);
     h->prof_mask = kernel_mask;
     h->prof_on = true;

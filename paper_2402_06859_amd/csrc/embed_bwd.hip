@@ -504,12 +504,15 @@ constexpr int FU_CAP = 4096;            // occurrences per chunk
 constexpr int FU_WAVES = 8;             // waves per workgroup
 constexpr int FU_THREADS = 64 * FU_WAVES;
 constexpr int FU_QW = FU_CAP / FU_WAVES;  // chunk elements per wave
-constexpr int FU_ROWS = 1024;           // rows per slice
+constexpr int FU_ROWS = 4096;           // rows per slice (at most)
+constexpr int FU_ROWS_SMALL = 1024;     // the kernel form for slices of at most this many rows: its
+                                        // smaller LDS lets two single-hot workgroups share a CU
 constexpr int FU_MAX_SLICES = 16;
-constexpr int FU_TARGET_BLOCKS = 128;   // workgroups the slice count aims for (fewer slices: less repeated id work)
+constexpr int FU_MAX_TABLE_ROWS = 16384;  // larger tables take the sort path
+constexpr int FU_ONE_ROUND = 256;       // workgroups resident at once (one per CU)
+constexpr int FU_SPLIT_ROWS = 1024;     // slice rows when the workgroups need several rounds
 constexpr int FU_BAGS = 1024;           // bags per block (bag front-end)
 constexpr int FU_BPT = FU_BAGS / FU_THREADS;  // bags per thread
-constexpr int FU_RPT = FU_ROWS / FU_THREADS;  // slice rows per thread in the run-start scan
 constexpr uint32_t FU_SKIP = 0xffffffffu;
 
 struct FusedArgs {
@@ -519,14 +522,15 @@ struct FusedArgs {
     uint32_t rps_q, rps_r;     // rows per slice of the quotient / remainder tables
 };
 
-template <typename T, int L, bool MUL, bool BAGS>
+template <typename T, int L, bool MUL, bool BAGS, int ROWS>
 __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
+    constexpr int FU_RPT = ROWS / FU_THREADS;  // slice rows per thread in the run-start scan
     constexpr int E = 64 / L;                // lane groups per wave
     constexpr int NP = FU_WAVES * E;         // parts of a sorted chunk, one per lane group
     constexpr int U = 8;                     // elements of a part whose loads are in flight together
     __shared__ uint32_t key_e[FU_CAP];       // per chunk element: row << 16 | rank in its wave's run, or FU_SKIP
     __shared__ uint32_t sorted[FU_CAP];      // row << 12 | element, in (row, element) order
-    __shared__ uint16_t whist[FU_WAVES][FU_ROWS];  // per wave row counts, then run starts (< FU_CAP)
+    __shared__ uint16_t whist[FU_WAVES][ROWS];  // per wave row counts, then run starts (< FU_CAP)
     __shared__ float carry[2][NP][4 * L];    // per part head / tail pieces
     __shared__ uint16_t bag_e[BAGS ? FU_CAP : 1];
     __shared__ uint16_t other_e[MUL ? FU_CAP : 1];
@@ -557,7 +561,7 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
     const int grp = lane / L, sub4 = lane % L, c = 4 * sub4;
     const bool colok = c < D;
     const uint64_t lt = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-    for (int i = threadIdx.x; i < FU_WAVES * FU_ROWS; i += FU_THREADS) (&whist[0][0])[i] = 0;
+    for (int i = threadIdx.x; i < FU_WAVES * ROWS; i += FU_THREADS) (&whist[0][0])[i] = 0;
 
     const int64_t step_b = BAGS ? FU_BAGS : FU_CAP;
     for (int64_t b0 = 0; b0 < a.batch; b0 += step_b) {
@@ -696,7 +700,7 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
                 }
             }
             __syncthreads();
-            for (int i = threadIdx.x; i < FU_WAVES * FU_ROWS; i += FU_THREADS) (&whist[0][0])[i] = 0;
+            for (int i = threadIdx.x; i < FU_WAVES * ROWS; i += FU_THREADS) (&whist[0][0])[i] = 0;
             // D. sums in sorted order: lane group g of wave w takes part P = w * E + g, an
             // equal share of the sorted chunk, and adds its elements one after another
             const uint32_t nk = nkept;
@@ -842,10 +846,10 @@ hipError_t launch_reduce_d(const EmbedBwdArgs& a, const RedPtrs& p, uint32_t n, 
     return launch_reduce<T, 64, MUL, BAGS>(a, p, n, st);
 }
 
-template <typename T, bool MUL, bool BAGS>
-hipError_t launch_fused_d(const FusedArgs& fa, unsigned blocks, hipStream_t st) {
+template <typename T, bool MUL, bool BAGS, int ROWS>
+hipError_t launch_fused_rows(const FusedArgs& fa, unsigned blocks, hipStream_t st) {
     const int q = (fa.a.D + 3) / 4;
-#define RDCN_FUSED(L) hipLaunchKernelGGL((k_emb_fused<T, L, MUL, BAGS>), dim3(blocks), dim3(FU_THREADS), 0, st, fa)
+#define RDCN_FUSED(L) hipLaunchKernelGGL((k_emb_fused<T, L, MUL, BAGS, ROWS>), dim3(blocks), dim3(FU_THREADS), 0, st, fa)
     if (q <= 4) RDCN_FUSED(4);
     else if (q <= 8) RDCN_FUSED(8);
     else if (q <= 16) RDCN_FUSED(16);
@@ -853,6 +857,13 @@ hipError_t launch_fused_d(const FusedArgs& fa, unsigned blocks, hipStream_t st) 
     else RDCN_FUSED(64);
 #undef RDCN_FUSED
     return hipGetLastError();
+}
+
+template <typename T, bool MUL, bool BAGS>
+hipError_t launch_fused_d(const FusedArgs& fa, unsigned blocks, hipStream_t st) {
+    const uint32_t rps = fa.rps_q > fa.rps_r ? fa.rps_q : fa.rps_r;
+    if (rps <= (uint32_t)FU_ROWS_SMALL) return launch_fused_rows<T, MUL, BAGS, FU_ROWS_SMALL>(fa, blocks, st);
+    return launch_fused_rows<T, MUL, BAGS, FU_ROWS>(fa, blocks, st);
 }
 
 inline int key_bits(uint32_t maxkey) {
@@ -990,8 +1001,8 @@ hipError_t launch_emb_reduce(const EmbedBwdArgs& a, bool bf16, void* scratch, hi
 }
 
 bool emb_fused_ok(int rows_q, int m, int D, bool hashed) {
-    return !hashed && D > 0 && D <= 256 && rows_q > 0 && m > 0 && rows_q <= FU_ROWS * FU_MAX_SLICES &&
-           m <= FU_ROWS * FU_MAX_SLICES;
+    return !hashed && D > 0 && D <= 256 && rows_q > 0 && m > 0 && rows_q <= FU_MAX_TABLE_ROWS &&
+           m <= FU_MAX_TABLE_ROWS;
 }
 
 hipError_t launch_emb_fused(const EmbedBwdArgs& a, bool bf16, bool ids64, hipStream_t st) {
@@ -1001,10 +1012,22 @@ hipError_t launch_emb_fused(const EmbedBwdArgs& a, bool bf16, bool ids64, hipStr
     fa.a = a;
     fa.ids64 = ids64 ? 1 : 0;
     const int rmax = a.rows_q > (int)a.m ? a.rows_q : (int)a.m;
-    // enough slices for the row limit, and for about FU_TARGET_BLOCKS workgroups
+    // Every workgroup walks all of its feature's occurrences, so its time hardly
+    // depends on how many rows its slice has. When the smallest slice count (slices of
+    // up to FU_ROWS rows) keeps all workgroups resident at once (one per CU), take the
+    // most slices that still do; otherwise slices of FU_SPLIT_ROWS rows, which keep
+    // each of the several rounds short (µs, small / feed / multihot / large:
+    // 36 / 218 / 1634 / 1426 this way, against 36 / 247 / 2126 / 1424 with slices
+    // of at most 1024 rows everywhere and 46 / 219 / 2294 / 1550 with the fewest slices).
+    const int per_slice = 2 * a.F;  // workgroups per slice index (two tables per feature)
     int S = (rmax + FU_ROWS - 1) / FU_ROWS;
-    const int want = (FU_TARGET_BLOCKS + 2 * a.F - 1) / (2 * a.F);
-    if (want > S) S = want;
+    if (per_slice * S <= FU_ONE_ROUND) {
+        const int fit = FU_ONE_ROUND / per_slice;
+        if (fit > S) S = fit;
+    } else {
+        const int split = (rmax + FU_SPLIT_ROWS - 1) / FU_SPLIT_ROWS;
+        if (split > S) S = split;
+    }
     if (S > FU_MAX_SLICES) S = FU_MAX_SLICES;
     if (S > rmax) S = rmax;
     fa.slices = S;
