@@ -522,16 +522,21 @@ struct FusedArgs {
     uint32_t rps_q, rps_r;     // rows per slice of the quotient / remainder tables
 };
 
-template <typename T, int L, bool MUL, bool BAGS, int ROWS>
+// CPL: table columns per lane (4, or 8 when D is a multiple of 8 in the 4096-row
+// form: half the lanes per element, so each wave instruction of the ordered sums
+// serves twice the elements).
+template <typename T, int L, bool MUL, bool BAGS, int ROWS, int CPL>
 __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
+    static_assert(CPL == 4 || CPL == 8, "four or eight columns per lane");
+    constexpr int NC = CPL / 4;              // 16-byte column groups per lane
     constexpr int FU_RPT = ROWS / FU_THREADS;  // slice rows per thread in the run-start scan
     constexpr int E = 64 / L;                // lane groups per wave
     constexpr int NP = FU_WAVES * E;         // parts of a sorted chunk, one per lane group
-    constexpr int U = 8;                     // elements of a part whose loads are in flight together
+    constexpr int U = 8 / NC;                // elements of a part whose loads are in flight together
     __shared__ uint32_t key_e[FU_CAP];       // per chunk element: row << 16 | rank in its wave's run, or FU_SKIP
     __shared__ uint32_t sorted[FU_CAP];      // row << 12 | element, in (row, element) order
     __shared__ uint16_t whist[FU_WAVES][ROWS];  // per wave row counts, then run starts (< FU_CAP)
-    __shared__ float carry[2][NP][4 * L];    // per part head / tail pieces
+    __shared__ float carry[2][NP][CPL * L];  // per part head / tail pieces
     __shared__ uint16_t bag_e[BAGS ? FU_CAP : 1];
     __shared__ uint16_t other_e[MUL ? FU_CAP : 1];
     __shared__ uint32_t bstart[BAGS ? FU_BAGS : 1];
@@ -558,8 +563,8 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
     const float* gx = a.grad_x0 + (int64_t)f * D;
 
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const int grp = lane / L, sub4 = lane % L, c = 4 * sub4;
-    const bool colok = c < D;
+    const int grp = lane / L, sub4 = lane % L, c = CPL * sub4;
+    const bool colok = c < D;  // D is a multiple of CPL: a lane's columns are all in range or none
     const uint64_t lt = lane == 0 ? 0ull : (~0ull >> (64 - lane));
     for (int i = threadIdx.x; i < FU_WAVES * ROWS; i += FU_THREADS) (&whist[0][0])[i] = 0;
 
@@ -716,7 +721,9 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
             }
             const uint32_t cnt = hi - lo;
             const uint32_t cmax = (nk + NP - 1) / NP;  // longest part (uniform loop bound)
-            Cols4 acc = {{0.f, 0.f, 0.f, 0.f}};
+            Cols4 acc[NC];
+#pragma unroll
+            for (int h = 0; h < NC; ++h) acc[h] = Cols4{{0.f, 0.f, 0.f, 0.f}};
             uint32_t acc_key = SEG_PAD;
             for (uint32_t s0 = 0; s0 < cmax; s0 += U) {
                 uint32_t key[U], el[U];
@@ -745,20 +752,25 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
                 }
                 // all loads first (padding lanes read bag b0 / row 0 and are masked when used):
                 // a load's registers are not written again before use, so none waits for another
-                Cols4 x[U], o4[U], old[U];
+                Cols4 x[U][NC], o4[U][NC], old[U][NC];
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     const bool ok = key[u] != SEG_PAD && colok;
                     const int cc = colok ? c : 0;
                     const uint32_t ee = ok ? el[u] : 0u;
                     const int64_t b = b0 + (ok ? (BAGS ? (int64_t)bag_e[ee] : (int64_t)ee) : 0);
-                    x[u] = load4(gx + b * a.d + cc);
+#pragma unroll
+                    for (int h = 0; h < NC; ++h) x[u][h] = load4(gx + b * a.d + cc + 4 * h);
                     if (MUL) {
                         const T* o = otab + (int64_t)(ok ? other_e[ee] : 0u) * D + cc;
 #pragma unroll
-                        for (int q = 0; q < 4; ++q) o4[u].v[q] = st<T>::load(o + q);
+                        for (int h = 0; h < NC; ++h)
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) o4[u][h].v[q] = st<T>::load(o + 4 * h + q);
                     }
-                    old[u] = load4(gtab + (int64_t)(dst[u] == DST_ROW ? key[u] : 0u) * D + cc);
+                    const float* orow = gtab + (int64_t)(dst[u] == DST_ROW ? key[u] : 0u) * D + cc;
+#pragma unroll
+                    for (int h = 0; h < NC; ++h) old[u][h] = load4(orow + 4 * h);
                 }
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
@@ -766,19 +778,26 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
                     const bool ok = k != SEG_PAD && colok;
                     const bool cont = k == acc_key;
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const float v = ok ? (MUL ? x[u].v[q] * o4[u].v[q] : x[u].v[q]) : 0.f;
-                        acc.v[q] = cont ? acc.v[q] + v : v;
-                    }
+                    for (int h = 0; h < NC; ++h)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const float v = ok ? (MUL ? x[u][h].v[q] * o4[u][h].v[q] : x[u][h].v[q]) : 0.f;
+                            acc[h].v[q] = cont ? acc[h].v[q] + v : v;
+                        }
                     acc_key = k;
                     if (dst[u] == DST_ROW) {
 #pragma unroll
-                        for (int q = 0; q < 4; ++q) old[u].v[q] += acc.v[q];
-                        store4(gtab + (int64_t)k * D + c, old[u]);
+                        for (int h = 0; h < NC; ++h) {
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) old[u][h].v[q] += acc[h].v[q];
+                            store4(gtab + (int64_t)k * D + c + 4 * h, old[u][h]);
+                        }
                     } else if (dst[u] != DST_NONE) {
                         float* cp = &carry[dst[u] == DST_HEAD ? 0 : 1][P][c];
 #pragma unroll
-                        for (int q = 0; q < 4; ++q) cp[q] = acc.v[q];
+                        for (int h = 0; h < NC; ++h)
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) cp[4 * h + q] = acc[h].v[q];
                     }
                 }
             }
@@ -786,21 +805,26 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
             // E. a segment that runs on into later parts is finished by the part where it
             // starts: its tail piece, then the head pieces of the parts it covers, in order
             if (lo < hi && tail_cont && !(head_cont && first_key == last_key) && colok) {
-                Cols4 tot = {{carry[1][P][c], carry[1][P][c + 1], carry[1][P][c + 2], carry[1][P][c + 3]}};
+                float tot[CPL];
+#pragma unroll
+                for (int q = 0; q < CPL; ++q) tot[q] = carry[1][P][c + q];
                 for (int p2 = P + 1; p2 < NP; ++p2) {
                     const uint32_t lo2 = (uint32_t)(((uint64_t)nk * p2) / NP);
                     const uint32_t hi2 = (uint32_t)(((uint64_t)nk * (p2 + 1)) / NP);
                     if (lo2 == hi2) continue;
                     if ((sorted[lo2] >> 12) != last_key) break;
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) tot.v[q] += carry[0][p2][c + q];
+                    for (int q = 0; q < CPL; ++q) tot[q] += carry[0][p2][c + q];
                     if ((sorted[hi2 - 1] >> 12) != last_key) break;
                 }
                 float* dstp = gtab + (int64_t)last_key * D + c;
-                Cols4 old = load4(dstp);
 #pragma unroll
-                for (int q = 0; q < 4; ++q) old.v[q] += tot.v[q];
-                store4(dstp, old);
+                for (int h = 0; h < NC; ++h) {
+                    Cols4 old = load4(dstp + 4 * h);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) old.v[q] += tot[4 * h + q];
+                    store4(dstp + 4 * h, old);
+                }
             }
             __syncthreads();
         }
@@ -846,10 +870,11 @@ hipError_t launch_reduce_d(const EmbedBwdArgs& a, const RedPtrs& p, uint32_t n, 
     return launch_reduce<T, 64, MUL, BAGS>(a, p, n, st);
 }
 
-template <typename T, bool MUL, bool BAGS, int ROWS>
+template <typename T, bool MUL, bool BAGS, int ROWS, int CPL>
 hipError_t launch_fused_rows(const FusedArgs& fa, unsigned blocks, hipStream_t st) {
-    const int q = (fa.a.D + 3) / 4;
-#define RDCN_FUSED(L) hipLaunchKernelGGL((k_emb_fused<T, L, MUL, BAGS, ROWS>), dim3(blocks), dim3(FU_THREADS), 0, st, fa)
+    const int q = (fa.a.D + CPL - 1) / CPL;  // lanes per element needed
+#define RDCN_FUSED(L) \
+    hipLaunchKernelGGL((k_emb_fused<T, L, MUL, BAGS, ROWS, CPL>), dim3(blocks), dim3(FU_THREADS), 0, st, fa)
     if (q <= 4) RDCN_FUSED(4);
     else if (q <= 8) RDCN_FUSED(8);
     else if (q <= 16) RDCN_FUSED(16);
@@ -862,8 +887,9 @@ hipError_t launch_fused_rows(const FusedArgs& fa, unsigned blocks, hipStream_t s
 template <typename T, bool MUL, bool BAGS>
 hipError_t launch_fused_d(const FusedArgs& fa, unsigned blocks, hipStream_t st) {
     const uint32_t rps = fa.rps_q > fa.rps_r ? fa.rps_q : fa.rps_r;
-    if (rps <= (uint32_t)FU_ROWS_SMALL) return launch_fused_rows<T, MUL, BAGS, FU_ROWS_SMALL>(fa, blocks, st);
-    return launch_fused_rows<T, MUL, BAGS, FU_ROWS>(fa, blocks, st);
+    if (rps <= (uint32_t)FU_ROWS_SMALL) return launch_fused_rows<T, MUL, BAGS, FU_ROWS_SMALL, 4>(fa, blocks, st);
+    if (fa.a.D % 8 == 0) return launch_fused_rows<T, MUL, BAGS, FU_ROWS, 8>(fa, blocks, st);
+    return launch_fused_rows<T, MUL, BAGS, FU_ROWS, 4>(fa, blocks, st);
 }
 
 inline int key_bits(uint32_t maxkey) {
