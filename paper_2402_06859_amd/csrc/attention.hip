@@ -612,9 +612,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 }
 
 // LDS of the backward, per sample (shared by its W waves): keys, row constants (8
-// bytes per row), Y^T (6 rows of f16, row stride rpad); per wave four slots for the
-// range check and the three scales.
-__host__ __device__ constexpr int attn_bwd_sample_floats(int rpad) { return rpad + 2 * rpad + 3 * rpad; }
+// bytes per row), Y^T (6 rows of f16 and two rows of zeros, row stride rpad); per
+// wave four slots for the range check and the three scales.
+__host__ __device__ constexpr int attn_bwd_sample_floats(int rpad) { return rpad + 2 * rpad + 4 * rpad; }
+
+// The backward's Y^T fragment of frag32<false>, every lane loading: the lanes whose
+// slots hold no quantity (the other half's, and quantities 6 and 7) read row 7, which
+// holds zeros, so the fragment needs no per-lane branches.
+__device__ __forceinline__ f16x8_t yfrag32(const _Float16* sy, int ld, int lane, int jb) {
+    const int qs = lane & 15, g4 = lane >> 4, q = qs & 7, h = g4 >> 1;
+    const int row = ((qs >> 3) != (g4 & 1) || q >= 6) ? 7 : q;
+    const f16x4_t lo = *(const f16x4_t*)(sy + xoff(row, jb + 4 * h, ld));
+    const f16x4_t hi = *(const f16x4_t*)(sy + xoff(row, jb + 8 + 4 * h, ld));
+    return f16x8_t{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+}
 __host__ __device__ constexpr int attn_bwd_wave_floats() { return 4; }
 __host__ __device__ constexpr int attn_bwd_block_floats(int rpad, int W) {
     return (4 / W) * attn_bwd_sample_floats(rpad) + 4 * attn_bwd_wave_floats();
@@ -735,6 +746,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             put_pair(sy, ldy, 0, i, ca[s] * ias);
             put_pair(sy, ldy, 2, i, cb[s] * ibs);
             put_pair(sy, ldy, 4, i, cg[s] * ics);
+            sy[xoff(6, i, ldy)] = (_Float16)0.f;
+            sy[xoff(7, i, ldy)] = (_Float16)0.f;
         }
     }
     if (W > 1) __syncthreads();
@@ -766,7 +779,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             const f32x16_t z16 = {};
             for (int i0 = 0; i0 < rpad; i0 += 32) {
                 const f16x4_t rec = *(const f16x4_t*)(scm + i0 + (lane & 31));
-                const f16x8_t y0 = frag32<false>(sy, ldy, lane, i0), y1 = frag32<false>(sy, ldy, lane, i0 + 16);
+                const f16x8_t y0 = yfrag32(sy, ldy, lane, i0), y1 = yfrag32(sy, ldy, lane, i0 + 16);
                 f32x16_t x[KB2];
 #pragma unroll
                 for (int q = 0; q < KB2; ++q) x[q] = __builtin_amdgcn_mfma_f32_32x32x8f16(rec, kf[q], z16, 0, 0, 0);
