@@ -440,13 +440,10 @@ __device__ __forceinline__ f16x8_t xfrag_fwd(const _Float16* sx, int ld, int n, 
 // quantities of row n to output slots 0-7 and those of row n + 16 to slots 8-15.
 // X^T fragment for such a sum at keys jb .. jb + 15: lane (g4, q) with q % 8 a
 // quantity row (row 3 and rows of the other half read as zero).
-// The backward's Y^T fragment is the same with K over rows and its 6 quantity rows
-// stored as they are (fwd = false).
-template <bool FWD>
 __device__ __forceinline__ f16x8_t frag32(const _Float16* sx, int ld, int lane, int jb) {
     const int qs = lane & 15, g4 = lane >> 4, q = qs & 7, h = g4 >> 1;
-    if ((qs >> 3) != (g4 & 1) || (FWD ? q == 3 : q >= 6)) return f16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
-    const int row = FWD ? xrow(q) : q;
+    if ((qs >> 3) != (g4 & 1) || q == 3) return f16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    const int row = xrow(q);
     const f16x4_t lo = *(const f16x4_t*)(sx + xoff(row, jb + 4 * h, ld));
     const f16x4_t hi = *(const f16x4_t*)(sx + xoff(row, jb + 8 + 4 * h, ld));
     return f16x8_t{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
@@ -541,7 +538,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             if (FAST) {
                 // 32-row tiles: acc[tt] holds rows 32 tt + n (lanes 0-31) and 32 tt + 16 + n
                 const f16x4_t kf = key_frag(sk[j0 + (lane & 31)], lane >> 5);
-                const f16x8_t a0 = frag32<true>(sx, ldx, lane, j0), a1 = frag32<true>(sx, ldx, lane, j0 + 16);
+                const f16x8_t a0 = frag32(sx, ldx, lane, j0), a1 = frag32(sx, ldx, lane, j0 + 16);
                 const f32x16_t z16 = {};
 #pragma unroll
                 for (int tt = 0; tt < NT / 2; ++tt) {
@@ -616,9 +613,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 // wave four slots for the range check and the three scales.
 __host__ __device__ constexpr int attn_bwd_sample_floats(int rpad) { return rpad + 2 * rpad + 4 * rpad; }
 
-// The backward's Y^T fragment of frag32<false>, every lane loading: the lanes whose
-// slots hold no quantity (the other half's, and quantities 6 and 7) read row 7, which
-// holds zeros, so the fragment needs no per-lane branches.
+// The backward's Y^T fragment, laid out as frag32's with K over rows and the 6
+// quantity rows stored as they are. Every lane loads: the lanes whose slots hold no
+// quantity (the other half's, and quantities 6 and 7) read row 7, which holds zeros,
+// so the fragment needs no per-lane branches.
 __device__ __forceinline__ f16x8_t yfrag32(const _Float16* sy, int ld, int lane, int jb) {
     const int qs = lane & 15, g4 = lane >> 4, q = qs & 7, h = g4 >> 1;
     const int row = ((qs >> 3) != (g4 & 1) || q >= 6) ? 7 : q;
