@@ -252,3 +252,26 @@ def test_batch_zero_and_batch_one():
     torch.cuda.synchronize()
     for t in db.g_w_down + db.g_u + db.g_bias:
         assert not torch.any(t)
+
+
+def test_f16_activation_overflow_is_reported():
+    """Activation mode 2 keeps x_l (l >= 1) in f16: a dense input of 7e4 (exact in bf16)
+    makes x_1 exceed the f16 range, and the forward reports RDCN_ERR_RANGE through the
+    device error word (read and cleared by rdcn_check_device_errors); a normal batch on
+    the same handle then reads as RDCN_OK."""
+    need_gpu()
+    from paper_2402_06859_amd import rdcn
+    wl = Workload("ovf_f16", 15, 64, 3, 5_000, 80, 16, 24, 2, 16, False, "bf16", "sum", 1.1, act_mode="f16")
+    inp = make_inputs(wl)
+    big = dict(inp, dense=torch.full_like(inp["dense"], 7.0e4))
+    db = DeviceBatch(wl, big)
+    db.gather()
+    db.forward()
+    torch.cuda.synchronize()
+    assert db.lib.check_device_errors() == rdcn.RDCN_ERR_RANGE
+    assert db.lib.check_device_errors() == rdcn.RDCN_OK  # cleared by the read
+    db2 = DeviceBatch(wl, inp)
+    db2.gather()
+    db2.forward()
+    torch.cuda.synchronize()
+    assert db2.lib.check_device_errors() == rdcn.RDCN_OK

@@ -248,3 +248,22 @@ def test_head_argument_errors():
         with pytest.raises(RdcnError) as ei:
             lib.head_configure(bad)
         assert ei.value.status == RDCN_ERR_ARG
+
+
+def test_head_f16_overflow_is_reported():
+    """The head's hidden activations go to the next layer as f16: an input of 1e6 (exact
+    enough in bf16) drives a_1 beyond the f16 range, and the forward reports
+    RDCN_ERR_RANGE through the device error word."""
+    need_gpu()
+    from paper_2402_06859_amd.rdcn import RDCN_ERR_RANGE, RDCN_OK
+    head = HeadSpec("ovf", (16, 8), gated=False, buckets=4, lo=-1.0, step=0.5)
+    hinp = make_head_inputs(RAGGED, head, batch=32)
+    lib = Rdcn(config_for(RAGGED, 32))
+    dh = DeviceHead(lib, head, dict(hinp, x=torch.full_like(hinp["x"], 1.0e6)), 32)
+    dh.forward()
+    torch.cuda.synchronize()
+    assert lib.check_device_errors() == RDCN_ERR_RANGE
+    dh2 = DeviceHead(lib, head, hinp, 32)
+    dh2.forward()
+    torch.cuda.synchronize()
+    assert lib.check_device_errors() == RDCN_OK
