@@ -503,8 +503,8 @@ __global__ __launch_bounds__(256) void k_seg_fixup(const uint32_t* __restrict__ 
 constexpr int FU_CAP = 4096;            // occurrences per chunk
 constexpr int FU_WAVES = 8;             // waves per workgroup
 constexpr int FU_THREADS = 64 * FU_WAVES;
-constexpr int FU_QW = FU_CAP / FU_WAVES;  // chunk elements per wave
 constexpr int FU_ROWS = 4096;           // rows per slice (at most)
+constexpr int FU_ROWS_MID = 2048;       // the form with chunks of 2 * FU_CAP occurrences
 constexpr int FU_ROWS_SMALL = 1024;     // the kernel form for slices of at most this many rows: its
                                         // smaller LDS lets two single-hot workgroups share a CU
 constexpr int FU_MAX_SLICES = 16;
@@ -525,20 +525,24 @@ struct FusedArgs {
 // CPL: table columns per lane (4, or 8 when D is a multiple of 8 in the 4096-row
 // form: half the lanes per element, so each wave instruction of the ordered sums
 // serves twice the elements).
-template <typename T, int L, bool MUL, bool BAGS, int ROWS, int CPL>
+template <typename T, int L, bool MUL, bool BAGS, int ROWS, int CPL, int CAP>
 __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
+    static_assert(CAP == 4096 || CAP == 8192, "chunk of 4096 or 8192 occurrences");
+    constexpr int QW = CAP / FU_WAVES;       // chunk elements per wave
+    constexpr int EB = CAP == 8192 ? 13 : 12;  // bits of a chunk element index in `sorted`
+    constexpr uint32_t EMASK = (1u << EB) - 1u;
     static_assert(CPL == 4 || CPL == 8, "four or eight columns per lane");
     constexpr int NC = CPL / 4;              // 16-byte column groups per lane
     constexpr int FU_RPT = ROWS / FU_THREADS;  // slice rows per thread in the run-start scan
     constexpr int E = 64 / L;                // lane groups per wave
     constexpr int NP = FU_WAVES * E;         // parts of a sorted chunk, one per lane group
     constexpr int U = 8 / NC;                // elements of a part whose loads are in flight together
-    __shared__ uint32_t key_e[FU_CAP];       // per chunk element: row << 16 | rank in its wave's run, or FU_SKIP
-    __shared__ uint32_t sorted[FU_CAP];      // row << 12 | element, in (row, element) order
-    __shared__ uint16_t whist[FU_WAVES][ROWS];  // per wave row counts, then run starts (< FU_CAP)
+    __shared__ uint32_t key_e[CAP];       // per chunk element: row << 16 | rank in its wave's run, or FU_SKIP
+    __shared__ uint32_t sorted[CAP];      // row << EB | element, in (row, element) order
+    __shared__ uint16_t whist[FU_WAVES][ROWS];  // per wave row counts, then run starts (< CAP)
     __shared__ float carry[2][NP][CPL * L];  // per part head / tail pieces
-    __shared__ uint16_t bag_e[BAGS ? FU_CAP : 1];
-    __shared__ uint16_t other_e[MUL ? FU_CAP : 1];
+    __shared__ uint16_t bag_e[BAGS ? CAP : 1];
+    __shared__ uint16_t other_e[MUL ? CAP : 1];
     __shared__ uint32_t bstart[BAGS ? FU_BAGS : 1];
     __shared__ int64_t boff[BAGS ? FU_BAGS : 1];
     __shared__ uint32_t sh[FU_WAVES];
@@ -568,7 +572,7 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
     const uint64_t lt = lane == 0 ? 0ull : (~0ull >> (64 - lane));
     for (int i = threadIdx.x; i < FU_WAVES * ROWS; i += FU_THREADS) (&whist[0][0])[i] = 0;
 
-    const int64_t step_b = BAGS ? FU_BAGS : FU_CAP;
+    const int64_t step_b = BAGS ? FU_BAGS : CAP;
     for (int64_t b0 = 0; b0 < a.batch; b0 += step_b) {
         const uint32_t nb = (uint32_t)(a.batch - b0 < step_b ? a.batch - b0 : step_b);
         uint32_t total = nb;  // occurrences of this block of bags
@@ -599,11 +603,11 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
             }
         }
         __syncthreads();
-        for (uint32_t c0 = 0; c0 < total; c0 += FU_CAP) {
-            const uint32_t n = total - c0 < (uint32_t)FU_CAP ? total - c0 : (uint32_t)FU_CAP;
+        for (uint32_t c0 = 0; c0 < total; c0 += CAP) {
+            const uint32_t n = total - c0 < (uint32_t)CAP ? total - c0 : (uint32_t)CAP;
             // A. rows of this wave's share (all id loads first, then the ranking); the
             // rank of each kept element among the wave's earlier elements of its row
-            constexpr int NIT = FU_QW / 64;
+            constexpr int NIT = QW / 64;
             int64_t pv[NIT];
             uint32_t bagv[NIT];
             if (BAGS) {
@@ -613,7 +617,7 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
                 uint32_t vv[NIT];
 #pragma unroll
                 for (int it = 0; it < NIT; ++it) {
-                    const uint32_t e = (uint32_t)(wv * FU_QW + it * 64 + lane);
+                    const uint32_t e = (uint32_t)(wv * QW + it * 64 + lane);
                     vv[it] = c0 + (e < n ? e : 0u);
                     bagv[it] = 0;
                 }
@@ -630,7 +634,7 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
             } else {
 #pragma unroll
                 for (int it = 0; it < NIT; ++it) {
-                    const uint32_t e = (uint32_t)(wv * FU_QW + it * 64 + lane);
+                    const uint32_t e = (uint32_t)(wv * QW + it * 64 + lane);
                     pv[it] = (b0 + (e < n ? e : 0u)) * a.F + f;
                     bagv[it] = 0;
                 }
@@ -647,7 +651,7 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
             const DivMagic dm{a.magic_m, a.shift_m, a.m};
 #pragma unroll
             for (int it = 0; it < NIT; ++it) {
-                const uint32_t e = (uint32_t)(wv * FU_QW + it * 64 + lane);
+                const uint32_t e = (uint32_t)(wv * QW + it * 64 + lane);
                 // ids below vocab <= rows_q * m <= 2^28 here: the 32-bit split is exact
                 const int64_t id = idv[it];
                 const uint32_t x = (uint32_t)id;
@@ -696,12 +700,12 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
             }
             __syncthreads();
             // C. placement
-            for (int it = 0; it < FU_QW / 64; ++it) {
-                const uint32_t e = (uint32_t)(wv * FU_QW + it * 64 + lane);
+            for (int it = 0; it < QW / 64; ++it) {
+                const uint32_t e = (uint32_t)(wv * QW + it * 64 + lane);
                 const uint32_t kv = key_e[e];
                 if (kv != FU_SKIP) {
                     const uint32_t row = kv >> 16;
-                    sorted[whist[wv][row] + (kv & 0xffffu)] = (row << 12) | e;
+                    sorted[whist[wv][row] + (kv & 0xffffu)] = (row << EB) | e;
                 }
             }
             __syncthreads();
@@ -714,10 +718,10 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
             uint32_t first_key = SEG_PAD, last_key = SEG_PAD;
             bool head_cont = false, tail_cont = false;
             if (lo < hi) {
-                first_key = sorted[lo] >> 12;
-                last_key = sorted[hi - 1] >> 12;
-                head_cont = lo > 0 && (sorted[lo - 1] >> 12) == first_key;
-                tail_cont = hi < nk && (sorted[hi] >> 12) == last_key;
+                first_key = sorted[lo] >> EB;
+                last_key = sorted[hi - 1] >> EB;
+                head_cont = lo > 0 && (sorted[lo - 1] >> EB) == first_key;
+                tail_cont = hi < nk && (sorted[hi] >> EB) == last_key;
             }
             const uint32_t cnt = hi - lo;
             const uint32_t cmax = (nk + NP - 1) / NP;  // longest part (uniform loop bound)
@@ -731,10 +735,10 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
                 for (int u = 0; u < U; ++u) {
                     const uint32_t i = s0 + u;
                     const uint32_t v = i < cnt ? sorted[lo + i] : 0u;
-                    key[u] = i < cnt ? v >> 12 : SEG_PAD;
-                    el[u] = v & 0xfffu;
+                    key[u] = i < cnt ? v >> EB : SEG_PAD;
+                    el[u] = v & EMASK;
                 }
-                const uint32_t key_after = s0 + U < cnt ? sorted[lo + s0 + U] >> 12 : SEG_PAD;
+                const uint32_t key_after = s0 + U < cnt ? sorted[lo + s0 + U] >> EB : SEG_PAD;
                 // where each segment that ends here goes: the table row, or this part's head /
                 // tail piece when the segment runs on into the previous / next part
                 int dst[U];
@@ -812,10 +816,10 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
                     const uint32_t lo2 = (uint32_t)(((uint64_t)nk * p2) / NP);
                     const uint32_t hi2 = (uint32_t)(((uint64_t)nk * (p2 + 1)) / NP);
                     if (lo2 == hi2) continue;
-                    if ((sorted[lo2] >> 12) != last_key) break;
+                    if ((sorted[lo2] >> EB) != last_key) break;
 #pragma unroll
                     for (int q = 0; q < CPL; ++q) tot[q] += carry[0][p2][c + q];
-                    if ((sorted[hi2 - 1] >> 12) != last_key) break;
+                    if ((sorted[hi2 - 1] >> EB) != last_key) break;
                 }
                 float* dstp = gtab + (int64_t)last_key * D + c;
 #pragma unroll
@@ -870,11 +874,11 @@ hipError_t launch_reduce_d(const EmbedBwdArgs& a, const RedPtrs& p, uint32_t n, 
     return launch_reduce<T, 64, MUL, BAGS>(a, p, n, st);
 }
 
-template <typename T, bool MUL, bool BAGS, int ROWS, int CPL>
+template <typename T, bool MUL, bool BAGS, int ROWS, int CPL, int CAP = FU_CAP>
 hipError_t launch_fused_rows(const FusedArgs& fa, unsigned blocks, hipStream_t st) {
     const int q = (fa.a.D + CPL - 1) / CPL;  // lanes per element needed
 #define RDCN_FUSED(L) \
-    hipLaunchKernelGGL((k_emb_fused<T, L, MUL, BAGS, ROWS, CPL>), dim3(blocks), dim3(FU_THREADS), 0, st, fa)
+    hipLaunchKernelGGL((k_emb_fused<T, L, MUL, BAGS, ROWS, CPL, CAP>), dim3(blocks), dim3(FU_THREADS), 0, st, fa)
     if (q <= 4) RDCN_FUSED(4);
     else if (q <= 8) RDCN_FUSED(8);
     else if (q <= 16) RDCN_FUSED(16);
@@ -888,6 +892,11 @@ template <typename T, bool MUL, bool BAGS>
 hipError_t launch_fused_d(const FusedArgs& fa, unsigned blocks, hipStream_t st) {
     const uint32_t rps = fa.rps_q > fa.rps_r ? fa.rps_q : fa.rps_r;
     if (rps <= (uint32_t)FU_ROWS_SMALL) return launch_fused_rows<T, MUL, BAGS, FU_ROWS_SMALL, 4>(fa, blocks, st);
+    // slices of up to 2048 rows without the product combine: chunks of 8192 occurrences,
+    // so each reached row of the slice is read and written half as often
+    if constexpr (!MUL)
+        if (rps <= (uint32_t)FU_ROWS_MID && fa.a.D % 8 == 0)
+            return launch_fused_rows<T, MUL, BAGS, FU_ROWS_MID, 8, 2 * FU_CAP>(fa, blocks, st);
     if (fa.a.D % 8 == 0) return launch_fused_rows<T, MUL, BAGS, FU_ROWS, 8>(fa, blocks, st);
     return launch_fused_rows<T, MUL, BAGS, FU_ROWS, 4>(fa, blocks, st);
 }

@@ -155,19 +155,22 @@ def test_embed_backward_single_hot_chunks(batch, mode):
     assert_unreached_zero(wl, inp, gq, gr)
 
 
-@pytest.mark.parametrize("combine", ["sum", "mul"])
-def test_embed_backward_bag_edges(combine):
-    """Bags: empty bags, a bag longer than a chunk (5000 ids), bags of one, and a hot id
-    that takes half of all occurrences; both combines."""
+@pytest.mark.parametrize("F,combine", [(3, "sum"), (3, "mul"), (64, "sum"), (64, "mul"), (120, "sum")])
+def test_embed_backward_bag_edges(F, combine):
+    """Bags: empty bags, a bag longer than a chunk, bags of one, and a hot id that takes
+    half of all occurrences; both combines. The feature count sets the slice count and
+    so the kernel form: 3 features, slices of at most 1024 rows (4096-occurrence
+    chunks); 64, slices of 1582 rows (8192-occurrence chunks with the sum combine, 4096
+    with the product); 120, whole 3163-row tables."""
     need_gpu()
-    F, B = 3, 700
+    B = 700
     wl = WORKLOADS["multihot"].with_(batch=B, num_cat=F, combine=combine, emb_dim=32, num_dense=16)
     inp = make_inputs(wl, with_weights=False, with_grad=False)
     rng = np.random.Generator(np.random.PCG64(11))
     lens = rng.integers(0, 12, size=(B, F))
     lens[rng.random((B, F)) < 0.2] = 0      # empty bags
-    lens[5, 1] = 5000                       # longer than one chunk
-    lens[600, 2] = 4500
+    lens[5, 1] = 5000 if F < 64 else 9000   # longer than one chunk
+    lens[600, 2] = 4500 if F < 64 else 8500
     lens[7, :] = 1
     offsets = np.zeros(B * F + 1, dtype=np.int64)
     np.cumsum(lens.reshape(-1), out=offsets[1:])
@@ -177,7 +180,7 @@ def test_embed_backward_bag_edges(combine):
     inp["ids"] = torch.from_numpy(ids.astype(np.int64))
     inp["offsets"] = torch.from_numpy(offsets)
     gx0 = grad_x0_like(wl, B, 12)
-    print("embed_bwd bag edges", combine, "nnz", nnz, flush=True)
+    print("embed_bwd bag edges", F, combine, "nnz", nnz, flush=True)
     gq, gr, status = run(wl, inp, gx0)
     assert status == rdcn.RDCN_OK
     rq, rr, _ = ref(wl, inp, gx0)
