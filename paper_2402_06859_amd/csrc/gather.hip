@@ -16,7 +16,10 @@
 // quotient- and remainder-row loads (the tables are small and stay in L2 / MALL),
 // and only then combines in float, pools over the bag in bag order, rounds to the
 // storage type and stores: the dependent id -> row load chains of its rows are in
-// flight together. Vectors of the dense block are copied.
+// flight together. A bag (multi-hot feature) is read in chunks of a few ids: the
+// chunk's id loads are issued together, then the row loads of all its ids, so a
+// bag of n ids costs about 2n/K dependent load latencies rather than 2n. Vectors of
+// the dense block are copied.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -40,6 +43,7 @@ __device__ __forceinline__ bool qr_split(ID id_raw, const GatherArgs& a, uint32_
 }
 
 constexpr int GATHER_ROWS = 4;  // rows per wave (their loads are issued together)
+constexpr int GATHER_BAG_CHUNK = 4;  // ids of a bag whose row loads are issued together
 
 // Table rows in the storage type: a lane's V values are one 16-byte vector.
 template <typename T>
@@ -113,14 +117,39 @@ __device__ __forceinline__ void hash_split(int64_t id, const GatherArgs& a, uint
     }
 }
 
+// Workgroup L of the one-dimensional grid of nx column blocks times ny row groups ->
+// (column block bx, row group by). Workgroups go round-robin to the 8 XCDs (L % 8).
+// Items are listed column block outermost, so a contiguous range of items touches the
+// tables of a few features only; each XCD takes an eighth of the ne * ny items of the
+// column blocks holding embedding columns as one contiguous range (those tables then
+// stay in its L2), followed by an eighth of the items of the dense-only blocks (plain
+// copies, far cheaper), so every XCD gets the same share of both kinds. Items left
+// over by the two divisions by 8 go to the last workgroups.
+__device__ __forceinline__ void gather_block(int L, int ne, int nx, int ny, int& bx, int& by) {
+    const int E = ne * ny, Q = (nx - ne) * ny;
+    const int eb = E / 8, qb = Q / 8;
+    int item;
+    if (L < 8 * (eb + qb)) {
+        const int k = L % 8, j = L / 8;
+        item = j < eb ? k * eb + j : E + k * qb + (j - eb);
+    } else {
+        const int i = L - 8 * (eb + qb), er = E - 8 * eb;
+        item = i < er ? 8 * eb + i : E + 8 * qb + (i - er);
+    }
+    bx = item / ny;
+    by = item - bx * ny;
+}
+
 template <typename T, typename ID, bool BAGS, class Rows, bool HASHED>
-__global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a) {
+__global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a, int ny) {
 #pragma clang fp contract(off)
     constexpr int V = st<T>::vec;
     const int cpf = a.D / V;                 // vectors per embedding segment
     const int emb_vecs = a.F * cpf;
     const int cpr = emb_vecs + a.Nd / V;     // vectors per x0 row
-    const int c = blockIdx.x * 64 + (threadIdx.x & 63);
+    int bx, by;
+    gather_block(blockIdx.x, (emb_vecs + 63) / 64, gridDim.x / ny, ny, bx, by);
+    const int c = bx * 64 + (threadIdx.x & 63);
     if (c >= cpr) return;
     const ID* ids = (const ID*)a.ids;
     T* x0 = (T*)a.x0;
@@ -131,8 +160,8 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a) {
     // table pair(s) of feature f: pair f, or pairs 2f (low hash half) and 2f + 1 (high)
     const Rows rows(a, HASHED ? 2 * f : f, cc);
     const Rows rows1(a, HASHED ? 2 * f + 1 : f, cc);
-    const int64_t row_step = (int64_t)gridDim.y * 4 * GATHER_ROWS;
-    for (int64_t b0 = ((int64_t)blockIdx.y * 4 + (threadIdx.x >> 6)) * GATHER_ROWS; b0 < a.batch; b0 += row_step) {
+    const int64_t row_step = (int64_t)ny * 4 * GATHER_ROWS;
+    for (int64_t b0 = ((int64_t)by * 4 + (threadIdx.x >> 6)) * GATHER_ROWS; b0 < a.batch; b0 += row_step) {
         const int nr = a.batch - b0 < GATHER_ROWS ? (int)(a.batch - b0) : GATHER_ROWS;
         u32x4_t out[GATHER_ROWS];
         if (!emb) {
@@ -200,52 +229,84 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a) {
             for (int u = 0; u < GATHER_ROWS; ++u) {
                 const int64_t bag = (b0 + (u < nr ? u : 0)) * a.F + f;
                 beg[u] = a.offsets[bag];
-                end[u] = a.offsets[bag + 1];
+                end[u] = u < nr ? a.offsets[bag + 1] : beg[u];
             }
+            // a bag is taken in chunks of K ids: the chunk's id loads, then all its row
+            // loads, are in flight together; the rows are then added in bag order
+            constexpr int K = HASHED ? (GATHER_BAG_CHUNK + 1) / 2 : GATHER_BAG_CHUNK;
             bool bad = false;
 #pragma unroll
             for (int u = 0; u < GATHER_ROWS; ++u) {
                 float acc[V];
+#pragma unroll
+                for (int e = 0; e < V; ++e) acc[e] = 0.0f;
                 bool started = false;
-                for (int64_t p = beg[u]; p < end[u]; ++p) {
-                    float x[V];
+                for (int64_t p0 = beg[u]; p0 < end[u]; p0 += K) {
+                    const int n = end[u] - p0 < K ? (int)(end[u] - p0) : K;
+                    ID id[K];
+#pragma unroll
+                    for (int k = 0; k < K; ++k)
+                        if (k < n) id[k] = ids[p0 + k];
                     if (HASHED) {
-                        uint32_t qi[2], ri[2];
-                        hash_split((int64_t)ids[p], a, qi, ri);
-                        float qa[V], ra[V], qb[V], rb[V];
-                        Rows::values(rows.load_q(qi[0]), qa);
-                        Rows::values(rows.load_r(ri[0]), ra);
-                        Rows::values(rows1.load_q(qi[1]), qb);
-                        Rows::values(rows1.load_r(ri[1]), rb);
+                        typename Rows::Raw q0[K], r0[K], q1[K], r1[K];
 #pragma unroll
-                        for (int e = 0; e < V; ++e) {
-                            const float e0 = a.combine == 0 ? qa[e] * ra[e] : qa[e] + ra[e];
-                            const float e1 = a.combine == 0 ? qb[e] * rb[e] : qb[e] + rb[e];
-                            x[e] = e0 + e1;
-                        }
+                        for (int k = 0; k < K; ++k)
+                            if (k < n) {
+                                uint32_t qi[2], ri[2];
+                                hash_split((int64_t)id[k], a, qi, ri);
+                                q0[k] = rows.load_q(qi[0]);
+                                r0[k] = rows.load_r(ri[0]);
+                                q1[k] = rows1.load_q(qi[1]);
+                                r1[k] = rows1.load_r(ri[1]);
+                            }
+#pragma unroll
+                        for (int k = 0; k < K; ++k)
+                            if (k < n) {
+                                float qa[V], ra[V], qb[V], rb[V];
+                                Rows::values(q0[k], qa);
+                                Rows::values(r0[k], ra);
+                                Rows::values(q1[k], qb);
+                                Rows::values(r1[k], rb);
+#pragma unroll
+                                for (int e = 0; e < V; ++e) {
+                                    const float e0 = a.combine == 0 ? qa[e] * ra[e] : qa[e] + ra[e];
+                                    const float e1 = a.combine == 0 ? qb[e] * rb[e] : qb[e] + rb[e];
+                                    acc[e] = started ? acc[e] + (e0 + e1) : e0 + e1;
+                                }
+                                started = true;
+                            }
                     } else {
-                        uint32_t qi, ri;
-                        if (!qr_split<ID>(ids[p], a, qi, ri)) {
-                            bad = true;
-                            continue;
+                        bool ok[K];
+                        typename Rows::Raw qw[K], rw[K];
+#pragma unroll
+                        for (int k = 0; k < K; ++k) {
+                            uint32_t qi = 0, ri = 0;
+                            ok[k] = k < n && qr_split<ID>(id[k], a, qi, ri);
+                            bad = bad || (k < n && !ok[k]);
+                            if (ok[k]) {
+                                qw[k] = rows.load_q(qi);
+                                rw[k] = rows.load_r(ri);
+                            }
                         }
-                        float qv[V], rv[V];
-                        Rows::values(rows.load_q(qi), qv);
-                        Rows::values(rows.load_r(ri), rv);
 #pragma unroll
-                        for (int e = 0; e < V; ++e) x[e] = a.combine == 0 ? qv[e] * rv[e] : qv[e] + rv[e];
+                        for (int k = 0; k < K; ++k)
+                            if (ok[k]) {
+                                float qv[V], rv[V];
+                                Rows::values(qw[k], qv);
+                                Rows::values(rw[k], rv);
+#pragma unroll
+                                for (int e = 0; e < V; ++e) {
+                                    const float x = a.combine == 0 ? qv[e] * rv[e] : qv[e] + rv[e];
+                                    acc[e] = started ? acc[e] + x : x;
+                                }
+                                started = true;
+                            }
                     }
-#pragma unroll
-                    for (int e = 0; e < V; ++e) acc[e] = started ? acc[e] + x[e] : x[e];
-                    started = true;
                 }
-                if (!started) {
-#pragma unroll
-                    for (int e = 0; e < V; ++e) acc[e] = 0.0f;
-                }
-                out[u] = st<T>::pack(acc);
+                if (u < nr) *(u32x4_t*)(x0 + (b0 + u) * d + (int64_t)c * V) = st<T>::pack(acc);
             }
             if (bad && cc == 0) atomicOr(a.err, 1);
+            continue;  // each bag's row was stored when its sum was complete
         }
 #pragma unroll
         for (int u = 0; u < GATHER_ROWS; ++u)
@@ -299,16 +360,21 @@ hipError_t launch_gather_rows(const GatherArgs& a, bool bf16, bool ids64, hipStr
     const int V = bf16 ? 8 : 4;
     const int64_t cpr = (a.F * (int64_t)a.D + a.Nd) / V;
     if (a.batch == 0 || cpr == 0) return hipSuccess;
-    // x: 64-column slices of a row; y: groups of 4 waves x GATHER_ROWS rows (grid-stride beyond)
+    // nx 64-column slices of a row times ny groups of 4 waves x GATHER_ROWS rows
+    // (grid-stride beyond), as one dimension
+    const int64_t nx = (cpr + 63) / 64;
     int64_t ygroups = (a.batch + 4 * GATHER_ROWS - 1) / (4 * GATHER_ROWS);
     if (ygroups > 65535) ygroups = 65535;
-    const dim3 grid((unsigned)((cpr + 63) / 64), (unsigned)ygroups);
+    if (nx * ygroups > (1 << 24) - 1) ygroups = ((1 << 24) - 1) / nx;  // grid of under 2^32 threads
+    if (ygroups < 1) return hipErrorInvalidValue;
+    const int ny = (int)ygroups;
+    const dim3 grid((unsigned)(nx * ygroups));
     const int threads = 256;
     const bool bags = a.offsets != nullptr;
 #define RDCN_GATHER(T, ID, BG)                                                                         \
     do {                                                                                               \
-        if (a.hashed) hipLaunchKernelGGL((k_qr_gather<T, ID, BG, R<T>, true>), grid, dim3(threads), 0, s, a);  \
-        else hipLaunchKernelGGL((k_qr_gather<T, ID, BG, R<T>, false>), grid, dim3(threads), 0, s, a);          \
+        if (a.hashed) hipLaunchKernelGGL((k_qr_gather<T, ID, BG, R<T>, true>), grid, dim3(threads), 0, s, a, ny); \
+        else hipLaunchKernelGGL((k_qr_gather<T, ID, BG, R<T>, false>), grid, dim3(threads), 0, s, a, ny);          \
     } while (0)
     if (bf16) {
         if (ids64) { if (bags) RDCN_GATHER(bf16_t, int64_t, true); else RDCN_GATHER(bf16_t, int64_t, false); }
