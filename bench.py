@@ -613,11 +613,14 @@ def main():
     if head is not None:
         work.update(head_work(wl, head, B))
     dominant = max((k for k in prof if k in work), key=lambda k: prof[k][0])
-    db.lib.profile_start(4 * args.steps * 64, [dominant])
+    # the gather (one launch per step) is timed over the same steps, not from one launch
+    timed = [dominant] + (["gather"] if dominant != "gather" and prof.get("gather", (0, 0))[1] else [])
+    db.lib.profile_start(4 * args.steps * 64, timed)
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
-    dom = db.lib.profile_stop()[dominant]
+    steps_prof = db.lib.profile_stop()
+    dom = steps_prof[dominant]
     db.lib.set_side_stream(side_on)
 
     ms_step = ms / args.steps
@@ -638,6 +641,10 @@ def main():
     kernels = {k: {"avg_us": (v[0] / v[1] * 1e3) if v[1] else 0.0, "per_step": v[1]} for k, v in prof.items() if v[1]}
     gemm_flops = sum(work[k][0] * prof[k][1] for k in work if k.endswith("_gemm") and k in prof)
     gemm_s = sum(prof[k][0] for k in prof if k.endswith("_gemm")) / 1e3
+    gprof = steps_prof.get("gather", (0.0, 0))
+    if gprof[1]:
+        prof["gather"] = gprof
+        kernels["gather"] = {"avg_us": gprof[0] / gprof[1] * 1e3, "per_step": 1, "launches_timed": gprof[1]}
     gather_s = prof["gather"][0] / prof["gather"][1] / 1e3 if prof["gather"][1] else 0.0
     counter_gbps = gather_counter_gbps(profile_tag(wl, head), prof)
     out = {
