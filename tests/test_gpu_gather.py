@@ -62,6 +62,31 @@ def test_gather_variants(name, combine, id_type, mode):
     assert_bitexact(wl, x0, oracle_x0(wl, inp))
 
 
+@pytest.mark.parametrize("batch,F,D,Nd,dtype,multi_hot", [
+    # 3 column blocks (two holding embedding columns, one dense-only), 37 row groups:
+    # both item counts leave remainders after the split over the 8 XCDs
+    (587, 10, 64, 896, "bf16", False),
+    (587, 10, 64, 896, "bf16", True),
+    # one column block, float storage, a ragged last column block of 13 vectors
+    (1001, 3, 4, 40, "f32", False),
+    # more than 65535 row groups of 16 rows: the row groups are walked grid-stride
+    (1_100_000, 2, 8, 8, "bf16", False),
+    (1_050_001, 1, 4, 4, "f32", True),
+])
+def test_gather_grid_shapes(batch, F, D, Nd, dtype, multi_hot):
+    """x0 bit-exact on shapes chosen for the launch's block mapping rather than for a
+    workload: remainders in the per-XCD split, a dense-only column block, and batches
+    past the grid's row-group limit."""
+    need_gpu()
+    wl = WORKLOADS["tiny"].with_(batch=batch, num_cat=F, emb_dim=D, num_dense=Nd, dtype=dtype,
+                                 multi_hot=multi_hot, bag_mean=3.0, bag_max=8)
+    inp = make_inputs(wl, with_weights=False, with_grad=False)
+    print("gather grid shape B %d F %d D %d Nd %d %s bags %s" % (batch, F, D, Nd, dtype, multi_hot), flush=True)
+    x0, status = run_gather(wl, inp)
+    assert status == rdcn.RDCN_OK
+    assert_bitexact(wl, x0, oracle_x0(wl, inp))
+
+
 def test_gather_ragged_batch_and_bags_with_empty_and_bad_ids():
     need_gpu()
     wl = WORKLOADS["multihot"].with_(batch=37, num_cat=3, num_dense=8)
