@@ -26,8 +26,11 @@ __device__ __forceinline__ u32x4_t pack_f16x8(const float* v, bool& ovf) {
     for (int i = 0; i < 4; ++i) {
         const half2_t p = {(_Float16)v[2 * i], (_Float16)v[2 * i + 1]};
         w[i] = __builtin_bit_cast(uint32_t, p);
-        ovf |= fabsf(v[2 * i]) >= F16_OVERFLOW || fabsf(v[2 * i + 1]) >= F16_OVERFLOW;
     }
+    // one test on the largest magnitude (fmaxf passes over NaN, which is not flagged)
+    const float mx = fmaxf(fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))),
+                           fmaxf(fmaxf(fabsf(v[4]), fabsf(v[5])), fmaxf(fabsf(v[6]), fabsf(v[7]))));
+    ovf |= mx >= F16_OVERFLOW;
     return u32x4_t{w[0], w[1], w[2], w[3]};
 }
 
@@ -41,16 +44,19 @@ __device__ __forceinline__ void unpack_f16x8(const u32x4_t& w, float* v) {
     }
 }
 
-// float -> bfloat16 bits, round to nearest, ties to even (NaN kept quiet).
-__device__ __forceinline__ uint32_t f32_to_bf16(float x) {
-    uint32_t u = __float_as_uint(x);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return u >> 16;
+// Two floats -> one word holding (lo, hi) bfloat16 values: gfx950's packed conversion
+// (v_cvt_pk_bf16_f32), one instruction for both. It rounds as the wave's float mode
+// says, and every kernel here runs with round to nearest, ties to even, and float
+// denormals kept, so the result is the nearest bfloat16 with ties to even for every
+// finite input (denormals and overflow to infinity included); NaN stays NaN.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    const bf16x2_t p = {(__bf16)lo, (__bf16)hi};
+    return __builtin_bit_cast(uint32_t, p);
 }
 
-// Two floats -> one word holding (lo, hi) bfloat16 values.
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) { return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16); }
+// float -> bfloat16 bits (as pack_bf16x2).
+__device__ __forceinline__ uint32_t f32_to_bf16(float x) { return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)x); }
 
 // Storage-type traits: T is float or bf16_t.
 template <typename T> struct st;

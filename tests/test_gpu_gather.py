@@ -87,6 +87,49 @@ def test_gather_grid_shapes(batch, F, D, Nd, dtype, multi_hot):
     assert_bitexact(wl, x0, oracle_x0(wl, inp))
 
 
+# Row 0 of both tables: per column, a pair whose combine rounds to bf16 at an edge.
+# sum: ties to even (down and up), a tie at the largest finite value (to infinity, both
+# signs), a tie at 3 (stays), values below and above half an ulp. mul: ties to even in the normal
+# range (down, up), products below the float normal range that round to a bf16 denormal
+# or to zero (ties to even, signed zero), above half an ulp, and a float overflow.
+_BF16_MAX = (2.0 - 2.0 ** -7) * 2.0 ** 127
+_EDGES = {
+    "sum": ([1.0, 1 + 2 ** -7, _BF16_MAX, -_BF16_MAX, 3.0, -(1 + 2 ** -7), 1.0, 2.0],
+            [2 ** -8, 2 ** -8, 2.0 ** 119, -2.0 ** 119, 2 ** -7, -2 ** -8, 2 ** -9, 3 * 2 ** -8]),
+    "mul": ([1 + 8 * 2 ** -7, 1 + 2 ** -7, 2.0 ** -67, 1.5 * 2.0 ** -66, 1.25 * 2.0 ** -65, 1.75 * 2.0 ** -66,
+             -(2.0 ** -67), (2 - 2 ** -7) * 2.0 ** 64],
+            [1 + 8 * 2 ** -7, 1 + 64 * 2 ** -7, 2.0 ** -67, 2.0 ** -67, 2.0 ** -67, 2.0 ** -67, 2.0 ** -67,
+             (2 - 2 ** -7) * 2.0 ** 63]),
+}
+
+
+@pytest.mark.parametrize("combine", ["sum", "mul"])
+def test_gather_bf16_rounding_edges(combine):
+    """x0 bit-exact where rounding the float combine to bf16 is decided by a tie, by a
+    result below the float normal range or by overflow: the conversion every bf16 output
+    of the library goes through."""
+    need_gpu()
+    wl = WORKLOADS["tiny"].with_(dtype="bf16", combine=combine, batch=40, num_cat=2, emb_dim=8, num_dense=8,
+                                 vocab=256, table_rows=16)
+    inp = make_inputs(wl, with_weights=False, with_grad=False)
+    qv, rv = _EDGES[combine]
+    for t, vals in (("q_tables", qv), ("r_tables", rv)):
+        tab = inp[t].float()
+        tab[:, 0, :] = torch.tensor(vals, dtype=torch.float32)
+        assert torch.equal(tab[:, 0, :].to(torch.bfloat16).float(), tab[:, 0, :]), "edge values are bf16 values"
+        inp[t] = tab.to(torch.bfloat16)
+    inp["ids"][::2, :] = 0  # even rows: id 0 = (quotient row 0, remainder row 0) in both features
+    x0, status = run_gather(wl, inp)
+    assert status == rdcn.RDCN_OK
+    ref = oracle_x0(wl, inp)
+    assert_bitexact(wl, x0, ref)
+    # the oracle's values on the edge rows are the ones intended
+    got = torch.from_numpy(np.ascontiguousarray(ref[0, :8])).to(torch.bfloat16).view(torch.int16).numpy().astype(np.int64) & 0xffff
+    want = {"sum": [0x3F80, 0x3F82, 0x7F80, 0xFF80, 0x4040, 0xBF82, 0x3F80, 0x4001],
+            "mul": [0x3F90, 0x3FC2, 0x0000, 0x0002, 0x0002, 0x0002, 0x8000, 0x7F80]}[combine]
+    assert got.tolist() == want, [hex(v) for v in got.tolist()]
+
+
 def test_gather_ragged_batch_and_bags_with_empty_and_bad_ids():
     need_gpu()
     wl = WORKLOADS["multihot"].with_(batch=37, num_cat=3, num_dense=8)
