@@ -8,18 +8,21 @@
 // features into x0.
 //
 // Work split: the output x0 [B, d] is cut into 16-byte vectors (8 bf16 or 4
-// floats). A wave owns 64 consecutive vector columns of x0 and a few rows: lane l
-// always produces column c = 64 * blockIdx.x + l, so its feature, the position
-// inside the feature's segment (or inside the dense block) and its table offsets
-// are fixed, and every store instruction writes one contiguous 1 KiB run of a row.
+// floats). A wave owns one block of 64 consecutive vector columns of x0 and a few
+// rows: lane l always produces column c = 64 * bx + l of its block bx, so its
+// feature, the position inside the feature's segment (or inside the dense block) and
+// its table offsets are fixed, and every store instruction writes one contiguous
+// 1 KiB run of a row. Blocks go to the XCDs in contiguous ranges of column blocks
+// (gather_block), so each XCD reads the tables of a few features and keeps them in
+// its L2.
 // The wave first issues the id (or bag-offset) loads of all its rows, then the
 // quotient- and remainder-row loads (the tables are small and stay in L2 / MALL),
 // and only then combines in float, pools over the bag in bag order, rounds to the
 // storage type and stores: the dependent id -> row load chains of its rows are in
-// flight together. A bag (multi-hot feature) is read in chunks of a few ids: the
-// chunk's id loads are issued together, then the row loads of all its ids, so a
-// bag of n ids costs about 2n/K dependent load latencies rather than 2n. Vectors of
-// the dense block are copied.
+// flight together. A bag (multi-hot feature) is read in chunks of K ids
+// (GATHER_BAG_CHUNK): the chunk's id loads are issued together, then the row loads of
+// all its ids, so a bag of n ids costs about 2n/K dependent load latencies rather
+// than 2n. Vectors of the dense block are copied.
 #include "device_common.h"
 #include "kernels.h"
 
