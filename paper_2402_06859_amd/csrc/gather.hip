@@ -45,7 +45,7 @@ __device__ __forceinline__ bool qr_split(ID id_raw, const GatherArgs& a, uint32_
     return qi < (uint32_t)a.rows_q && ri < a.m;
 }
 
-constexpr int GATHER_ROWS = 4;  // rows per wave (their loads are issued together)
+constexpr int GATHER_ROWS = 2;  // rows per wave (their loads are issued together)
 constexpr int GATHER_BAG_CHUNK = 4;  // ids of a bag whose row loads are issued together
 
 // Table rows in the storage type: a lane's V values are one 16-byte vector.
