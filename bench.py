@@ -84,8 +84,11 @@ def kernel_work(wl, B: int) -> dict:
     exp_f = 2.0 * EXP_SLOTS
     pair_fwd = (2.0 + exp_f + 1.0) if wl.dtype == "bf16" else (2.0 + exp_f + 3.0)
     pair_bwd = (2.0 + exp_f + 1.0) if wl.dtype == "bf16" else (2 * (2.0 + exp_f) + 11.0)
-    stats = 2 * r * 4 if wl.dtype == "bf16" else 0  # saved (o, Z) per row
-    w["fwd_attention"] = (0.0, B * (3 * r * 4 + r * eb + stats), pair_fwd * B * r * r)
+    # saved per row by the matrix-core forward: (o, Z) and the backward's row sums (W1, W2)
+    stats = 4 * r * 4 if wl.dtype == "bf16" else 0
+    # h, and its second plane when the activations are held as f16 or as bf16 hi + lo
+    h_out = r * eb * (2 if wl.act_mode in ("f16", "hilo") else 1)
+    w["fwd_attention"] = (0.0, B * (3 * r * 4 + h_out + stats), pair_fwd * B * r * r)
     # up projection + cross epilogue: h, U, bias, x0, x_l in; t, x_{l+1} out
     w["fwd_up_gemm"] = (2.0 * B * d * hr, B * hr * eb + d * hr * eb + d * eb + 4 * B * d * eb, 0.0)
     # average over layers of: g in (storage on the top layer, float below), x0, t, grad_x0 (rmw below top), gt out

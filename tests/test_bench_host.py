@@ -45,6 +45,21 @@ def test_work_model_large_products():
     assert w["fwd_attention"][2] / 7.0 == pytest.approx(wl.batch * wl.rank * wl.rank)
 
 
+def test_work_model_attention_bytes():
+    """Bytes of the attention kernels written out from what they move per sample: the
+    forward reads [v|q|k] (float) and writes h (bf16, plus its f16 copy when the
+    activations are held in f16) and four float statistics per row (o, Z, W1, W2); the
+    backward reads [v|q|k], the float gh and the statistics and writes [gv|gq|gk]."""
+    wl = WORKLOADS["large"]  # f16 activations
+    B, r = wl.batch, wl.rank
+    w = bench.kernel_work(wl, B)
+    assert w["fwd_attention"][1] == B * (3 * r * 4 + 2 * r * 2 + 4 * r * 4)
+    assert w["bwd_attention"][1] == B * (3 * r * 4 + r * 4 + 4 * r * 4 + 3 * r * 2)
+    small = WORKLOADS["small"]  # bf16 activations: one h plane
+    ws = bench.kernel_work(small, small.batch)
+    assert ws["fwd_attention"][1] == small.batch * (3 * small.rank * 4 + small.rank * 2 + 4 * small.rank * 4)
+
+
 def test_roofline_bound_selection():
     # attention of a bf16 model: exponential-bound, reported in exponentials per second
     r = bench.roofline_for("fwd_attention", (0.0, 1e9, 7.0e12), 1e-3, True)
