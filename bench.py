@@ -89,8 +89,13 @@ def kernel_work(wl, B: int) -> dict:
     # h, and its second plane when the activations are held as f16 or as bf16 hi + lo
     h_out = r * eb * (2 if wl.act_mode in ("f16", "hilo") else 1)
     w["fwd_attention"] = (0.0, B * (3 * r * 4 + h_out + stats), pair_fwd * B * r * r)
-    # up projection + cross epilogue: h, U, bias, x0, x_l in; t, x_{l+1} out
-    w["fwd_up_gemm"] = (2.0 * B * d * hr, B * hr * eb + d * hr * eb + d * eb + 4 * B * d * eb, 0.0)
+    # up projection + cross epilogue: h, U, bias, x0, x_l in; t, x_{l+1} out. With hi + lo
+    # activations x_l is read and x_{l+1} written as two planes; with f16 activations x_{l+1}
+    # is written as f16 and as a bf16 copy (the weight gradient's operand).
+    xl_planes = 2 if wl.act_mode == "hilo" else 1
+    xo_planes = 2 if wl.act_mode in ("f16", "hilo") else 1
+    w["fwd_up_gemm"] = (2.0 * B * d * hr,
+                        B * hr * eb + d * hr * eb + d * eb + B * d * eb * (2 + xl_planes + xo_planes), 0.0)
     # average over layers of: g in (storage on the top layer, float below), x0, t, grad_x0 (rmw below top), gt out
     gin = (eb + (L - 1) * 4) / L
     gx = (4 + (L - 1) * 8) / L

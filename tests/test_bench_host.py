@@ -55,6 +55,9 @@ def test_work_model_attention_bytes():
     w = bench.kernel_work(wl, B)
     assert w["fwd_attention"][1] == B * (3 * r * 4 + 2 * r * 2 + 4 * r * 4)
     assert w["bwd_attention"][1] == B * (3 * r * 4 + r * 4 + 4 * r * 4 + 3 * r * 2)
+    # up: h, U, bias, x0, x_l in; t, x_{l+1} (f16) and its bf16 copy out
+    d = wl.d
+    assert w["fwd_up_gemm"][1] == B * r * 2 + d * r * 2 + d * 2 + B * d * 2 * 5
     small = WORKLOADS["small"]  # bf16 activations: one h plane
     ws = bench.kernel_work(small, small.batch)
     assert ws["fwd_attention"][1] == small.batch * (3 * small.rank * 4 + small.rank * 2 + 4 * small.rank * 4)
