@@ -43,7 +43,7 @@ def _backward(task):
 
 
 def default_workers(weight_bytes: int) -> int:
-    """At most 16 processes (the GPU machine's CPU share), fewer when memory is short: each
+    """At most 16 processes (the host CPU share of one GPU), fewer when memory is short: each
     worker holds float64 copies of the weights and of their gradients."""
     n = min(16, os.cpu_count() or 1)
     try:
