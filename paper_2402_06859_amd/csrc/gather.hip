@@ -20,9 +20,11 @@
 // and only then combines in float, pools over the bag in bag order, rounds to the
 // storage type and stores: the dependent id -> row load chains of its rows are in
 // flight together. A bag (multi-hot feature) is read in chunks of K ids
-// (GATHER_BAG_CHUNK): the chunk's id loads are issued together, then the row loads of
-// all its ids, so a bag of n ids costs about 2n/K dependent load latencies rather
-// than 2n. Vectors of the dense block are copied.
+// (GATHER_BAG_CHUNK), and the next chunk's id loads are issued before this chunk's
+// row loads, so a bag of n ids costs about n/K + 1 dependent load latencies rather
+// than 2n. With bags a wave sums one bag at a time: K = 1 and one row per wave keep
+// the kernel small enough for 8 waves per SIMD, which hides more latency than
+// wider chunks at fewer waves. Vectors of the dense block are copied.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -46,7 +48,10 @@ __device__ __forceinline__ bool qr_split(ID id_raw, const GatherArgs& a, uint32_
 }
 
 constexpr int GATHER_ROWS = 2;  // rows per wave (their loads are issued together)
-constexpr int GATHER_BAG_CHUNK = 4;  // ids of a bag whose row loads are issued together
+// rows per wave when the features are bags: a wave sums its bags one after another,
+// so one bag per wave puts twice as many bags in flight across the chip
+constexpr int GATHER_BAG_ROWS = 1;
+constexpr int GATHER_BAG_CHUNK = 1;  // ids of a bag whose row loads are issued together
 
 // Table rows in the storage type: a lane's V values are one 16-byte vector.
 template <typename T>
@@ -146,6 +151,7 @@ __device__ __forceinline__ void gather_block(int L, int ne, int nx, int ny, int&
 template <typename T, typename ID, bool BAGS, class Rows, bool HASHED>
 __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a, int ny) {
 #pragma clang fp contract(off)
+    constexpr int RW = BAGS ? GATHER_BAG_ROWS : GATHER_ROWS;
     constexpr int V = st<T>::vec;
     const int cpf = a.D / V;                 // vectors per embedding segment
     const int emb_vecs = a.F * cpf;
@@ -163,21 +169,21 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a, int ny) {
     // table pair(s) of feature f: pair f, or pairs 2f (low hash half) and 2f + 1 (high)
     const Rows rows(a, HASHED ? 2 * f : f, cc);
     const Rows rows1(a, HASHED ? 2 * f + 1 : f, cc);
-    const int64_t row_step = (int64_t)ny * 4 * GATHER_ROWS;
-    for (int64_t b0 = ((int64_t)by * 4 + (threadIdx.x >> 6)) * GATHER_ROWS; b0 < a.batch; b0 += row_step) {
-        const int nr = a.batch - b0 < GATHER_ROWS ? (int)(a.batch - b0) : GATHER_ROWS;
-        u32x4_t out[GATHER_ROWS];
+    const int64_t row_step = (int64_t)ny * 4 * RW;
+    for (int64_t b0 = ((int64_t)by * 4 + (threadIdx.x >> 6)) * RW; b0 < a.batch; b0 += row_step) {
+        const int nr = a.batch - b0 < RW ? (int)(a.batch - b0) : RW;
+        u32x4_t out[RW];
         if (!emb) {
 #pragma unroll
-            for (int u = 0; u < GATHER_ROWS; ++u)
+            for (int u = 0; u < RW; ++u)
                 if (u < nr) out[u] = *(const u32x4_t*)((const T*)a.dense + (b0 + u) * a.Nd + (c - emb_vecs) * V);
         } else if (!BAGS && HASHED) {
-            ID id[GATHER_ROWS];
+            ID id[RW];
 #pragma unroll
-            for (int u = 0; u < GATHER_ROWS; ++u) id[u] = ids[(b0 + (u < nr ? u : 0)) * a.F + f];
-            typename Rows::Raw q0[GATHER_ROWS], r0[GATHER_ROWS], q1[GATHER_ROWS], r1[GATHER_ROWS];
+            for (int u = 0; u < RW; ++u) id[u] = ids[(b0 + (u < nr ? u : 0)) * a.F + f];
+            typename Rows::Raw q0[RW], r0[RW], q1[RW], r1[RW];
 #pragma unroll
-            for (int u = 0; u < GATHER_ROWS; ++u) {
+            for (int u = 0; u < RW; ++u) {
                 uint32_t qi[2], ri[2];
                 hash_split((int64_t)id[u], a, qi, ri);
                 q0[u] = rows.load_q(qi[0]);
@@ -186,7 +192,7 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a, int ny) {
                 r1[u] = rows1.load_r(ri[1]);
             }
 #pragma unroll
-            for (int u = 0; u < GATHER_ROWS; ++u) {
+            for (int u = 0; u < RW; ++u) {
                 float qa[V], ra[V], qb[V], rb[V], acc[V];
                 Rows::values(q0[u], qa);
                 Rows::values(r0[u], ra);
@@ -201,13 +207,13 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a, int ny) {
                 out[u] = st<T>::pack(acc);
             }
         } else if (!BAGS) {
-            ID id[GATHER_ROWS];
+            ID id[RW];
 #pragma unroll
-            for (int u = 0; u < GATHER_ROWS; ++u) id[u] = ids[(b0 + (u < nr ? u : 0)) * a.F + f];
-            bool ok[GATHER_ROWS];
-            typename Rows::Raw qw[GATHER_ROWS], rw[GATHER_ROWS];
+            for (int u = 0; u < RW; ++u) id[u] = ids[(b0 + (u < nr ? u : 0)) * a.F + f];
+            bool ok[RW];
+            typename Rows::Raw qw[RW], rw[RW];
 #pragma unroll
-            for (int u = 0; u < GATHER_ROWS; ++u) {
+            for (int u = 0; u < RW; ++u) {
                 uint32_t qi = 0, ri = 0;
                 ok[u] = qr_split<ID>(id[u], a, qi, ri);
                 if (!ok[u]) qi = ri = 0;
@@ -216,7 +222,7 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a, int ny) {
             }
             bool bad = false;
 #pragma unroll
-            for (int u = 0; u < GATHER_ROWS; ++u) {
+            for (int u = 0; u < RW; ++u) {
                 float qv[V], rv[V], acc[V];
                 Rows::values(qw[u], qv);
                 Rows::values(rw[u], rv);
@@ -227,9 +233,9 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a, int ny) {
             }
             if (bad && cc == 0) atomicOr(a.err, 1);
         } else {
-            int64_t beg[GATHER_ROWS], end[GATHER_ROWS];
+            int64_t beg[RW], end[RW];
 #pragma unroll
-            for (int u = 0; u < GATHER_ROWS; ++u) {
+            for (int u = 0; u < RW; ++u) {
                 const int64_t bag = (b0 + (u < nr ? u : 0)) * a.F + f;
                 beg[u] = a.offsets[bag];
                 end[u] = u < nr ? a.offsets[bag + 1] : beg[u];
@@ -239,17 +245,24 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a, int ny) {
             constexpr int K = HASHED ? (GATHER_BAG_CHUNK + 1) / 2 : GATHER_BAG_CHUNK;
             bool bad = false;
 #pragma unroll
-            for (int u = 0; u < GATHER_ROWS; ++u) {
+            for (int u = 0; u < RW; ++u) {
                 float acc[V];
 #pragma unroll
                 for (int e = 0; e < V; ++e) acc[e] = 0.0f;
                 bool started = false;
+                // the next chunk's ids are loaded before this chunk's rows, so a chunk
+                // waits for one row latency rather than an id latency and a row latency
+                ID nid[K];
+#pragma unroll
+                for (int k = 0; k < K; ++k) nid[k] = beg[u] + k < end[u] ? ids[beg[u] + k] : ID(0);
                 for (int64_t p0 = beg[u]; p0 < end[u]; p0 += K) {
                     const int n = end[u] - p0 < K ? (int)(end[u] - p0) : K;
                     ID id[K];
 #pragma unroll
-                    for (int k = 0; k < K; ++k)
-                        if (k < n) id[k] = ids[p0 + k];
+                    for (int k = 0; k < K; ++k) {
+                        id[k] = nid[k];
+                        if (p0 + K + k < end[u]) nid[k] = ids[p0 + K + k];
+                    }
                     if (HASHED) {
                         typename Rows::Raw q0[K], r0[K], q1[K], r1[K];
 #pragma unroll
@@ -312,7 +325,7 @@ __global__ __launch_bounds__(256) void k_qr_gather(GatherArgs a, int ny) {
             continue;  // each bag's row was stored when its sum was complete
         }
 #pragma unroll
-        for (int u = 0; u < GATHER_ROWS; ++u)
+        for (int u = 0; u < RW; ++u)
             if (u < nr) *(u32x4_t*)(x0 + (b0 + u) * d + (int64_t)c * V) = out[u];
     }
 }
@@ -363,17 +376,18 @@ hipError_t launch_gather_rows(const GatherArgs& a, bool bf16, bool ids64, hipStr
     const int V = bf16 ? 8 : 4;
     const int64_t cpr = (a.F * (int64_t)a.D + a.Nd) / V;
     if (a.batch == 0 || cpr == 0) return hipSuccess;
-    // nx 64-column slices of a row times ny groups of 4 waves x GATHER_ROWS rows
-    // (grid-stride beyond), as one dimension
+    // nx 64-column slices of a row times ny groups of 4 waves x rw rows (grid-stride
+    // beyond), as one dimension
+    const bool bags = a.offsets != nullptr;
+    const int rw = bags ? GATHER_BAG_ROWS : GATHER_ROWS;
     const int64_t nx = (cpr + 63) / 64;
-    int64_t ygroups = (a.batch + 4 * GATHER_ROWS - 1) / (4 * GATHER_ROWS);
+    int64_t ygroups = (a.batch + 4 * rw - 1) / (4 * rw);
     if (ygroups > 65535) ygroups = 65535;
     if (nx * ygroups > (1 << 24) - 1) ygroups = ((1 << 24) - 1) / nx;  // grid of under 2^32 threads
     if (ygroups < 1) return hipErrorInvalidValue;
     const int ny = (int)ygroups;
     const dim3 grid((unsigned)(nx * ygroups));
     const int threads = 256;
-    const bool bags = a.offsets != nullptr;
 #define RDCN_GATHER(T, ID, BG)                                                                         \
     do {                                                                                               \
         if (a.hashed) hipLaunchKernelGGL((k_qr_gather<T, ID, BG, R<T>, true>), grid, dim3(threads), 0, s, a, ny); \
