@@ -536,7 +536,9 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
     constexpr int FU_RPT = ROWS / FU_THREADS;  // slice rows per thread in the run-start scan
     constexpr int E = 64 / L;                // lane groups per wave
     constexpr int NP = FU_WAVES * E;         // parts of a sorted chunk, one per lane group
-    constexpr int U = 8 / NC;                // elements of a part whose loads are in flight together
+    // elements of a part whose loads are in flight together: twice as many in the bag
+    // forms with the sum combine, which run one workgroup per CU and have the registers
+    constexpr int U = (BAGS && !MUL && ROWS != FU_ROWS_SMALL ? 16 : 8) / NC;
     __shared__ uint32_t key_e[CAP];       // per chunk element: row << 16 | rank in its wave's run, or FU_SKIP
     __shared__ uint32_t sorted[CAP];      // row << EB | element, in (row, element) order
     __shared__ uint16_t whist[FU_WAVES][ROWS];  // per wave row counts, then run starts (< CAP)
@@ -772,9 +774,13 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
 #pragma unroll
                             for (int q = 0; q < 4; ++q) o4[u][h].v[q] = st<T>::load(o + 4 * h + q);
                     }
-                    const float* orow = gtab + (int64_t)(dst[u] == DST_ROW ? key[u] : 0u) * D + cc;
+                    // the table row is loaded only where a segment ends (in the forms
+                    // with one workgroup per CU: the branch costs registers)
+                    if (ROWS == FU_ROWS_SMALL || dst[u] == DST_ROW) {
+                        const float* orow = gtab + (int64_t)(dst[u] == DST_ROW ? key[u] : 0u) * D + cc;
 #pragma unroll
-                    for (int h = 0; h < NC; ++h) old[u][h] = load4(orow + 4 * h);
+                        for (int h = 0; h < NC; ++h) old[u][h] = load4(orow + 4 * h);
+                    }
                 }
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
