@@ -575,9 +575,10 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
     for (int i = threadIdx.x; i < FU_WAVES * ROWS; i += FU_THREADS) (&whist[0][0])[i] = 0;
 
     const int64_t step_b = BAGS ? FU_BAGS : CAP;
-    for (int64_t b0 = 0; b0 < a.batch; b0 += step_b) {
+    for (int64_t b0 = 0; b0 < a.batch;) {
         const uint32_t nb = (uint32_t)(a.batch - b0 < step_b ? a.batch - b0 : step_b);
         uint32_t total = nb;  // occurrences of this block of bags
+        uint32_t take = nb;   // bags (samples) taken in this pass
         if (BAGS) {
             uint32_t len[FU_BPT], s4 = 0;
             int64_t beg[FU_BPT];
@@ -597,6 +598,21 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
                 s4 += len[k];
             }
             uint32_t run = block_exclusive_scan_nw<FU_WAVES>(s4, sh, total);
+            // unless these are the last bags, take only the leading bags that fill whole
+            // chunks and leave the rest to the next pass: a partial chunk costs the
+            // ranking and placement of a full one (at least one bag is taken)
+            if (b0 + nb < a.batch && total > (uint32_t)CAP) {
+                const uint32_t limit = total / CAP * CAP;
+                uint32_t cnt = 0, end = run;
+#pragma unroll
+                for (int k = 0; k < FU_BPT; ++k) {
+                    end += len[k];
+                    cnt += FU_BPT * threadIdx.x + k < nb && end <= limit ? 1u : 0u;
+                }
+                uint32_t nfit;
+                block_exclusive_scan_nw<FU_WAVES>(cnt, sh, nfit);
+                take = nfit > 0 ? nfit : 1u;
+            }
 #pragma unroll
             for (int k = 0; k < FU_BPT; ++k) {
                 bstart[FU_BPT * threadIdx.x + k] = run;
@@ -605,6 +621,7 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
             }
         }
         __syncthreads();
+        if (BAGS && take < nb) total = bstart[take];  // the taken bags' occurrences
         for (uint32_t c0 = 0; c0 < total; c0 += CAP) {
             const uint32_t n = total - c0 < (uint32_t)CAP ? total - c0 : (uint32_t)CAP;
             // A. rows of this wave's share (all id loads first, then the ranking); the
@@ -838,6 +855,7 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
             }
             __syncthreads();
         }
+        b0 += take;
     }
 }
 
