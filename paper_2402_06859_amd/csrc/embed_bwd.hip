@@ -579,6 +579,7 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
         const uint32_t nb = (uint32_t)(a.batch - b0 < step_b ? a.batch - b0 : step_b);
         uint32_t total = nb;  // occurrences of this block of bags
         uint32_t take = nb;   // bags (samples) taken in this pass
+        uint32_t bbeg[FU_BPT], blen[FU_BPT];  // this thread's bags: first occurrence in the pass, length
         if (BAGS) {
             uint32_t len[FU_BPT], s4 = 0;
             int64_t beg[FU_BPT];
@@ -617,11 +618,14 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
             for (int k = 0; k < FU_BPT; ++k) {
                 bstart[FU_BPT * threadIdx.x + k] = run;
                 boff[FU_BPT * threadIdx.x + k] = beg[k];
+                bbeg[k] = run;
+                blen[k] = FU_BPT * threadIdx.x + k < take ? len[k] : 0u;
                 run += len[k];
             }
         }
         __syncthreads();
         if (BAGS && take < nb) total = bstart[take];  // the taken bags' occurrences
+        uint32_t carry_bag = 0;  // 1 + the bag of the previous chunk's last element
         for (uint32_t c0 = 0; c0 < total; c0 += CAP) {
             const uint32_t n = total - c0 < (uint32_t)CAP ? total - c0 : (uint32_t)CAP;
             // A. rows of this wave's share (all id loads first, then the ranking); the
@@ -630,23 +634,51 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
             int64_t pv[NIT];
             uint32_t bagv[NIT];
             if (BAGS) {
-                // last bag of the block whose start is <= the element: a branch-free search,
-                // all elements in lockstep (entries past the block's bags hold the total,
-                // which exceeds every element, so they are never taken)
+                // the bag of each element: every non-empty taken bag that starts in the chunk
+                // marks its first element with bag + 1 (in key_e, unused until the ranking);
+                // bag indices rise with the element, so an element's bag is the last mark at
+                // or before it, or before the chunk's first mark the previous chunk's last bag
+#pragma unroll
+                for (int it = 0; it < NIT; ++it) key_e[wv * QW + it * 64 + lane] = 0u;
+                __syncthreads();
+#pragma unroll
+                for (int k = 0; k < FU_BPT; ++k)
+                    if (blen[k] > 0 && bbeg[k] >= c0 && bbeg[k] - c0 < n)
+                        key_e[bbeg[k] - c0] = FU_BPT * threadIdx.x + k + 1;
+                __syncthreads();
+                uint32_t mk[NIT], lmax = 0;
+#pragma unroll
+                for (int it = 0; it < NIT; ++it) {
+                    mk[it] = key_e[wv * QW + it * 64 + lane];
+                    lmax = mk[it] > lmax ? mk[it] : lmax;
+                }
+#pragma unroll
+                for (int off = 32; off > 0; off >>= 1) {
+                    const uint32_t y = __shfl_xor(lmax, off);
+                    lmax = y > lmax ? y : lmax;
+                }
+                if (lane == 0) sh[wv] = lmax;
+                __syncthreads();
+                uint32_t cur = carry_bag;  // last mark before this wave's elements
+                for (int w = 0; w < wv; ++w) cur = sh[w] > cur ? sh[w] : cur;
+#pragma unroll
+                for (int it = 0; it < NIT; ++it) {
+                    // the last marked lane at or below this one, else the carry
+                    const uint64_t upto = __ballot(mk[it] != 0u) & ((2ull << lane) - 1ull);
+                    const uint32_t got = __shfl(mk[it], upto ? 63 - __clzll(upto) : 0);
+                    const uint32_t bg = upto ? got : cur;
+                    bag_e[wv * QW + it * 64 + lane] = (uint16_t)(bg - 1u);
+                    cur = __builtin_amdgcn_readlane(bg, 63);
+                }
+                __syncthreads();
+                carry_bag = (uint32_t)bag_e[n - 1] + 1u;
                 uint32_t vv[NIT];
 #pragma unroll
                 for (int it = 0; it < NIT; ++it) {
                     const uint32_t e = (uint32_t)(wv * QW + it * 64 + lane);
-                    vv[it] = c0 + (e < n ? e : 0u);
-                    bagv[it] = 0;
-                }
-#pragma unroll
-                for (uint32_t sstep = FU_BAGS / 2; sstep > 0; sstep >>= 1) {
-#pragma unroll
-                    for (int it = 0; it < NIT; ++it) {
-                        const uint32_t t = bagv[it] + sstep;
-                        bagv[it] = bstart[t] <= vv[it] ? t : bagv[it];
-                    }
+                    const uint32_t ee = e < n ? e : 0u;
+                    vv[it] = c0 + ee;
+                    bagv[it] = bag_e[ee];
                 }
 #pragma unroll
                 for (int it = 0; it < NIT; ++it) pv[it] = boff[bagv[it]] + (int64_t)(vv[it] - bstart[bagv[it]]);
@@ -687,7 +719,6 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
                 const uint32_t before = whist[wv][row];
                 const uint32_t rank = (uint32_t)__popcll(peers & lt);
                 key_e[e] = kept ? (row << 16) | (before + rank) : FU_SKIP;
-                if (BAGS) bag_e[e] = (uint16_t)bagv[it];
                 if (MUL) other_e[e] = (uint16_t)(isq ? ri : qi);
                 if (kept && rank == 0) whist[wv][row] = (uint16_t)(before + (uint32_t)__popcll(peers));
             }
