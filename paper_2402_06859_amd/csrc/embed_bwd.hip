@@ -833,13 +833,14 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     const uint32_t k = key[u];
-                    const bool ok = k != SEG_PAD && colok;
                     const bool cont = k == acc_key;
+                    // padding elements past the part's end and lanes past the row width add
+                    // stand-in values, but their sums are never stored or carried
 #pragma unroll
                     for (int h = 0; h < NC; ++h)
 #pragma unroll
                         for (int q = 0; q < 4; ++q) {
-                            const float v = ok ? (MUL ? x[u][h].v[q] * o4[u][h].v[q] : x[u][h].v[q]) : 0.f;
+                            const float v = MUL ? x[u][h].v[q] * o4[u][h].v[q] : x[u][h].v[q];
                             acc[h].v[q] = cont ? acc[h].v[q] + v : v;
                         }
                     acc_key = k;
@@ -884,7 +885,9 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
                     store4(dstp + 4 * h, old);
                 }
             }
-            __syncthreads();
+            // no barrier: E reads `sorted` and `carry`, which the next chunk writes only
+            // after its first barrier, and that barrier also orders E's row update before
+            // the next chunk's updates of the same rows
         }
         b0 += take;
     }
