@@ -188,6 +188,44 @@ def test_embed_backward_bag_edges(F, combine):
     assert_unreached_zero(wl, inp, gq, gr)
 
 
+@pytest.mark.parametrize("F,combine", [(3, "sum"), (64, "sum"), (64, "mul"), (120, "sum")])
+def test_embed_backward_bag_passes(F, combine):
+    """Bags over several passes of 1024 bags: a pass that is not the batch's last takes
+    only the leading bags that fill whole chunks, and the next pass starts after them.
+    Covered: a pass that starts with a bag longer than a chunk (only that bag is taken:
+    feature 1 with 8192-occurrence chunks, feature 2 with 4096), empty bags at the cuts,
+    bags that span chunk boundaries, a hot id; compared with the oracle and rerun
+    bitwise."""
+    need_gpu()
+    B = 2600
+    wl = WORKLOADS["multihot"].with_(batch=B, num_cat=F, combine=combine, emb_dim=32, num_dense=16)
+    inp = make_inputs(wl, with_weights=False, with_grad=False)
+    rng = np.random.Generator(np.random.PCG64(17))
+    lens = rng.integers(0, 12, size=(B, F))
+    lens[rng.random((B, F)) < 0.2] = 0      # empty bags
+    lens[1024, 1 % F] = 9000                 # first bag of the second pass, longer than any chunk
+    if F > 2:
+        lens[1025:2048, 2] = 0               # feature 2's second pass: one long bag and a few short ones
+        lens[1025:2048:100, 2] = 3
+        lens[1024, 2] = 5000
+    offsets = np.zeros(B * F + 1, dtype=np.int64)
+    np.cumsum(lens.reshape(-1), out=offsets[1:])
+    nnz = int(offsets[-1])
+    ids = rng.integers(0, wl.vocab, size=nnz)
+    ids[rng.random(nnz) < 0.5] = 123_457    # hot id: one long segment per table
+    inp["ids"] = torch.from_numpy(ids.astype(np.int64))
+    inp["offsets"] = torch.from_numpy(offsets)
+    gx0 = grad_x0_like(wl, B, 19)
+    print("embed_bwd bag passes", F, combine, "nnz", nnz, flush=True)
+    gq, gr, status = run(wl, inp, gx0)
+    assert status == rdcn.RDCN_OK
+    rq, rr, _ = ref(wl, inp, gx0)
+    assert max(relerr(gq.numpy(), rq), relerr(gr.numpy(), rr)) <= 1e-5
+    assert_unreached_zero(wl, inp, gq, gr)
+    gq2, gr2, _ = run(wl, inp, gx0)
+    assert torch.equal(gq, gq2) and torch.equal(gr, gr2)
+
+
 @pytest.mark.parametrize("D,dtype", [(4, "f32"), (48, "bf16"), (256, "bf16")])
 def test_embed_backward_widths(D, dtype):
     """Table widths from one column group to 256 (one pair per step)."""
