@@ -504,7 +504,7 @@ constexpr int FU_CAP = 4096;            // occurrences per chunk
 constexpr int FU_WAVES = 8;             // waves per workgroup
 constexpr int FU_THREADS = 64 * FU_WAVES;
 constexpr int FU_ROWS = 4096;           // rows per slice (at most)
-constexpr int FU_ROWS_MID = 2048;       // the form with chunks of 2 * FU_CAP occurrences
+constexpr int FU_ROWS_MID = 2048;       // the form with chunks of 2 * FU_CAP occurrences (10240 with bags)
 constexpr int FU_ROWS_SMALL = 1024;     // the kernel form for slices of at most this many rows: its
                                         // smaller LDS lets two single-hot workgroups share a CU
 constexpr int FU_MAX_SLICES = 16;
@@ -527,9 +527,14 @@ struct FusedArgs {
 // serves twice the elements).
 template <typename T, int L, bool MUL, bool BAGS, int ROWS, int CPL, int CAP>
 __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
-    static_assert(CAP == 4096 || CAP == 8192, "chunk of 4096 or 8192 occurrences");
+    static_assert(CAP == 4096 || CAP == 8192 || CAP == 10240, "chunk of 4096, 8192 or 10240 occurrences");
+    // bags with the sum combine: the sums need only each element's bag, so `sorted` carries
+    // the bag (below FU_BAGS) instead of the element and no per-element bag array is kept
+    constexpr bool BAGDIRECT = BAGS && !MUL;
+    static_assert(!BAGDIRECT || FU_BAGS <= 1024, "a bag index takes 10 bits");
+    static_assert(BAGDIRECT || CAP != 10240, "10240-occurrence chunks only in the bag-index form");
     constexpr int QW = CAP / FU_WAVES;       // chunk elements per wave
-    constexpr int EB = CAP == 8192 ? 13 : 12;  // bits of a chunk element index in `sorted`
+    constexpr int EB = BAGDIRECT ? 10 : CAP == 8192 ? 13 : 12;  // bits of the element (bag) index in `sorted`
     constexpr uint32_t EMASK = (1u << EB) - 1u;
     static_assert(CPL == 4 || CPL == 8, "four or eight columns per lane");
     constexpr int NC = CPL / 4;              // 16-byte column groups per lane
@@ -540,10 +545,11 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
     // forms with the sum combine, which run one workgroup per CU and have the registers
     constexpr int U = (BAGS && !MUL && ROWS != FU_ROWS_SMALL ? 16 : 8) / NC;
     __shared__ uint32_t key_e[CAP];       // per chunk element: row << 16 | rank in its wave's run, or FU_SKIP
-    __shared__ uint32_t sorted[CAP];      // row << EB | element, in (row, element) order
+    __shared__ uint32_t sorted[CAP];      // row << EB | element (bag), in (row, element) order
     __shared__ uint16_t whist[FU_WAVES][ROWS];  // per wave row counts, then run starts (< CAP)
     __shared__ float carry[2][NP][CPL * L];  // per part head / tail pieces
-    __shared__ uint16_t bag_e[BAGS ? CAP : 1];
+    __shared__ uint16_t bag_e[BAGS && !BAGDIRECT ? CAP : 1];
+    __shared__ uint32_t carry_sh;         // 1 + the bag of a chunk's last element (bag-index form)
     __shared__ uint16_t other_e[MUL ? CAP : 1];
     __shared__ uint32_t bstart[BAGS ? FU_BAGS : 1];
     __shared__ int64_t boff[BAGS ? FU_BAGS : 1];
@@ -658,6 +664,9 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
                     lmax = y > lmax ? y : lmax;
                 }
                 if (lane == 0) sh[wv] = lmax;
+                // the chunk's first element's bag (elements past the chunk end stand in for
+                // it, so their loads stay in bounds); read before the ranking reuses key_e
+                const uint32_t first_bag = (key_e[0] != 0u ? key_e[0] : carry_bag) - 1u;
                 __syncthreads();
                 uint32_t cur = carry_bag;  // last mark before this wave's elements
                 for (int w = 0; w < wv; ++w) cur = sh[w] > cur ? sh[w] : cur;
@@ -667,18 +676,24 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
                     const uint64_t upto = __ballot(mk[it] != 0u) & ((2ull << lane) - 1ull);
                     const uint32_t got = __shfl(mk[it], upto ? 63 - __clzll(upto) : 0);
                     const uint32_t bg = upto ? got : cur;
-                    bag_e[wv * QW + it * 64 + lane] = (uint16_t)(bg - 1u);
+                    if constexpr (BAGDIRECT) {
+                        bagv[it] = bg - 1u;
+                        if ((uint32_t)(wv * QW + it * 64 + lane) == n - 1) carry_sh = bg;
+                    } else {
+                        bag_e[wv * QW + it * 64 + lane] = (uint16_t)(bg - 1u);
+                    }
                     cur = __builtin_amdgcn_readlane(bg, 63);
                 }
                 __syncthreads();
-                carry_bag = (uint32_t)bag_e[n - 1] + 1u;
+                carry_bag = BAGDIRECT ? carry_sh : (uint32_t)bag_e[n - 1] + 1u;
                 uint32_t vv[NIT];
 #pragma unroll
                 for (int it = 0; it < NIT; ++it) {
                     const uint32_t e = (uint32_t)(wv * QW + it * 64 + lane);
                     const uint32_t ee = e < n ? e : 0u;
                     vv[it] = c0 + ee;
-                    bagv[it] = bag_e[ee];
+                    if constexpr (BAGDIRECT) bagv[it] = e < n ? bagv[it] : first_bag;
+                    else bagv[it] = bag_e[ee];
                 }
 #pragma unroll
                 for (int it = 0; it < NIT; ++it) pv[it] = boff[bagv[it]] + (int64_t)(vv[it] - bstart[bagv[it]]);
@@ -750,12 +765,13 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
             }
             __syncthreads();
             // C. placement
-            for (int it = 0; it < QW / 64; ++it) {
+#pragma unroll
+            for (int it = 0; it < NIT; ++it) {
                 const uint32_t e = (uint32_t)(wv * QW + it * 64 + lane);
                 const uint32_t kv = key_e[e];
                 if (kv != FU_SKIP) {
                     const uint32_t row = kv >> 16;
-                    sorted[whist[wv][row] + (kv & 0xffffu)] = (row << EB) | e;
+                    sorted[whist[wv][row] + (kv & 0xffffu)] = (row << EB) | (BAGDIRECT ? bagv[it] : e);
                 }
             }
             __syncthreads();
@@ -812,7 +828,7 @@ __global__ __launch_bounds__(FU_THREADS) void k_emb_fused(FusedArgs fa) {
                     const bool ok = key[u] != SEG_PAD && colok;
                     const int cc = colok ? c : 0;
                     const uint32_t ee = ok ? el[u] : 0u;
-                    const int64_t b = b0 + (ok ? (BAGS ? (int64_t)bag_e[ee] : (int64_t)ee) : 0);
+                    const int64_t b = b0 + (ok ? (BAGS && !BAGDIRECT ? (int64_t)bag_e[ee] : (int64_t)ee) : 0);
 #pragma unroll
                     for (int h = 0; h < NC; ++h) x[u][h] = load4(gx + b * a.d + cc + 4 * h);
                     if (MUL) {
@@ -950,11 +966,12 @@ template <typename T, bool MUL, bool BAGS>
 hipError_t launch_fused_d(const FusedArgs& fa, unsigned blocks, hipStream_t st) {
     const uint32_t rps = fa.rps_q > fa.rps_r ? fa.rps_q : fa.rps_r;
     if (rps <= (uint32_t)FU_ROWS_SMALL) return launch_fused_rows<T, MUL, BAGS, FU_ROWS_SMALL, 4>(fa, blocks, st);
-    // slices of up to 2048 rows without the product combine: chunks of 8192 occurrences,
-    // so each reached row of the slice is read and written half as often
+    // slices of up to 2048 rows without the product combine: chunks of 8192 occurrences
+    // (10240 with bags, whose sorted entries carry the bag and need no per-element bag
+    // array), so each reached row of the slice is read and written less often
     if constexpr (!MUL)
         if (rps <= (uint32_t)FU_ROWS_MID && fa.a.D % 8 == 0)
-            return launch_fused_rows<T, MUL, BAGS, FU_ROWS_MID, 8, 2 * FU_CAP>(fa, blocks, st);
+            return launch_fused_rows<T, MUL, BAGS, FU_ROWS_MID, 8, BAGS ? 10240 : 2 * FU_CAP>(fa, blocks, st);
     if (fa.a.D % 8 == 0) return launch_fused_rows<T, MUL, BAGS, FU_ROWS, 8>(fa, blocks, st);
     return launch_fused_rows<T, MUL, BAGS, FU_ROWS, 4>(fa, blocks, st);
 }
