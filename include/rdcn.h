@@ -176,7 +176,10 @@ rdcn_status rdcn_workspace_bytes(const rdcn_handle* h, int64_t batch, size_t* sa
 /*
  * QR embedding gather (forward), section "Model Dictionary Compression":
  *   ids      : single-hot [batch, F] (offsets == NULL), or multi-hot CSR values
- *              with offsets [batch*F + 1] (int64) over bag index b*F + f
+ *              with offsets [batch*F + 1] (int64) over bag index b*F + f;
+ *              the offsets must be nondecreasing from offsets[0] >= 0 and ids
+ *              must hold offsets[batch*F] values: the gather reads ids at those
+ *              positions without a bound (it is not given their count)
  *   q_tables : [F, qr_rows_q, D],  r_tables : [F, m, D],  dense : [batch, Nd]
  *   x0       : [batch, d] output, all in the storage dtype.
  * Per element the combine is one float operation on the two table values
