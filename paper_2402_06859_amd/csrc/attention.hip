@@ -540,10 +540,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 const f16x4_t kf = key_frag(sk[j0 + (lane & 31)], lane >> 5);
                 const f16x8_t a0 = frag32(sx, ldx, lane, j0), a1 = frag32(sx, ldx, lane, j0 + 16);
                 const f32x16_t z16 = {};
+                // the next tile's arguments are issued before this tile's exponentials, so
+                // the matrix core computes them while the wave's exponentials run
+                f32x16_t xn = __builtin_amdgcn_mfma_f32_32x32x8f16(kf, *(const f16x4_t*)(scm + (lane & 31)), z16, 0, 0, 0);
 #pragma unroll
                 for (int tt = 0; tt < NT / 2; ++tt) {
-                    const f16x4_t rec = *(const f16x4_t*)(scm + 32 * tt + (lane & 31));
-                    const f32x16_t x = __builtin_amdgcn_mfma_f32_32x32x8f16(kf, rec, z16, 0, 0, 0);
+                    const f32x16_t x = xn;
+                    if (tt + 1 < NT / 2) {
+                        const f16x4_t rec = *(const f16x4_t*)(scm + 32 * (tt + 1) + (lane & 31));
+                        xn = __builtin_amdgcn_mfma_f32_32x32x8f16(kf, rec, z16, 0, 0, 0);
+                    }
                     float e0[8], e1[8];
 #pragma unroll
                     for (int u = 0; u < 8; ++u) {
