@@ -152,6 +152,8 @@ __global__ __launch_bounds__(256) void k_colsum(const float* __restrict__ part, 
     const int64_t c = (int64_t)blockIdx.x * 64 + tx * 4;
     float s[4] = {0.f, 0.f, 0.f, 0.f};
     if (c < d) {
+        // unrolled so that eight rows' loads are in flight together (the sums stay in row order)
+#pragma unroll 8
         for (int y = ty; y < nrb; y += 16) {
             float p[4];
             ld4<float>(part + (int64_t)y * d + c, p);
