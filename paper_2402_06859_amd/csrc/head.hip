@@ -192,6 +192,8 @@ __global__ __launch_bounds__(256) void k_colsum_w(int64_t B, int64_t n, const T*
 #pragma unroll
     for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
     if (j < n) {
+        // unrolled so that four rows' loads are in flight together (the sums stay in row order)
+#pragma unroll 4
         for (int64_t b = b0 + wave; b < b1; b += 4) {
             const float wv = wgt ? wgt[b] : 1.f;
             float v[VEC];
@@ -224,6 +226,7 @@ __global__ __launch_bounds__(256) void k_chunk_reduce(int64_t nchunks, int64_t n
     const int64_t j = (int64_t)blockIdx.x * 64 + tx;
     float acc = 0.f;
     if (j < n)
+#pragma unroll 4
         for (int64_t c = ty; c < nchunks; c += 4) acc += part[c * n + j];
     red[ty][tx] = acc;
     __syncthreads();
@@ -237,6 +240,7 @@ __global__ __launch_bounds__(256) void k_vec_sums(int64_t B, VecSums v) {
     const int i = blockIdx.x, t = threadIdx.x;
     const float* x = v.x[i];
     float acc = 0.f;
+#pragma unroll 4
     for (int64_t b = t; b < B; b += 256) acc += x[b];
     red[t] = acc;
     __syncthreads();
